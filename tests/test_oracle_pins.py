@@ -1,0 +1,346 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix (no GPU needed).
+
+Each test names the passage or closed form it pins. A plausible mistake in the oracle (a dropped
+term, a wrong sign or index, a swapped operand, a wrong child order, ddof 1, a non-strict
+comparison, a wrong topological order) fails at least one of them.
+"""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy import special, stats
+
+import oracle
+from paper_2608_27612_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+LIN, SIG, TANH, GAUSS, SINE, ABS = range(6)
+
+
+def mk(kinds, acts, edges, bias=None, enabled=None):
+    """Genome from node kinds/acts and (src, dst, w) edges."""
+    n = len(kinds)
+    return {
+        "kind": np.array(kinds, np.uint8),
+        "act": np.array(acts, np.uint8),
+        "bias": np.zeros(n, np.float32) if bias is None else np.array(bias, np.float32),
+        "src": np.array([e[0] for e in edges], np.int32),
+        "dst": np.array([e[1] for e in edges], np.int32),
+        "w": np.array([e[2] for e in edges], np.float32),
+        "enabled": np.ones(len(edges), np.uint8) if enabled is None else np.array(enabled, np.uint8),
+    }
+
+
+INPUTS = [0, 1, 2, 3, 4]
+
+
+def linear_cppn(a, b, c):
+    """out = a*x2 + b*y2 + c*bias with a linear output node."""
+    return mk(INPUTS + [6], [0] * 5 + [LIN], [(2, 5, a), (3, 5, b), (4, 5, c)])
+
+
+def src_(x, y, d=0):
+    return W.sources_array([(x, y, d)])[0]
+
+
+# ---------------------------------------------------------------- P1: grid sizes (Eq. 1)
+
+def test_level_sizes_closed_form():
+    for D in range(0, 16):
+        assert oracle.n_positions(D) == (4 ** (D + 1) - 4) // 3
+        assert oracle.n_parents(D) == ((4 ** D - 1) // 3 if D > 0 else 0)
+
+
+def test_paper_printed_totals():
+    gold = json.load(open(os.path.join(GOLDEN, "paper_printed_values.json")))
+    nt = gold["n_total"]
+    # paper depth d_p == this library's depth d_p + 1
+    assert oracle.n_positions(5) == nt["paper_depth_4"]
+    assert oracle.n_positions(8) == nt["paper_depth_7"]
+    assert round(oracle.n_positions(14) / 1e6) == nt["paper_depth_13_millions_rounded"]
+    kib = oracle.n_positions(8) * 2 * 4 / 1024.0  # fp32 (x, y) per position
+    assert round(kib) == gold["grid_kilobytes_paper_depth_7"]["value"]
+
+
+# ---------------------------------------------------------------- P2: grid positions (Eq. 1)
+
+@pytest.mark.parametrize("D", [1, 2, 3, 5])
+def test_grid_is_eq1_per_level(D):
+    xy = oracle.grid(D)
+    start = 0
+    for lv in range(1, D + 1):
+        size = 4 ** lv
+        got = {(float(a), float(b)) for a, b in xy[start:start + size]}
+        want = {((2 * i + 1) / 2 ** lv - 1.0, (2 * j + 1) / 2 ** lv - 1.0)
+                for i in range(2 ** lv) for j in range(2 ** lv)}
+        assert got == want, lv
+        start += size
+    assert start == len(xy)
+
+
+def test_grid_coordinates_are_exact_dyadics_and_children_straddle_parent():
+    D = 6
+    for F in range(0, oracle.n_parents(D)):
+        px, py, lv = oracle.cell(F)
+        h = 2.0 ** -(lv + 1)
+        for k in range(4):
+            cx, cy, clv = oracle.cell(4 * F + 1 + k)
+            assert clv == lv + 1
+            # child k: bit 0 selects +x, bit 1 selects +y; offsets are exactly half the child width
+            assert cx == px + (h if k & 1 else -h)
+            assert cy == py + (h if k & 2 else -h)
+            n = (cx + 1.0) * 2 ** clv
+            assert n == int(n) and int(n) % 2 == 1
+
+
+# ---------------------------------------------------------------- P3: activations
+
+def test_activation_special_points():
+    assert oracle.act(SIG, 0.0) == 0.5
+    assert oracle.act(GAUSS, 0.0) == 1.0
+    assert oracle.act(TANH, 0.0) == 0.0
+    assert oracle.act(SINE, math.pi / 6) == pytest.approx(0.5, abs=1e-15)
+    assert oracle.act(SINE, math.pi / 2) == 1.0
+    assert oracle.act(ABS, -2.5) == 2.5
+    assert oracle.act(LIN, -1.25) == -1.25
+
+
+def test_activations_match_library_routines():
+    zs = np.linspace(-7.0, 7.0, 57)
+    for z in zs:
+        assert oracle.act(SIG, z) == pytest.approx(float(special.expit(z)), rel=1e-14)
+        assert oracle.act(TANH, z) == pytest.approx(math.tanh(z), rel=1e-14, abs=1e-300)
+        assert oracle.act(TANH, -z) == -oracle.act(TANH, z)
+        # e^{-z^2} = sqrt(pi) * N(0, 1/2) density
+        gauss = math.sqrt(math.pi) * stats.norm.pdf(z, scale=math.sqrt(0.5))
+        assert oracle.act(GAUSS, z) == pytest.approx(gauss, rel=1e-12, abs=1e-300)
+        assert oracle.act(SINE, z) == pytest.approx(math.sin(z), abs=1e-15)
+        assert oracle.act(ABS, z) == abs(z)
+
+
+# ---------------------------------------------------------------- CPPN evaluation semantics
+
+def hand_genome():
+    # ids: 5 = output (linear, bias 0.1), 6 = hidden A (abs), 7 = hidden B (sine).
+    # Edges are listed against dependency order; the y2 -> output edge is disabled.
+    kinds = INPUTS + [6, 5, 5]
+    acts = [0] * 5 + [LIN, ABS, SINE]
+    edges = [(7, 5, 2.0), (6, 5, -1.0), (6, 7, 3.0), (2, 6, 1.0), (4, 6, -0.5), (3, 5, 0.25),
+             (0, 7, 1.5)]
+    enabled = [1, 1, 1, 1, 1, 0, 1]
+    return mk(kinds, acts, edges, bias=[0, 0, 0, 0, 0, 0.1, 0, 0], enabled=enabled)
+
+
+def hand_value(x1, y1, x2, y2):
+    A = abs(x2 - 0.5)
+    B = math.sin(3.0 * A + 1.5 * x1)
+    return float(np.float32(0.1)) + 2.0 * B - A  # the bias is stored as float32
+
+
+def test_cppn_hand_genome():
+    g = hand_genome()
+    rng = np.random.default_rng(1)
+    pts = rng.uniform(-1, 1, size=(50, 4))
+    in5 = np.concatenate([pts, np.ones((50, 1))], axis=1)
+    got = oracle.eval_points(g, in5)
+    want = np.array([hand_value(*p) for p in pts])
+    np.testing.assert_allclose(got, want, rtol=1e-14, atol=1e-14)
+
+
+def test_topological_order_is_valid_and_cycles_rejected():
+    g = hand_genome()
+    order = oracle.topo_order(g)
+    pos = {int(v): i for i, v in enumerate(order)}
+    for s, d, en in zip(g["src"], g["dst"], g["enabled"]):
+        if en:
+            assert pos[int(s)] < pos[int(d)]
+    cyc = mk(INPUTS + [6, 5, 5], [0] * 5 + [LIN, LIN, LIN],
+             [(2, 6, 1.0), (6, 7, 1.0), (7, 6, 1.0), (7, 5, 1.0)])
+    assert oracle.topo_order(cyc) is None
+    # a disabled back edge is not a cycle
+    cyc["enabled"][2] = 0
+    assert oracle.topo_order(cyc) is not None
+
+
+# ---------------------------------------------------------------- P4: constant CPPN
+
+def test_constant_cppn_has_zero_variance_and_no_nodes():
+    # depends on x1, y1, bias only; an outgoing source puts the source in (x1, y1)
+    g = mk(INPUTS + [6, 5], [0] * 5 + [SIG, TANH], [(0, 6, 1.3), (1, 6, -0.7), (4, 5, 0.4),
+                                                      (6, 5, 2.0)])
+    r = oracle.discover([g], [src_(0.3, -1.0, W.DIR_OUT)], 5, np.float32(0.03))
+    assert r["pair_count"][0] == 0
+    r = oracle.discover([g], [src_(0.3, -1.0, W.DIR_OUT)], 4, -1.0)
+    Q = oracle.n_parents(4)
+    assert r["pair_count"][0] == Q
+    assert np.all(r["var"] == 0.0)
+    np.testing.assert_array_equal(r["parent"], np.arange(Q))
+
+
+# ---------------------------------------------------------------- P5: linear CPPN closed form
+
+@pytest.mark.parametrize("a,b,c", [(1.0, 0.0, 0.0), (3.0, 3.0, -0.5), (-1.5, 0.75, 2.0)])
+def test_linear_cppn_variance_closed_form(a, b, c):
+    D = 6
+    g = linear_cppn(a, b, c)
+    r = oracle.discover([g], [src_(0.0, -1.0)], D, -1.0)   # keep everything
+    assert r["pair_count"][0] == oracle.n_parents(D)
+    for P, w4, var in zip(r["parent"], r["w4"], r["var"]):
+        px, py, lv = oracle.cell(int(P))
+        k = lv + 1                      # level of the children
+        h = 2.0 ** -(lv + 1)
+        assert var == pytest.approx((a * a + b * b) / 4.0 ** k, rel=1e-12)
+        for kk in range(4):
+            x = px + (h if kk & 1 else -h)
+            y = py + (h if kk & 2 else -h)
+            assert w4[kk] == pytest.approx(a * x + b * y + c, rel=1e-13, abs=1e-13)
+
+
+@pytest.mark.parametrize("a,b,positions", [(1.0, 0.0, 20), (3.0, 3.0, 340)])
+def test_linear_cppn_kept_levels(a, b, positions):
+    # var at child level k is (a^2+b^2)/4^k; level k is kept iff a^2+b^2 > theta*4^k
+    D = 7
+    theta = np.float32(0.03)
+    r = oracle.discover([linear_cppn(a, b, 0.25)], [src_(0.0, -1.0)], D, theta)
+    assert 4 * r["pair_count"][0] == positions
+    levels = {oracle.cell(int(P))[2] + 1 for P in r["parent"]}
+    kstar = max(k for k in range(1, D + 1) if a * a + b * b > float(theta) * 4 ** k)
+    assert levels == set(range(1, kstar + 1))
+
+
+def test_threshold_is_strict():
+    # a = 1, b = 0: the children of level-1 cells (level 2) have variance exactly 1/16
+    g = linear_cppn(1.0, 0.0, 0.0)
+    r_eq = oracle.discover([g], [src_(0.0, -1.0)], 3, 1.0 / 16.0)
+    r_lt = oracle.discover([g], [src_(0.0, -1.0)], 3, np.nextafter(1.0 / 16.0, 0.0))
+    assert {oracle.cell(int(P))[2] for P in r_eq["parent"]} == {0}
+    assert {oracle.cell(int(P))[2] for P in r_lt["parent"]} == {0, 1}
+
+
+# ---------------------------------------------------------------- P6: sine CPPN closed form
+
+@pytest.mark.parametrize("omega", [1.0, 2.5, 9.0])
+def test_sine_cppn_variance_closed_form(omega):
+    D = 6
+    g = mk(INPUTS + [6, 5], [0] * 5 + [LIN, SINE], [(6, 5, 1.0), (2, 6, omega)])
+    r = oracle.discover([g], [src_(0.5, -1.0)], D, -1.0)
+    for P, var in zip(r["parent"], r["var"]):
+        px, _, lv = oracle.cell(int(P))
+        h = 2.0 ** -(lv + 1)
+        want = math.cos(omega * px) ** 2 * math.sin(omega * h) ** 2
+        assert var == pytest.approx(want, abs=1e-14)
+    theta = 0.05
+    r = oracle.discover([g], [src_(0.5, -1.0)], D, theta)
+    kept = set(int(P) for P in r["parent"])
+    for P in range(oracle.n_parents(D)):
+        px, _, lv = oracle.cell(P)
+        h = 2.0 ** -(lv + 1)
+        v = math.cos(omega * px) ** 2 * math.sin(omega * h) ** 2
+        if abs(v - theta) > 1e-12:
+            assert (P in kept) == (v > theta), P
+
+
+# ---------------------------------------------------------------- symmetries
+
+def test_in_out_duality_is_exact():
+    pop = W.population(3, 20, 8, 25)
+    for g in pop:
+        swapped = dict(g)
+        kind = g["kind"].copy()
+        # swap the roles x1 <-> x2 and y1 <-> y2
+        kind[0], kind[1], kind[2], kind[3] = 2, 3, 0, 1
+        swapped["kind"] = kind
+        a = oracle.discover([g], [src_(0.25, -0.75, W.DIR_OUT)], 4, -1.0)
+        b = oracle.discover([swapped], [src_(0.25, -0.75, W.DIR_IN)], 4, -1.0)
+        np.testing.assert_array_equal(a["w4"], b["w4"])
+
+
+def test_mirror_x_maps_i_to_reverse():
+    g = W.population(5, 1, 10, 30)[0]
+    m = dict(g)
+    m["w"] = np.where(g["src"] == 2, -g["w"], g["w"]).astype(np.float32)
+    D = 4
+    a = oracle.discover([g], [src_(0.0, -1.0)], D, -1.0)
+    b = oracle.discover([m], [src_(0.0, -1.0)], D, -1.0)
+    pos = {}
+    for P in range(oracle.n_parents(D)):
+        x, y, lv = oracle.cell(P)
+        pos[(x, y, lv)] = P
+    for P in range(oracle.n_parents(D)):
+        x, y, lv = oracle.cell(P)
+        Pm = pos[(-x, y, lv)]
+        # child k of P mirrors child k^1 of the mirrored parent
+        np.testing.assert_array_equal(a["w4"][P], b["w4"][Pm][[1, 0, 3, 2]])
+        assert a["var"][P] == pytest.approx(b["var"][Pm], rel=1e-13, abs=1e-300)
+
+
+# ---------------------------------------------------------------- P7: lazy vs eager (Theorem 1)
+
+def _heap_of_centres(D):
+    return {oracle.cell(P): P for P in range(oracle.n_parents(D))}
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_lazy_subset_of_eager_and_equal_to_chain(seed):
+    D = 5
+    theta = np.float32(0.03)
+    genomes = W.population(100 + seed, 4, 6, 18)
+    heap = _heap_of_centres(D)
+    for g in genomes:
+        for s in W.xor_sources():
+            eager = oracle.discover([g], [s], D, theta, oracle.PARENT)
+            chain = oracle.discover([g], [s], D, theta, oracle.CHAIN)
+            cent, lv, nq = oracle.lazy(g, s, D, theta)
+            lazy_set = {heap[(float(x), float(y), int(l))] for (x, y), l in zip(cent, lv)}
+            e, c = set(eager["parent"].tolist()), set(chain["parent"].tolist())
+            assert lazy_set <= e
+            assert lazy_set == c
+            assert nq <= 4 * oracle.n_parents(D)
+            # chain records carry the same weights as the eager ones for the same parent
+            ew = {int(P): w for P, w in zip(eager["parent"], eager["w4"])}
+            for P, w in zip(chain["parent"], chain["w4"]):
+                np.testing.assert_array_equal(ew[int(P)], w)
+
+
+def test_eager_recovers_what_lazy_misses():
+    # out = sin(2 pi x2): the root's children (x = +-1/2) sit on zeros of the sine, so the root
+    # fails the test and the lazy division stops; cells one level down have variance ~1
+    g = mk(INPUTS + [6, 5], [0] * 5 + [LIN, SINE], [(6, 5, 1.0), (2, 6, 2 * math.pi)])
+    D, theta = 5, 0.3
+    s = src_(0.0, -1.0)
+    eager = oracle.discover([g], [s], D, theta)
+    cent, lv, _ = oracle.lazy(g, s, D, theta)
+    assert len(cent) == 0
+    assert eager["pair_count"][0] > 0 and 0 not in set(eager["parent"].tolist())
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_selection_monotone_in_theta_and_extremes(seed):
+    D = 4
+    genomes = W.population(200 + seed, 5, 8, 25)
+    srcs = W.xor_sources()
+    prev = None
+    for theta in [-1.0, 0.0, 0.001, 0.01, 0.03, 0.1, 1.0, math.inf]:
+        r = oracle.discover(genomes, srcs, D, theta)
+        keys = set(zip(np.repeat(np.arange(len(r["pair_count"])), r["pair_count"]).tolist(),
+                       r["parent"].tolist()))
+        if prev is not None:
+            assert keys <= prev
+        prev = keys
+        if theta < 0:
+            assert len(keys) == len(genomes) * len(srcs) * oracle.n_parents(D)
+        if theta == math.inf:
+            assert len(keys) == 0
+
+
+def test_shared_and_csr_sources_agree():
+    genomes = W.population(7, 3, 6, 15)
+    srcs = W.xor_sources()
+    a = oracle.discover(genomes, srcs, 4, 0.01)
+    csr_src = np.concatenate([srcs] * 3)
+    b = oracle.discover(genomes, csr_src, 4, 0.01, src_offsets=[0, 4, 8, 12])
+    for k in ("pair_count", "parent", "w4", "var"):
+        np.testing.assert_array_equal(a[k], b[k])
