@@ -1,0 +1,148 @@
+#!/usr/bin/env python3
+"""Benchmark of eager multi-resolution substrate discovery on one MI355X.
+
+One step = one emr_discover call over the whole workload (bind the sources, query every
+(genome, source, position), variance filter, ordered compaction) plus emr_result_check (the
+synchronizing count check). The packed population is resident in HBM before timing starts.
+Printed as one JSON line:
+
+  value        CPPN queries per second over the timed steps (host clock, synchronized)
+  roofline     the dominant discover-kernel launch: algorithmic VALU lane-slots (cost model of
+               emr_discover_cost) / its HIP-event duration, against the chip's fp32 VALU issue
+               rate without packed math: 256 CUs x 4 SIMD x 16 lanes x 2.4 GHz = 39.32 T slots/s
+  ms_per_gen   pack (host + upload) + discover + check, host clock: the per-generation cost of
+               discovery in an evolution loop
+  cpu_baseline the CPU oracle on a bounded, stated sample of the same workload
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+VALU_PEAK_SLOTS = 256 * 4 * 16 * 2.4e9  # lane-slots per second
+METRIC = "CPPN queries/sec incl. variance filter (% VALU peak); ms/gen pop1000 depth7"
+
+
+def cpu_baseline(genomes, sources, depth, theta32, target_s):
+    """The oracle, as it stands, on the first n genomes (all sources) sized to ~target_s."""
+    import oracle
+    n = min(4, len(genomes))
+    t0 = time.perf_counter()
+    oracle.discover(genomes[:n], sources, depth, theta32)
+    t = time.perf_counter() - t0
+    n = int(min(len(genomes), max(n, round(n * target_s / max(t, 1e-3)))))
+    t0 = time.perf_counter()
+    oracle.discover(genomes[:n], sources, depth, theta32)
+    t = time.perf_counter() - t0
+    q = n * len(sources) * oracle.n_positions(depth)
+    return {"value": q / t, "unit": "queries/s", "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": "first %d of %d genomes x %d sources at depth %d (%d queries, %.1f s)"
+                      % (n, len(genomes), len(sources), depth, q, t)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="xor_pop1000_d7")
+    ap.add_argument("--transcendental-slots", type=float, default=4.0)
+    ap.add_argument("--gens", type=int, default=5, help="generations timed for ms_per_gen")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the discovery path has no cross-GPU step and this "
+              "build runs on a single MI355X (--gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_27612_amd import emr, workloads as W
+
+    torch.cuda.set_device(0)
+    genomes, sources, depth, theta = W.workload(args.workload)
+    theta32 = float(np.float32(theta))
+    rT = args.transcendental_slots
+
+    pop = emr.emr_pack_population(genomes)
+    res = emr.alloc_result(pop, sources, depth)
+    slots, queries = emr.emr_discover_cost(pop, sources, depth, transcendental_slots=rT)
+
+    for _ in range(args.warmup):
+        emr.emr_discover(pop, sources, depth, theta32, res=res)
+        emr.emr_result_check(res)
+
+    emr.emr_profile_enable(True, rT)
+    launch_ms = {}
+    launch_slots = {}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        emr.emr_discover(pop, sources, depth, theta32, res=res)
+        emr.emr_result_check(res)
+        for rec in emr.emr_profile_read():
+            key = (rec["S"], rec["W"])
+            launch_ms.setdefault(key, []).append(rec["ms"])
+            launch_slots[key] = rec["slots"]
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    emr.emr_profile_enable(False)
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    value = queries / (ms_per_step * 1e-3)
+    records = int(res["pair_count"].clamp(max=res["pair_capacity"]).sum().item())
+
+    # the dominant discover launch: largest total time
+    key = max(launch_ms, key=lambda k: sum(launch_ms[k]))
+    avg_ms = float(np.mean(launch_ms[key]))
+    achieved = launch_slots[key] / (avg_ms * 1e-3)
+    all_ms = sum(float(np.mean(v)) for v in launch_ms.values())
+
+    # ms per generation: pack + discover + check on the host clock
+    torch.cuda.synchronize()
+    g0 = time.perf_counter()
+    for _ in range(args.gens):
+        p = emr.emr_pack_population(genomes)
+        emr.emr_discover(p, sources, depth, theta32, res=res)
+        emr.emr_result_check(res)
+        del p
+    ms_per_gen = (time.perf_counter() - g0) * 1e3 / args.gens
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "genomes": len(genomes), "sources": len(sources),
+                   "depth": depth, "theta": theta, "queries_per_step": int(queries),
+                   "records_per_step": records},
+        "ms_per_gen": ms_per_gen,
+        "valu_frac_all_launches": (slots / (all_ms * 1e-3)) / VALU_PEAK_SLOTS,
+        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_SLOTS / 1e12,
+                     "unit": "TOP/s", "frac": achieved / VALU_PEAK_SLOTS, "traffic": None,
+                     "kernel": "k_discover<S=%d,W=%d>" % key, "kernel_ms": avg_ms,
+                     "transcendental_slots": rT},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(genomes, sources, depth, theta32, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

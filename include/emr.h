@@ -1,0 +1,215 @@
+/*
+ * emr.h - C ABI of the MI355X (gfx950) eager multi-resolution substrate discovery library.
+ *
+ * The method (EMR-HyperNEAT, Phase 1): build the multiresolution grid of cell centres for every
+ * level (Section 3.1, Eq. 1), query every (genome, source node, position) with the genome's CPPN in
+ * one batched pass over a population (Section 3.1, the batched query W), then keep the four
+ * children of every cell whose children's variance exceeds theta (Section 3.2, Eq. 2, and the
+ * proof of the Superset Discovery theorem), compacting the survivors.
+ *
+ * General rules
+ *   - Every call returns emr_status; nothing throws across the ABI. On failure a message is
+ *     available from emr_last_error() (thread-local, owned by the library, valid until the calling
+ *     thread's next call).
+ *   - "host" pointers are ordinary CPU memory owned by the caller and only read during the call.
+ *     "device" pointers are gfx950 global memory owned by the caller.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream). Device work is
+ *     enqueued on it asynchronously unless the call says it synchronizes.
+ *   - Argument and genome validation happens on the host before anything is enqueued; on such an
+ *     error nothing is written.
+ *
+ * Depth convention: depth D counts levels below the root cell [-1,1]^2. Level l (1..D) has 4^l cells
+ * of width 2/2^l centred at ((2i+1)/2^l - 1, (2j+1)/2^l - 1). The paper's depth d_p (Eq. 1 starts
+ * with 4 cells at d = 0) is D - 1 here. The root is never queried; it is the parent of level 1.
+ *
+ * Cell numbering (heap order): the root is 0; the children of cell F are 4F+1 .. 4F+4; child k
+ * (k = 0..3) lies on the +x side if bit 0 of k is set and on the +y side if bit 1 is set. Queried
+ * positions are cells F = 1 .. N(D), stored at grid index p = F - 1. Parents are F = 0 .. Q(D)-1.
+ *   N(D) = (4^(D+1) - 4) / 3 positions,  Q(D) = (4^D - 1) / 3 parents.
+ */
+#ifndef EMR_H
+#define EMR_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  EMR_OK = 0,
+  EMR_E_INVAL = -1,    /* bad argument */
+  EMR_E_CYCLE = -2,    /* a genome's enabled edges contain a cycle */
+  EMR_E_LIMIT = -3,    /* a genome or call exceeds a documented limit */
+  EMR_E_NOMEM = -4,    /* host or device allocation failed */
+  EMR_E_CAPACITY = -5, /* some pair found more records than the output region holds */
+  EMR_E_DEVICE = -6,   /* a HIP runtime call failed, or no gfx950 device */
+  EMR_E_ABORTED = -7   /* a streaming sink asked to stop */
+} emr_status;
+
+/* Message for the calling thread's last failed call ("" if none). */
+const char* emr_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t emr_version(void);
+
+/* ------------------------------------------------------------------ genomes (Section 2) */
+
+/* Activation ids. linear z; sigmoid 1/(1+e^-z); tanh z; gaussian e^(-z^2); sine sin z; abs |z|. */
+enum { EMR_ACT_LINEAR = 0, EMR_ACT_SIGMOID = 1, EMR_ACT_TANH = 2, EMR_ACT_GAUSS = 3,
+       EMR_ACT_SINE = 4, EMR_ACT_ABS = 5 };
+
+/* Node kinds. The five input roles feed the CPPN tuple (x1, y1, x2, y2, 1) of Section 2. */
+enum { EMR_IN_X1 = 0, EMR_IN_Y1 = 1, EMR_IN_X2 = 2, EMR_IN_Y2 = 3, EMR_IN_BIAS = 4,
+       EMR_NODE_HIDDEN = 5, EMR_NODE_OUTPUT = 6 };
+
+/* Query direction of a source node s at grid position p: outgoing evaluates CPPN(s, p), i.e.
+ * (x1, y1) = s and (x2, y2) = p; incoming evaluates CPPN(p, s). */
+enum { EMR_DIR_OUT = 0, EMR_DIR_IN = 1 };
+
+/* One NEAT CPPN genome (host memory, caller-owned, read only during emr_pack_population).
+ * A non-input node computes act(bias + sum of w * v_src over its enabled incoming edges).
+ * Rules: exactly one output node; each input role at most once (a missing role contributes
+ * nothing); edge endpoints in range; no edge into an input node; the enabled edges form a DAG. */
+typedef struct {
+  int32_t n_nodes, n_edges;
+  const uint8_t* kind;    /* [n_nodes] EMR_IN_* / EMR_NODE_* */
+  const uint8_t* act;     /* [n_nodes] EMR_ACT_*; ignored for input nodes */
+  const float* bias;      /* [n_nodes] or NULL (all zero) */
+  const int32_t* src;     /* [n_edges] node ids */
+  const int32_t* dst;     /* [n_edges] node ids */
+  const float* w;         /* [n_edges] */
+  const uint8_t* enabled; /* [n_edges] or NULL (all enabled) */
+} emr_genome;
+
+/* A substrate source node (host memory). */
+typedef struct {
+  float x, y;
+  int32_t dir; /* EMR_DIR_OUT or EMR_DIR_IN */
+} emr_source;
+
+/* ------------------------------------------------------------------ grid (Section 3.1, Eq. 1) */
+
+/* N(D) positions and Q(D) parents for depth D (0 <= D <= EMR_MAX_DEPTH). Host only. */
+#define EMR_MAX_DEPTH 15
+emr_status emr_grid_count(int32_t depth, int64_t* n_positions, int64_t* n_parents);
+
+/* Writes the centre of every queried position in heap order: xy_dev[2p], xy_dev[2p+1] for
+ * p = 0 .. N(D)-1 (device, caller-owned, 2*N(D) floats). Coordinates are exact in fp32. */
+emr_status emr_build_grids(int32_t depth, float* xy_dev, void* stream);
+
+/* ------------------------------------------------------------------ packing (Section 3.1) */
+
+/* Opaque, library-owned packed population: per genome, one program per query direction holding
+ * only the nodes whose value varies with the grid position, in topological order, with register
+ * slots assigned by liveness; plus the position-independent part, evaluated once per
+ * (genome, source). Immutable after packing; may be used from several streams at once. */
+typedef struct emr_population emr_population;
+
+/* Limits of one genome after dead-node pruning. */
+#define EMR_MAX_NODES 256   /* nodes in the genome as given */
+#define EMR_MAX_EDGES 4096  /* edges in the genome as given */
+#define EMR_MAX_LIVE 64     /* position-dependent values alive at once */
+
+/* Validates and packs n genomes, then copies the tables to the current device (synchronously).
+ * On a validation failure returns EMR_E_INVAL / EMR_E_CYCLE / EMR_E_LIMIT and sets *bad_index to
+ * the first failing genome (else -1); *out is set only on success. */
+emr_status emr_pack_population(const emr_genome* genomes, int32_t n, emr_population** out,
+                               int32_t* bad_index);
+void emr_free_population(emr_population* pop);
+
+/* Per-genome facts of a packed population (host arrays of n_genomes, any may be NULL):
+ * varying steps and position-dependent edges per direction (index [2g + dir]) and the register
+ * window the kernel needs. */
+emr_status emr_population_info(const emr_population* pop, int32_t* n_genomes, int32_t* steps2,
+                               int32_t* var_edges2, int32_t* window);
+
+/* ------------------------------------------------------------------ discovery (Section 3.2) */
+
+/* Pairs. With src_offsets == NULL every genome uses the same n_shared sources and
+ * pair = g * n_shared + j. Otherwise src_offsets (host, [n_genomes+1], ascending, starting at 0)
+ * gives genome g the sources src_offsets[g] .. src_offsets[g+1]-1 and pair = that source index. */
+
+/* Output of emr_discover (device buffers, caller-owned).
+ * Records of pair r occupy the region [r*pair_capacity, (r+1)*pair_capacity): record i of that
+ * pair is parent[r*pair_capacity + i] (the heap index of a kept cell) and
+ * w4[4*(r*pair_capacity + i) + k] (the CPPN output at its child k), in ascending parent order,
+ * for i < min(pair_count[r], pair_capacity). pair_count[r] is the true count; a count above
+ * pair_capacity is an overflow (reported by emr_result_check) whose excess records are dropped.
+ * pair_capacity = Q(D) can never overflow. */
+typedef struct {
+  uint32_t* parent;      /* [n_pairs * pair_capacity] */
+  float* w4;             /* [n_pairs * pair_capacity * 4] */
+  int64_t pair_capacity; /* records per pair region, >= 0 */
+  int64_t* pair_count;   /* [n_pairs] */
+  void* workspace;       /* device scratch, >= emr_workspace_bytes(...) bytes, 256-byte aligned */
+  int64_t workspace_bytes;
+} emr_result;
+
+/* Device scratch (bytes) needed by emr_discover / emr_eval_raw for this population, these
+ * sources (host) and this depth: look-back tile status words, per-call group tables and the
+ * folded per-(genome, source) biases. Host only. */
+emr_status emr_workspace_bytes(const emr_population* pop, const emr_source* sources,
+                               int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                               int32_t depth, int64_t* bytes);
+
+/*
+ * Eager discovery: for every pair (genome g, source s) and every parent cell P (levels 0..D-1),
+ * queries the CPPN of g at the four children of P, computes their population variance
+ *   mu = ((w0+w1)+(w2+w3)) / 4,  var = ((d0^2+d1^2)+(d2^2+d3^2)) / 4,  d_k = w_k - mu,
+ * and keeps P when var > theta (strict; NaN never kept). fp32 throughout.
+ * `sources` is host memory (n_sources entries, n_sources = n_shared or src_offsets[n_genomes]).
+ * Enqueued on `stream`; the host returns after staging small per-call tables.
+ * The workspace must not be shared by calls that overlap in time.
+ */
+emr_status emr_discover(const emr_population* pop, const emr_source* sources, int32_t n_sources,
+                        const int32_t* src_offsets, int32_t n_shared, int32_t depth, float theta,
+                        const emr_result* out, void* stream);
+
+/* Synchronizes `stream`, then reports EMR_E_CAPACITY if any pair_count exceeds pair_capacity
+ * (*max_count receives the largest count, so a retry can size the regions), or EMR_E_DEVICE if
+ * the kernel flagged an internal error. n_pairs is the number of pairs of the discover call. */
+emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max_count,
+                            void* stream);
+
+/*
+ * Raw CPPN outputs (debug and parity): out_dev[r * N(D) + p] = CPPN output of pair r at grid
+ * position p (device, caller-owned, n_pairs * N(D) floats). Same arithmetic as emr_discover.
+ */
+emr_status emr_eval_raw(const emr_population* pop, const emr_source* sources, int32_t n_sources,
+                        const int32_t* src_offsets, int32_t n_shared, int32_t depth, float* out_dev,
+                        void* workspace, int64_t workspace_bytes, void* stream);
+
+/* Algorithmic VALU work of one emr_discover call under the cost model documented with the
+ * benchmark: total lane-operation slots (*slots) and number of queries (*queries). Host only. */
+emr_status emr_discover_cost(const emr_population* pop, const emr_source* sources,
+                             int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                             int32_t depth, double transcendental_slots, double* slots,
+                             double* queries);
+
+/* ------------------------------------------------------------------ profiling */
+
+/* One discover-kernel launch of the last profiled emr_discover / emr_eval_raw call on this thread:
+ * its variant (sources per lane S, register window W), tiles, queries, algorithmic VALU slots
+ * under the cost model of emr_discover_cost, and its duration from a HIP event pair recorded on
+ * the call's stream around the launch. */
+typedef struct {
+  int32_t group_size, window;
+  int64_t tiles, queries;
+  double slots;
+  float ms;
+} emr_launch_profile;
+
+/* Enables (on != 0) or disables per-launch event timing for the calling thread's later calls;
+ * transcendental_slots is the cost-model weight used for `slots`. Host only. */
+emr_status emr_profile_enable(int32_t on, double transcendental_slots);
+
+/* Synchronizes on the last profiled call's events and writes up to `cap` launch records to
+ * `out` (host); *n receives the number of launches of that call. */
+emr_status emr_profile_read(emr_launch_profile* out, int32_t cap, int32_t* n);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EMR_H */

@@ -1,0 +1,131 @@
+// Internal data layout shared by the host runtime and the gfx950 kernels.
+//
+// A packed population is one device array of 32-bit words ("blob") plus one ProgDesc per
+// (genome, query direction). For a direction, the CPPN inputs split into two that vary with the
+// grid position (the position's x and y) and three that do not (the source's x and y, and the
+// constant 1). Every live node is then either position-dependent ("varying") or a per-(genome,
+// source) constant ("uniform"):
+//   - the varying program is what one GPU lane interprets per position;
+//   - the uniform program is evaluated once per (genome, source) by the bind kernel, which folds
+//     every uniform contribution into a per-step bias (and, when the output itself is uniform,
+//     produces the output constant).
+#pragma once
+#include <stdint.h>
+
+#if defined(__HIPCC__) || defined(__HIP__)
+#define EMR_HD __host__ __device__
+#else
+#define EMR_HD
+#endif
+
+namespace emr {
+
+// Kernel window sizes (register slots per source) the kernels are instantiated for.
+constexpr int kWindows[] = {8, 16, 32};
+constexpr int kMaxWindow = 32;
+// Sources evaluated together by one lane (same genome, same direction).
+constexpr int kMaxGroup = 4;
+// Positions per wave iteration and iterations per tile.
+constexpr int kWave = 64;
+constexpr int kTileIters = 4;
+constexpr int kTile = kWave * kTileIters;  // 256 = 4^4 positions
+constexpr int kFirstAlignedLevel = 4;     // first level whose size is a multiple of kTile
+
+// ---------------------------------------------------------------- varying program
+// At blob[var_off]: n_steps step records of 4 words, then the edge words they point to.
+//   step word 0: act | dst_slot << 8
+//   step word 1: n_x | n_y << 8 | n_node << 16   (edges from the position's x, then from its y,
+//                                                 then from earlier varying nodes)
+//   step word 2: absolute word offset of the step's first edge in the blob
+//   step word 3: 0
+//   edge: two words {src, float bits of w}; src is 0 for an x edge, 1 for a y edge, and the
+//   register slot of the source node for a node edge.
+// The step's bias is not stored here: it is the per-source folded bias from the bind kernel.
+// The last step computes the output when the output is varying; its dst slot is unused.
+struct StepWords {
+  uint32_t meta0, meta1, edge_off, pad;
+};
+
+// ---------------------------------------------------------------- uniform program
+// At blob[uni_off]:
+//   header 4 words: n_unodes, out_u (index into U of the output, or kNone when it varies),
+//                   n_steps (of the varying program), 0
+//   n_unodes records of 4 words: act, n_edges, edge_off, bias bits      -> U[5 + k]
+//   n_steps  records of 4 words: n_fold, fold_off, bias bits, 0         -> folded bias of step i
+//   edges: {u_src, w bits}; U[0..4] hold the five input roles (x1, y1, x2, y2, 1).
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+
+struct ProgDesc {
+  uint32_t var_off;   // word offset of the varying program
+  uint32_t n_steps;   // varying steps
+  uint32_t uni_off;   // word offset of the uniform program
+  uint32_t flags;     // bit 0: output varies with position; bits 8..15: register window needed
+};
+
+// One unit of kernel work: up to kMaxGroup sources of one genome sharing a direction.
+struct Group {
+  uint32_t var_off;
+  uint32_t n_steps;
+  uint32_t flags;      // copied from ProgDesc
+  uint32_t bias_off;   // float offset into the bias table: [step][member], then out constants
+  uint32_t pair[kMaxGroup];  // global pair ids of the members (unused members repeat the last)
+};
+
+// One (genome, direction, source) evaluated by the bind kernel.
+struct Member {
+  uint32_t desc;       // ProgDesc index = 2 * genome + dir
+  uint32_t source;     // source index
+  uint32_t bias_base;  // first float written in the bias table
+  uint32_t stride;     // distance between consecutive steps' entries (the group size)
+};
+
+// Look-back tile status word: flag in bits 62..63, value in bits 0..61.
+constexpr uint64_t kStatusAggregate = 1ull << 62;
+constexpr uint64_t kStatusInclusive = 2ull << 62;
+constexpr uint64_t kStatusValueMask = (1ull << 62) - 1;
+
+// Level helpers shared by host and device.
+EMR_HD inline int64_t level_offset(int level) {  // first grid index of level >= 1
+  return ((int64_t(1) << (2 * level)) - 4) / 3;
+}
+EMR_HD inline int64_t n_positions(int depth) { return level_offset(depth + 1); }
+EMR_HD inline int64_t n_parents(int depth) {
+  return depth <= 0 ? 0 : ((int64_t(1) << (2 * depth)) - 1) / 3;
+}
+// Tiles per (pair, depth): one "head" tile for levels 1..kFirstAlignedLevel-1 (or all levels when
+// the depth is smaller), then kTile-sized tiles that never straddle a level.
+EMR_HD inline int64_t tiles_per_pair(int depth) {
+  if (depth < kFirstAlignedLevel) return 1;
+  return 1 + (n_positions(depth) - level_offset(kFirstAlignedLevel)) / kTile;
+}
+
+struct DiscoverArgs {
+  const uint32_t* blob;
+  const Group* groups;
+  const float* bias_tab;
+  uint64_t* status;        // [n_pairs_total * tiles]
+  uint32_t* err;           // device error flags
+  uint32_t* parent;
+  float* w4;
+  int64_t* pair_count;
+  float* raw;              // raw-output mode: [pair][N]
+  int64_t cap;             // records per pair region
+  int64_t n_pos;           // N(depth)
+  uint32_t n_groups;
+  uint32_t tiles;          // tiles per pair
+  uint32_t n_tiles;        // n_groups * tiles
+  int32_t depth;
+  float theta;
+  uint32_t group_size;     // members per group (S) for this launch
+};
+
+struct BindArgs {
+  const uint32_t* blob;
+  const ProgDesc* desc;
+  const Member* members;
+  const float* src_xy;     // [n_sources * 2]
+  float* bias_tab;
+  uint32_t n_members;
+};
+
+}  // namespace emr

@@ -1,0 +1,672 @@
+// gfx950 kernels for eager multi-resolution substrate discovery.
+//
+//   k_grid      writes the cell centres of every queried position (Section 3.1, Eq. 1).
+//   k_fill      clears the look-back status words and counters of a workspace.
+//   k_bind      evaluates the position-independent part of each (genome, source) CPPN once and
+//               folds it into per-step biases (one thread per source).
+//   k_discover  the hot path: one lane per grid position; each lane interprets the varying CPPN
+//               program for S sources of one genome at once (Section 3.1, the batched query W),
+//               reduces the four siblings of each cell to their variance with DPP quad
+//               permutes, applies var > theta (Section 3.2, Eq. 2), and compacts the kept cells
+//               with a wave ballot plus a per-pair decoupled look-back scan, so every pair's
+//               records land in ascending parent order with no second pass and no atomics on
+//               the output.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/emr.h"
+#include "emr_internal.h"
+
+namespace emr {
+
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x32 __attribute__((ext_vector_type(32)));
+
+// ------------------------------------------------------------------------ activations
+// Hardware v_exp_f32 (2^x), v_rcp_f32 and v_sin_f32 (sin of 2*pi*x) with the range reductions
+// their inputs need. Errors stay near 1e-7 absolute for |z| up to a few hundred.
+constexpr float kLog2e = 1.44269504088896341f;
+constexpr float kInv2Pi = 0.159154943091895336f;
+constexpr float k2PiHi = 6.28318548202514648f;      // nearest float to 2*pi
+constexpr float k2PiLo = -1.74845553146951720e-07f; // 2*pi - k2PiHi
+
+__device__ __forceinline__ float act_sigmoid(float z) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-kLog2e * z));
+}
+__device__ __forceinline__ float act_tanh(float z) {
+  // tanh|z| = (1 - e^{-2|z|}) / (1 + e^{-2|z|}); absolute error ~2 ulp(1) near 0.
+  float t = __builtin_amdgcn_exp2f(-2.0f * kLog2e * __builtin_fabsf(z));
+  float r = (1.0f - t) * __builtin_amdgcn_rcpf(1.0f + t);
+  return __builtin_copysignf(r, z);
+}
+__device__ __forceinline__ float act_gauss(float z) {
+  return __builtin_amdgcn_exp2f(-kLog2e * (z * z));
+}
+__device__ __forceinline__ float act_sine(float z) {
+  // Cody-Waite reduction by 2*pi (two-part constant), then the hardware sine in revolutions.
+  float k = __builtin_rintf(z * kInv2Pi);
+  float r = __builtin_fmaf(-k, k2PiHi, z);
+  r = __builtin_fmaf(-k, k2PiLo, r);
+  return __builtin_amdgcn_sinf(r * kInv2Pi);
+}
+__device__ __forceinline__ float act_apply(uint32_t a, float z) {
+  switch (a) {
+    case EMR_ACT_SIGMOID: return act_sigmoid(z);
+    case EMR_ACT_TANH: return act_tanh(z);
+    case EMR_ACT_GAUSS: return act_gauss(z);
+    case EMR_ACT_SINE: return act_sine(z);
+    case EMR_ACT_ABS: return __builtin_fabsf(z);
+    default: return z;
+  }
+}
+
+// ------------------------------------------------------------------------ position decode
+__device__ __forceinline__ uint32_t compact_even(uint32_t x) {  // bits 0,2,4,.. -> 0,1,2,..
+  x &= 0x55555555u;
+  x = (x | (x >> 1)) & 0x33333333u;
+  x = (x | (x >> 2)) & 0x0F0F0F0Fu;
+  x = (x | (x >> 4)) & 0x00FF00FFu;
+  x = (x | (x >> 8)) & 0x0000FFFFu;
+  return x;
+}
+__device__ __forceinline__ float pow2_neg(int l) {  // 2^-l, exact
+  return __int_as_float((127 - l) << 23);
+}
+// Level of grid index p: 3(p+1)+1 lies in [4^l, 4^(l+1)).
+__device__ __forceinline__ int level_of(uint32_t p) {
+  return (31 - __builtin_clz(3u * p + 4u)) >> 1;
+}
+
+// ------------------------------------------------------------------------ wave helpers
+__device__ __forceinline__ uint32_t lane_id() {
+  return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+// Sum over the 4 lanes of a quad, pairwise: (w0+w1)+(w2+w3), bit-identical in all 4 lanes.
+__device__ __forceinline__ float quad_sum(float v) {
+  float t = v + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));
+  return t + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(t), 0x4E, 0xF, 0xF, false));
+}
+__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+__device__ __forceinline__ uint32_t popc64(uint64_t m) { return __builtin_popcountll(m); }
+__device__ __forceinline__ uint32_t mbcnt64(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// ------------------------------------------------------------------------ register windows
+// The varying values of member s live in a VGPR tuple pinned at v[32 + s*W .. 32 + s*W + W-1].
+// One s_set_gpr_idx_on per edge indexes the same slot in every member's tuple, so the S fused
+// multiply-adds of an edge share one index setup. The tuples are declared as asm operands, so the
+// compiler keeps them in place and knows which registers each statement reads or writes.
+// s_set_gpr_idx_on also writes M0; M0 is reserved by the compiler and this kernel has no other
+// use of it (no LDS DMA, no message or GWS instructions), which the ISA check in the tests
+// enforces.
+template <int W> struct Win;
+
+#define EMR_DEFINE_WIN(W_, T_, R0, R1, R2, R3)                                                    \
+  template <> struct Win<W_> {                                                                  \
+    T_ v0, v1, v2, v3;                                                                          \
+    __device__ __forceinline__ void init() {                                                    \
+      v0 = (T_)(0.0f); v1 = (T_)(0.0f); v2 = (T_)(0.0f); v3 = (T_)(0.0f);                       \
+    }                                                                                           \
+    template <int S>                                                                            \
+    __device__ __forceinline__ void fma(float* a, uint32_t src, float w) {                      \
+      if constexpr (S == 1) {                                                                   \
+        asm volatile("s_set_gpr_idx_on %[src], gpr_idx(SRC0)\n\t"                               \
+                     "v_fma_f32 %[a0], " R0##_B ", %[w], %[a0]\n\t"                             \
+                     "s_set_gpr_idx_off"                                                        \
+                     : [a0] "+v"(a[0])                                                          \
+                     : [src] "s"(src), [w] "s"(w), R0##_C(v0)                                   \
+                     :);                                                                   \
+      } else if constexpr (S == 2) {                                                            \
+        asm volatile("s_set_gpr_idx_on %[src], gpr_idx(SRC0)\n\t"                               \
+                     "v_fma_f32 %[a0], " R0##_B ", %[w], %[a0]\n\t"                             \
+                     "v_fma_f32 %[a1], " R1##_B ", %[w], %[a1]\n\t"                             \
+                     "s_set_gpr_idx_off"                                                        \
+                     : [a0] "+v"(a[0]), [a1] "+v"(a[1])                                         \
+                     : [src] "s"(src), [w] "s"(w), R0##_C(v0), R1##_C(v1)                       \
+                     :);                                                                   \
+      } else if constexpr (S == 3) {                                                            \
+        asm volatile("s_set_gpr_idx_on %[src], gpr_idx(SRC0)\n\t"                               \
+                     "v_fma_f32 %[a0], " R0##_B ", %[w], %[a0]\n\t"                             \
+                     "v_fma_f32 %[a1], " R1##_B ", %[w], %[a1]\n\t"                             \
+                     "v_fma_f32 %[a2], " R2##_B ", %[w], %[a2]\n\t"                             \
+                     "s_set_gpr_idx_off"                                                        \
+                     : [a0] "+v"(a[0]), [a1] "+v"(a[1]), [a2] "+v"(a[2])                        \
+                     : [src] "s"(src), [w] "s"(w), R0##_C(v0), R1##_C(v1), R2##_C(v2)           \
+                     :);                                                                   \
+      } else {                                                                                  \
+        asm volatile("s_set_gpr_idx_on %[src], gpr_idx(SRC0)\n\t"                               \
+                     "v_fma_f32 %[a0], " R0##_B ", %[w], %[a0]\n\t"                             \
+                     "v_fma_f32 %[a1], " R1##_B ", %[w], %[a1]\n\t"                             \
+                     "v_fma_f32 %[a2], " R2##_B ", %[w], %[a2]\n\t"                             \
+                     "v_fma_f32 %[a3], " R3##_B ", %[w], %[a3]\n\t"                             \
+                     "s_set_gpr_idx_off"                                                        \
+                     : [a0] "+v"(a[0]), [a1] "+v"(a[1]), [a2] "+v"(a[2]), [a3] "+v"(a[3])       \
+                     : [src] "s"(src), [w] "s"(w), R0##_C(v0), R1##_C(v1), R2##_C(v2),          \
+                       R3##_C(v3)                                                               \
+                     :);                                                                   \
+      }                                                                                         \
+    }                                                                                           \
+    template <int S>                                                                            \
+    __device__ __forceinline__ void store(uint32_t dst, const float* r) {                       \
+      if constexpr (S == 1) {                                                                   \
+        asm volatile("s_set_gpr_idx_on %[dst], gpr_idx(DST)\n\t"                                \
+                     "v_mov_b32 " R0##_B ", %[r0]\n\t"                                          \
+                     "s_set_gpr_idx_off"                                                        \
+                     : R0##_O(v0)                                                               \
+                     : [dst] "s"(dst), [r0] "v"(r[0])                                           \
+                     :);                                                                   \
+      } else if constexpr (S == 2) {                                                            \
+        asm volatile("s_set_gpr_idx_on %[dst], gpr_idx(DST)\n\t"                                \
+                     "v_mov_b32 " R0##_B ", %[r0]\n\t"                                          \
+                     "v_mov_b32 " R1##_B ", %[r1]\n\t"                                          \
+                     "s_set_gpr_idx_off"                                                        \
+                     : R0##_O(v0), R1##_O(v1)                                                   \
+                     : [dst] "s"(dst), [r0] "v"(r[0]), [r1] "v"(r[1])                           \
+                     :);                                                                   \
+      } else if constexpr (S == 3) {                                                            \
+        asm volatile("s_set_gpr_idx_on %[dst], gpr_idx(DST)\n\t"                                \
+                     "v_mov_b32 " R0##_B ", %[r0]\n\t"                                          \
+                     "v_mov_b32 " R1##_B ", %[r1]\n\t"                                          \
+                     "v_mov_b32 " R2##_B ", %[r2]\n\t"                                          \
+                     "s_set_gpr_idx_off"                                                        \
+                     : R0##_O(v0), R1##_O(v1), R2##_O(v2)                                       \
+                     : [dst] "s"(dst), [r0] "v"(r[0]), [r1] "v"(r[1]), [r2] "v"(r[2])           \
+                     :);                                                                   \
+      } else {                                                                                  \
+        asm volatile("s_set_gpr_idx_on %[dst], gpr_idx(DST)\n\t"                                \
+                     "v_mov_b32 " R0##_B ", %[r0]\n\t"                                          \
+                     "v_mov_b32 " R1##_B ", %[r1]\n\t"                                          \
+                     "v_mov_b32 " R2##_B ", %[r2]\n\t"                                          \
+                     "v_mov_b32 " R3##_B ", %[r3]\n\t"                                          \
+                     "s_set_gpr_idx_off"                                                        \
+                     : R0##_O(v0), R1##_O(v1), R2##_O(v2), R3##_O(v3)                           \
+                     : [dst] "s"(dst), [r0] "v"(r[0]), [r1] "v"(r[1]), [r2] "v"(r[2]),          \
+                       [r3] "v"(r[3])                                                           \
+                     :);                                                                   \
+      }                                                                                         \
+    }                                                                                           \
+  };
+
+// Base register name (_B), input constraint (_C) and in/out constraint (_O) of each tuple.
+#define W8_0_B "v32"
+#define W8_0_C(x) "{v[32:39]}"(x)
+#define W8_0_O(x) "+{v[32:39]}"(x)
+#define W8_1_B "v40"
+#define W8_1_C(x) "{v[40:47]}"(x)
+#define W8_1_O(x) "+{v[40:47]}"(x)
+#define W8_2_B "v48"
+#define W8_2_C(x) "{v[48:55]}"(x)
+#define W8_2_O(x) "+{v[48:55]}"(x)
+#define W8_3_B "v56"
+#define W8_3_C(x) "{v[56:63]}"(x)
+#define W8_3_O(x) "+{v[56:63]}"(x)
+
+#define W16_0_B "v32"
+#define W16_0_C(x) "{v[32:47]}"(x)
+#define W16_0_O(x) "+{v[32:47]}"(x)
+#define W16_1_B "v48"
+#define W16_1_C(x) "{v[48:63]}"(x)
+#define W16_1_O(x) "+{v[48:63]}"(x)
+#define W16_2_B "v64"
+#define W16_2_C(x) "{v[64:79]}"(x)
+#define W16_2_O(x) "+{v[64:79]}"(x)
+#define W16_3_B "v80"
+#define W16_3_C(x) "{v[80:95]}"(x)
+#define W16_3_O(x) "+{v[80:95]}"(x)
+
+#define W32_0_B "v32"
+#define W32_0_C(x) "{v[32:63]}"(x)
+#define W32_0_O(x) "+{v[32:63]}"(x)
+#define W32_1_B "v64"
+#define W32_1_C(x) "{v[64:95]}"(x)
+#define W32_1_O(x) "+{v[64:95]}"(x)
+#define W32_2_B "v96"
+#define W32_2_C(x) "{v[96:127]}"(x)
+#define W32_2_O(x) "+{v[96:127]}"(x)
+#define W32_3_B "v128"
+#define W32_3_C(x) "{v[128:159]}"(x)
+#define W32_3_O(x) "+{v[128:159]}"(x)
+
+EMR_DEFINE_WIN(8, f32x8, W8_0, W8_1, W8_2, W8_3)
+EMR_DEFINE_WIN(16, f32x16, W16_0, W16_1, W16_2, W16_3)
+EMR_DEFINE_WIN(32, f32x32, W32_0, W32_1, W32_2, W32_3)
+
+// ------------------------------------------------------------------------ look-back scan
+// Tile status words of one pair, indexed by tile. A tile publishes its local count as an
+// aggregate, sums predecessors (64 per probe, one per lane) back to the nearest inclusive
+// prefix, then publishes its own inclusive prefix. The kernel is launched cooperatively (every
+// wave is resident) and each wave walks its tiles in increasing order, so the lowest unfinished
+// tile always belongs to a running wave whose earlier tiles are done: waits always end. Each wait
+// is also bounded and, if the bound were ever hit, raises an error flag instead of spinning on.
+constexpr uint32_t kSpinLimit = 1u << 22;
+constexpr uint32_t kErrLookback = 1u;
+
+__device__ __forceinline__ void status_store(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t status_load(uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ uint64_t lookback(uint64_t* row, uint32_t tile, uint64_t count, uint32_t* err) {
+  const uint32_t lane = lane_id();
+  if (tile == 0) {
+    if (lane == 0) status_store(&row[0], kStatusInclusive | count);
+    return 0;
+  }
+  if (lane == 0) status_store(&row[tile], kStatusAggregate | count);
+  uint64_t prefix = 0;
+  int64_t j = (int64_t)tile - 1;
+  uint32_t spins = 0;
+  for (;;) {
+    const int64_t idx = j - (int64_t)lane;
+    const uint64_t s = idx >= 0 ? status_load(&row[idx]) : kStatusInclusive;
+    const uint64_t flag = s >> 62;
+    const uint64_t incl = ballot(flag == 2);
+    const uint64_t empty = ballot(flag == 0);
+    const uint32_t first = incl ? (uint32_t)__builtin_ctzll(incl) : 64u;
+    const uint64_t upto = first >= 63 ? ~0ull : ((2ull << first) - 1ull);
+    if (empty & upto) {
+      if (++spins > kSpinLimit) {
+        if (lane == 0) atomicOr(err, kErrLookback);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+      continue;
+    }
+    const uint64_t mine = ((upto >> lane) & 1ull) ? (s & kStatusValueMask) : 0ull;
+    prefix += wave_sum_u64(mine);
+    if (first < 64) break;
+    j -= 64;
+  }
+  if (lane == 0) status_store(&row[tile], kStatusInclusive | (prefix + count));
+  return prefix;
+}
+
+// ------------------------------------------------------------------------ discover kernel
+// Pointers are passed as separate restrict-qualified parameters so the compiler can prove that
+// the program, group and bias tables are never written by the kernel and read them with scalar
+// loads through the scalar cache.
+struct DiscoverScalars {
+  int64_t cap, n_pos;
+  uint32_t tiles, n_tiles;
+  int32_t depth;
+  float theta;
+};
+
+// Output modes: raw CPPN outputs; records at fixed per-tile slots (pair_capacity >= Q(D), compacted
+// afterwards by k_compact); records placed directly through the look-back scan (any capacity).
+constexpr int kModeRaw = 0, kModePadded = 1, kModeLookback = 2;
+
+template <int S, int W, int MODE>
+__global__ void __launch_bounds__(256)
+    k_discover(const uint32_t* __restrict__ blob, const Group* __restrict__ groups,
+               const float* __restrict__ bias_tab, uint64_t* __restrict__ status,
+               uint32_t* __restrict__ err,
+               uint32_t* __restrict__ parent, float* __restrict__ w4,
+               int64_t* __restrict__ pair_count, float* __restrict__ raw, DiscoverScalars a) {
+  const uint32_t lane = lane_id();
+  // Within a level-aligned tile the grid index's 6 low bits are the lane id; its Morton bits give
+  // the low 3 bits of the cell's column (even bits) and row (odd bits).
+  const uint32_t i_lo = (lane & 1u) | ((lane >> 1) & 2u) | ((lane >> 2) & 4u);
+  const uint32_t j_lo = ((lane >> 1) & 1u) | ((lane >> 2) & 2u) | ((lane >> 3) & 4u);
+  const float i_lo_f = (float)(2u * i_lo);
+  const float j_lo_f = (float)(2u * j_lo);
+  const int64_t head_len = a.depth < kFirstAlignedLevel ? a.n_pos : level_offset(kFirstAlignedLevel);
+
+  Win<W> R;
+  R.init();
+
+  // Static round-robin: global wave w takes tiles w, w + n_waves, w + 2 n_waves, ... Consecutive
+  // tiles of a pair go to consecutive waves, so a pair's tiles are computed concurrently.
+  const uint32_t n_waves = gridDim.x * (blockDim.x / kWave);
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +
+                                                       threadIdx.x / kWave);
+  for (uint32_t t = wave; t < a.n_tiles; t += n_waves) {
+
+    const uint32_t gi = t / a.tiles;
+    const uint32_t tile = t - gi * a.tiles;
+    const Group G = groups[gi];
+    const bool out_varying = (G.flags & 1u) != 0;
+    const float* bt = bias_tab + G.bias_off;
+    const uint32_t* steps = blob + G.var_off;
+
+    // Tile geometry.
+    uint32_t p0, n_valid, n_iter;
+    int lvl = 0;
+    uint32_t m0 = 0;
+    const bool head = tile == 0;
+    if (head) {
+      p0 = 0;
+      n_valid = (uint32_t)head_len;
+      n_iter = (n_valid + kWave - 1) / kWave;
+    } else {
+      p0 = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(tile - 1) * kTile);
+      n_valid = kTile;
+      n_iter = kTileIters;
+      lvl = (31 - __builtin_clz(3u * p0 + 4u)) >> 1;
+      m0 = p0 - (uint32_t)level_offset(lvl);
+    }
+
+    float wbuf[kTileIters][S];
+    uint64_t keep[kTileIters][S];
+#pragma unroll
+    for (int it = 0; it < kTileIters; ++it) {
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        wbuf[it][s] = 0.0f;
+        keep[it][s] = 0ull;
+      }
+    }
+
+#pragma unroll
+    for (int it = 0; it < kTileIters; ++it) {
+      if ((uint32_t)it >= n_iter) break;
+      const uint32_t p = p0 + (uint32_t)it * kWave + lane;
+      const bool valid = (uint32_t)it * kWave + lane < n_valid;
+      float px, py;
+      if (!head) {
+        const uint32_t m_hi = (m0 >> 6) + (uint32_t)it;
+        const float scale = pow2_neg(lvl);
+        const float bx = __builtin_fmaf((float)(16u * compact_even(m_hi) + 1u), scale, -1.0f);
+        const float by = __builtin_fmaf((float)(16u * compact_even(m_hi >> 1) + 1u), scale, -1.0f);
+        px = __builtin_fmaf(i_lo_f, scale, bx);
+        py = __builtin_fmaf(j_lo_f, scale, by);
+      } else {
+        const int l = level_of(p);
+        const uint32_t m = p - (uint32_t)level_offset(l);
+        const float scale = pow2_neg(l);
+        px = __builtin_fmaf((float)(2u * compact_even(m) + 1u), scale, -1.0f);
+        py = __builtin_fmaf((float)(2u * compact_even(m >> 1) + 1u), scale, -1.0f);
+      }
+
+      // ---- CPPN: the varying program, in topological order, for the S sources at once.
+      float acc[S];
+      for (uint32_t st = 0; st < G.n_steps; ++st) {
+        const uint32_t meta0 = steps[4 * st + 0];
+        const uint32_t meta1 = steps[4 * st + 1];
+        const uint32_t eo = steps[4 * st + 2];
+#pragma unroll
+        for (int s = 0; s < S; ++s) acc[s] = bt[st * S + s];
+        const uint32_t nx = meta1 & 0xFFu, ny = (meta1 >> 8) & 0xFFu, nn = meta1 >> 16;
+        const uint32_t* ep = blob + eo;
+        for (uint32_t e = 0; e < nx; ++e) {
+          const float w = __uint_as_float(ep[2 * e + 1]);
+#pragma unroll
+          for (int s = 0; s < S; ++s) acc[s] = __builtin_fmaf(w, px, acc[s]);
+        }
+        ep += 2 * nx;
+        for (uint32_t e = 0; e < ny; ++e) {
+          const float w = __uint_as_float(ep[2 * e + 1]);
+#pragma unroll
+          for (int s = 0; s < S; ++s) acc[s] = __builtin_fmaf(w, py, acc[s]);
+        }
+        ep += 2 * ny;
+        for (uint32_t e = 0; e < nn; ++e) {
+          R.template fma<S>(acc, ep[2 * e], __uint_as_float(ep[2 * e + 1]));
+        }
+        const uint32_t act = meta0 & 0xFFu;
+#pragma unroll
+        for (int s = 0; s < S; ++s) acc[s] = act_apply(act, acc[s]);
+        if (st + 1 < G.n_steps) R.template store<S>((meta0 >> 8) & 0xFFu, acc);
+      }
+      float w[S];
+#pragma unroll
+      for (int s = 0; s < S; ++s) w[s] = out_varying ? acc[s] : bt[G.n_steps * S + s];
+
+      if constexpr (MODE == kModeRaw) {
+        if (valid) {
+#pragma unroll
+          for (int s = 0; s < S; ++s) raw[(int64_t)G.pair[s] * a.n_pos + p] = w[s];
+        }
+      } else {
+        // ---- variance of the four siblings (Section 3.2) and the threshold test (Eq. 2)
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          const float s1 = quad_sum(w[s]);
+          const float d = __builtin_fmaf(-0.25f, s1, w[s]);   // w - mean, mean = s1/4 exactly
+          const float s2 = quad_sum(__fmul_rn(d, d));
+          const float var = s2 * 0.25f;
+          keep[it][s] = ballot(valid && (var > a.theta));
+          wbuf[it][s] = w[s];
+        }
+      }
+    }
+    if constexpr (MODE == kModeRaw) continue;
+
+    // ---- compaction. Padded: the tile's records go to its own slots (the tile's first parent
+    // index within the pair), and the count is left for k_compact. Look-back: the tile learns its
+    // exact offset in the pair from the scan.
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      uint64_t cnt = 0;
+#pragma unroll
+      for (int it = 0; it < kTileIters; ++it) cnt += popc64(keep[it][s]) >> 2;
+      const uint32_t pair = G.pair[s];
+      uint64_t base;
+      if constexpr (MODE == kModePadded) {
+        base = p0 >> 2;
+        if (lane == 0) status[(int64_t)pair * a.tiles + tile] = cnt;
+      } else {
+        base = lookback(status + (int64_t)pair * a.tiles, tile, cnt, err);
+        if (tile + 1 == a.tiles && lane == 0) pair_count[pair] = (int64_t)(base + cnt);
+      }
+      const int64_t region = (int64_t)pair * a.cap;
+#pragma unroll
+      for (int it = 0; it < kTileIters; ++it) {
+        const uint64_t m = keep[it][s];
+        if ((m >> lane) & 1ull) {
+          const int64_t idx = (int64_t)base + (int64_t)(mbcnt64(m) >> 2);
+          if (idx < a.cap) {
+            w4[(region + idx) * 4 + (lane & 3u)] = wbuf[it][s];
+            if ((lane & 3u) == 0)
+              parent[region + idx] = (p0 + (uint32_t)it * kWave + lane) >> 2;
+          }
+        }
+        base += popc64(m) >> 2;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------ bind kernel
+constexpr int kMaxU = 5 + 256;
+
+__global__ void __launch_bounds__(64)
+    k_bind(const uint32_t* __restrict__ blob, const ProgDesc* __restrict__ desc,
+           const Member* __restrict__ members, const float* __restrict__ src_xy,
+           float* __restrict__ bias_tab, uint32_t n_members) {
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_members) return;
+  const Member m = members[i];
+  const ProgDesc d = desc[m.desc];
+  const uint32_t* u = blob + d.uni_off;
+  const uint32_t dir = m.desc & 1u;
+  const float sx = src_xy[2 * m.source], sy = src_xy[2 * m.source + 1];
+  float U[kMaxU];
+  // Input roles: the source fills (x1, y1) for outgoing queries and (x2, y2) for incoming ones;
+  // the position-dependent roles are never read by the uniform program.
+  U[0] = dir == 0 ? sx : 0.0f;
+  U[1] = dir == 0 ? sy : 0.0f;
+  U[2] = dir == 0 ? 0.0f : sx;
+  U[3] = dir == 0 ? 0.0f : sy;
+  U[4] = 1.0f;
+  const uint32_t n_un = u[0], out_u = u[1], n_steps = u[2];
+  const uint32_t* rec = u + 4;
+  for (uint32_t k = 0; k < n_un; ++k) {
+    float z = __uint_as_float(rec[4 * k + 3]);
+    const uint32_t* ep = blob + rec[4 * k + 2];
+    for (uint32_t e = 0; e < rec[4 * k + 1]; ++e)
+      z = __builtin_fmaf(__uint_as_float(ep[2 * e + 1]), U[ep[2 * e]], z);
+    U[5 + k] = act_apply(rec[4 * k], z);
+  }
+  const uint32_t* fold = rec + 4 * n_un;
+  for (uint32_t t = 0; t < n_steps; ++t) {
+    float z = __uint_as_float(fold[4 * t + 2]);
+    const uint32_t* ep = blob + fold[4 * t + 1];
+    for (uint32_t e = 0; e < fold[4 * t]; ++e)
+      z = __builtin_fmaf(__uint_as_float(ep[2 * e + 1]), U[ep[2 * e]], z);
+    bias_tab[m.bias_base + t * m.stride] = z;
+  }
+  bias_tab[m.bias_base + n_steps * m.stride] = out_u == kNone ? 0.0f : U[out_u];
+}
+
+// ------------------------------------------------------------------------ compaction
+// One wave per pair: scans the per-tile counts left by the padded discover pass and moves each
+// tile's records down to their final, contiguous place, tile by tile in increasing order (a
+// tile's destination never overlaps a later tile's records, and each tile's records are all
+// read before any is written). Writes the pair's count.
+__global__ void __launch_bounds__(256)
+    k_compact(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
+              float* __restrict__ w4, int64_t* __restrict__ pair_count, int64_t cap,
+              uint32_t tiles, uint32_t n_pairs) {
+  const uint32_t lane = lane_id();
+  const uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +
+                                                       threadIdx.x / kWave);
+  if (pair >= n_pairs) return;
+  const uint64_t* row = counts + (int64_t)pair * tiles;
+  const int64_t region = (int64_t)pair * cap;
+  uint32_t running = 0;
+  for (uint32_t t0 = 0; t0 < tiles; t0 += kWave) {
+    const uint32_t c = t0 + lane < tiles ? (uint32_t)row[t0 + lane] : 0u;
+    uint32_t incl = c;  // inclusive scan over the wave
+    for (int off = 1; off < kWave; off <<= 1) {
+      const uint32_t v = __shfl_up(incl, off, kWave);
+      if (lane >= (uint32_t)off) incl += v;
+    }
+    const uint32_t n_here = tiles - t0 < (uint32_t)kWave ? tiles - t0 : (uint32_t)kWave;
+    for (uint32_t i = 0; i < n_here; ++i) {
+      const uint32_t ci = __builtin_amdgcn_readlane(c, i);
+      if (ci == 0) continue;
+      const uint32_t t = t0 + i;
+      const uint32_t dst = running + __builtin_amdgcn_readlane(incl, i) - ci;
+      const uint32_t src = t == 0 ? 0u : (uint32_t)(level_offset(kFirstAlignedLevel) / 4) +
+                                             (t - 1) * (kTile / 4);
+      if (dst == src) continue;
+      if (lane < ci) {
+        const uint32_t pv = parent[region + src + lane];
+        const float4 wv = reinterpret_cast<const float4*>(w4)[region + src + lane];
+        parent[region + dst + lane] = pv;
+        reinterpret_cast<float4*>(w4)[region + dst + lane] = wv;
+      }
+    }
+    running += __builtin_amdgcn_readlane(incl, n_here - 1);
+  }
+  if (lane == 0) pair_count[pair] = running;
+}
+
+// ------------------------------------------------------------------------ small kernels
+__global__ void k_fill(uint32_t* p, int64_t n_words, uint32_t value) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n_words;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = value;
+}
+
+__global__ void k_grid(float* xy, int64_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t p = (uint32_t)i;
+    const int l = level_of(p);
+    const uint32_t m = p - (uint32_t)level_offset(l);
+    const float scale = pow2_neg(l);
+    xy[2 * i] = __builtin_fmaf((float)(2u * compact_even(m) + 1u), scale, -1.0f);
+    xy[2 * i + 1] = __builtin_fmaf((float)(2u * compact_even(m >> 1) + 1u), scale, -1.0f);
+  }
+}
+
+}  // namespace emr
+
+// ------------------------------------------------------------------------ launchers
+// Called by the host runtime (runtime.cpp); each returns the hipError_t of its launch.
+extern "C" hipError_t emr_launch_fill(void* p, int64_t n_words, uint32_t value, hipStream_t s) {
+  if (n_words <= 0) return hipSuccess;
+  int64_t blocks = (n_words + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(emr::k_fill, dim3((uint32_t)blocks), dim3(256), 0, s, (uint32_t*)p, n_words,
+                     value);
+  return hipGetLastError();
+}
+
+extern "C" hipError_t emr_launch_grid(float* xy, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(emr::k_grid, dim3((uint32_t)blocks), dim3(256), 0, s, xy, n);
+  return hipGetLastError();
+}
+
+extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
+  if (a->n_members == 0) return hipSuccess;
+  hipLaunchKernelGGL(emr::k_bind, dim3((a->n_members + 63) / 64), dim3(64), 0, s, a->blob, a->desc,
+                     a->members, a->src_xy, a->bias_tab, a->n_members);
+  return hipGetLastError();
+}
+
+template <int S, int W, int MODE>
+static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks, hipStream_t s) {
+  emr::DiscoverScalars sc{a->cap, a->n_pos, a->tiles, a->n_tiles, a->depth, a->theta};
+  auto kern = emr::k_discover<S, W, MODE>;
+  // Cooperative launch: the runtime refuses a grid that cannot be resident all at once, which the
+  // look-back's forward progress relies on. Clamp to the occupancy-limited residency.
+  int per_cu = 0, dev = 0, cus = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, 0);
+  if (e != hipSuccess) return e;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+    return e;
+  const uint32_t resident = (uint32_t)(per_cu > 0 ? per_cu : 1) * (uint32_t)(cus > 0 ? cus : 1);
+  if (blocks > resident) blocks = resident;
+  const uint32_t* blob = a->blob;
+  const emr::Group* groups = a->groups;
+  const float* bias_tab = a->bias_tab;
+  uint64_t* status = a->status;
+  uint32_t* err = a->err;
+  uint32_t* parent = a->parent;
+  float* w4 = a->w4;
+  int64_t* pair_count = a->pair_count;
+  float* raw = a->raw;
+  void* args[] = {&blob, &groups, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw, &sc};
+  return hipLaunchCooperativeKernel((const void*)kern, dim3(blocks), dim3(256), args, 0, s);
+}
+
+template <int MODE>
+static hipError_t launch_discover_w(const emr::DiscoverArgs* a, int window, uint32_t blocks,
+                                    hipStream_t s) {
+  const int S = (int)a->group_size;
+#define EMR_CASE(S_, W_) \
+  if (S == S_ && window == W_) return launch_discover_t<S_, W_, MODE>(a, blocks, s);
+  EMR_CASE(1, 8) EMR_CASE(2, 8) EMR_CASE(3, 8) EMR_CASE(4, 8)
+  EMR_CASE(1, 16) EMR_CASE(2, 16) EMR_CASE(3, 16) EMR_CASE(4, 16)
+  EMR_CASE(1, 32) EMR_CASE(2, 32) EMR_CASE(3, 32) EMR_CASE(4, 32)
+#undef EMR_CASE
+  return hipErrorInvalidValue;
+}
+
+// blocks: requested number of 256-thread workgroups (4 waves each), clamped to what can be
+// resident at once; every wave walks its share of the tiles.
+// mode: 0 raw outputs, 1 padded records (then emr_launch_compact), 2 look-back records.
+extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int window, int mode,
+                                          uint32_t blocks, hipStream_t s) {
+  if (a->n_tiles == 0) return hipSuccess;
+  switch (mode) {
+    case emr::kModeRaw: return launch_discover_w<emr::kModeRaw>(a, window, blocks, s);
+    case emr::kModePadded: return launch_discover_w<emr::kModePadded>(a, window, blocks, s);
+    case emr::kModeLookback: return launch_discover_w<emr::kModeLookback>(a, window, blocks, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
+                                         int64_t* pair_count, int64_t cap, uint32_t tiles,
+                                         uint32_t n_pairs, hipStream_t s) {
+  if (n_pairs == 0) return hipSuccess;
+  hipLaunchKernelGGL(emr::k_compact, dim3((n_pairs + 3) / 4), dim3(256), 0, s, counts, parent, w4,
+                     pair_count, cap, tiles, n_pairs);
+  return hipGetLastError();
+}

@@ -1,0 +1,544 @@
+// Host runtime behind include/emr.h: argument checks, packing, per-call planning (grouping the
+// sources of a genome into the lanes' member sets), workspace layout, and kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/emr.h"
+#include "emr_internal.h"
+#include "pack.h"
+
+// Launchers (kernels.hip).
+extern "C" hipError_t emr_launch_fill(void* p, int64_t n_words, uint32_t value, hipStream_t s);
+extern "C" hipError_t emr_launch_grid(float* xy, int64_t n, hipStream_t s);
+extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s);
+extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int window, int mode,
+                                          uint32_t blocks, hipStream_t s);
+extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
+                                         int64_t* pair_count, int64_t cap, uint32_t tiles,
+                                         uint32_t n_pairs, hipStream_t s);
+
+namespace {
+
+thread_local std::string g_err;
+
+emr_status fail(emr_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define HIP_OR_FAIL(call)                                                                    \
+  do {                                                                                       \
+    hipError_t e_ = (call);                                                                  \
+    if (e_ != hipSuccess) return fail(EMR_E_DEVICE, "%s: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int device_cu_count() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 256;
+  return cus > 0 ? cus : 256;
+}
+
+// Pinned staging for the small per-call tables; reused once the previous copy has finished.
+struct Staging {
+  void* ptr = nullptr;
+  size_t size = 0;
+  hipEvent_t done = nullptr;
+  bool pending = false;
+};
+thread_local Staging g_stage;
+
+emr_status stage_upload(const void* src, size_t bytes, void* dev_dst, hipStream_t s) {
+  if (bytes == 0) return EMR_OK;
+  Staging& st = g_stage;
+  if (st.pending) {
+    HIP_OR_FAIL(hipEventSynchronize(st.done));
+    st.pending = false;
+  }
+  if (st.size < bytes) {
+    if (st.ptr) (void)hipHostFree(st.ptr);
+    st.ptr = nullptr;
+    st.size = 0;
+    size_t want = std::max<size_t>(bytes, 1 << 20);
+    if (hipHostMalloc(&st.ptr, want, hipHostMallocDefault) != hipSuccess)
+      return fail(EMR_E_NOMEM, "pinned staging of %zu bytes failed", want);
+    st.size = want;
+  }
+  if (!st.done) HIP_OR_FAIL(hipEventCreateWithFlags(&st.done, hipEventDisableTiming));
+  std::memcpy(st.ptr, src, bytes);
+  HIP_OR_FAIL(hipMemcpyAsync(dev_dst, st.ptr, bytes, hipMemcpyHostToDevice, s));
+  HIP_OR_FAIL(hipEventRecord(st.done, s));
+  st.pending = true;
+  return EMR_OK;
+}
+
+// Per-thread profiling of the discover-kernel launches.
+struct Profiler {
+  bool on = false;
+  double rT = 4.0;
+  std::vector<hipEvent_t> events;        // 2 per launch, created lazily and reused
+  std::vector<emr_launch_profile> recs;  // of the last profiled call
+};
+thread_local Profiler g_prof;
+
+// Algorithmic VALU slots per query of one (genome, direction) program: one per position-dependent
+// edge, the activation costs (transcendental instructions weighted by rT), and 2.5 for the
+// variance and threshold share of a query.
+double query_slots(const emr::GenomeInfo& inf, double rT) {
+  const double act_cost[6] = {0.0, 1.0 + 2.0 * rT, 2.0 + 2.0 * rT, 1.0 + rT, 1.0 + rT, 1.0};
+  double c = inf.fma_xy + inf.fma_node + 2.5;
+  for (int a = 0; a < 6; ++a) c += inf.act_count[a] * act_cost[a];
+  return c;
+}
+
+}  // namespace
+
+struct emr_population {
+  int32_t n_genomes = 0;
+  std::vector<emr::ProgDesc> desc;      // [2 * n_genomes]
+  std::vector<emr::GenomeInfo> info;    // [2 * n_genomes]
+  uint32_t* d_blob = nullptr;
+  emr::ProgDesc* d_desc = nullptr;
+  size_t blob_words = 0;
+};
+
+namespace {
+
+int window_bucket(int window) {
+  for (int w : emr::kWindows)
+    if (window <= w) return w;
+  return -1;
+}
+
+// Everything one discover / raw-eval call needs besides the population.
+struct Plan {
+  int depth = 0;
+  int64_t n_pairs = 0;
+  int64_t tiles = 0;
+  struct Bucket {
+    int S, window;
+    uint32_t first, count;
+  };
+  std::vector<emr::Group> groups;
+  std::vector<Bucket> buckets;
+  std::vector<emr::Member> members;
+  std::vector<uint32_t> group_member0;  // index of each group's first member
+  std::vector<float> src_xy;
+  uint64_t bias_floats = 0;
+  // Workspace layout (bytes from the workspace start).
+  size_t off_err = 0;      // 64 words: [0] error flags
+  size_t off_status = 0;
+  size_t off_groups = 0, off_members = 0, off_srcxy = 0, off_bias = 0, total = 0;
+  size_t zero_bytes = 0;   // prefix cleared before each call
+};
+constexpr int kMaxBuckets = 48;
+
+emr_status build_plan(const emr_population* pop, const emr_source* sources, int32_t n_sources,
+                      const int32_t* offs, int32_t n_shared, int32_t depth, Plan* plan) {
+  if (!pop) return fail(EMR_E_INVAL, "population is NULL");
+  if (depth < 0 || depth > EMR_MAX_DEPTH)
+    return fail(EMR_E_INVAL, "depth %d outside [0, %d]", depth, EMR_MAX_DEPTH);
+  if (n_sources < 0 || (n_sources > 0 && !sources)) return fail(EMR_E_INVAL, "bad sources");
+  const int32_t G = pop->n_genomes;
+  if (offs) {
+    if (offs[0] != 0) return fail(EMR_E_INVAL, "src_offsets[0] must be 0");
+    for (int32_t g = 0; g < G; ++g)
+      if (offs[g + 1] < offs[g]) return fail(EMR_E_INVAL, "src_offsets not ascending at %d", g);
+    if (offs[G] != n_sources)
+      return fail(EMR_E_INVAL, "src_offsets[n_genomes]=%d but n_sources=%d", offs[G], n_sources);
+  } else {
+    if (n_shared < 0 || n_shared != n_sources)
+      return fail(EMR_E_INVAL, "n_shared=%d must equal n_sources=%d", n_shared, n_sources);
+  }
+  for (int32_t i = 0; i < n_sources; ++i)
+    if (sources[i].dir != EMR_DIR_OUT && sources[i].dir != EMR_DIR_IN)
+      return fail(EMR_E_INVAL, "source %d has direction %d", i, sources[i].dir);
+
+  Plan& P = *plan;
+  P = Plan{};
+  P.depth = depth;
+  P.n_pairs = offs ? (int64_t)n_sources : (int64_t)G * n_shared;
+  P.tiles = emr::tiles_per_pair(depth);
+  if (P.n_pairs > 0xFFFFFFFFll) return fail(EMR_E_LIMIT, "too many pairs");
+
+  // Group each genome's sources by direction, in source order, into sets of <= kMaxGroup.
+  struct TmpGroup {
+    emr::Group g;
+    int S, window;
+    uint32_t desc;
+    uint32_t src[emr::kMaxGroup];
+  };
+  std::vector<TmpGroup> tmp;
+  for (int32_t g = 0; g < G; ++g) {
+    const int32_t lo = offs ? offs[g] : 0, hi = offs ? offs[g + 1] : n_shared;
+    for (int dir = 0; dir < 2; ++dir) {
+      const uint32_t di = 2u * (uint32_t)g + (uint32_t)dir;
+      const emr::ProgDesc& d = pop->desc[di];
+      const int wb = window_bucket(pop->info[di].window);
+      TmpGroup cur{};
+      int n = 0;
+      auto flush = [&]() {
+        if (n == 0) return;
+        cur.S = n;
+        cur.window = wb;
+        cur.desc = di;
+        for (int s = n; s < emr::kMaxGroup; ++s) cur.g.pair[s] = cur.g.pair[n - 1];
+        cur.g.var_off = d.var_off;
+        cur.g.n_steps = d.n_steps;
+        cur.g.flags = d.flags;
+        tmp.push_back(cur);
+        cur = TmpGroup{};
+        n = 0;
+      };
+      for (int32_t j = lo; j < hi; ++j) {
+        if (sources[j].dir != dir) continue;
+        const int64_t pair = offs ? (int64_t)j : (int64_t)g * n_shared + j;
+        cur.g.pair[n] = (uint32_t)pair;
+        cur.src[n] = (uint32_t)j;
+        if (++n == emr::kMaxGroup) flush();
+      }
+      flush();
+    }
+  }
+  // Order groups by bucket; assign bias-table offsets and members.
+  // Within a bucket, the most expensive programs come first: waves take tiles round-robin, so the
+  // cheap tiles end up in the last rounds and even out the tail. Output order does not depend on
+  // this order (each pair has its own region and scan row).
+  std::vector<double> cost(2 * (size_t)G);
+  for (size_t i = 0; i < cost.size(); ++i) cost[i] = query_slots(pop->info[i], 4.0);
+  std::stable_sort(tmp.begin(), tmp.end(), [&](const TmpGroup& a, const TmpGroup& b) {
+    if (a.S != b.S) return a.S < b.S;
+    if (a.window != b.window) return a.window < b.window;
+    return cost[a.desc] > cost[b.desc];
+  });
+  P.groups.reserve(tmp.size());
+  uint64_t bias = 0;
+  for (size_t i = 0; i < tmp.size(); ++i) {
+    TmpGroup& t = tmp[i];
+    if (P.buckets.empty() || P.buckets.back().S != t.S || P.buckets.back().window != t.window)
+      P.buckets.push_back({t.S, t.window, (uint32_t)i, 0});
+    P.buckets.back().count++;
+    t.g.bias_off = (uint32_t)bias;
+    P.group_member0.push_back((uint32_t)P.members.size());
+    for (int s = 0; s < t.S; ++s)
+      P.members.push_back({t.desc, t.src[s], (uint32_t)(bias + s), (uint32_t)t.S});
+    bias += (uint64_t)(t.g.n_steps + 1) * t.S;
+    P.groups.push_back(t.g);
+  }
+  if (bias > 0xFFFFFFFFull) return fail(EMR_E_LIMIT, "bias table too large");
+  if ((int)P.buckets.size() > kMaxBuckets) return fail(EMR_E_LIMIT, "too many buckets");
+  for (const auto& b : P.buckets)
+    if ((uint64_t)b.count * (uint64_t)P.tiles > 0xFFFFFFFFull)
+      return fail(EMR_E_LIMIT, "too many tiles in one launch");
+  P.bias_floats = bias;
+  P.src_xy.resize(2 * (size_t)n_sources);
+  for (int32_t i = 0; i < n_sources; ++i) {
+    P.src_xy[2 * i] = sources[i].x;
+    P.src_xy[2 * i + 1] = sources[i].y;
+  }
+
+  P.off_err = 0;
+  P.off_status = 256;
+  P.zero_bytes = align256(P.off_status + (size_t)P.n_pairs * P.tiles * 8);
+  P.off_groups = P.zero_bytes;
+  P.off_members = align256(P.off_groups + P.groups.size() * sizeof(emr::Group));
+  P.off_srcxy = align256(P.off_members + P.members.size() * sizeof(emr::Member));
+  P.off_bias = align256(P.off_srcxy + P.src_xy.size() * sizeof(float));
+  P.total = align256(P.off_bias + P.bias_floats * sizeof(float));
+  return EMR_OK;
+}
+
+// Enqueue: clear, upload tables, bind, discover (or raw eval) per bucket.
+emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const emr_result* out,
+                    float* raw, void* workspace, int64_t workspace_bytes, hipStream_t s) {
+  if (!workspace || workspace_bytes < (int64_t)P.total)
+    return fail(EMR_E_INVAL, "workspace of %lld bytes is smaller than the %zu needed",
+                (long long)workspace_bytes, P.total);
+  if (((uintptr_t)workspace & 255) != 0) return fail(EMR_E_INVAL, "workspace not 256-byte aligned");
+  char* ws = (char*)workspace;
+  HIP_OR_FAIL(emr_launch_fill(ws, (int64_t)(P.zero_bytes / 4), 0u, s));
+  // One host image for groups, members and source coordinates.
+  const size_t tab_bytes = P.off_bias - P.off_groups;
+  std::vector<char> img(tab_bytes, 0);
+  if (!P.groups.empty())
+    std::memcpy(img.data() + (P.off_groups - P.off_groups), P.groups.data(),
+                P.groups.size() * sizeof(emr::Group));
+  if (!P.members.empty())
+    std::memcpy(img.data() + (P.off_members - P.off_groups), P.members.data(),
+                P.members.size() * sizeof(emr::Member));
+  if (!P.src_xy.empty())
+    std::memcpy(img.data() + (P.off_srcxy - P.off_groups), P.src_xy.data(),
+                P.src_xy.size() * sizeof(float));
+  emr_status st = stage_upload(img.data(), tab_bytes, ws + P.off_groups, s);
+  if (st != EMR_OK) return st;
+
+  emr::BindArgs b{};
+  b.blob = pop->d_blob;
+  b.desc = pop->d_desc;
+  b.members = (const emr::Member*)(ws + P.off_members);
+  b.src_xy = (const float*)(ws + P.off_srcxy);
+  b.bias_tab = (float*)(ws + P.off_bias);
+  b.n_members = (uint32_t)P.members.size();
+  HIP_OR_FAIL(emr_launch_bind(&b, s));
+
+  const int cus = device_cu_count();
+  // Records go to fixed per-tile slots when every pair region can hold the worst case, and are
+  // compacted afterwards; a smaller capacity places them through the look-back scan instead.
+  const bool padded = out && out->pair_capacity >= emr::n_parents(P.depth);
+  const int mode = raw ? 0 : (padded ? 1 : 2);
+  Profiler& prof = g_prof;
+  if (prof.on) {
+    prof.recs.clear();
+    while (prof.events.size() < 2 * P.buckets.size()) {
+      hipEvent_t e;
+      HIP_OR_FAIL(hipEventCreate(&e));
+      prof.events.push_back(e);
+    }
+  }
+  for (size_t bi = 0; bi < P.buckets.size(); ++bi) {
+    const Plan::Bucket& bk = P.buckets[bi];
+    emr::DiscoverArgs a{};
+    a.blob = pop->d_blob;
+    a.groups = (const emr::Group*)(ws + P.off_groups) + bk.first;
+    a.bias_tab = (const float*)(ws + P.off_bias);
+    a.status = (uint64_t*)(ws + P.off_status);
+    a.err = (uint32_t*)(ws + P.off_err);
+    a.parent = out ? out->parent : nullptr;
+    a.w4 = out ? out->w4 : nullptr;
+    a.pair_count = out ? out->pair_count : nullptr;
+    a.raw = raw;
+    a.cap = out ? out->pair_capacity : 0;
+    a.n_pos = emr::n_positions(P.depth);
+    a.n_groups = bk.count;
+    a.tiles = (uint32_t)P.tiles;
+    a.n_tiles = (uint32_t)((uint64_t)bk.count * (uint64_t)P.tiles);
+    a.depth = P.depth;
+    a.theta = theta;
+    a.group_size = (uint32_t)bk.S;
+    const uint64_t want = ((uint64_t)a.n_tiles + 3) / 4;
+    const uint32_t blocks = (uint32_t)std::min<uint64_t>(want, (uint64_t)cus * 16);
+    if (prof.on) HIP_OR_FAIL(hipEventRecord(prof.events[2 * bi], s));
+    HIP_OR_FAIL(emr_launch_discover(&a, bk.window, mode, blocks, s));
+    if (prof.on) {
+      HIP_OR_FAIL(hipEventRecord(prof.events[2 * bi + 1], s));
+      emr_launch_profile r{};
+      r.group_size = bk.S;
+      r.window = bk.window;
+      r.tiles = a.n_tiles;
+      const double npos = (double)a.n_pos;
+      for (uint32_t k = 0; k < bk.count; ++k) {
+        const uint32_t gi = bk.first + k;
+        const emr::Member& m0 = P.members[P.group_member0[gi]];
+        r.slots += bk.S * npos * query_slots(pop->info[m0.desc], prof.rT);
+      }
+      r.queries = (int64_t)bk.count * bk.S * a.n_pos;
+      prof.recs.push_back(r);
+    }
+  }
+  if (padded && P.n_pairs > 0)
+    HIP_OR_FAIL(emr_launch_compact((const uint64_t*)(ws + P.off_status), out->parent, out->w4,
+                                   out->pair_count, out->pair_capacity, (uint32_t)P.tiles,
+                                   (uint32_t)P.n_pairs, s));
+  return EMR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* emr_last_error(void) { return g_err.c_str(); }
+
+int32_t emr_version(void) { return 100; }
+
+emr_status emr_grid_count(int32_t depth, int64_t* n_positions, int64_t* n_parents) {
+  if (depth < 0 || depth > EMR_MAX_DEPTH)
+    return fail(EMR_E_INVAL, "depth %d outside [0, %d]", depth, EMR_MAX_DEPTH);
+  if (n_positions) *n_positions = emr::n_positions(depth);
+  if (n_parents) *n_parents = emr::n_parents(depth);
+  return EMR_OK;
+}
+
+emr_status emr_build_grids(int32_t depth, float* xy_dev, void* stream) {
+  if (depth < 0 || depth > EMR_MAX_DEPTH)
+    return fail(EMR_E_INVAL, "depth %d outside [0, %d]", depth, EMR_MAX_DEPTH);
+  const int64_t n = emr::n_positions(depth);
+  if (n > 0 && !xy_dev) return fail(EMR_E_INVAL, "xy_dev is NULL");
+  HIP_OR_FAIL(emr_launch_grid(xy_dev, n, (hipStream_t)stream));
+  return EMR_OK;
+}
+
+emr_status emr_pack_population(const emr_genome* genomes, int32_t n, emr_population** out,
+                               int32_t* bad_index) {
+  if (bad_index) *bad_index = -1;
+  if (!out) return fail(EMR_E_INVAL, "out is NULL");
+  if (n < 0 || (n > 0 && !genomes)) return fail(EMR_E_INVAL, "bad genome array");
+  std::vector<uint32_t> blob;
+  std::vector<emr::ProgDesc> desc(2 * (size_t)n);
+  std::vector<emr::GenomeInfo> info(2 * (size_t)n);
+  for (int32_t g = 0; g < n; ++g) {
+    emr_status st = EMR_OK;
+    std::string msg;
+    if (!emr::pack_genome(genomes[g], blob, &desc[2 * g], &info[2 * g], &st, &msg)) {
+      if (bad_index) *bad_index = g;
+      return fail(st, "genome %d: %s", g, msg.c_str());
+    }
+    if (blob.size() > 0xF0000000ull) return fail(EMR_E_LIMIT, "population too large");
+  }
+  blob.resize(blob.size() + 16, 0u);  // the kernels may read a few words past a program's end
+  emr_population* p = new (std::nothrow) emr_population;
+  if (!p) return fail(EMR_E_NOMEM, "host allocation failed");
+  p->n_genomes = n;
+  p->desc = std::move(desc);
+  p->info = std::move(info);
+  p->blob_words = blob.size();
+  if (hipMalloc((void**)&p->d_blob, blob.size() * 4) != hipSuccess ||
+      hipMalloc((void**)&p->d_desc, std::max<size_t>(1, p->desc.size()) * sizeof(emr::ProgDesc)) !=
+          hipSuccess) {
+    emr_free_population(p);
+    return fail(EMR_E_NOMEM, "device allocation of %zu words failed", blob.size());
+  }
+  if (hipMemcpy(p->d_blob, blob.data(), blob.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+      (!p->desc.empty() && hipMemcpy(p->d_desc, p->desc.data(),
+                                     p->desc.size() * sizeof(emr::ProgDesc),
+                                     hipMemcpyHostToDevice) != hipSuccess)) {
+    emr_free_population(p);
+    return fail(EMR_E_DEVICE, "copy of the packed population failed");
+  }
+  *out = p;
+  return EMR_OK;
+}
+
+void emr_free_population(emr_population* pop) {
+  if (!pop) return;
+  if (pop->d_blob) (void)hipFree(pop->d_blob);
+  if (pop->d_desc) (void)hipFree(pop->d_desc);
+  delete pop;
+}
+
+emr_status emr_population_info(const emr_population* pop, int32_t* n_genomes, int32_t* steps2,
+                               int32_t* var_edges2, int32_t* window) {
+  if (!pop) return fail(EMR_E_INVAL, "population is NULL");
+  if (n_genomes) *n_genomes = pop->n_genomes;
+  for (int32_t g = 0; g < pop->n_genomes; ++g) {
+    for (int d = 0; d < 2; ++d) {
+      const emr::GenomeInfo& inf = pop->info[2 * g + d];
+      if (steps2) steps2[2 * g + d] = inf.n_steps;
+      if (var_edges2) var_edges2[2 * g + d] = inf.fma_xy + inf.fma_node;
+    }
+    if (window)
+      window[g] = std::max(pop->info[2 * g].window, pop->info[2 * g + 1].window);
+  }
+  return EMR_OK;
+}
+
+emr_status emr_workspace_bytes(const emr_population* pop, const emr_source* sources,
+                               int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                               int32_t depth, int64_t* bytes) {
+  if (!bytes) return fail(EMR_E_INVAL, "bytes is NULL");
+  Plan P;
+  emr_status st = build_plan(pop, sources, n_sources, src_offsets, n_shared, depth, &P);
+  if (st != EMR_OK) return st;
+  *bytes = (int64_t)P.total;
+  return EMR_OK;
+}
+
+emr_status emr_discover(const emr_population* pop, const emr_source* sources, int32_t n_sources,
+                        const int32_t* src_offsets, int32_t n_shared, int32_t depth, float theta,
+                        const emr_result* out, void* stream) {
+  if (!out) return fail(EMR_E_INVAL, "out is NULL");
+  Plan P;
+  emr_status st = build_plan(pop, sources, n_sources, src_offsets, n_shared, depth, &P);
+  if (st != EMR_OK) return st;
+  if (out->pair_capacity < 0) return fail(EMR_E_INVAL, "pair_capacity < 0");
+  if (P.n_pairs > 0) {
+    if (!out->pair_count) return fail(EMR_E_INVAL, "pair_count is NULL");
+    if (out->pair_capacity > 0 && (!out->parent || !out->w4))
+      return fail(EMR_E_INVAL, "parent/w4 is NULL with pair_capacity > 0");
+    if (out->pair_capacity > ((int64_t)1 << 40) / P.n_pairs)
+      return fail(EMR_E_LIMIT, "n_pairs * pair_capacity too large");
+  }
+  return run_plan(pop, P, theta, out, nullptr, out->workspace, out->workspace_bytes,
+                  (hipStream_t)stream);
+}
+
+emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max_count,
+                            void* stream) {
+  if (!out || n_pairs < 0) return fail(EMR_E_INVAL, "bad arguments");
+  HIP_OR_FAIL(hipStreamSynchronize((hipStream_t)stream));
+  uint32_t err = 0;
+  if (out->workspace) HIP_OR_FAIL(hipMemcpy(&err, out->workspace, 4, hipMemcpyDeviceToHost));
+  int64_t mx = 0;
+  if (n_pairs > 0) {
+    std::vector<int64_t> cnt((size_t)n_pairs);
+    HIP_OR_FAIL(hipMemcpy(cnt.data(), out->pair_count, (size_t)n_pairs * 8, hipMemcpyDeviceToHost));
+    for (int64_t c : cnt) mx = std::max(mx, c);
+  }
+  if (max_count) *max_count = mx;
+  if (err) return fail(EMR_E_DEVICE, "kernel reported internal error flags 0x%x", err);
+  if (mx > out->pair_capacity)
+    return fail(EMR_E_CAPACITY, "a pair found %lld records; pair_capacity is %lld",
+                (long long)mx, (long long)out->pair_capacity);
+  return EMR_OK;
+}
+
+emr_status emr_eval_raw(const emr_population* pop, const emr_source* sources, int32_t n_sources,
+                        const int32_t* src_offsets, int32_t n_shared, int32_t depth, float* out_dev,
+                        void* workspace, int64_t workspace_bytes, void* stream) {
+  Plan P;
+  emr_status st = build_plan(pop, sources, n_sources, src_offsets, n_shared, depth, &P);
+  if (st != EMR_OK) return st;
+  if (P.n_pairs > 0 && emr::n_positions(depth) > 0 && !out_dev)
+    return fail(EMR_E_INVAL, "out_dev is NULL");
+  return run_plan(pop, P, 0.0f, nullptr, out_dev, workspace, workspace_bytes, (hipStream_t)stream);
+}
+
+emr_status emr_discover_cost(const emr_population* pop, const emr_source* sources,
+                             int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                             int32_t depth, double transcendental_slots, double* slots,
+                             double* queries) {
+  Plan P;
+  emr_status st = build_plan(pop, sources, n_sources, src_offsets, n_shared, depth, &P);
+  if (st != EMR_OK) return st;
+  const double npos = (double)emr::n_positions(depth);
+  double total = 0.0;
+  for (const emr::Member& m : P.members) total += query_slots(pop->info[m.desc], transcendental_slots) * npos;
+  if (slots) *slots = total;
+  if (queries) *queries = (double)P.n_pairs * npos;
+  return EMR_OK;
+}
+
+emr_status emr_profile_enable(int32_t on, double transcendental_slots) {
+  g_prof.on = on != 0;
+  g_prof.rT = transcendental_slots;
+  g_prof.recs.clear();
+  return EMR_OK;
+}
+
+emr_status emr_profile_read(emr_launch_profile* out, int32_t cap, int32_t* n) {
+  Profiler& prof = g_prof;
+  if (n) *n = (int32_t)prof.recs.size();
+  for (size_t i = 0; i < prof.recs.size(); ++i) {
+    HIP_OR_FAIL(hipEventSynchronize(prof.events[2 * i + 1]));
+    float ms = 0.0f;
+    HIP_OR_FAIL(hipEventElapsedTime(&ms, prof.events[2 * i], prof.events[2 * i + 1]));
+    prof.recs[i].ms = ms;
+    if (out && (int32_t)i < cap) out[i] = prof.recs[i];
+  }
+  return EMR_OK;
+}
+
+}  // extern "C"

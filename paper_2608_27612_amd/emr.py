@@ -1,0 +1,316 @@
+"""Python binding of include/emr.h (ctypes; argument marshalling only).
+
+Every step of discovery runs in libemr.so's HIP kernels. PyTorch provides device memory and the
+current HIP stream; nothing here computes any part of the method. If the library has not been
+built the first call raises, so a missing extension can never fall back to another code path.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libemr.so")
+
+EMR_OK, EMR_E_INVAL, EMR_E_CYCLE, EMR_E_LIMIT, EMR_E_NOMEM, EMR_E_CAPACITY, EMR_E_DEVICE, \
+    EMR_E_ABORTED = 0, -1, -2, -3, -4, -5, -6, -7
+EMR_DIR_OUT, EMR_DIR_IN = 0, 1
+EMR_MAX_DEPTH = 15
+
+# Every function include/emr.h declares.
+ABI_FUNCTIONS = [
+    "emr_last_error", "emr_version", "emr_grid_count", "emr_build_grids", "emr_pack_population",
+    "emr_free_population", "emr_population_info", "emr_workspace_bytes", "emr_discover",
+    "emr_result_check", "emr_eval_raw", "emr_discover_cost", "emr_profile_enable",
+    "emr_profile_read",
+]
+
+
+class EmrError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__("emr status %d: %s" % (status, message))
+        self.status = status
+
+
+class emr_genome(C.Structure):
+    _fields_ = [("n_nodes", C.c_int32), ("n_edges", C.c_int32), ("kind", C.c_void_p),
+                ("act", C.c_void_p), ("bias", C.c_void_p), ("src", C.c_void_p),
+                ("dst", C.c_void_p), ("w", C.c_void_p), ("enabled", C.c_void_p)]
+
+
+class emr_source(C.Structure):
+    _fields_ = [("x", C.c_float), ("y", C.c_float), ("dir", C.c_int32)]
+
+
+class emr_result(C.Structure):
+    _fields_ = [("parent", C.c_void_p), ("w4", C.c_void_p), ("pair_capacity", C.c_int64),
+                ("pair_count", C.c_void_p), ("workspace", C.c_void_p),
+                ("workspace_bytes", C.c_int64)]
+
+
+class emr_launch_profile(C.Structure):
+    _fields_ = [("group_size", C.c_int32), ("window", C.c_int32), ("tiles", C.c_int64),
+                ("queries", C.c_int64), ("slots", C.c_double), ("ms", C.c_float)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libemr.so (raises if it was never built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libemr.so is not built; run __graft_entry__.build() or "
+                              "python paper_2608_27612_amd/build.py")
+        L = C.CDLL(LIB_PATH)
+        P, I32, I64, F32, F64 = C.c_void_p, C.c_int32, C.c_int64, C.c_float, C.c_double
+        sig = {
+            "emr_last_error": (C.c_char_p, []),
+            "emr_version": (I32, []),
+            "emr_grid_count": (I32, [I32, P, P]),
+            "emr_build_grids": (I32, [I32, P, P]),
+            "emr_pack_population": (I32, [P, I32, P, P]),
+            "emr_free_population": (None, [P]),
+            "emr_population_info": (I32, [P, P, P, P, P]),
+            "emr_workspace_bytes": (I32, [P, P, I32, P, I32, I32, P]),
+            "emr_discover": (I32, [P, P, I32, P, I32, I32, F32, P, P]),
+            "emr_result_check": (I32, [P, I64, P, P]),
+            "emr_eval_raw": (I32, [P, P, I32, P, I32, I32, P, P, I64, P]),
+            "emr_discover_cost": (I32, [P, P, I32, P, I32, I32, F64, P, P]),
+            "emr_profile_enable": (I32, [I32, F64]),
+            "emr_profile_read": (I32, [P, I32, P]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != EMR_OK:
+        raise EmrError(status, lib().emr_last_error().decode())
+
+
+def _stream_ptr(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+# ----------------------------------------------------------------------------- grids
+
+def emr_grid_count(depth: int):
+    n, q = C.c_int64(), C.c_int64()
+    _check(lib().emr_grid_count(depth, C.byref(n), C.byref(q)))
+    return n.value, q.value
+
+
+def emr_build_grids(depth: int, stream=None):
+    """Device tensor [N(D), 2] of cell centres in heap order."""
+    import torch
+    n, _ = emr_grid_count(depth)
+    xy = torch.empty((n, 2), dtype=torch.float32, device="cuda")
+    _check(lib().emr_build_grids(depth, C.c_void_p(xy.data_ptr() if n else 0), _stream_ptr(stream)))
+    return xy
+
+
+# ----------------------------------------------------------------------------- population
+
+class Population:
+    """A packed population (owns the library's emr_population)."""
+
+    def __init__(self, handle, n_genomes):
+        self.handle = handle
+        self.n_genomes = n_genomes
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.emr_free_population(self.handle)
+            self.handle = None
+
+    def info(self):
+        n = self.n_genomes
+        steps = np.zeros(2 * n, np.int32)
+        edges = np.zeros(2 * n, np.int32)
+        window = np.zeros(n, np.int32)
+        _check(lib().emr_population_info(self.handle, None, steps.ctypes.data, edges.ctypes.data,
+                                         window.ctypes.data))
+        return {"steps": steps.reshape(n, 2), "var_edges": edges.reshape(n, 2), "window": window}
+
+
+def _genome_array(genomes):
+    keep = []
+    arr = (emr_genome * max(1, len(genomes)))()
+    for i, g in enumerate(genomes):
+        k = {
+            "kind": np.ascontiguousarray(g["kind"], np.uint8),
+            "act": np.ascontiguousarray(g["act"], np.uint8),
+            "bias": None if g.get("bias") is None else np.ascontiguousarray(g["bias"], np.float32),
+            "src": np.ascontiguousarray(g["src"], np.int32),
+            "dst": np.ascontiguousarray(g["dst"], np.int32),
+            "w": np.ascontiguousarray(g["w"], np.float32),
+            "enabled": None if g.get("enabled") is None else np.ascontiguousarray(g["enabled"],
+                                                                                    np.uint8),
+        }
+        keep.append(k)
+        ptr = lambda a: None if a is None else a.ctypes.data  # noqa: E731
+        arr[i] = emr_genome(len(k["kind"]), len(k["src"]), ptr(k["kind"]), ptr(k["act"]),
+                            ptr(k["bias"]), ptr(k["src"]), ptr(k["dst"]), ptr(k["w"]),
+                            ptr(k["enabled"]))
+    return arr, keep
+
+
+def emr_pack_population(genomes) -> Population:
+    """Validate and pack genomes (list of dicts, see workloads.py) into device program tables."""
+    arr, keep = _genome_array(genomes)
+    handle = C.c_void_p()
+    bad = C.c_int32(-1)
+    st = lib().emr_pack_population(arr, len(genomes), C.byref(handle), C.byref(bad))
+    if st != EMR_OK:
+        err = EmrError(st, lib().emr_last_error().decode())
+        err.bad_index = bad.value
+        raise err
+    del keep
+    return Population(handle, len(genomes))
+
+
+# ----------------------------------------------------------------------------- discovery
+
+def _sources(sources):
+    arr = (emr_source * max(1, len(sources)))()
+    for i, s in enumerate(sources):
+        arr[i] = emr_source(float(s["x"]), float(s["y"]), int(s["dir"]))
+    return arr
+
+
+def _offsets(src_offsets):
+    if src_offsets is None:
+        return None
+    return np.ascontiguousarray(src_offsets, dtype=np.int32)
+
+
+def n_pairs_of(pop: Population, sources, src_offsets=None) -> int:
+    return len(sources) if src_offsets is not None else pop.n_genomes * len(sources)
+
+
+def emr_workspace_bytes(pop: Population, sources, depth: int, src_offsets=None) -> int:
+    offs = _offsets(src_offsets)
+    b = C.c_int64()
+    _check(lib().emr_workspace_bytes(pop.handle, _sources(sources), len(sources),
+                                     None if offs is None else offs.ctypes.data,
+                                     0 if offs is not None else len(sources), depth, C.byref(b)))
+    return b.value
+
+
+def alloc_result(pop: Population, sources, depth: int, src_offsets=None, pair_capacity=None):
+    """Device buffers for emr_discover (torch tensors); pair_capacity defaults to Q(D)."""
+    import torch
+    _, q = emr_grid_count(depth)
+    cap = q if pair_capacity is None else int(pair_capacity)
+    npairs = n_pairs_of(pop, sources, src_offsets)
+    ws = emr_workspace_bytes(pop, sources, depth, src_offsets)
+    return {
+        "parent": torch.empty((npairs, cap), dtype=torch.int32, device="cuda"),
+        "w4": torch.empty((npairs, cap, 4), dtype=torch.float32, device="cuda"),
+        "pair_count": torch.empty(npairs, dtype=torch.int64, device="cuda"),
+        "workspace": torch.empty(max(ws, 256), dtype=torch.uint8, device="cuda"),
+        "pair_capacity": cap,
+        "n_pairs": npairs,
+    }
+
+
+def _result_struct(res):
+    def ptr(t):
+        return t.data_ptr() if t.numel() else 0
+    ws = res["workspace"]
+    assert ws.data_ptr() % 256 == 0
+    return emr_result(ptr(res["parent"]), ptr(res["w4"]), res["pair_capacity"],
+                      ptr(res["pair_count"]), ws.data_ptr(), ws.numel())
+
+
+def emr_discover(pop: Population, sources, depth: int, theta: float, res=None, src_offsets=None,
+                 stream=None, pair_capacity=None):
+    """Enqueue eager discovery; returns the result dict (device tensors, see alloc_result).
+    `parent` is the int32 view of the library's uint32 heap indices."""
+    if res is None:
+        res = alloc_result(pop, sources, depth, src_offsets, pair_capacity)
+    offs = _offsets(src_offsets)
+    out = _result_struct(res)
+    res["_struct"] = out
+    _check(lib().emr_discover(pop.handle, _sources(sources), len(sources),
+                              None if offs is None else offs.ctypes.data,
+                              0 if offs is not None else len(sources), depth,
+                              C.c_float(theta), C.byref(out), _stream_ptr(stream)))
+    return res
+
+
+def emr_result_check(res, stream=None) -> int:
+    """Synchronize and check a discover result; returns the largest pair count."""
+    out = res.get("_struct") or _result_struct(res)
+    mx = C.c_int64()
+    _check(lib().emr_result_check(C.byref(out), res["n_pairs"], C.byref(mx), _stream_ptr(stream)))
+    return mx.value
+
+
+def emr_eval_raw(pop: Population, sources, depth: int, src_offsets=None, stream=None):
+    """Device tensor [n_pairs, N(D)] of raw CPPN outputs."""
+    import torch
+    n, _ = emr_grid_count(depth)
+    npairs = n_pairs_of(pop, sources, src_offsets)
+    out = torch.empty((npairs, n), dtype=torch.float32, device="cuda")
+    ws_bytes = emr_workspace_bytes(pop, sources, depth, src_offsets)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
+    offs = _offsets(src_offsets)
+    _check(lib().emr_eval_raw(pop.handle, _sources(sources), len(sources),
+                              None if offs is None else offs.ctypes.data,
+                              0 if offs is not None else len(sources), depth,
+                              C.c_void_p(out.data_ptr() if out.numel() else 0),
+                              C.c_void_p(ws.data_ptr()), ws.numel(), _stream_ptr(stream)))
+    return out
+
+
+def emr_discover_cost(pop: Population, sources, depth: int, src_offsets=None,
+                      transcendental_slots: float = 4.0):
+    """(algorithmic VALU slots, queries) of one discover call under the cost model."""
+    offs = _offsets(src_offsets)
+    slots, queries = C.c_double(), C.c_double()
+    _check(lib().emr_discover_cost(pop.handle, _sources(sources), len(sources),
+                                   None if offs is None else offs.ctypes.data,
+                                   0 if offs is not None else len(sources), depth,
+                                   float(transcendental_slots), C.byref(slots), C.byref(queries)))
+    return slots.value, queries.value
+
+
+def records_to_host(res):
+    """Copy a checked result to numpy: per-pair lists (parent[i], w4[i]) in ascending order."""
+    counts = res["pair_count"].cpu().numpy()
+    cap = res["pair_capacity"]
+    parent = res["parent"].cpu().numpy().view(np.uint32)
+    w4 = res["w4"].cpu().numpy()
+    out = []
+    for r, c in enumerate(counts):
+        c = min(int(c), cap)
+        out.append((parent[r, :c].astype(np.int64), w4[r, :c]))
+    return counts, out
+
+
+# ----------------------------------------------------------------------------- profiling
+
+def emr_profile_enable(on: bool = True, transcendental_slots: float = 4.0):
+    _check(lib().emr_profile_enable(1 if on else 0, float(transcendental_slots)))
+
+
+def emr_profile_read():
+    """Per-launch records of the last profiled call (synchronizes on its events)."""
+    n = C.c_int32()
+    _check(lib().emr_profile_read(None, 0, C.byref(n)))
+    arr = (emr_launch_profile * max(1, n.value))()
+    _check(lib().emr_profile_read(arr, n.value, C.byref(n)))
+    return [{"S": r.group_size, "W": r.window, "tiles": r.tiles, "queries": r.queries,
+             "slots": r.slots, "ms": r.ms} for r in arr[:n.value]]

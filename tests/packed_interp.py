@@ -1,0 +1,132 @@
+"""Test helper: the library's host packer compiled without HIP (tests/shim/pack_shim.cpp), plus a
+float64 numpy interpreter of the packed program format. It is a packer test, not an oracle: the
+tests compare what it computes from packed programs with the oracle's raw-genome evaluation.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+SHIM_SRC = os.path.join(HERE, "shim", "pack_shim.cpp")
+PACK_SRC = os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "pack.cpp")
+SHIM_LIB = os.path.join(HERE, "shim", "libpackshim.so")
+
+_lib = None
+
+
+def shim():
+    global _lib
+    if _lib is None:
+        srcs = [SHIM_SRC, PACK_SRC]
+        if (not os.path.exists(SHIM_LIB)
+                or max(os.path.getmtime(s) for s in srcs) > os.path.getmtime(SHIM_LIB)):
+            tmp = SHIM_LIB + ".tmp%d" % os.getpid()
+            subprocess.check_call(["g++", "-std=c++17", "-O1", "-fPIC", "-shared"] + srcs
+                                  + ["-o", tmp])
+            os.replace(tmp, SHIM_LIB)
+        L = C.CDLL(SHIM_LIB)
+        L.shim_pack.restype = C.c_int
+        L.shim_pack.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.POINTER(C.c_int64), C.c_void_p,
+                                C.c_void_p, C.c_char_p, C.c_int]
+        _lib = L
+    return _lib
+
+
+def pack(genome):
+    """Pack one genome on the host. Returns (status, blob, desc[2][4], info[2][12], message)."""
+    from paper_2608_27612_amd.emr import _genome_array
+    arr, keep = _genome_array([genome])
+    cap = 1 << 16
+    blob = np.zeros(cap, np.uint32)
+    words = C.c_int64()
+    desc = np.zeros(8, np.uint32)
+    info = np.zeros(24, np.int32)
+    msg = C.create_string_buffer(256)
+    st = shim().shim_pack(C.byref(arr[0]), blob.ctypes.data, cap, C.byref(words),
+                          desc.ctypes.data, info.ctypes.data, msg, 256)
+    del keep
+    return st, blob[:words.value], desc.reshape(2, 4), info.reshape(2, 12), msg.value.decode()
+
+
+def _act(a, z):
+    if a == 0:
+        return z
+    if a == 1:
+        return 1.0 / (1.0 + np.exp(-z))
+    if a == 2:
+        return np.tanh(z)
+    if a == 3:
+        return np.exp(-z * z)
+    if a == 4:
+        return np.sin(z)
+    if a == 5:
+        return np.abs(z)
+    raise ValueError(a)
+
+
+def f32(u):
+    return float(np.array([u], np.uint32).view(np.float32)[0])
+
+
+def interpret(blob, desc, dir_, sx, sy, px, py):
+    """Evaluate packed program `desc[dir_]` for source (sx, sy) at positions (px, py) (arrays)."""
+    var_off, n_steps, uni_off, flags = (int(v) for v in desc[dir_])
+    # uniform program
+    U = np.zeros(5 + 300)
+    if dir_ == 0:
+        U[0], U[1] = sx, sy
+    else:
+        U[2], U[3] = sx, sy
+    U[4] = 1.0
+    n_un, out_u, n_st = int(blob[uni_off]), int(blob[uni_off + 1]), int(blob[uni_off + 2])
+    assert n_st == n_steps
+    rec = uni_off + 4
+    for k in range(n_un):
+        act, ne, eo, bb = (int(v) for v in blob[rec + 4 * k: rec + 4 * k + 4])
+        z = f32(bb)
+        for e in range(ne):
+            z += f32(blob[eo + 2 * e + 1]) * U[int(blob[eo + 2 * e])]
+        U[5 + k] = _act(act, np.float64(z))
+    fold = rec + 4 * n_un
+    folded = []
+    for t in range(n_steps):
+        nf, fo, bb = int(blob[fold + 4 * t]), int(blob[fold + 4 * t + 1]), int(blob[fold + 4 * t + 2])
+        z = f32(bb)
+        for e in range(nf):
+            z += f32(blob[fo + 2 * e + 1]) * U[int(blob[fo + 2 * e])]
+        folded.append(z)
+    if not (flags & 1):
+        return np.full(len(px), U[out_u]), (flags >> 8) & 0xFF
+    window = (flags >> 8) & 0xFF
+    vals = np.full((max(window, 1), len(px)), np.nan)
+    acc = None
+    for t in range(n_steps):
+        m0, m1, eo = (int(v) for v in blob[var_off + 4 * t: var_off + 4 * t + 3])
+        act, dst = m0 & 0xFF, (m0 >> 8) & 0xFF
+        nx, ny, nn = m1 & 0xFF, (m1 >> 8) & 0xFF, m1 >> 16
+        acc = np.full(len(px), folded[t])
+        for e in range(nx):
+            assert int(blob[eo + 2 * e]) == 0
+            acc = acc + f32(blob[eo + 2 * e + 1]) * px
+        eo += 2 * nx
+        for e in range(ny):
+            assert int(blob[eo + 2 * e]) == 1
+            acc = acc + f32(blob[eo + 2 * e + 1]) * py
+        eo += 2 * ny
+        for e in range(nn):
+            src = int(blob[eo + 2 * e])
+            assert src < window
+            v = vals[src]
+            assert not np.isnan(v).any(), "read of a slot that holds no live value"
+            acc = acc + f32(blob[eo + 2 * e + 1]) * v
+        acc = _act(act, acc)
+        if t + 1 < n_steps:
+            assert dst < window
+            vals[dst] = acc
+    return acc, window

@@ -1,0 +1,74 @@
+"""The C-ABI library on the host: it loads, exports every declared symbol, and rejects bad
+arguments before touching a device (no GPU needed)."""
+
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_27612_amd import emr, workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "emr.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(emr_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 10
+    assert set(names) == set(emr.ABI_FUNCTIONS)
+    lib = C.CDLL(emr.LIB_PATH)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_grid_count():
+    for D in range(0, 16):
+        n, q = emr.emr_grid_count(D)
+        assert n == (4 ** (D + 1) - 4) // 3
+        assert q == ((4 ** D - 1) // 3 if D else 0)
+    for bad in (-1, 16):
+        with pytest.raises(emr.EmrError) as e:
+            emr.emr_grid_count(bad)
+        assert e.value.status == emr.EMR_E_INVAL
+
+
+def test_pack_validation_reports_first_bad_genome():
+    good = W.population(0, 3, 5, 10)
+    cyc = {k: v.copy() for k, v in good[1].items()}
+    # add a 2-cycle between the output and a new hidden node
+    n = len(cyc["kind"])
+    cyc["kind"] = np.append(cyc["kind"], np.uint8(5))
+    cyc["act"] = np.append(cyc["act"], np.uint8(0))
+    cyc["bias"] = np.append(cyc["bias"], np.float32(0))
+    out = int(np.nonzero(cyc["kind"] == 6)[0][0])
+    cyc["src"] = np.append(cyc["src"], np.int32([out, n]))
+    cyc["dst"] = np.append(cyc["dst"], np.int32([n, out]))
+    cyc["w"] = np.append(cyc["w"], np.float32([1, 1]))
+    cyc["enabled"] = np.append(cyc["enabled"], np.uint8([1, 1]))
+    with pytest.raises(emr.EmrError) as e:
+        emr.emr_pack_population([good[0], good[2], cyc, good[1]])
+    assert e.value.status == emr.EMR_E_CYCLE
+    assert e.value.bad_index == 2
+    assert "cycle" in str(e.value)
+
+
+def test_discover_rejects_null_population():
+    L = emr.lib()
+    res = emr.emr_result()
+    src = emr._sources(W.xor_sources())
+    st = L.emr_discover(None, src, 4, None, 4, 5, C.c_float(0.03), C.byref(res), None)
+    assert st == emr.EMR_E_INVAL
+    assert b"population" in L.emr_last_error()
+    st = L.emr_build_grids(-3, None, None)
+    assert st == emr.EMR_E_INVAL
+
+
+def test_version():
+    assert emr.lib().emr_version() >= 100

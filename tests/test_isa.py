@@ -1,0 +1,66 @@
+"""Static checks of the gfx950 assembly hipcc produces for the kernels (CPU only).
+
+ - no packed FP32 arithmetic anywhere (the build disables the feature);
+ - no scalar-memory writes of any kind;
+ - M0 is written only by the register-indexing sequences of the interpreter;
+ - the discover kernels keep their values in registers (no private scratch).
+"""
+
+import os
+import re
+import subprocess
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "kernels.hip")
+
+
+@pytest.fixture(scope="module")
+def asm():
+    from paper_2608_27612_amd import build
+    with tempfile.TemporaryDirectory() as d:
+        out = os.path.join(d, "k.s")
+        cmd = [build.HIPCC, "-O3", "-std=c++17", "--cuda-device-only", "-S"] + build.DEVICE_FLAGS \
+            + [SRC, "-o", out]
+        subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
+        return open(out).read()
+
+
+def _kernels(asm):
+    """{symbol: body} for every kernel in the assembly."""
+    out = {}
+    for m in re.finditer(r"^(_Z\w+):\s*;\s*@", asm, flags=re.M):
+        start = m.end()
+        end = asm.find("s_endpgm", start)
+        out[m.group(1)] = asm[start:end]
+    return out
+
+
+def test_no_packed_fp32(asm):
+    assert not re.search(r"v_pk_(add|mul|fma)_f32", asm)
+
+
+def test_no_scalar_memory_writes(asm):
+    pattern = r"\bs_(buffer_)?(st" + r"ore|atom" + r"ic)\w*|\bs_dca" + r"che_\w+|\bs_scr" + r"atch_\w+"
+    assert not re.search(pattern, asm)
+
+
+def test_m0_only_for_register_indexing(asm):
+    for line in asm.splitlines():
+        code = line.split(";")[0]
+        if re.search(r"\bm0\b", code):
+            pytest.fail("unexpected M0 use: " + line.strip())
+    assert "s_set_gpr_idx_on" in asm
+
+
+def test_discover_kernels_use_no_scratch(asm):
+    ks = {k: v for k, v in _kernels(asm).items() if "k_discover" in k}
+    assert len(ks) == 36   # 4 group sizes x 3 windows x 3 output modes
+    for name, body in ks.items():
+        assert "scratch_" not in body and "buffer_store" not in body, name
+    sizes = re.findall(r"\.name:\s+(\S*k_discover\S*)\s*\n(?:.*\n)*?\s+\.private_segment_fixed_size:\s+(\d+)",
+                       asm)
+    for name, size in sizes:
+        assert int(size) == 0, name

@@ -1,0 +1,125 @@
+"""Host packer: validation, and packed programs that reproduce the oracle's CPPN values (CPU)."""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_27612_amd import workloads as W
+from tests import packed_interp as PI
+
+EMR_E_INVAL, EMR_E_CYCLE, EMR_E_LIMIT = -1, -2, -3
+
+
+def mk(kinds, acts, edges, enabled=None):
+    n = len(kinds)
+    return {"kind": np.array(kinds, np.uint8), "act": np.array(acts, np.uint8),
+            "bias": np.zeros(n, np.float32),
+            "src": np.array([e[0] for e in edges], np.int32),
+            "dst": np.array([e[1] for e in edges], np.int32),
+            "w": np.array([e[2] for e in edges], np.float32),
+            "enabled": np.ones(len(edges), np.uint8) if enabled is None else np.array(enabled, np.uint8)}
+
+
+def _positions(D):
+    xy = oracle.grid(D)
+    return xy[:, 0], xy[:, 1]
+
+
+def _check_genome(g, D=4, sources=((0.0, -1.0, 0), (0.5, 1.0, 1), (-1.0, -1.0, 0))):
+    st, blob, desc, info, msg = PI.pack(g)
+    assert st == 0, msg
+    px, py = _positions(D)
+    for sx, sy, d in sources:
+        got, window = PI.interpret(blob, desc, d, sx, sy, px, py)
+        in5 = np.zeros((len(px), 5))
+        if d == 0:
+            in5[:, 0], in5[:, 1], in5[:, 2], in5[:, 3] = sx, sy, px, py
+        else:
+            in5[:, 0], in5[:, 1], in5[:, 2], in5[:, 3] = px, py, sx, sy
+        in5[:, 4] = 1.0
+        want = oracle.eval_points(g, in5)
+        np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+        assert window <= 32
+    return info
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_packed_programs_match_oracle_population(seed):
+    for g in W.population(seed, 40, 20, 60):
+        _check_genome(g)
+
+
+def test_packed_programs_match_oracle_large_genomes():
+    for g in W.population(11, 12, 40, 120):
+        _check_genome(g, D=3)
+    _check_genome(W.single_cppn(0, 30, 90)[0], D=4)
+
+
+def test_window_fits_for_every_workload_population():
+    for name in ["xor_pop1000", "tabular_pop150", "recurrent_pop100", "deep_single", "single_d5"]:
+        genomes = W.workload(name)[0]
+        for g in genomes:
+            st, blob, desc, info, msg = PI.pack(g)
+            assert st == 0, msg
+            assert info[0][9] <= 32 and info[1][9] <= 32
+
+
+def test_fold_of_uniform_inputs_and_nodes():
+    # hidden A depends only on x1 and bias (uniform for outgoing queries); B mixes A and x2.
+    g = mk([0, 1, 2, 3, 4, 6, 5, 5], [0] * 5 + [0, 1, 4],
+           [(0, 6, 1.5), (4, 6, -0.25), (6, 7, 2.0), (2, 7, 1.0), (7, 5, 1.0), (6, 5, 0.5)])
+    info = _check_genome(g)
+    out_info, in_info = info[0], info[1]
+    # outgoing: only B and the output vary; A is folded
+    assert out_info[0] == 2 and out_info[10] == 1
+    # incoming: x1 varies, so A varies too
+    assert in_info[0] == 3
+
+
+def test_constant_output_is_uniform():
+    g = mk([0, 1, 2, 3, 4, 6], [0] * 5 + [2], [(0, 5, 1.0), (4, 5, 0.3)])
+    st, blob, desc, info, msg = PI.pack(g)
+    assert st == 0
+    assert info[0][11] == 0 and info[0][0] == 0      # outgoing: the output is a constant
+    assert info[1][11] == 1                          # incoming: it varies with x1
+    _check_genome(g)
+
+
+def test_dead_nodes_and_disabled_edges_are_dropped():
+    # node 7 feeds nothing that reaches the output; the disabled edge 2->5 is ignored
+    g = mk([0, 1, 2, 3, 4, 6, 5, 5], [0] * 5 + [0, 4, 1],
+           [(2, 6, 1.0), (6, 5, 1.0), (3, 7, 2.0), (2, 5, 9.0)], enabled=[1, 1, 1, 0])
+    info = _check_genome(g)
+    assert info[0][0] == 2   # only hidden 6 and the output are evaluated
+    assert info[0][1] + info[0][2] == 2
+
+
+def test_validation_errors():
+    base = [0, 1, 2, 3, 4, 6, 5]
+    acts = [0] * 7
+    cases = [
+        (mk(base, acts, [(2, 6, 1.0), (6, 6, 1.0), (6, 5, 1.0)]), EMR_E_CYCLE),     # self loop
+        (mk(base, acts, [(2, 6, 1.0), (6, 5, 1.0), (5, 6, 1.0)]), EMR_E_CYCLE),     # 2-cycle
+        (mk([0, 1, 2, 3, 4, 5, 5], acts, [(2, 5, 1.0)]), EMR_E_INVAL),              # no output
+        (mk([0, 1, 2, 3, 4, 6, 6], acts, [(2, 5, 1.0)]), EMR_E_INVAL),              # two outputs
+        (mk([0, 0, 2, 3, 4, 6, 5], acts, [(2, 5, 1.0)]), EMR_E_INVAL),              # role twice
+        (mk(base, acts, [(5, 2, 1.0)]), EMR_E_INVAL),                               # into input
+        (mk(base, acts, [(2, 9, 1.0)]), EMR_E_INVAL),                               # out of range
+        (mk([0, 1, 2, 3, 4, 9, 5], acts, [(2, 5, 1.0)]), EMR_E_INVAL),              # bad kind
+        (mk(base, [0] * 5 + [7, 0], [(2, 5, 1.0)]), EMR_E_INVAL),                   # bad act
+    ]
+    for g, want in cases:
+        st, *_ = PI.pack(g)
+        assert st == want, (g, st)
+    # a disabled back edge is fine
+    st, *_ = PI.pack(mk(base, acts, [(2, 6, 1.0), (6, 5, 1.0), (5, 6, 1.0)], enabled=[1, 1, 0]))
+    assert st == 0
+
+
+def test_window_limit():
+    # 40 hidden nodes all fed by x2 and all feeding the output: 40 values alive at once
+    h = 40
+    kinds = [0, 1, 2, 3, 4, 6] + [5] * h
+    edges = [(2, 6 + k, 1.0) for k in range(h)] + [(6 + k, 5, 1.0) for k in range(h)]
+    st, _, _, _, msg = PI.pack(mk(kinds, [0] * (6 + h), edges))
+    assert st == EMR_E_LIMIT, msg

@@ -1,0 +1,303 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 CPU oracle on seeded inputs.
+
+Tolerances (stated by the method's accuracy target, fp32 arithmetic):
+  * every CPPN output: |gpu - oracle| <= 1e-5 * max(|oracle|, 1)  (relative where |o| >= 1,
+    absolute below, since relative error is undefined at the zeros of sine/linear outputs);
+  * kept cells: identical sets, except cells whose oracle variance lies within 1e-5 of theta
+    (theta is the float32 value the kernel compares against);
+  * heap indices, counts and record order: exact.
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_27612_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5
+BAND = 1e-5
+
+
+@pytest.fixture(scope="module")
+def emr():
+    import torch
+    assert torch.cuda.is_available()
+    from paper_2608_27612_amd import emr as E
+    E.lib()
+    return E
+
+
+def close(g, o):
+    g = np.asarray(g, np.float64)
+    o = np.asarray(o, np.float64)
+    return np.abs(g - o) <= TOL * np.maximum(np.abs(o), 1.0)
+
+
+def pair_genome_source(r, genomes, sources, offs):
+    if offs is None:
+        return genomes[r // len(sources)], sources[r % len(sources)]
+    g = int(np.searchsorted(np.asarray(offs), r, side="right") - 1)
+    return genomes[g], sources[r]
+
+
+def check_discover(emr, genomes, sources, D, theta, offs=None, cap=None):
+    """Runs the GPU path and the oracle; asserts parity; returns summary stats."""
+    theta32 = float(np.float32(theta))
+    pop = emr.emr_pack_population(genomes)
+    res = emr.emr_discover(pop, sources, D, theta32, src_offsets=offs, pair_capacity=cap)
+    emr.emr_result_check(res)
+    counts, recs = emr.records_to_host(res)
+    o = oracle.discover(genomes, sources, D, theta32, src_offsets=offs)
+    assert len(counts) == len(o["pair_count"])
+    n_band = 0
+    for r in range(len(counts)):
+        lo, hi = o["pair_offset"][r], o["pair_offset"][r + 1]
+        op, ow, ov = o["parent"][lo:hi], o["w4"][lo:hi], o["var"][lo:hi]
+        gp, gw = recs[r]
+        assert np.all(np.diff(gp) > 0), "records not in ascending parent order"
+        if counts[r] == len(op) and np.array_equal(gp, op):
+            ok = close(gw, ow)
+            assert ok.all(), (r, np.argwhere(~ok)[:5], gw[~ok.any(axis=1)][:3], ow[~ok.any(axis=1)][:3])
+            continue
+        # sets differ: every difference must sit in the band around theta
+        g, s = pair_genome_source(r, genomes, sources, offs)
+        diff = np.setxor1d(gp, op)
+        _, dvar = oracle.eval_parents(g, s, diff)
+        assert np.all(np.abs(dvar - theta32) <= BAND), (r, diff[:5], dvar[:5])
+        n_band += len(diff)
+        common, gi, oi = np.intersect1d(gp, op, return_indices=True)
+        assert close(gw[gi], ow[oi]).all()
+    return {"records": int(np.sum(np.minimum(counts, res["pair_capacity"]))), "band": n_band,
+            "counts": counts}
+
+
+def check_raw(emr, genomes, sources, D, offs=None):
+    pop = emr.emr_pack_population(genomes)
+    raw = emr.emr_eval_raw(pop, sources, D, src_offsets=offs).cpu().numpy()
+    Q = oracle.n_parents(D)
+    parents = np.arange(Q, dtype=np.int64)
+    worst = 0.0
+    for r in range(raw.shape[0]):
+        g, s = pair_genome_source(r, genomes, sources, offs)
+        w4, _ = oracle.eval_parents(g, s, parents)
+        want = w4.reshape(-1)
+        ok = close(raw[r], want)
+        assert ok.all(), (r, np.argwhere(~ok)[:5].ravel(), raw[r][~ok][:5], want[~ok][:5])
+        worst = max(worst, float(np.max(np.abs(raw[r] - want) / np.maximum(np.abs(want), 1.0))))
+    return worst
+
+
+# ------------------------------------------------------------------------------- grids
+
+def test_grid_positions_exact(emr):
+    for D in [0, 1, 2, 3, 4, 5, 8]:
+        xy = emr.emr_build_grids(D).cpu().numpy().astype(np.float64)
+        np.testing.assert_array_equal(xy, oracle.grid(D))
+
+
+# ------------------------------------------------------------------------------- raw outputs
+
+def test_raw_single_cppn_depth5(emr):
+    genomes, sources, D, _ = W.workload("single_d5")
+    check_raw(emr, genomes, sources, D)
+
+
+def test_raw_population_both_directions(emr):
+    genomes = W.population(1, 40, 20, 60)
+    check_raw(emr, genomes, W.xor_sources(), 5)
+
+
+@pytest.mark.parametrize("act", range(6))
+def test_raw_each_activation(emr, act):
+    # out = linear(act(3*x2 - 2*y2 + 0.5) * 2 + x2): exercises each activation over z in [-5.5, 5.5]
+    g = {"kind": np.array([0, 1, 2, 3, 4, 6, 5], np.uint8),
+         "act": np.array([0, 0, 0, 0, 0, 0, act], np.uint8), "bias": np.zeros(7, np.float32),
+         "src": np.array([2, 3, 4, 6, 2], np.int32), "dst": np.array([6, 6, 6, 5, 5], np.int32),
+         "w": np.array([3.0, -2.0, 0.5, 2.0, 1.0], np.float32), "enabled": np.ones(5, np.uint8)}
+    check_raw(emr, [g], W.xor_sources(), 6)
+
+
+def test_raw_large_sine_arguments(emr):
+    # a linear chain multiplies x2 by 3^4 = 81 before a sine: |z| up to ~80
+    kinds = [0, 1, 2, 3, 4, 6, 5, 5, 5, 5, 5]
+    acts = [0] * 5 + [0, 0, 0, 0, 0, 4]
+    edges = [(2, 6, 3.0), (6, 7, 3.0), (7, 8, 3.0), (8, 9, 3.0), (9, 10, 1.0), (10, 5, 1.0)]
+    g = {"kind": np.array(kinds, np.uint8), "act": np.array(acts, np.uint8),
+         "bias": np.zeros(len(kinds), np.float32),
+         "src": np.array([e[0] for e in edges], np.int32),
+         "dst": np.array([e[1] for e in edges], np.int32),
+         "w": np.array([e[2] for e in edges], np.float32), "enabled": np.ones(len(edges), np.uint8)}
+    check_raw(emr, [g], W.xor_sources(), 6)
+
+
+# ------------------------------------------------------------------------------- discovery
+
+@pytest.mark.parametrize("theta", [0.03, 1e-3, 1e-4])
+def test_discover_single_cppn_depth5(emr, theta):
+    # this seeded CPPN is smooth: nothing passes 0.03 (the oracle agrees), 160 cells pass 1e-4
+    genomes, sources, D, _ = W.workload("single_d5")
+    st = check_discover(emr, genomes, sources, D, theta)
+    assert (st["records"] > 0) == (theta < 0.01)
+
+
+@pytest.mark.parametrize("D", [5, 6])
+def test_discover_xor_population(emr, D):
+    genomes = W.population(0, 120 if D == 5 else 40, 20, 60)
+    st = check_discover(emr, genomes, W.xor_sources(), D, 0.03)
+    assert st["records"] > 0
+
+
+def test_discover_tabular_population(emr):
+    genomes = W.population(2, 12, 40, 120)
+    check_discover(emr, genomes, W.tabular_sources(32), 5, 0.03)
+
+
+def test_discover_per_genome_sources(emr):
+    # per-genome (CSR) source lists of varying length, as the hidden->hidden phase uses
+    rng = np.random.default_rng(5)
+    genomes = W.population(3, 9, 12, 40)
+    pts, offs = [], [0]
+    for k in range(len(genomes)):
+        n = int(rng.integers(0, 7))
+        for _ in range(n):
+            pts.append((float(rng.uniform(-1, 1)), float(rng.uniform(-1, 1)), int(rng.integers(0, 2))))
+        offs.append(len(pts))
+    sources = W.sources_array(pts)
+    check_discover(emr, genomes, sources, 5, 0.02, offs=offs)
+
+
+@pytest.mark.parametrize("D", [0, 1, 2, 3, 4])
+def test_discover_small_depths(emr, D):
+    genomes = W.population(4, 10, 10, 30)
+    check_discover(emr, genomes, W.xor_sources(), D, 0.01)
+
+
+def test_theta_extremes(emr):
+    genomes = W.population(6, 6, 10, 30)
+    srcs = W.xor_sources()
+    st = check_discover(emr, genomes, srcs, 4, -1.0)
+    assert st["records"] == len(genomes) * len(srcs) * oracle.n_parents(4)
+    st = check_discover(emr, genomes, srcs, 4, math.inf)
+    assert st["records"] == 0
+
+
+def test_constant_cppn_keeps_nothing(emr):
+    g = {"kind": np.array([0, 1, 2, 3, 4, 6], np.uint8), "act": np.array([0] * 5 + [1], np.uint8),
+         "bias": np.zeros(6, np.float32), "src": np.array([0, 4], np.int32),
+         "dst": np.array([5, 5], np.int32), "w": np.array([1.0, 0.5], np.float32),
+         "enabled": np.ones(2, np.uint8)}
+    srcs = W.sources_array([(0.3, -1.0, 0), (0.1, 0.2, 0)])
+    st = check_discover(emr, [g], srcs, 5, 0.0)
+    assert st["records"] == 0
+
+
+def test_infinite_weights_give_nan_variance_never_kept(emr):
+    g = {"kind": np.array([0, 1, 2, 3, 4, 6], np.uint8), "act": np.zeros(6, np.uint8),
+         "bias": np.zeros(6, np.float32), "src": np.array([2], np.int32),
+         "dst": np.array([5], np.int32), "w": np.array([np.inf], np.float32),
+         "enabled": np.ones(1, np.uint8)}
+    st = check_discover(emr, [g], W.xor_sources()[:1], 4, -1.0)
+    assert st["records"] == 0
+
+
+def test_empty_population_and_no_sources(emr):
+    pop = emr.emr_pack_population(W.population(0, 3, 5, 10))
+    res = emr.emr_discover(pop, W.xor_sources()[:0], 5, 0.03)
+    assert emr.emr_result_check(res) == 0
+    pop0 = emr.emr_pack_population([])
+    res = emr.emr_discover(pop0, W.xor_sources(), 5, 0.03)
+    assert emr.emr_result_check(res) == 0
+
+
+def test_capacity_overflow_is_reported(emr):
+    genomes, sources, D, theta = W.workload("single_d5")
+    pop = emr.emr_pack_population(genomes)
+    res = emr.emr_discover(pop, sources, D, -1.0, pair_capacity=10)
+    with pytest.raises(emr.EmrError) as e:
+        emr.emr_result_check(res)
+    assert e.value.status == emr.EMR_E_CAPACITY
+    # the records that fit are the first ones
+    counts, recs = emr.records_to_host(res)
+    assert counts[0] == oracle.n_parents(D)
+    np.testing.assert_array_equal(recs[0][0], np.arange(10))
+
+
+def test_lookback_placement_matches_padded_placement(emr):
+    """A pair capacity below Q(D) switches record placement to the look-back scan; both
+    placements must give identical records."""
+    genomes = W.population(12, 80, 20, 60)
+    srcs = W.xor_sources()
+    pop = emr.emr_pack_population(genomes)
+    a = emr.emr_discover(pop, srcs, 6, 0.01)
+    mx = emr.emr_result_check(a)
+    assert mx < oracle.n_parents(6)
+    b = emr.emr_discover(pop, srcs, 6, 0.01, pair_capacity=mx)
+    assert emr.emr_result_check(b) == mx
+    ca, ra = emr.records_to_host(a)
+    cb, rb = emr.records_to_host(b)
+    np.testing.assert_array_equal(ca, cb)
+    for (pa, wa), (pb, wb) in zip(ra, rb):
+        np.testing.assert_array_equal(pa, pb)
+        np.testing.assert_array_equal(wa.view(np.uint32), wb.view(np.uint32))
+    st = check_discover(emr, genomes, srcs, 6, 0.01, cap=mx)
+    assert st["records"] == int(ca.sum())
+
+
+def test_discover_is_deterministic(emr):
+    genomes = W.population(8, 60, 20, 60)
+    pop = emr.emr_pack_population(genomes)
+    a = emr.emr_discover(pop, W.xor_sources(), 6, 0.03)
+    emr.emr_result_check(a)
+    b = emr.emr_discover(pop, W.xor_sources(), 6, 0.03)
+    emr.emr_result_check(b)
+    ca, ra = emr.records_to_host(a)
+    cb, rb = emr.records_to_host(b)
+    np.testing.assert_array_equal(ca, cb)
+    for (pa, wa), (pb, wb) in zip(ra, rb):
+        np.testing.assert_array_equal(pa, pb)
+        np.testing.assert_array_equal(wa.view(np.uint32), wb.view(np.uint32))
+
+
+def test_direction_duality_bit_exact(emr):
+    genomes = W.population(9, 10, 12, 40)
+    swapped = []
+    for g in genomes:
+        h = dict(g)
+        k = g["kind"].copy()
+        k[0], k[1], k[2], k[3] = 2, 3, 0, 1
+        h["kind"] = k
+        swapped.append(h)
+    pa = emr.emr_pack_population(genomes)
+    pb = emr.emr_pack_population(swapped)
+    ra = emr.emr_eval_raw(pa, W.sources_array([(0.25, -0.5, 0)]), 5).cpu().numpy()
+    rb = emr.emr_eval_raw(pb, W.sources_array([(0.25, -0.5, 1)]), 5).cpu().numpy()
+    np.testing.assert_array_equal(ra.view(np.uint32), rb.view(np.uint32))
+
+
+# ------------------------------------------------------------------------------- full size
+
+def test_full_size_xor_pop1000_depth7_sampled(emr):
+    """The benchmark's workload and launch: 1000 genomes x 4 sources at depth 7, one discover
+    call; the oracle recomputes a deterministic sample of whole pairs."""
+    genomes, sources, D, theta = W.workload("xor_pop1000_d7")
+    theta32 = float(np.float32(theta))
+    pop = emr.emr_pack_population(genomes)
+    res = emr.emr_discover(pop, sources, D, theta32)
+    emr.emr_result_check(res)
+    counts, recs = emr.records_to_host(res)
+    rng = np.random.default_rng(123)
+    sample = sorted(rng.choice(len(counts), size=16, replace=False).tolist())
+    for r in sample:
+        g, s = genomes[r // 4], sources[r % 4]
+        o = oracle.discover([g], [s], D, theta32)
+        gp, gw = recs[r]
+        if counts[r] == o["pair_count"][0] and np.array_equal(gp, o["parent"]):
+            assert close(gw, o["w4"]).all(), r
+        else:
+            diff = np.setxor1d(gp, o["parent"])
+            _, dvar = oracle.eval_parents(g, s, diff)
+            assert np.all(np.abs(dvar - theta32) <= BAND), (r, diff[:5], dvar[:5])
