@@ -32,19 +32,23 @@ constexpr int kTile = kWave * kTileIters;  // 256 = 4^4 positions
 constexpr int kFirstAlignedLevel = 4;     // first level whose size is a multiple of kTile
 
 // ---------------------------------------------------------------- varying program
-// At blob[var_off]: n_steps step records of 4 words, then the edge words they point to.
-//   step word 0: act | dst_slot << 8
-//   step word 1: n_x | n_y << 8 | n_node << 16   (edges from the position's x, then from its y,
-//                                                 then from earlier varying nodes)
-//   step word 2: absolute word offset of the step's first edge in the blob
-//   step word 3: 0
-//   edge: two words {src, float bits of w}; src is 0 for an x edge, 1 for a y edge, and the
-//   register slot of the source node for a node edge.
+// At blob[var_off]: n_steps step headers of 4 words, one per position-dependent node in
+// topological order:
+//   word 0: act (bits 0..2) | dst slot (bits 8..15) | has_x (bit 16) | has_y (bit 17)
+//           | number of node edges (bits 20..31)
+//   word 1: float bits of the summed weights of the node's edges from the position's x
+//   word 2: the same for y
+//   word 3: 0
+// At blob[edge_off]: the node edges of all steps, step after step, two words each:
+//   {register slot of the source node, float bits of w}.
 // The step's bias is not stored here: it is the per-source folded bias from the bind kernel.
-// The last step computes the output when the output is varying; its dst slot is unused.
-struct StepWords {
-  uint32_t meta0, meta1, edge_off, pad;
-};
+// The last step computes the output when the output varies; its dst slot is unused.
+constexpr uint32_t kStepActMask = 7u;
+constexpr uint32_t kStepDstShift = 8;
+constexpr uint32_t kStepHasX = 1u << 16;
+constexpr uint32_t kStepHasY = 1u << 17;
+constexpr uint32_t kStepEdgeShift = 20;
+constexpr uint32_t kMaxStepEdges = (1u << 12) - 1;
 
 // ---------------------------------------------------------------- uniform program
 // At blob[uni_off]:
@@ -56,19 +60,23 @@ struct StepWords {
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 
 struct ProgDesc {
-  uint32_t var_off;   // word offset of the varying program
+  uint32_t var_off;   // word offset of the step headers
+  uint32_t edge_off;  // word offset of the node-edge stream
   uint32_t n_steps;   // varying steps
   uint32_t uni_off;   // word offset of the uniform program
   uint32_t flags;     // bit 0: output varies with position; bits 8..15: register window needed
+  uint32_t pad[3];
 };
 
 // One unit of kernel work: up to kMaxGroup sources of one genome sharing a direction.
 struct Group {
   uint32_t var_off;
+  uint32_t edge_off;
   uint32_t n_steps;
   uint32_t flags;      // copied from ProgDesc
-  uint32_t bias_off;   // float offset into the bias table: [step][member], then out constants
-  uint32_t pair[kMaxGroup];  // global pair ids of the members (unused members repeat the last)
+  uint32_t bias_off;   // float offset into the bias table: [step][source], then out constants
+  uint32_t pad[3];
+  uint32_t pair[kMaxGroup];  // global pair ids of the sources (unused entries repeat the last)
 };
 
 // One (genome, direction, source) evaluated by the bind kernel.

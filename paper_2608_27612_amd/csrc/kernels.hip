@@ -98,144 +98,13 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 }
 
 // ------------------------------------------------------------------------ register windows
-// The varying values of member s live in a VGPR tuple pinned at v[32 + s*W .. 32 + s*W + W-1].
-// One s_set_gpr_idx_on per edge indexes the same slot in every member's tuple, so the S fused
-// multiply-adds of an edge share one index setup. The tuples are declared as asm operands, so the
-// compiler keeps them in place and knows which registers each statement reads or writes.
+// RegWin<M, W>: the M instances' varying values in pinned VGPR tuples, the indexed edge FMAs and
+// the indexed activation stores (generated, see gen_regwin.py). The tuples are asm operands, so
+// the compiler keeps them in place and knows which registers each statement reads or writes.
 // s_set_gpr_idx_on also writes M0; M0 is reserved by the compiler and this kernel has no other
 // use of it (no LDS DMA, no message or GWS instructions), which the ISA check in the tests
 // enforces.
-template <int W> struct Win;
-
-#define EMR_DEFINE_WIN(W_, T_, R0, R1, R2, R3)                                                    \
-  template <> struct Win<W_> {                                                                  \
-    T_ v0, v1, v2, v3;                                                                          \
-    __device__ __forceinline__ void init() {                                                    \
-      v0 = (T_)(0.0f); v1 = (T_)(0.0f); v2 = (T_)(0.0f); v3 = (T_)(0.0f);                       \
-    }                                                                                           \
-    template <int S>                                                                            \
-    __device__ __forceinline__ void fma(float* a, uint32_t src, float w) {                      \
-      if constexpr (S == 1) {                                                                   \
-        asm volatile("s_set_gpr_idx_on %[src], gpr_idx(SRC0)\n\t"                               \
-                     "v_fma_f32 %[a0], " R0##_B ", %[w], %[a0]\n\t"                             \
-                     "s_set_gpr_idx_off"                                                        \
-                     : [a0] "+v"(a[0])                                                          \
-                     : [src] "s"(src), [w] "s"(w), R0##_C(v0)                                   \
-                     :);                                                                   \
-      } else if constexpr (S == 2) {                                                            \
-        asm volatile("s_set_gpr_idx_on %[src], gpr_idx(SRC0)\n\t"                               \
-                     "v_fma_f32 %[a0], " R0##_B ", %[w], %[a0]\n\t"                             \
-                     "v_fma_f32 %[a1], " R1##_B ", %[w], %[a1]\n\t"                             \
-                     "s_set_gpr_idx_off"                                                        \
-                     : [a0] "+v"(a[0]), [a1] "+v"(a[1])                                         \
-                     : [src] "s"(src), [w] "s"(w), R0##_C(v0), R1##_C(v1)                       \
-                     :);                                                                   \
-      } else if constexpr (S == 3) {                                                            \
-        asm volatile("s_set_gpr_idx_on %[src], gpr_idx(SRC0)\n\t"                               \
-                     "v_fma_f32 %[a0], " R0##_B ", %[w], %[a0]\n\t"                             \
-                     "v_fma_f32 %[a1], " R1##_B ", %[w], %[a1]\n\t"                             \
-                     "v_fma_f32 %[a2], " R2##_B ", %[w], %[a2]\n\t"                             \
-                     "s_set_gpr_idx_off"                                                        \
-                     : [a0] "+v"(a[0]), [a1] "+v"(a[1]), [a2] "+v"(a[2])                        \
-                     : [src] "s"(src), [w] "s"(w), R0##_C(v0), R1##_C(v1), R2##_C(v2)           \
-                     :);                                                                   \
-      } else {                                                                                  \
-        asm volatile("s_set_gpr_idx_on %[src], gpr_idx(SRC0)\n\t"                               \
-                     "v_fma_f32 %[a0], " R0##_B ", %[w], %[a0]\n\t"                             \
-                     "v_fma_f32 %[a1], " R1##_B ", %[w], %[a1]\n\t"                             \
-                     "v_fma_f32 %[a2], " R2##_B ", %[w], %[a2]\n\t"                             \
-                     "v_fma_f32 %[a3], " R3##_B ", %[w], %[a3]\n\t"                             \
-                     "s_set_gpr_idx_off"                                                        \
-                     : [a0] "+v"(a[0]), [a1] "+v"(a[1]), [a2] "+v"(a[2]), [a3] "+v"(a[3])       \
-                     : [src] "s"(src), [w] "s"(w), R0##_C(v0), R1##_C(v1), R2##_C(v2),          \
-                       R3##_C(v3)                                                               \
-                     :);                                                                   \
-      }                                                                                         \
-    }                                                                                           \
-    template <int S>                                                                            \
-    __device__ __forceinline__ void store(uint32_t dst, const float* r) {                       \
-      if constexpr (S == 1) {                                                                   \
-        asm volatile("s_set_gpr_idx_on %[dst], gpr_idx(DST)\n\t"                                \
-                     "v_mov_b32 " R0##_B ", %[r0]\n\t"                                          \
-                     "s_set_gpr_idx_off"                                                        \
-                     : R0##_O(v0)                                                               \
-                     : [dst] "s"(dst), [r0] "v"(r[0])                                           \
-                     :);                                                                   \
-      } else if constexpr (S == 2) {                                                            \
-        asm volatile("s_set_gpr_idx_on %[dst], gpr_idx(DST)\n\t"                                \
-                     "v_mov_b32 " R0##_B ", %[r0]\n\t"                                          \
-                     "v_mov_b32 " R1##_B ", %[r1]\n\t"                                          \
-                     "s_set_gpr_idx_off"                                                        \
-                     : R0##_O(v0), R1##_O(v1)                                                   \
-                     : [dst] "s"(dst), [r0] "v"(r[0]), [r1] "v"(r[1])                           \
-                     :);                                                                   \
-      } else if constexpr (S == 3) {                                                            \
-        asm volatile("s_set_gpr_idx_on %[dst], gpr_idx(DST)\n\t"                                \
-                     "v_mov_b32 " R0##_B ", %[r0]\n\t"                                          \
-                     "v_mov_b32 " R1##_B ", %[r1]\n\t"                                          \
-                     "v_mov_b32 " R2##_B ", %[r2]\n\t"                                          \
-                     "s_set_gpr_idx_off"                                                        \
-                     : R0##_O(v0), R1##_O(v1), R2##_O(v2)                                       \
-                     : [dst] "s"(dst), [r0] "v"(r[0]), [r1] "v"(r[1]), [r2] "v"(r[2])           \
-                     :);                                                                   \
-      } else {                                                                                  \
-        asm volatile("s_set_gpr_idx_on %[dst], gpr_idx(DST)\n\t"                                \
-                     "v_mov_b32 " R0##_B ", %[r0]\n\t"                                          \
-                     "v_mov_b32 " R1##_B ", %[r1]\n\t"                                          \
-                     "v_mov_b32 " R2##_B ", %[r2]\n\t"                                          \
-                     "v_mov_b32 " R3##_B ", %[r3]\n\t"                                          \
-                     "s_set_gpr_idx_off"                                                        \
-                     : R0##_O(v0), R1##_O(v1), R2##_O(v2), R3##_O(v3)                           \
-                     : [dst] "s"(dst), [r0] "v"(r[0]), [r1] "v"(r[1]), [r2] "v"(r[2]),          \
-                       [r3] "v"(r[3])                                                           \
-                     :);                                                                   \
-      }                                                                                         \
-    }                                                                                           \
-  };
-
-// Base register name (_B), input constraint (_C) and in/out constraint (_O) of each tuple.
-#define W8_0_B "v32"
-#define W8_0_C(x) "{v[32:39]}"(x)
-#define W8_0_O(x) "+{v[32:39]}"(x)
-#define W8_1_B "v40"
-#define W8_1_C(x) "{v[40:47]}"(x)
-#define W8_1_O(x) "+{v[40:47]}"(x)
-#define W8_2_B "v48"
-#define W8_2_C(x) "{v[48:55]}"(x)
-#define W8_2_O(x) "+{v[48:55]}"(x)
-#define W8_3_B "v56"
-#define W8_3_C(x) "{v[56:63]}"(x)
-#define W8_3_O(x) "+{v[56:63]}"(x)
-
-#define W16_0_B "v32"
-#define W16_0_C(x) "{v[32:47]}"(x)
-#define W16_0_O(x) "+{v[32:47]}"(x)
-#define W16_1_B "v48"
-#define W16_1_C(x) "{v[48:63]}"(x)
-#define W16_1_O(x) "+{v[48:63]}"(x)
-#define W16_2_B "v64"
-#define W16_2_C(x) "{v[64:79]}"(x)
-#define W16_2_O(x) "+{v[64:79]}"(x)
-#define W16_3_B "v80"
-#define W16_3_C(x) "{v[80:95]}"(x)
-#define W16_3_O(x) "+{v[80:95]}"(x)
-
-#define W32_0_B "v32"
-#define W32_0_C(x) "{v[32:63]}"(x)
-#define W32_0_O(x) "+{v[32:63]}"(x)
-#define W32_1_B "v64"
-#define W32_1_C(x) "{v[64:95]}"(x)
-#define W32_1_O(x) "+{v[64:95]}"(x)
-#define W32_2_B "v96"
-#define W32_2_C(x) "{v[96:127]}"(x)
-#define W32_2_O(x) "+{v[96:127]}"(x)
-#define W32_3_B "v128"
-#define W32_3_C(x) "{v[128:159]}"(x)
-#define W32_3_O(x) "+{v[128:159]}"(x)
-
-EMR_DEFINE_WIN(8, f32x8, W8_0, W8_1, W8_2, W8_3)
-EMR_DEFINE_WIN(16, f32x16, W16_0, W16_1, W16_2, W16_3)
-EMR_DEFINE_WIN(32, f32x32, W32_0, W32_1, W32_2, W32_3)
+#include "regwin_gen.h"
 
 // ------------------------------------------------------------------------ look-back scan
 // Tile status words of one pair, indexed by tile. A tile publishes its local count as an
@@ -304,13 +173,44 @@ struct DiscoverScalars {
 // afterwards by k_compact); records placed directly through the look-back scan (any capacity).
 constexpr int kModeRaw = 0, kModePadded = 1, kModeLookback = 2;
 
-template <int S, int W, int MODE>
+// Read-only tables are read through the constant address space: the kernel never writes them
+// during a launch, and uniform loads from it are always scalar loads (s_load through the scalar
+// cache), whatever the kernel stores elsewhere.
+typedef __attribute__((address_space(4))) const uint32_t cu32;
+typedef __attribute__((address_space(4))) const float cf32;
+
+// One Group record (12 words) through the constant address space.
+__device__ __forceinline__ Group load_group(cu32* p) {
+  Group g;
+  g.var_off = p[0];
+  g.edge_off = p[1];
+  g.n_steps = p[2];
+  g.flags = p[3];
+  g.bias_off = p[4];
+  g.pad[0] = g.pad[1] = g.pad[2] = 0;
+#pragma unroll
+  for (int k = 0; k < kMaxGroup; ++k) g.pair[k] = p[8 + k];
+  return g;
+}
+static_assert(sizeof(Group) == 12 * sizeof(uint32_t), "Group layout");
+
+struct Words4 {
+  uint32_t x, y, z, w;
+};
+// Four consecutive program words (scalar loads; the compiler merges them).
+__device__ __forceinline__ Words4 load4(cu32* p) { return Words4{p[0], p[1], p[2], p[3]}; }
+
+// S sources of one genome and direction per group; each lane evaluates them at P positions of the
+// tile at once (M = S * P instances; instance m = s * P + j is source s at position j). One walk of
+// the program therefore serves M queries.
+template <int S, int P, int W, int MODE>
 __global__ void __launch_bounds__(256)
     k_discover(const uint32_t* __restrict__ blob, const Group* __restrict__ groups,
                const float* __restrict__ bias_tab, uint64_t* __restrict__ status,
-               uint32_t* __restrict__ err,
-               uint32_t* __restrict__ parent, float* __restrict__ w4,
+               uint32_t* __restrict__ err, uint32_t* __restrict__ parent, float* __restrict__ w4,
                int64_t* __restrict__ pair_count, float* __restrict__ raw, DiscoverScalars a) {
+  constexpr int M = S * P;
+  constexpr int NPASS = kTileIters / P;
   const uint32_t lane = lane_id();
   // Within a level-aligned tile the grid index's 6 low bits are the lane id; its Morton bits give
   // the low 3 bits of the cell's column (even bits) and row (odd bits).
@@ -318,9 +218,10 @@ __global__ void __launch_bounds__(256)
   const uint32_t j_lo = ((lane >> 1) & 1u) | ((lane >> 2) & 2u) | ((lane >> 3) & 4u);
   const float i_lo_f = (float)(2u * i_lo);
   const float j_lo_f = (float)(2u * j_lo);
-  const int64_t head_len = a.depth < kFirstAlignedLevel ? a.n_pos : level_offset(kFirstAlignedLevel);
+  const uint32_t head_len =
+      (uint32_t)(a.depth < kFirstAlignedLevel ? a.n_pos : level_offset(kFirstAlignedLevel));
 
-  Win<W> R;
+  RegWin<M, W> R;
   R.init();
 
   // Static round-robin: global wave w takes tiles w, w + n_waves, w + 2 n_waves, ... Consecutive
@@ -328,148 +229,213 @@ __global__ void __launch_bounds__(256)
   const uint32_t n_waves = gridDim.x * (blockDim.x / kWave);
   const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +
                                                        threadIdx.x / kWave);
+  cu32* cblob = (cu32*)blob;
+  cu32* cgroups = (cu32*)groups;
+  cf32* cbias = (cf32*)bias_tab;
   for (uint32_t t = wave; t < a.n_tiles; t += n_waves) {
-
     const uint32_t gi = t / a.tiles;
     const uint32_t tile = t - gi * a.tiles;
-    const Group G = groups[gi];
+    const Group G = load_group(cgroups + 12 * gi);
     const bool out_varying = (G.flags & 1u) != 0;
-    const float* bt = bias_tab + G.bias_off;
-    const uint32_t* steps = blob + G.var_off;
+    cu32* hdr = cblob + G.var_off;
+    cf32* bt = cbias + G.bias_off;
 
-    // Tile geometry.
-    uint32_t p0, n_valid, n_iter;
-    int lvl = 0;
-    uint32_t m0 = 0;
+    // Tile geometry: the head tile holds levels 1..3 (84 positions), every other tile 256
+    // positions of one level, starting at Morton index m0 of level lvl.
     const bool head = tile == 0;
-    if (head) {
-      p0 = 0;
-      n_valid = (uint32_t)head_len;
-      n_iter = (n_valid + kWave - 1) / kWave;
-    } else {
+    uint32_t p0 = 0, n_valid = head_len, m0 = 0;
+    int lvl = 0;
+    if (!head) {
       p0 = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(tile - 1) * kTile);
       n_valid = kTile;
-      n_iter = kTileIters;
       lvl = (31 - __builtin_clz(3u * p0 + 4u)) >> 1;
       m0 = p0 - (uint32_t)level_offset(lvl);
     }
 
-    float wbuf[kTileIters][S];
+    uint32_t run[S];  // records so far in this tile, per source (padded mode)
+#pragma unroll
+    for (int s = 0; s < S; ++s) run[s] = 0;
+    float wbuf[kTileIters][S];      // look-back mode only: outputs and decisions of the tile
     uint64_t keep[kTileIters][S];
+    if constexpr (MODE == kModeLookback) {
 #pragma unroll
-    for (int it = 0; it < kTileIters; ++it) {
-#pragma unroll
-      for (int s = 0; s < S; ++s) {
-        wbuf[it][s] = 0.0f;
-        keep[it][s] = 0ull;
-      }
-    }
-
-#pragma unroll
-    for (int it = 0; it < kTileIters; ++it) {
-      if ((uint32_t)it >= n_iter) break;
-      const uint32_t p = p0 + (uint32_t)it * kWave + lane;
-      const bool valid = (uint32_t)it * kWave + lane < n_valid;
-      float px, py;
-      if (!head) {
-        const uint32_t m_hi = (m0 >> 6) + (uint32_t)it;
-        const float scale = pow2_neg(lvl);
-        const float bx = __builtin_fmaf((float)(16u * compact_even(m_hi) + 1u), scale, -1.0f);
-        const float by = __builtin_fmaf((float)(16u * compact_even(m_hi >> 1) + 1u), scale, -1.0f);
-        px = __builtin_fmaf(i_lo_f, scale, bx);
-        py = __builtin_fmaf(j_lo_f, scale, by);
-      } else {
-        const int l = level_of(p);
-        const uint32_t m = p - (uint32_t)level_offset(l);
-        const float scale = pow2_neg(l);
-        px = __builtin_fmaf((float)(2u * compact_even(m) + 1u), scale, -1.0f);
-        py = __builtin_fmaf((float)(2u * compact_even(m >> 1) + 1u), scale, -1.0f);
-      }
-
-      // ---- CPPN: the varying program, in topological order, for the S sources at once.
-      float acc[S];
-      for (uint32_t st = 0; st < G.n_steps; ++st) {
-        const uint32_t meta0 = steps[4 * st + 0];
-        const uint32_t meta1 = steps[4 * st + 1];
-        const uint32_t eo = steps[4 * st + 2];
-#pragma unroll
-        for (int s = 0; s < S; ++s) acc[s] = bt[st * S + s];
-        const uint32_t nx = meta1 & 0xFFu, ny = (meta1 >> 8) & 0xFFu, nn = meta1 >> 16;
-        const uint32_t* ep = blob + eo;
-        for (uint32_t e = 0; e < nx; ++e) {
-          const float w = __uint_as_float(ep[2 * e + 1]);
-#pragma unroll
-          for (int s = 0; s < S; ++s) acc[s] = __builtin_fmaf(w, px, acc[s]);
-        }
-        ep += 2 * nx;
-        for (uint32_t e = 0; e < ny; ++e) {
-          const float w = __uint_as_float(ep[2 * e + 1]);
-#pragma unroll
-          for (int s = 0; s < S; ++s) acc[s] = __builtin_fmaf(w, py, acc[s]);
-        }
-        ep += 2 * ny;
-        for (uint32_t e = 0; e < nn; ++e) {
-          R.template fma<S>(acc, ep[2 * e], __uint_as_float(ep[2 * e + 1]));
-        }
-        const uint32_t act = meta0 & 0xFFu;
-#pragma unroll
-        for (int s = 0; s < S; ++s) acc[s] = act_apply(act, acc[s]);
-        if (st + 1 < G.n_steps) R.template store<S>((meta0 >> 8) & 0xFFu, acc);
-      }
-      float w[S];
-#pragma unroll
-      for (int s = 0; s < S; ++s) w[s] = out_varying ? acc[s] : bt[G.n_steps * S + s];
-
-      if constexpr (MODE == kModeRaw) {
-        if (valid) {
-#pragma unroll
-          for (int s = 0; s < S; ++s) raw[(int64_t)G.pair[s] * a.n_pos + p] = w[s];
-        }
-      } else {
-        // ---- variance of the four siblings (Section 3.2) and the threshold test (Eq. 2)
+      for (int it = 0; it < kTileIters; ++it)
 #pragma unroll
         for (int s = 0; s < S; ++s) {
-          const float s1 = quad_sum(w[s]);
-          const float d = __builtin_fmaf(-0.25f, s1, w[s]);   // w - mean, mean = s1/4 exactly
+          wbuf[it][s] = 0.0f;
+          keep[it][s] = 0ull;
+        }
+    }
+
+#pragma unroll MODE == kModeLookback ? NPASS : 1
+    for (int pass = 0; pass < NPASS; ++pass) {
+      if ((uint32_t)(pass * P * kWave) >= n_valid) break;
+      // ---- positions of this pass (Eq. 1 cell centres, decoded from the grid index)
+      float px[P], py[P];
+      bool valid[P];
+      uint32_t pidx[P];
+#pragma unroll
+      for (int j = 0; j < P; ++j) {
+        const uint32_t it = (uint32_t)(pass * P + j);
+        const uint32_t p = p0 + it * kWave + lane;
+        pidx[j] = p;
+        valid[j] = it * kWave + lane < n_valid;
+        if (!head) {
+          const uint32_t m_hi = (m0 >> 6) + it;
+          const float scale = pow2_neg(lvl);
+          const float bx = __builtin_fmaf((float)(16u * compact_even(m_hi) + 1u), scale, -1.0f);
+          const float by = __builtin_fmaf((float)(16u * compact_even(m_hi >> 1) + 1u), scale, -1.0f);
+          px[j] = __builtin_fmaf(i_lo_f, scale, bx);
+          py[j] = __builtin_fmaf(j_lo_f, scale, by);
+        } else {
+          const int l = level_of(p);
+          const uint32_t m = p - (uint32_t)level_offset(l);
+          const float scale = pow2_neg(l);
+          px[j] = __builtin_fmaf((float)(2u * compact_even(m) + 1u), scale, -1.0f);
+          py[j] = __builtin_fmaf((float)(2u * compact_even(m >> 1) + 1u), scale, -1.0f);
+        }
+      }
+
+      // ---- CPPN (Section 2): the varying program in topological order, M instances at once.
+      float acc[M];
+      cu32* ep = cblob + G.edge_off;
+      cu32* hp = hdr;
+      cf32* bs = bt;
+      for (uint32_t st = 0; st < G.n_steps; ++st, hp += 4, bs += S) {
+        const Words4 h = load4(hp);
+        // the position's x and y terms (coefficient 0 when the node has no such edge), then the
+        // source's folded bias
+        const float ax = __uint_as_float(h.y), ay = __uint_as_float(h.z);
+        if constexpr (S == 1) {
+          const float b = bs[0];
+#pragma unroll
+          for (int j = 0; j < P; ++j)
+            acc[j] = __builtin_fmaf(py[j], ay, __builtin_fmaf(px[j], ax, b));
+        } else {
+          float lin[P];
+#pragma unroll
+          for (int j = 0; j < P; ++j) lin[j] = __builtin_fmaf(py[j], ay, px[j] * ax);
+#pragma unroll
+          for (int m = 0; m < M; ++m) acc[m] = lin[m % P] + bs[m / P];
+        }
+        uint32_t nn = h.x >> kStepEdgeShift;
+        while (nn >= 4) {
+          const Words4 e0 = load4(ep);
+          const Words4 e1 = load4(ep + 4);
+          R.fma4(acc, e0.x, __uint_as_float(e0.y), e0.z, __uint_as_float(e0.w), e1.x,
+                 __uint_as_float(e1.y), e1.z, __uint_as_float(e1.w));
+          ep += 8;
+          nn -= 4;
+        }
+        if (nn != 0) {
+          // may read past the program's last edge; the population table is padded for it
+          const Words4 e0 = load4(ep);
+          const Words4 e1 = load4(ep + 4);
+          if (nn == 1) {
+            R.fma1(acc, e0.x, __uint_as_float(e0.y));
+          } else if (nn == 2) {
+            R.fma2(acc, e0.x, __uint_as_float(e0.y), e0.z, __uint_as_float(e0.w));
+          } else {
+            R.fma3(acc, e0.x, __uint_as_float(e0.y), e0.z, __uint_as_float(e0.w), e1.x,
+                   __uint_as_float(e1.y));
+          }
+          ep += 2 * nn;
+        }
+        switch (h.x & kStepActMask) {
+          case EMR_ACT_SIGMOID:
+#pragma unroll
+            for (int m = 0; m < M; ++m) acc[m] = act_sigmoid(acc[m]);
+            break;
+          case EMR_ACT_TANH:
+#pragma unroll
+            for (int m = 0; m < M; ++m) acc[m] = act_tanh(acc[m]);
+            break;
+          case EMR_ACT_GAUSS:
+#pragma unroll
+            for (int m = 0; m < M; ++m) acc[m] = act_gauss(acc[m]);
+            break;
+          case EMR_ACT_SINE:
+#pragma unroll
+            for (int m = 0; m < M; ++m) acc[m] = act_sine(acc[m]);
+            break;
+          case EMR_ACT_ABS:
+#pragma unroll
+            for (int m = 0; m < M; ++m) acc[m] = __builtin_fabsf(acc[m]);
+            break;
+          default:
+            break;
+        }
+        if (st + 1 < G.n_steps) R.st_mov((h.x >> kStepDstShift) & 0xFFu, acc);
+      }
+      float w[M];
+      cf32* bo = bt + G.n_steps * S;  // output constants when the output is uniform
+#pragma unroll
+      for (int m = 0; m < M; ++m) w[m] = out_varying ? acc[m] : bo[m / P];
+
+      // ---- variance of the four siblings (Section 3.2) and the threshold test (Eq. 2)
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+#pragma unroll
+        for (int j = 0; j < P; ++j) {
+          const int m = s * P + j;
+          if constexpr (MODE == kModeRaw) {
+            if (valid[j]) raw[(int64_t)G.pair[s] * a.n_pos + pidx[j]] = w[m];
+            continue;
+          }
+          const float s1 = quad_sum(w[m]);
+          const float d = __builtin_fmaf(-0.25f, s1, w[m]);  // w - mean, mean = s1/4 exactly
           const float s2 = quad_sum(__fmul_rn(d, d));
           const float var = s2 * 0.25f;
-          keep[it][s] = ballot(valid && (var > a.theta));
-          wbuf[it][s] = w[s];
+          const uint64_t kb = ballot(valid[j] && (var > a.theta));
+          if constexpr (MODE == kModeLookback) {
+            keep[pass * P + j][s] = kb;
+            wbuf[pass * P + j][s] = w[m];
+          } else {
+            if (kb != 0ull) {
+              if ((kb >> lane) & 1ull) {
+                // this tile's records start at its first parent index within the pair
+                const int64_t slot = (int64_t)G.pair[s] * a.cap + (p0 >> 2) + run[s] +
+                                     (mbcnt64(kb) >> 2);
+                w4[slot * 4 + (lane & 3u)] = w[m];
+                if ((lane & 3u) == 0) parent[slot] = pidx[j] >> 2;
+              }
+              run[s] += popc64(kb) >> 2;
+            }
+          }
         }
       }
     }
-    if constexpr (MODE == kModeRaw) continue;
 
-    // ---- compaction. Padded: the tile's records go to its own slots (the tile's first parent
-    // index within the pair), and the count is left for k_compact. Look-back: the tile learns its
-    // exact offset in the pair from the scan.
+    if constexpr (MODE == kModePadded) {
+      if (lane == 0) {
 #pragma unroll
-    for (int s = 0; s < S; ++s) {
-      uint64_t cnt = 0;
-#pragma unroll
-      for (int it = 0; it < kTileIters; ++it) cnt += popc64(keep[it][s]) >> 2;
-      const uint32_t pair = G.pair[s];
-      uint64_t base;
-      if constexpr (MODE == kModePadded) {
-        base = p0 >> 2;
-        if (lane == 0) status[(int64_t)pair * a.tiles + tile] = cnt;
-      } else {
-        base = lookback(status + (int64_t)pair * a.tiles, tile, cnt, err);
-        if (tile + 1 == a.tiles && lane == 0) pair_count[pair] = (int64_t)(base + cnt);
+        for (int s = 0; s < S; ++s) status[(int64_t)G.pair[s] * a.tiles + tile] = run[s];
       }
-      const int64_t region = (int64_t)pair * a.cap;
+    }
+    if constexpr (MODE == kModeLookback) {
+      // ---- the tile learns its exact offset within each pair from the look-back scan
 #pragma unroll
-      for (int it = 0; it < kTileIters; ++it) {
-        const uint64_t m = keep[it][s];
-        if ((m >> lane) & 1ull) {
-          const int64_t idx = (int64_t)base + (int64_t)(mbcnt64(m) >> 2);
-          if (idx < a.cap) {
-            w4[(region + idx) * 4 + (lane & 3u)] = wbuf[it][s];
-            if ((lane & 3u) == 0)
-              parent[region + idx] = (p0 + (uint32_t)it * kWave + lane) >> 2;
+      for (int s = 0; s < S; ++s) {
+        uint64_t cnt = 0;
+#pragma unroll
+        for (int it = 0; it < kTileIters; ++it) cnt += popc64(keep[it][s]) >> 2;
+        const uint32_t pair = G.pair[s];
+        uint64_t base = lookback(status + (int64_t)pair * a.tiles, tile, cnt, err);
+        if (tile + 1 == a.tiles && lane == 0) pair_count[pair] = (int64_t)(base + cnt);
+        const int64_t region = (int64_t)pair * a.cap;
+#pragma unroll
+        for (int it = 0; it < kTileIters; ++it) {
+          const uint64_t m = keep[it][s];
+          if ((m >> lane) & 1ull) {
+            const int64_t idx = (int64_t)base + (int64_t)(mbcnt64(m) >> 2);
+            if (idx < a.cap) {
+              w4[(region + idx) * 4 + (lane & 3u)] = wbuf[it][s];
+              if ((lane & 3u) == 0)
+                parent[region + idx] = (p0 + (uint32_t)it * kWave + lane) >> 2;
+            }
           }
+          base += popc64(m) >> 2;
         }
-        base += popc64(m) >> 2;
       }
     }
   }
@@ -610,8 +576,9 @@ extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
 
 template <int S, int W, int MODE>
 static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks, hipStream_t s) {
+  constexpr int P = S == 1 ? 4 : (S == 2 ? 2 : 1);
   emr::DiscoverScalars sc{a->cap, a->n_pos, a->tiles, a->n_tiles, a->depth, a->theta};
-  auto kern = emr::k_discover<S, W, MODE>;
+  auto kern = emr::k_discover<S, P, W, MODE>;
   // Cooperative launch: the runtime refuses a grid that cannot be resident all at once, which the
   // look-back's forward progress relies on. Clamp to the occupancy-limited residency.
   int per_cu = 0, dev = 0, cus = 0;

@@ -213,44 +213,53 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       return false;
     }
 
-    // ---- varying program
+    // ---- varying program: step headers, then the node-edge stream
     ProgDesc& d = desc[dir];
     GenomeInfo& inf = info[dir];
     inf = GenomeInfo{};
     d.var_off = (uint32_t)blob.size();
     d.n_steps = (uint32_t)vsteps.size();
     d.flags = (out_varying ? 1u : 0u) | ((uint32_t)window << 8);
-    size_t step_base = blob.size();
+    d.pad[0] = d.pad[1] = d.pad[2] = 0;
+    const size_t step_base = blob.size();
     blob.resize(blob.size() + 4 * vsteps.size(), 0u);
+    d.edge_off = (uint32_t)blob.size();
     for (int t = 0; t < (int)vsteps.size(); ++t) {
-      int v = vsteps[t];
-      std::vector<std::pair<uint32_t, float>> ex, ey, en;
+      const int v = vsteps[t];
+      float ax = 0.0f, ay = 0.0f;
+      bool has_x = false, has_y = false;
+      uint32_t nn = 0;
       for (int ei : in_edges[v]) {
         const Edge& E = edges[ei];
         if (!live[E.src] || !varying[E.src]) continue;  // uniform: folded by the bind kernel
-        int k = g.kind[E.src];
-        if (k == vx_role) ex.push_back({0u, E.w});
-        else if (k == vy_role) ey.push_back({1u, E.w});
-        else en.push_back({(uint32_t)assigned[E.src], E.w});
+        const int k = g.kind[E.src];
+        if (k == vx_role) {
+          ax += E.w;  // parallel edges from x add their weights
+          has_x = true;
+          inf.fma_xy++;
+        } else if (k == vy_role) {
+          ay += E.w;
+          has_y = true;
+          inf.fma_xy++;
+        } else {
+          blob.push_back((uint32_t)assigned[E.src]);
+          blob.push_back(fbits(E.w));
+          nn++;
+          inf.fma_node++;
+        }
       }
-      if (ex.size() > 255 || ey.size() > 255 || en.size() > 65535) {
+      if (nn > kMaxStepEdges) {
         *st = EMR_E_LIMIT;
-        *msg = "too many parallel edges into one node";
+        *msg = "too many edges into one node";
         return false;
       }
+      const uint32_t dst = (out_varying && v == out_node) ? 0u : (uint32_t)assigned[v];
       uint32_t* sw = &blob[step_base + 4 * t];
-      uint32_t dst = (out_varying && v == out_node) ? 0u : (uint32_t)assigned[v];
-      sw[0] = (uint32_t)g.act[v] | (dst << 8);
-      sw[1] = (uint32_t)ex.size() | ((uint32_t)ey.size() << 8) | ((uint32_t)en.size() << 16);
-      sw[2] = (uint32_t)blob.size();
+      sw[0] = (uint32_t)g.act[v] | (dst << kStepDstShift) | (has_x ? kStepHasX : 0u) |
+              (has_y ? kStepHasY : 0u) | (nn << kStepEdgeShift);
+      sw[1] = fbits(ax);
+      sw[2] = fbits(ay);
       sw[3] = 0;
-      for (auto* lst : {&ex, &ey, &en})
-        for (auto& pe : *lst) {
-          blob.push_back(pe.first);
-          blob.push_back(fbits(pe.second));
-        }
-      inf.fma_xy += (int)(ex.size() + ey.size());
-      inf.fma_node += (int)en.size();
       inf.act_count[g.act[v]]++;
     }
     inf.n_steps = (int)vsteps.size();

@@ -198,6 +198,7 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
         cur.desc = di;
         for (int s = n; s < emr::kMaxGroup; ++s) cur.g.pair[s] = cur.g.pair[n - 1];
         cur.g.var_off = d.var_off;
+        cur.g.edge_off = d.edge_off;
         cur.g.n_steps = d.n_steps;
         cur.g.flags = d.flags;
         tmp.push_back(cur);

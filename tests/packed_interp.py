@@ -45,13 +45,13 @@ def pack(genome):
     cap = 1 << 16
     blob = np.zeros(cap, np.uint32)
     words = C.c_int64()
-    desc = np.zeros(8, np.uint32)
+    desc = np.zeros(16, np.uint32)
     info = np.zeros(24, np.int32)
     msg = C.create_string_buffer(256)
     st = shim().shim_pack(C.byref(arr[0]), blob.ctypes.data, cap, C.byref(words),
                           desc.ctypes.data, info.ctypes.data, msg, 256)
     del keep
-    return st, blob[:words.value], desc.reshape(2, 4), info.reshape(2, 12), msg.value.decode()
+    return st, blob[:words.value], desc.reshape(2, 8), info.reshape(2, 12), msg.value.decode()
 
 
 def _act(a, z):
@@ -76,7 +76,7 @@ def f32(u):
 
 def interpret(blob, desc, dir_, sx, sy, px, py):
     """Evaluate packed program `desc[dir_]` for source (sx, sy) at positions (px, py) (arrays)."""
-    var_off, n_steps, uni_off, flags = (int(v) for v in desc[dir_])
+    var_off, edge_off, n_steps, uni_off, flags = (int(v) for v in desc[dir_][:5])
     # uniform program
     U = np.zeros(5 + 300)
     if dir_ == 0:
@@ -102,29 +102,27 @@ def interpret(blob, desc, dir_, sx, sy, px, py):
             z += f32(blob[fo + 2 * e + 1]) * U[int(blob[fo + 2 * e])]
         folded.append(z)
     if not (flags & 1):
+        assert n_steps == 0
         return np.full(len(px), U[out_u]), (flags >> 8) & 0xFF
     window = (flags >> 8) & 0xFF
     vals = np.full((max(window, 1), len(px)), np.nan)
     acc = None
+    ep = edge_off
     for t in range(n_steps):
-        m0, m1, eo = (int(v) for v in blob[var_off + 4 * t: var_off + 4 * t + 3])
-        act, dst = m0 & 0xFF, (m0 >> 8) & 0xFF
-        nx, ny, nn = m1 & 0xFF, (m1 >> 8) & 0xFF, m1 >> 16
-        acc = np.full(len(px), folded[t])
-        for e in range(nx):
-            assert int(blob[eo + 2 * e]) == 0
-            acc = acc + f32(blob[eo + 2 * e + 1]) * px
-        eo += 2 * nx
-        for e in range(ny):
-            assert int(blob[eo + 2 * e]) == 1
-            acc = acc + f32(blob[eo + 2 * e + 1]) * py
-        eo += 2 * ny
+        w0 = int(blob[var_off + 4 * t])
+        ax, ay = f32(blob[var_off + 4 * t + 1]), f32(blob[var_off + 4 * t + 2])
+        act, dst = w0 & 7, (w0 >> 8) & 0xFF
+        has_x, has_y, nn = (w0 >> 16) & 1, (w0 >> 17) & 1, w0 >> 20
+        assert has_x or ax == 0.0
+        assert has_y or ay == 0.0
+        acc = folded[t] + ax * px + ay * py
         for e in range(nn):
-            src = int(blob[eo + 2 * e])
+            src = int(blob[ep + 2 * e])
             assert src < window
             v = vals[src]
             assert not np.isnan(v).any(), "read of a slot that holds no live value"
-            acc = acc + f32(blob[eo + 2 * e + 1]) * v
+            acc = acc + f32(blob[ep + 2 * e + 1]) * v
+        ep += 2 * nn
         acc = _act(act, acc)
         if t + 1 < n_steps:
             assert dst < window
