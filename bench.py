@@ -8,8 +8,9 @@ Printed as one JSON line:
 
   value        CPPN queries per second over the timed steps (host clock, synchronized)
   roofline     the dominant discover-kernel launch: algorithmic VALU lane-slots (cost model of
-               emr_discover_cost) / its HIP-event duration, against the chip's fp32 VALU issue
-               rate without packed math: 256 CUs x 4 SIMD x 16 lanes x 2.4 GHz = 39.32 T slots/s
+               emr_discover_cost: one slot per fp32 FMA / add / mul, transcendentals weighted by
+               their measured 1/4 rate) / its HIP-event duration, against the chip's fp32 vector
+               peak: 157.3 TFLOP/s = 78.64 T lane-slots/s (an FMA is one slot, two flops)
   ms_per_gen   pack (host + upload) + discover + check, host clock: the per-generation cost of
                discovery in an evolution loop
   cpu_baseline the CPU oracle on a bounded, stated sample of the same workload
@@ -28,7 +29,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-VALU_PEAK_SLOTS = 256 * 4 * 16 * 2.4e9  # lane-slots per second
+VALU_PEAK_SLOTS = 157.3e12 / 2.0  # lane-slots per second (fp32 vector peak, FMA = 2 flops)
 METRIC = "CPPN queries/sec incl. variance filter (% VALU peak); ms/gen pop1000 depth7"
 
 

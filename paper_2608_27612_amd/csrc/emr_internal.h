@@ -65,7 +65,9 @@ struct ProgDesc {
   uint32_t n_steps;   // varying steps
   uint32_t uni_off;   // word offset of the uniform program
   uint32_t flags;     // bit 0: output varies with position; bits 8..15: register window needed
-  uint32_t pad[3];
+  uint32_t edge_end;  // word offset one past the node-edge stream
+  uint32_t uni_end;   // word offset one past the uniform program and its edges
+  uint32_t pad;
 };
 
 // One unit of kernel work: up to kMaxGroup sources of one genome sharing a direction.
@@ -75,9 +77,15 @@ struct Group {
   uint32_t n_steps;
   uint32_t flags;      // copied from ProgDesc
   uint32_t bias_off;   // float offset into the bias table: [step][source], then out constants
-  uint32_t pad[3];
+  uint32_t edge_end;   // word offset one past the program's node-edge stream
+  uint32_t pad[2];
   uint32_t pair[kMaxGroup];  // global pair ids of the sources (unused entries repeat the last)
 };
+
+// Device error flags (first word of a workspace).
+constexpr uint32_t kErrLookback = 1u;  // a look-back wait hit its bound
+constexpr uint32_t kErrTable = 2u;     // a table entry pointed outside its table (entry skipped)
+constexpr uint32_t kMaxSteps = 256;
 
 // One (genome, direction, source) evaluated by the bind kernel.
 struct Member {
@@ -125,6 +133,9 @@ struct DiscoverArgs {
   int32_t depth;
   float theta;
   uint32_t group_size;     // members per group (S) for this launch
+  uint32_t blob_words;     // size of the population table
+  uint32_t n_pairs;        // pairs of the call (bound for pair ids)
+  uint64_t bias_floats;    // size of the bias table
 };
 
 struct BindArgs {
@@ -133,7 +144,12 @@ struct BindArgs {
   const Member* members;
   const float* src_xy;     // [n_sources * 2]
   float* bias_tab;
+  uint32_t* err;
   uint32_t n_members;
+  uint32_t n_desc;         // entries of desc
+  uint32_t n_sources;
+  uint32_t blob_words;
+  uint64_t bias_floats;
 };
 
 }  // namespace emr

@@ -35,10 +35,9 @@ __device__ __forceinline__ float act_sigmoid(float z) {
   return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-kLog2e * z));
 }
 __device__ __forceinline__ float act_tanh(float z) {
-  // tanh|z| = (1 - e^{-2|z|}) / (1 + e^{-2|z|}); absolute error ~2 ulp(1) near 0.
-  float t = __builtin_amdgcn_exp2f(-2.0f * kLog2e * __builtin_fabsf(z));
-  float r = (1.0f - t) * __builtin_amdgcn_rcpf(1.0f + t);
-  return __builtin_copysignf(r, z);
+  // tanh z = 2 / (1 + e^{-2z}) - 1; absolute error ~2 ulp(1) near 0, exact +-1 in the tails.
+  return __builtin_fmaf(2.0f, __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-2.0f * kLog2e * z)),
+                        -1.0f);
 }
 __device__ __forceinline__ float act_gauss(float z) {
   return __builtin_amdgcn_exp2f(-kLog2e * (z * z));
@@ -82,10 +81,20 @@ __device__ __forceinline__ int level_of(uint32_t p) {
 __device__ __forceinline__ uint32_t lane_id() {
   return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
 }
-// Sum over the 4 lanes of a quad, pairwise: (w0+w1)+(w2+w3), bit-identical in all 4 lanes.
+// Sum over the 4 lanes of a quad, pairwise: (w0+w1)+(w2+w3). Each lane adds its neighbour's value
+// to its own (IEEE addition commutes), so the result is bit-identical in all 4 lanes.
 __device__ __forceinline__ float quad_sum(float v) {
-  float t = v + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));
-  return t + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(t), 0x4E, 0xF, 0xF, false));
+  float t = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, true)) + v;
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(t), 0x4E, 0xF, 0xF, true)) + t;
+}
+// Population variance of the quad's four values, identical in its four lanes. Contraction is off:
+// a fused d*d + neighbour would round differently in different lanes.
+__device__ __forceinline__ float quad_variance(float w) {
+#pragma clang fp contract(off)
+  const float s1 = quad_sum(w);
+  const float d = __builtin_fmaf(-0.25f, s1, w);  // w - mean; 0.25 * s1 (the mean) is exact
+  const float s2 = quad_sum(d * d);
+  return s2 * 0.25f;
 }
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
 __device__ __forceinline__ uint32_t popc64(uint64_t m) { return __builtin_popcountll(m); }
@@ -114,7 +123,6 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 // tile always belongs to a running wave whose earlier tiles are done: waits always end. Each wait
 // is also bounded and, if the bound were ever hit, raises an error flag instead of spinning on.
 constexpr uint32_t kSpinLimit = 1u << 22;
-constexpr uint32_t kErrLookback = 1u;
 
 __device__ __forceinline__ void status_store(uint64_t* p, uint64_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -167,6 +175,8 @@ struct DiscoverScalars {
   uint32_t tiles, n_tiles;
   int32_t depth;
   float theta;
+  uint32_t blob_words, n_pairs;
+  uint64_t bias_floats;
 };
 
 // Output modes: raw CPPN outputs; records at fixed per-tile slots (pair_capacity >= Q(D), compacted
@@ -187,7 +197,8 @@ __device__ __forceinline__ Group load_group(cu32* p) {
   g.n_steps = p[2];
   g.flags = p[3];
   g.bias_off = p[4];
-  g.pad[0] = g.pad[1] = g.pad[2] = 0;
+  g.edge_end = p[5];
+  g.pad[0] = g.pad[1] = 0;
 #pragma unroll
   for (int k = 0; k < kMaxGroup; ++k) g.pair[k] = p[8 + k];
   return g;
@@ -236,6 +247,20 @@ __global__ void __launch_bounds__(256)
     const uint32_t gi = t / a.tiles;
     const uint32_t tile = t - gi * a.tiles;
     const Group G = load_group(cgroups + 12 * gi);
+    // Every table-derived offset, count and id is checked before use: an entry that points outside
+    // its table raises an error flag and the tile is skipped instead of reading or writing wild.
+    {
+      bool ok = G.n_steps <= kMaxSteps &&
+                (uint64_t)G.var_off + 4ull * G.n_steps <= a.blob_words &&
+                G.edge_off <= G.edge_end && G.edge_end + 8ull <= a.blob_words &&
+                (uint64_t)G.bias_off + (uint64_t)(G.n_steps + 1) * S <= a.bias_floats;
+#pragma unroll
+      for (int s = 0; s < S; ++s) ok = ok && G.pair[s] < a.n_pairs;
+      if (!ok) {
+        if (lane == 0) atomicOr(err, kErrTable);
+        continue;
+      }
+    }
     const bool out_varying = (G.flags & 1u) != 0;
     cu32* hdr = cblob + G.var_off;
     cf32* bt = cbias + G.bias_off;
@@ -273,6 +298,7 @@ __global__ void __launch_bounds__(256)
       // ---- positions of this pass (Eq. 1 cell centres, decoded from the grid index)
       float px[P], py[P];
       bool valid[P];
+      uint64_t vmask[P];  // lanes holding a position of the tile (all but the head tile's tail)
       uint32_t pidx[P];
 #pragma unroll
       for (int j = 0; j < P; ++j) {
@@ -280,6 +306,10 @@ __global__ void __launch_bounds__(256)
         const uint32_t p = p0 + it * kWave + lane;
         pidx[j] = p;
         valid[j] = it * kWave + lane < n_valid;
+        const uint32_t first = it * kWave;  // uniform: lanes [0, n_valid - first) are valid
+        vmask[j] = first >= n_valid ? 0ull
+                   : (n_valid - first >= (uint32_t)kWave ? ~0ull
+                                                         : ((1ull << (n_valid - first)) - 1ull));
         if (!head) {
           const uint32_t m_hi = (m0 >> 6) + it;
           const float scale = pow2_neg(lvl);
@@ -298,7 +328,7 @@ __global__ void __launch_bounds__(256)
 
       // ---- CPPN (Section 2): the varying program in topological order, M instances at once.
       float acc[M];
-      cu32* ep = cblob + G.edge_off;
+      uint32_t e_off = G.edge_off;  // word offset of the next node edge; stays <= G.edge_end
       cu32* hp = hdr;
       cf32* bs = bt;
       for (uint32_t st = 0; st < G.n_steps; ++st, hp += 4, bs += S) {
@@ -318,28 +348,31 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
           for (int m = 0; m < M; ++m) acc[m] = lin[m % P] + bs[m / P];
         }
-        uint32_t nn = h.x >> kStepEdgeShift;
+        // node edges: at most what is left of the program's edge stream; slot indices are taken
+        // modulo the window, so an index can never leave the instance's register tuple
+        constexpr uint32_t wm = W - 1;
+        uint32_t nn = min(h.x >> kStepEdgeShift, (G.edge_end - e_off) >> 1);
         while (nn >= 4) {
-          const Words4 e0 = load4(ep);
-          const Words4 e1 = load4(ep + 4);
-          R.fma4(acc, e0.x, __uint_as_float(e0.y), e0.z, __uint_as_float(e0.w), e1.x,
-                 __uint_as_float(e1.y), e1.z, __uint_as_float(e1.w));
-          ep += 8;
+          const Words4 e0 = load4(cblob + e_off);
+          const Words4 e1 = load4(cblob + e_off + 4);
+          R.fma4(acc, e0.x & wm, __uint_as_float(e0.y), e0.z & wm, __uint_as_float(e0.w),
+                 e1.x & wm, __uint_as_float(e1.y), e1.z & wm, __uint_as_float(e1.w));
+          e_off += 8;
           nn -= 4;
         }
         if (nn != 0) {
-          // may read past the program's last edge; the population table is padded for it
-          const Words4 e0 = load4(ep);
-          const Words4 e1 = load4(ep + 4);
+          // may read up to 6 words past the program's last edge; the table is padded for it
+          const Words4 e0 = load4(cblob + e_off);
+          const Words4 e1 = load4(cblob + e_off + 4);
           if (nn == 1) {
-            R.fma1(acc, e0.x, __uint_as_float(e0.y));
+            R.fma1(acc, e0.x & wm, __uint_as_float(e0.y));
           } else if (nn == 2) {
-            R.fma2(acc, e0.x, __uint_as_float(e0.y), e0.z, __uint_as_float(e0.w));
+            R.fma2(acc, e0.x & wm, __uint_as_float(e0.y), e0.z & wm, __uint_as_float(e0.w));
           } else {
-            R.fma3(acc, e0.x, __uint_as_float(e0.y), e0.z, __uint_as_float(e0.w), e1.x,
-                   __uint_as_float(e1.y));
+            R.fma3(acc, e0.x & wm, __uint_as_float(e0.y), e0.z & wm, __uint_as_float(e0.w),
+                   e1.x & wm, __uint_as_float(e1.y));
           }
-          ep += 2 * nn;
+          e_off += 2 * nn;
         }
         switch (h.x & kStepActMask) {
           case EMR_ACT_SIGMOID:
@@ -365,7 +398,7 @@ __global__ void __launch_bounds__(256)
           default:
             break;
         }
-        if (st + 1 < G.n_steps) R.st_mov((h.x >> kStepDstShift) & 0xFFu, acc);
+        if (st + 1 < G.n_steps) R.st_mov((h.x >> kStepDstShift) & wm, acc);
       }
       float w[M];
       cf32* bo = bt + G.n_steps * S;  // output constants when the output is uniform
@@ -382,11 +415,7 @@ __global__ void __launch_bounds__(256)
             if (valid[j]) raw[(int64_t)G.pair[s] * a.n_pos + pidx[j]] = w[m];
             continue;
           }
-          const float s1 = quad_sum(w[m]);
-          const float d = __builtin_fmaf(-0.25f, s1, w[m]);  // w - mean, mean = s1/4 exactly
-          const float s2 = quad_sum(__fmul_rn(d, d));
-          const float var = s2 * 0.25f;
-          const uint64_t kb = ballot(valid[j] && (var > a.theta));
+          const uint64_t kb = ballot(quad_variance(w[m]) > a.theta) & vmask[j];
           if constexpr (MODE == kModeLookback) {
             keep[pass * P + j][s] = kb;
             wbuf[pass * P + j][s] = w[m];
@@ -447,12 +476,29 @@ constexpr int kMaxU = 5 + 256;
 __global__ void __launch_bounds__(64)
     k_bind(const uint32_t* __restrict__ blob, const ProgDesc* __restrict__ desc,
            const Member* __restrict__ members, const float* __restrict__ src_xy,
-           float* __restrict__ bias_tab, uint32_t n_members) {
+           float* __restrict__ bias_tab, uint32_t* __restrict__ err, uint32_t n_members,
+           uint32_t n_desc, uint32_t n_sources, uint32_t blob_words, uint64_t bias_floats) {
   const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n_members) return;
   const Member m = members[i];
-  const ProgDesc d = desc[m.desc];
+  bool ok = m.desc < n_desc && m.source < n_sources;
+  const ProgDesc d = desc[ok ? m.desc : 0];
   const uint32_t* u = blob + d.uni_off;
+  uint32_t n_un = 0, out_u = kNone, n_steps = 0;
+  ok = ok && d.uni_off + 4ull <= d.uni_end && d.uni_end <= blob_words;
+  if (ok) {
+    n_un = u[0];
+    out_u = u[1];
+    n_steps = u[2];
+    ok = n_un <= kMaxU - 5 && n_steps <= kMaxSteps &&
+         (uint64_t)d.uni_off + 4ull + 4ull * (n_un + n_steps) <= d.uni_end &&
+         (out_u == kNone || out_u < 5 + n_un) &&
+         (uint64_t)m.bias_base + (uint64_t)n_steps * m.stride < bias_floats;
+  }
+  if (!ok) {
+    atomicOr(err, kErrTable);
+    return;
+  }
   const uint32_t dir = m.desc & 1u;
   const float sx = src_xy[2 * m.source], sy = src_xy[2 * m.source + 1];
   float U[kMaxU];
@@ -463,21 +509,34 @@ __global__ void __launch_bounds__(64)
   U[2] = dir == 0 ? 0.0f : sx;
   U[3] = dir == 0 ? 0.0f : sy;
   U[4] = 1.0f;
-  const uint32_t n_un = u[0], out_u = u[1], n_steps = u[2];
   const uint32_t* rec = u + 4;
+  // Edge lists must lie inside this program; value indices must name an input or an earlier node.
+  auto edges_ok = [&](uint32_t off, uint32_t cnt) {
+    return (uint64_t)off + 2ull * cnt <= d.uni_end && off >= d.uni_off;
+  };
   for (uint32_t k = 0; k < n_un; ++k) {
     float z = __uint_as_float(rec[4 * k + 3]);
-    const uint32_t* ep = blob + rec[4 * k + 2];
-    for (uint32_t e = 0; e < rec[4 * k + 1]; ++e)
-      z = __builtin_fmaf(__uint_as_float(ep[2 * e + 1]), U[ep[2 * e]], z);
+    const uint32_t cnt = rec[4 * k + 1], off = rec[4 * k + 2];
+    if (!edges_ok(off, cnt)) {
+      atomicOr(err, kErrTable);
+      return;
+    }
+    const uint32_t* ep = blob + off;
+    for (uint32_t e = 0; e < cnt; ++e)
+      z = __builtin_fmaf(__uint_as_float(ep[2 * e + 1]), U[min(ep[2 * e], 4u + k)], z);
     U[5 + k] = act_apply(rec[4 * k], z);
   }
   const uint32_t* fold = rec + 4 * n_un;
   for (uint32_t t = 0; t < n_steps; ++t) {
     float z = __uint_as_float(fold[4 * t + 2]);
-    const uint32_t* ep = blob + fold[4 * t + 1];
-    for (uint32_t e = 0; e < fold[4 * t]; ++e)
-      z = __builtin_fmaf(__uint_as_float(ep[2 * e + 1]), U[ep[2 * e]], z);
+    const uint32_t cnt = fold[4 * t], off = fold[4 * t + 1];
+    if (!edges_ok(off, cnt)) {
+      atomicOr(err, kErrTable);
+      return;
+    }
+    const uint32_t* ep = blob + off;
+    for (uint32_t e = 0; e < cnt; ++e)
+      z = __builtin_fmaf(__uint_as_float(ep[2 * e + 1]), U[min(ep[2 * e], 4u + n_un)], z);
     bias_tab[m.bias_base + t * m.stride] = z;
   }
   bias_tab[m.bias_base + n_steps * m.stride] = out_u == kNone ? 0.0f : U[out_u];
@@ -491,7 +550,7 @@ __global__ void __launch_bounds__(64)
 __global__ void __launch_bounds__(256)
     k_compact(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
               float* __restrict__ w4, int64_t* __restrict__ pair_count, int64_t cap,
-              uint32_t tiles, uint32_t n_pairs) {
+              uint32_t tiles, uint32_t n_pairs, uint32_t head_slots) {
   const uint32_t lane = lane_id();
   const uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +
                                                        threadIdx.x / kWave);
@@ -500,7 +559,10 @@ __global__ void __launch_bounds__(256)
   const int64_t region = (int64_t)pair * cap;
   uint32_t running = 0;
   for (uint32_t t0 = 0; t0 < tiles; t0 += kWave) {
-    const uint32_t c = t0 + lane < tiles ? (uint32_t)row[t0 + lane] : 0u;
+    // a tile holds at most its own slot count (64, or the head tile's parents)
+    const uint32_t t_lane = t0 + lane;
+    const uint32_t slots = t_lane == 0 ? head_slots : (uint32_t)(kTile / 4);
+    const uint32_t c = t_lane < tiles ? min((uint32_t)row[t_lane], slots) : 0u;
     uint32_t incl = c;  // inclusive scan over the wave
     for (int off = 1; off < kWave; off <<= 1) {
       const uint32_t v = __shfl_up(incl, off, kWave);
@@ -570,17 +632,20 @@ extern "C" hipError_t emr_launch_grid(float* xy, int64_t n, hipStream_t s) {
 extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
   if (a->n_members == 0) return hipSuccess;
   hipLaunchKernelGGL(emr::k_bind, dim3((a->n_members + 63) / 64), dim3(64), 0, s, a->blob, a->desc,
-                     a->members, a->src_xy, a->bias_tab, a->n_members);
+                     a->members, a->src_xy, a->bias_tab, a->err, a->n_members, a->n_desc,
+                     a->n_sources, a->blob_words, a->bias_floats);
   return hipGetLastError();
 }
 
 template <int S, int W, int MODE>
 static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks, hipStream_t s) {
   constexpr int P = S == 1 ? 4 : (S == 2 ? 2 : 1);
-  emr::DiscoverScalars sc{a->cap, a->n_pos, a->tiles, a->n_tiles, a->depth, a->theta};
+  emr::DiscoverScalars sc{a->cap,     a->n_pos,      a->tiles,  a->n_tiles,    a->depth,
+                          a->theta,   a->blob_words, a->n_pairs, a->bias_floats};
   auto kern = emr::k_discover<S, P, W, MODE>;
-  // Cooperative launch: the runtime refuses a grid that cannot be resident all at once, which the
-  // look-back's forward progress relies on. Clamp to the occupancy-limited residency.
+  // Clamp the grid to what can be resident at once: the waves walk their tiles. The look-back mode
+  // is launched cooperatively (the runtime refuses a grid that cannot be resident all at once),
+  // which its forward progress relies on; the other modes have no dependences between waves.
   int per_cu = 0, dev = 0, cus = 0;
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, 0);
   if (e != hipSuccess) return e;
@@ -598,8 +663,14 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
   float* w4 = a->w4;
   int64_t* pair_count = a->pair_count;
   float* raw = a->raw;
-  void* args[] = {&blob, &groups, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw, &sc};
-  return hipLaunchCooperativeKernel((const void*)kern, dim3(blocks), dim3(256), args, 0, s);
+  if constexpr (MODE == emr::kModeLookback) {
+    void* args[] = {&blob, &groups, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw, &sc};
+    return hipLaunchCooperativeKernel((const void*)kern, dim3(blocks), dim3(256), args, 0, s);
+  } else {
+    hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, s, blob, groups, bias_tab, status, err,
+                       parent, w4, pair_count, raw, sc);
+    return hipGetLastError();
+  }
 }
 
 template <int MODE>
@@ -631,9 +702,9 @@ extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int window
 
 extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
                                          int64_t* pair_count, int64_t cap, uint32_t tiles,
-                                         uint32_t n_pairs, hipStream_t s) {
+                                         uint32_t n_pairs, uint32_t head_slots, hipStream_t s) {
   if (n_pairs == 0) return hipSuccess;
   hipLaunchKernelGGL(emr::k_compact, dim3((n_pairs + 3) / 4), dim3(256), 0, s, counts, parent, w4,
-                     pair_count, cap, tiles, n_pairs);
+                     pair_count, cap, tiles, n_pairs, head_slots);
   return hipGetLastError();
 }

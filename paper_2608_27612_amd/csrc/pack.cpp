@@ -220,7 +220,7 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
     d.var_off = (uint32_t)blob.size();
     d.n_steps = (uint32_t)vsteps.size();
     d.flags = (out_varying ? 1u : 0u) | ((uint32_t)window << 8);
-    d.pad[0] = d.pad[1] = d.pad[2] = 0;
+    d.pad = 0;
     const size_t step_base = blob.size();
     blob.resize(blob.size() + 4 * vsteps.size(), 0u);
     d.edge_off = (uint32_t)blob.size();
@@ -262,6 +262,7 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       sw[3] = 0;
       inf.act_count[g.act[v]]++;
     }
+    d.edge_end = (uint32_t)blob.size();
     inf.n_steps = (int)vsteps.size();
     inf.window = window;
     inf.out_varying = out_varying;
@@ -305,6 +306,7 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       r[2] = fbits(g.bias ? g.bias[v] : 0.0f);
       r[3] = 0;
     }
+    d.uni_end = (uint32_t)blob.size();
     inf.n_unodes = (int)unodes.size();
   }
   (void)role_node;

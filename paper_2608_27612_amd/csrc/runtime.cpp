@@ -21,7 +21,7 @@ extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int window
                                           uint32_t blocks, hipStream_t s);
 extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
                                          int64_t* pair_count, int64_t cap, uint32_t tiles,
-                                         uint32_t n_pairs, hipStream_t s);
+                                         uint32_t n_pairs, uint32_t head_slots, hipStream_t s);
 
 namespace {
 
@@ -201,6 +201,7 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
         cur.g.edge_off = d.edge_off;
         cur.g.n_steps = d.n_steps;
         cur.g.flags = d.flags;
+        cur.g.edge_end = d.edge_end;
         tmp.push_back(cur);
         cur = TmpGroup{};
         n = 0;
@@ -293,7 +294,12 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
   b.members = (const emr::Member*)(ws + P.off_members);
   b.src_xy = (const float*)(ws + P.off_srcxy);
   b.bias_tab = (float*)(ws + P.off_bias);
+  b.err = (uint32_t*)(ws + P.off_err);
   b.n_members = (uint32_t)P.members.size();
+  b.n_desc = (uint32_t)pop->desc.size();
+  b.n_sources = (uint32_t)(P.src_xy.size() / 2);
+  b.blob_words = (uint32_t)pop->blob_words;
+  b.bias_floats = P.bias_floats;
   HIP_OR_FAIL(emr_launch_bind(&b, s));
 
   const int cus = device_cu_count();
@@ -330,6 +336,9 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
     a.depth = P.depth;
     a.theta = theta;
     a.group_size = (uint32_t)bk.S;
+    a.blob_words = (uint32_t)pop->blob_words;
+    a.n_pairs = (uint32_t)P.n_pairs;
+    a.bias_floats = P.bias_floats;
     const uint64_t want = ((uint64_t)a.n_tiles + 3) / 4;
     const uint32_t blocks = (uint32_t)std::min<uint64_t>(want, (uint64_t)cus * 16);
     if (prof.on) HIP_OR_FAIL(hipEventRecord(prof.events[2 * bi], s));
@@ -351,9 +360,12 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
     }
   }
   if (padded && P.n_pairs > 0)
-    HIP_OR_FAIL(emr_launch_compact((const uint64_t*)(ws + P.off_status), out->parent, out->w4,
-                                   out->pair_count, out->pair_capacity, (uint32_t)P.tiles,
-                                   (uint32_t)P.n_pairs, s));
+    HIP_OR_FAIL(emr_launch_compact(
+        (const uint64_t*)(ws + P.off_status), out->parent, out->w4, out->pair_count,
+        out->pair_capacity, (uint32_t)P.tiles, (uint32_t)P.n_pairs,
+        (uint32_t)(P.depth < emr::kFirstAlignedLevel ? emr::n_parents(P.depth)
+                                                     : emr::level_offset(emr::kFirstAlignedLevel) / 4),
+        s));
   return EMR_OK;
 }
 
@@ -418,6 +430,13 @@ emr_status emr_pack_population(const emr_genome* genomes, int32_t n, emr_populat
                                      hipMemcpyHostToDevice) != hipSuccess)) {
     emr_free_population(p);
     return fail(EMR_E_DEVICE, "copy of the packed population failed");
+  }
+  // The tables must be complete on the device before any stream reads them: copies from pageable
+  // host memory may still be in flight when hipMemcpy returns, and the caller's stream is not
+  // necessarily ordered after them.
+  if (hipDeviceSynchronize() != hipSuccess) {
+    emr_free_population(p);
+    return fail(EMR_E_DEVICE, "synchronizing the packed population's upload failed");
   }
   *out = p;
   return EMR_OK;
@@ -489,7 +508,9 @@ emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max
     for (int64_t c : cnt) mx = std::max(mx, c);
   }
   if (max_count) *max_count = mx;
-  if (err) return fail(EMR_E_DEVICE, "kernel reported internal error flags 0x%x", err);
+  if (err)
+    return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (1: look-back wait bound, 2: a "
+                "table entry out of range)", err);
   if (mx > out->pair_capacity)
     return fail(EMR_E_CAPACITY, "a pair found %lld records; pair_capacity is %lld",
                 (long long)mx, (long long)out->pair_capacity);
