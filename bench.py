@@ -33,6 +33,38 @@ VALU_PEAK_SLOTS = 157.3e12 / 2.0  # lane-slots per second (fp32 vector peak, FMA
 METRIC = "CPPN queries/sec incl. variance filter (% VALU peak); ms/gen pop1000 depth7"
 
 
+KERNEL_SOURCES = ["paper_2608_27612_amd/csrc/kernels.hip", "paper_2608_27612_amd/csrc/regwin_gen.h",
+                  "paper_2608_27612_amd/csrc/emr_internal.h"]
+
+
+def kernel_source_sha():
+    """First 16 hex digits of sha256 over `sha256sum` lines of the kernel sources."""
+    import hashlib
+    lines = ""
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            lines += hashlib.sha256(f.read()).hexdigest() + "  " + rel + "\n"
+    return hashlib.sha256(lines.encode()).hexdigest()[:16]
+
+
+def profiled_traffic(kernel, workload):
+    """HBM bytes per launch from the committed counter summary, if it was taken on these kernel
+    sources (else None: the counters no longer describe the kernel)."""
+    import glob
+    import re
+    sha = kernel_source_sha()
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*.md")):
+        for block in re.findall(r"```json\n(.*?)\n```", open(path).read(), flags=re.S):
+            try:
+                d = json.loads(block)
+            except ValueError:
+                continue
+            if (d.get("kernel") == kernel and d.get("workload") == workload
+                    and d.get("source_sha") == sha):
+                return d.get("traffic_bytes_per_launch")
+    return None
+
+
 def cpu_baseline(genomes, sources, depth, theta32, target_s):
     """The oracle, as it stands, on the first n genomes (all sources) sized to ~target_s."""
     import oracle
@@ -60,6 +92,9 @@ def main():
     ap.add_argument("--gens", type=int, default=5, help="generations timed for ms_per_gen")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run one device-to-device copy of this size first (outside the timed "
+                         "region), as a known-size reference for memory counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the discovery path has no cross-GPU step and this "
@@ -70,6 +105,13 @@ def main():
     from paper_2608_27612_amd import emr, workloads as W
 
     torch.cuda.set_device(0)
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     genomes, sources, depth, theta = W.workload(args.workload)
     theta32 = float(np.float32(theta))
     rT = args.transcendental_slots
@@ -103,6 +145,9 @@ def main():
 
     # the dominant discover launch: largest total time
     key = max(launch_ms, key=lambda k: sum(launch_ms[k]))
+    S, W = key
+    P = 4 if S == 1 else (2 if S == 2 else 1)
+    kernel_name = "k_discover<%d, %d, %d, 1>" % (S, P, W)
     avg_ms = float(np.mean(launch_ms[key]))
     achieved = launch_slots[key] / (avg_ms * 1e-3)
     all_ms = sum(float(np.mean(v)) for v in launch_ms.values())
@@ -136,8 +181,9 @@ def main():
         "ms_per_gen": ms_per_gen,
         "valu_frac_all_launches": (slots / (all_ms * 1e-3)) / VALU_PEAK_SLOTS,
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_SLOTS / 1e12,
-                     "unit": "TOP/s", "frac": achieved / VALU_PEAK_SLOTS, "traffic": None,
-                     "kernel": "k_discover<S=%d,W=%d>" % key, "kernel_ms": avg_ms,
+                     "unit": "TOP/s", "frac": achieved / VALU_PEAK_SLOTS,
+                     "traffic": profiled_traffic(kernel_name, args.workload),
+                     "kernel": kernel_name, "kernel_ms": avg_ms,
                      "transcendental_slots": rT},
     }
     if not args.no_cpu_baseline:
