@@ -146,7 +146,7 @@ def main():
     # the dominant discover launch: largest total time
     key = max(launch_ms, key=lambda k: sum(launch_ms[k]))
     S, W = key
-    P = 4 if S == 1 else (2 if S == 2 else 1)
+    P = 4 if S * 4 * W <= 128 else (2 if S * 2 * W <= 128 else 1)  # positions per lane
     kernel_name = "k_discover<%d, %d, %d, 1>" % (S, P, W)
     avg_ms = float(np.mean(launch_ms[key]))
     achieved = launch_slots[key] / (avg_ms * 1e-3)

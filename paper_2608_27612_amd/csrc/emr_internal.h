@@ -25,6 +25,8 @@ constexpr int kWindows[] = {8, 16, 32};
 constexpr int kMaxWindow = 32;
 // Sources evaluated together by one lane (same genome, same direction).
 constexpr int kMaxGroup = 4;
+// Register budget of the value windows: S sources x P positions x W slots <= 128 VGPRs per lane.
+constexpr int kWindowRegs = 128;
 // Positions per wave iteration and iterations per tile.
 constexpr int kWave = 64;
 constexpr int kTileIters = 4;
@@ -32,23 +34,34 @@ constexpr int kTile = kWave * kTileIters;  // 256 = 4^4 positions
 constexpr int kFirstAlignedLevel = 4;     // first level whose size is a multiple of kTile
 
 // ---------------------------------------------------------------- varying program
-// At blob[var_off]: n_steps step headers of 4 words, one per position-dependent node in
-// topological order:
-//   word 0: act (bits 0..2) | dst slot (bits 8..15) | has_x (bit 16) | has_y (bit 17)
-//           | number of node edges (bits 20..31)
-//   word 1: float bits of the summed weights of the node's edges from the position's x
+// At blob[var_off] (a multiple of 16 words): n_rec records of 16 words, in topological order of the
+// position-dependent nodes. A node with e node-to-node edges takes max(1, ceil(e / 11)) records:
+//   word 0: meta   bits 0..3  tail: 0 = more records of this node follow;
+//                             1 + a = the node ends with activation a and its value is stored to
+//                                     the dst slot (a in 0..5, EMR_ACT_*);
+//                             7 + a = the node is the output: activation a, value kept
+//                  bit 4      first record of a node: the accumulator starts at bias + ax x + ay y
+//                  bits 8..12 dst slot
+//                  bits 16..19 number of edges in this record (0..11)
+//   word 1: float bits of the summed weights of the node's edges from the position's x (first
+//           record only, else 0)
 //   word 2: the same for y
-//   word 3: 0
-// At blob[edge_off]: the node edges of all steps, step after step, two words each:
-//   {register slot of the source node, float bits of w}.
-// The step's bias is not stored here: it is the per-source folded bias from the bind kernel.
-// The last step computes the output when the output varies; its dst slot is unused.
-constexpr uint32_t kStepActMask = 7u;
-constexpr uint32_t kStepDstShift = 8;
-constexpr uint32_t kStepHasX = 1u << 16;
-constexpr uint32_t kStepHasY = 1u << 17;
-constexpr uint32_t kStepEdgeShift = 20;
-constexpr uint32_t kMaxStepEdges = (1u << 12) - 1;
+//   word 3: source slots of record positions 0..5, 5 bits each (position k at bit 5k)
+//   word 4: source slots of positions 6..10, 5 bits each
+//   words 5..15: float bits of the edge weights of positions 0..10
+// A record with n edges uses positions 0..n-1 and they are accumulated from position n-1 down
+// to 0, so the packer stores the node's edges in reverse.
+// The node's bias is not stored here: it is the per-source folded bias from the bind kernel.
+// n_rec is even: an odd program is padded with one all-zero record, which does nothing.
+constexpr uint32_t kRecWords = 16;
+constexpr uint32_t kRecEdges = 11;
+constexpr uint32_t kRecTailMask = 15u;
+constexpr uint32_t kRecTailStore = 1u;   // + activation
+constexpr uint32_t kRecTailOutput = 7u;  // + activation
+constexpr uint32_t kRecFirst = 1u << 4;
+constexpr uint32_t kRecDstShift = 8;
+constexpr uint32_t kRecEdgeShift = 16;
+constexpr uint32_t kSlotBits = 5;
 
 // ---------------------------------------------------------------- uniform program
 // At blob[uni_off]:
@@ -60,25 +73,27 @@ constexpr uint32_t kMaxStepEdges = (1u << 12) - 1;
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 
 struct ProgDesc {
-  uint32_t var_off;   // word offset of the step headers
-  uint32_t edge_off;  // word offset of the node-edge stream
-  uint32_t n_steps;   // varying steps
+  uint32_t var_off;   // word offset of the record stream
+  uint32_t n_rec;     // records
+  uint32_t n_steps;   // varying nodes
   uint32_t uni_off;   // word offset of the uniform program
   uint32_t flags;     // bit 0: output varies with position; bits 8..15: register window needed
-  uint32_t edge_end;  // word offset one past the node-edge stream
   uint32_t uni_end;   // word offset one past the uniform program and its edges
-  uint32_t pad;
+  uint32_t pad[2];
 };
 
 // One unit of kernel work: up to kMaxGroup sources of one genome sharing a direction.
+// Its bias rows (4 floats each, one per source slot) start at bias_off, a multiple of 4: row 0 holds
+// the output constants (used when the output is uniform), row 1 + t the folded bias of varying
+// node t. The group owns n_rec + 2 rows, so a walk that advances one row per record, plus the
+// prefetch of the next row, never leaves its own rows.
 struct Group {
   uint32_t var_off;
-  uint32_t edge_off;
+  uint32_t n_rec;
   uint32_t n_steps;
   uint32_t flags;      // copied from ProgDesc
-  uint32_t bias_off;   // float offset into the bias table: [step][source], then out constants
-  uint32_t edge_end;   // word offset one past the program's node-edge stream
-  uint32_t pad[2];
+  uint32_t bias_off;   // float offset into the bias table
+  uint32_t pad[3];
   uint32_t pair[kMaxGroup];  // global pair ids of the sources (unused entries repeat the last)
 };
 
@@ -86,19 +101,26 @@ struct Group {
 constexpr uint32_t kErrLookback = 1u;  // a look-back wait hit its bound
 constexpr uint32_t kErrTable = 2u;     // a table entry pointed outside its table (entry skipped)
 constexpr uint32_t kMaxSteps = 256;
+constexpr uint32_t kMaxRecords = kMaxSteps + 4096 / kRecEdges + 1;
 
 // One (genome, direction, source) evaluated by the bind kernel.
 struct Member {
   uint32_t desc;       // ProgDesc index = 2 * genome + dir
   uint32_t source;     // source index
-  uint32_t bias_base;  // first float written in the bias table
-  uint32_t stride;     // distance between consecutive steps' entries (the group size)
+  uint32_t bias_base;  // its group's bias_off + its slot in the group
+  uint32_t bias_rows;  // rows owned by its group (n_rec + 2)
 };
 
 // Look-back tile status word: flag in bits 62..63, value in bits 0..61.
 constexpr uint64_t kStatusAggregate = 1ull << 62;
 constexpr uint64_t kStatusInclusive = 2ull << 62;
 constexpr uint64_t kStatusValueMask = (1ull << 62) - 1;
+
+// Positions per lane per program walk for S sources and window W: the largest of 4, 2, 1 whose
+// value windows fit the register budget.
+EMR_HD constexpr int positions_per_lane(int S, int W) {
+  return S * 4 * W <= kWindowRegs ? 4 : (S * 2 * W <= kWindowRegs ? 2 : 1);
+}
 
 // Level helpers shared by host and device.
 EMR_HD inline int64_t level_offset(int level) {  // first grid index of level >= 1

@@ -1,104 +1,200 @@
 #!/usr/bin/env python3
-"""Generates regwin_gen.h: the register-window inline-assembly helpers of the discover kernel.
+"""Generates regwin_gen.h: the program-record step of the discover kernel, as inline assembly.
 
-A lane evaluates M CPPN instances at once (M = sources x positions, 3 or 4). Instance m keeps its
-position-dependent node values in a VGPR tuple pinned at v[32 + m*W .. 32 + m*W + W - 1]. With
-s_set_gpr_idx_on / s_set_gpr_idx_idx one uniform slot index serves the M fused multiply-adds of an
-edge, and a node's activation writes its last instruction straight into the indexed slot.
-Inline assembly needs literal register names, so every (M, W) variant is spelled out here.
+A lane evaluates M = S * P CPPN instances at once (S sources of one genome at P grid positions).
+Instance m = s * P + j keeps
+  - its accumulator in v[ACC + m], and
+  - its position-dependent node values in a VGPR tuple v[base(m) .. base(m) + W - 1].
+Walker<S, P, W>::step() processes one 16-word program record (layout in emr_internal.h) for all M
+instances in ONE asm statement, so the accumulators and tuples are bound to their registers at a
+single site inside the program loop and the compiler never needs to move them:
 
+  1. first record of a node: acc = bias_s + ax x_j + ay y_j
+  2. the record's n edges: a computed jump into 11 fixed-size blocks (entered at block 11 - n);
+     each block extracts one slot index (s_bfe_u32 of log2(W) bits, which also confines it to the
+     instance's own tuple), sets it as the source-operand index (s_set_gpr_idx_idx) and issues the
+     M fused multiply-adds acc_m += w * tuple_m[slot]. The packer stores a node's edges in reverse
+     record positions, so they are accumulated in edge-list order.
+  3. the tail, through a branch table on meta bits 0..3: the node's activation, whose last
+     instruction writes straight into the destination slot of every tuple (DST indexing), or
+     nothing (a continuation record, or the output node, whose activation is applied by the
+     caller).
+
+The statement declares SCC and M0 as clobbered: its scalar arithmetic writes SCC, and the
+register-indexing instructions write M0.
+
+Hazards: the statement is opaque to the compiler's hazard recognizer, so it keeps the one that
+applies here itself: a non-transcendental VALU instruction that reads the result of a
+transcendental one (v_exp, v_rcp, v_sin) needs one wait state in between; every such pair below
+is at least M >= 3 instructions apart. Branch targets are computed from label differences, so the
+jump arithmetic follows the assembler's actual encodings.
+
+Inline assembly needs literal register names, so every variant is spelled out here.
 Run from this directory: python gen_regwin.py > regwin_gen.h
 """
 
-WINDOWS = (8, 16, 32)
-INSTANCES = (3, 4)
-BASE = 32
+ACC = 4
+PC = 36  # SGPR pair s[PC:PC+1] for the computed jumps (bound as an early-clobber output)
+MAX_EDGES = 11
+SLOT_BITS = 5
+# (S, P, W) variants; M * W <= 128 VGPRs of value tuples.
+VARIANTS = [(S, P, W) for W in (8, 16, 32) for S in (1, 2, 3, 4)
+            for P in [4 if S * 4 * W <= 128 else (2 if S * 2 * W <= 128 else 1)]]
+
+NEG_LOG2E = "0xbfb8aa3b"       # -log2(e) as float bits
+NEG_2LOG2E = "0xc038aa3b"      # -2 log2(e)
+INV_2PI = "0.15915494"         # 1/(2 pi): an inline constant of the ISA
 
 
-def tuple_range(m, w):
-    lo = BASE + m * w
-    return lo, lo + w - 1
+def base(M, m, W):
+    first = ACC + M
+    first += first & 1  # tuples start on an even register
+    return first + m * W
 
 
-def operands_pinned(M, W, inout):
-    out = []
-    for m in range(M):
-        lo, hi = tuple_range(m, W)
-        out.append('"%s{v[%d:%d]}"(v%d)' % ("+" if inout else "", lo, hi, m))
-    return out
+def log2(w):
+    return {8: 3, 16: 4, 32: 5}[w]
 
 
-def gen_fma(M, W, k):
-    args = ", ".join("uint32_t s%d, float w%d" % (e, e) for e in range(k))
-    lines = []
-    for e in range(k):
-        if e == 0:
-            lines.append('"s_set_gpr_idx_on %[s0], gpr_idx(SRC0)\\n\\t"')
-        else:
-            lines.append('"s_set_gpr_idx_idx %%[s%d]\\n\\t"' % e)
-        for m in range(M):
-            lo, _ = tuple_range(m, W)
-            lines.append('"v_fma_f32 %%[a%d], v%d, %%[w%d], %%[a%d]\\n\\t"' % (m, lo, e, m))
-    lines.append('"s_set_gpr_idx_off"')
-    outs = ", ".join('[a%d] "+v"(a[%d])' % (m, m) for m in range(M))
-    ins = ", ".join(['[s%d] "s"(s%d), [w%d] "s"(w%d)' % (e, e, e, e) for e in range(k)]
-                    + operands_pinned(M, W, False))
-    body = "\n                 ".join(lines)
-    return ("  __device__ __forceinline__ void fma%d(float* a, %s) {\n"
-            "    asm volatile(%s\n                 : %s\n                 : %s);\n  }\n"
-            % (k, args, body, outs, ins))
+def bfe_imm(offset, width):
+    return "0x%x" % (offset | (width << 16))
 
 
-def gen_store(M, W, name, fmt, extra_in=None):
-    """fmt: instruction with {d} (indexed destination base) and {x} (this instance's operand)."""
-    lines = ['"s_set_gpr_idx_on %[d], gpr_idx(DST)\\n\\t"']
-    for m in range(M):
-        lo, _ = tuple_range(m, W)
-        lines.append('"%s\\n\\t"' % fmt.format(d="v%d" % lo, x="%%[x%d]" % m, z="%%[z%d]" % m))
-    lines.append('"s_set_gpr_idx_off"')
-    outs = ", ".join(operands_pinned(M, W, True))
-    ins = ['[d] "s"(d)'] + ['[x%d] "v"(x[%d])' % (m, m) for m in range(M)]
-    sig = "uint32_t d, const float* x"
-    if extra_in == "bfi":
-        ins.append('[mask] "s"(0x7fffffffu)')
-        ins += ['[z%d] "v"(z[%d])' % (m, m) for m in range(M)]
-        sig += ", const float* z"
-    body = "\n                 ".join(lines)
-    return ("  __device__ __forceinline__ void %s(%s) {\n"
-            "    asm volatile(%s\n                 : %s\n                 : %s);\n  }\n"
-            % (name, sig, body, outs, ", ".join(ins)))
+def gen_walker(S, P, W):
+    M = S * P
+    A = ["v%d" % (ACC + m) for m in range(M)]
+    T = ["v%d" % base(M, m, W) for m in range(M)]
+    L = []
+    # ---- 1. first record of a node: the accumulator starts at bias + ax x + ay y
+    L += ["s_bitcmp1_b32 %[meta], 4", "s_cbranch_scc0 .Lni_%="]
+    if S == 1:
+        L.append("v_mov_b32 %[tb], %[b0]")
+        L += ["v_fma_f32 %s, %%[x%d], %%[ax], %%[tb]" % (A[j], j) for j in range(P)]
+        L += ["v_fma_f32 %s, %%[y%d], %%[ay], %s" % (A[j], j, A[j]) for j in range(P)]
+    else:
+        L += ["v_mul_f32 %%[l%d], %%[ax], %%[x%d]" % (j, j) for j in range(P)]
+        L += ["v_fma_f32 %%[l%d], %%[y%d], %%[ay], %%[l%d]" % (j, j, j) for j in range(P)]
+        L += ["v_add_f32 %s, %%[b%d], %%[l%d]" % (A[s * P + j], s, j)
+              for s in range(S) for j in range(P)]
+    L.append(".Lni_%=:")
+    # ---- 2. edges: jump to block 11 - n; block i handles record position 10 - i
+    L += ["s_bfe_u32 %[t], %[meta], 0x40010",
+          "s_min_u32 %%[t], %%[t], %d" % MAX_EDGES,  # a 4-bit count above 11 is clamped
+          "s_mul_i32 %[t], %[t], (.Le1_%= - .Le0_%=)",
+          "s_sub_u32 %[t], (.Lee_%= - .Lep_%=), %[t]",
+          "s_set_gpr_idx_on %[t], gpr_idx(SRC0)",
+          "s_getpc_b64 s[%d:%d]" % (PC, PC + 1),
+          ".Lep_%=:",
+          "s_add_u32 s%d, s%d, %%[t]" % (PC, PC),
+          "s_addc_u32 s%d, s%d, 0" % (PC + 1, PC + 1),
+          "s_setpc_b64 s[%d:%d]" % (PC, PC + 1)]
+    for i in range(MAX_EDGES):
+        p = MAX_EDGES - 1 - i
+        L.append(".Le%d_%%=:" % i)
+        L.append("s_bfe_u32 %%[t], %%[sw%d], %s" % (p // 6, bfe_imm(SLOT_BITS * (p % 6), log2(W))))
+        L.append("s_set_gpr_idx_idx %[t]")
+        L += ["v_fma_f32 %s, %s, %%[w%d], %s" % (A[m], T[m], p, A[m]) for m in range(M)]
+    L += [".Lee_%=:", "s_set_gpr_idx_off"]
+    # ---- 3. tail: branch table on meta & 15
+    L += ["s_and_b32 %[t], %[meta], 15",
+          "s_lshl_b32 %[t], %[t], 2",
+          "s_add_u32 %[t], %[t], (.Lt0_%= - .Ltp_%=)",
+          "s_bfe_u32 %%[u], %%[meta], %s" % bfe_imm(8, log2(W)),
+          "s_getpc_b64 s[%d:%d]" % (PC, PC + 1),
+          ".Ltp_%=:",
+          "s_add_u32 s%d, s%d, %%[t]" % (PC, PC),
+          "s_addc_u32 s%d, s%d, 0" % (PC + 1, PC + 1),
+          "s_setpc_b64 s[%d:%d]" % (PC, PC + 1),
+          ".Lt0_%=:"]
+    targets = ["x", "lin", "sig", "tanh", "gau", "sin", "abs"] + ["x"] * 9
+    L += ["s_branch .L%s_%%=" % t for t in targets]
 
+    def dst_block(label, pre, final):
+        out = [".L%s_%%=:" % label]
+        for step in pre:
+            out += [step.format(a=A[m]) for m in range(M)]
+        out.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
+        out += [final.format(a=A[m], d=T[m]) for m in range(M)]
+        out.append("s_branch .Lxo_%=")
+        return out
 
-def gen_struct(M, W):
+    L += dst_block("lin", [], "v_mov_b32 {d}, {a}")
+    L += dst_block("abs", [], "v_and_b32 {d}, 0x7fffffff, {a}")
+    L += dst_block("sig", ["v_mul_f32 {a}, %s, {a}" % NEG_LOG2E, "v_exp_f32 {a}, {a}",
+                           "v_add_f32 {a}, 1.0, {a}"], "v_rcp_f32 {d}, {a}")
+    L += dst_block("tanh", ["v_mul_f32 {a}, %s, {a}" % NEG_2LOG2E, "v_exp_f32 {a}, {a}",
+                            "v_add_f32 {a}, 1.0, {a}", "v_rcp_f32 {a}, {a}"],
+                   "v_fma_f32 {d}, {a}, 2.0, -1.0")
+    L += dst_block("gau", ["v_mul_f32 {a}, {a}, {a}", "v_mul_f32 {a}, %s, {a}" % NEG_LOG2E],
+                   "v_exp_f32 {d}, {a}")
+    # sine: k = rint(z / 2pi) in the destination slot, z - k 2pi with a two-part 2pi (Cody-Waite)
+    # in the accumulator, then the hardware sine of the reduced argument in revolutions
+    L.append(".Lsin_%=:")
+    L.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
+    L += ["v_mul_f32 %s, %s, %s" % (T[m], INV_2PI, A[m]) for m in range(M)]
+    L.append("s_set_gpr_idx_mode gpr_idx(SRC0,DST)")
+    L += ["v_rndne_f32 %s, %s" % (T[m], T[m]) for m in range(M)]
+    L.append("s_set_gpr_idx_mode gpr_idx(SRC0)")
+    L += ["v_fma_f32 %s, -%s, %%[hi], %s" % (A[m], T[m], A[m]) for m in range(M)]
+    L += ["v_fma_f32 %s, -%s, %%[lo], %s" % (A[m], T[m], A[m]) for m in range(M)]
+    L.append("s_set_gpr_idx_off")
+    L += ["v_mul_f32 %s, %s, %s" % (A[m], INV_2PI, A[m]) for m in range(M)]
+    L.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
+    L += ["v_sin_f32 %s, %s" % (T[m], A[m]) for m in range(M)]
+    L += [".Lxo_%=:", "s_set_gpr_idx_off", ".Lx_%=:"]
+
+    outs = ['[pc] "=&{s[%d:%d]}"(pc)' % (PC, PC + 1), '[t] "=&s"(t)', '[u] "=&s"(u)']
+    if S == 1:
+        outs.append('[tb] "=&v"(tb)')
+    else:
+        outs += ['[l%d] "=&v"(l[%d])' % (j, j) for j in range(P)]
+    outs += ['"+{%s}"(acc[%d])' % (A[m], m) for m in range(M)]
+    outs += ['"+{v[%d:%d]}"(v%d)' % (base(M, m, W), base(M, m, W) + W - 1, m) for m in range(M)]
+    ins = ['[meta] "s"(r[0])', '[ax] "s"(r[1])', '[ay] "s"(r[2])', '[sw0] "s"(r[3])',
+           '[sw1] "s"(r[4])'] + ['[w%d] "s"(r[%d])' % (p, 5 + p) for p in range(MAX_EDGES)]
+    ins += ['[b%d] "s"(b[%d])' % (s, s) for s in range(S)]
+    ins += ['[x%d] "v"(x[%d]), [y%d] "v"(y[%d])' % (j, j, j, j) for j in range(P)]
+    ins += ['[hi] "s"(hi), [lo] "s"(lo)']
+
+    body = "\n".join('        "%s\\n"' % l for l in L)
     vec = "f32x%d" % W
-    out = ["template <> struct RegWin<%d, %d> {" % (M, W)]
+    out = []
+    out.append("template <> struct Walker<%d, %d, %d> {" % (S, P, W))
+    out.append("  static constexpr int M = %d;" % M)
+    out.append("  float acc[%d];" % M)
     out.append("  %s %s;" % (vec, ", ".join("v%d" % m for m in range(M))))
     out.append("  __device__ __forceinline__ void init() {")
     for m in range(M):
+        out.append("    acc[%d] = 0.0f;" % m)
         out.append("    v%d = (%s)(0.0f);" % (m, vec))
     out.append("  }")
-    text = "\n".join(out) + "\n"
-    for k in range(1, 5):
-        text += gen_fma(M, W, k)
-    text += gen_store(M, W, "st_mov", "v_mov_b32 {d}, {x}")
-    text += gen_store(M, W, "st_rcp", "v_rcp_f32 {d}, {x}")
-    text += gen_store(M, W, "st_exp", "v_exp_f32 {d}, {x}")
-    text += gen_store(M, W, "st_sin", "v_sin_f32 {d}, {x}")
-    text += gen_store(M, W, "st_abs", "v_and_b32 {d}, 0x7fffffff, {x}")
-    text += gen_store(M, W, "st_copysign", "v_bfi_b32 {d}, %[mask], {x}, {z}", extra_in="bfi")
-    return text + "};\n"
+    out.append("  // r: the record's 16 words; b: the node's bias row (one float per source);")
+    out.append("  // x, y: the P positions; hi, lo: the two parts of 2 pi.")
+    out.append("  __device__ __forceinline__ void step(const uint32_t* r, const float* b, "
+               "const float* x, const float* y, float hi, float lo) {")
+    out.append("    uint64_t pc;")
+    out.append("    uint32_t t, u;")
+    out.append("    float tb;" if S == 1 else "    float l[%d];" % P)
+    out.append("    asm volatile(")
+    out.append(body)
+    out.append("        : %s" % ",\n          ".join(outs))
+    out.append("        : %s" % ",\n          ".join(ins))
+    # SCC is written by the scalar arithmetic and M0 by the indexing instructions
+    out.append('        : "scc", "m0");')
+    out.append("  }")
+    out.append("};")
+    return "\n".join(out) + "\n"
 
 
 def main():
-    print("// Generated by gen_regwin.py (register-window helpers of the discover kernel).")
+    print("// Generated by gen_regwin.py (the program-record step of the discover kernel).")
     print("// Do not edit; regenerate with: python gen_regwin.py > regwin_gen.h")
     print("#pragma once")
     print()
-    print("template <int M, int W> struct RegWin;")
+    print("template <int S, int P, int W> struct Walker;")
     print()
-    for W in WINDOWS:
-        for M in INSTANCES:
-            print(gen_struct(M, W))
+    for S, P, W in VARIANTS:
+        print(gen_walker(S, P, W))
 
 
 if __name__ == "__main__":

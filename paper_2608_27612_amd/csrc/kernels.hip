@@ -107,12 +107,11 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 }
 
 // ------------------------------------------------------------------------ register windows
-// RegWin<M, W>: the M instances' varying values in pinned VGPR tuples, the indexed edge FMAs and
-// the indexed activation stores (generated, see gen_regwin.py). The tuples are asm operands, so
-// the compiler keeps them in place and knows which registers each statement reads or writes.
-// s_set_gpr_idx_on also writes M0; M0 is reserved by the compiler and this kernel has no other
-// use of it (no LDS DMA, no message or GWS instructions), which the ISA check in the tests
-// enforces.
+// Walker<S, P, W>: the M = S * P instances' accumulators and varying values in pinned VGPRs, and
+// step(), which runs one program record for all of them in a single asm statement (generated,
+// see gen_regwin.py). s_set_gpr_idx_on also writes M0; M0 is reserved by the compiler and this
+// kernel has no other use of it (no LDS DMA, no message or GWS instructions), which the ISA check
+// in the tests enforces.
 #include "regwin_gen.h"
 
 // ------------------------------------------------------------------------ look-back scan
@@ -193,23 +192,32 @@ typedef __attribute__((address_space(4))) const float cf32;
 __device__ __forceinline__ Group load_group(cu32* p) {
   Group g;
   g.var_off = p[0];
-  g.edge_off = p[1];
+  g.n_rec = p[1];
   g.n_steps = p[2];
   g.flags = p[3];
   g.bias_off = p[4];
-  g.edge_end = p[5];
-  g.pad[0] = g.pad[1] = 0;
+  g.pad[0] = g.pad[1] = g.pad[2] = 0;
 #pragma unroll
   for (int k = 0; k < kMaxGroup; ++k) g.pair[k] = p[8 + k];
   return g;
 }
 static_assert(sizeof(Group) == 12 * sizeof(uint32_t), "Group layout");
 
-struct Words4 {
-  uint32_t x, y, z, w;
+// One 16-word program record and one 4-float bias row (scalar loads; the compiler merges each
+// into a single s_load).
+struct Rec {
+  uint32_t w[kRecWords];
 };
-// Four consecutive program words (scalar loads; the compiler merges them).
-__device__ __forceinline__ Words4 load4(cu32* p) { return Words4{p[0], p[1], p[2], p[3]}; }
+__device__ __forceinline__ Rec load_rec(cu32* p) {
+  Rec r;
+#pragma unroll
+  for (int k = 0; k < (int)kRecWords; ++k) r.w[k] = p[k];
+  return r;
+}
+struct Row {
+  float b[4];
+};
+__device__ __forceinline__ Row load_row(cf32* p) { return Row{{p[0], p[1], p[2], p[3]}}; }
 
 // S sources of one genome and direction per group; each lane evaluates them at P positions of the
 // tile at once (M = S * P instances; instance m = s * P + j is source s at position j). One walk of
@@ -232,7 +240,7 @@ __global__ void __launch_bounds__(256)
   const uint32_t head_len =
       (uint32_t)(a.depth < kFirstAlignedLevel ? a.n_pos : level_offset(kFirstAlignedLevel));
 
-  RegWin<M, W> R;
+  Walker<S, P, W> R;
   R.init();
 
   // Static round-robin: global wave w takes tiles w, w + n_waves, w + 2 n_waves, ... Consecutive
@@ -249,11 +257,13 @@ __global__ void __launch_bounds__(256)
     const Group G = load_group(cgroups + 12 * gi);
     // Every table-derived offset, count and id is checked before use: an entry that points outside
     // its table raises an error flag and the tile is skipped instead of reading or writing wild.
+    // The walk reads records var_off .. var_off + 16 n_rec (one past the last: the prefetch) and
+    // bias rows inside the group's n_rec + 2.
     {
-      bool ok = G.n_steps <= kMaxSteps &&
-                (uint64_t)G.var_off + 4ull * G.n_steps <= a.blob_words &&
-                G.edge_off <= G.edge_end && G.edge_end + 8ull <= a.blob_words &&
-                (uint64_t)G.bias_off + (uint64_t)(G.n_steps + 1) * S <= a.bias_floats;
+      bool ok = G.n_rec <= kMaxRecords && G.n_steps <= G.n_rec && (G.n_rec & 1u) == 0 &&
+                (G.var_off & (kRecWords - 1)) == 0 && (G.bias_off & 3u) == 0 &&
+                (uint64_t)G.var_off + (uint64_t)kRecWords * (G.n_rec + 1) <= a.blob_words &&
+                (uint64_t)G.bias_off + 4ull * (G.n_rec + 2) <= a.bias_floats;
 #pragma unroll
       for (int s = 0; s < S; ++s) ok = ok && G.pair[s] < a.n_pairs;
       if (!ok) {
@@ -262,8 +272,6 @@ __global__ void __launch_bounds__(256)
       }
     }
     const bool out_varying = (G.flags & 1u) != 0;
-    cu32* hdr = cblob + G.var_off;
-    cf32* bt = cbias + G.bias_off;
 
     // Tile geometry: the head tile holds levels 1..3 (84 positions), every other tile 256
     // positions of one level, starting at Morton index m0 of level lvl.
@@ -327,83 +335,38 @@ __global__ void __launch_bounds__(256)
       }
 
       // ---- CPPN (Section 2): the varying program in topological order, M instances at once.
-      float acc[M];
-      uint32_t e_off = G.edge_off;  // word offset of the next node edge; stays <= G.edge_end
-      cu32* hp = hdr;
-      cf32* bs = bt;
-      for (uint32_t st = 0; st < G.n_steps; ++st, hp += 4, bs += S) {
-        const Words4 h = load4(hp);
-        // the position's x and y terms (coefficient 0 when the node has no such edge), then the
-        // source's folded bias
-        const float ax = __uint_as_float(h.y), ay = __uint_as_float(h.z);
-        if constexpr (S == 1) {
-          const float b = bs[0];
-#pragma unroll
-          for (int j = 0; j < P; ++j)
-            acc[j] = __builtin_fmaf(py[j], ay, __builtin_fmaf(px[j], ax, b));
-        } else {
-          float lin[P];
-#pragma unroll
-          for (int j = 0; j < P; ++j) lin[j] = __builtin_fmaf(py[j], ay, px[j] * ax);
-#pragma unroll
-          for (int m = 0; m < M; ++m) acc[m] = lin[m % P] + bs[m / P];
-        }
-        // node edges: at most what is left of the program's edge stream; slot indices are taken
-        // modulo the window, so an index can never leave the instance's register tuple
-        constexpr uint32_t wm = W - 1;
-        uint32_t nn = min(h.x >> kStepEdgeShift, (G.edge_end - e_off) >> 1);
-        while (nn >= 4) {
-          const Words4 e0 = load4(cblob + e_off);
-          const Words4 e1 = load4(cblob + e_off + 4);
-          R.fma4(acc, e0.x & wm, __uint_as_float(e0.y), e0.z & wm, __uint_as_float(e0.w),
-                 e1.x & wm, __uint_as_float(e1.y), e1.z & wm, __uint_as_float(e1.w));
-          e_off += 8;
-          nn -= 4;
-        }
-        if (nn != 0) {
-          // may read up to 6 words past the program's last edge; the table is padded for it
-          const Words4 e0 = load4(cblob + e_off);
-          const Words4 e1 = load4(cblob + e_off + 4);
-          if (nn == 1) {
-            R.fma1(acc, e0.x & wm, __uint_as_float(e0.y));
-          } else if (nn == 2) {
-            R.fma2(acc, e0.x & wm, __uint_as_float(e0.y), e0.z & wm, __uint_as_float(e0.w));
-          } else {
-            R.fma3(acc, e0.x & wm, __uint_as_float(e0.y), e0.z & wm, __uint_as_float(e0.w),
-                   e1.x & wm, __uint_as_float(e1.y));
-          }
-          e_off += 2 * nn;
-        }
-        switch (h.x & kStepActMask) {
-          case EMR_ACT_SIGMOID:
-#pragma unroll
-            for (int m = 0; m < M; ++m) acc[m] = act_sigmoid(acc[m]);
-            break;
-          case EMR_ACT_TANH:
-#pragma unroll
-            for (int m = 0; m < M; ++m) acc[m] = act_tanh(acc[m]);
-            break;
-          case EMR_ACT_GAUSS:
-#pragma unroll
-            for (int m = 0; m < M; ++m) acc[m] = act_gauss(acc[m]);
-            break;
-          case EMR_ACT_SINE:
-#pragma unroll
-            for (int m = 0; m < M; ++m) acc[m] = act_sine(acc[m]);
-            break;
-          case EMR_ACT_ABS:
-#pragma unroll
-            for (int m = 0; m < M; ++m) acc[m] = __builtin_fabsf(acc[m]);
-            break;
-          default:
-            break;
-        }
-        if (st + 1 < G.n_steps) R.st_mov((h.x >> kStepDstShift) & wm, acc);
+      // Records are processed in pairs (A, B; the record count is even) so that the next record
+      // is always being loaded into the other buffer while the current one is computed.
+      cu32* rp = cblob + G.var_off;
+      cf32* bp = cbias + G.bias_off + 4;  // row 1: the first varying node
+      Rec A = load_rec(rp);
+      Row ra = load_row(bp);
+      for (uint32_t r = 0; r < G.n_rec; r += 2) {
+        const Rec B = load_rec(rp + kRecWords);
+        cf32* bpb = bp + ((A.w[0] & kRecTailMask) != 0 ? 4 : 0);
+        const Row rb = load_row(bpb);
+        R.step(A.w, ra.b, px, py, k2PiHi, k2PiLo);
+        rp += 2 * kRecWords;
+        A = load_rec(rp);
+        bp = bpb + ((B.w[0] & kRecTailMask) != 0 ? 4 : 0);
+        ra = load_row(bp);
+        R.step(B.w, rb.b, px, py, k2PiHi, k2PiLo);
       }
       float w[M];
-      cf32* bo = bt + G.n_steps * S;  // output constants when the output is uniform
+      if (out_varying && G.n_rec > 0) {
+        // the output node is the last record but for the padding one; its activation is applied
+        // here
+        const uint32_t m1 = cblob[G.var_off + kRecWords * (G.n_rec - 1)];
+        const uint32_t m2 = cblob[G.var_off + kRecWords * (G.n_rec - 2)];
+        const uint32_t tail = ((m1 & kRecTailMask) != 0 ? m1 : m2) & kRecTailMask;
+        const uint32_t oa = tail >= kRecTailOutput ? tail - kRecTailOutput : (uint32_t)EMR_ACT_LINEAR;
 #pragma unroll
-      for (int m = 0; m < M; ++m) w[m] = out_varying ? acc[m] : bo[m / P];
+        for (int m = 0; m < M; ++m) w[m] = act_apply(oa, R.acc[m]);
+      } else {
+        cf32* bo = cbias + G.bias_off;  // row 0: output constants when the output is uniform
+#pragma unroll
+        for (int m = 0; m < M; ++m) w[m] = bo[m / P];
+      }
 
       // ---- variance of the four siblings (Section 3.2) and the threshold test (Eq. 2)
 #pragma unroll
@@ -471,75 +434,101 @@ __global__ void __launch_bounds__(256)
 }
 
 // ------------------------------------------------------------------------ bind kernel
+// One wave per member (genome, direction, source). The wave copies the genome's uniform program
+// into LDS with one coalesced pass, evaluates the uniform nodes in topological order (every lane
+// computes the same values, fmaf in edge order), then each lane folds the uniform contributions
+// of one varying node into that node's bias row entry.
 constexpr int kMaxU = 5 + 256;
+constexpr int kBindWaves = 4;
+constexpr uint32_t kBindProgWords = 1024;  // larger uniform programs are read from global memory
 
-__global__ void __launch_bounds__(64)
+__global__ void __launch_bounds__(kBindWaves * kWave)
     k_bind(const uint32_t* __restrict__ blob, const ProgDesc* __restrict__ desc,
            const Member* __restrict__ members, const float* __restrict__ src_xy,
            float* __restrict__ bias_tab, uint32_t* __restrict__ err, uint32_t n_members,
            uint32_t n_desc, uint32_t n_sources, uint32_t blob_words, uint64_t bias_floats) {
-  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  __shared__ float U_all[kBindWaves][kMaxU];
+  __shared__ uint32_t prog_all[kBindWaves][kBindProgWords];
+  const uint32_t lane = lane_id();
+  const uint32_t wv = threadIdx.x / kWave;
+  const uint32_t i = __builtin_amdgcn_readfirstlane(blockIdx.x * kBindWaves + wv);
   if (i >= n_members) return;
+  float* U = U_all[wv];
   const Member m = members[i];
   bool ok = m.desc < n_desc && m.source < n_sources;
   const ProgDesc d = desc[ok ? m.desc : 0];
-  const uint32_t* u = blob + d.uni_off;
-  uint32_t n_un = 0, out_u = kNone, n_steps = 0;
   ok = ok && d.uni_off + 4ull <= d.uni_end && d.uni_end <= blob_words;
+  const uint32_t words = ok ? d.uni_end - d.uni_off : 0u;
+  // Program words relative to uni_off, from LDS when they fit.
+  const uint32_t* prog = blob + d.uni_off;
+  if (ok && words <= kBindProgWords) {
+    for (uint32_t k = lane; k < words; k += kWave) prog_all[wv][k] = prog[k];
+    prog = prog_all[wv];
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  uint32_t n_un = 0, out_u = kNone, n_steps = 0;
   if (ok) {
-    n_un = u[0];
-    out_u = u[1];
-    n_steps = u[2];
-    ok = n_un <= kMaxU - 5 && n_steps <= kMaxSteps &&
-         (uint64_t)d.uni_off + 4ull + 4ull * (n_un + n_steps) <= d.uni_end &&
-         (out_u == kNone || out_u < 5 + n_un) &&
-         (uint64_t)m.bias_base + (uint64_t)n_steps * m.stride < bias_floats;
+    n_un = prog[0];
+    out_u = prog[1];
+    n_steps = prog[2];
+    // The member's bias rows: row 0 and rows 1..n_steps, all inside the group's rows.
+    const uint64_t row0 = m.bias_base & ~3u;
+    ok = n_un <= kMaxU - 5 && n_steps <= kMaxSteps && n_steps + 2 <= m.bias_rows &&
+         4ull + 4ull * (n_un + n_steps) <= words && (out_u == kNone || out_u < 5 + n_un) &&
+         row0 + 4ull * m.bias_rows <= bias_floats;
   }
   if (!ok) {
-    atomicOr(err, kErrTable);
+    if (lane == 0) atomicOr(err, kErrTable);
     return;
   }
   const uint32_t dir = m.desc & 1u;
   const float sx = src_xy[2 * m.source], sy = src_xy[2 * m.source + 1];
-  float U[kMaxU];
   // Input roles: the source fills (x1, y1) for outgoing queries and (x2, y2) for incoming ones;
   // the position-dependent roles are never read by the uniform program.
-  U[0] = dir == 0 ? sx : 0.0f;
-  U[1] = dir == 0 ? sy : 0.0f;
-  U[2] = dir == 0 ? 0.0f : sx;
-  U[3] = dir == 0 ? 0.0f : sy;
-  U[4] = 1.0f;
-  const uint32_t* rec = u + 4;
-  // Edge lists must lie inside this program; value indices must name an input or an earlier node.
+  if (lane < 5) {
+    const float in5[5] = {dir == 0 ? sx : 0.0f, dir == 0 ? sy : 0.0f, dir == 0 ? 0.0f : sx,
+                          dir == 0 ? 0.0f : sy, 1.0f};
+    U[lane] = in5[lane];
+  }
+  // Edge lists are word offsets into the blob and must lie inside this uniform program.
   auto edges_ok = [&](uint32_t off, uint32_t cnt) {
-    return (uint64_t)off + 2ull * cnt <= d.uni_end && off >= d.uni_off;
+    return off >= d.uni_off && (uint64_t)off + 2ull * cnt <= d.uni_end;
   };
-  for (uint32_t k = 0; k < n_un; ++k) {
-    float z = __uint_as_float(rec[4 * k + 3]);
-    const uint32_t cnt = rec[4 * k + 1], off = rec[4 * k + 2];
+  bool bad = false;
+  for (uint32_t k = 0; k < n_un && !bad; ++k) {
+    const uint32_t* rec = prog + 4 + 4 * k;
+    const uint32_t act = rec[0], cnt = rec[1], off = rec[2];
+    float z = __uint_as_float(rec[3]);
     if (!edges_ok(off, cnt)) {
-      atomicOr(err, kErrTable);
-      return;
+      bad = true;
+      break;
     }
-    const uint32_t* ep = blob + off;
+    const uint32_t* ep = prog + (off - d.uni_off);
     for (uint32_t e = 0; e < cnt; ++e)
       z = __builtin_fmaf(__uint_as_float(ep[2 * e + 1]), U[min(ep[2 * e], 4u + k)], z);
-    U[5 + k] = act_apply(rec[4 * k], z);
+    // every lane computed the same value and stores it to the same word
+    U[5 + k] = act_apply(act, z);
   }
-  const uint32_t* fold = rec + 4 * n_un;
-  for (uint32_t t = 0; t < n_steps; ++t) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const uint32_t* fold = prog + 4 + 4 * n_un;
+  for (uint32_t t = lane; t < n_steps && !bad; t += kWave) {
     float z = __uint_as_float(fold[4 * t + 2]);
     const uint32_t cnt = fold[4 * t], off = fold[4 * t + 1];
     if (!edges_ok(off, cnt)) {
-      atomicOr(err, kErrTable);
-      return;
+      bad = true;
+      break;
     }
-    const uint32_t* ep = blob + off;
+    const uint32_t* ep = prog + (off - d.uni_off);
     for (uint32_t e = 0; e < cnt; ++e)
       z = __builtin_fmaf(__uint_as_float(ep[2 * e + 1]), U[min(ep[2 * e], 4u + n_un)], z);
-    bias_tab[m.bias_base + t * m.stride] = z;
+    bias_tab[m.bias_base + 4 * (1 + t)] = z;
   }
-  bias_tab[m.bias_base + n_steps * m.stride] = out_u == kNone ? 0.0f : U[out_u];
+  if (bad) atomicOr(err, kErrTable);
+  if (lane == 0) bias_tab[m.bias_base] = out_u == kNone ? 0.0f : U[out_u];
 }
 
 // ------------------------------------------------------------------------ compaction
@@ -631,7 +620,8 @@ extern "C" hipError_t emr_launch_grid(float* xy, int64_t n, hipStream_t s) {
 
 extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
   if (a->n_members == 0) return hipSuccess;
-  hipLaunchKernelGGL(emr::k_bind, dim3((a->n_members + 63) / 64), dim3(64), 0, s, a->blob, a->desc,
+  hipLaunchKernelGGL(emr::k_bind, dim3((a->n_members + emr::kBindWaves - 1) / emr::kBindWaves),
+                     dim3(emr::kBindWaves * emr::kWave), 0, s, a->blob, a->desc,
                      a->members, a->src_xy, a->bias_tab, a->err, a->n_members, a->n_desc,
                      a->n_sources, a->blob_words, a->bias_floats);
   return hipGetLastError();
@@ -639,7 +629,7 @@ extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
 
 template <int S, int W, int MODE>
 static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks, hipStream_t s) {
-  constexpr int P = S == 1 ? 4 : (S == 2 ? 2 : 1);
+  constexpr int P = emr::positions_per_lane(S, W);
   emr::DiscoverScalars sc{a->cap,     a->n_pos,      a->tiles,  a->n_tiles,    a->depth,
                           a->theta,   a->blob_words, a->n_pairs, a->bias_floats};
   auto kern = emr::k_discover<S, P, W, MODE>;

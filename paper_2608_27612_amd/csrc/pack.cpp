@@ -14,6 +14,7 @@
 #include <cstdio>
 #include <cstring>
 #include <queue>
+#include <utility>
 
 namespace emr {
 
@@ -213,56 +214,69 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       return false;
     }
 
-    // ---- varying program: step headers, then the node-edge stream
+    // ---- varying program: 16-word records (layout in emr_internal.h)
     ProgDesc& d = desc[dir];
     GenomeInfo& inf = info[dir];
     inf = GenomeInfo{};
+    while (blob.size() % kRecWords) blob.push_back(0u);
     d.var_off = (uint32_t)blob.size();
     d.n_steps = (uint32_t)vsteps.size();
     d.flags = (out_varying ? 1u : 0u) | ((uint32_t)window << 8);
-    d.pad = 0;
-    const size_t step_base = blob.size();
-    blob.resize(blob.size() + 4 * vsteps.size(), 0u);
-    d.edge_off = (uint32_t)blob.size();
+    d.pad[0] = d.pad[1] = 0;
+    uint32_t n_rec = 0;
     for (int t = 0; t < (int)vsteps.size(); ++t) {
       const int v = vsteps[t];
       float ax = 0.0f, ay = 0.0f;
-      bool has_x = false, has_y = false;
-      uint32_t nn = 0;
+      std::vector<std::pair<uint32_t, float>> node_edges;  // (source slot, w) in edge-list order
       for (int ei : in_edges[v]) {
         const Edge& E = edges[ei];
         if (!live[E.src] || !varying[E.src]) continue;  // uniform: folded by the bind kernel
         const int k = g.kind[E.src];
         if (k == vx_role) {
           ax += E.w;  // parallel edges from x add their weights
-          has_x = true;
           inf.fma_xy++;
         } else if (k == vy_role) {
           ay += E.w;
-          has_y = true;
           inf.fma_xy++;
         } else {
-          blob.push_back((uint32_t)assigned[E.src]);
-          blob.push_back(fbits(E.w));
-          nn++;
+          node_edges.push_back({(uint32_t)assigned[E.src], E.w});
           inf.fma_node++;
         }
       }
-      if (nn > kMaxStepEdges) {
-        *st = EMR_E_LIMIT;
-        *msg = "too many edges into one node";
-        return false;
+      const bool is_out = out_varying && v == out_node;
+      const uint32_t dst = is_out ? 0u : (uint32_t)assigned[v];
+      const size_t ne = node_edges.size();
+      const size_t n_chunks = ne == 0 ? 1 : (ne + kRecEdges - 1) / kRecEdges;
+      for (size_t c = 0; c < n_chunks; ++c) {
+        const size_t r = blob.size();
+        blob.resize(r + kRecWords, 0u);
+        const size_t k0 = c * kRecEdges, k1 = std::min(ne, k0 + kRecEdges);
+        uint32_t meta = ((uint32_t)(k1 - k0) << kRecEdgeShift) | (dst << kRecDstShift);
+        if (c == 0) {
+          meta |= kRecFirst;
+          blob[r + 1] = fbits(ax);
+          blob[r + 2] = fbits(ay);
+        }
+        if (c + 1 == n_chunks) meta |= (is_out ? kRecTailOutput : kRecTailStore) + g.act[v];
+        blob[r] = meta;
+        // The kernel runs a record's edges from position n - 1 down to 0, so the node's edges
+        // go in reverse positions and are accumulated in edge-list order.
+        for (size_t k = k0; k < k1; ++k) {
+          const size_t e = k1 - 1 - k;
+          blob[r + 3 + e / 6] |= node_edges[k].first << (kSlotBits * (e % 6));
+          blob[r + 5 + e] = fbits(node_edges[k].second);
+        }
+        n_rec++;
       }
-      const uint32_t dst = (out_varying && v == out_node) ? 0u : (uint32_t)assigned[v];
-      uint32_t* sw = &blob[step_base + 4 * t];
-      sw[0] = (uint32_t)g.act[v] | (dst << kStepDstShift) | (has_x ? kStepHasX : 0u) |
-              (has_y ? kStepHasY : 0u) | (nn << kStepEdgeShift);
-      sw[1] = fbits(ax);
-      sw[2] = fbits(ay);
-      sw[3] = 0;
       inf.act_count[g.act[v]]++;
     }
-    d.edge_end = (uint32_t)blob.size();
+    if (n_rec & 1u) {
+      // The kernel walks records in pairs: an odd program ends with a record that does nothing
+      // (not a node start, no edges, no tail).
+      blob.resize(blob.size() + kRecWords, 0u);
+      n_rec++;
+    }
+    d.n_rec = n_rec;
     inf.n_steps = (int)vsteps.size();
     inf.window = window;
     inf.out_varying = out_varying;
@@ -308,6 +322,7 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
     }
     d.uni_end = (uint32_t)blob.size();
     inf.n_unodes = (int)unodes.size();
+    inf.n_rec = (int)n_rec;
   }
   (void)role_node;
   return true;

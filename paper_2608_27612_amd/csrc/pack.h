@@ -18,6 +18,7 @@ struct GenomeInfo {
   int act_count[6] = {0, 0, 0, 0, 0, 0};  // varying nodes per activation id
   int window = 0;        // register slots needed
   int n_unodes = 0;      // uniform computed nodes
+  int n_rec = 0;         // program records
   bool out_varying = false;
 };
 

@@ -198,10 +198,9 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
         cur.desc = di;
         for (int s = n; s < emr::kMaxGroup; ++s) cur.g.pair[s] = cur.g.pair[n - 1];
         cur.g.var_off = d.var_off;
-        cur.g.edge_off = d.edge_off;
+        cur.g.n_rec = d.n_rec;
         cur.g.n_steps = d.n_steps;
         cur.g.flags = d.flags;
-        cur.g.edge_end = d.edge_end;
         tmp.push_back(cur);
         cur = TmpGroup{};
         n = 0;
@@ -236,9 +235,10 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
     P.buckets.back().count++;
     t.g.bias_off = (uint32_t)bias;
     P.group_member0.push_back((uint32_t)P.members.size());
+    const uint32_t rows = t.g.n_rec + 2;  // output row, one per record at most, prefetch row
     for (int s = 0; s < t.S; ++s)
-      P.members.push_back({t.desc, t.src[s], (uint32_t)(bias + s), (uint32_t)t.S});
-    bias += (uint64_t)(t.g.n_steps + 1) * t.S;
+      P.members.push_back({t.desc, t.src[s], (uint32_t)(bias + s), rows});
+    bias += 4ull * rows;
     P.groups.push_back(t.g);
   }
   if (bias > 0xFFFFFFFFull) return fail(EMR_E_LIMIT, "bias table too large");

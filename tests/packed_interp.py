@@ -76,7 +76,7 @@ def f32(u):
 
 def interpret(blob, desc, dir_, sx, sy, px, py):
     """Evaluate packed program `desc[dir_]` for source (sx, sy) at positions (px, py) (arrays)."""
-    var_off, edge_off, n_steps, uni_off, flags = (int(v) for v in desc[dir_][:5])
+    var_off, n_rec, n_steps, uni_off, flags = (int(v) for v in desc[dir_][:5])
     # uniform program
     U = np.zeros(5 + 300)
     if dir_ == 0:
@@ -102,29 +102,46 @@ def interpret(blob, desc, dir_, sx, sy, px, py):
             z += f32(blob[fo + 2 * e + 1]) * U[int(blob[fo + 2 * e])]
         folded.append(z)
     if not (flags & 1):
-        assert n_steps == 0
+        assert n_steps == 0 and n_rec == 0
         return np.full(len(px), U[out_u]), (flags >> 8) & 0xFF
     window = (flags >> 8) & 0xFF
+    assert var_off % 16 == 0
     vals = np.full((max(window, 1), len(px)), np.nan)
     acc = None
-    ep = edge_off
-    for t in range(n_steps):
-        w0 = int(blob[var_off + 4 * t])
-        ax, ay = f32(blob[var_off + 4 * t + 1]), f32(blob[var_off + 4 * t + 2])
-        act, dst = w0 & 7, (w0 >> 8) & 0xFF
-        has_x, has_y, nn = (w0 >> 16) & 1, (w0 >> 17) & 1, w0 >> 20
-        assert has_x or ax == 0.0
-        assert has_y or ay == 0.0
-        acc = folded[t] + ax * px + ay * py
-        for e in range(nn):
-            src = int(blob[ep + 2 * e])
+    step = 0
+    nodes_done = 0
+    out = None
+    for r in range(n_rec):
+        w = blob[var_off + 16 * r: var_off + 16 * r + 16].astype(np.int64)
+        meta = int(w[0])
+        tail, first = meta & 15, (meta >> 4) & 1
+        dst, ne = (meta >> 8) & 31, (meta >> 16) & 15
+        assert ne <= 11 and (meta >> 20) == 0 and (meta >> 5) & 7 == 0 and (meta >> 13) & 7 == 0
+        if out is not None:
+            assert r == n_rec - 1 and not w.any(), "record after the output node"
+            continue
+        if first:
+            assert acc is None, "a node starts before the previous one ended"
+            acc = folded[step] + f32(w[1]) * px + f32(w[2]) * py
+        else:
+            assert acc is not None and w[1] == 0 and w[2] == 0
+        for e in reversed(range(ne)):   # positions n-1 .. 0 hold the edges in edge-list order
+            src = (int(w[3 + e // 6]) >> (5 * (e % 6))) & 31
             assert src < window
             v = vals[src]
             assert not np.isnan(v).any(), "read of a slot that holds no live value"
-            acc = acc + f32(blob[ep + 2 * e + 1]) * v
-        ep += 2 * nn
-        acc = _act(act, acc)
-        if t + 1 < n_steps:
+            acc = acc + f32(w[5 + e]) * v
+        for e in range(ne, 11):
+            assert w[5 + e] == 0 and ((int(w[3 + e // 6]) >> (5 * (e % 6))) & 31) == 0
+        if tail == 0:
+            continue
+        assert 1 <= tail <= 12
+        if tail <= 6:
             assert dst < window
-            vals[dst] = acc
-    return acc, window
+            vals[dst] = _act(tail - 1, acc)
+        else:
+            out = _act(tail - 7, acc)
+        acc = None
+        step += 1
+    assert step == n_steps and out is not None and n_rec % 2 == 0
+    return out, window

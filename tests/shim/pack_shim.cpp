@@ -23,10 +23,11 @@ extern "C" int shim_pack(const emr_genome* g, uint32_t* blob, int64_t blob_cap, 
   std::memcpy(blob, b.data(), b.size() * 4);
   for (int k = 0; k < 2; ++k) {
     desc8[8 * k + 0] = d[k].var_off;
-    desc8[8 * k + 1] = d[k].edge_off;
+    desc8[8 * k + 1] = d[k].n_rec;
     desc8[8 * k + 2] = d[k].n_steps;
     desc8[8 * k + 3] = d[k].uni_off;
     desc8[8 * k + 4] = d[k].flags;
+    desc8[8 * k + 5] = d[k].uni_end;
     int32_t* o = info_out + 12 * k;
     o[0] = inf[k].n_steps; o[1] = inf[k].fma_xy; o[2] = inf[k].fma_node;
     for (int a = 0; a < 6; ++a) o[3 + a] = inf[k].act_count[a];

@@ -64,3 +64,36 @@ def test_discover_kernels_use_no_scratch(asm):
                        asm)
     for name, size in sizes:
         assert int(size) == 0, name
+
+
+# Scalar instructions that read SCC, and ones that write it without reading it first.
+_SCC_READERS = re.compile(r"^\s*(s_cbranch_scc[01]|s_cselect_\w+|s_addc_u32|s_subb_u32|s_cmov\w*)\b")
+_SCC_WRITERS = re.compile(
+    r"^\s*(s_cmp\w*|s_bitcmp\w*|s_(add|sub)_[ui]32|s_(and|or|xor|andn2|orn2|nand|nor|xnor)_\w+|"
+    r"s_(lshl|lshr|ashr)\w*|s_bfe_\w+|s_(min|max)_\w+|s_not_\w+|s_abs_\w+|s_absdiff\w*|s_bcnt\w*|"
+    r"s_wqm\w*|s_quadmask\w*|s_bfm_\w+)\b")
+
+
+def test_scc_is_not_carried_across_inline_asm(asm):
+    """The record step's asm statement writes SCC; a compiler-made SCC value must never be read
+    after it without being recomputed (a loop exit test carried across it would be garbage)."""
+    lines = asm.splitlines()
+    blocks = 0
+    for i, line in enumerate(lines):
+        if ";;#ASMEND" not in line:
+            continue
+        blocks += 1
+        for k in range(i + 1, min(i + 80, len(lines))):
+            code = lines[k].split(";")[0]
+            if not code.strip() or code.strip().startswith("."):
+                continue
+            assert not _SCC_READERS.match(code), "SCC read after inline asm: " + code.strip()
+            if _SCC_WRITERS.match(code) or re.match(r"^\s*s_(branch|endpgm|setpc)", code):
+                break
+    assert blocks >= 36
+
+
+def test_record_step_clobbers_scc_and_m0():
+    hdr = open(os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "regwin_gen.h")).read()
+    n_asm = hdr.count("asm volatile(")
+    assert n_asm > 0 and hdr.count('"scc", "m0"') == n_asm
