@@ -168,7 +168,9 @@ emr_status emr_discover(const emr_population* pop, const emr_source* sources, in
 
 /* Synchronizes `stream`, then reports EMR_E_CAPACITY if any pair_count exceeds pair_capacity
  * (*max_count receives the largest count, so a retry can size the regions), or EMR_E_DEVICE if
- * the kernel flagged an internal error. n_pairs is the number of pairs of the discover call. */
+ * the kernel flagged an internal error. n_pairs is the number of pairs of the discover call.
+ * The flags and the largest count are read from the workspace of `out` (the discover call
+ * leaves them there); without a workspace the counts themselves are read. */
 emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max_count,
                             void* stream);
 
@@ -190,11 +192,11 @@ emr_status emr_discover_cost(const emr_population* pop, const emr_source* source
 /* ------------------------------------------------------------------ profiling */
 
 /* One discover-kernel launch of the last profiled emr_discover / emr_eval_raw call on this thread:
- * its variant (sources per lane S, register window W), tiles, queries, algorithmic VALU slots
- * under the cost model of emr_discover_cost, and its duration from a HIP event pair recorded on
- * the call's stream around the launch. */
+ * its variant (sources per lane S, register window W, positions per lane P), tiles, queries,
+ * algorithmic VALU slots under the cost model of emr_discover_cost, and its duration from a HIP
+ * event pair recorded on the call's stream around the launch. */
 typedef struct {
-  int32_t group_size, window;
+  int32_t group_size, window, positions, reserved;
   int64_t tiles, queries;
   double slots;
   float ms;
@@ -205,7 +207,9 @@ typedef struct {
 emr_status emr_profile_enable(int32_t on, double transcendental_slots);
 
 /* Synchronizes on the last profiled call's events and writes up to `cap` launch records to
- * `out` (host); *n receives the number of launches of that call. */
+ * `out` (host); *n receives the number of launches of that call. Records are in launch order:
+ * launches go out costliest first, the first on the call's stream and the others (except in the
+ * look-back placement mode) on library side streams that run alongside it. */
 emr_status emr_profile_read(emr_launch_profile* out, int32_t cap, int32_t* n);
 
 #ifdef __cplusplus

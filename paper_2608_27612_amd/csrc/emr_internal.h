@@ -68,7 +68,8 @@ constexpr uint32_t kSlotBits = 5;
 //   header 4 words: n_unodes, out_u (index into U of the output, or kNone when it varies),
 //                   n_steps (of the varying program), 0
 //   n_unodes records of 4 words: act, n_edges, edge_off, bias bits      -> U[5 + k]
-//   n_steps  records of 4 words: n_fold, fold_off, bias bits, 0         -> folded bias of step i
+//   n_steps  records of 4 words: n_fold, fold_off, bias bits, r         -> folded bias of varying
+//            node i, for its first program record r
 //   edges: {u_src, w bits}; U[0..4] hold the five input roles (x1, y1, x2, y2, 1).
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 
@@ -84,9 +85,9 @@ struct ProgDesc {
 
 // One unit of kernel work: up to kMaxGroup sources of one genome sharing a direction.
 // Its bias rows (4 floats each, one per source slot) start at bias_off, a multiple of 4: row 0 holds
-// the output constants (used when the output is uniform), row 1 + t the folded bias of varying
-// node t. The group owns n_rec + 2 rows, so a walk that advances one row per record, plus the
-// prefetch of the next row, never leaves its own rows.
+// the output constants (used when the output is uniform), row 1 + r the folded bias of the node
+// whose first program record is r (rows of other records are unused). The group owns n_rec + 2
+// rows: the walk reads row 1 + r with record r, for r up to n_rec (the prefetch past the end).
 struct Group {
   uint32_t var_off;
   uint32_t n_rec;
@@ -116,10 +117,14 @@ constexpr uint64_t kStatusAggregate = 1ull << 62;
 constexpr uint64_t kStatusInclusive = 2ull << 62;
 constexpr uint64_t kStatusValueMask = (1ull << 62) - 1;
 
-// Positions per lane per program walk for S sources and window W: the largest of 4, 2, 1 whose
-// value windows fit the register budget.
+// Positions per lane per program walk for S sources and window W: the largest of 8, 4, 2, 1 whose
+// M = S P value windows fit the register budget and whose estimated VGPR total (accumulators,
+// windows, positions, outputs and variance temporaries) leaves room for 3 waves per SIMD.
+EMR_HD constexpr bool fits_lane(int S, int P, int W) {
+  return S * P * W <= kWindowRegs && S * P <= 16 && 16 + 3 * S * P + S * P * W + 2 * P <= 168;
+}
 EMR_HD constexpr int positions_per_lane(int S, int W) {
-  return S * 4 * W <= kWindowRegs ? 4 : (S * 2 * W <= kWindowRegs ? 2 : 1);
+  return fits_lane(S, 8, W) ? 8 : fits_lane(S, 4, W) ? 4 : fits_lane(S, 2, W) ? 2 : 1;
 }
 
 // Level helpers shared by host and device.

@@ -16,9 +16,9 @@ single site inside the program loop and the compiler never needs to move them:
      M fused multiply-adds acc_m += w * tuple_m[slot]. The packer stores a node's edges in reverse
      record positions, so they are accumulated in edge-list order.
   3. the tail, through a branch table on meta bits 0..3: the node's activation, whose last
-     instruction writes straight into the destination slot of every tuple (DST indexing), or
-     nothing (a continuation record, or the output node, whose activation is applied by the
-     caller).
+     instruction writes straight into the destination slot of every tuple (DST indexing), or, for
+     the output node, the activation in place on the accumulators; nothing for a continuation
+     record.
 
 The statement declares SCC and M0 as clobbered: its scalar arithmetic writes SCC, and the
 register-indexing instructions write M0.
@@ -26,7 +26,8 @@ register-indexing instructions write M0.
 Hazards: the statement is opaque to the compiler's hazard recognizer, so it keeps the one that
 applies here itself: a non-transcendental VALU instruction that reads the result of a
 transcendental one (v_exp, v_rcp, v_sin) needs one wait state in between; every such pair below
-is at least M >= 3 instructions apart. Branch targets are computed from label differences, so the
+is at least M >= 3 instructions apart. The output tails end with s_nop 1, since the caller reads
+the accumulators next, possibly with DPP (two wait states after a VALU write). Branch targets are computed from label differences, so the
 jump arithmetic follows the assembler's actual encodings.
 
 Inline assembly needs literal register names, so every variant is spelled out here.
@@ -37,13 +38,24 @@ ACC = 4
 PC = 36  # SGPR pair s[PC:PC+1] for the computed jumps (bound as an early-clobber output)
 MAX_EDGES = 11
 SLOT_BITS = 5
-# (S, P, W) variants; M * W <= 128 VGPRs of value tuples.
-VARIANTS = [(S, P, W) for W in (8, 16, 32) for S in (1, 2, 3, 4)
-            for P in [4 if S * 4 * W <= 128 else (2 if S * 2 * W <= 128 else 1)]]
+
+
+def fits_lane(S, P, W):
+    """The positions-per-lane policy of the kernels (emr_internal.h), restated."""
+    return S * P * W <= 128 and S * P <= 16 and 16 + 3 * S * P + S * P * W + 2 * P <= 168
+
+
+def positions_per_lane(S, W):
+    return next(P for P in (8, 4, 2, 1) if P == 1 or fits_lane(S, P, W))
+
+
+# (S, P, W) variants
+VARIANTS = [(S, positions_per_lane(S, W), W) for W in (8, 16, 32) for S in (1, 2, 3, 4)]
 
 NEG_LOG2E = "0xbfb8aa3b"       # -log2(e) as float bits
 NEG_2LOG2E = "0xc038aa3b"      # -2 log2(e)
 INV_2PI = "0.15915494"         # 1/(2 pi): an inline constant of the ISA
+ACTS = ["lin", "sig", "tanh", "gau", "sin", "abs"]  # activation ids 0..5
 
 
 def base(M, m, W):
@@ -106,41 +118,64 @@ def gen_walker(S, P, W):
           "s_addc_u32 s%d, s%d, 0" % (PC + 1, PC + 1),
           "s_setpc_b64 s[%d:%d]" % (PC, PC + 1),
           ".Lt0_%=:"]
-    targets = ["x", "lin", "sig", "tanh", "gau", "sin", "abs"] + ["x"] * 9
+    # tails: 0 continuation; 1..6 activation then store to the destination slot; 7..12 the
+    # output node's activation, applied to the accumulators in place
+    targets = ["x"] + ["%s%s" % (a, k) for k in ("", "o") for a in ACTS] + ["x"] * 3
     L += ["s_branch .L%s_%%=" % t for t in targets]
 
-    def dst_block(label, pre, final):
+    # The activations. pre: in-place steps on the accumulator; final: the last instruction, which
+    # writes the destination slot (store tails, DST indexing) or the accumulator (output tails).
+    def block(label, pre, final, store):
         out = [".L%s_%%=:" % label]
         for step in pre:
             out += [step.format(a=A[m]) for m in range(M)]
-        out.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
-        out += [final.format(a=A[m], d=T[m]) for m in range(M)]
-        out.append("s_branch .Lxo_%=")
+        if store:
+            out.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
+            out += [final.format(a=A[m], d=T[m]) for m in range(M)]
+            out.append("s_branch .Lxo_%=")
+        else:
+            out += [final.format(a=A[m], d=A[m]) for m in range(M) if final]
+            out += ["s_nop 1", "s_branch .Lx_%="]  # the caller may read these with DPP next
         return out
 
-    L += dst_block("lin", [], "v_mov_b32 {d}, {a}")
-    L += dst_block("abs", [], "v_and_b32 {d}, 0x7fffffff, {a}")
-    L += dst_block("sig", ["v_mul_f32 {a}, %s, {a}" % NEG_LOG2E, "v_exp_f32 {a}, {a}",
-                           "v_add_f32 {a}, 1.0, {a}"], "v_rcp_f32 {d}, {a}")
-    L += dst_block("tanh", ["v_mul_f32 {a}, %s, {a}" % NEG_2LOG2E, "v_exp_f32 {a}, {a}",
-                            "v_add_f32 {a}, 1.0, {a}", "v_rcp_f32 {a}, {a}"],
-                   "v_fma_f32 {d}, {a}, 2.0, -1.0")
-    L += dst_block("gau", ["v_mul_f32 {a}, {a}, {a}", "v_mul_f32 {a}, %s, {a}" % NEG_LOG2E],
-                   "v_exp_f32 {d}, {a}")
-    # sine: k = rint(z / 2pi) in the destination slot, z - k 2pi with a two-part 2pi (Cody-Waite)
-    # in the accumulator, then the hardware sine of the reduced argument in revolutions
-    L.append(".Lsin_%=:")
-    L.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
-    L += ["v_mul_f32 %s, %s, %s" % (T[m], INV_2PI, A[m]) for m in range(M)]
-    L.append("s_set_gpr_idx_mode gpr_idx(SRC0,DST)")
-    L += ["v_rndne_f32 %s, %s" % (T[m], T[m]) for m in range(M)]
-    L.append("s_set_gpr_idx_mode gpr_idx(SRC0)")
-    L += ["v_fma_f32 %s, -%s, %%[hi], %s" % (A[m], T[m], A[m]) for m in range(M)]
-    L += ["v_fma_f32 %s, -%s, %%[lo], %s" % (A[m], T[m], A[m]) for m in range(M)]
-    L.append("s_set_gpr_idx_off")
-    L += ["v_mul_f32 %s, %s, %s" % (A[m], INV_2PI, A[m]) for m in range(M)]
-    L.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
-    L += ["v_sin_f32 %s, %s" % (T[m], A[m]) for m in range(M)]
+    defs = {
+        "lin": ([], "v_mov_b32 {d}, {a}"),
+        "abs": ([], "v_and_b32 {d}, 0x7fffffff, {a}"),
+        "sig": (["v_mul_f32 {a}, %s, {a}" % NEG_LOG2E, "v_exp_f32 {a}, {a}",
+                 "v_add_f32 {a}, 1.0, {a}"], "v_rcp_f32 {d}, {a}"),
+        "tanh": (["v_mul_f32 {a}, %s, {a}" % NEG_2LOG2E, "v_exp_f32 {a}, {a}",
+                  "v_add_f32 {a}, 1.0, {a}", "v_rcp_f32 {a}, {a}"], "v_fma_f32 {d}, {a}, 2.0, -1.0"),
+        "gau": (["v_mul_f32 {a}, {a}, {a}", "v_mul_f32 {a}, %s, {a}" % NEG_LOG2E],
+                "v_exp_f32 {d}, {a}"),
+    }
+    for store in (True, False):
+        for name, (pre, final) in defs.items():
+            if not store and name == "lin":
+                L += [".Llino_%=:", "s_branch .Lx_%="]
+                continue
+            L += block(name + ("" if store else "o"), pre, final, store)
+    # sine: k = rint(z / 2pi) kept in the destination slot (whose old value is dead here; the
+    # output node's slot is 0 and no value is live after it), z - k 2pi with a two-part 2pi
+    # (Cody-Waite) in the accumulator, then the hardware sine of the reduced argument in
+    # revolutions, written to the slot (store) or the accumulator (output)
+    for store in (True, False):
+        L.append(".Lsin%s_%%=:" % ("" if store else "o"))
+        L.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
+        L += ["v_mul_f32 %s, %s, %s" % (T[m], INV_2PI, A[m]) for m in range(M)]
+        L.append("s_set_gpr_idx_mode gpr_idx(SRC0,DST)")
+        L += ["v_rndne_f32 %s, %s" % (T[m], T[m]) for m in range(M)]
+        L.append("s_set_gpr_idx_mode gpr_idx(SRC0)")
+        L += ["v_fma_f32 %s, -%s, %%[hi], %s" % (A[m], T[m], A[m]) for m in range(M)]
+        L += ["v_fma_f32 %s, -%s, %%[lo], %s" % (A[m], T[m], A[m]) for m in range(M)]
+        L.append("s_set_gpr_idx_off")
+        L += ["v_mul_f32 %s, %s, %s" % (A[m], INV_2PI, A[m]) for m in range(M)]
+        if store:
+            L.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
+            L += ["v_sin_f32 %s, %s" % (T[m], A[m]) for m in range(M)]
+            L.append("s_branch .Lxo_%=")
+        else:
+            L += ["v_sin_f32 %s, %s" % (A[m], A[m]) for m in range(M)]
+            L += ["s_nop 1", "s_branch .Lx_%="]
     L += [".Lxo_%=:", "s_set_gpr_idx_off", ".Lx_%=:"]
 
     outs = ['[pc] "=&{s[%d:%d]}"(pc)' % (PC, PC + 1), '[t] "=&s"(t)', '[u] "=&s"(u)']
@@ -186,6 +221,29 @@ def gen_walker(S, P, W):
     return "\n".join(out) + "\n"
 
 
+def gen_quad(M):
+    """s[m] = the sum over the lane's quad of (w - quad mean)^2, for m < M, stage by stage:
+    t = w + perm1(w); t = t + perm2(t); t = w - t/4; t = t*t; t = t + perm1(t); t = t + perm2(t)
+    (perm1 swaps lanes 0<->1, 2<->3 of each quad, perm2 swaps the pairs). A DPP instruction reads
+    a VGPR two wait states after a VALU write at the earliest: each stage reads the previous one
+    M >= 3 instructions back, and the statement starts with s_nop 1 for its inputs."""
+    p1 = "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1"
+    p2 = "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf bound_ctrl:1"
+    L = ["s_nop 1"]
+    L += ["v_add_f32_dpp %%[t%d], %%[w%d], %%[w%d] %s" % (m, m, m, p1) for m in range(M)]
+    L += ["v_add_f32_dpp %%[t%d], %%[t%d], %%[t%d] %s" % (m, m, m, p2) for m in range(M)]
+    L += ["v_fmamk_f32 %%[t%d], %%[t%d], 0xbe800000, %%[w%d]" % (m, m, m) for m in range(M)]
+    L += ["v_mul_f32 %%[t%d], %%[t%d], %%[t%d]" % (m, m, m) for m in range(M)]
+    L += ["v_add_f32_dpp %%[t%d], %%[t%d], %%[t%d] %s" % (m, m, m, p1) for m in range(M)]
+    L += ["v_add_f32_dpp %%[t%d], %%[t%d], %%[t%d] %s" % (m, m, m, p2) for m in range(M)]
+    body = "\n".join('        "%s\\n"' % l for l in L)
+    outs = ",\n          ".join('[t%d] "=&v"(s[%d])' % (m, m) for m in range(M))
+    ins = ",\n          ".join('[w%d] "v"(w[%d])' % (m, m) for m in range(M))
+    return ("template <> __device__ __forceinline__ void quad_sumsq_dev<%d>(const float* w, "
+            "float* s) {\n    asm volatile(\n%s\n        : %s\n        : %s);\n}\n"
+            % (M, body, outs, ins))
+
+
 def main():
     print("// Generated by gen_regwin.py (the program-record step of the discover kernel).")
     print("// Do not edit; regenerate with: python gen_regwin.py > regwin_gen.h")
@@ -195,6 +253,11 @@ def main():
     print()
     for S, P, W in VARIANTS:
         print(gen_walker(S, P, W))
+    print("// Sum of squared deviations from the quad mean, for M values per lane at once.")
+    print("template <int M> __device__ void quad_sumsq_dev(const float* w, float* s);")
+    print()
+    for M in sorted(set(S * P for S, P, W in VARIANTS)):
+        print(gen_quad(M))
 
 
 if __name__ == "__main__":

@@ -81,21 +81,10 @@ __device__ __forceinline__ int level_of(uint32_t p) {
 __device__ __forceinline__ uint32_t lane_id() {
   return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
 }
-// Sum over the 4 lanes of a quad, pairwise: (w0+w1)+(w2+w3). Each lane adds its neighbour's value
-// to its own (IEEE addition commutes), so the result is bit-identical in all 4 lanes.
-__device__ __forceinline__ float quad_sum(float v) {
-  float t = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, true)) + v;
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(t), 0x4E, 0xF, 0xF, true)) + t;
-}
-// Population variance of the quad's four values, identical in its four lanes. Contraction is off:
-// a fused d*d + neighbour would round differently in different lanes.
-__device__ __forceinline__ float quad_variance(float w) {
-#pragma clang fp contract(off)
-  const float s1 = quad_sum(w);
-  const float d = __builtin_fmaf(-0.25f, s1, w);  // w - mean; 0.25 * s1 (the mean) is exact
-  const float s2 = quad_sum(d * d);
-  return s2 * 0.25f;
-}
+// var > theta (Section 3.2, Eq. 2) is tested as s2 > 4 theta, where s2 = the sum over the quad of
+// the squared deviations from the quad mean = 4 var (quad_sumsq_dev, generated): both scalings by
+// 4 are exact, barring overflow or a subnormal variance. The sums are pairwise, (w0+w1)+(w2+w3),
+// and each lane adds its neighbour's value to its own, so all four lanes hold the same bits.
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
 __device__ __forceinline__ uint32_t popc64(uint64_t m) { return __builtin_popcountll(m); }
 __device__ __forceinline__ uint32_t mbcnt64(uint64_t m) {
@@ -113,6 +102,12 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 // kernel has no other use of it (no LDS DMA, no message or GWS instructions), which the ISA check
 // in the tests enforces.
 #include "regwin_gen.h"
+
+// Raises *p to at least v. The plain read first keeps the many waves whose value is not larger
+// from all queueing on the one word.
+__device__ __forceinline__ void raise_max(uint32_t* p, uint32_t v) {
+  if (v > __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicMax(p, v);
+}
 
 // ------------------------------------------------------------------------ look-back scan
 // Tile status words of one pair, indexed by tile. A tile publishes its local count as an
@@ -171,11 +166,11 @@ __device__ uint64_t lookback(uint64_t* row, uint32_t tile, uint64_t count, uint3
 // loads through the scalar cache.
 struct DiscoverScalars {
   int64_t cap, n_pos;
-  uint32_t tiles, n_tiles;
+  uint32_t tiles, n_chunks, chunks_per_group, chunk_tiles;
   int32_t depth;
-  float theta;
+  float theta4;  // 4 theta
   uint32_t blob_words, n_pairs;
-  uint64_t bias_floats;
+  uint32_t bias_floats;  // the host keeps the bias table below 2^32 floats
 };
 
 // Output modes: raw CPPN outputs; records at fixed per-tile slots (pair_capacity >= Q(D), compacted
@@ -219,9 +214,10 @@ struct Row {
 };
 __device__ __forceinline__ Row load_row(cf32* p) { return Row{{p[0], p[1], p[2], p[3]}}; }
 
-// S sources of one genome and direction per group; each lane evaluates them at P positions of the
-// tile at once (M = S * P instances; instance m = s * P + j is source s at position j). One walk of
-// the program therefore serves M queries.
+// S sources of one genome and direction per group; each lane evaluates them at P positions at once
+// (M = S * P instances; instance m = s * P + j is source s at position block j). One walk of the
+// program therefore serves M queries per lane. A walk covers TPW = P / 4 whole tiles when P >= 4,
+// else a quarter or half of one tile (NPASS = 4 / P walks per tile).
 template <int S, int P, int W, int MODE>
 __global__ void __launch_bounds__(256)
     k_discover(const uint32_t* __restrict__ blob, const Group* __restrict__ groups,
@@ -229,7 +225,10 @@ __global__ void __launch_bounds__(256)
                uint32_t* __restrict__ err, uint32_t* __restrict__ parent, float* __restrict__ w4,
                int64_t* __restrict__ pair_count, float* __restrict__ raw, DiscoverScalars a) {
   constexpr int M = S * P;
-  constexpr int NPASS = kTileIters / P;
+  constexpr int TPW = P >= kTileIters ? P / kTileIters : 1;  // tiles per walk
+  constexpr int NPASS = P >= kTileIters ? 1 : kTileIters / P;  // walks per tile
+  constexpr int KB = TPW * kTileIters;                        // 64-position blocks per tile set
+  // (the launcher makes chunk_tiles a multiple of TPW, so a walk's tiles lie in one chunk)
   const uint32_t lane = lane_id();
   // Within a level-aligned tile the grid index's 6 low bits are the lane id; its Morton bits give
   // the low 3 bits of the cell's column (even bits) and row (odd bits).
@@ -243,27 +242,30 @@ __global__ void __launch_bounds__(256)
   Walker<S, P, W> R;
   R.init();
 
-  // Static round-robin: global wave w takes tiles w, w + n_waves, w + 2 n_waves, ... Consecutive
-  // tiles of a pair go to consecutive waves, so a pair's tiles are computed concurrently.
+  // Work is handed out in chunks of chunk_tiles consecutive tiles of one group, round-robin over
+  // the waves: chunk c goes to wave c mod n_waves. A group's chunks go to consecutive waves, so a
+  // pair's tiles are computed concurrently, and each wave visits its tiles in increasing order.
   const uint32_t n_waves = gridDim.x * (blockDim.x / kWave);
   const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +
                                                        threadIdx.x / kWave);
   cu32* cblob = (cu32*)blob;
   cu32* cgroups = (cu32*)groups;
   cf32* cbias = (cf32*)bias_tab;
-  for (uint32_t t = wave; t < a.n_tiles; t += n_waves) {
-    const uint32_t gi = t / a.tiles;
-    const uint32_t tile = t - gi * a.tiles;
+  for (uint32_t c = wave; c < a.n_chunks; c += n_waves) {
+    const uint32_t gi = c / a.chunks_per_group;
+    const uint32_t chunk_tile = (c - gi * a.chunks_per_group) * a.chunk_tiles;
     const Group G = load_group(cgroups + 12 * gi);
     // Every table-derived offset, count and id is checked before use: an entry that points outside
-    // its table raises an error flag and the tile is skipped instead of reading or writing wild.
+    // its table raises an error flag and the chunk is skipped instead of reading or writing wild.
     // The walk reads records var_off .. var_off + 16 n_rec (one past the last: the prefetch) and
     // bias rows inside the group's n_rec + 2.
+    // (32-bit arithmetic throughout: n_rec is bounded first, and no sum below can wrap.)
     {
+      const uint32_t rec_words = kRecWords * (G.n_rec + 1), row_floats = 4u * (G.n_rec + 2);
       bool ok = G.n_rec <= kMaxRecords && G.n_steps <= G.n_rec && (G.n_rec & 1u) == 0 &&
                 (G.var_off & (kRecWords - 1)) == 0 && (G.bias_off & 3u) == 0 &&
-                (uint64_t)G.var_off + (uint64_t)kRecWords * (G.n_rec + 1) <= a.blob_words &&
-                (uint64_t)G.bias_off + 4ull * (G.n_rec + 2) <= a.bias_floats;
+                rec_words <= a.blob_words && G.var_off <= a.blob_words - rec_words &&
+                row_floats <= a.bias_floats && G.bias_off <= a.bias_floats - row_floats;
 #pragma unroll
       for (int s = 0; s < S; ++s) ok = ok && G.pair[s] < a.n_pairs;
       if (!ok) {
@@ -272,161 +274,205 @@ __global__ void __launch_bounds__(256)
       }
     }
     const bool out_varying = (G.flags & 1u) != 0;
+    const Row orow = load_row(cbias + G.bias_off);  // row 0: output constants (uniform output)
 
-    // Tile geometry: the head tile holds levels 1..3 (84 positions), every other tile 256
-    // positions of one level, starting at Morton index m0 of level lvl.
-    const bool head = tile == 0;
-    uint32_t p0 = 0, n_valid = head_len, m0 = 0;
-    int lvl = 0;
-    if (!head) {
-      p0 = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(tile - 1) * kTile);
-      n_valid = kTile;
-      lvl = (31 - __builtin_clz(3u * p0 + 4u)) >> 1;
-      m0 = p0 - (uint32_t)level_offset(lvl);
-    }
-
-    uint32_t run[S];  // records so far in this tile, per source (padded mode)
+    for (uint32_t t0 = chunk_tile; t0 < chunk_tile + a.chunk_tiles && t0 < a.tiles; t0 += TPW) {
+      // ---- geometry of the walk's tiles. Tile 0 holds levels 1..3 (84 positions); every other
+      // tile 256 positions of one level, starting at Morton index m0 of level lvl. m0 is a
+      // multiple of 256, so the tile's 64-position blocks it = 0..3 have Morton prefixes
+      // (m0 >> 6) | it, whose column and row bits are those of m0 >> 6 with it's two bits or-ed in.
+      uint32_t p0[TPW], n_valid[TPW], cx[TPW], cy[TPW];
+      float scale[TPW];
 #pragma unroll
-    for (int s = 0; s < S; ++s) run[s] = 0;
-    float wbuf[kTileIters][S];      // look-back mode only: outputs and decisions of the tile
-    uint64_t keep[kTileIters][S];
-    if constexpr (MODE == kModeLookback) {
-#pragma unroll
-      for (int it = 0; it < kTileIters; ++it)
-#pragma unroll
-        for (int s = 0; s < S; ++s) {
-          wbuf[it][s] = 0.0f;
-          keep[it][s] = 0ull;
+      for (int k = 0; k < TPW; ++k) {
+        const uint32_t tile = t0 + k;
+        p0[k] = 0;
+        n_valid[k] = tile == 0 ? head_len : (tile < a.tiles ? (uint32_t)kTile : 0u);
+        scale[k] = 1.0f;
+        cx[k] = cy[k] = 0;
+        if (tile != 0 && tile < a.tiles) {
+          p0[k] = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(tile - 1) * kTile);
+          const int lvl = (31 - __builtin_clz(3u * p0[k] + 4u)) >> 1;
+          const uint32_t m0 = p0[k] - (uint32_t)level_offset(lvl);
+          scale[k] = pow2_neg(lvl);
+          cx[k] = compact_even(m0 >> 6);
+          cy[k] = compact_even(m0 >> 7);
         }
-    }
+      }
+      uint32_t run[S][TPW];  // records so far per source and tile (padded mode)
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+#pragma unroll
+        for (int k = 0; k < TPW; ++k) run[s][k] = 0;
+      float wbuf[KB][S];  // look-back mode only: outputs and decisions of the tiles
+      uint64_t keep[KB][S];
+      if constexpr (MODE == kModeLookback) {
+#pragma unroll
+        for (int b = 0; b < KB; ++b)
+#pragma unroll
+          for (int s = 0; s < S; ++s) {
+            wbuf[b][s] = 0.0f;
+            keep[b][s] = 0ull;
+          }
+      }
 
 #pragma unroll MODE == kModeLookback ? NPASS : 1
-    for (int pass = 0; pass < NPASS; ++pass) {
-      if ((uint32_t)(pass * P * kWave) >= n_valid) break;
-      // ---- positions of this pass (Eq. 1 cell centres, decoded from the grid index)
-      float px[P], py[P];
-      bool valid[P];
-      uint64_t vmask[P];  // lanes holding a position of the tile (all but the head tile's tail)
-      uint32_t pidx[P];
-#pragma unroll
-      for (int j = 0; j < P; ++j) {
-        const uint32_t it = (uint32_t)(pass * P + j);
-        const uint32_t p = p0 + it * kWave + lane;
-        pidx[j] = p;
-        valid[j] = it * kWave + lane < n_valid;
-        const uint32_t first = it * kWave;  // uniform: lanes [0, n_valid - first) are valid
-        vmask[j] = first >= n_valid ? 0ull
-                   : (n_valid - first >= (uint32_t)kWave ? ~0ull
-                                                         : ((1ull << (n_valid - first)) - 1ull));
-        if (!head) {
-          const uint32_t m_hi = (m0 >> 6) + it;
-          const float scale = pow2_neg(lvl);
-          const float bx = __builtin_fmaf((float)(16u * compact_even(m_hi) + 1u), scale, -1.0f);
-          const float by = __builtin_fmaf((float)(16u * compact_even(m_hi >> 1) + 1u), scale, -1.0f);
-          px[j] = __builtin_fmaf(i_lo_f, scale, bx);
-          py[j] = __builtin_fmaf(j_lo_f, scale, by);
-        } else {
-          const int l = level_of(p);
-          const uint32_t m = p - (uint32_t)level_offset(l);
-          const float scale = pow2_neg(l);
-          px[j] = __builtin_fmaf((float)(2u * compact_even(m) + 1u), scale, -1.0f);
-          py[j] = __builtin_fmaf((float)(2u * compact_even(m >> 1) + 1u), scale, -1.0f);
-        }
-      }
-
-      // ---- CPPN (Section 2): the varying program in topological order, M instances at once.
-      // Records are processed in pairs (A, B; the record count is even) so that the next record
-      // is always being loaded into the other buffer while the current one is computed.
-      cu32* rp = cblob + G.var_off;
-      cf32* bp = cbias + G.bias_off + 4;  // row 1: the first varying node
-      Rec A = load_rec(rp);
-      Row ra = load_row(bp);
-      for (uint32_t r = 0; r < G.n_rec; r += 2) {
-        const Rec B = load_rec(rp + kRecWords);
-        cf32* bpb = bp + ((A.w[0] & kRecTailMask) != 0 ? 4 : 0);
-        const Row rb = load_row(bpb);
-        R.step(A.w, ra.b, px, py, k2PiHi, k2PiLo);
-        rp += 2 * kRecWords;
-        A = load_rec(rp);
-        bp = bpb + ((B.w[0] & kRecTailMask) != 0 ? 4 : 0);
-        ra = load_row(bp);
-        R.step(B.w, rb.b, px, py, k2PiHi, k2PiLo);
-      }
-      float w[M];
-      if (out_varying && G.n_rec > 0) {
-        // the output node is the last record but for the padding one; its activation is applied
-        // here
-        const uint32_t m1 = cblob[G.var_off + kRecWords * (G.n_rec - 1)];
-        const uint32_t m2 = cblob[G.var_off + kRecWords * (G.n_rec - 2)];
-        const uint32_t tail = ((m1 & kRecTailMask) != 0 ? m1 : m2) & kRecTailMask;
-        const uint32_t oa = tail >= kRecTailOutput ? tail - kRecTailOutput : (uint32_t)EMR_ACT_LINEAR;
-#pragma unroll
-        for (int m = 0; m < M; ++m) w[m] = act_apply(oa, R.acc[m]);
-      } else {
-        cf32* bo = cbias + G.bias_off;  // row 0: output constants when the output is uniform
-#pragma unroll
-        for (int m = 0; m < M; ++m) w[m] = bo[m / P];
-      }
-
-      // ---- variance of the four siblings (Section 3.2) and the threshold test (Eq. 2)
-#pragma unroll
-      for (int s = 0; s < S; ++s) {
+      for (int pass = 0; pass < NPASS; ++pass) {
+        if (TPW == 1 && (uint32_t)(pass * P * kWave) >= n_valid[0]) break;
+        // ---- positions of this walk (Eq. 1 cell centres, decoded from the grid index)
+        float px[P], py[P];
+        uint64_t vmask[P];  // lanes holding a position (all but the head tile's tail, and none
+                            // of a tile past the pair's last)
 #pragma unroll
         for (int j = 0; j < P; ++j) {
-          const int m = s * P + j;
-          if constexpr (MODE == kModeRaw) {
-            if (valid[j]) raw[(int64_t)G.pair[s] * a.n_pos + pidx[j]] = w[m];
-            continue;
-          }
-          const uint64_t kb = ballot(quad_variance(w[m]) > a.theta) & vmask[j];
-          if constexpr (MODE == kModeLookback) {
-            keep[pass * P + j][s] = kb;
-            wbuf[pass * P + j][s] = w[m];
+          const int k = P >= kTileIters ? j / kTileIters : 0;
+          const uint32_t it = P >= kTileIters ? (uint32_t)(j % kTileIters) : (uint32_t)(pass * P + j);
+          const uint32_t first = it * kWave;  // uniform: lanes [0, n_valid - first) are valid
+          if (t0 + k != 0) {
+            vmask[j] = t0 + k < a.tiles ? ~0ull : 0ull;
+            const float bx =
+                __builtin_fmaf((float)(16u * (cx[k] | (it & 1u)) + 1u), scale[k], -1.0f);
+            const float by =
+                __builtin_fmaf((float)(16u * (cy[k] | (it >> 1)) + 1u), scale[k], -1.0f);
+            px[j] = __builtin_fmaf(i_lo_f, scale[k], bx);
+            py[j] = __builtin_fmaf(j_lo_f, scale[k], by);
           } else {
-            if (kb != 0ull) {
+            vmask[j] = first >= n_valid[k] ? 0ull
+                       : (n_valid[k] - first >= (uint32_t)kWave
+                              ? ~0ull
+                              : ((1ull << (n_valid[k] - first)) - 1ull));
+            const uint32_t p = first + lane;
+            const int l = level_of(p);
+            const uint32_t mm = p - (uint32_t)level_offset(l);
+            const float sc = pow2_neg(l);
+            px[j] = __builtin_fmaf((float)(2u * compact_even(mm) + 1u), sc, -1.0f);
+            py[j] = __builtin_fmaf((float)(2u * compact_even(mm >> 1) + 1u), sc, -1.0f);
+          }
+        }
+
+        // ---- CPPN (Section 2): the varying program in topological order, M instances at once.
+        // Records are processed in pairs (A, B; the record count is even) so that the next
+        // record and its bias row are always being loaded into the other buffer while the
+        // current one is computed. Record r reads bias row 1 + r. A uniform output is the
+        // constant of row 0 (its program has no records).
+        if (out_varying) {
+          cu32* rp = cblob + G.var_off;
+          cf32* bp = cbias + G.bias_off + 4;
+          Rec A = load_rec(rp);
+          Row ra = load_row(bp);
+          for (uint32_t r = 0; r < G.n_rec; r += 2) {
+            const Rec B = load_rec(rp + kRecWords);
+            const Row rb = load_row(bp + 4);
+            R.step(A.w, ra.b, px, py, k2PiHi, k2PiLo);
+            rp += 2 * kRecWords;
+            bp += 8;
+            A = load_rec(rp);
+            ra = load_row(bp);
+            R.step(B.w, rb.b, px, py, k2PiHi, k2PiLo);
+          }
+        } else {
+#pragma unroll
+          for (int m = 0; m < M; ++m) R.acc[m] = orow.b[m / P];
+        }
+        // the output node's activation was applied by its record's tail
+        const float* w = R.acc;
+
+        // grid index of block j's position in this lane
+        auto pos_index = [&](int j) -> uint32_t {
+          const int k = P >= kTileIters ? j / kTileIters : 0;
+          const uint32_t it = P >= kTileIters ? (uint32_t)(j % kTileIters) : (uint32_t)(pass * P + j);
+          return p0[k] + it * kWave + lane;
+        };
+        if constexpr (MODE == kModeRaw) {
+#pragma unroll
+          for (int s = 0; s < S; ++s)
+#pragma unroll
+            for (int j = 0; j < P; ++j)
+              if ((vmask[j] >> lane) & 1ull)
+                raw[(int64_t)G.pair[s] * a.n_pos + pos_index(j)] = w[s * P + j];
+          continue;
+        }
+        // ---- variance of the four siblings (Section 3.2) and the threshold test (Eq. 2), for
+        // all M instances in lockstep. Nearly every quad is dropped, so one test on the maximum
+        // over the instances decides whether any record is kept at all.
+        float s2[M];
+        quad_sumsq_dev<M>(w, s2);
+        float mx = s2[0];
+#pragma unroll
+        for (int m = 1; m < M; ++m) mx = __builtin_fmaxf(mx, s2[m]);
+        const bool some = ballot(mx > a.theta4) != 0ull;
+        if constexpr (MODE == kModeLookback) {
+#pragma unroll
+          for (int s = 0; s < S; ++s)
+#pragma unroll
+            for (int j = 0; j < P; ++j) {
+              const int b = P >= kTileIters ? j : pass * P + j;
+              keep[b][s] = some ? ballot(s2[s * P + j] > a.theta4) & vmask[j] : 0ull;
+              wbuf[b][s] = w[s * P + j];
+            }
+        } else if (some) {
+#pragma unroll
+          for (int s = 0; s < S; ++s) {
+#pragma unroll
+            for (int j = 0; j < P; ++j) {
+              const int k = P >= kTileIters ? j / kTileIters : 0;
+              const uint64_t kb = ballot(s2[s * P + j] > a.theta4) & vmask[j];
+              if (kb == 0ull) continue;
               if ((kb >> lane) & 1ull) {
-                // this tile's records start at its first parent index within the pair
-                const int64_t slot = (int64_t)G.pair[s] * a.cap + (p0 >> 2) + run[s] +
+                // a tile's records start at its first parent index within the pair
+                const int64_t slot = (int64_t)G.pair[s] * a.cap + (p0[k] >> 2) + run[s][k] +
                                      (mbcnt64(kb) >> 2);
-                w4[slot * 4 + (lane & 3u)] = w[m];
-                if ((lane & 3u) == 0) parent[slot] = pidx[j] >> 2;
+                w4[slot * 4 + (lane & 3u)] = w[s * P + j];
+                if ((lane & 3u) == 0) parent[slot] = pos_index(j) >> 2;
               }
-              run[s] += popc64(kb) >> 2;
+              run[s][k] += popc64(kb) >> 2;
             }
           }
         }
       }
-    }
 
-    if constexpr (MODE == kModePadded) {
-      if (lane == 0) {
+      if constexpr (MODE == kModePadded) {
+        if (lane == 0) {
 #pragma unroll
-        for (int s = 0; s < S; ++s) status[(int64_t)G.pair[s] * a.tiles + tile] = run[s];
+          for (int s = 0; s < S; ++s)
+#pragma unroll
+            for (int k = 0; k < TPW; ++k)
+              if (t0 + k < a.tiles) status[(int64_t)G.pair[s] * a.tiles + t0 + k] = run[s][k];
+        }
       }
-    }
-    if constexpr (MODE == kModeLookback) {
-      // ---- the tile learns its exact offset within each pair from the look-back scan
+      if constexpr (MODE == kModeLookback) {
+        // ---- each tile learns its exact offset within each pair from the look-back scan, in
+        // increasing tile order
 #pragma unroll
-      for (int s = 0; s < S; ++s) {
-        uint64_t cnt = 0;
+        for (int k = 0; k < TPW; ++k) {
+          const uint32_t tile = t0 + k;
+          if (tile >= a.tiles) break;
 #pragma unroll
-        for (int it = 0; it < kTileIters; ++it) cnt += popc64(keep[it][s]) >> 2;
-        const uint32_t pair = G.pair[s];
-        uint64_t base = lookback(status + (int64_t)pair * a.tiles, tile, cnt, err);
-        if (tile + 1 == a.tiles && lane == 0) pair_count[pair] = (int64_t)(base + cnt);
-        const int64_t region = (int64_t)pair * a.cap;
+          for (int s = 0; s < S; ++s) {
+            uint64_t cnt = 0;
 #pragma unroll
-        for (int it = 0; it < kTileIters; ++it) {
-          const uint64_t m = keep[it][s];
-          if ((m >> lane) & 1ull) {
-            const int64_t idx = (int64_t)base + (int64_t)(mbcnt64(m) >> 2);
-            if (idx < a.cap) {
-              w4[(region + idx) * 4 + (lane & 3u)] = wbuf[it][s];
-              if ((lane & 3u) == 0)
-                parent[region + idx] = (p0 + (uint32_t)it * kWave + lane) >> 2;
+            for (int it = 0; it < kTileIters; ++it) cnt += popc64(keep[k * kTileIters + it][s]) >> 2;
+            const uint32_t pair = G.pair[s];
+            uint64_t base = lookback(status + (int64_t)pair * a.tiles, tile, cnt, err);
+            if (tile + 1 == a.tiles && lane == 0) {
+              pair_count[pair] = (int64_t)(base + cnt);
+              raise_max(err + 1, (uint32_t)min(base + cnt, (uint64_t)0xFFFFFFFFu));
+            }
+            const int64_t region = (int64_t)pair * a.cap;
+#pragma unroll
+            for (int it = 0; it < kTileIters; ++it) {
+              const uint64_t m = keep[k * kTileIters + it][s];
+              if ((m >> lane) & 1ull) {
+                const int64_t idx = (int64_t)base + (int64_t)(mbcnt64(m) >> 2);
+                if (idx < a.cap) {
+                  w4[(region + idx) * 4 + (lane & 3u)] = wbuf[k * kTileIters + it][s];
+                  if ((lane & 3u) == 0)
+                    parent[region + idx] = (p0[k] + (uint32_t)it * kWave + lane) >> 2;
+                }
+              }
+              base += popc64(m) >> 2;
             }
           }
-          base += popc64(m) >> 2;
         }
       }
     }
@@ -517,33 +563,26 @@ __global__ void __launch_bounds__(kBindWaves * kWave)
   const uint32_t* fold = prog + 4 + 4 * n_un;
   for (uint32_t t = lane; t < n_steps && !bad; t += kWave) {
     float z = __uint_as_float(fold[4 * t + 2]);
-    const uint32_t cnt = fold[4 * t], off = fold[4 * t + 1];
-    if (!edges_ok(off, cnt)) {
+    const uint32_t cnt = fold[4 * t], off = fold[4 * t + 1], rec = fold[4 * t + 3];
+    if (!edges_ok(off, cnt) || rec + 2 >= m.bias_rows) {
       bad = true;
       break;
     }
     const uint32_t* ep = prog + (off - d.uni_off);
     for (uint32_t e = 0; e < cnt; ++e)
       z = __builtin_fmaf(__uint_as_float(ep[2 * e + 1]), U[min(ep[2 * e], 4u + n_un)], z);
-    bias_tab[m.bias_base + 4 * (1 + t)] = z;
+    bias_tab[m.bias_base + 4 * (1 + rec)] = z;
   }
   if (bad) atomicOr(err, kErrTable);
   if (lane == 0) bias_tab[m.bias_base] = out_u == kNone ? 0.0f : U[out_u];
 }
 
 // ------------------------------------------------------------------------ compaction
-// One wave per pair: scans the per-tile counts left by the padded discover pass and moves each
-// tile's records down to their final, contiguous place, tile by tile in increasing order (a
-// tile's destination never overlaps a later tile's records, and each tile's records are all
-// read before any is written). Writes the pair's count.
-__global__ void __launch_bounds__(256)
-    k_compact(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
-              float* __restrict__ w4, int64_t* __restrict__ pair_count, int64_t cap,
-              uint32_t tiles, uint32_t n_pairs, uint32_t head_slots) {
-  const uint32_t lane = lane_id();
-  const uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +
-                                                       threadIdx.x / kWave);
-  if (pair >= n_pairs) return;
+// One pair of the compaction (see k_compact); returns the pair's count.
+__device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
+                                 float* __restrict__ w4, int64_t* __restrict__ pair_count,
+                                 int64_t cap, uint32_t tiles, uint32_t pair, uint32_t head_slots,
+                                 uint32_t lane) {
   const uint64_t* row = counts + (int64_t)pair * tiles;
   const int64_t region = (int64_t)pair * cap;
   uint32_t running = 0;
@@ -576,6 +615,38 @@ __global__ void __launch_bounds__(256)
     running += __builtin_amdgcn_readlane(incl, n_here - 1);
   }
   if (lane == 0) pair_count[pair] = running;
+  return running;
+}
+
+// Each wave takes pairs pair = wave, wave + n_waves, ...: scans the per-tile counts left by the
+// padded discover pass and moves each tile's records down to their final, contiguous place,
+// tile by tile in increasing order (a tile's destination never overlaps a later tile's records,
+// and each tile's records are all read before any is written), and writes the pair's count. The
+// workgroup's largest count is then raised into *max_count with one atomic.
+constexpr int kCompactWaves = 4;
+
+__global__ void __launch_bounds__(kCompactWaves * kWave)
+    k_compact(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
+              float* __restrict__ w4, int64_t* __restrict__ pair_count,
+              uint32_t* __restrict__ max_count, int64_t cap, uint32_t tiles, uint32_t n_pairs,
+              uint32_t head_slots) {
+  __shared__ uint32_t wave_max[kCompactWaves];
+  const uint32_t lane = lane_id();
+  const uint32_t wv = threadIdx.x / kWave;
+  const uint32_t n_waves = gridDim.x * kCompactWaves;
+  uint32_t my_max = 0;
+  for (uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * kCompactWaves + wv);
+       pair < n_pairs; pair += n_waves) {
+    my_max = max(my_max, compact_pair(counts, parent, w4, pair_count, cap, tiles, pair,
+                                      head_slots, lane));
+  }
+  if (lane == 0) wave_max[wv] = my_max;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t m = 0;
+    for (int k = 0; k < kCompactWaves; ++k) m = max(m, wave_max[k]);
+    raise_max(max_count, m);
+  }
 }
 
 // ------------------------------------------------------------------------ small kernels
@@ -630,20 +701,45 @@ extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
 template <int S, int W, int MODE>
 static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks, hipStream_t s) {
   constexpr int P = emr::positions_per_lane(S, W);
-  emr::DiscoverScalars sc{a->cap,     a->n_pos,      a->tiles,  a->n_tiles,    a->depth,
-                          a->theta,   a->blob_words, a->n_pairs, a->bias_floats};
+  constexpr int TPW = P >= emr::kTileIters ? P / emr::kTileIters : 1;
   auto kern = emr::k_discover<S, P, W, MODE>;
-  // Clamp the grid to what can be resident at once: the waves walk their tiles. The look-back mode
-  // is launched cooperatively (the runtime refuses a grid that cannot be resident all at once),
-  // which its forward progress relies on; the other modes have no dependences between waves.
-  int per_cu = 0, dev = 0, cus = 0;
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, 0);
-  if (e != hipSuccess) return e;
+  int dev = 0, cus = 0;
+  hipError_t e;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
     return e;
-  const uint32_t resident = (uint32_t)(per_cu > 0 ? per_cu : 1) * (uint32_t)(cus > 0 ? cus : 1);
+  if (cus <= 0) cus = 1;
+  // Workgroups of this kernel that fit on one CU (a property of the compiled kernel).
+  static const int per_cu = [&] {
+    int n = 0;
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, 256, 0) == hipSuccess && n > 0
+               ? n
+               : 1;
+  }();
+  // Chunks of 4 tiles when the launch has work for at least 4 such chunks per SIMD; else each
+  // chunk is one walk's worth of tiles, for parallelism.
+  const uint32_t chunk =
+      (uint64_t)a->n_groups * a->tiles >= 16ull * 4ull * (uint64_t)cus ? 4u : (uint32_t)TPW;
+  const uint32_t cpg = (a->tiles + chunk - 1) / chunk;
+  emr::DiscoverScalars sc{a->cap,
+                          a->n_pos,
+                          a->tiles,
+                          a->n_groups * cpg,
+                          cpg,
+                          chunk,
+                          a->depth,
+                          4.0f * a->theta,
+                          a->blob_words,
+                          a->n_pairs,
+                          (uint32_t)a->bias_floats};
+  // Clamp the grid to what can be resident at once: the waves walk their chunks. The look-back
+  // mode is launched cooperatively (the runtime refuses a grid that cannot be resident all at
+  // once), which its forward progress relies on; the other modes have no dependences between waves.
+  const uint32_t resident = (uint32_t)per_cu * (uint32_t)cus;
+  const uint32_t needed = (sc.n_chunks + 3) / 4;  // one wave per chunk, 4 waves per workgroup
+  if (blocks > needed) blocks = needed;
   if (blocks > resident) blocks = resident;
+  if (blocks == 0) return hipSuccess;
   const uint32_t* blob = a->blob;
   const emr::Group* groups = a->groups;
   const float* bias_tab = a->bias_tab;
@@ -676,8 +772,9 @@ static hipError_t launch_discover_w(const emr::DiscoverArgs* a, int window, uint
   return hipErrorInvalidValue;
 }
 
-// blocks: requested number of 256-thread workgroups (4 waves each), clamped to what can be
-// resident at once; every wave walks its share of the tiles.
+// blocks: the most 256-thread workgroups (4 waves each) to launch; the launch uses at most one
+// wave per chunk of tiles and no more workgroups than can be resident at once; every wave walks its
+// share of the chunks.
 // mode: 0 raw outputs, 1 padded records (then emr_launch_compact), 2 look-back records.
 extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int window, int mode,
                                           uint32_t blocks, hipStream_t s) {
@@ -691,10 +788,14 @@ extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int window
 }
 
 extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
-                                         int64_t* pair_count, int64_t cap, uint32_t tiles,
-                                         uint32_t n_pairs, uint32_t head_slots, hipStream_t s) {
+                                         int64_t* pair_count, uint32_t* max_count, int64_t cap,
+                                         uint32_t tiles, uint32_t n_pairs, uint32_t head_slots,
+                                         hipStream_t s) {
   if (n_pairs == 0) return hipSuccess;
-  hipLaunchKernelGGL(emr::k_compact, dim3((n_pairs + 3) / 4), dim3(256), 0, s, counts, parent, w4,
-                     pair_count, cap, tiles, n_pairs, head_slots);
+  uint32_t blocks = (n_pairs + emr::kCompactWaves - 1) / emr::kCompactWaves;
+  if (blocks > 512) blocks = 512;  // waves loop over pairs beyond this
+  hipLaunchKernelGGL(emr::k_compact, dim3(blocks), dim3(emr::kCompactWaves * emr::kWave), 0, s,
+                     counts, parent, w4,
+                     pair_count, max_count, cap, tiles, n_pairs, head_slots);
   return hipGetLastError();
 }

@@ -224,8 +224,10 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
     d.flags = (out_varying ? 1u : 0u) | ((uint32_t)window << 8);
     d.pad[0] = d.pad[1] = 0;
     uint32_t n_rec = 0;
+    std::vector<uint32_t> first_rec(vsteps.size(), 0);  // record index of each node's first record
     for (int t = 0; t < (int)vsteps.size(); ++t) {
       const int v = vsteps[t];
+      first_rec[t] = n_rec;
       float ax = 0.0f, ay = 0.0f;
       std::vector<std::pair<uint32_t, float>> node_edges;  // (source slot, w) in edge-list order
       for (int ei : in_edges[v]) {
@@ -318,7 +320,7 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       r[0] = cnt;
       r[1] = first;
       r[2] = fbits(g.bias ? g.bias[v] : 0.0f);
-      r[3] = 0;
+      r[3] = first_rec[t];
     }
     d.uni_end = (uint32_t)blob.size();
     inf.n_unodes = (int)unodes.size();

@@ -3,9 +3,12 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <memory>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -20,8 +23,9 @@ extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s);
 extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int window, int mode,
                                           uint32_t blocks, hipStream_t s);
 extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
-                                         int64_t* pair_count, int64_t cap, uint32_t tiles,
-                                         uint32_t n_pairs, uint32_t head_slots, hipStream_t s);
+                                         int64_t* pair_count, uint32_t* max_count, int64_t cap,
+                                         uint32_t tiles, uint32_t n_pairs, uint32_t head_slots,
+                                         hipStream_t s);
 
 namespace {
 
@@ -45,12 +49,18 @@ emr_status fail(emr_status st, const char* fmt, ...) {
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Compute units of the current device, queried once per device.
 int device_cu_count() {
+  static std::atomic<int> cached[64];
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 256;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+  if (dev >= 0 && dev < 64 && cached[dev].load(std::memory_order_relaxed) > 0)
+    return cached[dev].load(std::memory_order_relaxed);
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
     return 256;
-  return cus > 0 ? cus : 256;
+  if (dev >= 0 && dev < 64) cached[dev].store(cus, std::memory_order_relaxed);
+  return cus;
 }
 
 // Pinned staging for the small per-call tables; reused once the previous copy has finished.
@@ -86,6 +96,39 @@ emr_status stage_upload(const void* src, size_t bytes, void* dev_dst, hipStream_
   return EMR_OK;
 }
 
+// Streams a call's discover launches run on besides the caller's: one launch per bucket (sources
+// per lane, register window), forked from the caller's stream after the bind kernel and joined
+// back before compaction, so a bucket with little work runs alongside the others instead of after
+// them. Per thread and device; created on first use at default priority.
+constexpr int kAuxStreams = 3;
+struct StreamPool {
+  int device = -1;
+  hipStream_t aux[kAuxStreams] = {};
+  hipEvent_t fork = nullptr;
+  hipEvent_t join[kAuxStreams] = {};
+};
+thread_local std::vector<StreamPool> g_pools;
+
+emr_status stream_pool(StreamPool** out) {
+  int dev = 0;
+  HIP_OR_FAIL(hipGetDevice(&dev));
+  for (StreamPool& p : g_pools)
+    if (p.device == dev) {
+      *out = &p;
+      return EMR_OK;
+    }
+  StreamPool p;
+  p.device = dev;
+  for (int i = 0; i < kAuxStreams; ++i) {
+    HIP_OR_FAIL(hipStreamCreateWithFlags(&p.aux[i], hipStreamNonBlocking));
+    HIP_OR_FAIL(hipEventCreateWithFlags(&p.join[i], hipEventDisableTiming));
+  }
+  HIP_OR_FAIL(hipEventCreateWithFlags(&p.fork, hipEventDisableTiming));
+  g_pools.push_back(p);
+  *out = &g_pools.back();
+  return EMR_OK;
+}
+
 // Per-thread profiling of the discover-kernel launches.
 struct Profiler {
   bool on = false;
@@ -107,6 +150,10 @@ double query_slots(const emr::GenomeInfo& inf, double rT) {
 
 }  // namespace
 
+namespace {
+struct Plan;
+}
+
 struct emr_population {
   int32_t n_genomes = 0;
   std::vector<emr::ProgDesc> desc;      // [2 * n_genomes]
@@ -114,6 +161,9 @@ struct emr_population {
   uint32_t* d_blob = nullptr;
   emr::ProgDesc* d_desc = nullptr;
   size_t blob_words = 0;
+  // The plan of the last call (see plan_for): calls with the same sources and depth reuse it.
+  mutable std::mutex plan_mu;
+  mutable std::shared_ptr<const Plan> plan;
 };
 
 namespace {
@@ -132,6 +182,7 @@ struct Plan {
   struct Bucket {
     int S, window;
     uint32_t first, count;
+    double cost;  // summed per-query cost of its groups' programs (launch order)
   };
   std::vector<emr::Group> groups;
   std::vector<Bucket> buckets;
@@ -139,8 +190,16 @@ struct Plan {
   std::vector<uint32_t> group_member0;  // index of each group's first member
   std::vector<float> src_xy;
   uint64_t bias_floats = 0;
+  // Host image of the per-call tables (groups, members, source coordinates), uploaded to
+  // [off_groups, off_bias) of the workspace.
+  std::vector<char> img;
+  // What the plan was built for (exact copies, compared on reuse).
+  std::vector<emr_source> key_sources;
+  std::vector<int32_t> key_offs;
+  bool key_has_offs = false;
+  int32_t key_n_shared = 0;
   // Workspace layout (bytes from the workspace start).
-  size_t off_err = 0;      // 64 words: [0] error flags
+  size_t off_err = 0;      // 64 words: [0] error flags, [1] largest pair count (saturating)
   size_t off_status = 0;
   size_t off_groups = 0, off_members = 0, off_srcxy = 0, off_bias = 0, total = 0;
   size_t zero_bytes = 0;   // prefix cleared before each call
@@ -231,8 +290,9 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
   for (size_t i = 0; i < tmp.size(); ++i) {
     TmpGroup& t = tmp[i];
     if (P.buckets.empty() || P.buckets.back().S != t.S || P.buckets.back().window != t.window)
-      P.buckets.push_back({t.S, t.window, (uint32_t)i, 0});
+      P.buckets.push_back({t.S, t.window, (uint32_t)i, 0, 0.0});
     P.buckets.back().count++;
+    P.buckets.back().cost += t.S * cost[t.desc];
     t.g.bias_off = (uint32_t)bias;
     P.group_member0.push_back((uint32_t)P.members.size());
     const uint32_t rows = t.g.n_rec + 2;  // output row, one per record at most, prefetch row
@@ -242,6 +302,10 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
     P.groups.push_back(t.g);
   }
   if (bias > 0xFFFFFFFFull) return fail(EMR_E_LIMIT, "bias table too large");
+  // Launch order: the costliest bucket first (it goes on the caller's stream and starts at once;
+  // the others run alongside it as it drains).
+  std::stable_sort(P.buckets.begin(), P.buckets.end(),
+                   [](const Plan::Bucket& a, const Plan::Bucket& b) { return a.cost > b.cost; });
   if ((int)P.buckets.size() > kMaxBuckets) return fail(EMR_E_LIMIT, "too many buckets");
   for (const auto& b : P.buckets)
     if ((uint64_t)b.count * (uint64_t)P.tiles > 0xFFFFFFFFull)
@@ -261,6 +325,55 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
   P.off_srcxy = align256(P.off_members + P.members.size() * sizeof(emr::Member));
   P.off_bias = align256(P.off_srcxy + P.src_xy.size() * sizeof(float));
   P.total = align256(P.off_bias + P.bias_floats * sizeof(float));
+  P.img.assign(P.off_bias - P.off_groups, 0);
+  if (!P.groups.empty())
+    std::memcpy(P.img.data(), P.groups.data(), P.groups.size() * sizeof(emr::Group));
+  if (!P.members.empty())
+    std::memcpy(P.img.data() + (P.off_members - P.off_groups), P.members.data(),
+                P.members.size() * sizeof(emr::Member));
+  if (!P.src_xy.empty())
+    std::memcpy(P.img.data() + (P.off_srcxy - P.off_groups), P.src_xy.data(),
+                P.src_xy.size() * sizeof(float));
+  P.key_sources.assign(sources, sources + n_sources);
+  P.key_has_offs = offs != nullptr;
+  if (offs) P.key_offs.assign(offs, offs + G + 1);
+  P.key_n_shared = n_shared;
+  return EMR_OK;
+}
+
+bool plan_matches(const Plan& P, const emr_source* sources, int32_t n_sources, const int32_t* offs,
+                  int32_t n_shared, int32_t depth, int32_t n_genomes) {
+  if (P.depth != depth || (int64_t)P.key_sources.size() != n_sources ||
+      P.key_has_offs != (offs != nullptr) || P.key_n_shared != n_shared)
+    return false;
+  if (n_sources > 0 &&
+      std::memcmp(P.key_sources.data(), sources, sizeof(emr_source) * (size_t)n_sources) != 0)
+    return false;
+  return !offs ||
+         std::memcmp(P.key_offs.data(), offs, sizeof(int32_t) * (size_t)(n_genomes + 1)) == 0;
+}
+
+// The plan for these sources and depth: the population's last plan when it was built for exactly
+// the same arguments, else a new one (which then replaces it). Planning is host work that depends
+// only on the population, the sources and the depth; every call still runs all kernels.
+emr_status plan_for(const emr_population* pop, const emr_source* sources, int32_t n_sources,
+                    const int32_t* offs, int32_t n_shared, int32_t depth,
+                    std::shared_ptr<const Plan>* out) {
+  if (!pop) return fail(EMR_E_INVAL, "population is NULL");
+  {
+    std::lock_guard<std::mutex> lock(pop->plan_mu);
+    if (pop->plan && (n_sources == 0 || sources) && n_sources >= 0 &&
+        plan_matches(*pop->plan, sources, n_sources, offs, n_shared, depth, pop->n_genomes)) {
+      *out = pop->plan;
+      return EMR_OK;
+    }
+  }
+  auto P = std::make_shared<Plan>();
+  emr_status st = build_plan(pop, sources, n_sources, offs, n_shared, depth, P.get());
+  if (st != EMR_OK) return st;
+  std::lock_guard<std::mutex> lock(pop->plan_mu);
+  pop->plan = P;
+  *out = P;
   return EMR_OK;
 }
 
@@ -273,19 +386,7 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
   if (((uintptr_t)workspace & 255) != 0) return fail(EMR_E_INVAL, "workspace not 256-byte aligned");
   char* ws = (char*)workspace;
   HIP_OR_FAIL(emr_launch_fill(ws, (int64_t)(P.zero_bytes / 4), 0u, s));
-  // One host image for groups, members and source coordinates.
-  const size_t tab_bytes = P.off_bias - P.off_groups;
-  std::vector<char> img(tab_bytes, 0);
-  if (!P.groups.empty())
-    std::memcpy(img.data() + (P.off_groups - P.off_groups), P.groups.data(),
-                P.groups.size() * sizeof(emr::Group));
-  if (!P.members.empty())
-    std::memcpy(img.data() + (P.off_members - P.off_groups), P.members.data(),
-                P.members.size() * sizeof(emr::Member));
-  if (!P.src_xy.empty())
-    std::memcpy(img.data() + (P.off_srcxy - P.off_groups), P.src_xy.data(),
-                P.src_xy.size() * sizeof(float));
-  emr_status st = stage_upload(img.data(), tab_bytes, ws + P.off_groups, s);
+  emr_status st = stage_upload(P.img.data(), P.img.size(), ws + P.off_groups, s);
   if (st != EMR_OK) return st;
 
   emr::BindArgs b{};
@@ -316,8 +417,24 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
       prof.events.push_back(e);
     }
   }
+  // Look-back launches are cooperative and stay on the caller's stream, one after the other.
+  const bool fork = mode != 2 && P.buckets.size() > 1;
+  StreamPool* pool = nullptr;
+  bool aux_used[kAuxStreams] = {};
+  if (fork) {
+    emr_status pst = stream_pool(&pool);
+    if (pst != EMR_OK) return pst;
+    HIP_OR_FAIL(hipEventRecord(pool->fork, s));
+  }
   for (size_t bi = 0; bi < P.buckets.size(); ++bi) {
     const Plan::Bucket& bk = P.buckets[bi];
+    hipStream_t ls = s;
+    if (fork && bi > 0) {
+      const int k = (int)((bi - 1) % kAuxStreams);
+      ls = pool->aux[k];
+      if (!aux_used[k]) HIP_OR_FAIL(hipStreamWaitEvent(ls, pool->fork, 0));
+      aux_used[k] = true;
+    }
     emr::DiscoverArgs a{};
     a.blob = pop->d_blob;
     a.groups = (const emr::Group*)(ws + P.off_groups) + bk.first;
@@ -339,15 +456,15 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
     a.blob_words = (uint32_t)pop->blob_words;
     a.n_pairs = (uint32_t)P.n_pairs;
     a.bias_floats = P.bias_floats;
-    const uint64_t want = ((uint64_t)a.n_tiles + 3) / 4;
-    const uint32_t blocks = (uint32_t)std::min<uint64_t>(want, (uint64_t)cus * 16);
-    if (prof.on) HIP_OR_FAIL(hipEventRecord(prof.events[2 * bi], s));
-    HIP_OR_FAIL(emr_launch_discover(&a, bk.window, mode, blocks, s));
+    const uint32_t blocks = (uint32_t)cus * 16;  // the launcher sizes the grid below this
+    if (prof.on) HIP_OR_FAIL(hipEventRecord(prof.events[2 * bi], ls));
+    HIP_OR_FAIL(emr_launch_discover(&a, bk.window, mode, blocks, ls));
     if (prof.on) {
-      HIP_OR_FAIL(hipEventRecord(prof.events[2 * bi + 1], s));
+      HIP_OR_FAIL(hipEventRecord(prof.events[2 * bi + 1], ls));
       emr_launch_profile r{};
       r.group_size = bk.S;
       r.window = bk.window;
+      r.positions = emr::positions_per_lane(bk.S, bk.window);
       r.tiles = a.n_tiles;
       const double npos = (double)a.n_pos;
       for (uint32_t k = 0; k < bk.count; ++k) {
@@ -359,10 +476,16 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
       prof.recs.push_back(r);
     }
   }
+  if (fork)
+    for (int k = 0; k < kAuxStreams; ++k)
+      if (aux_used[k]) {
+        HIP_OR_FAIL(hipEventRecord(pool->join[k], pool->aux[k]));
+        HIP_OR_FAIL(hipStreamWaitEvent(s, pool->join[k], 0));
+      }
   if (padded && P.n_pairs > 0)
     HIP_OR_FAIL(emr_launch_compact(
         (const uint64_t*)(ws + P.off_status), out->parent, out->w4, out->pair_count,
-        out->pair_capacity, (uint32_t)P.tiles, (uint32_t)P.n_pairs,
+        (uint32_t*)(ws + P.off_err) + 1, out->pair_capacity, (uint32_t)P.tiles, (uint32_t)P.n_pairs,
         (uint32_t)(P.depth < emr::kFirstAlignedLevel ? emr::n_parents(P.depth)
                                                      : emr::level_offset(emr::kFirstAlignedLevel) / 4),
         s));
@@ -469,9 +592,10 @@ emr_status emr_workspace_bytes(const emr_population* pop, const emr_source* sour
                                int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
                                int32_t depth, int64_t* bytes) {
   if (!bytes) return fail(EMR_E_INVAL, "bytes is NULL");
-  Plan P;
-  emr_status st = build_plan(pop, sources, n_sources, src_offsets, n_shared, depth, &P);
+  std::shared_ptr<const Plan> plan;
+  emr_status st = plan_for(pop, sources, n_sources, src_offsets, n_shared, depth, &plan);
   if (st != EMR_OK) return st;
+  const Plan& P = *plan;
   *bytes = (int64_t)P.total;
   return EMR_OK;
 }
@@ -480,9 +604,10 @@ emr_status emr_discover(const emr_population* pop, const emr_source* sources, in
                         const int32_t* src_offsets, int32_t n_shared, int32_t depth, float theta,
                         const emr_result* out, void* stream) {
   if (!out) return fail(EMR_E_INVAL, "out is NULL");
-  Plan P;
-  emr_status st = build_plan(pop, sources, n_sources, src_offsets, n_shared, depth, &P);
+  std::shared_ptr<const Plan> plan;
+  emr_status st = plan_for(pop, sources, n_sources, src_offsets, n_shared, depth, &plan);
   if (st != EMR_OK) return st;
+  const Plan& P = *plan;
   if (out->pair_capacity < 0) return fail(EMR_E_INVAL, "pair_capacity < 0");
   if (P.n_pairs > 0) {
     if (!out->pair_count) return fail(EMR_E_INVAL, "pair_count is NULL");
@@ -499,14 +624,18 @@ emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max
                             void* stream) {
   if (!out || n_pairs < 0) return fail(EMR_E_INVAL, "bad arguments");
   HIP_OR_FAIL(hipStreamSynchronize((hipStream_t)stream));
-  uint32_t err = 0;
-  if (out->workspace) HIP_OR_FAIL(hipMemcpy(&err, out->workspace, 4, hipMemcpyDeviceToHost));
+  // Workspace words 0 and 1: the error flags and the largest pair count of the call.
+  uint32_t w2[2] = {0, 0};
   int64_t mx = 0;
-  if (n_pairs > 0) {
+  if (out->workspace) {
+    HIP_OR_FAIL(hipMemcpy(w2, out->workspace, 8, hipMemcpyDeviceToHost));
+    mx = w2[1];
+  } else if (n_pairs > 0) {
     std::vector<int64_t> cnt((size_t)n_pairs);
     HIP_OR_FAIL(hipMemcpy(cnt.data(), out->pair_count, (size_t)n_pairs * 8, hipMemcpyDeviceToHost));
     for (int64_t c : cnt) mx = std::max(mx, c);
   }
+  const uint32_t err = w2[0];
   if (max_count) *max_count = mx;
   if (err)
     return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (1: look-back wait bound, 2: a "
@@ -520,9 +649,10 @@ emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max
 emr_status emr_eval_raw(const emr_population* pop, const emr_source* sources, int32_t n_sources,
                         const int32_t* src_offsets, int32_t n_shared, int32_t depth, float* out_dev,
                         void* workspace, int64_t workspace_bytes, void* stream) {
-  Plan P;
-  emr_status st = build_plan(pop, sources, n_sources, src_offsets, n_shared, depth, &P);
+  std::shared_ptr<const Plan> plan;
+  emr_status st = plan_for(pop, sources, n_sources, src_offsets, n_shared, depth, &plan);
   if (st != EMR_OK) return st;
+  const Plan& P = *plan;
   if (P.n_pairs > 0 && emr::n_positions(depth) > 0 && !out_dev)
     return fail(EMR_E_INVAL, "out_dev is NULL");
   return run_plan(pop, P, 0.0f, nullptr, out_dev, workspace, workspace_bytes, (hipStream_t)stream);
@@ -532,9 +662,10 @@ emr_status emr_discover_cost(const emr_population* pop, const emr_source* source
                              int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
                              int32_t depth, double transcendental_slots, double* slots,
                              double* queries) {
-  Plan P;
-  emr_status st = build_plan(pop, sources, n_sources, src_offsets, n_shared, depth, &P);
+  std::shared_ptr<const Plan> plan;
+  emr_status st = plan_for(pop, sources, n_sources, src_offsets, n_shared, depth, &plan);
   if (st != EMR_OK) return st;
+  const Plan& P = *plan;
   const double npos = (double)emr::n_positions(depth);
   double total = 0.0;
   for (const emr::Member& m : P.members) total += query_slots(pop->info[m.desc], transcendental_slots) * npos;

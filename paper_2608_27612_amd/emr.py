@@ -52,8 +52,9 @@ class emr_result(C.Structure):
 
 
 class emr_launch_profile(C.Structure):
-    _fields_ = [("group_size", C.c_int32), ("window", C.c_int32), ("tiles", C.c_int64),
-                ("queries", C.c_int64), ("slots", C.c_double), ("ms", C.c_float)]
+    _fields_ = [("group_size", C.c_int32), ("window", C.c_int32), ("positions", C.c_int32),
+                ("reserved", C.c_int32), ("tiles", C.c_int64), ("queries", C.c_int64),
+                ("slots", C.c_double), ("ms", C.c_float)]
 
 
 _lib = None
@@ -312,5 +313,6 @@ def emr_profile_read():
     _check(lib().emr_profile_read(None, 0, C.byref(n)))
     arr = (emr_launch_profile * max(1, n.value))()
     _check(lib().emr_profile_read(arr, n.value, C.byref(n)))
-    return [{"S": r.group_size, "W": r.window, "tiles": r.tiles, "queries": r.queries,
-             "slots": r.slots, "ms": r.ms} for r in arr[:n.value]]
+    return [{"S": r.group_size, "W": r.window, "P": r.positions, "tiles": r.tiles,
+             "queries": r.queries, "first": i == 0,
+             "slots": r.slots, "ms": r.ms} for i, r in enumerate(arr[:n.value])]

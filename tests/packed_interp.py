@@ -95,6 +95,7 @@ def interpret(blob, desc, dir_, sx, sy, px, py):
         U[5 + k] = _act(act, np.float64(z))
     fold = rec + 4 * n_un
     folded = []
+    fold_rec = [int(blob[fold + 4 * t + 3]) for t in range(n_steps)]
     for t in range(n_steps):
         nf, fo, bb = int(blob[fold + 4 * t]), int(blob[fold + 4 * t + 1]), int(blob[fold + 4 * t + 2])
         z = f32(bb)
@@ -122,6 +123,7 @@ def interpret(blob, desc, dir_, sx, sy, px, py):
             continue
         if first:
             assert acc is None, "a node starts before the previous one ended"
+            assert fold_rec[step] == r, "the node's bias row is not its first record's"
             acc = folded[step] + f32(w[1]) * px + f32(w[2]) * py
         else:
             assert acc is not None and w[1] == 0 and w[2] == 0

@@ -44,12 +44,13 @@ def pair_genome_source(r, genomes, sources, offs):
     return genomes[g], sources[r]
 
 
-def check_discover(emr, genomes, sources, D, theta, offs=None, cap=None):
+def check_discover(emr, genomes, sources, D, theta, offs=None, cap=None, pop=None):
     """Runs the GPU path and the oracle; asserts parity; returns summary stats."""
     theta32 = float(np.float32(theta))
-    pop = emr.emr_pack_population(genomes)
+    if pop is None:
+        pop = emr.emr_pack_population(genomes)
     res = emr.emr_discover(pop, sources, D, theta32, src_offsets=offs, pair_capacity=cap)
-    emr.emr_result_check(res)
+    mx = emr.emr_result_check(res)
     counts, recs = emr.records_to_host(res)
     o = oracle.discover(genomes, sources, D, theta32, src_offsets=offs)
     assert len(counts) == len(o["pair_count"])
@@ -71,6 +72,7 @@ def check_discover(emr, genomes, sources, D, theta, offs=None, cap=None):
         n_band += len(diff)
         common, gi, oi = np.intersect1d(gp, op, return_indices=True)
         assert close(gw[gi], ow[oi]).all()
+    assert mx == (int(counts.max()) if len(counts) else 0)
     return {"records": int(np.sum(np.minimum(counts, res["pair_capacity"]))), "band": n_band,
             "counts": counts}
 
@@ -211,6 +213,20 @@ def test_empty_population_and_no_sources(emr):
     pop0 = emr.emr_pack_population([])
     res = emr.emr_discover(pop0, W.xor_sources(), 5, 0.03)
     assert emr.emr_result_check(res) == 0
+
+
+def test_one_population_many_calls(emr):
+    """A population serves calls with different sources, source layouts and depths in any
+    order; each call must be planned for its own arguments."""
+    genomes = W.population(21, 24, 20, 60)
+    pop = emr.emr_pack_population(genomes)
+    xs, ts = W.xor_sources(), W.tabular_sources(8)
+    offs = np.array([0] + list(np.cumsum([2 + g % 3 for g in range(len(genomes))])), np.int32)
+    csr = np.concatenate([ts[-(2 + g % 3):] if g % 2 else ts[: 2 + g % 3]
+                          for g in range(len(genomes))])
+    for D, srcs, o in [(5, xs, None), (4, xs, None), (5, ts, None), (5, xs, None),
+                       (4, csr, offs), (5, csr, offs), (5, xs, None)]:
+        check_discover(emr, genomes, srcs, D, 0.03, offs=o, pop=pop)
 
 
 def test_capacity_overflow_is_reported(emr):
