@@ -174,6 +174,47 @@ emr_status emr_discover(const emr_population* pop, const emr_source* sources, in
 emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max_count,
                             void* stream);
 
+/* ------------------------------------------------------------------ streaming
+ * Deep runs stream their output between device and host memory (Section 5.2: the depth-7 note of
+ * the per-generation timing table and the depth 8..13 runs of the total-runtime figure; Section 6
+ * on depth 13). Here the stream carries only the compacted records, chunk by chunk. */
+
+/* Receives the records of one pair for one chunk: n_records (> 0) kept parent cells in ascending
+ * order, parent[i] their heap indices and w4[4 i + k] the CPPN outputs at their children. The
+ * pointers are host memory owned by the library (pinned staging) and valid only during the call.
+ * Return 0 to continue; any other value stops the run before these records count as delivered. */
+typedef int32_t (*emr_sink)(int64_t pair, int64_t chunk, const uint32_t* parent, const float* w4,
+                            int64_t n_records, void* user);
+
+/* Number of chunks a streamed call at this depth and chunk size has. A chunk is a run of
+ * chunk_positions / 256 tiles of every pair; a tile is 256 grid positions of one level, except
+ * the first tile, which holds levels 1..3 (84 positions). chunk_positions must be a positive
+ * multiple of 256. Host only. */
+emr_status emr_stream_chunks(int32_t depth, int64_t chunk_positions, int64_t* n_chunks);
+
+/*
+ * Eager discovery in chunks, for depths whose output does not fit one device buffer: for chunk
+ * c = 0, 1, ... (see emr_stream_chunks) every pair's kept parents whose children lie in the chunk
+ * are found exactly as by emr_discover, then passed to `sink` once per (chunk, pair) with records,
+ * chunk after chunk and pair after pair, each pair's records in ascending parent order. So the
+ * concatenation over chunks of a pair's records equals its emr_discover output.
+ * Work and delivery overlap: the GPU computes chunk c + 1 on `stream` while the records of chunk c
+ * are copied to pinned host memory on a library side stream and delivered.
+ * Cursor: deliveries are numbered k = chunk * n_pairs + pair. The run starts at cursor `start`
+ * (0 for a full run; deliveries below it are skipped), and *next (may be NULL) receives the
+ * cursor to resume from: n_chunks * n_pairs after a complete run, or, when the sink returns
+ * nonzero, the cursor of the delivery it refused (status EMR_E_ABORTED). Returns when done.
+ * Device memory: the library allocates the workspace and three record buffers of
+ * n_pairs * min(64 chunk_positions / 256, Q(D)) records (20 bytes each) for the call and frees
+ * them before returning; EMR_E_LIMIT if they would exceed 48 GiB (use smaller chunks).
+ * Errors: EMR_E_INVAL for bad arguments (checked before any GPU work), EMR_E_NOMEM, EMR_E_DEVICE
+ * (also when a kernel flagged an internal error), EMR_E_ABORTED.
+ */
+emr_status emr_discover_stream(const emr_population* pop, const emr_source* sources,
+                               int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                               int32_t depth, float theta, int64_t chunk_positions, int64_t start,
+                               emr_sink sink, void* user, int64_t* next, void* stream);
+
 /*
  * Raw CPPN outputs (debug and parity): out_dev[r * N(D) + p] = CPPN output of pair r at grid
  * position p (device, caller-owned, n_pairs * N(D) floats). Same arithmetic as emr_discover.

@@ -142,6 +142,14 @@ EMR_HD inline int64_t tiles_per_pair(int depth) {
   return 1 + (n_positions(depth) - level_offset(kFirstAlignedLevel)) / kTile;
 }
 
+// First parent index of a pair's tile T (T = tiles_per_pair(depth) gives n_parents(depth)): tile 0
+// holds the parents of levels 0..2 (or all of them when the depth is smaller), every other tile 64.
+EMR_HD inline int64_t tile_parent_offset(int64_t T, int depth) {
+  if (T == 0) return 0;
+  if (depth < kFirstAlignedLevel) return n_parents(depth);
+  return level_offset(kFirstAlignedLevel) / 4 + (T - 1) * (kTile / 4);
+}
+
 struct DiscoverArgs {
   const uint32_t* blob;
   const Group* groups;
@@ -155,7 +163,9 @@ struct DiscoverArgs {
   int64_t cap;             // records per pair region
   int64_t n_pos;           // N(depth)
   uint32_t n_groups;
-  uint32_t tiles;          // tiles per pair
+  uint32_t tile_lo;        // first tile of the launch (of every pair)
+  uint32_t parent_lo;      // first parent index of tile tile_lo (record slots count from it)
+  uint32_t tiles;          // tiles of the launch per pair
   uint32_t n_tiles;        // n_groups * tiles
   int32_t depth;
   float theta;

@@ -166,6 +166,9 @@ __device__ uint64_t lookback(uint64_t* row, uint32_t tile, uint64_t count, uint3
 // loads through the scalar cache.
 struct DiscoverScalars {
   int64_t cap, n_pos;
+  // The launch covers tiles tile_lo .. tile_lo + tiles - 1 of every pair; record slots of a pair
+  // region count from parent_lo, the first parent index of tile tile_lo.
+  uint32_t tile_lo, parent_lo;
   uint32_t tiles, n_chunks, chunks_per_group, chunk_tiles;
   int32_t depth;
   float theta4;  // 4 theta
@@ -277,7 +280,8 @@ __global__ void __launch_bounds__(256)
     const Row orow = load_row(cbias + G.bias_off);  // row 0: output constants (uniform output)
 
     for (uint32_t t0 = chunk_tile; t0 < chunk_tile + a.chunk_tiles && t0 < a.tiles; t0 += TPW) {
-      // ---- geometry of the walk's tiles. Tile 0 holds levels 1..3 (84 positions); every other
+      // ---- geometry of the walk's tiles (t0 counts from the launch's first tile, tile_lo). The
+      // pair's tile 0 holds levels 1..3 (84 positions); every other
       // tile 256 positions of one level, starting at Morton index m0 of level lvl. m0 is a
       // multiple of 256, so the tile's 64-position blocks it = 0..3 have Morton prefixes
       // (m0 >> 6) | it, whose column and row bits are those of m0 >> 6 with it's two bits or-ed in.
@@ -285,12 +289,13 @@ __global__ void __launch_bounds__(256)
       float scale[TPW];
 #pragma unroll
       for (int k = 0; k < TPW; ++k) {
-        const uint32_t tile = t0 + k;
+        const uint32_t tile = a.tile_lo + t0 + k;  // the pair's tile index
+        const bool in_range = t0 + k < a.tiles;
         p0[k] = 0;
-        n_valid[k] = tile == 0 ? head_len : (tile < a.tiles ? (uint32_t)kTile : 0u);
+        n_valid[k] = !in_range ? 0u : (tile == 0 ? head_len : (uint32_t)kTile);
         scale[k] = 1.0f;
         cx[k] = cy[k] = 0;
-        if (tile != 0 && tile < a.tiles) {
+        if (tile != 0 && in_range) {
           p0[k] = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(tile - 1) * kTile);
           const int lvl = (31 - __builtin_clz(3u * p0[k] + 4u)) >> 1;
           const uint32_t m0 = p0[k] - (uint32_t)level_offset(lvl);
@@ -328,7 +333,7 @@ __global__ void __launch_bounds__(256)
           const int k = P >= kTileIters ? j / kTileIters : 0;
           const uint32_t it = P >= kTileIters ? (uint32_t)(j % kTileIters) : (uint32_t)(pass * P + j);
           const uint32_t first = it * kWave;  // uniform: lanes [0, n_valid - first) are valid
-          if (t0 + k != 0) {
+          if (a.tile_lo + t0 + k != 0) {
             vmask[j] = t0 + k < a.tiles ? ~0ull : 0ull;
             const float bx =
                 __builtin_fmaf((float)(16u * (cx[k] | (it & 1u)) + 1u), scale[k], -1.0f);
@@ -420,8 +425,8 @@ __global__ void __launch_bounds__(256)
               if (kb == 0ull) continue;
               if ((kb >> lane) & 1ull) {
                 // a tile's records start at its first parent index within the pair
-                const int64_t slot = (int64_t)G.pair[s] * a.cap + (p0[k] >> 2) + run[s][k] +
-                                     (mbcnt64(kb) >> 2);
+                const int64_t slot = (int64_t)G.pair[s] * a.cap + ((p0[k] >> 2) - a.parent_lo) +
+                                     run[s][k] + (mbcnt64(kb) >> 2);
                 w4[slot * 4 + (lane & 3u)] = w[s * P + j];
                 if ((lane & 3u) == 0) parent[slot] = pos_index(j) >> 2;
               }
@@ -578,18 +583,25 @@ __global__ void __launch_bounds__(kBindWaves * kWave)
 }
 
 // ------------------------------------------------------------------------ compaction
+// First parent index of a pair's tile T: tile 0 holds the parents of levels 1..3, every other tile
+// 64 parents.
+__device__ __forceinline__ uint32_t tile_parent_offset(uint32_t T) {
+  return T == 0 ? 0u : (uint32_t)(level_offset(kFirstAlignedLevel) / 4) + (T - 1) * (kTile / 4);
+}
+
 // One pair of the compaction (see k_compact); returns the pair's count.
 __device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
                                  float* __restrict__ w4, int64_t* __restrict__ pair_count,
-                                 int64_t cap, uint32_t tiles, uint32_t pair, uint32_t head_slots,
-                                 uint32_t lane) {
+                                 int64_t cap, uint32_t tile_lo, uint32_t tiles, uint32_t pair,
+                                 uint32_t head_slots, uint32_t lane) {
+  const uint32_t parent_lo = tile_parent_offset(tile_lo);
   const uint64_t* row = counts + (int64_t)pair * tiles;
   const int64_t region = (int64_t)pair * cap;
   uint32_t running = 0;
   for (uint32_t t0 = 0; t0 < tiles; t0 += kWave) {
     // a tile holds at most its own slot count (64, or the head tile's parents)
     const uint32_t t_lane = t0 + lane;
-    const uint32_t slots = t_lane == 0 ? head_slots : (uint32_t)(kTile / 4);
+    const uint32_t slots = tile_lo + t_lane == 0 ? head_slots : (uint32_t)(kTile / 4);
     const uint32_t c = t_lane < tiles ? min((uint32_t)row[t_lane], slots) : 0u;
     uint32_t incl = c;  // inclusive scan over the wave
     for (int off = 1; off < kWave; off <<= 1) {
@@ -602,8 +614,7 @@ __device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* 
       if (ci == 0) continue;
       const uint32_t t = t0 + i;
       const uint32_t dst = running + __builtin_amdgcn_readlane(incl, i) - ci;
-      const uint32_t src = t == 0 ? 0u : (uint32_t)(level_offset(kFirstAlignedLevel) / 4) +
-                                             (t - 1) * (kTile / 4);
+      const uint32_t src = tile_parent_offset(tile_lo + t) - parent_lo;
       if (dst == src) continue;
       if (lane < ci) {
         const uint32_t pv = parent[region + src + lane];
@@ -628,8 +639,8 @@ constexpr int kCompactWaves = 4;
 __global__ void __launch_bounds__(kCompactWaves * kWave)
     k_compact(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
               float* __restrict__ w4, int64_t* __restrict__ pair_count,
-              uint32_t* __restrict__ max_count, int64_t cap, uint32_t tiles, uint32_t n_pairs,
-              uint32_t head_slots) {
+              uint32_t* __restrict__ max_count, int64_t cap, uint32_t tile_lo, uint32_t tiles,
+              uint32_t n_pairs, uint32_t head_slots) {
   __shared__ uint32_t wave_max[kCompactWaves];
   const uint32_t lane = lane_id();
   const uint32_t wv = threadIdx.x / kWave;
@@ -637,7 +648,7 @@ __global__ void __launch_bounds__(kCompactWaves * kWave)
   uint32_t my_max = 0;
   for (uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * kCompactWaves + wv);
        pair < n_pairs; pair += n_waves) {
-    my_max = max(my_max, compact_pair(counts, parent, w4, pair_count, cap, tiles, pair,
+    my_max = max(my_max, compact_pair(counts, parent, w4, pair_count, cap, tile_lo, tiles, pair,
                                       head_slots, lane));
   }
   if (lane == 0) wave_max[wv] = my_max;
@@ -646,6 +657,47 @@ __global__ void __launch_bounds__(kCompactWaves * kWave)
     uint32_t m = 0;
     for (int k = 0; k < kCompactWaves; ++k) m = max(m, wave_max[k]);
     raise_max(max_count, m);
+  }
+}
+
+// ------------------------------------------------------------------------ gather
+// Packs the compacted records of all pairs into one contiguous list, pair after pair: pair r's
+// min(count_r, cap) records go to offset sum_{q < r} min(count_q, cap). Workgroup b handles pairs
+// 64 b .. 64 b + 63; it sums the counts before its first pair itself, so no other pass is needed.
+constexpr int kGatherPairs = 64;
+
+__global__ void __launch_bounds__(256)
+    k_gather(const int64_t* __restrict__ counts, const uint32_t* __restrict__ parent,
+             const float* __restrict__ w4, int64_t cap, uint32_t n_pairs,
+             uint32_t* __restrict__ out_parent, float* __restrict__ out_w4) {
+  __shared__ uint64_t part[256];
+  __shared__ uint64_t offs[kGatherPairs + 1];
+  const uint32_t first = blockIdx.x * kGatherPairs;
+  auto clamp = [&](uint32_t r) -> uint64_t {
+    const int64_t c = counts[r];
+    return (uint64_t)(c < 0 ? 0 : (c < cap ? c : cap));
+  };
+  uint64_t mine = 0;
+  for (uint32_t r = threadIdx.x; r < first; r += blockDim.x) mine += clamp(r);
+  part[threadIdx.x] = mine;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t base = 0;
+    for (int k = 0; k < 256; ++k) base += part[k];
+    offs[0] = base;
+    for (int i = 0; i < kGatherPairs; ++i)
+      offs[i + 1] = offs[i] + (first + i < n_pairs ? clamp(first + i) : 0ull);
+  }
+  __syncthreads();
+  const uint32_t lane = lane_id();
+  for (uint32_t i = threadIdx.x / kWave; i < (uint32_t)kGatherPairs && first + i < n_pairs;
+       i += blockDim.x / kWave) {
+    const uint64_t n = offs[i + 1] - offs[i], dst = offs[i];
+    const int64_t src = (int64_t)(first + i) * cap;
+    for (uint64_t e = lane; e < n; e += kWave) {
+      out_parent[dst + e] = parent[src + e];
+      reinterpret_cast<float4*>(out_w4)[dst + e] = reinterpret_cast<const float4*>(w4)[src + e];
+    }
   }
 }
 
@@ -723,6 +775,8 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
   const uint32_t cpg = (a->tiles + chunk - 1) / chunk;
   emr::DiscoverScalars sc{a->cap,
                           a->n_pos,
+                          a->tile_lo,
+                          a->parent_lo,
                           a->tiles,
                           a->n_groups * cpg,
                           cpg,
@@ -787,15 +841,24 @@ extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int window
   }
 }
 
+extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
+                                        const float* w4, int64_t cap, uint32_t n_pairs,
+                                        uint32_t* out_parent, float* out_w4, hipStream_t s) {
+  if (n_pairs == 0) return hipSuccess;
+  hipLaunchKernelGGL(emr::k_gather, dim3((n_pairs + emr::kGatherPairs - 1) / emr::kGatherPairs),
+                     dim3(256), 0, s, counts, parent, w4, cap, n_pairs, out_parent, out_w4);
+  return hipGetLastError();
+}
+
 extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
                                          int64_t* pair_count, uint32_t* max_count, int64_t cap,
-                                         uint32_t tiles, uint32_t n_pairs, uint32_t head_slots,
-                                         hipStream_t s) {
+                                         uint32_t tile_lo, uint32_t tiles, uint32_t n_pairs,
+                                         uint32_t head_slots, hipStream_t s) {
   if (n_pairs == 0) return hipSuccess;
   uint32_t blocks = (n_pairs + emr::kCompactWaves - 1) / emr::kCompactWaves;
   if (blocks > 512) blocks = 512;  // waves loop over pairs beyond this
   hipLaunchKernelGGL(emr::k_compact, dim3(blocks), dim3(emr::kCompactWaves * emr::kWave), 0, s,
-                     counts, parent, w4,
-                     pair_count, max_count, cap, tiles, n_pairs, head_slots);
+                     counts, parent, w4, pair_count, max_count, cap, tile_lo, tiles, n_pairs,
+                     head_slots);
   return hipGetLastError();
 }

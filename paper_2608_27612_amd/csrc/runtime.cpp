@@ -22,10 +22,13 @@ extern "C" hipError_t emr_launch_grid(float* xy, int64_t n, hipStream_t s);
 extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s);
 extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int window, int mode,
                                           uint32_t blocks, hipStream_t s);
+extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
+                                        const float* w4, int64_t cap, uint32_t n_pairs,
+                                        uint32_t* out_parent, float* out_w4, hipStream_t s);
 extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
                                          int64_t* pair_count, uint32_t* max_count, int64_t cap,
-                                         uint32_t tiles, uint32_t n_pairs, uint32_t head_slots,
-                                         hipStream_t s);
+                                         uint32_t tile_lo, uint32_t tiles, uint32_t n_pairs,
+                                         uint32_t head_slots, hipStream_t s);
 
 namespace {
 
@@ -377,9 +380,9 @@ emr_status plan_for(const emr_population* pop, const emr_source* sources, int32_
   return EMR_OK;
 }
 
-// Enqueue: clear, upload tables, bind, discover (or raw eval) per bucket.
-emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const emr_result* out,
-                    float* raw, void* workspace, int64_t workspace_bytes, hipStream_t s) {
+// Clears the workspace's flags and tile words, uploads the call's tables and runs the bind kernel.
+emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspace,
+                        int64_t workspace_bytes, hipStream_t s) {
   if (!workspace || workspace_bytes < (int64_t)P.total)
     return fail(EMR_E_INVAL, "workspace of %lld bytes is smaller than the %zu needed",
                 (long long)workspace_bytes, P.total);
@@ -402,12 +405,26 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
   b.blob_words = (uint32_t)pop->blob_words;
   b.bias_floats = P.bias_floats;
   HIP_OR_FAIL(emr_launch_bind(&b, s));
+  return EMR_OK;
+}
 
+// Enqueues the discover launches (one per bucket) for tiles tile_lo .. tile_lo + n_tiles - 1 of
+// every pair, then the compaction when records go to padded slots. Records of pair r go to its
+// region of `out` counted from the range's first parent; raw outputs to raw[r * N(D) + p].
+emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
+                        const emr_result* out, float* raw, void* workspace, hipStream_t s,
+                        int64_t tile_lo, int64_t n_tiles) {
+  char* ws = (char*)workspace;
   const int cus = device_cu_count();
+  const int64_t parent_lo = emr::tile_parent_offset(tile_lo, P.depth);
+  const int64_t range_parents = emr::tile_parent_offset(tile_lo + n_tiles, P.depth) - parent_lo;
   // Records go to fixed per-tile slots when every pair region can hold the worst case, and are
   // compacted afterwards; a smaller capacity places them through the look-back scan instead.
-  const bool padded = out && out->pair_capacity >= emr::n_parents(P.depth);
+  const bool padded = out && out->pair_capacity >= range_parents;
   const int mode = raw ? 0 : (padded ? 1 : 2);
+  if (mode == 2 && (tile_lo != 0 || n_tiles != P.tiles))
+    return fail(EMR_E_INVAL, "a tile range needs pair_capacity >= its %lld parents",
+                (long long)range_parents);
   Profiler& prof = g_prof;
   if (prof.on) {
     prof.recs.clear();
@@ -448,8 +465,10 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
     a.cap = out ? out->pair_capacity : 0;
     a.n_pos = emr::n_positions(P.depth);
     a.n_groups = bk.count;
-    a.tiles = (uint32_t)P.tiles;
-    a.n_tiles = (uint32_t)((uint64_t)bk.count * (uint64_t)P.tiles);
+    a.tile_lo = (uint32_t)tile_lo;
+    a.parent_lo = (uint32_t)parent_lo;
+    a.tiles = (uint32_t)n_tiles;
+    a.n_tiles = (uint32_t)((uint64_t)bk.count * (uint64_t)n_tiles);
     a.depth = P.depth;
     a.theta = theta;
     a.group_size = (uint32_t)bk.S;
@@ -466,13 +485,16 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
       r.window = bk.window;
       r.positions = emr::positions_per_lane(bk.S, bk.window);
       r.tiles = a.n_tiles;
-      const double npos = (double)a.n_pos;
+      // queries of the range: every tile holds 256 positions but the head tile
+      const double npos = (double)(tile_lo == 0 ? emr::n_positions(P.depth) -
+                                                      emr::kTile * (P.tiles - n_tiles)
+                                                : emr::kTile * n_tiles);
       for (uint32_t k = 0; k < bk.count; ++k) {
         const uint32_t gi = bk.first + k;
         const emr::Member& m0 = P.members[P.group_member0[gi]];
         r.slots += bk.S * npos * query_slots(pop->info[m0.desc], prof.rT);
       }
-      r.queries = (int64_t)bk.count * bk.S * a.n_pos;
+      r.queries = (int64_t)((double)bk.count * bk.S * npos);
       prof.recs.push_back(r);
     }
   }
@@ -485,11 +507,20 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
   if (padded && P.n_pairs > 0)
     HIP_OR_FAIL(emr_launch_compact(
         (const uint64_t*)(ws + P.off_status), out->parent, out->w4, out->pair_count,
-        (uint32_t*)(ws + P.off_err) + 1, out->pair_capacity, (uint32_t)P.tiles, (uint32_t)P.n_pairs,
+        (uint32_t*)(ws + P.off_err) + 1, out->pair_capacity, (uint32_t)tile_lo, (uint32_t)n_tiles,
+        (uint32_t)P.n_pairs,
         (uint32_t)(P.depth < emr::kFirstAlignedLevel ? emr::n_parents(P.depth)
                                                      : emr::level_offset(emr::kFirstAlignedLevel) / 4),
         s));
   return EMR_OK;
+}
+
+// Enqueue a whole call: prepare, then every tile of every pair.
+emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const emr_result* out,
+                    float* raw, void* workspace, int64_t workspace_bytes, hipStream_t s) {
+  emr_status st = prepare_plan(pop, P, workspace, workspace_bytes, s);
+  if (st != EMR_OK) return st;
+  return launch_range(pop, P, theta, out, raw, workspace, s, 0, P.tiles);
 }
 
 }  // namespace
@@ -691,6 +722,202 @@ emr_status emr_profile_read(emr_launch_profile* out, int32_t cap, int32_t* n) {
     prof.recs[i].ms = ms;
     if (out && (int32_t)i < cap) out[i] = prof.recs[i];
   }
+  return EMR_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------ streaming
+namespace {
+
+// Device and pinned buffers of one emr_discover_stream call. The destructor drains both streams
+// before freeing, so an early return (an error, or a sink that stops the run) never frees memory
+// a queued kernel or copy still uses.
+struct StreamRun {
+  hipStream_t s = nullptr, side = nullptr;
+  void* ws = nullptr;
+  uint32_t* pad_parent = nullptr;   // padded per-pair regions of the current chunk
+  float* pad_w4 = nullptr;
+  int64_t* counts = nullptr;        // per-pair counts of the current chunk
+  uint32_t* g_parent[2] = {};       // gathered records, double buffered
+  float* g_w4[2] = {};
+  int64_t* counts_h[2] = {};        // pinned copies of the counts
+  uint32_t* stage_parent[2] = {};   // pinned staging of the gathered records
+  float* stage_w4[2] = {};
+  int64_t stage_cap[2] = {0, 0};
+  hipEvent_t ev_count[2] = {}, ev_copy[2] = {};
+  bool copy_pending[2] = {false, false};
+
+  ~StreamRun() {
+    if (s) (void)hipStreamSynchronize(s);
+    if (side) (void)hipStreamSynchronize(side);
+    for (int b = 0; b < 2; ++b) {
+      if (g_parent[b]) (void)hipFree(g_parent[b]);
+      if (g_w4[b]) (void)hipFree(g_w4[b]);
+      if (counts_h[b]) (void)hipHostFree(counts_h[b]);
+      if (stage_parent[b]) (void)hipHostFree(stage_parent[b]);
+      if (stage_w4[b]) (void)hipHostFree(stage_w4[b]);
+      if (ev_count[b]) (void)hipEventDestroy(ev_count[b]);
+      if (ev_copy[b]) (void)hipEventDestroy(ev_copy[b]);
+    }
+    if (ws) (void)hipFree(ws);
+    if (pad_parent) (void)hipFree(pad_parent);
+    if (pad_w4) (void)hipFree(pad_w4);
+    if (counts) (void)hipFree(counts);
+    if (side) (void)hipStreamDestroy(side);
+  }
+};
+
+// Largest device footprint of one streamed call's record buffers (padded + two gathered sets).
+constexpr int64_t kStreamBufferLimit = int64_t(48) << 30;
+
+}  // namespace
+
+extern "C" {
+
+emr_status emr_stream_chunks(int32_t depth, int64_t chunk_positions, int64_t* n_chunks) {
+  if (depth < 0 || depth > EMR_MAX_DEPTH)
+    return fail(EMR_E_INVAL, "depth %d outside [0, %d]", depth, EMR_MAX_DEPTH);
+  if (chunk_positions < emr::kTile || chunk_positions % emr::kTile != 0)
+    return fail(EMR_E_INVAL, "chunk_positions=%lld must be a positive multiple of %d",
+                (long long)chunk_positions, emr::kTile);
+  if (!n_chunks) return fail(EMR_E_INVAL, "n_chunks is NULL");
+  const int64_t tpc = chunk_positions / emr::kTile, tiles = emr::tiles_per_pair(depth);
+  *n_chunks = (tiles + tpc - 1) / tpc;
+  return EMR_OK;
+}
+
+emr_status emr_discover_stream(const emr_population* pop, const emr_source* sources,
+                               int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                               int32_t depth, float theta, int64_t chunk_positions, int64_t start,
+                               emr_sink sink, void* user, int64_t* next, void* stream) {
+  if (next) *next = start;
+  if (!sink) return fail(EMR_E_INVAL, "sink is NULL");
+  int64_t n_chunks = 0;
+  emr_status st = emr_stream_chunks(depth, chunk_positions, &n_chunks);
+  if (st != EMR_OK) return st;
+  std::shared_ptr<const Plan> plan;
+  st = plan_for(pop, sources, n_sources, src_offsets, n_shared, depth, &plan);
+  if (st != EMR_OK) return st;
+  const Plan& P = *plan;
+  const int64_t n_pairs = P.n_pairs, tpc = chunk_positions / emr::kTile;
+  const int64_t total = n_chunks * n_pairs;
+  if (start < 0 || start > total)
+    return fail(EMR_E_INVAL, "start=%lld outside [0, %lld]", (long long)start, (long long)total);
+  if (start == total) {
+    if (next) *next = total;
+    return EMR_OK;
+  }
+  // A pair region holds a chunk's parents: at most 64 per tile, and never more than Q(D).
+  const int64_t cap = std::min<int64_t>(tpc * (emr::kTile / 4), emr::n_parents(depth));
+  const int64_t set_bytes = n_pairs * cap * 20;
+  if (set_bytes > kStreamBufferLimit / 3)
+    return fail(EMR_E_LIMIT, "%lld pairs x %lld-position chunks need %lld bytes of record buffers; "
+                "use smaller chunks", (long long)n_pairs, (long long)chunk_positions,
+                (long long)(3 * set_bytes));
+
+  StreamRun R;
+  R.s = (hipStream_t)stream;
+  HIP_OR_FAIL(hipStreamCreateWithFlags(&R.side, hipStreamNonBlocking));
+  for (int b = 0; b < 2; ++b) {
+    HIP_OR_FAIL(hipEventCreateWithFlags(&R.ev_count[b], hipEventDisableTiming));
+    HIP_OR_FAIL(hipEventCreateWithFlags(&R.ev_copy[b], hipEventDisableTiming));
+  }
+  auto dmalloc = [](void** p, int64_t bytes) {
+    return hipMalloc(p, (size_t)std::max<int64_t>(bytes, 256));
+  };
+  if (dmalloc(&R.ws, (int64_t)P.total) != hipSuccess ||
+      dmalloc((void**)&R.pad_parent, n_pairs * cap * 4) != hipSuccess ||
+      dmalloc((void**)&R.pad_w4, n_pairs * cap * 16) != hipSuccess ||
+      dmalloc((void**)&R.counts, n_pairs * 8) != hipSuccess)
+    return fail(EMR_E_NOMEM, "device buffers of a streamed call (%lld bytes per record set)",
+                (long long)set_bytes);
+  for (int b = 0; b < 2; ++b) {
+    if (dmalloc((void**)&R.g_parent[b], n_pairs * cap * 4) != hipSuccess ||
+        dmalloc((void**)&R.g_w4[b], n_pairs * cap * 16) != hipSuccess)
+      return fail(EMR_E_NOMEM, "gather buffers of a streamed call");
+    if (hipHostMalloc((void**)&R.counts_h[b], (size_t)std::max<int64_t>(n_pairs, 1) * 8,
+                      hipHostMallocDefault) != hipSuccess)
+      return fail(EMR_E_NOMEM, "pinned counts of a streamed call");
+  }
+
+  st = prepare_plan(pop, P, R.ws, (int64_t)P.total, R.s);
+  if (st != EMR_OK) return st;
+  emr_result chunk_out{R.pad_parent, R.pad_w4, cap, R.counts, R.ws, (int64_t)P.total};
+
+  // Chunk c on the compute stream: discover + compact over its tiles, gather into buffer c & 1,
+  // counts to pinned memory.
+  auto enqueue = [&](int64_t c) -> emr_status {
+    const int b = (int)(c & 1);
+    if (R.copy_pending[b]) HIP_OR_FAIL(hipStreamWaitEvent(R.s, R.ev_copy[b], 0));
+    const int64_t tile_lo = c * tpc, n = std::min<int64_t>(tpc, P.tiles - tile_lo);
+    emr_status e = launch_range(pop, P, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n);
+    if (e != EMR_OK) return e;
+    HIP_OR_FAIL(emr_launch_gather(R.counts, R.pad_parent, R.pad_w4, cap, (uint32_t)n_pairs,
+                                  R.g_parent[b], R.g_w4[b], R.s));
+    if (n_pairs > 0)
+      HIP_OR_FAIL(hipMemcpyAsync(R.counts_h[b], R.counts, (size_t)n_pairs * 8,
+                                 hipMemcpyDeviceToHost, R.s));
+    HIP_OR_FAIL(hipEventRecord(R.ev_count[b], R.s));
+    return EMR_OK;
+  };
+
+  const int64_t c0 = start / n_pairs, skip = start % n_pairs;
+  st = enqueue(c0);
+  if (st != EMR_OK) return st;
+  for (int64_t c = c0; c < n_chunks; ++c) {
+    const int b = (int)(c & 1);
+    if (c + 1 < n_chunks) {
+      st = enqueue(c + 1);  // the GPU computes the next chunk while this one is delivered
+      if (st != EMR_OK) return st;
+    }
+    HIP_OR_FAIL(hipEventSynchronize(R.ev_count[b]));
+    int64_t n_rec = 0;
+    for (int64_t r = 0; r < n_pairs; ++r) n_rec += std::min<int64_t>(std::max<int64_t>(R.counts_h[b][r], 0), cap);
+    if (n_rec > R.stage_cap[b]) {
+      if (R.stage_parent[b]) (void)hipHostFree(R.stage_parent[b]);
+      if (R.stage_w4[b]) (void)hipHostFree(R.stage_w4[b]);
+      R.stage_parent[b] = nullptr;
+      R.stage_w4[b] = nullptr;
+      R.stage_cap[b] = 0;
+      const int64_t want = std::max<int64_t>(n_rec, int64_t(1) << 16);
+      if (hipHostMalloc((void**)&R.stage_parent[b], (size_t)want * 4, hipHostMallocDefault) !=
+              hipSuccess ||
+          hipHostMalloc((void**)&R.stage_w4[b], (size_t)want * 16, hipHostMallocDefault) !=
+              hipSuccess)
+        return fail(EMR_E_NOMEM, "pinned staging of %lld records", (long long)want);
+      R.stage_cap[b] = want;
+    }
+    if (n_rec > 0) {
+      HIP_OR_FAIL(hipStreamWaitEvent(R.side, R.ev_count[b], 0));
+      HIP_OR_FAIL(hipMemcpyAsync(R.stage_parent[b], R.g_parent[b], (size_t)n_rec * 4,
+                                 hipMemcpyDeviceToHost, R.side));
+      HIP_OR_FAIL(hipMemcpyAsync(R.stage_w4[b], R.g_w4[b], (size_t)n_rec * 16,
+                                 hipMemcpyDeviceToHost, R.side));
+      HIP_OR_FAIL(hipEventRecord(R.ev_copy[b], R.side));
+      R.copy_pending[b] = true;
+      HIP_OR_FAIL(hipEventSynchronize(R.ev_copy[b]));
+    }
+    int64_t off = 0;
+    for (int64_t r = 0; r < n_pairs; ++r) {
+      const int64_t nr = std::min<int64_t>(std::max<int64_t>(R.counts_h[b][r], 0), cap);
+      if (nr > 0 && !(c == c0 && r < skip)) {
+        if (sink(r, c, R.stage_parent[b] + off, R.stage_w4[b] + 4 * off, nr, user) != 0) {
+          if (next) *next = c * n_pairs + r;
+          return fail(EMR_E_ABORTED, "the sink stopped the run at chunk %lld, pair %lld",
+                      (long long)c, (long long)r);
+        }
+      }
+      off += nr;
+    }
+    if (next) *next = (c + 1) * n_pairs;
+  }
+  HIP_OR_FAIL(hipStreamSynchronize(R.s));
+  uint32_t err = 0;
+  HIP_OR_FAIL(hipMemcpy(&err, R.ws, 4, hipMemcpyDeviceToHost));
+  if (err)
+    return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (2: a table entry out of range)",
+                err);
   return EMR_OK;
 }
 

@@ -25,7 +25,7 @@ ABI_FUNCTIONS = [
     "emr_last_error", "emr_version", "emr_grid_count", "emr_build_grids", "emr_pack_population",
     "emr_free_population", "emr_population_info", "emr_workspace_bytes", "emr_discover",
     "emr_result_check", "emr_eval_raw", "emr_discover_cost", "emr_profile_enable",
-    "emr_profile_read",
+    "emr_profile_read", "emr_stream_chunks", "emr_discover_stream",
 ]
 
 
@@ -59,6 +59,11 @@ class emr_launch_profile(C.Structure):
 
 _lib = None
 
+# int32_t sink(int64_t pair, int64_t chunk, const uint32_t* parent, const float* w4, int64_t n,
+#              void* user)
+SINK = C.CFUNCTYPE(C.c_int32, C.c_int64, C.c_int64, C.POINTER(C.c_uint32), C.POINTER(C.c_float),
+                   C.c_int64, C.c_void_p)
+
 
 def lib():
     """The loaded libemr.so (raises if it was never built)."""
@@ -84,6 +89,8 @@ def lib():
             "emr_discover_cost": (I32, [P, P, I32, P, I32, I32, F64, P, P]),
             "emr_profile_enable": (I32, [I32, F64]),
             "emr_profile_read": (I32, [P, I32, P]),
+            "emr_stream_chunks": (I32, [I32, I64, P]),
+            "emr_discover_stream": (I32, [P, P, I32, P, I32, I32, F32, I64, I64, SINK, P, P, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -316,3 +323,47 @@ def emr_profile_read():
     return [{"S": r.group_size, "W": r.window, "P": r.positions, "tiles": r.tiles,
              "queries": r.queries, "first": i == 0,
              "slots": r.slots, "ms": r.ms} for i, r in enumerate(arr[:n.value])]
+
+
+# ----------------------------------------------------------------------------- streaming
+
+def emr_stream_chunks(depth: int, chunk_positions: int = 1 << 24) -> int:
+    n = C.c_int64()
+    _check(lib().emr_stream_chunks(depth, chunk_positions, C.byref(n)))
+    return n.value
+
+
+def emr_discover_stream(pop: Population, sources, depth: int, theta: float, sink,
+                        chunk_positions: int = 1 << 24, start: int = 0, src_offsets=None,
+                        stream=None) -> int:
+    """Streamed eager discovery. `sink(pair, chunk, parent, w4)` receives numpy copies of each
+    (chunk, pair) delivery (parent uint32 [n], w4 float32 [n, 4]) and returns True/None to go on,
+    False to stop. Returns the cursor after the run; a stop raises EmrError(EMR_E_ABORTED) whose
+    `next_cursor` is the refused delivery's cursor (see emr_discover_stream in include/emr.h)."""
+    offs = _offsets(src_offsets)
+    errors = []
+
+    def _sink(pair, chunk, parent, w4, n, user):
+        try:
+            p = np.ctypeslib.as_array(parent, shape=(n,)).copy()
+            w = np.ctypeslib.as_array(w4, shape=(n * 4,)).reshape(n, 4).copy()
+            return 0 if sink(int(pair), int(chunk), p, w) is not False else 1
+        except BaseException as e:  # an exception in the sink stops the run and is re-raised
+            errors.append(e)
+            return 1
+
+    cb = SINK(_sink)
+    nxt = C.c_int64(start)
+    st = lib().emr_discover_stream(pop.handle, _sources(sources), len(sources),
+                                   None if offs is None else offs.ctypes.data,
+                                   0 if offs is not None else len(sources), depth,
+                                   C.c_float(theta), chunk_positions, start, cb, None,
+                                   C.byref(nxt), _stream_ptr(stream))
+    if errors:
+        raise errors[0]
+    if st != EMR_OK:
+        err = EmrError(st, lib().emr_last_error().decode())
+        err.next_cursor = nxt.value
+        raise err
+    return nxt.value
+

@@ -72,3 +72,31 @@ def test_discover_rejects_null_population():
 
 def test_version():
     assert emr.lib().emr_version() >= 100
+
+
+def test_stream_chunk_count_and_argument_errors():
+    """emr_stream_chunks counts tiles of 256 positions (the first holding levels 1..3); streaming
+    refuses bad arguments before touching a GPU."""
+    from paper_2608_27612_amd import emr
+    import oracle
+    for D in [0, 3, 4, 7, 13]:
+        tiles = 1 if D < 4 else 1 + (oracle.n_positions(D) - 84) // 256
+        for chunk in [256, 512, 256 * 7, 1 << 24]:
+            assert emr.emr_stream_chunks(D, chunk) == -(-tiles // (chunk // 256))
+    assert emr.emr_stream_chunks(13, 1 << 24) == 6
+    for chunk in [0, 255, 300, -256]:
+        with pytest.raises(emr.EmrError) as e:
+            emr.emr_stream_chunks(7, chunk)
+        assert e.value.status == emr.EMR_E_INVAL
+    with pytest.raises(emr.EmrError) as e:
+        emr.emr_stream_chunks(16, 256)
+    assert e.value.status == emr.EMR_E_INVAL
+    L = emr.lib()
+    sink = emr.SINK(lambda *a: 0)
+    nxt = C.c_int64(-5)
+    st = L.emr_discover_stream(None, None, 0, None, 0, 7, C.c_float(0.03), 256, 0, sink, None,
+                               C.byref(nxt), None)
+    assert st == emr.EMR_E_INVAL and nxt.value == 0
+    st = L.emr_discover_stream(None, None, 0, None, 0, 7, C.c_float(0.03), 256, 0,
+                               C.cast(None, emr.SINK), None, None, None)
+    assert st == emr.EMR_E_INVAL
