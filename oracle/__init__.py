@@ -218,3 +218,37 @@ def lazy(g: dict, source, depth: int, theta: float):
 
 def max_threads() -> int:
     return int(lib().orc_max_threads())
+
+
+def hidden_sources(records, genomes_sources, sources, depth: int):
+    """Sources of the hidden-to-hidden phase, from this oracle's own phase-1 output (the reading of
+    'from every discovered hidden node' used for the recurrent substrate): for each genome, the
+    union over its outgoing input sources of the four children 4P+1..4P+4 of every kept parent P,
+    deduplicated by heap index in ascending order, each an outgoing source at its cell centre.
+
+    records: the dict returned by discover() for `genomes_sources` genomes x `sources` (shared).
+    Returns (sources array, offsets[n_genomes + 1]) in the layout of discover's src_offsets;
+    the sources of a genome are ordered by heap index.
+    """
+    n_src = len(sources)
+    xy = grid(depth)
+    out_x, out_y, offs = [], [], [0]
+    for g in range(genomes_sources):
+        kids = []
+        for j in range(n_src):
+            if int(sources[j]["dir"]) != 0:
+                continue
+            r = g * n_src + j
+            lo, hi = records["pair_offset"][r], records["pair_offset"][r + 1]
+            P = records["parent"][lo:hi].astype(np.int64)
+            # heap cell F sits at grid index F - 1: the children 4P+1..4P+4 at 4P..4P+3
+            kids.append((4 * P[:, None] + np.arange(4)[None, :]).ravel())
+        idx = np.unique(np.concatenate(kids)) if kids else np.zeros(0, np.int64)
+        out_x.append(xy[idx, 0])
+        out_y.append(xy[idx, 1])
+        offs.append(offs[-1] + len(idx))
+    src = np.zeros(offs[-1], dtype=[("x", "<f4"), ("y", "<f4"), ("dir", "<i4")])
+    if offs[-1]:
+        src["x"] = np.concatenate(out_x)
+        src["y"] = np.concatenate(out_y)
+    return src, np.array(offs, np.int32)

@@ -367,3 +367,28 @@ def emr_discover_stream(pop: Population, sources, depth: int, theta: float, sink
         raise err
     return nxt.value
 
+
+
+# ----------------------------------------------------------------------------- h->h sources
+
+def hidden_sources(counts, recs, sources, depth: int, n_genomes: int, grid_xy=None):
+    """Host glue for the hidden-to-hidden phase: per genome, the union over its outgoing input
+    sources of the children of kept parents (records_to_host output of a shared-source discover
+    call), deduplicated by heap index in ascending order, as outgoing sources at the cell centres
+    of the library's grid (emr_build_grids). Returns (sources, src_offsets) for a CSR call."""
+    if grid_xy is None:
+        grid_xy = emr_build_grids(depth).cpu().numpy()
+    n_src = len(sources)
+    xs, ys, offs = [], [], [0]
+    for g in range(n_genomes):
+        kids = [4 * recs[g * n_src + j][0][:, None] + np.arange(4)[None, :]
+                for j in range(n_src) if int(sources[j]["dir"]) == EMR_DIR_OUT]
+        idx = np.unique(np.concatenate([k.ravel() for k in kids])) if kids else np.zeros(0, np.int64)
+        xs.append(grid_xy[idx, 0])
+        ys.append(grid_xy[idx, 1])
+        offs.append(offs[-1] + len(idx))
+    src = np.zeros(offs[-1], dtype=[("x", "<f4"), ("y", "<f4"), ("dir", "<i4")])
+    if offs[-1]:
+        src["x"] = np.concatenate(xs)
+        src["y"] = np.concatenate(ys)
+    return src, np.array(offs, np.int32)

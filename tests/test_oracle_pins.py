@@ -344,3 +344,26 @@ def test_shared_and_csr_sources_agree():
     b = oracle.discover(genomes, csr_src, 4, 0.01, src_offsets=[0, 4, 8, 12])
     for k in ("pair_count", "parent", "w4", "var"):
         np.testing.assert_array_equal(a[k], b[k])
+
+
+def test_hidden_sources_are_children_of_kept_cells():
+    """The hidden-to-hidden sources are exactly the cell centres of the children of kept parents
+    over the outgoing input sources, deduplicated (checked against a direct enumeration)."""
+    g = W.single_cppn(3, 8, 20)[0]
+    srcs = W.xor_sources()
+    D, theta = 4, 0.01
+    rec = oracle.discover([g], srcs, D, theta)
+    hs, offs = oracle.hidden_sources(rec, 1, srcs, D)
+    assert offs[0] == 0 and offs[-1] == len(hs)
+    want = set()
+    for j in range(len(srcs)):
+        if srcs[j]["dir"] != 0:
+            continue
+        lo, hi = rec["pair_offset"][j], rec["pair_offset"][j + 1]
+        for P in rec["parent"][lo:hi]:
+            for k in range(1, 5):
+                x, y, _ = oracle.cell(int(4 * P + k))
+                want.add((np.float32(x), np.float32(y)))
+    got = set(zip(hs["x"].tolist(), hs["y"].tolist()))
+    assert got == {(float(a), float(b)) for a, b in want}
+    assert len(hs) == len(want) and np.all(hs["dir"] == 0)

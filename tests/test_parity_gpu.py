@@ -317,3 +317,77 @@ def test_full_size_xor_pop1000_depth7_sampled(emr):
             diff = np.setxor1d(gp, o["parent"])
             _, dvar = oracle.eval_parents(g, s, diff)
             assert np.all(np.abs(dvar - theta32) <= BAND), (r, diff[:5], dvar[:5])
+
+
+@pytest.mark.parametrize("D", [5, 6])
+def test_config2_xor_pop1000_full(emr, D):
+    """The XOR population workload (1000 genomes x 4 sources) at depths 5 and 6, every pair."""
+    genomes, sources, _, theta = W.workload("xor_pop1000_d%d" % D)
+    st = check_discover(emr, genomes, sources, D, theta)
+    assert st["records"] > 0
+
+
+def test_config3_tabular_pop150_full(emr):
+    """The tabular workload: 150 genomes (up to 40 hidden nodes, 120 edges) x 33 sources at depth
+    6, every pair."""
+    genomes, sources, D, theta = W.workload("tabular_pop150")
+    st = check_discover(emr, genomes, sources, D, theta)
+    assert st["records"] > 0
+
+
+def test_config4_recurrent_depth10_two_phases(emr):
+    """The recurrent workload at depth 10 on its first 6 genomes: phase 1 (the XOR sources) in
+    full against the oracle; hidden-to-hidden sources built from each side's own phase-1 output
+    agree; phase 2 (per-genome CSR sources, one per discovered hidden node) on sampled pairs."""
+    genomes, sources, D, theta = W.workload("recurrent_pop100")
+    genomes = genomes[:6]
+    theta32 = float(np.float32(theta))
+    pop = emr.emr_pack_population(genomes)
+    res = emr.emr_discover(pop, sources, D, theta32)
+    emr.emr_result_check(res)
+    counts, recs = emr.records_to_host(res)
+    o = oracle.discover(genomes, sources, D, theta32)
+    same = True
+    for r in range(len(counts)):
+        lo, hi = o["pair_offset"][r], o["pair_offset"][r + 1]
+        gp, gw = recs[r]
+        if not np.array_equal(gp, o["parent"][lo:hi]):
+            same = False
+            g, s = pair_genome_source(r, genomes, sources, None)
+            diff = np.setxor1d(gp, o["parent"][lo:hi])
+            _, dvar = oracle.eval_parents(g, s, diff)
+            assert np.all(np.abs(dvar - theta32) <= BAND)
+        else:
+            assert close(gw, o["w4"][lo:hi]).all()
+    hs_o, offs_o = oracle.hidden_sources(o, len(genomes), sources, D)
+    hs_g, offs_g = emr.hidden_sources(counts, recs, sources, D, len(genomes))
+    if same:
+        np.testing.assert_array_equal(offs_g, offs_o)
+        np.testing.assert_array_equal(hs_g["x"], hs_o["x"].astype(np.float32))
+        np.testing.assert_array_equal(hs_g["y"], hs_o["y"].astype(np.float32))
+    assert offs_o[-1] > 0
+    # phase 2 on the oracle's sources: records per pair are few, so regions of 8192 (look-back
+    # placement) suffice; an overflow would be reported and retried at the reported size
+    cap = 8192
+    res2 = emr.emr_discover(pop, hs_o, D, theta32, src_offsets=offs_o, pair_capacity=cap)
+    try:
+        emr.emr_result_check(res2)
+    except emr.EmrError as e:
+        assert e.status == emr.EMR_E_CAPACITY
+        cap = int(res2["pair_count"].max().item())  # true counts survive an overflow
+        res2 = emr.emr_discover(pop, hs_o, D, theta32, src_offsets=offs_o, pair_capacity=cap)
+        emr.emr_result_check(res2)
+    counts2, recs2 = emr.records_to_host(res2)
+    rng = np.random.default_rng(4)
+    for r in sorted(rng.choice(len(counts2), size=min(8, len(counts2)), replace=False).tolist()):
+        g = genomes[int(np.searchsorted(offs_o, r, side="right") - 1)]
+        s = hs_o[r]
+        oo = oracle.discover([g], [s], D, theta32)
+        gp, gw = recs2[r]
+        assert counts2[r] <= cap
+        if np.array_equal(gp, oo["parent"]):
+            assert close(gw, oo["w4"]).all(), r
+        else:
+            diff = np.setxor1d(gp, oo["parent"])
+            _, dvar = oracle.eval_parents(g, s, diff)
+            assert np.all(np.abs(dvar - theta32) <= BAND), (r, diff[:5], dvar[:5])
