@@ -116,6 +116,17 @@ typedef struct emr_population emr_population;
  * the first failing genome (else -1); *out is set only on success. */
 emr_status emr_pack_population(const emr_genome* genomes, int32_t n, emr_population** out,
                                int32_t* bad_index);
+
+/* The same for genomes given as concatenated arrays (host, caller-owned, read only during the
+ * call): genome g has nodes node_off[g] .. node_off[g+1]-1 of kind/act/bias and edges
+ * edge_off[g] .. edge_off[g+1]-1 of src/dst/w/enabled, node ids counted from the genome's first
+ * node. node_off and edge_off have n+1 ascending entries starting at 0; bias and enabled may be
+ * NULL (all 0, all enabled). Per-genome rules and errors as emr_pack_population. */
+emr_status emr_pack_population_flat(int32_t n, const int64_t* node_off, const uint8_t* kind,
+                                    const uint8_t* act, const float* bias, const int64_t* edge_off,
+                                    const int32_t* src, const int32_t* dst, const float* w,
+                                    const uint8_t* enabled, emr_population** out,
+                                    int32_t* bad_index);
 void emr_free_population(emr_population* pop);
 
 /* Per-genome facts of a packed population (host arrays of n_genomes, any may be NULL):

@@ -71,6 +71,7 @@ constexpr uint32_t kSlotBits = 5;
 //   n_steps  records of 4 words: n_fold, fold_off, bias bits, r         -> folded bias of varying
 //            node i, for its first program record r
 //   edges: {u_src, w bits}; U[0..4] hold the five input roles (x1, y1, x2, y2, 1).
+// edge_off and fold_off count words from uni_off, so a genome's words can be moved as a block.
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 
 struct ProgDesc {

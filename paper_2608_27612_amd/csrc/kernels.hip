@@ -543,10 +543,8 @@ __global__ void __launch_bounds__(kBindWaves * kWave)
                           dir == 0 ? 0.0f : sy, 1.0f};
     U[lane] = in5[lane];
   }
-  // Edge lists are word offsets into the blob and must lie inside this uniform program.
-  auto edges_ok = [&](uint32_t off, uint32_t cnt) {
-    return off >= d.uni_off && (uint64_t)off + 2ull * cnt <= d.uni_end;
-  };
+  // Edge lists are word offsets from uni_off and must lie inside this uniform program.
+  auto edges_ok = [&](uint32_t off, uint32_t cnt) { return (uint64_t)off + 2ull * cnt <= words; };
   bool bad = false;
   for (uint32_t k = 0; k < n_un && !bad; ++k) {
     const uint32_t* rec = prog + 4 + 4 * k;
@@ -556,7 +554,7 @@ __global__ void __launch_bounds__(kBindWaves * kWave)
       bad = true;
       break;
     }
-    const uint32_t* ep = prog + (off - d.uni_off);
+    const uint32_t* ep = prog + off;
     for (uint32_t e = 0; e < cnt; ++e)
       z = __builtin_fmaf(__uint_as_float(ep[2 * e + 1]), U[min(ep[2 * e], 4u + k)], z);
     // every lane computed the same value and stores it to the same word
@@ -573,7 +571,7 @@ __global__ void __launch_bounds__(kBindWaves * kWave)
       bad = true;
       break;
     }
-    const uint32_t* ep = prog + (off - d.uni_off);
+    const uint32_t* ep = prog + off;
     for (uint32_t e = 0; e < cnt; ++e)
       z = __builtin_fmaf(__uint_as_float(ep[2 * e + 1]), U[min(ep[2 * e], 4u + n_un)], z);
     bias_tab[m.bias_base + 4 * (1 + rec)] = z;

@@ -303,7 +303,7 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       uint32_t* r = &blob[ub + 4 + 4 * k];
       r[0] = g.act[v];
       r[1] = cnt;
-      r[2] = first;
+      r[2] = first - (uint32_t)ub;
       r[3] = fbits(g.bias ? g.bias[v] : 0.0f);
     }
     for (int t = 0; t < (int)vsteps.size(); ++t) {
@@ -318,7 +318,7 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       }
       uint32_t* r = &blob[ub + 4 + 4 * unodes.size() + 4 * t];
       r[0] = cnt;
-      r[1] = first;
+      r[1] = first - (uint32_t)ub;
       r[2] = fbits(g.bias ? g.bias[v] : 0.0f);
       r[3] = first_rec[t];
     }

@@ -7,9 +7,11 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <memory>
 #include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "../../include/emr.h"
@@ -548,52 +550,172 @@ emr_status emr_build_grids(int32_t depth, float* xy_dev, void* stream) {
   return EMR_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Packs genomes on host threads (each thread a contiguous range into its own word vector, then
+// the vectors are concatenated and their genomes' descriptors moved by the vector's base), and
+// uploads the tables through pinned staging. *bad_index receives the lowest failing genome.
+emr_status pack_and_upload(int32_t n, const std::function<emr_genome(int32_t)>& genome_at,
+                           emr_population** out, int32_t* bad_index) {
+  std::vector<emr::ProgDesc> desc(2 * (size_t)n);
+  std::vector<emr::GenomeInfo> info(2 * (size_t)n);
+  const int hw = (int)std::max(1u, std::thread::hardware_concurrency());
+  const int n_threads = std::max(1, std::min({hw, 16, n / 32}));
+  struct Part {
+    std::vector<uint32_t> words;
+    int32_t bad = -1;
+    emr_status st = EMR_OK;
+    std::string msg;
+  };
+  std::vector<Part> parts((size_t)n_threads);
+  auto work = [&](int t) {
+    const int32_t lo = (int32_t)((int64_t)n * t / n_threads);
+    const int32_t hi = (int32_t)((int64_t)n * (t + 1) / n_threads);
+    Part& p = parts[(size_t)t];
+    for (int32_t g = lo; g < hi; ++g) {
+      emr_status st = EMR_OK;
+      std::string msg;
+      if (!emr::pack_genome(genome_at(g), p.words, &desc[2 * (size_t)g], &info[2 * (size_t)g], &st,
+                            &msg)) {
+        p.bad = g;
+        p.st = st;
+        p.msg = msg;
+        return;
+      }
+      if (p.words.size() > 0xF0000000ull) {
+        p.bad = g;
+        p.st = EMR_E_LIMIT;
+        p.msg = "population too large";
+        return;
+      }
+    }
+    while (p.words.size() % emr::kRecWords) p.words.push_back(0u);  // keep bases aligned
+  };
+  if (n_threads == 1) {
+    work(0);
+  } else {
+    std::vector<std::thread> pool;
+    for (int t = 0; t < n_threads; ++t) pool.emplace_back(work, t);
+    for (auto& th : pool) th.join();
+  }
+  for (const Part& p : parts)
+    if (p.bad >= 0) {  // the parts cover increasing genome ranges: the first is the lowest
+      if (bad_index) *bad_index = p.bad;
+      return fail(p.st, "genome %d: %s", p.bad, p.msg.c_str());
+    }
+  // concatenate, moving each part's descriptors by its base
+  size_t total = 16;  // the kernels may read a few words past a program's end
+  for (const Part& p : parts) total += p.words.size();
+  if (total > 0xF0000000ull) return fail(EMR_E_LIMIT, "population too large");
+  emr_population* pop = new (std::nothrow) emr_population;
+  if (!pop) return fail(EMR_E_NOMEM, "host allocation failed");
+  std::unique_ptr<emr_population, void (*)(emr_population*)> guard(pop, emr_free_population);
+  size_t base = 0;
+  for (int t = 0; t < n_threads; ++t) {
+    const int32_t lo = (int32_t)((int64_t)n * t / n_threads);
+    const int32_t hi = (int32_t)((int64_t)n * (t + 1) / n_threads);
+    for (size_t d = 2 * (size_t)lo; d < 2 * (size_t)hi; ++d) {
+      desc[d].var_off += (uint32_t)base;
+      desc[d].uni_off += (uint32_t)base;
+      desc[d].uni_end += (uint32_t)base;
+    }
+    base += parts[(size_t)t].words.size();
+  }
+  pop->n_genomes = n;
+  pop->desc = std::move(desc);
+  pop->info = std::move(info);
+  pop->blob_words = total;
+  const size_t blob_bytes = total * 4, desc_bytes = std::max<size_t>(1, pop->desc.size()) *
+                                                    sizeof(emr::ProgDesc);
+  if (hipMalloc((void**)&pop->d_blob, blob_bytes) != hipSuccess ||
+      hipMalloc((void**)&pop->d_desc, desc_bytes) != hipSuccess)
+    return fail(EMR_E_NOMEM, "device allocation of %zu words failed", total);
+  // one pinned image (words, then descriptors), copied on a library stream and waited for: the
+  // tables are complete on the device before the call returns, whatever stream reads them next
+  static std::mutex up_mu;
+  static void* up_buf = nullptr;
+  static size_t up_size = 0;
+  std::lock_guard<std::mutex> lock(up_mu);
+  if (up_size < blob_bytes + desc_bytes) {
+    if (up_buf) (void)hipHostFree(up_buf);
+    up_buf = nullptr;
+    up_size = 0;
+    const size_t want = std::max<size_t>(blob_bytes + desc_bytes, size_t(4) << 20);
+    if (hipHostMalloc(&up_buf, want, hipHostMallocDefault) != hipSuccess)
+      return fail(EMR_E_NOMEM, "pinned upload staging of %zu bytes failed", want);
+    up_size = want;
+  }
+  char* img = (char*)up_buf;
+  size_t off = 0;
+  for (const Part& p : parts) {
+    std::memcpy(img + off, p.words.data(), p.words.size() * 4);
+    off += p.words.size() * 4;
+  }
+  std::memset(img + off, 0, 16 * 4);
+  std::memcpy(img + blob_bytes, pop->desc.data(), pop->desc.size() * sizeof(emr::ProgDesc));
+  StreamPool* sp = nullptr;
+  emr_status st = stream_pool(&sp);
+  if (st != EMR_OK) return st;
+  HIP_OR_FAIL(hipMemcpyAsync(pop->d_blob, img, blob_bytes, hipMemcpyHostToDevice, sp->aux[0]));
+  if (!pop->desc.empty())
+    HIP_OR_FAIL(hipMemcpyAsync(pop->d_desc, img + blob_bytes,
+                               pop->desc.size() * sizeof(emr::ProgDesc), hipMemcpyHostToDevice,
+                               sp->aux[0]));
+  HIP_OR_FAIL(hipStreamSynchronize(sp->aux[0]));
+  *out = guard.release();
+  return EMR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 emr_status emr_pack_population(const emr_genome* genomes, int32_t n, emr_population** out,
                                int32_t* bad_index) {
   if (bad_index) *bad_index = -1;
   if (!out) return fail(EMR_E_INVAL, "out is NULL");
   if (n < 0 || (n > 0 && !genomes)) return fail(EMR_E_INVAL, "bad genome array");
-  std::vector<uint32_t> blob;
-  std::vector<emr::ProgDesc> desc(2 * (size_t)n);
-  std::vector<emr::GenomeInfo> info(2 * (size_t)n);
+  return pack_and_upload(n, [&](int32_t g) { return genomes[g]; }, out, bad_index);
+}
+
+emr_status emr_pack_population_flat(int32_t n, const int64_t* node_off, const uint8_t* kind,
+                                    const uint8_t* act, const float* bias, const int64_t* edge_off,
+                                    const int32_t* src, const int32_t* dst, const float* w,
+                                    const uint8_t* enabled, emr_population** out,
+                                    int32_t* bad_index) {
+  if (bad_index) *bad_index = -1;
+  if (!out) return fail(EMR_E_INVAL, "out is NULL");
+  if (n < 0 || (n > 0 && (!node_off || !edge_off))) return fail(EMR_E_INVAL, "bad offsets");
+  if (n > 0 && (node_off[0] != 0 || edge_off[0] != 0))
+    return fail(EMR_E_INVAL, "node_off[0] and edge_off[0] must be 0");
   for (int32_t g = 0; g < n; ++g) {
-    emr_status st = EMR_OK;
-    std::string msg;
-    if (!emr::pack_genome(genomes[g], blob, &desc[2 * g], &info[2 * g], &st, &msg)) {
+    const int64_t nn = node_off[g + 1] - node_off[g], ne = edge_off[g + 1] - edge_off[g];
+    if (nn < 0 || ne < 0 || nn > EMR_MAX_NODES || ne > EMR_MAX_EDGES) {
       if (bad_index) *bad_index = g;
-      return fail(st, "genome %d: %s", g, msg.c_str());
+      return fail(nn < 0 || ne < 0 ? EMR_E_INVAL : EMR_E_LIMIT,
+                  "genome %d: %lld nodes, %lld edges", g, (long long)nn, (long long)ne);
     }
-    if (blob.size() > 0xF0000000ull) return fail(EMR_E_LIMIT, "population too large");
   }
-  blob.resize(blob.size() + 16, 0u);  // the kernels may read a few words past a program's end
-  emr_population* p = new (std::nothrow) emr_population;
-  if (!p) return fail(EMR_E_NOMEM, "host allocation failed");
-  p->n_genomes = n;
-  p->desc = std::move(desc);
-  p->info = std::move(info);
-  p->blob_words = blob.size();
-  if (hipMalloc((void**)&p->d_blob, blob.size() * 4) != hipSuccess ||
-      hipMalloc((void**)&p->d_desc, std::max<size_t>(1, p->desc.size()) * sizeof(emr::ProgDesc)) !=
-          hipSuccess) {
-    emr_free_population(p);
-    return fail(EMR_E_NOMEM, "device allocation of %zu words failed", blob.size());
-  }
-  if (hipMemcpy(p->d_blob, blob.data(), blob.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
-      (!p->desc.empty() && hipMemcpy(p->d_desc, p->desc.data(),
-                                     p->desc.size() * sizeof(emr::ProgDesc),
-                                     hipMemcpyHostToDevice) != hipSuccess)) {
-    emr_free_population(p);
-    return fail(EMR_E_DEVICE, "copy of the packed population failed");
-  }
-  // The tables must be complete on the device before any stream reads them: copies from pageable
-  // host memory may still be in flight when hipMemcpy returns, and the caller's stream is not
-  // necessarily ordered after them.
-  if (hipDeviceSynchronize() != hipSuccess) {
-    emr_free_population(p);
-    return fail(EMR_E_DEVICE, "synchronizing the packed population's upload failed");
-  }
-  *out = p;
-  return EMR_OK;
+  if (n > 0 && ((node_off[n] > 0 && (!kind || !act)) ||
+                (edge_off[n] > 0 && (!src || !dst || !w))))
+    return fail(EMR_E_INVAL, "a node or edge array is NULL");
+  auto at = [&](int32_t g) {
+    emr_genome e;
+    const int64_t n0 = node_off[g], e0 = edge_off[g];
+    e.n_nodes = (int32_t)(node_off[g + 1] - n0);
+    e.n_edges = (int32_t)(edge_off[g + 1] - e0);
+    e.kind = kind ? kind + n0 : nullptr;
+    e.act = act ? act + n0 : nullptr;
+    e.bias = bias ? bias + n0 : nullptr;
+    e.src = src ? src + e0 : nullptr;
+    e.dst = dst ? dst + e0 : nullptr;
+    e.w = w ? w + e0 : nullptr;
+    e.enabled = enabled ? enabled + e0 : nullptr;
+    return e;
+  };
+  return pack_and_upload(n, at, out, bad_index);
 }
 
 void emr_free_population(emr_population* pop) {

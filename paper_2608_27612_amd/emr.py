@@ -25,7 +25,7 @@ ABI_FUNCTIONS = [
     "emr_last_error", "emr_version", "emr_grid_count", "emr_build_grids", "emr_pack_population",
     "emr_free_population", "emr_population_info", "emr_workspace_bytes", "emr_discover",
     "emr_result_check", "emr_eval_raw", "emr_discover_cost", "emr_profile_enable",
-    "emr_profile_read", "emr_stream_chunks", "emr_discover_stream",
+    "emr_profile_read", "emr_stream_chunks", "emr_discover_stream", "emr_pack_population_flat",
 ]
 
 
@@ -90,6 +90,7 @@ def lib():
             "emr_profile_enable": (I32, [I32, F64]),
             "emr_profile_read": (I32, [P, I32, P]),
             "emr_stream_chunks": (I32, [I32, I64, P]),
+            "emr_pack_population_flat": (I32, [I32, P, P, P, P, P, P, P, P, P, P, P]),
             "emr_discover_stream": (I32, [P, P, I32, P, I32, I32, F32, I64, I64, SINK, P, P, P]),
         }
         for name, (res, args) in sig.items():
@@ -174,12 +175,47 @@ def _genome_array(genomes):
     return arr, keep
 
 
-def emr_pack_population(genomes) -> Population:
-    """Validate and pack genomes (list of dicts, see workloads.py) into device program tables."""
-    arr, keep = _genome_array(genomes)
+def flat_genomes(genomes):
+    """The concatenated-array layout of emr_pack_population_flat for a list of genome dicts."""
+    n = len(genomes)
+    nn = np.fromiter((len(g["kind"]) for g in genomes), np.int64, n)
+    ne = np.fromiter((len(g["src"]) for g in genomes), np.int64, n)
+    node_off = np.zeros(n + 1, np.int64)
+    edge_off = np.zeros(n + 1, np.int64)
+    np.cumsum(nn, out=node_off[1:])
+    np.cumsum(ne, out=edge_off[1:])
+
+    def cat(key, dtype, per_genome_default):
+        parts = [np.asarray(g[key] if g.get(key) is not None else per_genome_default(g), dtype)
+                 for g in genomes]
+        return np.ascontiguousarray(np.concatenate(parts) if parts else np.zeros(0, dtype), dtype)
+
+    return {
+        "n": n, "node_off": node_off, "edge_off": edge_off,
+        "kind": cat("kind", np.uint8, None), "act": cat("act", np.uint8, None),
+        "bias": cat("bias", np.float32, lambda g: np.zeros(len(g["kind"]), np.float32)),
+        "src": cat("src", np.int32, None), "dst": cat("dst", np.int32, None),
+        "w": cat("w", np.float32, None),
+        "enabled": cat("enabled", np.uint8, lambda g: np.ones(len(g["src"]), np.uint8)),
+    }
+
+
+def emr_pack_population(genomes, layout: str = "flat") -> Population:
+    """Validate and pack genomes (list of dicts, see workloads.py) into device program tables,
+    through emr_pack_population_flat (layout "flat") or emr_pack_population ("structs")."""
     handle = C.c_void_p()
     bad = C.c_int32(-1)
-    st = lib().emr_pack_population(arr, len(genomes), C.byref(handle), C.byref(bad))
+    if layout == "flat":
+        f = flat_genomes(genomes)
+        d = lambda a: a.ctypes.data if len(a) else None  # noqa: E731
+        st = lib().emr_pack_population_flat(f["n"], f["node_off"].ctypes.data, d(f["kind"]),
+                                            d(f["act"]), d(f["bias"]), f["edge_off"].ctypes.data,
+                                            d(f["src"]), d(f["dst"]), d(f["w"]), d(f["enabled"]),
+                                            C.byref(handle), C.byref(bad))
+        keep = f
+    else:
+        arr, keep = _genome_array(genomes)
+        st = lib().emr_pack_population(arr, len(genomes), C.byref(handle), C.byref(bad))
     if st != EMR_OK:
         err = EmrError(st, lib().emr_last_error().decode())
         err.bad_index = bad.value

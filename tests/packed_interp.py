@@ -90,8 +90,8 @@ def interpret(blob, desc, dir_, sx, sy, px, py):
     for k in range(n_un):
         act, ne, eo, bb = (int(v) for v in blob[rec + 4 * k: rec + 4 * k + 4])
         z = f32(bb)
-        for e in range(ne):
-            z += f32(blob[eo + 2 * e + 1]) * U[int(blob[eo + 2 * e])]
+        for e in range(ne):  # edge offsets count from uni_off
+            z += f32(blob[uni_off + eo + 2 * e + 1]) * U[int(blob[uni_off + eo + 2 * e])]
         U[5 + k] = _act(act, np.float64(z))
     fold = rec + 4 * n_un
     folded = []
@@ -100,7 +100,7 @@ def interpret(blob, desc, dir_, sx, sy, px, py):
         nf, fo, bb = int(blob[fold + 4 * t]), int(blob[fold + 4 * t + 1]), int(blob[fold + 4 * t + 2])
         z = f32(bb)
         for e in range(nf):
-            z += f32(blob[fo + 2 * e + 1]) * U[int(blob[fo + 2 * e])]
+            z += f32(blob[uni_off + fo + 2 * e + 1]) * U[int(blob[uni_off + fo + 2 * e])]
         folded.append(z)
     if not (flags & 1):
         assert n_steps == 0 and n_rec == 0

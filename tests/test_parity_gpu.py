@@ -391,3 +391,32 @@ def test_config4_recurrent_depth10_two_phases(emr):
             diff = np.setxor1d(gp, oo["parent"])
             _, dvar = oracle.eval_parents(g, s, diff)
             assert np.all(np.abs(dvar - theta32) <= BAND), (r, diff[:5], dvar[:5])
+
+
+def test_flat_and_struct_packing_agree(emr):
+    """emr_pack_population_flat (threaded packing, concatenated arrays) and emr_pack_population
+    give the same programs: identical raw outputs; validation reports the lowest failing genome."""
+    genomes = W.population(41, 300, 20, 60)
+    sources = W.xor_sources()
+    a = emr.emr_eval_raw(emr.emr_pack_population(genomes, layout="flat"), sources, 5).cpu().numpy()
+    b = emr.emr_eval_raw(emr.emr_pack_population(genomes, layout="structs"), sources, 5).cpu().numpy()
+    np.testing.assert_array_equal(a, b)
+    bad = [dict(g) for g in genomes]
+    for k in (250, 77):  # two failures: the lowest index is reported
+        g = bad[k]
+        src = np.concatenate([g["src"], g["dst"][:1]]).astype(np.int32)
+        dst = np.concatenate([g["dst"], g["src"][:1]]).astype(np.int32)
+        # close a cycle through a hidden node when the genome has one
+        hidden = np.nonzero(np.asarray(g["kind"]) == 5)[0]
+        if len(hidden) == 0:
+            continue
+        h = int(hidden[0])
+        bad[k] = dict(g, src=np.concatenate([g["src"], [h, h]]).astype(np.int32),
+                      dst=np.concatenate([g["dst"], [h, h]]).astype(np.int32),
+                      w=np.concatenate([g["w"], [1.0, 1.0]]).astype(np.float32),
+                      enabled=np.concatenate([np.ones(len(g["src"]), np.uint8), [1, 1]]))
+    for layout in ("flat", "structs"):
+        with pytest.raises(emr.EmrError) as e:
+            emr.emr_pack_population(bad, layout=layout)
+        assert e.value.status == emr.EMR_E_CYCLE
+        assert e.value.bad_index == 77
