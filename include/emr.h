@@ -158,8 +158,9 @@ typedef struct {
 } emr_result;
 
 /* Device scratch (bytes) needed by emr_discover / emr_eval_raw for this population, these
- * sources (host) and this depth: look-back tile status words, per-call group tables and the
- * folded per-(genome, source) biases. Host only. */
+ * sources (host) and this depth: flags, tile status words and the folded per-(genome, source)
+ * biases. Host only. (The grouping tables of a call live with the population: it keeps those of
+ * its last sources and depth on the device, and a call with different ones replaces them.) */
 emr_status emr_workspace_bytes(const emr_population* pop, const emr_source* sources,
                                int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
                                int32_t depth, int64_t* bytes);
@@ -248,20 +249,22 @@ emr_status emr_discover_cost(const emr_population* pop, const emr_source* source
  * algorithmic VALU slots under the cost model of emr_discover_cost, and its duration from a HIP
  * event pair recorded on the call's stream around the launch. */
 typedef struct {
-  int32_t group_size, window, positions, reserved;
+  int32_t group_size, window, positions;
+  int32_t call;  /* profiled call the launch belongs to, counted from 0 */
   int64_t tiles, queries;
   double slots;
   float ms;
 } emr_launch_profile;
 
-/* Enables (on != 0) or disables per-launch event timing for the calling thread's later calls;
- * transcendental_slots is the cost-model weight used for `slots`. Host only. */
+/* Enables (on != 0) or disables per-launch event timing for the calling thread's later calls and
+ * drops the records held; transcendental_slots is the cost-model weight used for `slots`. */
 emr_status emr_profile_enable(int32_t on, double transcendental_slots);
 
-/* Synchronizes on the last profiled call's events and writes up to `cap` launch records to
- * `out` (host); *n receives the number of launches of that call. Records are in launch order:
- * launches go out costliest first, the first on the call's stream and the others (except in the
- * look-back placement mode) on library side streams that run alongside it. */
+/* *n receives the number of launch records held (every launch of the profiled calls since the
+ * last enable or read). With out != NULL, synchronizes on their events, writes up to `cap` of
+ * them to `out` (host) and drops them. Records are in launch order: a call's launches go out
+ * costliest first, the first on the call's stream and the others (except in the look-back
+ * placement mode) on library side streams that run alongside it. */
 emr_status emr_profile_read(emr_launch_profile* out, int32_t cap, int32_t* n);
 
 #ifdef __cplusplus

@@ -68,44 +68,11 @@ int device_cu_count() {
   return cus;
 }
 
-// Pinned staging for the small per-call tables; reused once the previous copy has finished.
-struct Staging {
-  void* ptr = nullptr;
-  size_t size = 0;
-  hipEvent_t done = nullptr;
-  bool pending = false;
-};
-thread_local Staging g_stage;
-
-emr_status stage_upload(const void* src, size_t bytes, void* dev_dst, hipStream_t s) {
-  if (bytes == 0) return EMR_OK;
-  Staging& st = g_stage;
-  if (st.pending) {
-    HIP_OR_FAIL(hipEventSynchronize(st.done));
-    st.pending = false;
-  }
-  if (st.size < bytes) {
-    if (st.ptr) (void)hipHostFree(st.ptr);
-    st.ptr = nullptr;
-    st.size = 0;
-    size_t want = std::max<size_t>(bytes, 1 << 20);
-    if (hipHostMalloc(&st.ptr, want, hipHostMallocDefault) != hipSuccess)
-      return fail(EMR_E_NOMEM, "pinned staging of %zu bytes failed", want);
-    st.size = want;
-  }
-  if (!st.done) HIP_OR_FAIL(hipEventCreateWithFlags(&st.done, hipEventDisableTiming));
-  std::memcpy(st.ptr, src, bytes);
-  HIP_OR_FAIL(hipMemcpyAsync(dev_dst, st.ptr, bytes, hipMemcpyHostToDevice, s));
-  HIP_OR_FAIL(hipEventRecord(st.done, s));
-  st.pending = true;
-  return EMR_OK;
-}
-
 // Streams a call's discover launches run on besides the caller's: one launch per bucket (sources
 // per lane, register window), forked from the caller's stream after the bind kernel and joined
 // back before compaction, so a bucket with little work runs alongside the others instead of after
 // them. Per thread and device; created on first use at default priority.
-constexpr int kAuxStreams = 3;
+constexpr int kAuxStreams = 1;
 struct StreamPool {
   int device = -1;
   hipStream_t aux[kAuxStreams] = {};
@@ -138,8 +105,9 @@ emr_status stream_pool(StreamPool** out) {
 struct Profiler {
   bool on = false;
   double rT = 4.0;
-  std::vector<hipEvent_t> events;        // 2 per launch, created lazily and reused
-  std::vector<emr_launch_profile> recs;  // of the last profiled call
+  int32_t calls = 0;                     // profiled calls since enabled or read
+  std::vector<hipEvent_t> events;        // 2 per record, created lazily and reused
+  std::vector<emr_launch_profile> recs;  // accumulated since enabled or read
 };
 thread_local Profiler g_prof;
 
@@ -195,9 +163,18 @@ struct Plan {
   std::vector<uint32_t> group_member0;  // index of each group's first member
   std::vector<float> src_xy;
   uint64_t bias_floats = 0;
-  // Host image of the per-call tables (groups, members, source coordinates), uploaded to
-  // [off_groups, off_bias) of the workspace.
+  // The plan's tables (groups at t_groups, members at t_members, source coordinates at
+  // t_srcxy): a host image, and its device copy, uploaded on first use and freed with the plan.
   std::vector<char> img;
+  size_t t_groups = 0, t_members = 0, t_srcxy = 0;
+  mutable std::mutex dev_mu;
+  mutable char* d_tables = nullptr;
+  Plan() = default;
+  Plan(const Plan&) = delete;
+  Plan& operator=(const Plan&) = delete;
+  ~Plan() {
+    if (d_tables) (void)hipFree(d_tables);
+  }
   // What the plan was built for (exact copies, compared on reuse).
   std::vector<emr_source> key_sources;
   std::vector<int32_t> key_offs;
@@ -206,8 +183,8 @@ struct Plan {
   // Workspace layout (bytes from the workspace start).
   size_t off_err = 0;      // 64 words: [0] error flags, [1] largest pair count (saturating)
   size_t off_status = 0;
-  size_t off_groups = 0, off_members = 0, off_srcxy = 0, off_bias = 0, total = 0;
-  size_t zero_bytes = 0;   // prefix cleared before each call
+  size_t off_bias = 0, total = 0;
+  size_t status_bytes = 0;  // cleared before a call only for look-back placement
 };
 constexpr int kMaxBuckets = 48;
 
@@ -232,8 +209,7 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
     if (sources[i].dir != EMR_DIR_OUT && sources[i].dir != EMR_DIR_IN)
       return fail(EMR_E_INVAL, "source %d has direction %d", i, sources[i].dir);
 
-  Plan& P = *plan;
-  P = Plan{};
+  Plan& P = *plan;  // a freshly made plan
   P.depth = depth;
   P.n_pairs = offs ? (int64_t)n_sources : (int64_t)G * n_shared;
   P.tiles = emr::tiles_per_pair(depth);
@@ -322,23 +298,24 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
     P.src_xy[2 * i + 1] = sources[i].y;
   }
 
+  // workspace: flags, tile status words, bias rows
   P.off_err = 0;
   P.off_status = 256;
-  P.zero_bytes = align256(P.off_status + (size_t)P.n_pairs * P.tiles * 8);
-  P.off_groups = P.zero_bytes;
-  P.off_members = align256(P.off_groups + P.groups.size() * sizeof(emr::Group));
-  P.off_srcxy = align256(P.off_members + P.members.size() * sizeof(emr::Member));
-  P.off_bias = align256(P.off_srcxy + P.src_xy.size() * sizeof(float));
+  P.status_bytes = (size_t)P.n_pairs * P.tiles * 8;
+  P.off_bias = align256(P.off_status + P.status_bytes);
   P.total = align256(P.off_bias + P.bias_floats * sizeof(float));
-  P.img.assign(P.off_bias - P.off_groups, 0);
+  // tables
+  P.t_groups = 0;
+  P.t_members = align256(P.groups.size() * sizeof(emr::Group));
+  P.t_srcxy = align256(P.t_members + P.members.size() * sizeof(emr::Member));
+  P.img.assign(align256(P.t_srcxy + P.src_xy.size() * sizeof(float)) + 256, 0);
   if (!P.groups.empty())
-    std::memcpy(P.img.data(), P.groups.data(), P.groups.size() * sizeof(emr::Group));
+    std::memcpy(P.img.data() + P.t_groups, P.groups.data(), P.groups.size() * sizeof(emr::Group));
   if (!P.members.empty())
-    std::memcpy(P.img.data() + (P.off_members - P.off_groups), P.members.data(),
+    std::memcpy(P.img.data() + P.t_members, P.members.data(),
                 P.members.size() * sizeof(emr::Member));
   if (!P.src_xy.empty())
-    std::memcpy(P.img.data() + (P.off_srcxy - P.off_groups), P.src_xy.data(),
-                P.src_xy.size() * sizeof(float));
+    std::memcpy(P.img.data() + P.t_srcxy, P.src_xy.data(), P.src_xy.size() * sizeof(float));
   P.key_sources.assign(sources, sources + n_sources);
   P.key_has_offs = offs != nullptr;
   if (offs) P.key_offs.assign(offs, offs + G + 1);
@@ -382,23 +359,69 @@ emr_status plan_for(const emr_population* pop, const emr_source* sources, int32_
   return EMR_OK;
 }
 
-// Clears the workspace's flags and tile words, uploads the call's tables and runs the bind kernel.
+// The plan's tables on the device, uploaded (and waited for) on first use.
+emr_status plan_tables(const Plan& P, char** out) {
+  std::lock_guard<std::mutex> lock(P.dev_mu);
+  if (!P.d_tables) {
+    char* d = nullptr;
+    if (hipMalloc((void**)&d, P.img.size()) != hipSuccess)
+      return fail(EMR_E_NOMEM, "device tables of %zu bytes", P.img.size());
+    StreamPool* sp = nullptr;
+    emr_status st = stream_pool(&sp);
+    if (st == EMR_OK &&
+        (hipMemcpyAsync(d, P.img.data(), P.img.size(), hipMemcpyHostToDevice, sp->aux[0]) !=
+             hipSuccess ||
+         hipStreamSynchronize(sp->aux[0]) != hipSuccess))
+      st = fail(EMR_E_DEVICE, "upload of the call tables failed");
+    if (st != EMR_OK) {
+      (void)hipFree(d);
+      return st;
+    }
+    P.d_tables = d;
+  }
+  *out = P.d_tables;
+  return EMR_OK;
+}
+
+// 256 zero bytes in pinned memory (clears a workspace's flags with one async copy).
+emr_status zero_block(const void** out) {
+  static void* z = nullptr;
+  static std::mutex mu;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!z) {
+    if (hipHostMalloc(&z, 256, hipHostMallocDefault) != hipSuccess) {
+      z = nullptr;
+      return fail(EMR_E_NOMEM, "pinned zero block");
+    }
+    std::memset(z, 0, 256);
+  }
+  *out = z;
+  return EMR_OK;
+}
+
+// Clears the workspace's flags (and its tile status words when the look-back placement needs
+// them) and runs the bind kernel over the plan's tables.
 emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspace,
-                        int64_t workspace_bytes, hipStream_t s) {
+                        int64_t workspace_bytes, hipStream_t s, bool clear_status) {
   if (!workspace || workspace_bytes < (int64_t)P.total)
     return fail(EMR_E_INVAL, "workspace of %lld bytes is smaller than the %zu needed",
                 (long long)workspace_bytes, P.total);
   if (((uintptr_t)workspace & 255) != 0) return fail(EMR_E_INVAL, "workspace not 256-byte aligned");
   char* ws = (char*)workspace;
-  HIP_OR_FAIL(emr_launch_fill(ws, (int64_t)(P.zero_bytes / 4), 0u, s));
-  emr_status st = stage_upload(P.img.data(), P.img.size(), ws + P.off_groups, s);
+  char* tables = nullptr;
+  emr_status st = plan_tables(P, &tables);
   if (st != EMR_OK) return st;
+  const void* zeros = nullptr;
+  if ((st = zero_block(&zeros)) != EMR_OK) return st;
+  HIP_OR_FAIL(hipMemcpyAsync(ws + P.off_err, zeros, 256, hipMemcpyHostToDevice, s));
+  if (clear_status)
+    HIP_OR_FAIL(emr_launch_fill(ws + P.off_status, (int64_t)(P.status_bytes / 4), 0u, s));
 
   emr::BindArgs b{};
   b.blob = pop->d_blob;
   b.desc = pop->d_desc;
-  b.members = (const emr::Member*)(ws + P.off_members);
-  b.src_xy = (const float*)(ws + P.off_srcxy);
+  b.members = (const emr::Member*)(tables + P.t_members);
+  b.src_xy = (const float*)(tables + P.t_srcxy);
   b.bias_tab = (float*)(ws + P.off_bias);
   b.err = (uint32_t*)(ws + P.off_err);
   b.n_members = (uint32_t)P.members.size();
@@ -417,6 +440,9 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
                         const emr_result* out, float* raw, void* workspace, hipStream_t s,
                         int64_t tile_lo, int64_t n_tiles) {
   char* ws = (char*)workspace;
+  char* tables = nullptr;
+  emr_status tst = plan_tables(P, &tables);
+  if (tst != EMR_OK) return tst;
   const int cus = device_cu_count();
   const int64_t parent_lo = emr::tile_parent_offset(tile_lo, P.depth);
   const int64_t range_parents = emr::tile_parent_offset(tile_lo + n_tiles, P.depth) - parent_lo;
@@ -428,9 +454,9 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
     return fail(EMR_E_INVAL, "a tile range needs pair_capacity >= its %lld parents",
                 (long long)range_parents);
   Profiler& prof = g_prof;
+  const size_t rec0 = prof.recs.size();
   if (prof.on) {
-    prof.recs.clear();
-    while (prof.events.size() < 2 * P.buckets.size()) {
+    while (prof.events.size() < 2 * (rec0 + P.buckets.size())) {
       hipEvent_t e;
       HIP_OR_FAIL(hipEventCreate(&e));
       prof.events.push_back(e);
@@ -456,7 +482,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
     }
     emr::DiscoverArgs a{};
     a.blob = pop->d_blob;
-    a.groups = (const emr::Group*)(ws + P.off_groups) + bk.first;
+    a.groups = (const emr::Group*)(tables + P.t_groups) + bk.first;
     a.bias_tab = (const float*)(ws + P.off_bias);
     a.status = (uint64_t*)(ws + P.off_status);
     a.err = (uint32_t*)(ws + P.off_err);
@@ -478,11 +504,12 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
     a.n_pairs = (uint32_t)P.n_pairs;
     a.bias_floats = P.bias_floats;
     const uint32_t blocks = (uint32_t)cus * 16;  // the launcher sizes the grid below this
-    if (prof.on) HIP_OR_FAIL(hipEventRecord(prof.events[2 * bi], ls));
+    if (prof.on) HIP_OR_FAIL(hipEventRecord(prof.events[2 * (rec0 + bi)], ls));
     HIP_OR_FAIL(emr_launch_discover(&a, bk.window, mode, blocks, ls));
     if (prof.on) {
-      HIP_OR_FAIL(hipEventRecord(prof.events[2 * bi + 1], ls));
+      HIP_OR_FAIL(hipEventRecord(prof.events[2 * (rec0 + bi) + 1], ls));
       emr_launch_profile r{};
+      r.call = prof.calls;
       r.group_size = bk.S;
       r.window = bk.window;
       r.positions = emr::positions_per_lane(bk.S, bk.window);
@@ -500,6 +527,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
       prof.recs.push_back(r);
     }
   }
+  if (prof.on) prof.calls++;
   if (fork)
     for (int k = 0; k < kAuxStreams; ++k)
       if (aux_used[k]) {
@@ -517,12 +545,38 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
   return EMR_OK;
 }
 
+// The last call's flags (error bits, largest pair count), copied to pinned memory on its stream
+// so that emr_result_check on the same workspace only waits for them.
+struct FlagReadback {
+  uint32_t* host = nullptr;
+  hipEvent_t done = nullptr;
+  const void* ws = nullptr;
+};
+thread_local FlagReadback g_flags;
+
+emr_status queue_flags_readback(void* workspace, hipStream_t s) {
+  FlagReadback& f = g_flags;
+  f.ws = nullptr;
+  if (!f.host && hipHostMalloc((void**)&f.host, 64, hipHostMallocDefault) != hipSuccess) {
+    f.host = nullptr;
+    return EMR_OK;  // the check then reads the workspace itself
+  }
+  if (!f.done) HIP_OR_FAIL(hipEventCreateWithFlags(&f.done, hipEventDisableTiming));
+  HIP_OR_FAIL(hipMemcpyAsync(f.host, workspace, 8, hipMemcpyDeviceToHost, s));
+  HIP_OR_FAIL(hipEventRecord(f.done, s));
+  f.ws = workspace;
+  return EMR_OK;
+}
+
 // Enqueue a whole call: prepare, then every tile of every pair.
 emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const emr_result* out,
                     float* raw, void* workspace, int64_t workspace_bytes, hipStream_t s) {
-  emr_status st = prepare_plan(pop, P, workspace, workspace_bytes, s);
+  const bool lookback = out && !raw && out->pair_capacity < emr::n_parents(P.depth);
+  emr_status st = prepare_plan(pop, P, workspace, workspace_bytes, s, lookback);
   if (st != EMR_OK) return st;
-  return launch_range(pop, P, theta, out, raw, workspace, s, 0, P.tiles);
+  st = launch_range(pop, P, theta, out, raw, workspace, s, 0, P.tiles);
+  if (st != EMR_OK) return st;
+  return queue_flags_readback(workspace, s);
 }
 
 }  // namespace
@@ -780,7 +834,12 @@ emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max
   // Workspace words 0 and 1: the error flags and the largest pair count of the call.
   uint32_t w2[2] = {0, 0};
   int64_t mx = 0;
-  if (out->workspace) {
+  if (out->workspace && g_flags.ws == out->workspace) {
+    HIP_OR_FAIL(hipEventSynchronize(g_flags.done));
+    w2[0] = g_flags.host[0];
+    w2[1] = g_flags.host[1];
+    mx = w2[1];
+  } else if (out->workspace) {
     HIP_OR_FAIL(hipMemcpy(w2, out->workspace, 8, hipMemcpyDeviceToHost));
     mx = w2[1];
   } else if (n_pairs > 0) {
@@ -831,19 +890,23 @@ emr_status emr_profile_enable(int32_t on, double transcendental_slots) {
   g_prof.on = on != 0;
   g_prof.rT = transcendental_slots;
   g_prof.recs.clear();
+  g_prof.calls = 0;
   return EMR_OK;
 }
 
 emr_status emr_profile_read(emr_launch_profile* out, int32_t cap, int32_t* n) {
   Profiler& prof = g_prof;
   if (n) *n = (int32_t)prof.recs.size();
+  if (!out) return EMR_OK;
   for (size_t i = 0; i < prof.recs.size(); ++i) {
     HIP_OR_FAIL(hipEventSynchronize(prof.events[2 * i + 1]));
     float ms = 0.0f;
     HIP_OR_FAIL(hipEventElapsedTime(&ms, prof.events[2 * i], prof.events[2 * i + 1]));
     prof.recs[i].ms = ms;
-    if (out && (int32_t)i < cap) out[i] = prof.recs[i];
+    if ((int32_t)i < cap) out[i] = prof.recs[i];
   }
+  prof.recs.clear();
+  prof.calls = 0;
   return EMR_OK;
 }
 
@@ -963,7 +1026,7 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
       return fail(EMR_E_NOMEM, "pinned counts of a streamed call");
   }
 
-  st = prepare_plan(pop, P, R.ws, (int64_t)P.total, R.s);
+  st = prepare_plan(pop, P, R.ws, (int64_t)P.total, R.s, false);
   if (st != EMR_OK) return st;
   emr_result chunk_out{R.pad_parent, R.pad_w4, cap, R.counts, R.ws, (int64_t)P.total};
 

@@ -53,7 +53,7 @@ class emr_result(C.Structure):
 
 class emr_launch_profile(C.Structure):
     _fields_ = [("group_size", C.c_int32), ("window", C.c_int32), ("positions", C.c_int32),
-                ("reserved", C.c_int32), ("tiles", C.c_int64), ("queries", C.c_int64),
+                ("call", C.c_int32), ("tiles", C.c_int64), ("queries", C.c_int64),
                 ("slots", C.c_double), ("ms", C.c_float)]
 
 
@@ -351,14 +351,18 @@ def emr_profile_enable(on: bool = True, transcendental_slots: float = 4.0):
 
 
 def emr_profile_read():
-    """Per-launch records of the last profiled call (synchronizes on its events)."""
+    """Every launch record held (profiled calls since enable or the last read), in launch order;
+    synchronizes on their events and drops them. "first" marks a call's first launch."""
     n = C.c_int32()
     _check(lib().emr_profile_read(None, 0, C.byref(n)))
     arr = (emr_launch_profile * max(1, n.value))()
     _check(lib().emr_profile_read(arr, n.value, C.byref(n)))
-    return [{"S": r.group_size, "W": r.window, "P": r.positions, "tiles": r.tiles,
-             "queries": r.queries, "first": i == 0,
-             "slots": r.slots, "ms": r.ms} for i, r in enumerate(arr[:n.value])]
+    out = []
+    for i, r in enumerate(arr[:n.value]):
+        out.append({"S": r.group_size, "W": r.window, "P": r.positions, "call": r.call,
+                    "tiles": r.tiles, "queries": r.queries, "slots": r.slots, "ms": r.ms,
+                    "first": i == 0 or arr[i - 1].call != r.call})
+    return out
 
 
 # ----------------------------------------------------------------------------- streaming
