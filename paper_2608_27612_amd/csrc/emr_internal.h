@@ -118,14 +118,19 @@ constexpr uint64_t kStatusAggregate = 1ull << 62;
 constexpr uint64_t kStatusInclusive = 2ull << 62;
 constexpr uint64_t kStatusValueMask = (1ull << 62) - 1;
 
-// Positions per lane per program walk for S sources and window W: the largest of 8, 4, 2, 1 whose
-// M = S P value windows fit the register budget and whose estimated VGPR total (accumulators,
-// windows, positions, outputs and variance temporaries) leaves room for 3 waves per SIMD.
+// Positions per lane per program walk. A lane holds whole sibling quads: the four children of
+// one parent (P = 4) or of two parents in consecutive tiles (P = 8), so a cell's variance is
+// computed inside the lane. S sources of one genome share the walk (M = S P instances); a
+// (S, P, W) combination fits when the M value windows fit the register budget and the estimated
+// VGPR total (accumulators, windows, positions, per-source variances and ~16 others) leaves room
+// for 3 waves per SIMD.
 EMR_HD constexpr bool fits_lane(int S, int P, int W) {
-  return S * P * W <= kWindowRegs && S * P <= 16 && 16 + 3 * S * P + S * P * W + 2 * P <= 168;
+  return S * P * W <= kWindowRegs && 16 + S * P + S * P * W + 2 * P + 2 * S <= 168;
 }
-EMR_HD constexpr int positions_per_lane(int S, int W) {
-  return fits_lane(S, 8, W) ? 8 : fits_lane(S, 4, W) ? 4 : fits_lane(S, 2, W) ? 2 : 1;
+EMR_HD constexpr int positions_per_lane(int S, int W) { return fits_lane(S, 8, W) ? 8 : 4; }
+// Sources per walk for window W: the most that fit with P = 4.
+EMR_HD constexpr int max_group(int W) {
+  return fits_lane(4, 4, W) ? 4 : fits_lane(3, 4, W) ? 3 : fits_lane(2, 4, W) ? 2 : 1;
 }
 
 // Level helpers shared by host and device.

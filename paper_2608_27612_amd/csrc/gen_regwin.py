@@ -1,7 +1,8 @@
 #!/usr/bin/env python3
 """Generates regwin_gen.h: the program-record step of the discover kernel, as inline assembly.
 
-A lane evaluates M = S * P CPPN instances at once (S sources of one genome at P grid positions).
+A lane evaluates M = S * P CPPN instances at once (S sources of one genome at P grid positions:
+the four children of one or two parent cells).
 Instance m = s * P + j keeps
   - its accumulator in v[ACC + m], and
   - its position-dependent node values in a VGPR tuple v[base(m) .. base(m) + W - 1].
@@ -18,7 +19,9 @@ single site inside the program loop and the compiler never needs to move them:
   3. the tail, through a branch table on meta bits 0..3: the node's activation, whose last
      instruction writes straight into the destination slot of every tuple (DST indexing), or, for
      the output node, the activation in place on the accumulators; nothing for a continuation
-     record.
+     record. The accumulator holds the node's input already multiplied by its activation's input
+     scale (the packer scales the weights and biases), which leaves 1 to 4 instructions per
+     activation.
 
 The statement declares SCC and M0 as clobbered: its scalar arithmetic writes SCC, and the
 register-indexing instructions write M0.
@@ -26,9 +29,9 @@ register-indexing instructions write M0.
 Hazards: the statement is opaque to the compiler's hazard recognizer, so it keeps the one that
 applies here itself: a non-transcendental VALU instruction that reads the result of a
 transcendental one (v_exp, v_rcp, v_sin) needs one wait state in between; every such pair below
-is at least M >= 3 instructions apart. The output tails end with s_nop 1, since the caller reads
-the accumulators next, possibly with DPP (two wait states after a VALU write). Branch targets are computed from label differences, so the
-jump arithmetic follows the assembler's actual encodings.
+is at least M >= 4 instructions apart, and the output tails end with s_nop 1, since the caller
+reads the accumulators next. Branch targets are computed from label differences, so the jump
+arithmetic follows the assembler's actual encodings.
 
 Inline assembly needs literal register names, so every variant is spelled out here.
 Run from this directory: python gen_regwin.py > regwin_gen.h
@@ -42,19 +45,20 @@ SLOT_BITS = 5
 
 def fits_lane(S, P, W):
     """The positions-per-lane policy of the kernels (emr_internal.h), restated."""
-    return S * P * W <= 128 and S * P <= 16 and 16 + 3 * S * P + S * P * W + 2 * P <= 168
+    return S * P * W <= 128 and 16 + S * P + S * P * W + 2 * P + 2 * S <= 168
 
 
 def positions_per_lane(S, W):
-    return next(P for P in (8, 4, 2, 1) if P == 1 or fits_lane(S, P, W))
+    return 8 if fits_lane(S, 8, W) else 4
+
+
+def max_group(W):
+    return next(S for S in (4, 3, 2, 1) if S == 1 or fits_lane(S, 4, W))
 
 
 # (S, P, W) variants
-VARIANTS = [(S, positions_per_lane(S, W), W) for W in (8, 16, 32) for S in (1, 2, 3, 4)]
+VARIANTS = [(S, positions_per_lane(S, W), W) for W in (8, 16, 32) for S in range(1, max_group(W) + 1)]
 
-NEG_LOG2E = "0xbfb8aa3b"       # -log2(e) as float bits
-NEG_2LOG2E = "0xc038aa3b"      # -2 log2(e)
-INV_2PI = "0.15915494"         # 1/(2 pi): an inline constant of the ISA
 ACTS = ["lin", "sig", "tanh", "gau", "sin", "abs"]  # activation ids 0..5
 
 
@@ -138,15 +142,21 @@ def gen_walker(S, P, W):
             out += ["s_nop 1", "s_branch .Lx_%="]  # the caller may read these with DPP next
         return out
 
+    # The packer scales every weight and bias feeding a varying node by its activation's input
+    # scale (emr_internal.h), so the accumulator holds z' = c z and the tails are short:
+    #   sigmoid  c = -log2 e:     1 / (1 + 2^z')
+    #   tanh     c = -2 log2 e:   2 / (1 + 2^z') - 1
+    #   gaussian c = sqrt(log2 e): 2^-(z'^2)
+    #   sine     c = 1 / (2 pi):  v_sin_f32 (the sine of 2 pi times its input) of fract(z'), which
+    #                             is exact and in [0, 1)
     defs = {
         "lin": ([], "v_mov_b32 {d}, {a}"),
         "abs": ([], "v_and_b32 {d}, 0x7fffffff, {a}"),
-        "sig": (["v_mul_f32 {a}, %s, {a}" % NEG_LOG2E, "v_exp_f32 {a}, {a}",
-                 "v_add_f32 {a}, 1.0, {a}"], "v_rcp_f32 {d}, {a}"),
-        "tanh": (["v_mul_f32 {a}, %s, {a}" % NEG_2LOG2E, "v_exp_f32 {a}, {a}",
-                  "v_add_f32 {a}, 1.0, {a}", "v_rcp_f32 {a}, {a}"], "v_fma_f32 {d}, {a}, 2.0, -1.0"),
-        "gau": (["v_mul_f32 {a}, {a}, {a}", "v_mul_f32 {a}, %s, {a}" % NEG_LOG2E],
-                "v_exp_f32 {d}, {a}"),
+        "sig": (["v_exp_f32 {a}, {a}", "v_add_f32 {a}, 1.0, {a}"], "v_rcp_f32 {d}, {a}"),
+        "tanh": (["v_exp_f32 {a}, {a}", "v_add_f32 {a}, 1.0, {a}", "v_rcp_f32 {a}, {a}"],
+                 "v_fma_f32 {d}, {a}, 2.0, -1.0"),
+        "gau": (["v_mul_f32_e64 {a}, {a}, -{a}"], "v_exp_f32 {d}, {a}"),
+        "sin": (["v_fract_f32 {a}, {a}"], "v_sin_f32 {d}, {a}"),
     }
     for store in (True, False):
         for name, (pre, final) in defs.items():
@@ -154,28 +164,6 @@ def gen_walker(S, P, W):
                 L += [".Llino_%=:", "s_branch .Lx_%="]
                 continue
             L += block(name + ("" if store else "o"), pre, final, store)
-    # sine: k = rint(z / 2pi) kept in the destination slot (whose old value is dead here; the
-    # output node's slot is 0 and no value is live after it), z - k 2pi with a two-part 2pi
-    # (Cody-Waite) in the accumulator, then the hardware sine of the reduced argument in
-    # revolutions, written to the slot (store) or the accumulator (output)
-    for store in (True, False):
-        L.append(".Lsin%s_%%=:" % ("" if store else "o"))
-        L.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
-        L += ["v_mul_f32 %s, %s, %s" % (T[m], INV_2PI, A[m]) for m in range(M)]
-        L.append("s_set_gpr_idx_mode gpr_idx(SRC0,DST)")
-        L += ["v_rndne_f32 %s, %s" % (T[m], T[m]) for m in range(M)]
-        L.append("s_set_gpr_idx_mode gpr_idx(SRC0)")
-        L += ["v_fma_f32 %s, -%s, %%[hi], %s" % (A[m], T[m], A[m]) for m in range(M)]
-        L += ["v_fma_f32 %s, -%s, %%[lo], %s" % (A[m], T[m], A[m]) for m in range(M)]
-        L.append("s_set_gpr_idx_off")
-        L += ["v_mul_f32 %s, %s, %s" % (A[m], INV_2PI, A[m]) for m in range(M)]
-        if store:
-            L.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
-            L += ["v_sin_f32 %s, %s" % (T[m], A[m]) for m in range(M)]
-            L.append("s_branch .Lxo_%=")
-        else:
-            L += ["v_sin_f32 %s, %s" % (A[m], A[m]) for m in range(M)]
-            L += ["s_nop 1", "s_branch .Lx_%="]
     L += [".Lxo_%=:", "s_set_gpr_idx_off", ".Lx_%=:"]
 
     outs = ['[pc] "=&{s[%d:%d]}"(pc)' % (PC, PC + 1), '[t] "=&s"(t)', '[u] "=&s"(u)']
@@ -189,7 +177,6 @@ def gen_walker(S, P, W):
            '[sw1] "s"(r[4])'] + ['[w%d] "s"(r[%d])' % (p, 5 + p) for p in range(MAX_EDGES)]
     ins += ['[b%d] "s"(b[%d])' % (s, s) for s in range(S)]
     ins += ['[x%d] "v"(x[%d]), [y%d] "v"(y[%d])' % (j, j, j, j) for j in range(P)]
-    ins += ['[hi] "s"(hi), [lo] "s"(lo)']
 
     body = "\n".join('        "%s\\n"' % l for l in L)
     vec = "f32x%d" % W
@@ -204,9 +191,9 @@ def gen_walker(S, P, W):
         out.append("    v%d = (%s)(0.0f);" % (m, vec))
     out.append("  }")
     out.append("  // r: the record's 16 words; b: the node's bias row (one float per source);")
-    out.append("  // x, y: the P positions; hi, lo: the two parts of 2 pi.")
+    out.append("  // x, y: the P positions.")
     out.append("  __device__ __forceinline__ void step(const uint32_t* r, const float* b, "
-               "const float* x, const float* y, float hi, float lo) {")
+               "const float* x, const float* y) {")
     out.append("    uint64_t pc;")
     out.append("    uint32_t t, u;")
     out.append("    float tb;" if S == 1 else "    float l[%d];" % P)
@@ -221,29 +208,6 @@ def gen_walker(S, P, W):
     return "\n".join(out) + "\n"
 
 
-def gen_quad(M):
-    """s[m] = the sum over the lane's quad of (w - quad mean)^2, for m < M, stage by stage:
-    t = w + perm1(w); t = t + perm2(t); t = w - t/4; t = t*t; t = t + perm1(t); t = t + perm2(t)
-    (perm1 swaps lanes 0<->1, 2<->3 of each quad, perm2 swaps the pairs). A DPP instruction reads
-    a VGPR two wait states after a VALU write at the earliest: each stage reads the previous one
-    M >= 3 instructions back, and the statement starts with s_nop 1 for its inputs."""
-    p1 = "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1"
-    p2 = "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf bound_ctrl:1"
-    L = ["s_nop 1"]
-    L += ["v_add_f32_dpp %%[t%d], %%[w%d], %%[w%d] %s" % (m, m, m, p1) for m in range(M)]
-    L += ["v_add_f32_dpp %%[t%d], %%[t%d], %%[t%d] %s" % (m, m, m, p2) for m in range(M)]
-    L += ["v_fmamk_f32 %%[t%d], %%[t%d], 0xbe800000, %%[w%d]" % (m, m, m) for m in range(M)]
-    L += ["v_mul_f32 %%[t%d], %%[t%d], %%[t%d]" % (m, m, m) for m in range(M)]
-    L += ["v_add_f32_dpp %%[t%d], %%[t%d], %%[t%d] %s" % (m, m, m, p1) for m in range(M)]
-    L += ["v_add_f32_dpp %%[t%d], %%[t%d], %%[t%d] %s" % (m, m, m, p2) for m in range(M)]
-    body = "\n".join('        "%s\\n"' % l for l in L)
-    outs = ",\n          ".join('[t%d] "=&v"(s[%d])' % (m, m) for m in range(M))
-    ins = ",\n          ".join('[w%d] "v"(w[%d])' % (m, m) for m in range(M))
-    return ("template <> __device__ __forceinline__ void quad_sumsq_dev<%d>(const float* w, "
-            "float* s) {\n    asm volatile(\n%s\n        : %s\n        : %s);\n}\n"
-            % (M, body, outs, ins))
-
-
 def main():
     print("// Generated by gen_regwin.py (the program-record step of the discover kernel).")
     print("// Do not edit; regenerate with: python gen_regwin.py > regwin_gen.h")
@@ -253,11 +217,6 @@ def main():
     print()
     for S, P, W in VARIANTS:
         print(gen_walker(S, P, W))
-    print("// Sum of squared deviations from the quad mean, for M values per lane at once.")
-    print("template <int M> __device__ void quad_sumsq_dev(const float* w, float* s);")
-    print()
-    for M in sorted(set(S * P for S, P, W in VARIANTS)):
-        print(gen_quad(M))
 
 
 if __name__ == "__main__":

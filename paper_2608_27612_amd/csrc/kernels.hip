@@ -4,13 +4,13 @@
 //   k_fill      clears the look-back status words and counters of a workspace.
 //   k_bind      evaluates the position-independent part of each (genome, source) CPPN once and
 //               folds it into per-step biases (one thread per source).
-//   k_discover  the hot path: one lane per grid position; each lane interprets the varying CPPN
-//               program for S sources of one genome at once (Section 3.1, the batched query W),
-//               reduces the four siblings of each cell to their variance with DPP quad
-//               permutes, applies var > theta (Section 3.2, Eq. 2), and compacts the kept cells
-//               with a wave ballot plus a per-pair decoupled look-back scan, so every pair's
-//               records land in ascending parent order with no second pass and no atomics on
-//               the output.
+//   k_discover  the hot path: one lane per parent cell; each lane interprets the varying CPPN
+//               program for S sources of one genome at the cell's four children at once
+//               (Section 3.1, the batched query W), reduces the four siblings to their variance
+//               in registers, applies var > theta (Section 3.2, Eq. 2), and places the kept cells
+//               with a wave ballot at per-tile slots (compacted by k_compact) or through a
+//               per-pair decoupled look-back scan, so every pair's records land in ascending
+//               parent order with no atomics on the output.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -24,8 +24,9 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x32 __attribute__((ext_vector_type(32)));
 
 // ------------------------------------------------------------------------ activations
-// Hardware v_exp_f32 (2^x), v_rcp_f32 and v_sin_f32 (sin of 2*pi*x) with the range reductions
-// their inputs need. Errors stay near 1e-7 absolute for |z| up to a few hundred.
+// The bind kernel's activations (uniform nodes): hardware v_exp_f32 (2^x), v_rcp_f32 and
+// v_sin_f32 (sin of 2*pi*x) with the range reductions their inputs need. Errors stay near 1e-7
+// absolute for |z| up to a few hundred. (Varying nodes are activated inside the record step.)
 constexpr float kLog2e = 1.44269504088896341f;
 constexpr float kInv2Pi = 0.159154943091895336f;
 constexpr float k2PiHi = 6.28318548202514648f;      // nearest float to 2*pi
@@ -81,10 +82,6 @@ __device__ __forceinline__ int level_of(uint32_t p) {
 __device__ __forceinline__ uint32_t lane_id() {
   return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
 }
-// var > theta (Section 3.2, Eq. 2) is tested as s2 > 4 theta, where s2 = the sum over the quad of
-// the squared deviations from the quad mean = 4 var (quad_sumsq_dev, generated): both scalings by
-// 4 are exact, barring overflow or a subnormal variance. The sums are pairwise, (w0+w1)+(w2+w3),
-// and each lane adds its neighbour's value to its own, so all four lanes hold the same bits.
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
 __device__ __forceinline__ uint32_t popc64(uint64_t m) { return __builtin_popcountll(m); }
 __device__ __forceinline__ uint32_t mbcnt64(uint64_t m) {
@@ -217,30 +214,34 @@ struct Row {
 };
 __device__ __forceinline__ Row load_row(cf32* p) { return Row{{p[0], p[1], p[2], p[3]}}; }
 
-// S sources of one genome and direction per group; each lane evaluates them at P positions at once
-// (M = S * P instances; instance m = s * P + j is source s at position block j). One walk of the
-// program therefore serves M queries per lane. A walk covers TPW = P / 4 whole tiles when P >= 4,
-// else a quarter or half of one tile (NPASS = 4 / P walks per tile).
+// S sources of one genome and direction per group. A lane holds the four children (grid indices
+// 4 q .. 4 q + 3) of TPW = P / 4 parent cells q, one in each tile of the walk, and evaluates the S
+// sources at those P positions at once (M = S * P instances; instance m = s * P + 4 k + c is
+// source s at child c of the lane's parent in tile k). One walk of the program therefore serves
+// M queries per lane, and a cell's variance is formed inside the lane.
 template <int S, int P, int W, int MODE>
 __global__ void __launch_bounds__(256)
     k_discover(const uint32_t* __restrict__ blob, const Group* __restrict__ groups,
                const float* __restrict__ bias_tab, uint64_t* __restrict__ status,
                uint32_t* __restrict__ err, uint32_t* __restrict__ parent, float* __restrict__ w4,
                int64_t* __restrict__ pair_count, float* __restrict__ raw, DiscoverScalars a) {
+  static_assert(P == 4 || P == 8, "a lane holds whole sibling quads");
   constexpr int M = S * P;
-  constexpr int TPW = P >= kTileIters ? P / kTileIters : 1;  // tiles per walk
-  constexpr int NPASS = P >= kTileIters ? 1 : kTileIters / P;  // walks per tile
-  constexpr int KB = TPW * kTileIters;                        // 64-position blocks per tile set
+  constexpr int TPW = P / kTileIters;  // tiles per walk
   // (the launcher makes chunk_tiles a multiple of TPW, so a walk's tiles lie in one chunk)
   const uint32_t lane = lane_id();
-  // Within a level-aligned tile the grid index's 6 low bits are the lane id; its Morton bits give
-  // the low 3 bits of the cell's column (even bits) and row (odd bits).
+  // Lane l holds parent q0 + l of a tile whose first parent is q0. In a level-aligned tile the
+  // children's Morton indices are m0 + 4 l + c (m0 a multiple of 256): lane bits 0, 2, 4 are the
+  // cell column's bits 1..3, lane bits 1, 3, 5 the row's, and child c adds column bit 0 = c & 1
+  // and row bit 0 = c >> 1. Eq. 1: x = (2 column + 1) 2^-level - 1, and likewise y.
   const uint32_t i_lo = (lane & 1u) | ((lane >> 1) & 2u) | ((lane >> 2) & 4u);
   const uint32_t j_lo = ((lane >> 1) & 1u) | ((lane >> 2) & 2u) | ((lane >> 3) & 4u);
-  const float i_lo_f = (float)(2u * i_lo);
-  const float j_lo_f = (float)(2u * j_lo);
-  const uint32_t head_len =
-      (uint32_t)(a.depth < kFirstAlignedLevel ? a.n_pos : level_offset(kFirstAlignedLevel));
+  const float xl[2] = {(float)(4u * i_lo), (float)(4u * i_lo + 2u)};
+  const float yl[2] = {(float)(4u * j_lo), (float)(4u * j_lo + 2u)};
+  // parents in the head tile (levels 1..3, or all levels of a shallower grid)
+  const uint32_t head_parents = (uint32_t)(a.depth < kFirstAlignedLevel
+                                               ? n_parents(a.depth)
+                                               : level_offset(kFirstAlignedLevel) / 4);
 
   Walker<S, P, W> R;
   R.init();
@@ -281,162 +282,130 @@ __global__ void __launch_bounds__(256)
 
     for (uint32_t t0 = chunk_tile; t0 < chunk_tile + a.chunk_tiles && t0 < a.tiles; t0 += TPW) {
       // ---- geometry of the walk's tiles (t0 counts from the launch's first tile, tile_lo). The
-      // pair's tile 0 holds levels 1..3 (84 positions); every other
-      // tile 256 positions of one level, starting at Morton index m0 of level lvl. m0 is a
-      // multiple of 256, so the tile's 64-position blocks it = 0..3 have Morton prefixes
-      // (m0 >> 6) | it, whose column and row bits are those of m0 >> 6 with it's two bits or-ed in.
-      uint32_t p0[TPW], n_valid[TPW], cx[TPW], cy[TPW];
-      float scale[TPW];
+      // pair's tile 0 holds the parents of levels 1..3 (21 of them; the positions decoded one by
+      // one); every other tile 64 parents of one level, whose 256 children start at grid index p0.
+      uint32_t p0[TPW];
+      uint64_t vmask[TPW];  // lanes holding a queried parent
+      float px[P], py[P];
 #pragma unroll
       for (int k = 0; k < TPW; ++k) {
         const uint32_t tile = a.tile_lo + t0 + k;  // the pair's tile index
         const bool in_range = t0 + k < a.tiles;
-        p0[k] = 0;
-        n_valid[k] = !in_range ? 0u : (tile == 0 ? head_len : (uint32_t)kTile);
-        scale[k] = 1.0f;
-        cx[k] = cy[k] = 0;
-        if (tile != 0 && in_range) {
-          p0[k] = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(tile - 1) * kTile);
-          const int lvl = (31 - __builtin_clz(3u * p0[k] + 4u)) >> 1;
-          const uint32_t m0 = p0[k] - (uint32_t)level_offset(lvl);
-          scale[k] = pow2_neg(lvl);
-          cx[k] = compact_even(m0 >> 6);
-          cy[k] = compact_even(m0 >> 7);
-        }
-      }
-      uint32_t run[S][TPW];  // records so far per source and tile (padded mode)
+        if (tile == 0) {
+          p0[k] = 0;
+          vmask[k] = !in_range ? 0ull : head_parents >= 64u ? ~0ull : (1ull << head_parents) - 1ull;
 #pragma unroll
-      for (int s = 0; s < S; ++s)
-#pragma unroll
-        for (int k = 0; k < TPW; ++k) run[s][k] = 0;
-      float wbuf[KB][S];  // look-back mode only: outputs and decisions of the tiles
-      uint64_t keep[KB][S];
-      if constexpr (MODE == kModeLookback) {
-#pragma unroll
-        for (int b = 0; b < KB; ++b)
-#pragma unroll
-          for (int s = 0; s < S; ++s) {
-            wbuf[b][s] = 0.0f;
-            keep[b][s] = 0ull;
-          }
-      }
-
-#pragma unroll MODE == kModeLookback ? NPASS : 1
-      for (int pass = 0; pass < NPASS; ++pass) {
-        if (TPW == 1 && (uint32_t)(pass * P * kWave) >= n_valid[0]) break;
-        // ---- positions of this walk (Eq. 1 cell centres, decoded from the grid index)
-        float px[P], py[P];
-        uint64_t vmask[P];  // lanes holding a position (all but the head tile's tail, and none
-                            // of a tile past the pair's last)
-#pragma unroll
-        for (int j = 0; j < P; ++j) {
-          const int k = P >= kTileIters ? j / kTileIters : 0;
-          const uint32_t it = P >= kTileIters ? (uint32_t)(j % kTileIters) : (uint32_t)(pass * P + j);
-          const uint32_t first = it * kWave;  // uniform: lanes [0, n_valid - first) are valid
-          if (a.tile_lo + t0 + k != 0) {
-            vmask[j] = t0 + k < a.tiles ? ~0ull : 0ull;
-            const float bx =
-                __builtin_fmaf((float)(16u * (cx[k] | (it & 1u)) + 1u), scale[k], -1.0f);
-            const float by =
-                __builtin_fmaf((float)(16u * (cy[k] | (it >> 1)) + 1u), scale[k], -1.0f);
-            px[j] = __builtin_fmaf(i_lo_f, scale[k], bx);
-            py[j] = __builtin_fmaf(j_lo_f, scale[k], by);
-          } else {
-            vmask[j] = first >= n_valid[k] ? 0ull
-                       : (n_valid[k] - first >= (uint32_t)kWave
-                              ? ~0ull
-                              : ((1ull << (n_valid[k] - first)) - 1ull));
-            const uint32_t p = first + lane;
+          for (int c = 0; c < 4; ++c) {
+            const uint32_t p = 4u * lane + (uint32_t)c;
             const int l = level_of(p);
             const uint32_t mm = p - (uint32_t)level_offset(l);
             const float sc = pow2_neg(l);
-            px[j] = __builtin_fmaf((float)(2u * compact_even(mm) + 1u), sc, -1.0f);
-            py[j] = __builtin_fmaf((float)(2u * compact_even(mm >> 1) + 1u), sc, -1.0f);
-          }
-        }
-
-        // ---- CPPN (Section 2): the varying program in topological order, M instances at once.
-        // Records are processed in pairs (A, B; the record count is even) so that the next
-        // record and its bias row are always being loaded into the other buffer while the
-        // current one is computed. Record r reads bias row 1 + r. A uniform output is the
-        // constant of row 0 (its program has no records).
-        if (out_varying) {
-          cu32* rp = cblob + G.var_off;
-          cf32* bp = cbias + G.bias_off + 4;
-          Rec A = load_rec(rp);
-          Row ra = load_row(bp);
-          for (uint32_t r = 0; r < G.n_rec; r += 2) {
-            const Rec B = load_rec(rp + kRecWords);
-            const Row rb = load_row(bp + 4);
-            R.step(A.w, ra.b, px, py, k2PiHi, k2PiLo);
-            rp += 2 * kRecWords;
-            bp += 8;
-            A = load_rec(rp);
-            ra = load_row(bp);
-            R.step(B.w, rb.b, px, py, k2PiHi, k2PiLo);
+            px[4 * k + c] = __builtin_fmaf((float)(2u * compact_even(mm) + 1u), sc, -1.0f);
+            py[4 * k + c] = __builtin_fmaf((float)(2u * compact_even(mm >> 1) + 1u), sc, -1.0f);
           }
         } else {
+          p0[k] = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(tile - 1) * kTile);
+          vmask[k] = in_range ? ~0ull : 0ull;
+          const int lvl = level_of(p0[k]);
+          const uint32_t m0 = p0[k] - (uint32_t)level_offset(lvl);
+          const float sc = pow2_neg(lvl);
+          const float bx = __builtin_fmaf((float)(32u * compact_even(m0 >> 8) + 1u), sc, -1.0f);
+          const float by = __builtin_fmaf((float)(32u * compact_even(m0 >> 9) + 1u), sc, -1.0f);
 #pragma unroll
-          for (int m = 0; m < M; ++m) R.acc[m] = orow.b[m / P];
-        }
-        // the output node's activation was applied by its record's tail
-        const float* w = R.acc;
-
-        // grid index of block j's position in this lane
-        auto pos_index = [&](int j) -> uint32_t {
-          const int k = P >= kTileIters ? j / kTileIters : 0;
-          const uint32_t it = P >= kTileIters ? (uint32_t)(j % kTileIters) : (uint32_t)(pass * P + j);
-          return p0[k] + it * kWave + lane;
-        };
-        if constexpr (MODE == kModeRaw) {
-#pragma unroll
-          for (int s = 0; s < S; ++s)
-#pragma unroll
-            for (int j = 0; j < P; ++j)
-              if ((vmask[j] >> lane) & 1ull)
-                raw[(int64_t)G.pair[s] * a.n_pos + pos_index(j)] = w[s * P + j];
-          continue;
-        }
-        // ---- variance of the four siblings (Section 3.2) and the threshold test (Eq. 2), for
-        // all M instances in lockstep. Nearly every quad is dropped, so one test on the maximum
-        // over the instances decides whether any record is kept at all.
-        float s2[M];
-        quad_sumsq_dev<M>(w, s2);
-        float mx = s2[0];
-#pragma unroll
-        for (int m = 1; m < M; ++m) mx = __builtin_fmaxf(mx, s2[m]);
-        const bool some = ballot(mx > a.theta4) != 0ull;
-        if constexpr (MODE == kModeLookback) {
-#pragma unroll
-          for (int s = 0; s < S; ++s)
-#pragma unroll
-            for (int j = 0; j < P; ++j) {
-              const int b = P >= kTileIters ? j : pass * P + j;
-              keep[b][s] = some ? ballot(s2[s * P + j] > a.theta4) & vmask[j] : 0ull;
-              wbuf[b][s] = w[s * P + j];
-            }
-        } else if (some) {
-#pragma unroll
-          for (int s = 0; s < S; ++s) {
-#pragma unroll
-            for (int j = 0; j < P; ++j) {
-              const int k = P >= kTileIters ? j / kTileIters : 0;
-              const uint64_t kb = ballot(s2[s * P + j] > a.theta4) & vmask[j];
-              if (kb == 0ull) continue;
-              if ((kb >> lane) & 1ull) {
-                // a tile's records start at its first parent index within the pair
-                const int64_t slot = (int64_t)G.pair[s] * a.cap + ((p0[k] >> 2) - a.parent_lo) +
-                                     run[s][k] + (mbcnt64(kb) >> 2);
-                w4[slot * 4 + (lane & 3u)] = w[s * P + j];
-                if ((lane & 3u) == 0) parent[slot] = pos_index(j) >> 2;
-              }
-              run[s][k] += popc64(kb) >> 2;
-            }
+          for (int c = 0; c < 4; ++c) {
+            px[4 * k + c] = __builtin_fmaf(xl[c & 1], sc, bx);
+            py[4 * k + c] = __builtin_fmaf(yl[c >> 1], sc, by);
           }
         }
       }
 
+      // ---- CPPN (Section 2): the varying program in topological order, M instances at once.
+      // Records are processed in pairs (A, B; the record count is even) so that the next
+      // record and its bias row are always being loaded into the other buffer while the
+      // current one is computed. Record r reads bias row 1 + r. A uniform output is the
+      // constant of row 0 (its program has no records).
+      if (out_varying) {
+        cu32* rp = cblob + G.var_off;
+        cf32* bp = cbias + G.bias_off + 4;
+        Rec A = load_rec(rp);
+        Row ra = load_row(bp);
+        for (uint32_t r = 0; r < G.n_rec; r += 2) {
+          const Rec B = load_rec(rp + kRecWords);
+          const Row rb = load_row(bp + 4);
+          R.step(A.w, ra.b, px, py);
+          rp += 2 * kRecWords;
+          bp += 8;
+          A = load_rec(rp);
+          ra = load_row(bp);
+          R.step(B.w, rb.b, px, py);
+        }
+      } else {
+#pragma unroll
+        for (int m = 0; m < M; ++m) R.acc[m] = orow.b[m / P];
+      }
+      // the output node's activation was applied by its record's tail
+      const float* w = R.acc;
+
+      if constexpr (MODE == kModeRaw) {
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+#pragma unroll
+          for (int k = 0; k < TPW; ++k)
+            if ((vmask[k] >> lane) & 1ull) {
+              float* o = raw + (int64_t)G.pair[s] * a.n_pos + p0[k] + 4u * lane;
+#pragma unroll
+              for (int c = 0; c < 4; ++c) o[c] = w[s * P + 4 * k + c];
+            }
+        continue;
+      }
+      // ---- variance of the four siblings (Section 3.2) and the threshold test (Eq. 2), inside
+      // the lane: s2 = the sum of the squared deviations from their mean = 4 var, tested as
+      // s2 > 4 theta (both scalings by 4 exact, barring overflow or a subnormal variance).
+      float s2[S][TPW];
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+#pragma unroll
+        for (int k = 0; k < TPW; ++k) {
+          const float* q = w + s * P + 4 * k;
+          const float sum = (q[0] + q[1]) + (q[2] + q[3]);
+          const float d0 = __builtin_fmaf(sum, -0.25f, q[0]);
+          const float d1 = __builtin_fmaf(sum, -0.25f, q[1]);
+          const float d2 = __builtin_fmaf(sum, -0.25f, q[2]);
+          const float d3 = __builtin_fmaf(sum, -0.25f, q[3]);
+          s2[s][k] = __builtin_fmaf(d3, d3, __builtin_fmaf(d2, d2, __builtin_fmaf(d1, d1, d0 * d0)));
+        }
+      // Nearly every cell is dropped: one test on the maximum decides whether any record is kept.
+      float mx = s2[0][0];
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+#pragma unroll
+        for (int k = 0; k < TPW; ++k) mx = __builtin_fmaxf(mx, s2[s][k]);
+      const bool some = ballot(mx > a.theta4) != 0ull;
+
       if constexpr (MODE == kModePadded) {
+        uint32_t run[S][TPW];  // records so far per source and tile
+        if (some) {
+#pragma unroll
+          for (int s = 0; s < S; ++s)
+#pragma unroll
+            for (int k = 0; k < TPW; ++k) {
+              const uint64_t kb = ballot(s2[s][k] > a.theta4) & vmask[k];
+              run[s][k] = popc64(kb);
+              if ((kb >> lane) & 1ull) {
+                // a tile's records start at its first parent index within the pair
+                const int64_t slot = (int64_t)G.pair[s] * a.cap + ((p0[k] >> 2) - a.parent_lo) +
+                                     mbcnt64(kb);
+                parent[slot] = (p0[k] >> 2) + lane;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) w4[slot * 4 + c] = w[s * P + 4 * k + c];
+              }
+            }
+        } else {
+#pragma unroll
+          for (int s = 0; s < S; ++s)
+#pragma unroll
+            for (int k = 0; k < TPW; ++k) run[s][k] = 0;
+        }
         if (lane == 0) {
 #pragma unroll
           for (int s = 0; s < S; ++s)
@@ -454,28 +423,22 @@ __global__ void __launch_bounds__(256)
           if (tile >= a.tiles) break;
 #pragma unroll
           for (int s = 0; s < S; ++s) {
-            uint64_t cnt = 0;
-#pragma unroll
-            for (int it = 0; it < kTileIters; ++it) cnt += popc64(keep[k * kTileIters + it][s]) >> 2;
+            const uint64_t kb = some ? ballot(s2[s][k] > a.theta4) & vmask[k] : 0ull;
+            const uint64_t cnt = popc64(kb);
             const uint32_t pair = G.pair[s];
-            uint64_t base = lookback(status + (int64_t)pair * a.tiles, tile, cnt, err);
+            const uint64_t base = lookback(status + (int64_t)pair * a.tiles, tile, cnt, err);
             if (tile + 1 == a.tiles && lane == 0) {
               pair_count[pair] = (int64_t)(base + cnt);
               raise_max(err + 1, (uint32_t)min(base + cnt, (uint64_t)0xFFFFFFFFu));
             }
-            const int64_t region = (int64_t)pair * a.cap;
+            if ((kb >> lane) & 1ull) {
+              const int64_t idx = (int64_t)base + (int64_t)mbcnt64(kb);
+              if (idx < a.cap) {
+                const int64_t slot = (int64_t)pair * a.cap + idx;
+                parent[slot] = (p0[k] >> 2) + lane;
 #pragma unroll
-            for (int it = 0; it < kTileIters; ++it) {
-              const uint64_t m = keep[k * kTileIters + it][s];
-              if ((m >> lane) & 1ull) {
-                const int64_t idx = (int64_t)base + (int64_t)(mbcnt64(m) >> 2);
-                if (idx < a.cap) {
-                  w4[(region + idx) * 4 + (lane & 3u)] = wbuf[k * kTileIters + it][s];
-                  if ((lane & 3u) == 0)
-                    parent[region + idx] = (p0[k] + (uint32_t)it * kWave + lane) >> 2;
-                }
+                for (int c = 0; c < 4; ++c) w4[slot * 4 + c] = w[s * P + 4 * k + c];
               }
-              base += popc64(m) >> 2;
             }
           }
         }
@@ -751,7 +714,7 @@ extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
 template <int S, int W, int MODE>
 static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks, hipStream_t s) {
   constexpr int P = emr::positions_per_lane(S, W);
-  constexpr int TPW = P >= emr::kTileIters ? P / emr::kTileIters : 1;
+  constexpr int TPW = P / emr::kTileIters;
   auto kern = emr::k_discover<S, P, W, MODE>;
   int dev = 0, cus = 0;
   hipError_t e;
@@ -817,9 +780,11 @@ static hipError_t launch_discover_w(const emr::DiscoverArgs* a, int window, uint
   const int S = (int)a->group_size;
 #define EMR_CASE(S_, W_) \
   if (S == S_ && window == W_) return launch_discover_t<S_, W_, MODE>(a, blocks, s);
-  EMR_CASE(1, 8) EMR_CASE(2, 8) EMR_CASE(3, 8) EMR_CASE(4, 8)
-  EMR_CASE(1, 16) EMR_CASE(2, 16) EMR_CASE(3, 16) EMR_CASE(4, 16)
-  EMR_CASE(1, 32) EMR_CASE(2, 32) EMR_CASE(3, 32) EMR_CASE(4, 32)
+  static_assert(emr::max_group(8) == 3 && emr::max_group(16) == 2 && emr::max_group(32) == 1,
+                "the instantiated (S, window) variants");
+  EMR_CASE(1, 8) EMR_CASE(2, 8) EMR_CASE(3, 8)
+  EMR_CASE(1, 16) EMR_CASE(2, 16)
+  EMR_CASE(1, 32)
 #undef EMR_CASE
   return hipErrorInvalidValue;
 }

@@ -18,6 +18,25 @@
 
 namespace emr {
 
+// Input scale of each activation for varying nodes: the packer multiplies every weight and bias
+// that feeds a varying node by it, so the kernel's activation code starts from c z (see the record
+// tails of the discover kernel): sigmoid and tanh need -log2 e and -2 log2 e (for 2^x), the
+// gaussian sqrt(log2 e) (2^-(c z)^2 = e^-z^2), the sine 1 / (2 pi) (the hardware sine takes
+// revolutions). Each scaled value is the product of the float weight and the exact constant,
+// rounded once.
+static double act_input_scale(int act) {
+  const double log2e = 1.4426950408889634074;
+  const double inv_2pi = 0.15915494309189533577;
+  switch (act) {
+    case EMR_ACT_SIGMOID: return -log2e;
+    case EMR_ACT_TANH: return -2.0 * log2e;
+    case EMR_ACT_GAUSS: return 1.2011224087864497555;  // sqrt(log2 e)
+    case EMR_ACT_SINE: return inv_2pi;
+    default: return 1.0;
+  }
+}
+static float scaled(float w, double c) { return (float)((double)w * c); }
+
 namespace {
 
 struct Err {
@@ -247,6 +266,7 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       }
       const bool is_out = out_varying && v == out_node;
       const uint32_t dst = is_out ? 0u : (uint32_t)assigned[v];
+      const double c_act = act_input_scale(g.act[v]);
       const size_t ne = node_edges.size();
       const size_t n_chunks = ne == 0 ? 1 : (ne + kRecEdges - 1) / kRecEdges;
       for (size_t c = 0; c < n_chunks; ++c) {
@@ -256,8 +276,8 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
         uint32_t meta = ((uint32_t)(k1 - k0) << kRecEdgeShift) | (dst << kRecDstShift);
         if (c == 0) {
           meta |= kRecFirst;
-          blob[r + 1] = fbits(ax);
-          blob[r + 2] = fbits(ay);
+          blob[r + 1] = fbits(scaled(ax, c_act));
+          blob[r + 2] = fbits(scaled(ay, c_act));
         }
         if (c + 1 == n_chunks) meta |= (is_out ? kRecTailOutput : kRecTailStore) + g.act[v];
         blob[r] = meta;
@@ -266,7 +286,7 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
         for (size_t k = k0; k < k1; ++k) {
           const size_t e = k1 - 1 - k;
           blob[r + 3 + e / 6] |= node_edges[k].first << (kSlotBits * (e % 6));
-          blob[r + 5 + e] = fbits(node_edges[k].second);
+          blob[r + 5 + e] = fbits(scaled(node_edges[k].second, c_act));
         }
         n_rec++;
       }
@@ -308,18 +328,19 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
     }
     for (int t = 0; t < (int)vsteps.size(); ++t) {
       int v = vsteps[t];
+      const double c_act = act_input_scale(g.act[v]);  // the fold feeds the scaled accumulator
       uint32_t first = (uint32_t)blob.size(), cnt = 0;
       for (int ei : in_edges[v]) {
         const Edge& E = edges[ei];
         if (!live[E.src] || varying[E.src]) continue;
         blob.push_back((uint32_t)uidx[E.src]);
-        blob.push_back(fbits(E.w));
+        blob.push_back(fbits(scaled(E.w, c_act)));
         cnt++;
       }
       uint32_t* r = &blob[ub + 4 + 4 * unodes.size() + 4 * t];
       r[0] = cnt;
       r[1] = first - (uint32_t)ub;
-      r[2] = fbits(g.bias ? g.bias[v] : 0.0f);
+      r[2] = fbits(scaled(g.bias ? g.bias[v] : 0.0f, c_act));
       r[3] = first_rec[t];
     }
     d.uni_end = (uint32_t)blob.size();

@@ -215,7 +215,7 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
   P.tiles = emr::tiles_per_pair(depth);
   if (P.n_pairs > 0xFFFFFFFFll) return fail(EMR_E_LIMIT, "too many pairs");
 
-  // Group each genome's sources by direction, in source order, into sets of <= kMaxGroup.
+  // Group each genome's sources by direction, in source order, into sets of <= max_group(window).
   struct TmpGroup {
     emr::Group g;
     int S, window;
@@ -229,6 +229,8 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
       const uint32_t di = 2u * (uint32_t)g + (uint32_t)dir;
       const emr::ProgDesc& d = pop->desc[di];
       const int wb = window_bucket(pop->info[di].window);
+      if (wb < 0) return fail(EMR_E_LIMIT, "genome %d needs a value window of %d", g, pop->info[di].window);
+      const int gmax = emr::max_group(wb);
       TmpGroup cur{};
       int n = 0;
       auto flush = [&]() {
@@ -250,7 +252,7 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
         const int64_t pair = offs ? (int64_t)j : (int64_t)g * n_shared + j;
         cur.g.pair[n] = (uint32_t)pair;
         cur.src[n] = (uint32_t)j;
-        if (++n == emr::kMaxGroup) flush();
+        if (++n == gmax) flush();
       }
       flush();
     }

@@ -70,6 +70,20 @@ def _act(a, z):
     raise ValueError(a)
 
 
+def _act_scaled(a, zs):
+    """A varying node's activation of its scaled input zs = c z, with the input scales the packer
+    applies (sigmoid -log2 e, tanh -2 log2 e, gaussian sqrt(log2 e), sine 1 / (2 pi))."""
+    if a == 1:
+        return 1.0 / (1.0 + np.exp2(zs))
+    if a == 2:
+        return 2.0 / (1.0 + np.exp2(zs)) - 1.0
+    if a == 3:
+        return np.exp2(-zs * zs)
+    if a == 4:
+        return np.sin(2.0 * np.pi * (zs - np.floor(zs)))
+    return _act(a, zs)
+
+
 def f32(u):
     return float(np.array([u], np.uint32).view(np.float32)[0])
 
@@ -140,9 +154,9 @@ def interpret(blob, desc, dir_, sx, sy, px, py):
         assert 1 <= tail <= 12
         if tail <= 6:
             assert dst < window
-            vals[dst] = _act(tail - 1, acc)
+            vals[dst] = _act_scaled(tail - 1, acc)
         else:
-            out = _act(tail - 7, acc)
+            out = _act_scaled(tail - 7, acc)
         acc = None
         step += 1
     assert step == n_steps and out is not None and n_rec % 2 == 0
