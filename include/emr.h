@@ -244,10 +244,12 @@ emr_status emr_discover_cost(const emr_population* pop, const emr_source* source
 
 /* ------------------------------------------------------------------ profiling */
 
-/* One discover-kernel launch of the last profiled emr_discover / emr_eval_raw call on this thread:
- * its variant (sources per lane S, register window W, positions per lane P), tiles, queries,
- * algorithmic VALU slots under the cost model of emr_discover_cost, and its duration from a HIP
- * event pair recorded on the call's stream around the launch. */
+/* One discover-kernel launch of a profiled emr_discover / emr_eval_raw call on this thread (a call
+ * makes one launch for every tile range it covers: one for emr_discover, one per chunk when
+ * streamed): the variant of its costliest part (sources per walk S, register window W, positions
+ * per lane P), its tiles, queries and algorithmic VALU slots over all its parts under the cost
+ * model of emr_discover_cost, and its duration from a HIP event pair recorded on the call's stream
+ * around the launch. */
 typedef struct {
   int32_t group_size, window, positions;
   int32_t call;  /* profiled call the launch belongs to, counted from 0 */
@@ -256,15 +258,16 @@ typedef struct {
   float ms;
 } emr_launch_profile;
 
-/* Enables (on != 0) or disables per-launch event timing for the calling thread's later calls and
- * drops the records held; transcendental_slots is the cost-model weight used for `slots`. */
-emr_status emr_profile_enable(int32_t on, double transcendental_slots);
+/* Sets per-launch event timing for the calling thread's later calls and drops the records held:
+ * on = 0 off, 1 every discover launch, 2 only the first discover launch of a call; `every` >= 1:
+ * only one call in `every` is timed (the first, then every `every`-th), which keeps the events'
+ * own cost off the other calls. transcendental_slots is the cost-model weight used for `slots`.
+ * EMR_E_INVAL for another `on` or `every` < 1. */
+emr_status emr_profile_enable(int32_t on, int32_t every, double transcendental_slots);
 
-/* *n receives the number of launch records held (every launch of the profiled calls since the
- * last enable or read). With out != NULL, synchronizes on their events, writes up to `cap` of
- * them to `out` (host) and drops them. Records are in launch order: a call's launches go out
- * costliest first, the first on the call's stream and the others (except in the look-back
- * placement mode) on library side streams that run alongside it. */
+/* *n receives the number of launch records held (the timed launches of the profiled calls since
+ * the last enable or read). With out != NULL, synchronizes on their events, writes up to `cap` of
+ * them to `out` (host) and drops them. Records are in launch order. */
 emr_status emr_profile_read(emr_launch_profile* out, int32_t cap, int32_t* n);
 
 #ifdef __cplusplus

@@ -25,6 +25,7 @@ constexpr int kWindows[] = {8, 16, 32};
 constexpr int kMaxWindow = 32;
 // Sources evaluated together by one lane (same genome, same direction).
 constexpr int kMaxGroup = 4;
+constexpr int kMaxParts = 6;  // (sources per walk, register window) variants of a launch
 // Register budget of the value windows: S sources x P positions x W slots <= 128 VGPRs per lane.
 constexpr int kWindowRegs = 128;
 // Positions per wave iteration and iterations per tile.
@@ -52,7 +53,6 @@ constexpr int kFirstAlignedLevel = 4;     // first level whose size is a multipl
 // A record with n edges uses positions 0..n-1 and they are accumulated from position n-1 down
 // to 0, so the packer stores the node's edges in reverse.
 // The node's bias is not stored here: it is the per-source folded bias from the bind kernel.
-// n_rec is even: an odd program is padded with one all-zero record, which does nothing.
 constexpr uint32_t kRecWords = 16;
 constexpr uint32_t kRecEdges = 11;
 constexpr uint32_t kRecTailMask = 15u;
@@ -158,7 +158,7 @@ EMR_HD inline int64_t tile_parent_offset(int64_t T, int depth) {
 
 struct DiscoverArgs {
   const uint32_t* blob;
-  const Group* groups;
+  const Group* groups;     // the plan's group table (parts index into it)
   const float* bias_tab;
   uint64_t* status;        // [n_pairs_total * tiles]
   uint32_t* err;           // device error flags
@@ -168,14 +168,15 @@ struct DiscoverArgs {
   float* raw;              // raw-output mode: [pair][N]
   int64_t cap;             // records per pair region
   int64_t n_pos;           // N(depth)
-  uint32_t n_groups;
+  // The launch's parts: groups part_group0[k] .. + part_groups[k] - 1, with part_S[k] sources
+  // per walk and register window part_W[k], in launch order.
+  uint32_t n_parts;
+  uint32_t part_S[kMaxParts], part_W[kMaxParts], part_group0[kMaxParts], part_groups[kMaxParts];
   uint32_t tile_lo;        // first tile of the launch (of every pair)
   uint32_t parent_lo;      // first parent index of tile tile_lo (record slots count from it)
   uint32_t tiles;          // tiles of the launch per pair
-  uint32_t n_tiles;        // n_groups * tiles
   int32_t depth;
   float theta;
-  uint32_t group_size;     // members per group (S) for this launch
   uint32_t blob_words;     // size of the population table
   uint32_t n_pairs;        // pairs of the call (bound for pair ids)
   uint64_t bias_floats;    // size of the bias table

@@ -38,7 +38,6 @@ Run from this directory: python gen_regwin.py > regwin_gen.h
 """
 
 ACC = 4
-PC = 36  # SGPR pair s[PC:PC+1] for the computed jumps (bound as an early-clobber output)
 MAX_EDGES = 11
 SLOT_BITS = 5
 
@@ -76,56 +75,99 @@ def bfe_imm(offset, width):
     return "0x%x" % (offset | (width << 16))
 
 
+# Fixed scalar registers of the walk statement: the current record (16 words), the current bias
+# row (4 floats), the record and row pointers, and the computed-jump PC pair.
+REC = 40   # s[40:55]: meta, ax, ay, sw0, sw1, w0..w10
+ROW = 56   # s[56:59]
+RP = 60    # s[60:61]
+BP = 62    # s[62:63]
+PC = 64    # s[64:65]
+
+
 def gen_walker(S, P, W):
     M = S * P
     A = ["v%d" % (ACC + m) for m in range(M)]
     T = ["v%d" % base(M, m, W) for m in range(M)]
+    meta, ax, ay = "s%d" % REC, "s%d" % (REC + 1), "s%d" % (REC + 2)
+    sw = ["s%d" % (REC + 3), "s%d" % (REC + 4)]
+    wt = ["s%d" % (REC + 5 + p) for p in range(MAX_EDGES)]
+    bias = ["s%d" % (ROW + s) for s in range(S)]
+    pc = "s[%d:%d]" % (PC, PC + 1)
     L = []
-    # ---- 1. first record of a node: the accumulator starts at bias + ax x + ay y
-    L += ["s_bitcmp1_b32 %[meta], 4", "s_cbranch_scc0 .Lni_%="]
+    # ---- a program without records (uniform output): the outputs are the constants of row 0
+    L += ["s_cmp_lg_u32 %[n], 0",
+          "s_cbranch_scc1 .Lstart_%=",
+          "s_load_dwordx4 s[%d:%d], s[%d:%d], 0x0" % (ROW, ROW + 3, BP, BP + 1),
+          "s_waitcnt lgkmcnt(0)"]
+    L += ["v_mov_b32 %s, %s" % (A[s * P + j], bias[s]) for s in range(S) for j in range(P)]
+    L += ["s_branch .Ldone_%="]
+    # ---- else load record 0 and its row (row 1)
+    L += [".Lstart_%=:",
+          "s_add_u32 s%d, s%d, 16" % (BP, BP),
+          "s_addc_u32 s%d, s%d, 0" % (BP + 1, BP + 1),
+          "s_load_dwordx16 s[%d:%d], s[%d:%d], 0x0" % (REC, REC + 15, RP, RP + 1),
+          "s_load_dwordx4 s[%d:%d], s[%d:%d], 0x0" % (ROW, ROW + 3, BP, BP + 1)]
+    # ---- one record per iteration; its record and row were loaded during the previous one
+    L += [".Lrec_%=:",
+          "s_waitcnt lgkmcnt(0)",
+          "s_add_u32 s%d, s%d, 64" % (RP, RP),
+          "s_addc_u32 s%d, s%d, 0" % (RP + 1, RP + 1)]
+    # 1. first record of a node: the accumulator starts at bias + ax x + ay y
+    L += ["s_bitcmp1_b32 %s, 4" % meta, "s_cbranch_scc0 .Lni_%="]
     if S == 1:
-        L.append("v_mov_b32 %[tb], %[b0]")
-        L += ["v_fma_f32 %s, %%[x%d], %%[ax], %%[tb]" % (A[j], j) for j in range(P)]
-        L += ["v_fma_f32 %s, %%[y%d], %%[ay], %s" % (A[j], j, A[j]) for j in range(P)]
+        L.append("v_mov_b32 %%[tb], %s" % bias[0])
+        L += ["v_fma_f32 %s, %%[x%d], %s, %%[tb]" % (A[j], j, ax) for j in range(P)]
+        L += ["v_fma_f32 %s, %%[y%d], %s, %s" % (A[j], j, ay, A[j]) for j in range(P)]
     else:
-        L += ["v_mul_f32 %%[l%d], %%[ax], %%[x%d]" % (j, j) for j in range(P)]
-        L += ["v_fma_f32 %%[l%d], %%[y%d], %%[ay], %%[l%d]" % (j, j, j) for j in range(P)]
-        L += ["v_add_f32 %s, %%[b%d], %%[l%d]" % (A[s * P + j], s, j)
+        L += ["v_mul_f32 %%[l%d], %s, %%[x%d]" % (j, ax, j) for j in range(P)]
+        L += ["v_fma_f32 %%[l%d], %%[y%d], %s, %%[l%d]" % (j, j, ay, j) for j in range(P)]
+        L += ["v_add_f32 %s, %s, %%[l%d]" % (A[s * P + j], bias[s], j)
               for s in range(S) for j in range(P)]
-    L.append(".Lni_%=:")
-    # ---- 2. edges: jump to block 11 - n; block i handles record position 10 - i
-    L += ["s_bfe_u32 %[t], %[meta], 0x40010",
+    # the row is read: load the next record's
+    L += [".Lni_%=:",
+          "s_load_dwordx4 s[%d:%d], s[%d:%d], 0x10" % (ROW, ROW + 3, BP, BP + 1),
+          "s_add_u32 s%d, s%d, 16" % (BP, BP),
+          "s_addc_u32 s%d, s%d, 0" % (BP + 1, BP + 1)]
+    # 2. edges: jump to block 11 - n; block i handles record position 10 - i
+    L += ["s_bfe_u32 %%[t], %s, 0x40010" % meta,
           "s_min_u32 %%[t], %%[t], %d" % MAX_EDGES,  # a 4-bit count above 11 is clamped
           "s_mul_i32 %[t], %[t], (.Le1_%= - .Le0_%=)",
           "s_sub_u32 %[t], (.Lee_%= - .Lep_%=), %[t]",
           "s_set_gpr_idx_on %[t], gpr_idx(SRC0)",
-          "s_getpc_b64 s[%d:%d]" % (PC, PC + 1),
+          "s_getpc_b64 %s" % pc,
           ".Lep_%=:",
           "s_add_u32 s%d, s%d, %%[t]" % (PC, PC),
           "s_addc_u32 s%d, s%d, 0" % (PC + 1, PC + 1),
-          "s_setpc_b64 s[%d:%d]" % (PC, PC + 1)]
+          "s_setpc_b64 %s" % pc]
     for i in range(MAX_EDGES):
         p = MAX_EDGES - 1 - i
         L.append(".Le%d_%%=:" % i)
-        L.append("s_bfe_u32 %%[t], %%[sw%d], %s" % (p // 6, bfe_imm(SLOT_BITS * (p % 6), log2(W))))
+        L.append("s_bfe_u32 %%[t], %s, %s" % (sw[p // 6], bfe_imm(SLOT_BITS * (p % 6), log2(W))))
         L.append("s_set_gpr_idx_idx %[t]")
-        L += ["v_fma_f32 %s, %s, %%[w%d], %s" % (A[m], T[m], p, A[m]) for m in range(M)]
+        L += ["v_fma_f32 %s, %s, %s, %s" % (A[m], T[m], wt[p], A[m]) for m in range(M)]
     L += [".Lee_%=:", "s_set_gpr_idx_off"]
-    # ---- 3. tail: branch table on meta & 15
-    L += ["s_and_b32 %[t], %[meta], 15",
+    # 3. tail: branch table on meta & 15; the record is read once the table index and the
+    # destination slot are taken, so the next record is loaded while the activation runs
+    L += ["s_and_b32 %%[t], %s, 15" % meta,
           "s_lshl_b32 %[t], %[t], 2",
           "s_add_u32 %[t], %[t], (.Lt0_%= - .Ltp_%=)",
-          "s_bfe_u32 %%[u], %%[meta], %s" % bfe_imm(8, log2(W)),
-          "s_getpc_b64 s[%d:%d]" % (PC, PC + 1),
+          "s_bfe_u32 %%[u], %s, %s" % (meta, bfe_imm(8, log2(W))),
+          "s_load_dwordx16 s[%d:%d], s[%d:%d], 0x0" % (REC, REC + 15, RP, RP + 1),
+          "s_getpc_b64 %s" % pc,
           ".Ltp_%=:",
           "s_add_u32 s%d, s%d, %%[t]" % (PC, PC),
           "s_addc_u32 s%d, s%d, 0" % (PC + 1, PC + 1),
-          "s_setpc_b64 s[%d:%d]" % (PC, PC + 1),
+          "s_setpc_b64 %s" % pc,
           ".Lt0_%=:"]
     # tails: 0 continuation; 1..6 activation then store to the destination slot; 7..12 the
     # output node's activation, applied to the accumulators in place
     targets = ["x"] + ["%s%s" % (a, k) for k in ("", "o") for a in ACTS] + ["x"] * 3
     L += ["s_branch .L%s_%%=" % t for t in targets]
+    # the end of every tail: the next record, or out of the loop
+    loop_end = ["s_sub_u32 %[n], %[n], 1",
+                "s_cmp_lg_u32 %[n], 0",
+                "s_cbranch_scc1 .Lrec_%=",
+                "s_branch .Ldone_%="]
 
     # The activations. pre: in-place steps on the accumulator; final: the last instruction, which
     # writes the destination slot (store tails, DST indexing) or the accumulator (output tails).
@@ -136,11 +178,11 @@ def gen_walker(S, P, W):
         if store:
             out.append("s_set_gpr_idx_on %[u], gpr_idx(DST)")
             out += [final.format(a=A[m], d=T[m]) for m in range(M)]
-            out.append("s_branch .Lxo_%=")
+            out.append("s_set_gpr_idx_off")
         else:
             out += [final.format(a=A[m], d=A[m]) for m in range(M) if final]
-            out += ["s_nop 1", "s_branch .Lx_%="]  # the caller may read these with DPP next
-        return out
+            out.append("s_nop 1")  # the caller reads these next
+        return out + loop_end
 
     # The packer scales every weight and bias feeding a varying node by its activation's input
     # scale (emr_internal.h), so the accumulator holds z' = c z and the tails are short:
@@ -161,22 +203,25 @@ def gen_walker(S, P, W):
     for store in (True, False):
         for name, (pre, final) in defs.items():
             if not store and name == "lin":
-                L += [".Llino_%=:", "s_branch .Lx_%="]
+                L += [".Llino_%=:"] + loop_end
                 continue
             L += block(name + ("" if store else "o"), pre, final, store)
-    L += [".Lxo_%=:", "s_set_gpr_idx_off", ".Lx_%=:"]
+    L += [".Lx_%=:"] + loop_end
+    # the last prefetch (one record and one row past the program, inside the tables) is drained
+    # before the statement ends: its registers are the compiler's again after it
+    L += [".Ldone_%=:", "s_waitcnt lgkmcnt(0)"]
 
-    outs = ['[pc] "=&{s[%d:%d]}"(pc)' % (PC, PC + 1), '[t] "=&s"(t)', '[u] "=&s"(u)']
+    outs = ['[t] "=&s"(t)', '[u] "=&s"(u)', '[n] "+s"(n)',
+            '"+{s[%d:%d]}"(rp)' % (RP, RP + 1), '"+{s[%d:%d]}"(bp)' % (BP, BP + 1)]
     if S == 1:
         outs.append('[tb] "=&v"(tb)')
     else:
         outs += ['[l%d] "=&v"(l[%d])' % (j, j) for j in range(P)]
     outs += ['"+{%s}"(acc[%d])' % (A[m], m) for m in range(M)]
     outs += ['"+{v[%d:%d]}"(v%d)' % (base(M, m, W), base(M, m, W) + W - 1, m) for m in range(M)]
-    ins = ['[meta] "s"(r[0])', '[ax] "s"(r[1])', '[ay] "s"(r[2])', '[sw0] "s"(r[3])',
-           '[sw1] "s"(r[4])'] + ['[w%d] "s"(r[%d])' % (p, 5 + p) for p in range(MAX_EDGES)]
-    ins += ['[b%d] "s"(b[%d])' % (s, s) for s in range(S)]
-    ins += ['[x%d] "v"(x[%d]), [y%d] "v"(y[%d])' % (j, j, j, j) for j in range(P)]
+    ins = ['[x%d] "v"(x[%d]), [y%d] "v"(y[%d])' % (j, j, j, j) for j in range(P)]
+    clob = ['"scc"', '"m0"'] + ['"s%d"' % r for r in range(REC, ROW + 4)] + \
+        ['"s%d"' % PC, '"s%d"' % (PC + 1)]
 
     body = "\n".join('        "%s\\n"' % l for l in L)
     vec = "f32x%d" % W
@@ -185,24 +230,31 @@ def gen_walker(S, P, W):
     out.append("  static constexpr int M = %d;" % M)
     out.append("  float acc[%d];" % M)
     out.append("  %s %s;" % (vec, ", ".join("v%d" % m for m in range(M))))
-    out.append("  __device__ __forceinline__ void init() {")
-    for m in range(M):
-        out.append("    acc[%d] = 0.0f;" % m)
-        out.append("    v%d = (%s)(0.0f);" % (m, vec))
+    # def(): an empty statement that "defines" the accumulators and windows in their registers.
+    # Placed before each walk, it tells the compiler that nothing from a previous walk is live in
+    # them (a walk writes every value before reading it), so they cost no initialization and the
+    # registers are free for other values between walks.
+    defs_ = ['"={%s}"(acc[%d])' % (A[m], m) for m in range(M)]
+    defs_ += ['"={v[%d:%d]}"(v%d)' % (base(M, m, W), base(M, m, W) + W - 1, m) for m in range(M)]
+    out.append("  __device__ __forceinline__ void def() {")
+    out.append('    asm volatile(""')
+    out.append("                 : %s);" % ",\n                   ".join(defs_))
     out.append("  }")
-    out.append("  // r: the record's 16 words; b: the node's bias row (one float per source);")
-    out.append("  // x, y: the P positions.")
-    out.append("  __device__ __forceinline__ void step(const uint32_t* r, const float* b, "
+    out.append("  // The whole program walk at the P positions (x, y): n records from rec (16 words each);")
+    out.append("  // row: the group's bias rows (4 floats each), row 0 holding the outputs of a program")
+    out.append("  // without records (n = 0) and row 1 + r the biases of record r.")
+    out.append("  __device__ __forceinline__ void walk(uint64_t rec, uint64_t row, uint32_t n, "
                "const float* x, const float* y) {")
-    out.append("    uint64_t pc;")
+    out.append("    uint64_t rp = rec, bp = row;")
     out.append("    uint32_t t, u;")
     out.append("    float tb;" if S == 1 else "    float l[%d];" % P)
     out.append("    asm volatile(")
     out.append(body)
     out.append("        : %s" % ",\n          ".join(outs))
     out.append("        : %s" % ",\n          ".join(ins))
-    # SCC is written by the scalar arithmetic and M0 by the indexing instructions
-    out.append('        : "scc", "m0");')
+    # SCC is written by the scalar arithmetic, M0 by the indexing instructions; the record, row
+    # and PC registers are the statement's own
+    out.append("        : %s);" % ", ".join(clob))
     out.append("  }")
     out.append("};")
     return "\n".join(out) + "\n"

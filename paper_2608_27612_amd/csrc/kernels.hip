@@ -3,7 +3,7 @@
 //   k_grid      writes the cell centres of every queried position (Section 3.1, Eq. 1).
 //   k_fill      clears the look-back status words and counters of a workspace.
 //   k_bind      evaluates the position-independent part of each (genome, source) CPPN once and
-//               folds it into per-step biases (one thread per source).
+//               folds it into per-step biases (one wave per pair).
 //   k_discover  the hot path: one lane per parent cell; each lane interprets the varying CPPN
 //               program for S sources of one genome at the cell's four children at once
 //               (Section 3.1, the batched query W), reduces the four siblings to their variance
@@ -81,6 +81,13 @@ __device__ __forceinline__ int level_of(uint32_t p) {
 // ------------------------------------------------------------------------ wave helpers
 __device__ __forceinline__ uint32_t lane_id() {
   return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+// The lane id read where it is used: values derived from it on rarely taken paths are then
+// computed there instead of being hoisted to the kernel start and held in registers throughout.
+__device__ __forceinline__ uint32_t lane_id_here() {
+  uint32_t l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n v_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
 }
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
 __device__ __forceinline__ uint32_t popc64(uint64_t m) { return __builtin_popcountll(m); }
@@ -161,20 +168,31 @@ __device__ uint64_t lookback(uint64_t* row, uint32_t tile, uint64_t count, uint3
 // Pointers are passed as separate restrict-qualified parameters so the compiler can prove that
 // the program, group and bias tables are never written by the kernel and read them with scalar
 // loads through the scalar cache.
+//
+// One launch covers every group of a call, in up to kMaxParts parts: the groups with S sources
+// per walk and register window W, one part per (S, W) present (costliest part first). The
+// launch's chunks are those of its parts, one after the other.
+struct DiscoverPart {
+  uint32_t S, W, group0;                     // sources per walk, window; the part's first group
+  uint32_t n_chunks, chunks_per_group, chunk_tiles;
+};
 struct DiscoverScalars {
   int64_t cap, n_pos;
   // The launch covers tiles tile_lo .. tile_lo + tiles - 1 of every pair; record slots of a pair
   // region count from parent_lo, the first parent index of tile tile_lo.
-  uint32_t tile_lo, parent_lo;
-  uint32_t tiles, n_chunks, chunks_per_group, chunk_tiles;
+  uint32_t tile_lo, parent_lo, tiles;
+  uint32_t n_parts, n_chunks;  // chunks of all parts
+  DiscoverPart part[kMaxParts];
   int32_t depth;
   float theta4;  // 4 theta
   uint32_t blob_words, n_pairs;
   uint32_t bias_floats;  // the host keeps the bias table below 2^32 floats
+  uint32_t head_parents;  // parents in a pair's tile 0 (levels 1..3, or all levels of a shallower grid)
 };
 
-// Output modes: raw CPPN outputs; records at fixed per-tile slots (pair_capacity >= Q(D), compacted
-// afterwards by k_compact); records placed directly through the look-back scan (any capacity).
+// Output modes: raw CPPN outputs; records at fixed per-tile slots (pair_capacity >= Q(D)),
+// compacted afterwards by k_compact; records placed directly through the look-back scan (any
+// capacity).
 constexpr int kModeRaw = 0, kModePadded = 1, kModeLookback = 2;
 
 // Read-only tables are read through the constant address space: the kernel never writes them
@@ -198,247 +216,291 @@ __device__ __forceinline__ Group load_group(cu32* p) {
 }
 static_assert(sizeof(Group) == 12 * sizeof(uint32_t), "Group layout");
 
-// One 16-word program record and one 4-float bias row (scalar loads; the compiler merges each
-// into a single s_load).
-struct Rec {
-  uint32_t w[kRecWords];
-};
-__device__ __forceinline__ Rec load_rec(cu32* p) {
-  Rec r;
-#pragma unroll
-  for (int k = 0; k < (int)kRecWords; ++k) r.w[k] = p[k];
-  return r;
-}
-struct Row {
-  float b[4];
-};
-__device__ __forceinline__ Row load_row(cf32* p) { return Row{{p[0], p[1], p[2], p[3]}}; }
 
-// S sources of one genome and direction per group. A lane holds the four children (grid indices
-// 4 q .. 4 q + 3) of TPW = P / 4 parent cells q, one in each tile of the walk, and evaluates the S
-// sources at those P positions at once (M = S * P instances; instance m = s * P + 4 k + c is
-// source s at child c of the lane's parent in tile k). One walk of the program therefore serves
-// M queries per lane, and a cell's variance is formed inside the lane.
-template <int S, int P, int W, int MODE>
-__global__ void __launch_bounds__(256)
-    k_discover(const uint32_t* __restrict__ blob, const Group* __restrict__ groups,
-               const float* __restrict__ bias_tab, uint64_t* __restrict__ status,
-               uint32_t* __restrict__ err, uint32_t* __restrict__ parent, float* __restrict__ w4,
-               int64_t* __restrict__ pair_count, float* __restrict__ raw, DiscoverScalars a) {
+// ------------------------------------------------------------------------ compaction
+// First parent index of a pair's tile T: tile 0 holds the parents of levels 1..3, every other tile
+// 64 parents.
+__device__ __forceinline__ uint32_t tile_parent_offset(uint32_t T) {
+  return T == 0 ? 0u : (uint32_t)(level_offset(kFirstAlignedLevel) / 4) + (T - 1) * (kTile / 4);
+}
+
+// Compaction of one pair by one wave, once every tile of the range has left its records at the
+// tile's own slots and its count in counts[pair * tiles + t]: scans the counts and moves
+// each tile's records down to their final, contiguous place, tile by tile in increasing order (a
+// tile's destination never overlaps a later tile's records, and each tile's records are all read
+// before any is written), then writes the pair's count and returns it.
+__device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
+                                 float* __restrict__ w4, int64_t* __restrict__ pair_count,
+                                 int64_t cap, uint32_t tile_lo, uint32_t tiles, uint32_t pair,
+                                 uint32_t head_slots, uint32_t lane) {
+  const uint32_t parent_lo = tile_parent_offset(tile_lo);
+  const uint64_t* row = counts + (int64_t)pair * tiles;
+  const int64_t region = (int64_t)pair * cap;
+  uint32_t running = 0;
+  for (uint32_t t0 = 0; t0 < tiles; t0 += kWave) {
+    // a tile holds at most its own slot count (64, or the head tile's parents)
+    const uint32_t t_lane = t0 + lane;
+    const uint32_t slots = tile_lo + t_lane == 0 ? head_slots : (uint32_t)(kTile / 4);
+    const uint32_t c = t_lane < tiles ? min((uint32_t)row[t_lane], slots) : 0u;
+    // inclusive scan over the wave, bit-sliced: c < 128, so the counts of the lanes below are
+    // the sum over bits b of 2^b times the number of lanes below with bit b set (mbcnt)
+    uint32_t incl = c;
+#pragma unroll
+    for (int b = 0; b < 7; ++b) incl += mbcnt64(ballot((c >> b) & 1u)) << b;
+    // only tiles with records, in increasing order
+    for (uint64_t m = ballot(c != 0u); m != 0ull; m &= m - 1ull) {
+      const uint32_t i = (uint32_t)__builtin_ctzll(m);
+      const uint32_t ci = __builtin_amdgcn_readlane(c, i);
+      const uint32_t dst = running + __builtin_amdgcn_readlane(incl, i) - ci;
+      const uint32_t src = tile_parent_offset(tile_lo + t0 + i) - parent_lo;
+      if (dst == src) continue;
+      if (lane < ci) {
+        const uint32_t pv = parent[region + src + lane];
+        const float4 wv = reinterpret_cast<const float4*>(w4)[region + src + lane];
+        parent[region + dst + lane] = pv;
+        reinterpret_cast<float4*>(w4)[region + dst + lane] = wv;
+      }
+    }
+    running += __builtin_amdgcn_readlane(incl, kWave - 1);
+  }
+  if (lane == 0) pair_count[pair] = running;
+  return running;
+}
+
+// Each wave takes pairs pair = wave, wave + n_waves, ...: compacts them once every discover launch
+// of the range has finished, and the workgroup's largest count is raised into *max_count with one
+// atomic.
+constexpr int kCompactWaves = 4;
+
+__global__ void __launch_bounds__(kCompactWaves * kWave)
+    k_compact(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
+              float* __restrict__ w4, int64_t* __restrict__ pair_count,
+              uint32_t* __restrict__ max_count, int64_t cap, uint32_t tile_lo, uint32_t tiles,
+              uint32_t n_pairs, uint32_t head_slots) {
+  __shared__ uint32_t wave_max[kCompactWaves];
+  const uint32_t lane = lane_id();
+  const uint32_t wv = threadIdx.x / kWave;
+  const uint32_t n_waves = gridDim.x * kCompactWaves;
+  uint32_t my_max = 0;
+  for (uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * kCompactWaves + wv);
+       pair < n_pairs; pair += n_waves) {
+    my_max = max(my_max, compact_pair(counts, parent, w4, pair_count, cap, tile_lo, tiles, pair,
+                                      head_slots, lane));
+  }
+  if (lane == 0) wave_max[wv] = my_max;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t m = 0;
+    for (int k = 0; k < kCompactWaves; ++k) m = max(m, wave_max[k]);
+    raise_max(max_count, m);
+  }
+}
+
+// Per-lane constants of the position decode. Lane l holds parent q0 + l of a tile whose first
+// parent is q0. In a level-aligned tile the children's Morton indices are m0 + 4 l + c (m0 a
+// multiple of 256): lane bits 0, 2, 4 are the cell column's bits 1..3, lane bits 1, 3, 5 the row's,
+// and child c adds column bit 0 = c & 1 and row bit 0 = c >> 1. Eq. 1: x = (2 column + 1)
+// 2^-level - 1, and likewise y; xl, yl hold the lane's and child's part of 2 column and 2 row.
+struct LaneGeo {
+  float xl[2], yl[2];
+};
+
+// The tables and outputs of a launch.
+struct DiscoverPtrs {
+  cu32* blob;
+  cu32* groups;
+  cf32* bias;
+  uint64_t* status;
+  uint32_t* err;
+  uint32_t* parent;
+  float* w4;
+  int64_t* pair_count;
+  float* raw;
+};
+
+// One chunk (chunk_tiles consecutive tiles of one group) of a part with S sources per walk. A lane
+// holds the four children (grid indices 4 q .. 4 q + 3) of TPW = P / 4 parent cells q, one in each
+// tile of the walk, and evaluates the S sources at those P positions at once (M = S * P
+// instances; instance m = s * P + 4 k + c is source s at child c of the lane's parent in tile k).
+// One walk of the program therefore serves M queries per lane, and a cell's variance is formed
+// inside the lane.
+template <int S, int W, int MODE>
+__device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& pt,
+                                               const DiscoverScalars& a, const DiscoverPtrs& d,
+                                               const LaneGeo& geo, uint32_t lane) {
+  constexpr int P = positions_per_lane(S, W);
   static_assert(P == 4 || P == 8, "a lane holds whole sibling quads");
   constexpr int M = S * P;
   constexpr int TPW = P / kTileIters;  // tiles per walk
   // (the launcher makes chunk_tiles a multiple of TPW, so a walk's tiles lie in one chunk)
-  const uint32_t lane = lane_id();
-  // Lane l holds parent q0 + l of a tile whose first parent is q0. In a level-aligned tile the
-  // children's Morton indices are m0 + 4 l + c (m0 a multiple of 256): lane bits 0, 2, 4 are the
-  // cell column's bits 1..3, lane bits 1, 3, 5 the row's, and child c adds column bit 0 = c & 1
-  // and row bit 0 = c >> 1. Eq. 1: x = (2 column + 1) 2^-level - 1, and likewise y.
-  const uint32_t i_lo = (lane & 1u) | ((lane >> 1) & 2u) | ((lane >> 2) & 4u);
-  const uint32_t j_lo = ((lane >> 1) & 1u) | ((lane >> 2) & 2u) | ((lane >> 3) & 4u);
-  const float xl[2] = {(float)(4u * i_lo), (float)(4u * i_lo + 2u)};
-  const float yl[2] = {(float)(4u * j_lo), (float)(4u * j_lo + 2u)};
-  // parents in the head tile (levels 1..3, or all levels of a shallower grid)
-  const uint32_t head_parents = (uint32_t)(a.depth < kFirstAlignedLevel
-                                               ? n_parents(a.depth)
-                                               : level_offset(kFirstAlignedLevel) / 4);
+  const uint32_t gi = pt.group0 + c / pt.chunks_per_group;
+  const uint32_t chunk_tile = (c % pt.chunks_per_group) * pt.chunk_tiles;
+  const Group G = load_group(d.groups + 12 * gi);
+  // Every table-derived offset, count and id is checked before use: an entry that points outside
+  // its table raises an error flag and the chunk is skipped instead of reading or writing wild.
+  // The walk reads records var_off .. var_off + 16 n_rec (one past the last: the prefetch) and
+  // bias rows inside the group's n_rec + 2.
+  // (32-bit arithmetic throughout: n_rec is bounded first, and no sum below can wrap.)
+  {
+    const uint32_t rec_words = kRecWords * (G.n_rec + 1), row_floats = 4u * (G.n_rec + 2);
+    bool ok = G.n_rec <= kMaxRecords && G.n_steps <= G.n_rec &&
+              (G.var_off & (kRecWords - 1)) == 0 && (G.bias_off & 3u) == 0 &&
+              rec_words <= a.blob_words && G.var_off <= a.blob_words - rec_words &&
+              row_floats <= a.bias_floats && G.bias_off <= a.bias_floats - row_floats;
+#pragma unroll
+    for (int s = 0; s < S; ++s) ok = ok && G.pair[s] < a.n_pairs;
+    if (!ok) {
+      if (lane == 0) atomicOr(d.err, kErrTable);
+      return;
+    }
+  }
+  const uint32_t n_rec = (G.flags & 1u) != 0 ? G.n_rec : 0u;  // no records: a uniform output
+  const uint32_t chunk_end = min(chunk_tile + pt.chunk_tiles, a.tiles);
 
   Walker<S, P, W> R;
-  R.init();
-
-  // Work is handed out in chunks of chunk_tiles consecutive tiles of one group, round-robin over
-  // the waves: chunk c goes to wave c mod n_waves. A group's chunks go to consecutive waves, so a
-  // pair's tiles are computed concurrently, and each wave visits its tiles in increasing order.
-  const uint32_t n_waves = gridDim.x * (blockDim.x / kWave);
-  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +
-                                                       threadIdx.x / kWave);
-  cu32* cblob = (cu32*)blob;
-  cu32* cgroups = (cu32*)groups;
-  cf32* cbias = (cf32*)bias_tab;
-  for (uint32_t c = wave; c < a.n_chunks; c += n_waves) {
-    const uint32_t gi = c / a.chunks_per_group;
-    const uint32_t chunk_tile = (c - gi * a.chunks_per_group) * a.chunk_tiles;
-    const Group G = load_group(cgroups + 12 * gi);
-    // Every table-derived offset, count and id is checked before use: an entry that points outside
-    // its table raises an error flag and the chunk is skipped instead of reading or writing wild.
-    // The walk reads records var_off .. var_off + 16 n_rec (one past the last: the prefetch) and
-    // bias rows inside the group's n_rec + 2.
-    // (32-bit arithmetic throughout: n_rec is bounded first, and no sum below can wrap.)
-    {
-      const uint32_t rec_words = kRecWords * (G.n_rec + 1), row_floats = 4u * (G.n_rec + 2);
-      bool ok = G.n_rec <= kMaxRecords && G.n_steps <= G.n_rec && (G.n_rec & 1u) == 0 &&
-                (G.var_off & (kRecWords - 1)) == 0 && (G.bias_off & 3u) == 0 &&
-                rec_words <= a.blob_words && G.var_off <= a.blob_words - rec_words &&
-                row_floats <= a.bias_floats && G.bias_off <= a.bias_floats - row_floats;
+  for (uint32_t t0 = chunk_tile; t0 < chunk_end; t0 += TPW) {
+    // ---- geometry of the walk's tiles (t0 counts from the launch's first tile, tile_lo). The
+    // pair's tile 0 holds the parents of levels 1..3 (21 of them; the positions decoded one by
+    // one); every other tile 64 parents of one level, whose 256 children start at grid index p0.
+    uint32_t p0[TPW];
+    uint64_t vmask[TPW];  // lanes holding a queried parent
+    float px[P], py[P];
 #pragma unroll
-      for (int s = 0; s < S; ++s) ok = ok && G.pair[s] < a.n_pairs;
-      if (!ok) {
-        if (lane == 0) atomicOr(err, kErrTable);
-        continue;
-      }
-    }
-    const bool out_varying = (G.flags & 1u) != 0;
-    const Row orow = load_row(cbias + G.bias_off);  // row 0: output constants (uniform output)
-
-    for (uint32_t t0 = chunk_tile; t0 < chunk_tile + a.chunk_tiles && t0 < a.tiles; t0 += TPW) {
-      // ---- geometry of the walk's tiles (t0 counts from the launch's first tile, tile_lo). The
-      // pair's tile 0 holds the parents of levels 1..3 (21 of them; the positions decoded one by
-      // one); every other tile 64 parents of one level, whose 256 children start at grid index p0.
-      uint32_t p0[TPW];
-      uint64_t vmask[TPW];  // lanes holding a queried parent
-      float px[P], py[P];
+    for (int k = 0; k < TPW; ++k) {
+      const uint32_t tile = a.tile_lo + t0 + k;  // the pair's tile index
+      const bool in_range = t0 + k < a.tiles;
+      if (tile == 0) {
+        p0[k] = 0;
+        vmask[k] = !in_range ? 0ull
+                   : a.head_parents >= 64u ? ~0ull
+                                           : (1ull << a.head_parents) - 1ull;
+        const uint32_t ln = lane_id_here();
 #pragma unroll
-      for (int k = 0; k < TPW; ++k) {
-        const uint32_t tile = a.tile_lo + t0 + k;  // the pair's tile index
-        const bool in_range = t0 + k < a.tiles;
-        if (tile == 0) {
-          p0[k] = 0;
-          vmask[k] = !in_range ? 0ull : head_parents >= 64u ? ~0ull : (1ull << head_parents) - 1ull;
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const uint32_t p = 4u * lane + (uint32_t)c;
-            const int l = level_of(p);
-            const uint32_t mm = p - (uint32_t)level_offset(l);
-            const float sc = pow2_neg(l);
-            px[4 * k + c] = __builtin_fmaf((float)(2u * compact_even(mm) + 1u), sc, -1.0f);
-            py[4 * k + c] = __builtin_fmaf((float)(2u * compact_even(mm >> 1) + 1u), sc, -1.0f);
-          }
-        } else {
-          p0[k] = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(tile - 1) * kTile);
-          vmask[k] = in_range ? ~0ull : 0ull;
-          const int lvl = level_of(p0[k]);
-          const uint32_t m0 = p0[k] - (uint32_t)level_offset(lvl);
-          const float sc = pow2_neg(lvl);
-          const float bx = __builtin_fmaf((float)(32u * compact_even(m0 >> 8) + 1u), sc, -1.0f);
-          const float by = __builtin_fmaf((float)(32u * compact_even(m0 >> 9) + 1u), sc, -1.0f);
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            px[4 * k + c] = __builtin_fmaf(xl[c & 1], sc, bx);
-            py[4 * k + c] = __builtin_fmaf(yl[c >> 1], sc, by);
-          }
-        }
-      }
-
-      // ---- CPPN (Section 2): the varying program in topological order, M instances at once.
-      // Records are processed in pairs (A, B; the record count is even) so that the next
-      // record and its bias row are always being loaded into the other buffer while the
-      // current one is computed. Record r reads bias row 1 + r. A uniform output is the
-      // constant of row 0 (its program has no records).
-      if (out_varying) {
-        cu32* rp = cblob + G.var_off;
-        cf32* bp = cbias + G.bias_off + 4;
-        Rec A = load_rec(rp);
-        Row ra = load_row(bp);
-        for (uint32_t r = 0; r < G.n_rec; r += 2) {
-          const Rec B = load_rec(rp + kRecWords);
-          const Row rb = load_row(bp + 4);
-          R.step(A.w, ra.b, px, py);
-          rp += 2 * kRecWords;
-          bp += 8;
-          A = load_rec(rp);
-          ra = load_row(bp);
-          R.step(B.w, rb.b, px, py);
+        for (int c4 = 0; c4 < 4; ++c4) {
+          const uint32_t p = 4u * ln + (uint32_t)c4;
+          const int l = level_of(p);
+          const uint32_t mm = p - (uint32_t)level_offset(l);
+          const float sc = pow2_neg(l);
+          px[4 * k + c4] = __builtin_fmaf((float)(2u * compact_even(mm) + 1u), sc, -1.0f);
+          py[4 * k + c4] = __builtin_fmaf((float)(2u * compact_even(mm >> 1) + 1u), sc, -1.0f);
         }
       } else {
+        p0[k] = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(tile - 1) * kTile);
+        vmask[k] = in_range ? ~0ull : 0ull;
+        const int lvl = level_of(p0[k]);
+        const uint32_t m0 = p0[k] - (uint32_t)level_offset(lvl);
+        const float sc = pow2_neg(lvl);
+        const float bx = __builtin_fmaf((float)(32u * compact_even(m0 >> 8) + 1u), sc, -1.0f);
+        const float by = __builtin_fmaf((float)(32u * compact_even(m0 >> 9) + 1u), sc, -1.0f);
 #pragma unroll
-        for (int m = 0; m < M; ++m) R.acc[m] = orow.b[m / P];
+        for (int c4 = 0; c4 < 4; ++c4) {
+          px[4 * k + c4] = __builtin_fmaf(geo.xl[c4 & 1], sc, bx);
+          py[4 * k + c4] = __builtin_fmaf(geo.yl[c4 >> 1], sc, by);
+        }
       }
-      // the output node's activation was applied by its record's tail
-      const float* w = R.acc;
+    }
 
-      if constexpr (MODE == kModeRaw) {
+    // ---- CPPN (Section 2): the varying program in topological order, M instances at once, in
+    // one statement (the record step, generated): record r reads bias row 1 + r, and the next
+    // record and row are loaded while the current one is computed. A uniform output is the
+    // constant of row 0 (its program has no records).
+    R.def();
+    R.walk((uint64_t)(d.blob + G.var_off), (uint64_t)(d.bias + G.bias_off), n_rec, px, py);
+    // the output node's activation was applied by its record's tail
+    const float* w = R.acc;
+
+    if constexpr (MODE == kModeRaw) {
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+#pragma unroll
+        for (int k = 0; k < TPW; ++k)
+          if ((vmask[k] >> lane) & 1ull) {
+            float* o = d.raw + (int64_t)G.pair[s] * a.n_pos + p0[k] + 4u * lane;
+#pragma unroll
+            for (int c4 = 0; c4 < 4; ++c4) o[c4] = w[s * P + 4 * k + c4];
+          }
+      continue;
+    }
+    // ---- variance of the four siblings (Section 3.2) and the threshold test (Eq. 2), inside
+    // the lane: s2 = the sum of the squared deviations from their mean = 4 var, tested as
+    // s2 > 4 theta (both scalings by 4 exact, barring overflow or a subnormal variance).
+    float s2[S][TPW];
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+#pragma unroll
+      for (int k = 0; k < TPW; ++k) {
+        const float* q = w + s * P + 4 * k;
+        const float sum = (q[0] + q[1]) + (q[2] + q[3]);
+        const float d0 = __builtin_fmaf(sum, -0.25f, q[0]);
+        const float d1 = __builtin_fmaf(sum, -0.25f, q[1]);
+        const float d2 = __builtin_fmaf(sum, -0.25f, q[2]);
+        const float d3 = __builtin_fmaf(sum, -0.25f, q[3]);
+        s2[s][k] = __builtin_fmaf(d3, d3, __builtin_fmaf(d2, d2, __builtin_fmaf(d1, d1, d0 * d0)));
+      }
+    // Nearly every cell is dropped: one test on the maximum decides whether any record is kept.
+    float mx = s2[0][0];
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+#pragma unroll
+      for (int k = 0; k < TPW; ++k) mx = __builtin_fmaxf(mx, s2[s][k]);
+    const bool some = ballot(mx > a.theta4) != 0ull;
+
+    if constexpr (MODE == kModePadded) {
+      uint32_t run[S][TPW];  // records per source and tile
+      if (some) {
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+#pragma unroll
+          for (int k = 0; k < TPW; ++k) {
+            const uint64_t kb = ballot(s2[s][k] > a.theta4) & vmask[k];
+            run[s][k] = popc64(kb);
+            if ((kb >> lane) & 1ull) {
+              // a tile's records start at its first parent index within the pair
+              const int64_t slot = (int64_t)G.pair[s] * a.cap + ((p0[k] >> 2) - a.parent_lo) +
+                                   mbcnt64(kb);
+              d.parent[slot] = (p0[k] >> 2) + lane;
+#pragma unroll
+              for (int c4 = 0; c4 < 4; ++c4) d.w4[slot * 4 + c4] = w[s * P + 4 * k + c4];
+            }
+          }
+      } else {
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+#pragma unroll
+          for (int k = 0; k < TPW; ++k) run[s][k] = 0;
+      }
+      if (lane == 0) {
 #pragma unroll
         for (int s = 0; s < S; ++s)
 #pragma unroll
           for (int k = 0; k < TPW; ++k)
-            if ((vmask[k] >> lane) & 1ull) {
-              float* o = raw + (int64_t)G.pair[s] * a.n_pos + p0[k] + 4u * lane;
-#pragma unroll
-              for (int c = 0; c < 4; ++c) o[c] = w[s * P + 4 * k + c];
-            }
-        continue;
+            if (t0 + k < a.tiles) d.status[(int64_t)G.pair[s] * a.tiles + t0 + k] = run[s][k];
       }
-      // ---- variance of the four siblings (Section 3.2) and the threshold test (Eq. 2), inside
-      // the lane: s2 = the sum of the squared deviations from their mean = 4 var, tested as
-      // s2 > 4 theta (both scalings by 4 exact, barring overflow or a subnormal variance).
-      float s2[S][TPW];
+    }
+    if constexpr (MODE == kModeLookback) {
+      // ---- each tile learns its exact offset within each pair from the look-back scan, in
+      // increasing tile order
 #pragma unroll
-      for (int s = 0; s < S; ++s)
+      for (int k = 0; k < TPW; ++k) {
+        const uint32_t tile = t0 + k;
+        if (tile >= a.tiles) break;
 #pragma unroll
-        for (int k = 0; k < TPW; ++k) {
-          const float* q = w + s * P + 4 * k;
-          const float sum = (q[0] + q[1]) + (q[2] + q[3]);
-          const float d0 = __builtin_fmaf(sum, -0.25f, q[0]);
-          const float d1 = __builtin_fmaf(sum, -0.25f, q[1]);
-          const float d2 = __builtin_fmaf(sum, -0.25f, q[2]);
-          const float d3 = __builtin_fmaf(sum, -0.25f, q[3]);
-          s2[s][k] = __builtin_fmaf(d3, d3, __builtin_fmaf(d2, d2, __builtin_fmaf(d1, d1, d0 * d0)));
-        }
-      // Nearly every cell is dropped: one test on the maximum decides whether any record is kept.
-      float mx = s2[0][0];
+        for (int s = 0; s < S; ++s) {
+          const uint64_t kb = some ? ballot(s2[s][k] > a.theta4) & vmask[k] : 0ull;
+          const uint64_t cnt = popc64(kb);
+          const uint32_t pair = G.pair[s];
+          const uint64_t base = lookback(d.status + (int64_t)pair * a.tiles, tile, cnt, d.err);
+          if (tile + 1 == a.tiles && lane == 0) {
+            d.pair_count[pair] = (int64_t)(base + cnt);
+            raise_max(d.err + 1, (uint32_t)min(base + cnt, (uint64_t)0xFFFFFFFFu));
+          }
+          if ((kb >> lane) & 1ull) {
+            const int64_t idx = (int64_t)base + (int64_t)mbcnt64(kb);
+            if (idx < a.cap) {
+              const int64_t slot = (int64_t)pair * a.cap + idx;
+              d.parent[slot] = (p0[k] >> 2) + lane;
 #pragma unroll
-      for (int s = 0; s < S; ++s)
-#pragma unroll
-        for (int k = 0; k < TPW; ++k) mx = __builtin_fmaxf(mx, s2[s][k]);
-      const bool some = ballot(mx > a.theta4) != 0ull;
-
-      if constexpr (MODE == kModePadded) {
-        uint32_t run[S][TPW];  // records so far per source and tile
-        if (some) {
-#pragma unroll
-          for (int s = 0; s < S; ++s)
-#pragma unroll
-            for (int k = 0; k < TPW; ++k) {
-              const uint64_t kb = ballot(s2[s][k] > a.theta4) & vmask[k];
-              run[s][k] = popc64(kb);
-              if ((kb >> lane) & 1ull) {
-                // a tile's records start at its first parent index within the pair
-                const int64_t slot = (int64_t)G.pair[s] * a.cap + ((p0[k] >> 2) - a.parent_lo) +
-                                     mbcnt64(kb);
-                parent[slot] = (p0[k] >> 2) + lane;
-#pragma unroll
-                for (int c = 0; c < 4; ++c) w4[slot * 4 + c] = w[s * P + 4 * k + c];
-              }
-            }
-        } else {
-#pragma unroll
-          for (int s = 0; s < S; ++s)
-#pragma unroll
-            for (int k = 0; k < TPW; ++k) run[s][k] = 0;
-        }
-        if (lane == 0) {
-#pragma unroll
-          for (int s = 0; s < S; ++s)
-#pragma unroll
-            for (int k = 0; k < TPW; ++k)
-              if (t0 + k < a.tiles) status[(int64_t)G.pair[s] * a.tiles + t0 + k] = run[s][k];
-        }
-      }
-      if constexpr (MODE == kModeLookback) {
-        // ---- each tile learns its exact offset within each pair from the look-back scan, in
-        // increasing tile order
-#pragma unroll
-        for (int k = 0; k < TPW; ++k) {
-          const uint32_t tile = t0 + k;
-          if (tile >= a.tiles) break;
-#pragma unroll
-          for (int s = 0; s < S; ++s) {
-            const uint64_t kb = some ? ballot(s2[s][k] > a.theta4) & vmask[k] : 0ull;
-            const uint64_t cnt = popc64(kb);
-            const uint32_t pair = G.pair[s];
-            const uint64_t base = lookback(status + (int64_t)pair * a.tiles, tile, cnt, err);
-            if (tile + 1 == a.tiles && lane == 0) {
-              pair_count[pair] = (int64_t)(base + cnt);
-              raise_max(err + 1, (uint32_t)min(base + cnt, (uint64_t)0xFFFFFFFFu));
-            }
-            if ((kb >> lane) & 1ull) {
-              const int64_t idx = (int64_t)base + (int64_t)mbcnt64(kb);
-              if (idx < a.cap) {
-                const int64_t slot = (int64_t)pair * a.cap + idx;
-                parent[slot] = (p0[k] >> 2) + lane;
-#pragma unroll
-                for (int c = 0; c < 4; ++c) w4[slot * 4 + c] = w[s * P + 4 * k + c];
-              }
+              for (int c4 = 0; c4 < 4; ++c4) d.w4[slot * 4 + c4] = w[s * P + 4 * k + c4];
             }
           }
         }
@@ -446,6 +508,49 @@ __global__ void __launch_bounds__(256)
     }
   }
 }
+
+// One launch: every part, each chunk dispatched to the code of its part's (S, W). Chunks are
+// handed out round-robin over the waves: chunk c goes to wave c mod n_waves. A group's chunks go
+// to consecutive waves, so a pair's tiles are computed concurrently, and each wave visits its
+// tiles in increasing order.
+template <int MODE>
+__global__ void __launch_bounds__(256)
+    k_discover(const uint32_t* __restrict__ blob, const Group* __restrict__ groups,
+               const float* __restrict__ bias_tab, uint64_t* __restrict__ status,
+               uint32_t* __restrict__ err, uint32_t* __restrict__ parent, float* __restrict__ w4,
+               int64_t* __restrict__ pair_count, float* __restrict__ raw, DiscoverScalars a) {
+  const uint32_t lane = lane_id();
+  const uint32_t i_lo = (lane & 1u) | ((lane >> 1) & 2u) | ((lane >> 2) & 4u);
+  const uint32_t j_lo = ((lane >> 1) & 1u) | ((lane >> 2) & 2u) | ((lane >> 3) & 4u);
+  const LaneGeo geo{{(float)(4u * i_lo), (float)(4u * i_lo + 2u)},
+                    {(float)(4u * j_lo), (float)(4u * j_lo + 2u)}};
+  const DiscoverPtrs d{(cu32*)blob, (cu32*)groups, (cf32*)bias_tab, status, err,
+                       parent, w4, pair_count, raw};
+  const uint32_t n_waves = gridDim.x * (blockDim.x / kWave);
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +
+                                                       threadIdx.x / kWave);
+  for (uint32_t c = wave; c < a.n_chunks; c += n_waves) {
+    // the chunk's part, and its index within the part
+    uint32_t k = 0, cl = c;
+    while (k + 1 < a.n_parts && cl >= a.part[k].n_chunks) {
+      cl -= a.part[k].n_chunks;
+      ++k;
+    }
+    const DiscoverPart pt = a.part[k];
+    switch (pt.W * 4u + pt.S) {
+      case 8 * 4 + 3: discover_chunk<3, 8, MODE>(cl, pt, a, d, geo, lane); break;
+      case 8 * 4 + 2: discover_chunk<2, 8, MODE>(cl, pt, a, d, geo, lane); break;
+      case 8 * 4 + 1: discover_chunk<1, 8, MODE>(cl, pt, a, d, geo, lane); break;
+      case 16 * 4 + 2: discover_chunk<2, 16, MODE>(cl, pt, a, d, geo, lane); break;
+      case 16 * 4 + 1: discover_chunk<1, 16, MODE>(cl, pt, a, d, geo, lane); break;
+      case 32 * 4 + 1: discover_chunk<1, 32, MODE>(cl, pt, a, d, geo, lane); break;
+      default:
+        if (lane == 0) atomicOr(err, kErrTable);
+    }
+  }
+}
+static_assert(max_group(8) == 3 && max_group(16) == 2 && max_group(32) == 1,
+              "the (S, W) variants of k_discover");
 
 // ------------------------------------------------------------------------ bind kernel
 // One wave per member (genome, direction, source). The wave copies the genome's uniform program
@@ -543,84 +648,6 @@ __global__ void __launch_bounds__(kBindWaves * kWave)
   if (lane == 0) bias_tab[m.bias_base] = out_u == kNone ? 0.0f : U[out_u];
 }
 
-// ------------------------------------------------------------------------ compaction
-// First parent index of a pair's tile T: tile 0 holds the parents of levels 1..3, every other tile
-// 64 parents.
-__device__ __forceinline__ uint32_t tile_parent_offset(uint32_t T) {
-  return T == 0 ? 0u : (uint32_t)(level_offset(kFirstAlignedLevel) / 4) + (T - 1) * (kTile / 4);
-}
-
-// One pair of the compaction (see k_compact); returns the pair's count.
-__device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
-                                 float* __restrict__ w4, int64_t* __restrict__ pair_count,
-                                 int64_t cap, uint32_t tile_lo, uint32_t tiles, uint32_t pair,
-                                 uint32_t head_slots, uint32_t lane) {
-  const uint32_t parent_lo = tile_parent_offset(tile_lo);
-  const uint64_t* row = counts + (int64_t)pair * tiles;
-  const int64_t region = (int64_t)pair * cap;
-  uint32_t running = 0;
-  for (uint32_t t0 = 0; t0 < tiles; t0 += kWave) {
-    // a tile holds at most its own slot count (64, or the head tile's parents)
-    const uint32_t t_lane = t0 + lane;
-    const uint32_t slots = tile_lo + t_lane == 0 ? head_slots : (uint32_t)(kTile / 4);
-    const uint32_t c = t_lane < tiles ? min((uint32_t)row[t_lane], slots) : 0u;
-    uint32_t incl = c;  // inclusive scan over the wave
-    for (int off = 1; off < kWave; off <<= 1) {
-      const uint32_t v = __shfl_up(incl, off, kWave);
-      if (lane >= (uint32_t)off) incl += v;
-    }
-    const uint32_t n_here = tiles - t0 < (uint32_t)kWave ? tiles - t0 : (uint32_t)kWave;
-    for (uint32_t i = 0; i < n_here; ++i) {
-      const uint32_t ci = __builtin_amdgcn_readlane(c, i);
-      if (ci == 0) continue;
-      const uint32_t t = t0 + i;
-      const uint32_t dst = running + __builtin_amdgcn_readlane(incl, i) - ci;
-      const uint32_t src = tile_parent_offset(tile_lo + t) - parent_lo;
-      if (dst == src) continue;
-      if (lane < ci) {
-        const uint32_t pv = parent[region + src + lane];
-        const float4 wv = reinterpret_cast<const float4*>(w4)[region + src + lane];
-        parent[region + dst + lane] = pv;
-        reinterpret_cast<float4*>(w4)[region + dst + lane] = wv;
-      }
-    }
-    running += __builtin_amdgcn_readlane(incl, n_here - 1);
-  }
-  if (lane == 0) pair_count[pair] = running;
-  return running;
-}
-
-// Each wave takes pairs pair = wave, wave + n_waves, ...: scans the per-tile counts left by the
-// padded discover pass and moves each tile's records down to their final, contiguous place,
-// tile by tile in increasing order (a tile's destination never overlaps a later tile's records,
-// and each tile's records are all read before any is written), and writes the pair's count. The
-// workgroup's largest count is then raised into *max_count with one atomic.
-constexpr int kCompactWaves = 4;
-
-__global__ void __launch_bounds__(kCompactWaves * kWave)
-    k_compact(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
-              float* __restrict__ w4, int64_t* __restrict__ pair_count,
-              uint32_t* __restrict__ max_count, int64_t cap, uint32_t tile_lo, uint32_t tiles,
-              uint32_t n_pairs, uint32_t head_slots) {
-  __shared__ uint32_t wave_max[kCompactWaves];
-  const uint32_t lane = lane_id();
-  const uint32_t wv = threadIdx.x / kWave;
-  const uint32_t n_waves = gridDim.x * kCompactWaves;
-  uint32_t my_max = 0;
-  for (uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * kCompactWaves + wv);
-       pair < n_pairs; pair += n_waves) {
-    my_max = max(my_max, compact_pair(counts, parent, w4, pair_count, cap, tile_lo, tiles, pair,
-                                      head_slots, lane));
-  }
-  if (lane == 0) wave_max[wv] = my_max;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t m = 0;
-    for (int k = 0; k < kCompactWaves; ++k) m = max(m, wave_max[k]);
-    raise_max(max_count, m);
-  }
-}
-
 // ------------------------------------------------------------------------ gather
 // Packs the compacted records of all pairs into one contiguous list, pair after pair: pair r's
 // min(count_r, cap) records go to offset sum_{q < r} min(count_q, cap). Workgroup b handles pairs
@@ -711,11 +738,10 @@ extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int S, int W, int MODE>
-static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks, hipStream_t s) {
-  constexpr int P = emr::positions_per_lane(S, W);
-  constexpr int TPW = P / emr::kTileIters;
-  auto kern = emr::k_discover<S, P, W, MODE>;
+template <int MODE>
+static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks, hipStream_t s,
+                                    hipEvent_t start, hipEvent_t stop) {
+  auto kern = emr::k_discover<MODE>;
   int dev = 0, cus = 0;
   hipError_t e;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
@@ -729,34 +755,59 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
                ? n
                : 1;
   }();
+  if (a->n_parts == 0 || a->n_parts > (uint32_t)emr::kMaxParts) return hipErrorInvalidValue;
+  uint64_t groups = 0;
+  for (uint32_t k = 0; k < a->n_parts; ++k) {
+    const int S = (int)a->part_S[k], W = (int)a->part_W[k];
+    if ((W != 8 && W != 16 && W != 32) || S < 1 || S > emr::max_group(W))
+      return hipErrorInvalidValue;
+    groups += a->part_groups[k];
+  }
   // Chunks of 4 tiles when the launch has work for at least 4 such chunks per SIMD; else each
   // chunk is one walk's worth of tiles, for parallelism.
-  const uint32_t chunk =
-      (uint64_t)a->n_groups * a->tiles >= 16ull * 4ull * (uint64_t)cus ? 4u : (uint32_t)TPW;
-  const uint32_t cpg = (a->tiles + chunk - 1) / chunk;
-  emr::DiscoverScalars sc{a->cap,
-                          a->n_pos,
-                          a->tile_lo,
-                          a->parent_lo,
-                          a->tiles,
-                          a->n_groups * cpg,
-                          cpg,
-                          chunk,
-                          a->depth,
-                          4.0f * a->theta,
-                          a->blob_words,
-                          a->n_pairs,
-                          (uint32_t)a->bias_floats};
+  const bool big = groups * a->tiles >= 16ull * 4ull * (uint64_t)cus;
+  emr::DiscoverScalars sc{};
+  sc.cap = a->cap;
+  sc.n_pos = a->n_pos;
+  sc.tile_lo = a->tile_lo;
+  sc.parent_lo = a->parent_lo;
+  sc.tiles = a->tiles;
+  sc.n_parts = a->n_parts;
+  uint64_t chunks = 0;
+  for (uint32_t k = 0; k < a->n_parts; ++k) {
+    const int S = (int)a->part_S[k], W = (int)a->part_W[k];
+    const uint32_t tpw = (uint32_t)emr::positions_per_lane(S, W) / emr::kTileIters;
+    const uint32_t chunk = big ? 4u : tpw;
+    const uint32_t cpg = (a->tiles + chunk - 1) / chunk;
+    sc.part[k] = emr::DiscoverPart{(uint32_t)S, (uint32_t)W, a->part_group0[k],
+                                   a->part_groups[k] * cpg, cpg, chunk};
+    chunks += (uint64_t)a->part_groups[k] * cpg;
+  }
+  if (chunks > 0xFFFFFFFFull) return hipErrorInvalidValue;
+  sc.n_chunks = (uint32_t)chunks;
+  sc.depth = a->depth;
+  sc.theta4 = 4.0f * a->theta;
+  sc.blob_words = a->blob_words;
+  sc.n_pairs = a->n_pairs;
+  sc.bias_floats = (uint32_t)a->bias_floats;
+  sc.head_parents =
+      (uint32_t)(a->depth < emr::kFirstAlignedLevel ? emr::n_parents(a->depth)
+                                                    : emr::level_offset(emr::kFirstAlignedLevel) / 4);
   // Clamp the grid to what can be resident at once: the waves walk their chunks. The look-back
   // mode is launched cooperatively (the runtime refuses a grid that cannot be resident all at
-  // once), which its forward progress relies on; the other modes have no dependences between waves.
+  // once), which its forward progress relies on; the other modes have no waits between waves.
   const uint32_t resident = (uint32_t)per_cu * (uint32_t)cus;
-  const uint32_t needed = (sc.n_chunks + 3) / 4;  // one wave per chunk, 4 waves per workgroup
+  const uint32_t needed = (uint32_t)((chunks + 3) / 4);  // one wave per chunk, 4 per workgroup
   if (blocks > needed) blocks = needed;
   if (blocks > resident) blocks = resident;
-  if (blocks == 0) return hipSuccess;
+  if (blocks == 0) {
+    // nothing to run: the events still bracket the (empty) launch position
+    if (start && (e = hipEventRecord(start, s)) != hipSuccess) return e;
+    if (stop && (e = hipEventRecord(stop, s)) != hipSuccess) return e;
+    return hipSuccess;
+  }
   const uint32_t* blob = a->blob;
-  const emr::Group* groups = a->groups;
+  const emr::Group* grp = a->groups;
   const float* bias_tab = a->bias_tab;
   uint64_t* status = a->status;
   uint32_t* err = a->err;
@@ -764,42 +815,31 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
   float* w4 = a->w4;
   int64_t* pair_count = a->pair_count;
   float* raw = a->raw;
+  if (start && (e = hipEventRecord(start, s)) != hipSuccess) return e;
   if constexpr (MODE == emr::kModeLookback) {
-    void* args[] = {&blob, &groups, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw, &sc};
-    return hipLaunchCooperativeKernel((const void*)kern, dim3(blocks), dim3(256), args, 0, s);
+    void* args[] = {&blob, &grp, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw, &sc};
+    e = hipLaunchCooperativeKernel((const void*)kern, dim3(blocks), dim3(256), args, 0, s);
   } else {
-    hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, s, blob, groups, bias_tab, status, err,
+    hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, s, blob, grp, bias_tab, status, err,
                        parent, w4, pair_count, raw, sc);
-    return hipGetLastError();
+    e = hipGetLastError();
   }
+  if (e != hipSuccess) return e;
+  return stop ? hipEventRecord(stop, s) : hipSuccess;
 }
 
-template <int MODE>
-static hipError_t launch_discover_w(const emr::DiscoverArgs* a, int window, uint32_t blocks,
-                                    hipStream_t s) {
-  const int S = (int)a->group_size;
-#define EMR_CASE(S_, W_) \
-  if (S == S_ && window == W_) return launch_discover_t<S_, W_, MODE>(a, blocks, s);
-  static_assert(emr::max_group(8) == 3 && emr::max_group(16) == 2 && emr::max_group(32) == 1,
-                "the instantiated (S, window) variants");
-  EMR_CASE(1, 8) EMR_CASE(2, 8) EMR_CASE(3, 8)
-  EMR_CASE(1, 16) EMR_CASE(2, 16)
-  EMR_CASE(1, 32)
-#undef EMR_CASE
-  return hipErrorInvalidValue;
-}
-
-// blocks: the most 256-thread workgroups (4 waves each) to launch; the launch uses at most one
-// wave per chunk of tiles and no more workgroups than can be resident at once; every wave walks its
-// share of the chunks.
+// One launch for all the parts (sources per walk and register window) listed in *a. blocks: the
+// most 256-thread workgroups (4 waves each) to launch; the launch uses at most one wave per chunk
+// of tiles and no more workgroups than can be resident at once; every wave walks its share of the
+// chunks. start, stop: events recorded on s around the launch, or NULL.
 // mode: 0 raw outputs, 1 padded records (then emr_launch_compact), 2 look-back records.
-extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int window, int mode,
-                                          uint32_t blocks, hipStream_t s) {
-  if (a->n_tiles == 0) return hipSuccess;
+extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int mode, uint32_t blocks,
+                                          hipStream_t s, hipEvent_t start, hipEvent_t stop) {
   switch (mode) {
-    case emr::kModeRaw: return launch_discover_w<emr::kModeRaw>(a, window, blocks, s);
-    case emr::kModePadded: return launch_discover_w<emr::kModePadded>(a, window, blocks, s);
-    case emr::kModeLookback: return launch_discover_w<emr::kModeLookback>(a, window, blocks, s);
+    case emr::kModeRaw: return launch_discover_t<emr::kModeRaw>(a, blocks, s, start, stop);
+    case emr::kModePadded: return launch_discover_t<emr::kModePadded>(a, blocks, s, start, stop);
+    case emr::kModeLookback:
+      return launch_discover_t<emr::kModeLookback>(a, blocks, s, start, stop);
     default: return hipErrorInvalidValue;
   }
 }
@@ -819,7 +859,7 @@ extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* paren
                                          uint32_t head_slots, hipStream_t s) {
   if (n_pairs == 0) return hipSuccess;
   uint32_t blocks = (n_pairs + emr::kCompactWaves - 1) / emr::kCompactWaves;
-  if (blocks > 512) blocks = 512;  // waves loop over pairs beyond this
+  if (blocks > 1024) blocks = 1024;  // waves loop over pairs beyond this
   hipLaunchKernelGGL(emr::k_compact, dim3(blocks), dim3(emr::kCompactWaves * emr::kWave), 0, s,
                      counts, parent, w4, pair_count, max_count, cap, tile_lo, tiles, n_pairs,
                      head_slots);

@@ -292,12 +292,6 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       }
       inf.act_count[g.act[v]]++;
     }
-    if (n_rec & 1u) {
-      // The kernel walks records in pairs: an odd program ends with a record that does nothing
-      // (not a node start, no edges, no tail).
-      blob.resize(blob.size() + kRecWords, 0u);
-      n_rec++;
-    }
     d.n_rec = n_rec;
     inf.n_steps = (int)vsteps.size();
     inf.window = window;

@@ -22,15 +22,15 @@
 extern "C" hipError_t emr_launch_fill(void* p, int64_t n_words, uint32_t value, hipStream_t s);
 extern "C" hipError_t emr_launch_grid(float* xy, int64_t n, hipStream_t s);
 extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s);
-extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int window, int mode,
-                                          uint32_t blocks, hipStream_t s);
-extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
-                                        const float* w4, int64_t cap, uint32_t n_pairs,
-                                        uint32_t* out_parent, float* out_w4, hipStream_t s);
+extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int mode, uint32_t blocks,
+                                          hipStream_t s, hipEvent_t start, hipEvent_t stop);
 extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
                                          int64_t* pair_count, uint32_t* max_count, int64_t cap,
                                          uint32_t tile_lo, uint32_t tiles, uint32_t n_pairs,
                                          uint32_t head_slots, hipStream_t s);
+extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
+                                        const float* w4, int64_t cap, uint32_t n_pairs,
+                                        uint32_t* out_parent, float* out_w4, hipStream_t s);
 
 namespace {
 
@@ -68,16 +68,11 @@ int device_cu_count() {
   return cus;
 }
 
-// Streams a call's discover launches run on besides the caller's: one launch per bucket (sources
-// per lane, register window), forked from the caller's stream after the bind kernel and joined
-// back before compaction, so a bucket with little work runs alongside the others instead of after
-// them. Per thread and device; created on first use at default priority.
-constexpr int kAuxStreams = 1;
+// The library's own stream per thread and device, for uploads the caller's stream does not order
+// (population and plan tables, waited for before use). Created on first use at default priority.
 struct StreamPool {
   int device = -1;
-  hipStream_t aux[kAuxStreams] = {};
-  hipEvent_t fork = nullptr;
-  hipEvent_t join[kAuxStreams] = {};
+  hipStream_t aux[1] = {};
 };
 thread_local std::vector<StreamPool> g_pools;
 
@@ -91,11 +86,7 @@ emr_status stream_pool(StreamPool** out) {
     }
   StreamPool p;
   p.device = dev;
-  for (int i = 0; i < kAuxStreams; ++i) {
-    HIP_OR_FAIL(hipStreamCreateWithFlags(&p.aux[i], hipStreamNonBlocking));
-    HIP_OR_FAIL(hipEventCreateWithFlags(&p.join[i], hipEventDisableTiming));
-  }
-  HIP_OR_FAIL(hipEventCreateWithFlags(&p.fork, hipEventDisableTiming));
+  HIP_OR_FAIL(hipStreamCreateWithFlags(&p.aux[0], hipStreamNonBlocking));
   g_pools.push_back(p);
   *out = &g_pools.back();
   return EMR_OK;
@@ -104,6 +95,9 @@ emr_status stream_pool(StreamPool** out) {
 // Per-thread profiling of the discover-kernel launches.
 struct Profiler {
   bool on = false;
+  bool first_only = false;               // time only a call's first launch
+  int32_t every = 1;                     // time one call in `every`
+  int64_t seen = 0;                      // calls since enabled
   double rT = 4.0;
   int32_t calls = 0;                     // profiled calls since enabled or read
   std::vector<hipEvent_t> events;        // 2 per record, created lazily and reused
@@ -114,11 +108,22 @@ thread_local Profiler g_prof;
 // Algorithmic VALU slots per query of one (genome, direction) program: one per position-dependent
 // edge, the activation costs (transcendental instructions weighted by rT), and 2.5 for the
 // variance and threshold share of a query.
-double query_slots(const emr::GenomeInfo& inf, double rT) {
-  const double act_cost[6] = {0.0, 1.0 + 2.0 * rT, 2.0 + 2.0 * rT, 1.0 + rT, 1.0 + rT, 1.0};
+// The cost is base + rT * trans: query_base() is the part without transcendentals, query_trans()
+// their count per query.
+double query_base(const emr::GenomeInfo& inf) {
+  const double other[6] = {0.0, 1.0, 2.0, 1.0, 1.0, 1.0};
   double c = inf.fma_xy + inf.fma_node + 2.5;
-  for (int a = 0; a < 6; ++a) c += inf.act_count[a] * act_cost[a];
+  for (int a = 0; a < 6; ++a) c += inf.act_count[a] * other[a];
   return c;
+}
+double query_trans(const emr::GenomeInfo& inf) {
+  const double trans[6] = {0.0, 2.0, 2.0, 1.0, 1.0, 0.0};
+  double c = 0.0;
+  for (int a = 0; a < 6; ++a) c += inf.act_count[a] * trans[a];
+  return c;
+}
+double query_slots(const emr::GenomeInfo& inf, double rT) {
+  return query_base(inf) + rT * query_trans(inf);
 }
 
 }  // namespace
@@ -157,8 +162,19 @@ struct Plan {
     uint32_t first, count;
     double cost;  // summed per-query cost of its groups' programs (launch order)
   };
+  // The discover launch of a call: its buckets (one per sources per walk and register window),
+  // costliest first.
+  struct Launch {
+    int n_parts;
+    int part[emr::kMaxParts];  // bucket indices
+    double cost;
+    // per position of the range, over all the launch's queries: cost-model slots without
+    // transcendentals, transcendental instructions, and queries (sources)
+    double slots_base, slots_trans, sources;
+  };
   std::vector<emr::Group> groups;
   std::vector<Bucket> buckets;
+  std::vector<Launch> launches;  // one (none without groups)
   std::vector<emr::Member> members;
   std::vector<uint32_t> group_member0;  // index of each group's first member
   std::vector<float> src_xy;
@@ -186,7 +202,6 @@ struct Plan {
   size_t off_bias = 0, total = 0;
   size_t status_bytes = 0;  // cleared before a call only for look-back placement
 };
-constexpr int kMaxBuckets = 48;
 
 emr_status build_plan(const emr_population* pop, const emr_source* sources, int32_t n_sources,
                       const int32_t* offs, int32_t n_shared, int32_t depth, Plan* plan) {
@@ -285,11 +300,26 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
     P.groups.push_back(t.g);
   }
   if (bias > 0xFFFFFFFFull) return fail(EMR_E_LIMIT, "bias table too large");
-  // Launch order: the costliest bucket first (it goes on the caller's stream and starts at once;
-  // the others run alongside it as it drains).
+  // Part order within the launch: the costliest bucket first (its chunks are handed out first).
   std::stable_sort(P.buckets.begin(), P.buckets.end(),
                    [](const Plan::Bucket& a, const Plan::Bucket& b) { return a.cost > b.cost; });
-  if ((int)P.buckets.size() > kMaxBuckets) return fail(EMR_E_LIMIT, "too many buckets");
+  // One launch with every bucket as a part, in cost order.
+  if ((int)P.buckets.size() > emr::kMaxParts) return fail(EMR_E_LIMIT, "too many buckets");
+  if (!P.buckets.empty()) {
+    Plan::Launch L{};
+    for (size_t bi = 0; bi < P.buckets.size(); ++bi) {
+      const Plan::Bucket& b = P.buckets[bi];
+      L.part[L.n_parts++] = (int)bi;
+      L.cost += b.cost;
+      for (uint32_t g = 0; g < b.count; ++g) {
+        const emr::GenomeInfo& inf = pop->info[P.members[P.group_member0[b.first + g]].desc];
+        L.slots_base += b.S * query_base(inf);
+        L.slots_trans += b.S * query_trans(inf);
+      }
+      L.sources += (double)b.S * b.count;
+    }
+    P.launches.push_back(L);
+  }
   for (const auto& b : P.buckets)
     if ((uint64_t)b.count * (uint64_t)P.tiles > 0xFFFFFFFFull)
       return fail(EMR_E_LIMIT, "too many tiles in one launch");
@@ -435,9 +465,10 @@ emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspac
   return EMR_OK;
 }
 
-// Enqueues the discover launches (one per bucket) for tiles tile_lo .. tile_lo + n_tiles - 1 of
-// every pair, then the compaction when records go to padded slots. Records of pair r go to its
-// region of `out` counted from the range's first parent; raw outputs to raw[r * N(D) + p].
+// Enqueues the discover launch (every bucket, on the caller's stream) for tiles
+// tile_lo .. tile_lo + n_tiles - 1 of every pair, then the compaction when records go to padded
+// slots. Records of pair r go to its region of `out` counted from the range's first parent; raw
+// outputs to raw[r * N(D) + p].
 emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
                         const emr_result* out, float* raw, void* workspace, hipStream_t s,
                         int64_t tile_lo, int64_t n_tiles) {
@@ -457,34 +488,22 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
                 (long long)range_parents);
   Profiler& prof = g_prof;
   const size_t rec0 = prof.recs.size();
-  if (prof.on) {
-    while (prof.events.size() < 2 * (rec0 + P.buckets.size())) {
-      hipEvent_t e;
-      HIP_OR_FAIL(hipEventCreate(&e));
-      prof.events.push_back(e);
-    }
+  const bool timed_call = prof.on && prof.seen++ % prof.every == 0;
+  const size_t n_timed = timed_call ? (prof.first_only ? 1 : P.launches.size()) : 0;
+  while (prof.events.size() < 2 * (rec0 + n_timed)) {
+    hipEvent_t e;
+    HIP_OR_FAIL(hipEventCreate(&e));
+    prof.events.push_back(e);
   }
-  // Look-back launches are cooperative and stay on the caller's stream, one after the other.
-  const bool fork = mode != 2 && P.buckets.size() > 1;
-  StreamPool* pool = nullptr;
-  bool aux_used[kAuxStreams] = {};
-  if (fork) {
-    emr_status pst = stream_pool(&pool);
-    if (pst != EMR_OK) return pst;
-    HIP_OR_FAIL(hipEventRecord(pool->fork, s));
-  }
-  for (size_t bi = 0; bi < P.buckets.size(); ++bi) {
-    const Plan::Bucket& bk = P.buckets[bi];
-    hipStream_t ls = s;
-    if (fork && bi > 0) {
-      const int k = (int)((bi - 1) % kAuxStreams);
-      ls = pool->aux[k];
-      if (!aux_used[k]) HIP_OR_FAIL(hipStreamWaitEvent(ls, pool->fork, 0));
-      aux_used[k] = true;
-    }
+  // queries of the range per source: every tile holds 256 positions but the head tile
+  const double npos = (double)(tile_lo == 0 ? emr::n_positions(P.depth) -
+                                                  emr::kTile * (P.tiles - n_tiles)
+                                            : emr::kTile * n_tiles);
+  for (size_t li = 0; li < P.launches.size(); ++li) {
+    const Plan::Launch& L = P.launches[li];
     emr::DiscoverArgs a{};
     a.blob = pop->d_blob;
-    a.groups = (const emr::Group*)(tables + P.t_groups) + bk.first;
+    a.groups = (const emr::Group*)(tables + P.t_groups);
     a.bias_tab = (const float*)(ws + P.off_bias);
     a.status = (uint64_t*)(ws + P.off_status);
     a.err = (uint32_t*)(ws + P.off_err);
@@ -494,48 +513,42 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
     a.raw = raw;
     a.cap = out ? out->pair_capacity : 0;
     a.n_pos = emr::n_positions(P.depth);
-    a.n_groups = bk.count;
+    a.n_parts = (uint32_t)L.n_parts;
+    for (int k = 0; k < L.n_parts; ++k) {
+      const Plan::Bucket& bk = P.buckets[(size_t)L.part[k]];
+      a.part_S[k] = (uint32_t)bk.S;
+      a.part_W[k] = (uint32_t)bk.window;
+      a.part_group0[k] = bk.first;
+      a.part_groups[k] = bk.count;
+    }
     a.tile_lo = (uint32_t)tile_lo;
     a.parent_lo = (uint32_t)parent_lo;
     a.tiles = (uint32_t)n_tiles;
-    a.n_tiles = (uint32_t)((uint64_t)bk.count * (uint64_t)n_tiles);
     a.depth = P.depth;
     a.theta = theta;
-    a.group_size = (uint32_t)bk.S;
     a.blob_words = (uint32_t)pop->blob_words;
     a.n_pairs = (uint32_t)P.n_pairs;
     a.bias_floats = P.bias_floats;
     const uint32_t blocks = (uint32_t)cus * 16;  // the launcher sizes the grid below this
-    if (prof.on) HIP_OR_FAIL(hipEventRecord(prof.events[2 * (rec0 + bi)], ls));
-    HIP_OR_FAIL(emr_launch_discover(&a, bk.window, mode, blocks, ls));
-    if (prof.on) {
-      HIP_OR_FAIL(hipEventRecord(prof.events[2 * (rec0 + bi) + 1], ls));
+    const bool timed = li < n_timed;
+    HIP_OR_FAIL(emr_launch_discover(&a, mode, blocks, s,
+                                    timed ? prof.events[2 * (rec0 + li)] : nullptr,
+                                    timed ? prof.events[2 * (rec0 + li) + 1] : nullptr));
+    if (timed) {
       emr_launch_profile r{};
       r.call = prof.calls;
-      r.group_size = bk.S;
-      r.window = bk.window;
-      r.positions = emr::positions_per_lane(bk.S, bk.window);
-      r.tiles = a.n_tiles;
-      // queries of the range: every tile holds 256 positions but the head tile
-      const double npos = (double)(tile_lo == 0 ? emr::n_positions(P.depth) -
-                                                      emr::kTile * (P.tiles - n_tiles)
-                                                : emr::kTile * n_tiles);
-      for (uint32_t k = 0; k < bk.count; ++k) {
-        const uint32_t gi = bk.first + k;
-        const emr::Member& m0 = P.members[P.group_member0[gi]];
-        r.slots += bk.S * npos * query_slots(pop->info[m0.desc], prof.rT);
-      }
-      r.queries = (int64_t)((double)bk.count * bk.S * npos);
+      const Plan::Bucket& b0 = P.buckets[(size_t)L.part[0]];
+      r.group_size = b0.S;
+      r.window = b0.window;
+      r.positions = emr::positions_per_lane(b0.S, b0.window);
+      for (int k = 0; k < L.n_parts; ++k)
+        r.tiles += (int64_t)P.buckets[(size_t)L.part[k]].count * n_tiles;
+      r.slots = npos * (L.slots_base + prof.rT * L.slots_trans);
+      r.queries = (int64_t)(npos * L.sources);
       prof.recs.push_back(r);
     }
   }
-  if (prof.on) prof.calls++;
-  if (fork)
-    for (int k = 0; k < kAuxStreams; ++k)
-      if (aux_used[k]) {
-        HIP_OR_FAIL(hipEventRecord(pool->join[k], pool->aux[k]));
-        HIP_OR_FAIL(hipStreamWaitEvent(s, pool->join[k], 0));
-      }
+  if (timed_call) prof.calls++;
   if (padded && P.n_pairs > 0)
     HIP_OR_FAIL(emr_launch_compact(
         (const uint64_t*)(ws + P.off_status), out->parent, out->w4, out->pair_count,
@@ -888,8 +901,13 @@ emr_status emr_discover_cost(const emr_population* pop, const emr_source* source
   return EMR_OK;
 }
 
-emr_status emr_profile_enable(int32_t on, double transcendental_slots) {
+emr_status emr_profile_enable(int32_t on, int32_t every, double transcendental_slots) {
+  if (on < 0 || on > 2) return fail(EMR_E_INVAL, "profile mode %d (0 off, 1 every launch, 2 first)", on);
+  if (every < 1) return fail(EMR_E_INVAL, "profile every %d calls", every);
   g_prof.on = on != 0;
+  g_prof.first_only = on == 2;
+  g_prof.every = every;
+  g_prof.seen = 0;
   g_prof.rT = transcendental_slots;
   g_prof.recs.clear();
   g_prof.calls = 0;

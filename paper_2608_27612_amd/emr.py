@@ -87,7 +87,7 @@ def lib():
             "emr_result_check": (I32, [P, I64, P, P]),
             "emr_eval_raw": (I32, [P, P, I32, P, I32, I32, P, P, I64, P]),
             "emr_discover_cost": (I32, [P, P, I32, P, I32, I32, F64, P, P]),
-            "emr_profile_enable": (I32, [I32, F64]),
+            "emr_profile_enable": (I32, [I32, I32, F64]),
             "emr_profile_read": (I32, [P, I32, P]),
             "emr_stream_chunks": (I32, [I32, I64, P]),
             "emr_pack_population_flat": (I32, [I32, P, P, P, P, P, P, P, P, P, P, P]),
@@ -346,8 +346,11 @@ def records_to_host(res):
 
 # ----------------------------------------------------------------------------- profiling
 
-def emr_profile_enable(on: bool = True, transcendental_slots: float = 4.0):
-    _check(lib().emr_profile_enable(1 if on else 0, float(transcendental_slots)))
+def emr_profile_enable(on=True, transcendental_slots: float = 4.0, every: int = 1):
+    """on: False/0 off, True/1 every discover launch, "first"/2 a call's first launch only;
+    every: time one call in `every`."""
+    mode = 2 if on == "first" else int(on)
+    _check(lib().emr_profile_enable(mode, int(every), float(transcendental_slots)))
 
 
 def emr_profile_read():

@@ -133,8 +133,7 @@ def interpret(blob, desc, dir_, sx, sy, px, py):
         dst, ne = (meta >> 8) & 31, (meta >> 16) & 15
         assert ne <= 11 and (meta >> 20) == 0 and (meta >> 5) & 7 == 0 and (meta >> 13) & 7 == 0
         if out is not None:
-            assert r == n_rec - 1 and not w.any(), "record after the output node"
-            continue
+            raise AssertionError("record after the output node")
         if first:
             assert acc is None, "a node starts before the previous one ended"
             assert fold_rec[step] == r, "the node's bias row is not its first record's"
@@ -159,5 +158,5 @@ def interpret(blob, desc, dir_, sx, sy, px, py):
             out = _act_scaled(tail - 7, acc)
         acc = None
         step += 1
-    assert step == n_steps and out is not None and n_rec % 2 == 0
+    assert step == n_steps and out is not None
     return out, window

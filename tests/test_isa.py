@@ -57,7 +57,7 @@ def test_m0_only_for_register_indexing(asm):
 
 def test_discover_kernels_use_no_scratch(asm):
     ks = {k: v for k, v in _kernels(asm).items() if "k_discover" in k}
-    assert len(ks) == 18   # 6 (sources per walk, window) variants x 3 output modes
+    assert len(ks) == 3   # one per output mode
     for name, body in ks.items():
         assert "scratch_" not in body and "buffer_store" not in body, name
     sizes = re.findall(r"\.name:\s+(\S*k_discover\S*)\s*\n(?:.*\n)*?\s+\.private_segment_fixed_size:\s+(\d+)",
