@@ -21,11 +21,11 @@
 namespace emr {
 
 // Kernel window sizes (register slots per source) the kernels are instantiated for.
-constexpr int kWindows[] = {8, 16, 32};
+constexpr int kWindows[] = {4, 8, 16, 32};
 constexpr int kMaxWindow = 32;
 // Sources evaluated together by one lane (same genome, same direction).
 constexpr int kMaxGroup = 4;
-constexpr int kMaxParts = 6;  // (sources per walk, register window) variants of a launch
+constexpr int kMaxParts = 9;  // (sources per walk, register window) variants of a launch
 // Register budget of the value windows: S sources x P positions x W slots <= 128 VGPRs per lane.
 constexpr int kWindowRegs = 128;
 // Positions per wave iteration and iterations per tile.
@@ -119,18 +119,21 @@ constexpr uint64_t kStatusInclusive = 2ull << 62;
 constexpr uint64_t kStatusValueMask = (1ull << 62) - 1;
 
 // Positions per lane per program walk. A lane holds whole sibling quads: the four children of
-// one parent (P = 4) or of two parents in consecutive tiles (P = 8), so a cell's variance is
-// computed inside the lane. S sources of one genome share the walk (M = S P instances); a
-// (S, P, W) combination fits when the M value windows fit the register budget and the estimated
-// VGPR total (accumulators, windows, positions, per-source variances and ~16 others) leaves room
-// for 3 waves per SIMD.
+// one parent (P = 4) or of a parent in each of P / 4 consecutive tiles (P = 8, 16), so a cell's
+// variance is computed inside the lane. S sources of one genome share the walk (M = S P
+// instances); a (S, P, W) combination fits when the M value windows fit the register budget and
+// the estimated VGPR total (accumulators, windows, positions, per-source variances and ~16
+// others) leaves room for 3 waves per SIMD. The record step's scalar work is shared by the M
+// instances, so the largest P that fits is taken.
 EMR_HD constexpr bool fits_lane(int S, int P, int W) {
   return S * P * W <= kWindowRegs && 16 + S * P + S * P * W + 2 * P + 2 * S <= 168;
 }
-EMR_HD constexpr int positions_per_lane(int S, int W) { return fits_lane(S, 8, W) ? 8 : 4; }
-// Sources per walk for window W: the most that fit with P = 4.
+EMR_HD constexpr int positions_per_lane(int S, int W) {
+  return fits_lane(S, 16, W) ? 16 : fits_lane(S, 8, W) ? 8 : 4;
+}
+// Sources per walk for window W: the most (up to 3) that fit with P = 4.
 EMR_HD constexpr int max_group(int W) {
-  return fits_lane(4, 4, W) ? 4 : fits_lane(3, 4, W) ? 3 : fits_lane(2, 4, W) ? 2 : 1;
+  return fits_lane(3, 4, W) ? 3 : fits_lane(2, 4, W) ? 2 : 1;
 }
 
 // Level helpers shared by host and device.

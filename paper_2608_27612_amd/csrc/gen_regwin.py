@@ -48,15 +48,16 @@ def fits_lane(S, P, W):
 
 
 def positions_per_lane(S, W):
-    return 8 if fits_lane(S, 8, W) else 4
+    return next(P for P in (16, 8, 4) if P == 4 or fits_lane(S, P, W))
 
 
 def max_group(W):
-    return next(S for S in (4, 3, 2, 1) if S == 1 or fits_lane(S, 4, W))
+    return next(S for S in (3, 2, 1) if S == 1 or fits_lane(S, 4, W))
 
 
 # (S, P, W) variants
-VARIANTS = [(S, positions_per_lane(S, W), W) for W in (8, 16, 32) for S in range(1, max_group(W) + 1)]
+VARIANTS = [(S, positions_per_lane(S, W), W) for W in (4, 8, 16, 32)
+            for S in range(1, max_group(W) + 1)]
 
 ACTS = ["lin", "sig", "tanh", "gau", "sin", "abs"]  # activation ids 0..5
 
@@ -68,7 +69,7 @@ def base(M, m, W):
 
 
 def log2(w):
-    return {8: 3, 16: 4, 32: 5}[w]
+    return {4: 2, 8: 3, 16: 4, 32: 5}[w]
 
 
 def bfe_imm(offset, width):

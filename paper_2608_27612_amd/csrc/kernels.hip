@@ -19,6 +19,7 @@
 
 namespace emr {
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x32 __attribute__((ext_vector_type(32)));
@@ -225,10 +226,9 @@ __device__ __forceinline__ uint32_t tile_parent_offset(uint32_t T) {
 }
 
 // Compaction of one pair by one wave, once every tile of the range has left its records at the
-// tile's own slots and its count in counts[pair * tiles + t]: scans the counts and moves
-// each tile's records down to their final, contiguous place, tile by tile in increasing order (a
-// tile's destination never overlaps a later tile's records, and each tile's records are all read
-// before any is written), then writes the pair's count and returns it.
+// tile's own slots and its count in counts[pair * tiles + t]: scans the counts, 64 tiles at a time,
+// and moves the records down to their final, contiguous place, then writes the pair's count and
+// returns it.
 __device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
                                  float* __restrict__ w4, int64_t* __restrict__ pair_count,
                                  int64_t cap, uint32_t tile_lo, uint32_t tiles, uint32_t pair,
@@ -247,21 +247,30 @@ __device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* 
     uint32_t incl = c;
 #pragma unroll
     for (int b = 0; b < 7; ++b) incl += mbcnt64(ballot((c >> b) & 1u)) << b;
-    // only tiles with records, in increasing order
-    for (uint64_t m = ballot(c != 0u); m != 0ull; m &= m - 1ull) {
-      const uint32_t i = (uint32_t)__builtin_ctzll(m);
-      const uint32_t ci = __builtin_amdgcn_readlane(c, i);
-      const uint32_t dst = running + __builtin_amdgcn_readlane(incl, i) - ci;
-      const uint32_t src = tile_parent_offset(tile_lo + t0 + i) - parent_lo;
-      if (dst == src) continue;
-      if (lane < ci) {
-        const uint32_t pv = parent[region + src + lane];
-        const float4 wv = reinterpret_cast<const float4*>(w4)[region + src + lane];
-        parent[region + dst + lane] = pv;
-        reinterpret_cast<float4*>(w4)[region + dst + lane] = wv;
+    // These tiles' records in batches of 64, lane l moving the batch's l-th record: its tile is
+    // the one (among the tiles with records) whose scan range holds it. A batch's loads all come
+    // before its stores, and no record moves up, so a batch never overwrites a later batch's
+    // records before they are read.
+    const uint32_t total = __builtin_amdgcn_readlane(incl, kWave - 1);
+    const uint64_t nz = ballot(c != 0u);
+    for (uint32_t b = 0; b < total; b += kWave) {
+      const uint32_t q = b + lane;  // the record's rank among these tiles' records
+      uint32_t src = running + q;
+      for (uint64_t m = nz; m != 0ull; m &= m - 1ull) {
+        const uint32_t i = (uint32_t)__builtin_ctzll(m);
+        const uint32_t hi = __builtin_amdgcn_readlane(incl, i);
+        const uint32_t lo = hi - __builtin_amdgcn_readlane(c, i);
+        if (q >= lo && q < hi) src = tile_parent_offset(tile_lo + t0 + i) - parent_lo + (q - lo);
+      }
+      const uint32_t dst = running + q;
+      if (q < total && src != dst) {
+        const uint32_t pv = parent[region + src];
+        const float4 wv = reinterpret_cast<const float4*>(w4)[region + src];
+        parent[region + dst] = pv;
+        reinterpret_cast<float4*>(w4)[region + dst] = wv;
       }
     }
-    running += __builtin_amdgcn_readlane(incl, kWave - 1);
+    running += total;
   }
   if (lane == 0) pair_count[pair] = running;
   return running;
@@ -329,7 +338,7 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
                                                const DiscoverScalars& a, const DiscoverPtrs& d,
                                                const LaneGeo& geo, uint32_t lane) {
   constexpr int P = positions_per_lane(S, W);
-  static_assert(P == 4 || P == 8, "a lane holds whole sibling quads");
+  static_assert(P == 4 || P == 8 || P == 16, "a lane holds whole sibling quads");
   constexpr int M = S * P;
   constexpr int TPW = P / kTileIters;  // tiles per walk
   // (the launcher makes chunk_tiles a multiple of TPW, so a walk's tiles lie in one chunk)
@@ -538,6 +547,9 @@ __global__ void __launch_bounds__(256)
     }
     const DiscoverPart pt = a.part[k];
     switch (pt.W * 4u + pt.S) {
+      case 4 * 4 + 3: discover_chunk<3, 4, MODE>(cl, pt, a, d, geo, lane); break;
+      case 4 * 4 + 2: discover_chunk<2, 4, MODE>(cl, pt, a, d, geo, lane); break;
+      case 4 * 4 + 1: discover_chunk<1, 4, MODE>(cl, pt, a, d, geo, lane); break;
       case 8 * 4 + 3: discover_chunk<3, 8, MODE>(cl, pt, a, d, geo, lane); break;
       case 8 * 4 + 2: discover_chunk<2, 8, MODE>(cl, pt, a, d, geo, lane); break;
       case 8 * 4 + 1: discover_chunk<1, 8, MODE>(cl, pt, a, d, geo, lane); break;
@@ -549,7 +561,7 @@ __global__ void __launch_bounds__(256)
     }
   }
 }
-static_assert(max_group(8) == 3 && max_group(16) == 2 && max_group(32) == 1,
+static_assert(max_group(4) == 3 && max_group(8) == 3 && max_group(16) == 2 && max_group(32) == 1,
               "the (S, W) variants of k_discover");
 
 // ------------------------------------------------------------------------ bind kernel
@@ -759,7 +771,7 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
   uint64_t groups = 0;
   for (uint32_t k = 0; k < a->n_parts; ++k) {
     const int S = (int)a->part_S[k], W = (int)a->part_W[k];
-    if ((W != 8 && W != 16 && W != 32) || S < 1 || S > emr::max_group(W))
+    if ((W != 4 && W != 8 && W != 16 && W != 32) || S < 1 || S > emr::max_group(W))
       return hipErrorInvalidValue;
     groups += a->part_groups[k];
   }

@@ -101,4 +101,4 @@ def test_scc_is_not_carried_across_inline_asm(asm):
 def test_record_step_clobbers_scc_and_m0():
     hdr = open(os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "regwin_gen.h")).read()
     n_walkers = hdr.count("struct Walker<")
-    assert n_walkers == 6 and hdr.count('"scc", "m0"') == n_walkers
+    assert n_walkers == 9 and hdr.count('"scc", "m0"') == n_walkers
