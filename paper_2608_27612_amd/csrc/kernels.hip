@@ -365,6 +365,27 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
   }
   const uint32_t n_rec = (G.flags & 1u) != 0 ? G.n_rec : 0u;  // no records: a uniform output
   const uint32_t chunk_end = min(chunk_tile + pt.chunk_tiles, a.tiles);
+  if constexpr (MODE != kModeRaw) {
+    if (n_rec == 0 && !(0.0f > a.theta4)) {
+      // A uniform output has variance 0 everywhere: with theta >= 0 every tile of the chunk keeps
+      // nothing, and its counts (padded) or inclusive prefixes (look-back: all zero, no
+      // predecessor needed) are written at once.
+      if (lane == 0) {
+        for (uint32_t t = chunk_tile; t < chunk_end; ++t)
+#pragma unroll
+          for (int s = 0; s < S; ++s) {
+            uint64_t* w = d.status + (int64_t)G.pair[s] * a.tiles + t;
+            if constexpr (MODE == kModePadded) {
+              *w = 0ull;
+            } else {
+              status_store(w, kStatusInclusive);
+              if (t + 1 == a.tiles) d.pair_count[G.pair[s]] = 0;
+            }
+          }
+      }
+      return;
+    }
+  }
 
   Walker<S, P, W> R;
   for (uint32_t t0 = chunk_tile; t0 < chunk_end; t0 += TPW) {
