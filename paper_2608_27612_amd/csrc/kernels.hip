@@ -305,6 +305,38 @@ __global__ void __launch_bounds__(kCompactWaves * kWave)
   }
 }
 
+// Where a level-aligned tile (a pair's tile T >= 1, 256 positions of one level) lies: its level
+// and the column and row of its 16 x 16 block of cells within the level, whose Morton index is z.
+// Consecutive tiles are stepped with a Morton increment instead of a fresh bit de-interleave.
+struct TileGeo {
+  uint32_t T, lvl, z, cx, cy;
+};
+__device__ __forceinline__ void tile_geo_set(TileGeo& g, uint32_t T) {
+  const uint32_t p0 = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(T - 1) * kTile);
+  g.T = T;
+  g.lvl = (uint32_t)level_of(p0);
+  g.z = (p0 - (uint32_t)level_offset((int)g.lvl)) >> 8;
+  g.cx = compact_even(g.z);
+  g.cy = compact_even(g.z >> 1);
+}
+__device__ __forceinline__ void tile_geo_next(TileGeo& g) {
+  g.T++;
+  if (g.z + 1u == 1u << (2u * (g.lvl - (uint32_t)kFirstAlignedLevel))) {  // the level's last tile
+    g.lvl++;
+    g.z = g.cx = g.cy = 0;
+    return;
+  }
+  // z + 1 clears z's t trailing ones (ceil(t/2) column bits, floor(t/2) row bits) and sets bit t
+  const uint32_t t = (uint32_t)__builtin_ctz(~g.z);
+  g.z++;
+  g.cx &= ~((1u << ((t + 1u) >> 1)) - 1u);
+  g.cy &= ~((1u << (t >> 1)) - 1u);
+  if (t & 1u)
+    g.cy |= 1u << (t >> 1);
+  else
+    g.cx |= 1u << (t >> 1);
+}
+
 // Per-lane constants of the position decode. Lane l holds parent q0 + l of a tile whose first
 // parent is q0. In a level-aligned tile the children's Morton indices are m0 + 4 l + c (m0 a
 // multiple of 256): lane bits 0, 2, 4 are the cell column's bits 1..3, lane bits 1, 3, 5 the row's,
@@ -388,6 +420,7 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
   }
 
   Walker<S, P, W> R;
+  TileGeo tg{0u, 0u, 0u, 0u, 0u};  // T = 0: not set yet
   for (uint32_t t0 = chunk_tile; t0 < chunk_end; t0 += TPW) {
     // ---- geometry of the walk's tiles (t0 counts from the launch's first tile, tile_lo). The
     // pair's tile 0 holds the parents of levels 1..3 (21 of them; the positions decoded one by
@@ -417,11 +450,13 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
       } else {
         p0[k] = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(tile - 1) * kTile);
         vmask[k] = in_range ? ~0ull : 0ull;
-        const int lvl = level_of(p0[k]);
-        const uint32_t m0 = p0[k] - (uint32_t)level_offset(lvl);
-        const float sc = pow2_neg(lvl);
-        const float bx = __builtin_fmaf((float)(32u * compact_even(m0 >> 8) + 1u), sc, -1.0f);
-        const float by = __builtin_fmaf((float)(32u * compact_even(m0 >> 9) + 1u), sc, -1.0f);
+        if (tg.T != 0u && tile == tg.T + 1u)
+          tile_geo_next(tg);
+        else
+          tile_geo_set(tg, tile);
+        const float sc = pow2_neg((int)tg.lvl);
+        const float bx = __builtin_fmaf((float)(32u * tg.cx + 1u), sc, -1.0f);
+        const float by = __builtin_fmaf((float)(32u * tg.cy + 1u), sc, -1.0f);
 #pragma unroll
         for (int c4 = 0; c4 < 4; ++c4) {
           px[4 * k + c4] = __builtin_fmaf(geo.xl[c4 & 1], sc, bx);
