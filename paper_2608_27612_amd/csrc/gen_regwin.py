@@ -85,6 +85,13 @@ BP = 62    # s[62:63]
 PC = 64    # s[64:65]
 
 
+def tail_stride(M):
+    """Byte stride of the activation tails: a power of two above the longest tail (the tanh
+    store, 4 M vector instructions and 6 scalar ones), at 8 bytes per instruction at most."""
+    longest = 8 * (4 * M + 6)
+    return 1 << (longest - 1).bit_length()
+
+
 def gen_walker(S, P, W):
     M = S * P
     A = ["v%d" % (ACC + m) for m in range(M)]
@@ -147,10 +154,14 @@ def gen_walker(S, P, W):
         L.append("s_set_gpr_idx_idx %[t]")
         L += ["v_fma_f32 %s, %s, %s, %s" % (A[m], T[m], wt[p], A[m]) for m in range(M)]
     L += [".Lee_%=:", "s_set_gpr_idx_off"]
-    # 3. tail: branch table on meta & 15; the record is read once the table index and the
-    # destination slot are taken, so the next record is loaded while the activation runs
+    # 3. tail: a computed jump to tail meta & 15 (tails 13..15 do not exist and go to the loop
+    # end, like a continuation record); the tails sit at a fixed stride. The record is read once
+    # the tail index and the destination slot are taken, so the next record is loaded while the
+    # activation runs.
+    stride = tail_stride(M)
     L += ["s_and_b32 %%[t], %s, 15" % meta,
-          "s_lshl_b32 %[t], %[t], 2",
+          "s_min_u32 %[t], %[t], 13",
+          "s_lshl_b32 %%[t], %%[t], %d" % (stride.bit_length() - 1),
           "s_add_u32 %[t], %[t], (.Lt0_%= - .Ltp_%=)",
           "s_bfe_u32 %%[u], %s, %s" % (meta, bfe_imm(8, log2(W))),
           "s_load_dwordx16 s[%d:%d], s[%d:%d], 0x0" % (REC, REC + 15, RP, RP + 1),
@@ -158,12 +169,7 @@ def gen_walker(S, P, W):
           ".Ltp_%=:",
           "s_add_u32 s%d, s%d, %%[t]" % (PC, PC),
           "s_addc_u32 s%d, s%d, 0" % (PC + 1, PC + 1),
-          "s_setpc_b64 %s" % pc,
-          ".Lt0_%=:"]
-    # tails: 0 continuation; 1..6 activation then store to the destination slot; 7..12 the
-    # output node's activation, applied to the accumulators in place
-    targets = ["x"] + ["%s%s" % (a, k) for k in ("", "o") for a in ACTS] + ["x"] * 3
-    L += ["s_branch .L%s_%%=" % t for t in targets]
+          "s_setpc_b64 %s" % pc]
     # the end of every tail: the next record, or out of the loop
     loop_end = ["s_sub_u32 %[n], %[n], 1",
                 "s_cmp_lg_u32 %[n], 0",
@@ -201,13 +207,29 @@ def gen_walker(S, P, W):
         "gau": (["v_mul_f32_e64 {a}, {a}, -{a}"], "v_exp_f32 {d}, {a}"),
         "sin": (["v_fract_f32 {a}, {a}"], "v_sin_f32 {d}, {a}"),
     }
+    # tails in index order: 0 continuation; 1..6 activation then store to the destination slot;
+    # 7..12 the output node's activation, applied to the accumulators in place; 13 the rest.
+    # Each is padded to the stride with never-executed words (s_nop encodings), so tail k starts
+    # at .Lt0 + k * stride; the assembler refuses a tail longer than the stride.
+    tails = [[".Lx_%=:"] + loop_end]
     for store in (True, False):
-        for name, (pre, final) in defs.items():
+        for name in ACTS:  # activation ids 0..5
+            pre, final = defs[name]
             if not store and name == "lin":
-                L += [".Llino_%=:"] + loop_end
+                tails.append([".Llino_%=:"] + loop_end)
                 continue
-            L += block(name + ("" if store else "o"), pre, final, store)
-    L += [".Lx_%=:"] + loop_end
+            tails.append(block(name + ("" if store else "o"), pre, final, store))
+    tails.append([".Linv_%=:"] + loop_end)
+    assert len(tails) == 14
+    for k, body in enumerate(tails):
+        assert 8 * sum(1 for l in body if not l.startswith(".")) <= stride, (M, k)
+        if k == 0:
+            L.append(".Lt0_%=:")
+        L += [".Ltb%d_%%=:" % k] + body + [".Lte%d_%%=:" % k,
+              ".if .Lte%d_%%= - .Ltb%d_%%= > %d" % (k, k, stride),
+              '.error \\"tail longer than its stride\\"',
+              ".endif",
+              ".fill (%d - (.Lte%d_%%= - .Ltb%d_%%=)) / 4, 4, 0xbf800000" % (stride, k, k)]
     # the last prefetch (one record and one row past the program, inside the tables) is drained
     # before the statement ends: its registers are the compiler's again after it
     L += [".Ldone_%=:", "s_waitcnt lgkmcnt(0)"]

@@ -185,7 +185,7 @@ struct DiscoverScalars {
   uint32_t n_parts, n_chunks;  // chunks of all parts
   DiscoverPart part[kMaxParts];
   int32_t depth;
-  float theta4;  // 4 theta
+  float theta16;  // 16 theta
   uint32_t blob_words, n_pairs;
   uint32_t bias_floats;  // the host keeps the bias table below 2^32 floats
   uint32_t head_parents;  // parents in a pair's tile 0 (levels 1..3, or all levels of a shallower grid)
@@ -398,7 +398,7 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
   const uint32_t n_rec = (G.flags & 1u) != 0 ? G.n_rec : 0u;  // no records: a uniform output
   const uint32_t chunk_end = min(chunk_tile + pt.chunk_tiles, a.tiles);
   if constexpr (MODE != kModeRaw) {
-    if (n_rec == 0 && !(0.0f > a.theta4)) {
+    if (n_rec == 0 && !(0.0f > a.theta16)) {
       // A uniform output has variance 0 everywhere: with theta >= 0 every tile of the chunk keeps
       // nothing, and its counts (padded) or inclusive prefixes (look-back: all zero, no
       // predecessor needed) are written at once.
@@ -487,20 +487,18 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
       continue;
     }
     // ---- variance of the four siblings (Section 3.2) and the threshold test (Eq. 2), inside
-    // the lane: s2 = the sum of the squared deviations from their mean = 4 var, tested as
-    // s2 > 4 theta (both scalings by 4 exact, barring overflow or a subnormal variance).
+    // the lane, from the pairwise split of the sum of squared deviations from the mean:
+    // 16 var = 2 (w0 - w1)^2 + 2 (w2 - w3)^2 + ((w0 + w1) - (w2 + w3))^2, tested as
+    // 16 var > 16 theta (both scalings by 16 exact, barring overflow or a subnormal variance).
     float s2[S][TPW];
 #pragma unroll
     for (int s = 0; s < S; ++s)
 #pragma unroll
       for (int k = 0; k < TPW; ++k) {
         const float* q = w + s * P + 4 * k;
-        const float sum = (q[0] + q[1]) + (q[2] + q[3]);
-        const float d0 = __builtin_fmaf(sum, -0.25f, q[0]);
-        const float d1 = __builtin_fmaf(sum, -0.25f, q[1]);
-        const float d2 = __builtin_fmaf(sum, -0.25f, q[2]);
-        const float d3 = __builtin_fmaf(sum, -0.25f, q[3]);
-        s2[s][k] = __builtin_fmaf(d3, d3, __builtin_fmaf(d2, d2, __builtin_fmaf(d1, d1, d0 * d0)));
+        const float c = q[0] - q[1], d = q[2] - q[3];
+        const float e = (q[0] + q[1]) - (q[2] + q[3]);
+        s2[s][k] = __builtin_fmaf(__builtin_fmaf(d, d, c * c), 2.0f, e * e);
       }
     // Nearly every cell is dropped: one test on the maximum decides whether any record is kept.
     float mx = s2[0][0];
@@ -508,7 +506,7 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
     for (int s = 0; s < S; ++s)
 #pragma unroll
       for (int k = 0; k < TPW; ++k) mx = __builtin_fmaxf(mx, s2[s][k]);
-    const bool some = ballot(mx > a.theta4) != 0ull;
+    const bool some = ballot(mx > a.theta16) != 0ull;
 
     if constexpr (MODE == kModePadded) {
       uint32_t run[S][TPW];  // records per source and tile
@@ -517,7 +515,7 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
         for (int s = 0; s < S; ++s)
 #pragma unroll
           for (int k = 0; k < TPW; ++k) {
-            const uint64_t kb = ballot(s2[s][k] > a.theta4) & vmask[k];
+            const uint64_t kb = ballot(s2[s][k] > a.theta16) & vmask[k];
             run[s][k] = popc64(kb);
             if ((kb >> lane) & 1ull) {
               // a tile's records start at its first parent index within the pair
@@ -551,7 +549,7 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
         if (tile >= a.tiles) break;
 #pragma unroll
         for (int s = 0; s < S; ++s) {
-          const uint64_t kb = some ? ballot(s2[s][k] > a.theta4) & vmask[k] : 0ull;
+          const uint64_t kb = some ? ballot(s2[s][k] > a.theta16) & vmask[k] : 0ull;
           const uint64_t cnt = popc64(kb);
           const uint32_t pair = G.pair[s];
           const uint64_t base = lookback(d.status + (int64_t)pair * a.tiles, tile, cnt, d.err);
@@ -854,7 +852,7 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
   if (chunks > 0xFFFFFFFFull) return hipErrorInvalidValue;
   sc.n_chunks = (uint32_t)chunks;
   sc.depth = a->depth;
-  sc.theta4 = 4.0f * a->theta;
+  sc.theta16 = 16.0f * a->theta;
   sc.blob_words = a->blob_words;
   sc.n_pairs = a->n_pairs;
   sc.bias_floats = (uint32_t)a->bias_floats;

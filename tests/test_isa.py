@@ -102,3 +102,52 @@ def test_record_step_clobbers_scc_and_m0():
     hdr = open(os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "regwin_gen.h")).read()
     n_walkers = hdr.count("struct Walker<")
     assert n_walkers == 9 and hdr.count('"scc", "m0"') == n_walkers
+
+
+def test_tail_jumps_land_on_their_tails():
+    """The record step jumps to tail (meta & 15) at .Lt0 + index * stride: in the disassembled
+    code object, every such jump site's tail slots begin with the instructions of their tails
+    (continuation and unknown tails: the loop end; store tails: the index switch or the first
+    activation step; output tails: the first activation step)."""
+    from paper_2608_27612_amd import build
+    llvm = "/opt/rocm/llvm/bin"
+    with tempfile.TemporaryDirectory() as d:
+        obj, dev = os.path.join(d, "k.o"), os.path.join(d, "k_gfx950.o")
+        subprocess.check_call([build.HIPCC, "-O3", "-std=c++17", "--cuda-device-only", "-c"]
+                              + build.DEVICE_FLAGS + [SRC, "-o", obj], stderr=subprocess.DEVNULL)
+        subprocess.check_call([os.path.join(llvm, "clang-offload-bundler"), "--unbundle",
+                               "--type=o", "--input=" + obj,
+                               "--targets=hipv4-amdgcn-amd-amdhsa--gfx950", "--output=" + dev])
+        out = subprocess.run([os.path.join(llvm, "llvm-objdump"), "-d", "--no-show-raw-insn", dev],
+                             capture_output=True, text=True, check=True).stdout
+    ins = []
+    for line in out.splitlines():
+        m = re.match(r"\s+(.*?)\s*//\s*([0-9A-Fa-f]+):", line)
+        if m:
+            ins.append((int(m.group(2), 16), m.group(1).strip()))
+    at = dict(ins)
+    # activation ids: 0 linear, 1 sigmoid, 2 tanh, 3 gaussian, 4 sine, 5 abs
+    first = ["s_sub_u32",                                   # 0 continuation
+             "s_set_gpr_idx_on", "v_exp_f32", "v_exp_f32", "v_mul_f32", "v_fract_f32",
+             "s_set_gpr_idx_on",                            # 1..6 store tails
+             "s_sub_u32", "v_exp_f32", "v_exp_f32", "v_mul_f32", "v_fract_f32",
+             "v_and_b32",                                   # 7..12 output tails
+             "s_sub_u32"]                                   # 13 unknown
+    sites = 0
+    for k, (_, text) in enumerate(ins):
+        m = re.match(r"s_lshl_b32 (\w+), \1, (\d+)$", text)
+        if not m or k + 1 >= len(ins):
+            continue
+        m2 = re.match(r"s_add_u32 %s, %s, (0x[0-9a-fA-F]+|\d+)" % (m.group(1), m.group(1)),
+                      ins[k + 1][1])
+        if not m2:
+            continue
+        j = k + 2
+        while not ins[j][1].startswith("s_getpc_b64"):
+            j += 1
+        t0 = ins[j + 1][0] + int(m2.group(1), 0)
+        stride = 1 << int(m.group(2))
+        got = [at.get(t0 + i * stride, "?") for i in range(14)]
+        assert all(g.startswith(f) for g, f in zip(got, first)), (stride, got)
+        sites += 1
+    assert sites == 3 * 9  # one per walker (9 sources-per-walk and window variants) per mode
