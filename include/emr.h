@@ -242,6 +242,33 @@ emr_status emr_discover_cost(const emr_population* pop, const emr_source* source
                              int32_t depth, double transcendental_slots, double* slots,
                              double* queries);
 
+/* ------------------------------------------------------------------ compiled tier */
+
+/* The discover kernel runs a call's varying CPPN programs either through the interpreter (the
+ * record step walks each packed program record by record) or as machine code compiled for the
+ * population: each (genome, direction) program is translated on the host into gfx950 instructions
+ * with its weights as literal operands, written into the code area of a copy of a template code
+ * object, and loaded as a module (Sections 3.1-3.2 compute the same thing either way; the compiled
+ * program performs the interpreter's arithmetic instruction for instruction, so both produce the
+ * same bits). Compilation costs host time (translation, about 1 ms per MB of code to load) and
+ * pays off for repeated or large calls. Policies:
+ *   EMR_JIT_OFF     always interpret;
+ *   EMR_JIT_AUTO    compile a plan (a population with the same sources and depth) when it is run
+ *                   a second time, or at once when the call is large; a failed compilation leaves
+ *                   the plan interpreted (see emr_jit_info);
+ *   EMR_JIT_ALWAYS  compile on the first call; a failed compilation fails the call. */
+enum { EMR_JIT_OFF = 0, EMR_JIT_AUTO = 1, EMR_JIT_ALWAYS = 2 };
+
+/* Sets the process-wide policy (default EMR_JIT_AUTO) for later calls. EMR_E_INVAL otherwise. */
+emr_status emr_set_jit(int32_t policy);
+
+/* The compiled tier of the population's current plan (the plan of its last call): *state 0 not
+ * compiled, 1 compiled, -1 compilation failed (emr_last_error then holds the reason); *programs the
+ * distinct programs compiled, *code_bytes their machine code, *compile_ms the host translation time
+ * and *load_ms the module load. Any output pointer may be NULL. Host only. */
+emr_status emr_jit_info(const emr_population* pop, int32_t* state, int64_t* programs,
+                        int64_t* code_bytes, double* compile_ms, double* load_ms);
+
 /* ------------------------------------------------------------------ profiling */
 
 /* One discover-kernel launch of a profiled emr_discover / emr_eval_raw call on this thread (a call
@@ -256,6 +283,7 @@ typedef struct {
   int64_t tiles, queries;
   double slots;
   float ms;
+  int32_t compiled; /* 1: the launch ran compiled programs, 0: the interpreter */
 } emr_launch_profile;
 
 /* Sets per-launch event timing for the calling thread's later calls and drops the records held:

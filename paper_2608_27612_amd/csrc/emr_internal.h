@@ -95,7 +95,8 @@ struct Group {
   uint32_t n_steps;
   uint32_t flags;      // copied from ProgDesc
   uint32_t bias_off;   // float offset into the bias table
-  uint32_t pad[3];
+  uint32_t code_off;   // compiled tier: byte offset of the group's program in the code area
+  uint32_t pad[2];
   uint32_t pair[kMaxGroup];  // global pair ids of the sources (unused entries repeat the last)
 };
 
@@ -158,6 +159,58 @@ EMR_HD inline int64_t tile_parent_offset(int64_t T, int depth) {
   if (depth < kFirstAlignedLevel) return n_parents(depth);
   return level_offset(kFirstAlignedLevel) / 4 + (T - 1) * (kTile / 4);
 }
+
+
+// ---------------------------------------------------------------- discover launch scalars
+// One launch covers every group of a call, in up to kMaxParts parts: the groups with S sources
+// per walk and register window W, one part per (S, W) present (costliest part first). The
+// launch's chunks are those of its parts, one after the other.
+struct DiscoverPart {
+  uint32_t S, W, group0;                     // sources per walk, window; the part's first group
+  uint32_t n_chunks, chunks_per_group, chunk_tiles;
+};
+struct DiscoverScalars {
+  int64_t cap, n_pos;
+  // The launch covers tiles tile_lo .. tile_lo + tiles - 1 of every pair; record slots of a pair
+  // region count from parent_lo, the first parent index of tile tile_lo.
+  uint32_t tile_lo, parent_lo, tiles;
+  uint32_t n_parts, n_chunks;  // chunks of all parts
+  DiscoverPart part[kMaxParts];
+  int32_t depth;
+  float theta16;  // 16 theta
+  uint32_t code_bytes;  // compiled tier: size of the code area (0 for the interpreter)
+  uint32_t blob_words, n_pairs;
+  uint32_t bias_floats;  // the host keeps the bias table below 2^32 floats
+  uint32_t head_parents;  // parents in a pair's tile 0 (levels 1..3, or all levels of a shallower grid)
+};
+
+// Output modes: raw CPPN outputs; records at fixed per-tile slots (pair_capacity >= Q(D)),
+// compacted afterwards by k_compact; records placed directly through the look-back scan (any
+// capacity).
+constexpr int kModeRaw = 0, kModePadded = 1, kModeLookback = 2;
+
+// ---------------------------------------------------------------- compiled tier
+// A walk calls its group's compiled program (machine code written at run time into the code area
+// of the template code object) with this register convention, shared by the call site in the
+// kernel and the host code generator. For M = S P instances:
+//   v[kJitAcc + m]                    accumulator of instance m (the program's outputs)
+//   v[jit_window(M, W, m) + k]        slot k of instance m's value window (k < W)
+//   v[jit_x(M, W) + j], + P + j       the x and y of position j (read only)
+//   v[jit_x(M, W) + 2 P ...]          temporaries: P partial sums and S bias copies (S > 1), or
+//                                     one bias copy (S = 1)
+//   s[kJitRow .. kJitRow + 31]        bias rows of up to 8 records (4 floats each)
+//   s[kJitBp, kJitBp + 1]             the group's bias rows (row 0 outputs of a program without
+//                                     records, row 1 + r the biases of the node starting at record r)
+//   s[kJitRet, kJitRet + 1]           the return address
+// A program touches nothing else: no memory writes, no exec, vcc or m0, no other registers.
+constexpr int kJitAcc = 4;
+constexpr int kJitRow = 40;
+constexpr int kJitBp = 72;
+constexpr int kJitRet = 74;
+constexpr uint32_t kJitTailPad = 1024;  // s_endpgm bytes kept after the last program
+EMR_HD constexpr int jit_window(int M, int W, int m) { return ((kJitAcc + M + 1) & ~1) + m * W; }
+EMR_HD constexpr int jit_x(int M, int W) { return jit_window(M, W, M); }
+EMR_HD constexpr int jit_temps(int S, int P) { return S > 1 ? P + S : 1; }
 
 struct DiscoverArgs {
   const uint32_t* blob;

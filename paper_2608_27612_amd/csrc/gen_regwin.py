@@ -283,15 +283,67 @@ def gen_walker(S, P, W):
     return "\n".join(out) + "\n"
 
 
+# The compiled tier's call convention (restated in emr_internal.h for the host code generator):
+# accumulators and value windows where the walker keeps them, the positions right after the
+# windows (x at XY .. XY + P - 1, y at XY + P ..), then the generated code's temporaries (P
+# partial sums and S bias copies for S > 1, one bias copy for S = 1); s[40:71] bias rows,
+# s[72:73] the group's bias row base, s[74:75] the return address.
+JIT_ROW, JIT_BP, JIT_RET = 40, 72, 74
+
+
+def jit_temps(S, P):
+    return P + S if S > 1 else 1
+
+
+def gen_jitcall(S, P, W):
+    M = S * P
+    xy = base(M, M, W)
+    tmp0 = xy + 2 * P
+    L = ["s_getpc_b64 s[%d:%d]" % (JIT_RET, JIT_RET + 1),
+         ".Lcall_%=:",
+         "s_add_u32 s%d, s%d, .Lret_%%= - .Lcall_%%=" % (JIT_RET, JIT_RET),
+         "s_addc_u32 s%d, s%d, 0" % (JIT_RET + 1, JIT_RET + 1),
+         "s_setpc_b64 %[tgt]",
+         ".Lret_%=:"]
+    outs = ['"={v%d}"(acc[%d])' % (ACC + m, m) for m in range(M)]
+    outs += ['"=&{v[%d:%d]}"(w%d)' % (base(M, m, W), base(M, m, W) + W - 1, m) for m in range(M)]
+    outs += ['"=&{v%d}"(t[%d])' % (tmp0 + k, k) for k in range(jit_temps(S, P))]
+    ins = ['[tgt] "s"(target)', '"{s[%d:%d]}"(bp)' % (JIT_BP, JIT_BP + 1)]
+    ins += ['"{v%d}"(x[%d]), "{v%d}"(y[%d])' % (xy + j, j, xy + P + j, j) for j in range(P)]
+    clob = ['"scc"'] + ['"s%d"' % r for r in range(JIT_ROW, JIT_BP)] + \
+        ['"s%d"' % JIT_RET, '"s%d"' % (JIT_RET + 1)]
+    body = "\n".join('        "%s\\n"' % l for l in L)
+    out = []
+    out.append("template <> struct JitCall<%d, %d, %d> {" % (S, P, W))
+    out.append("  float acc[%d];" % M)
+    out.append("  // Runs the compiled program at `target` for the P positions (x, y); bp: the group's bias rows.")
+    out.append("  __device__ __forceinline__ void call(uint64_t target, uint64_t bp, const float* x, "
+               "const float* y) {")
+    out.append("    f32x%d %s;" % (W, ", ".join("w%d" % m for m in range(M))))
+    out.append("    float t[%d];" % jit_temps(S, P))
+    out.append("    asm volatile(")
+    out.append(body)
+    out.append("        : %s" % ",\n          ".join(outs))
+    out.append("        : %s" % ",\n          ".join(ins))
+    out.append("        : %s);" % ", ".join(clob))
+    out.append("  }")
+    out.append("};")
+    return "\n".join(out) + "\n"
+
+
 def main():
-    print("// Generated by gen_regwin.py (the program-record step of the discover kernel).")
-    print("// Do not edit; regenerate with: python gen_regwin.py > regwin_gen.h")
+    print("// Generated by gen_regwin.py (the program-record step of the discover kernel, and the")
+    print("// call into a compiled program). Do not edit; regenerate with:")
+    print("// python gen_regwin.py > regwin_gen.h")
     print("#pragma once")
     print()
     print("template <int S, int P, int W> struct Walker;")
+    print("template <int S, int P, int W> struct JitCall;")
     print()
     for S, P, W in VARIANTS:
         print(gen_walker(S, P, W))
+    for S, P, W in VARIANTS:
+        print(gen_jitcall(S, P, W))
 
 
 if __name__ == "__main__":

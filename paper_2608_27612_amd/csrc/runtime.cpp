@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -16,6 +17,7 @@
 
 #include "../../include/emr.h"
 #include "emr_internal.h"
+#include "jit.h"
 #include "pack.h"
 
 // Launchers (kernels.hip).
@@ -31,6 +33,10 @@ extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* paren
 extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
                                         const float* w4, int64_t cap, uint32_t n_pairs,
                                         uint32_t* out_parent, float* out_w4, hipStream_t s);
+extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t blocks, int per_cu,
+                                         int cus, emr::DiscoverScalars* out, uint32_t* grid);
+// The compiled tier's template code object (jit_image.cpp).
+extern "C" const uint8_t emr_jit_template_begin[], emr_jit_template_end[];
 
 namespace {
 
@@ -139,6 +145,7 @@ struct emr_population {
   uint32_t* d_blob = nullptr;
   emr::ProgDesc* d_desc = nullptr;
   size_t blob_words = 0;
+  std::vector<uint32_t> h_blob;         // host copy of the program words (the code generator's input)
   // The plan of the last call (see plan_for): calls with the same sources and depth reuse it.
   mutable std::mutex plan_mu;
   mutable std::shared_ptr<const Plan> plan;
@@ -151,6 +158,32 @@ int window_bucket(int window) {
     if (window <= w) return w;
   return -1;
 }
+
+// The compiled tier of one plan: its groups' programs translated to machine code, written into the
+// code area of a copy of the template code object, loaded as a module on one device.
+struct JitModule {
+  int device = -1;
+  hipModule_t mod = nullptr;
+  hipFunction_t fn[3] = {};   // by output mode: raw, padded, look-back
+  int per_cu[3] = {1, 1, 1};  // workgroups per CU of each
+  uint32_t code_bytes = 0;    // size of the code area
+  emr::Group* d_groups = nullptr;  // the plan's group table with the code offsets
+  hipEvent_t last = nullptr;  // recorded after every launch from the module
+  size_t programs = 0, program_bytes = 0, image_bytes = 0;
+  double compile_ms = 0.0, load_ms = 0.0;
+  JitModule() = default;
+  JitModule(const JitModule&) = delete;
+  JitModule& operator=(const JitModule&) = delete;
+  ~JitModule() {
+    // nothing queued may still run the module's code or read its tables
+    if (last) {
+      (void)hipEventSynchronize(last);
+      (void)hipEventDestroy(last);
+    }
+    if (d_groups) (void)hipFree(d_groups);
+    if (mod) (void)hipModuleUnload(mod);
+  }
+};
 
 // Everything one discover / raw-eval call needs besides the population.
 struct Plan {
@@ -189,8 +222,15 @@ struct Plan {
   Plan(const Plan&) = delete;
   Plan& operator=(const Plan&) = delete;
   ~Plan() {
+    jit.reset();  // waits for the compiled tier's last launch
     if (d_tables) (void)hipFree(d_tables);
   }
+  // The compiled tier (jit_use): built at most once per plan, under jit_mu.
+  mutable std::mutex jit_mu;
+  mutable std::unique_ptr<JitModule> jit;
+  mutable int jit_state = 0;  // 0 not built, 1 ready, -1 failed (reason in jit_error)
+  mutable std::string jit_error;
+  mutable std::atomic<int> calls{0};  // calls that ran this plan
   // What the plan was built for (exact copies, compared on reuse).
   std::vector<emr_source> key_sources;
   std::vector<int32_t> key_offs;
@@ -465,13 +505,206 @@ emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspac
   return EMR_OK;
 }
 
+// ------------------------------------------------------------------ compiled tier
+std::atomic<int> g_jit_policy{EMR_JIT_AUTO};
+
+// The template's code area: 1024 words of s_endpgm (jit.hip).
+constexpr size_t kTemplateArea = 4096;
+
+// Translates every distinct (program, sources per walk, window) of the plan's groups to machine
+// code, writes the programs (64-byte aligned) into a copy of the template whose code area is
+// grown to fit them, loads the copy as a module on the current device, and uploads the plan's
+// group table with each group's code offset.
+emr_status jit_build(const emr_population* pop, const Plan& P, std::unique_ptr<JitModule>* out) {
+  using clock = std::chrono::steady_clock;
+  const auto t0 = clock::now();
+  auto M = std::make_unique<JitModule>();
+  // distinct programs: key (desc, bucket) -> index
+  struct Job {
+    uint32_t desc;
+    int S, W;
+  };
+  std::vector<Job> jobs;
+  std::vector<uint32_t> job_of_group(P.groups.size());
+  {
+    std::vector<std::pair<uint64_t, uint32_t>> keys;
+    keys.reserve(P.groups.size());
+    for (const Plan::Bucket& b : P.buckets)
+      for (uint32_t g = b.first; g < b.first + b.count; ++g) {
+        const uint32_t desc = P.members[P.group_member0[g]].desc;
+        keys.push_back({((uint64_t)desc << 16) | ((uint64_t)b.S << 8) | (uint64_t)b.window, g});
+      }
+    std::sort(keys.begin(), keys.end());
+    for (size_t i = 0; i < keys.size(); ++i) {
+      if (i == 0 || keys[i].first != keys[i - 1].first)
+        jobs.push_back({(uint32_t)(keys[i].first >> 16), (int)((keys[i].first >> 8) & 0xFF),
+                        (int)(keys[i].first & 0xFF)});
+      job_of_group[keys[i].second] = (uint32_t)(jobs.size() - 1);
+    }
+  }
+  std::vector<emr::jit::Code> code(jobs.size());
+  std::vector<std::string> errs(jobs.size());
+  std::vector<char> ok(jobs.size(), 0);
+  auto work = [&](size_t lo, size_t hi) {
+    for (size_t j = lo; j < hi; ++j) {
+      const Job& J = jobs[j];
+      const emr::ProgDesc& d = pop->desc[J.desc];
+      if ((uint64_t)d.var_off + 16ull * d.n_rec > pop->h_blob.size()) {
+        errs[j] = "program outside the population table";
+        continue;
+      }
+      ok[j] = emr::jit::compile_program(pop->h_blob.data() + d.var_off, d.n_rec,
+                                        (d.flags & 1u) != 0, J.S,
+                                        emr::positions_per_lane(J.S, J.W), J.W, false, &code[j],
+                                        &errs[j]);
+    }
+  };
+  const int hw = (int)std::max(1u, std::thread::hardware_concurrency());
+  const int n_threads = (int)std::max<size_t>(1, std::min<size_t>({(size_t)hw, 16, jobs.size() / 64}));
+  if (n_threads == 1) {
+    work(0, jobs.size());
+  } else {
+    std::vector<std::thread> pool;
+    for (int t = 0; t < n_threads; ++t)
+      pool.emplace_back(work, jobs.size() * t / n_threads, jobs.size() * (t + 1) / n_threads);
+    for (auto& th : pool) th.join();
+  }
+  std::vector<uint32_t> offs(jobs.size());
+  size_t bytes = 0;
+  for (size_t j = 0; j < jobs.size(); ++j) {
+    if (!ok[j]) return fail(EMR_E_INVAL, "compiling a program: %s", errs[j].c_str());
+    offs[j] = (uint32_t)bytes;
+    bytes += (code[j].words.size() * 4 + 63) & ~size_t(63);
+    if (bytes > (size_t(1) << 30)) return fail(EMR_E_LIMIT, "compiled programs exceed 1 GiB");
+  }
+  const size_t need = bytes + emr::kJitTailPad;
+  const size_t area = need <= kTemplateArea ? kTemplateArea
+                                            : kTemplateArea + ((need - kTemplateArea + 4095) & ~size_t(4095));
+  // the template copy, grown, with the programs written into its area
+  const uint8_t* tpl = emr_jit_template_begin;
+  const size_t tpl_n = (size_t)(emr_jit_template_end - emr_jit_template_begin);
+  emr::jit::AreaInfo ai;
+  std::string msg;
+  std::vector<uint8_t> img;
+  if (!emr::jit::find_area(tpl, tpl_n, kTemplateArea, &ai, &msg) ||
+      !emr::jit::grow_area(tpl, tpl_n, ai, area, &img, &msg))
+    return fail(EMR_E_DEVICE, "compiled tier: %s", msg.c_str());
+  for (size_t j = 0; j < jobs.size(); ++j)
+    std::memcpy(img.data() + ai.file_off + offs[j], code[j].words.data(), code[j].words.size() * 4);
+  const auto t1 = clock::now();
+  HIP_OR_FAIL(hipGetDevice(&M->device));
+  HIP_OR_FAIL(hipModuleLoadData(&M->mod, img.data()));
+  static const char* names[3] = {"emr_discover_jit_raw", "emr_discover_jit_padded",
+                                 "emr_discover_jit_lookback"};
+  for (int k = 0; k < 3; ++k) {
+    HIP_OR_FAIL(hipModuleGetFunction(&M->fn[k], M->mod, names[k]));
+    int n = 0;
+    if (hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&n, M->fn[k], 256, 0) == hipSuccess && n > 0)
+      M->per_cu[k] = n;
+  }
+  M->code_bytes = (uint32_t)area;
+  std::vector<emr::Group> groups = P.groups;
+  for (size_t g = 0; g < groups.size(); ++g) groups[g].code_off = offs[job_of_group[g]];
+  if (!groups.empty()) {
+    HIP_OR_FAIL(hipMalloc((void**)&M->d_groups, groups.size() * sizeof(emr::Group)));
+    HIP_OR_FAIL(hipMemcpy(M->d_groups, groups.data(), groups.size() * sizeof(emr::Group),
+                          hipMemcpyHostToDevice));
+  }
+  HIP_OR_FAIL(hipEventCreateWithFlags(&M->last, hipEventDisableTiming));
+  const auto t2 = clock::now();
+  M->programs = jobs.size();
+  M->program_bytes = bytes;
+  M->image_bytes = img.size();
+  M->compile_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
+  M->load_ms = std::chrono::duration<double, std::milli>(t2 - t1).count();
+  *out = std::move(M);
+  return EMR_OK;
+}
+
+// Whether a call of `slots` algorithmic slots runs the plan's compiled programs, building them
+// first when the policy asks for it: EMR_JIT_ALWAYS builds on the first call (and a failed build
+// fails the call); EMR_JIT_AUTO builds when the plan is run a second time (the same population
+// and sources again: a benchmark loop, or repeated queries), or at once for a call large enough
+// that the faster kernel repays the build (an interpreted call above ~10 ms); a failed build
+// leaves the plan interpreted (the reason is kept for emr_jit_info).
+emr_status jit_use(const emr_population* pop, const Plan& P, double slots, bool* use) {
+  *use = false;
+  const int policy = g_jit_policy.load();
+  const int n = ++P.calls;
+  if (policy == EMR_JIT_OFF || P.groups.empty()) return EMR_OK;
+  std::lock_guard<std::mutex> lock(P.jit_mu);
+  int dev = 0;
+  HIP_OR_FAIL(hipGetDevice(&dev));
+  if (P.jit_state == 1) {
+    *use = P.jit->device == dev;
+    return EMR_OK;
+  }
+  if (P.jit_state == -1) {
+    if (policy == EMR_JIT_ALWAYS)
+      return fail(EMR_E_DEVICE, "the compiled tier failed for this plan: %s", P.jit_error.c_str());
+    return EMR_OK;
+  }
+  const double interp_ms = slots / 2.2e10;  // the interpreter's measured rate, ~22 T slots/s
+  if (policy == EMR_JIT_AUTO && n < 2 && interp_ms < 10.0) return EMR_OK;
+  std::unique_ptr<JitModule> M;
+  emr_status st = jit_build(pop, P, &M);
+  if (st != EMR_OK) {
+    P.jit_state = -1;
+    P.jit_error = g_err;
+    return policy == EMR_JIT_ALWAYS ? st : EMR_OK;
+  }
+  P.jit = std::move(M);
+  P.jit_state = 1;
+  *use = true;
+  return EMR_OK;
+}
+
+// Algorithmic slots of a whole call (every tile of every pair) under the default cost model.
+double plan_slots(const Plan& P) {
+  double s = 0.0;
+  for (const Plan::Launch& L : P.launches) s += L.slots_base + 4.0 * L.slots_trans;
+  return s * (double)emr::n_positions(P.depth);
+}
+
 // Enqueues the discover launch (every bucket, on the caller's stream) for tiles
 // tile_lo .. tile_lo + n_tiles - 1 of every pair, then the compaction when records go to padded
 // slots. Records of pair r go to its region of `out` counted from the range's first parent; raw
 // outputs to raw[r * N(D) + p].
+// The compiled tier's discover launch: the same scalars and grid sizing as the interpreter's,
+// through the plan's module.
+emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint32_t blocks,
+                      hipStream_t s, hipEvent_t start, hipEvent_t stop) {
+  const JitModule& M = *P.jit;
+  emr::DiscoverScalars sc{};
+  uint32_t grid = 0;
+  HIP_OR_FAIL(emr_discover_setup(&a, blocks, M.per_cu[mode], device_cu_count(), &sc, &grid));
+  sc.code_bytes = M.code_bytes;
+  if (start) HIP_OR_FAIL(hipEventRecord(start, s));
+  if (grid > 0) {
+    const uint32_t* blob = a.blob;
+    const emr::Group* grp = a.groups;
+    const float* bias_tab = a.bias_tab;
+    uint64_t* status = a.status;
+    uint32_t* err = a.err;
+    uint32_t* parent = a.parent;
+    float* w4 = a.w4;
+    int64_t* pair_count = a.pair_count;
+    float* raw = a.raw;
+    void* args[] = {&blob, &grp, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw, &sc};
+    if (mode == 2)  // look-back placement relies on every wave being resident
+      HIP_OR_FAIL(hipModuleLaunchCooperativeKernel(M.fn[mode], grid, 1, 1, 256, 1, 1, 0, s, args));
+    else
+      HIP_OR_FAIL(hipModuleLaunchKernel(M.fn[mode], grid, 1, 1, 256, 1, 1, 0, s, args, nullptr));
+  }
+  if (stop) HIP_OR_FAIL(hipEventRecord(stop, s));
+  HIP_OR_FAIL(hipEventRecord(M.last, s));
+  return EMR_OK;
+}
+
+// jit: run the plan's compiled programs (jit_use said so) instead of the interpreter.
 emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
                         const emr_result* out, float* raw, void* workspace, hipStream_t s,
-                        int64_t tile_lo, int64_t n_tiles) {
+                        int64_t tile_lo, int64_t n_tiles, bool jit) {
   char* ws = (char*)workspace;
   char* tables = nullptr;
   emr_status tst = plan_tables(P, &tables);
@@ -503,7 +736,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
     const Plan::Launch& L = P.launches[li];
     emr::DiscoverArgs a{};
     a.blob = pop->d_blob;
-    a.groups = (const emr::Group*)(tables + P.t_groups);
+    a.groups = jit ? P.jit->d_groups : (const emr::Group*)(tables + P.t_groups);
     a.bias_tab = (const float*)(ws + P.off_bias);
     a.status = (uint64_t*)(ws + P.off_status);
     a.err = (uint32_t*)(ws + P.off_err);
@@ -531,9 +764,14 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
     a.bias_floats = P.bias_floats;
     const uint32_t blocks = (uint32_t)cus * 16;  // the launcher sizes the grid below this
     const bool timed = li < n_timed;
-    HIP_OR_FAIL(emr_launch_discover(&a, mode, blocks, s,
-                                    timed ? prof.events[2 * (rec0 + li)] : nullptr,
-                                    timed ? prof.events[2 * (rec0 + li) + 1] : nullptr));
+    hipEvent_t e0 = timed ? prof.events[2 * (rec0 + li)] : nullptr;
+    hipEvent_t e1 = timed ? prof.events[2 * (rec0 + li) + 1] : nullptr;
+    if (jit) {
+      emr_status js = jit_launch(P, a, mode, blocks, s, e0, e1);
+      if (js != EMR_OK) return js;
+    } else {
+      HIP_OR_FAIL(emr_launch_discover(&a, mode, blocks, s, e0, e1));
+    }
     if (timed) {
       emr_launch_profile r{};
       r.call = prof.calls;
@@ -545,6 +783,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
         r.tiles += (int64_t)P.buckets[(size_t)L.part[k]].count * n_tiles;
       r.slots = npos * (L.slots_base + prof.rT * L.slots_trans);
       r.queries = (int64_t)(npos * L.sources);
+      r.compiled = jit ? 1 : 0;
       prof.recs.push_back(r);
     }
   }
@@ -589,7 +828,10 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
   const bool lookback = out && !raw && out->pair_capacity < emr::n_parents(P.depth);
   emr_status st = prepare_plan(pop, P, workspace, workspace_bytes, s, lookback);
   if (st != EMR_OK) return st;
-  st = launch_range(pop, P, theta, out, raw, workspace, s, 0, P.tiles);
+  bool jit = false;
+  st = jit_use(pop, P, plan_slots(P), &jit);
+  if (st != EMR_OK) return st;
+  st = launch_range(pop, P, theta, out, raw, workspace, s, 0, P.tiles, jit);
   if (st != EMR_OK) return st;
   return queue_flags_readback(workspace, s);
 }
@@ -716,13 +958,14 @@ emr_status pack_and_upload(int32_t n, const std::function<emr_genome(int32_t)>& 
       return fail(EMR_E_NOMEM, "pinned upload staging of %zu bytes failed", want);
     up_size = want;
   }
-  char* img = (char*)up_buf;
+  pop->h_blob.assign(total, 0u);
   size_t off = 0;
   for (const Part& p : parts) {
-    std::memcpy(img + off, p.words.data(), p.words.size() * 4);
-    off += p.words.size() * 4;
+    std::copy(p.words.begin(), p.words.end(), pop->h_blob.begin() + (ptrdiff_t)off);
+    off += p.words.size();
   }
-  std::memset(img + off, 0, 16 * 4);
+  char* img = (char*)up_buf;
+  std::memcpy(img, pop->h_blob.data(), blob_bytes);
   std::memcpy(img + blob_bytes, pop->desc.data(), pop->desc.size() * sizeof(emr::ProgDesc));
   StreamPool* sp = nullptr;
   emr_status st = stream_pool(&sp);
@@ -901,6 +1144,44 @@ emr_status emr_discover_cost(const emr_population* pop, const emr_source* source
   return EMR_OK;
 }
 
+emr_status emr_set_jit(int32_t policy) {
+  if (policy != EMR_JIT_OFF && policy != EMR_JIT_AUTO && policy != EMR_JIT_ALWAYS)
+    return fail(EMR_E_INVAL, "compiled-tier policy %d (0 off, 1 auto, 2 always)", policy);
+  g_jit_policy.store(policy);
+  return EMR_OK;
+}
+
+emr_status emr_jit_info(const emr_population* pop, int32_t* state, int64_t* programs,
+                        int64_t* code_bytes, double* compile_ms, double* load_ms) {
+  if (!pop) return fail(EMR_E_INVAL, "population is NULL");
+  std::shared_ptr<const Plan> plan;
+  {
+    std::lock_guard<std::mutex> lock(pop->plan_mu);
+    plan = pop->plan;
+  }
+  int32_t st = 0;
+  int64_t np = 0, nb = 0;
+  double cm = 0.0, lm = 0.0;
+  if (plan) {
+    std::lock_guard<std::mutex> lock(plan->jit_mu);
+    st = plan->jit_state;
+    if (st == 1) {
+      np = (int64_t)plan->jit->programs;
+      nb = (int64_t)plan->jit->program_bytes;
+      cm = plan->jit->compile_ms;
+      lm = plan->jit->load_ms;
+    } else if (st == -1) {
+      g_err = plan->jit_error;
+    }
+  }
+  if (state) *state = st;
+  if (programs) *programs = np;
+  if (code_bytes) *code_bytes = nb;
+  if (compile_ms) *compile_ms = cm;
+  if (load_ms) *load_ms = lm;
+  return EMR_OK;
+}
+
 emr_status emr_profile_enable(int32_t on, int32_t every, double transcendental_slots) {
   if (on < 0 || on > 2) return fail(EMR_E_INVAL, "profile mode %d (0 off, 1 every launch, 2 first)", on);
   if (every < 1) return fail(EMR_E_INVAL, "profile every %d calls", every);
@@ -1049,6 +1330,9 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
   st = prepare_plan(pop, P, R.ws, (int64_t)P.total, R.s, false);
   if (st != EMR_OK) return st;
   emr_result chunk_out{R.pad_parent, R.pad_w4, cap, R.counts, R.ws, (int64_t)P.total};
+  bool jit = false;
+  st = jit_use(pop, P, plan_slots(P) * (double)(total - start) / (double)total, &jit);
+  if (st != EMR_OK) return st;
 
   // Chunk c on the compute stream: discover + compact over its tiles, gather into buffer c & 1,
   // counts to pinned memory.
@@ -1056,7 +1340,7 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     const int b = (int)(c & 1);
     if (R.copy_pending[b]) HIP_OR_FAIL(hipStreamWaitEvent(R.s, R.ev_copy[b], 0));
     const int64_t tile_lo = c * tpc, n = std::min<int64_t>(tpc, P.tiles - tile_lo);
-    emr_status e = launch_range(pop, P, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n);
+    emr_status e = launch_range(pop, P, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n, jit);
     if (e != EMR_OK) return e;
     HIP_OR_FAIL(emr_launch_gather(R.counts, R.pad_parent, R.pad_w4, cap, (uint32_t)n_pairs,
                                   R.g_parent[b], R.g_w4[b], R.s));

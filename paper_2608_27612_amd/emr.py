@@ -26,7 +26,9 @@ ABI_FUNCTIONS = [
     "emr_free_population", "emr_population_info", "emr_workspace_bytes", "emr_discover",
     "emr_result_check", "emr_eval_raw", "emr_discover_cost", "emr_profile_enable",
     "emr_profile_read", "emr_stream_chunks", "emr_discover_stream", "emr_pack_population_flat",
+    "emr_set_jit", "emr_jit_info",
 ]
+EMR_JIT_OFF, EMR_JIT_AUTO, EMR_JIT_ALWAYS = 0, 1, 2
 
 
 class EmrError(RuntimeError):
@@ -54,7 +56,7 @@ class emr_result(C.Structure):
 class emr_launch_profile(C.Structure):
     _fields_ = [("group_size", C.c_int32), ("window", C.c_int32), ("positions", C.c_int32),
                 ("call", C.c_int32), ("tiles", C.c_int64), ("queries", C.c_int64),
-                ("slots", C.c_double), ("ms", C.c_float)]
+                ("slots", C.c_double), ("ms", C.c_float), ("compiled", C.c_int32)]
 
 
 _lib = None
@@ -92,6 +94,8 @@ def lib():
             "emr_stream_chunks": (I32, [I32, I64, P]),
             "emr_pack_population_flat": (I32, [I32, P, P, P, P, P, P, P, P, P, P, P]),
             "emr_discover_stream": (I32, [P, P, I32, P, I32, I32, F32, I64, I64, SINK, P, P, P]),
+            "emr_set_jit": (I32, [I32]),
+            "emr_jit_info": (I32, [P, P, P, P, P, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -364,7 +368,29 @@ def emr_profile_read():
     for i, r in enumerate(arr[:n.value]):
         out.append({"S": r.group_size, "W": r.window, "P": r.positions, "call": r.call,
                     "tiles": r.tiles, "queries": r.queries, "slots": r.slots, "ms": r.ms,
+                    "compiled": bool(r.compiled),
                     "first": i == 0 or arr[i - 1].call != r.call})
+    return out
+
+
+# ----------------------------------------------------------------------------- compiled tier
+
+def emr_set_jit(policy: int):
+    """Process-wide compiled-tier policy: EMR_JIT_OFF, EMR_JIT_AUTO (default), EMR_JIT_ALWAYS."""
+    _check(lib().emr_set_jit(int(policy)))
+
+
+def emr_jit_info(pop: Population):
+    """The compiled tier of the population's current plan: {"state": 0 not compiled / 1 compiled /
+    -1 failed, "programs", "code_bytes", "compile_ms", "load_ms", "error" (when failed)}."""
+    st, npg, nb = C.c_int32(), C.c_int64(), C.c_int64()
+    cm, lm = C.c_double(), C.c_double()
+    _check(lib().emr_jit_info(pop.handle, C.byref(st), C.byref(npg), C.byref(nb), C.byref(cm),
+                              C.byref(lm)))
+    out = {"state": st.value, "programs": npg.value, "code_bytes": nb.value,
+           "compile_ms": cm.value, "load_ms": lm.value}
+    if st.value == -1:
+        out["error"] = lib().emr_last_error().decode()
     return out
 
 

@@ -35,3 +35,43 @@ extern "C" int shim_pack(const emr_genome* g, uint32_t* blob, int64_t blob_cap, 
   }
   return 0;
 }
+
+// The compiled tier's host side: one program's machine words and listing.
+#include "../../paper_2608_27612_amd/csrc/jit.h"
+
+extern "C" int shim_compile(const uint32_t* rec, uint32_t n_rec, int output_varies, int S, int P,
+                            int W, uint32_t* words, int64_t cap, int64_t* n_words, char* listing,
+                            int64_t listing_cap, char* msg, int msg_cap) {
+  emr::jit::Code code;
+  std::string m;
+  if (!emr::jit::compile_program(rec, n_rec, output_varies != 0, S, P, W, true, &code, &m)) {
+    std::strncpy(msg, m.c_str(), (size_t)msg_cap - 1);
+    msg[msg_cap - 1] = 0;
+    return 1;
+  }
+  *n_words = (int64_t)code.words.size();
+  if ((int64_t)code.words.size() > cap || (int64_t)code.listing.size() + 1 > listing_cap) return 2;
+  std::memcpy(words, code.words.data(), code.words.size() * 4);
+  std::memcpy(listing, code.listing.c_str(), code.listing.size() + 1);
+  return 0;
+}
+
+// The template code object with its code area grown to new_bytes; *area_off: the area's file offset.
+extern "C" int shim_grow(const uint8_t* img, int64_t n, int64_t area_bytes, int64_t new_bytes,
+                         uint8_t* out, int64_t cap, int64_t* n_out, int64_t* area_off, char* msg,
+                         int msg_cap) {
+  emr::jit::AreaInfo info;
+  std::string m;
+  std::vector<uint8_t> o;
+  if (!emr::jit::find_area(img, (size_t)n, (size_t)area_bytes, &info, &m) ||
+      !emr::jit::grow_area(img, (size_t)n, info, (size_t)new_bytes, &o, &m)) {
+    std::strncpy(msg, m.c_str(), (size_t)msg_cap - 1);
+    msg[msg_cap - 1] = 0;
+    return 1;
+  }
+  *n_out = (int64_t)o.size();
+  *area_off = (int64_t)info.file_off;
+  if ((int64_t)o.size() > cap) return 2;
+  std::memcpy(out, o.data(), o.size());
+  return 0;
+}

@@ -151,3 +151,79 @@ def test_tail_jumps_land_on_their_tails():
         assert all(g.startswith(f) for g, f in zip(got, first)), (stride, got)
         sites += 1
     assert sites == 3 * 9  # one per walker (9 sources-per-walk and window variants) per mode
+
+
+# ------------------------------------------------------------------ the compiled tier's template
+JIT_SRC = os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "jit.hip")
+
+
+@pytest.fixture(scope="module")
+def jit_asm():
+    from paper_2608_27612_amd import build
+    with tempfile.TemporaryDirectory() as d:
+        out = os.path.join(d, "j.s")
+        cmd = [build.HIPCC, "-O3", "-std=c++17", "--cuda-device-only", "-S"] + build.DEVICE_FLAGS \
+            + [JIT_SRC, "-o", out]
+        subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
+        return open(out).read()
+
+
+def test_template_has_no_packed_fp32_scalar_writes_m0_or_scratch(jit_asm):
+    assert not re.search(r"v_pk_(add|mul|fma)_f32", jit_asm)
+    pattern = r"\bs_(buffer_)?(st" + r"ore|atom" + r"ic)\w*|\bs_dca" + r"che_\w+|\bs_scr" + r"atch_\w+"
+    assert not re.search(pattern, jit_asm)
+    for line in jit_asm.splitlines():
+        code = line.split(";")[0]
+        assert not re.search(r"\bm0\b", code), line
+        assert "s_set_gpr_idx" not in code, line
+    for size in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", jit_asm):
+        assert int(size) == 0
+
+
+def test_template_does_not_carry_scc_across_calls(jit_asm):
+    lines = jit_asm.splitlines()
+    calls = 0
+    for i, line in enumerate(lines):
+        if "s_setpc_b64" not in line.split(";")[0]:
+            continue
+        calls += 1
+        for k in range(i + 1, min(i + 80, len(lines))):
+            code = lines[k].split(";")[0]
+            if not code.strip() or code.strip().startswith("."):
+                continue
+            assert not _SCC_READERS.match(code), "SCC read after a call: " + code.strip()
+            if _SCC_WRITERS.match(code) or re.match(r"^\s*s_(branch|endpgm|setpc)", code):
+                break
+    assert calls == 3 * 9  # one call site per (sources per walk, window) variant per mode
+
+
+def test_template_kernels_allocate_the_convention_registers(jit_asm):
+    """Every kernel of the template declares at least the VGPRs the compiled programs of its
+    variants use (accumulators, windows, positions and temporaries)."""
+    import sys
+    sys.path.insert(0, os.path.join(ROOT, "paper_2608_27612_amd", "csrc"))
+    import gen_regwin as G
+    top = max(G.base(S * P, S * P, W) + 2 * P + G.jit_temps(S, P) for S, P, W in G.VARIANTS)
+    counts = re.findall(r"\.name:\s+(emr_discover_jit_\w+)\s*\n(?:.*\n)*?\s+\.vgpr_count:\s+(\d+)",
+                        jit_asm)
+    assert len(counts) == 3
+    for name, n in counts:
+        assert int(n) >= top, (name, n, top)
+
+
+def test_code_area_ends_the_template_text():
+    """The area's holder is the last function of the object's .text, so growing the area moves
+    nothing the kernels refer to."""
+    co = os.path.join(ROOT, "paper_2608_27612_amd", "libemr_jit.co")
+    if not os.path.exists(co):
+        pytest.skip("template code object not built")
+    out = subprocess.run(["/opt/rocm/llvm/bin/llvm-readelf", "-s", "-S", co], capture_output=True,
+                         text=True, check=True).stdout
+    funcs = [(int(v, 16), int(sz), n) for v, sz, n in
+             re.findall(r"^\s*\d+:\s+([0-9a-f]{16})\s+(\d+)\s+FUNC\s+\w+\s+\w+\s+\S+\s+(\S+)\s*$",
+                        out, flags=re.M)]
+    last = max(funcs)
+    assert last[2] == "emr_code_area_holder"
+    area = re.search(r"^\s*\d+:\s+([0-9a-f]{16})\s+\d+\s+NOTYPE\s+LOCAL\s+\w+\s+\S+\s+emr_code_area\s*$",
+                     out, flags=re.M)
+    assert area and last[0] < int(area.group(1), 16) < last[0] + last[1]
