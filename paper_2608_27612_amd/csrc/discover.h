@@ -194,6 +194,7 @@ struct LaneGeo {
 
 // The tables and outputs of a launch.
 struct DiscoverPtrs {
+  cu32* geo;  // tile geometry rows {bx, by, 2^-level, p0} (k_tile_geo)
   cu32* blob;
   cu32* groups;
   cf32* bias;
@@ -204,6 +205,22 @@ struct DiscoverPtrs {
   int64_t* pair_count;
   float* raw;
 };
+
+// Padded placement: the record counts of a chunk's tiles, source s and tile chunk_tile + k held
+// in lane 16 s + k, stored by those lanes at once (the status words of the tiles outside the
+// launch range are never written).
+template <int S>
+__device__ __forceinline__ void store_chunk_counts(const DiscoverPtrs& d, const DiscoverScalars& a,
+                                                   const Group& G, uint32_t chunk_tile,
+                                                   uint32_t chunk_end, uint32_t counts,
+                                                   uint32_t lane) {
+  // one store per source (its pair id uniform), lanes 16 s .. 16 s + 15
+  const uint32_t k = lane & 15u;
+#pragma unroll
+  for (int s = 0; s < S; ++s)
+    if ((lane >> 4) == (uint32_t)s && chunk_tile + k < chunk_end)
+      d.status[(int64_t)G.pair[s] * a.tiles + chunk_tile + k] = (uint64_t)counts;
+}
 
 // One chunk (chunk_tiles consecutive tiles of one group) of a part with S sources per walk. A lane
 // holds the four children (grid indices 4 q .. 4 q + 3) of TPW = P / 4 parent cells q, one in each
@@ -254,17 +271,14 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
       // A uniform output has variance 0 everywhere: with theta >= 0 every tile of the chunk keeps
       // nothing, and its counts (padded) or inclusive prefixes (look-back: all zero, no
       // predecessor needed) are written at once.
-      if (lane == 0) {
+      if constexpr (MODE == kModePadded) {
+        store_chunk_counts<S>(d, a, G, chunk_tile, chunk_end, 0u, lane);
+      } else if (lane == 0) {
         for (uint32_t t = chunk_tile; t < chunk_end; ++t)
 #pragma unroll
           for (int s = 0; s < S; ++s) {
-            uint64_t* w = d.status + (int64_t)G.pair[s] * a.tiles + t;
-            if constexpr (MODE == kModePadded) {
-              *w = 0ull;
-            } else {
-              status_store(w, kStatusInclusive);
-              if (t + 1 == a.tiles) d.pair_count[G.pair[s]] = 0;
-            }
+            status_store(d.status + (int64_t)G.pair[s] * a.tiles + t, kStatusInclusive);
+            if (t + 1 == a.tiles) d.pair_count[G.pair[s]] = 0;
           }
       }
       return;
@@ -273,11 +287,14 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
 
   Walker<S, P, W> R;
   JitCall<S, P, W> J;
-  TileGeo tg{0u, 0u, 0u, 0u, 0u};  // T = 0: not set yet
+  // Padded placement: the chunk's record counts, source s and tile chunk_tile + k in lane
+  // 16 s + k; they stay zero unless a walk keeps a cell, and go out with one store per chunk.
+  uint32_t chunk_counts = 0;
   for (uint32_t t0 = chunk_tile; t0 < chunk_end; t0 += TPW) {
     // ---- geometry of the walk's tiles (t0 counts from the launch's first tile, tile_lo). The
     // pair's tile 0 holds the parents of levels 1..3 (21 of them; the positions decoded one by
-    // one); every other tile 64 parents of one level, whose 256 children start at grid index p0.
+    // one); every other tile 64 parents of one level, whose 256 children start at grid index p0,
+    // with its block's corner and the level's cell size from the geometry table.
     uint32_t p0[TPW];
     uint64_t vmask[TPW];  // lanes holding a queried parent
     float px[P], py[P];
@@ -285,7 +302,7 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
     for (int k = 0; k < TPW; ++k) {
       const uint32_t tile = a.tile_lo + t0 + k;  // the pair's tile index
       const bool in_range = t0 + k < a.tiles;
-      if (tile == 0) {
+      if (k == 0 && tile == 0) {
         p0[k] = 0;
         vmask[k] = !in_range ? 0ull
                    : a.head_parents >= 64u ? ~0ull
@@ -301,15 +318,13 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
           py[4 * k + c4] = __builtin_fmaf((float)(2u * compact_even(mm >> 1) + 1u), sc, -1.0f);
         }
       } else {
-        p0[k] = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(tile - 1) * kTile);
+        // The host sizes the table for the launch's range (emr_discover_setup); the row index is
+        // still bounded, and a walk past the range end reads the last row and keeps nothing.
+        cu32* gt = d.geo + 4u * min(tile, a.geo_rows - 1u);
+        const float bx = __uint_as_float(gt[0]), by = __uint_as_float(gt[1]);
+        const float sc = __uint_as_float(gt[2]);
+        p0[k] = gt[3];
         vmask[k] = in_range ? ~0ull : 0ull;
-        if (tg.T != 0u && tile == tg.T + 1u)
-          tile_geo_next(tg);
-        else
-          tile_geo_set(tg, tile);
-        const float sc = pow2_neg((int)tg.lvl);
-        const float bx = __builtin_fmaf((float)(32u * tg.cx + 1u), sc, -1.0f);
-        const float by = __builtin_fmaf((float)(32u * tg.cy + 1u), sc, -1.0f);
 #pragma unroll
         for (int c4 = 0; c4 < 4; ++c4) {
           px[4 * k + c4] = __builtin_fmaf(geo.xl[c4 & 1], sc, bx);
@@ -368,14 +383,14 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
     const bool some = ballot(mx > a.theta16) != 0ull;
 
     if constexpr (MODE == kModePadded) {
-      uint32_t run[S][TPW];  // records per source and tile
       if (some) {
 #pragma unroll
         for (int s = 0; s < S; ++s)
 #pragma unroll
           for (int k = 0; k < TPW; ++k) {
             const uint64_t kb = ballot(s2[s][k] > a.theta16) & vmask[k];
-            run[s][k] = popc64(kb);
+            if (lane == 16u * (uint32_t)s + min(t0 + (uint32_t)k - chunk_tile, 15u))
+              chunk_counts = popc64(kb);
             if ((kb >> lane) & 1ull) {
               // a tile's records start at its first parent index within the pair
               const int64_t slot = (int64_t)G.pair[s] * a.cap + ((p0[k] >> 2) - a.parent_lo) +
@@ -385,18 +400,6 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
               for (int c4 = 0; c4 < 4; ++c4) d.w4[slot * 4 + c4] = w[s * P + 4 * k + c4];
             }
           }
-      } else {
-#pragma unroll
-        for (int s = 0; s < S; ++s)
-#pragma unroll
-          for (int k = 0; k < TPW; ++k) run[s][k] = 0;
-      }
-      if (lane == 0) {
-#pragma unroll
-        for (int s = 0; s < S; ++s)
-#pragma unroll
-          for (int k = 0; k < TPW; ++k)
-            if (t0 + k < a.tiles) d.status[(int64_t)G.pair[s] * a.tiles + t0 + k] = run[s][k];
       }
     }
     if constexpr (MODE == kModeLookback) {
@@ -429,6 +432,8 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
       }
     }
   }
+  if constexpr (MODE == kModePadded)
+    store_chunk_counts<S>(d, a, G, chunk_tile, chunk_end, chunk_counts, lane);
 }
 
 // One launch: every part, each chunk dispatched to the code of its part's (S, W). Chunks are
@@ -438,7 +443,8 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
 // (The body of the discover kernels: k_discover below runs the interpreter, the template code
 // object's kernels the compiled programs.)
 template <int MODE, bool JIT>
-__device__ __forceinline__ void discover_body(const uint32_t* __restrict__ blob,
+__device__ __forceinline__ void discover_body(const uint32_t* __restrict__ geo_tab,
+                                              const uint32_t* __restrict__ blob,
                                               const Group* __restrict__ groups,
                                               const float* __restrict__ bias_tab,
                                               uint64_t* __restrict__ status, uint32_t* __restrict__ err,
@@ -450,7 +456,7 @@ __device__ __forceinline__ void discover_body(const uint32_t* __restrict__ blob,
   const uint32_t j_lo = ((lane >> 1) & 1u) | ((lane >> 2) & 2u) | ((lane >> 3) & 4u);
   const LaneGeo geo{{(float)(4u * i_lo), (float)(4u * i_lo + 2u)},
                     {(float)(4u * j_lo), (float)(4u * j_lo + 2u)}};
-  const DiscoverPtrs d{(cu32*)blob, (cu32*)groups, (cf32*)bias_tab, status, err,
+  const DiscoverPtrs d{(cu32*)geo_tab, (cu32*)blob, (cu32*)groups, (cf32*)bias_tab, status, err,
                        parent, w4, pair_count, raw};
   const uint32_t n_waves = gridDim.x * (blockDim.x / kWave);
   const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +

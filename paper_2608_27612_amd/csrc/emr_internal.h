@@ -179,6 +179,7 @@ struct DiscoverScalars {
   int32_t depth;
   float theta16;  // 16 theta
   uint32_t code_bytes;  // compiled tier: size of the code area (0 for the interpreter)
+  uint32_t geo_rows;    // rows of the tile geometry table (tiles per pair)
   uint32_t blob_words, n_pairs;
   uint32_t bias_floats;  // the host keeps the bias table below 2^32 floats
   uint32_t head_parents;  // parents in a pair's tile 0 (levels 1..3, or all levels of a shallower grid)
@@ -196,23 +197,29 @@ constexpr int kModeRaw = 0, kModePadded = 1, kModeLookback = 2;
 //   v[kJitAcc + m]                    accumulator of instance m (the program's outputs)
 //   v[jit_window(M, W, m) + k]        slot k of instance m's value window (k < W)
 //   v[jit_x(M, W) + j], + P + j       the x and y of position j (read only)
-//   v[jit_x(M, W) + 2 P ...]          temporaries: P partial sums and S bias copies (S > 1), or
-//                                     one bias copy (S = 1)
-//   s[kJitRow .. kJitRow + 31]        bias rows of up to 8 records (4 floats each)
+//   v[jit_x(M, W) + 2 P]              one bias copy (S = 1; for S > 1 the last source's
+//                                     accumulators hold the partial sums)
+//   s[kJitRow .. kJitRow + 15]        bias rows of up to kJitRowBlock records (4 floats each)
 //   s[kJitBp, kJitBp + 1]             the group's bias rows (row 0 outputs of a program without
 //                                     records, row 1 + r the biases of the node starting at record r)
 //   s[kJitRet, kJitRet + 1]           the return address
 // A program touches nothing else: no memory writes, no exec, vcc or m0, no other registers.
 constexpr int kJitAcc = 4;
 constexpr int kJitRow = 40;
-constexpr int kJitBp = 72;
-constexpr int kJitRet = 74;
+constexpr int kJitRowBlock = 4;  // records whose bias rows are loaded together
+constexpr int kJitBp = 56;
+constexpr int kJitRet = 58;
 constexpr uint32_t kJitTailPad = 1024;  // s_endpgm bytes kept after the last program
 EMR_HD constexpr int jit_window(int M, int W, int m) { return ((kJitAcc + M + 1) & ~1) + m * W; }
 EMR_HD constexpr int jit_x(int M, int W) { return jit_window(M, W, M); }
-EMR_HD constexpr int jit_temps(int S, int P) { return S > 1 ? P + S : 1; }
+EMR_HD constexpr int jit_temps(int S) { return S > 1 ? 0 : 1; }
+
+// Tiles of one chunk at most (a chunk's record counts are held one per lane, 16 per source).
+constexpr uint32_t kChunkTilesMax = 16;
 
 struct DiscoverArgs {
+  const uint32_t* geo;     // tile geometry table of the depth (k_tile_geo), geo_rows rows
+  uint32_t geo_rows;
   const uint32_t* blob;
   const Group* groups;     // the plan's group table (parts index into it)
   const float* bias_tab;

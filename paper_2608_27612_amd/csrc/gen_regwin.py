@@ -285,14 +285,14 @@ def gen_walker(S, P, W):
 
 # The compiled tier's call convention (restated in emr_internal.h for the host code generator):
 # accumulators and value windows where the walker keeps them, the positions right after the
-# windows (x at XY .. XY + P - 1, y at XY + P ..), then the generated code's temporaries (P
-# partial sums and S bias copies for S > 1, one bias copy for S = 1); s[40:71] bias rows,
-# s[72:73] the group's bias row base, s[74:75] the return address.
-JIT_ROW, JIT_BP, JIT_RET = 40, 72, 74
+# windows (x at XY .. XY + P - 1, y at XY + P ..), then the generated code's temporary (one bias
+# copy for S = 1; none for S > 1, whose partial sums use accumulators); s[40:55] bias rows,
+# s[56:57] the group's bias row base, s[58:59] the return address.
+JIT_ROW, JIT_BP, JIT_RET = 40, 56, 58
 
 
 def jit_temps(S, P):
-    return P + S if S > 1 else 1
+    return 0 if S > 1 else 1
 
 
 def gen_jitcall(S, P, W):
@@ -320,7 +320,8 @@ def gen_jitcall(S, P, W):
     out.append("  __device__ __forceinline__ void call(uint64_t target, uint64_t bp, const float* x, "
                "const float* y) {")
     out.append("    f32x%d %s;" % (W, ", ".join("w%d" % m for m in range(M))))
-    out.append("    float t[%d];" % jit_temps(S, P))
+    if jit_temps(S, P):
+        out.append("    float t[%d];" % jit_temps(S, P))
     out.append("    asm volatile(")
     out.append(body)
     out.append("        : %s" % ",\n          ".join(outs))

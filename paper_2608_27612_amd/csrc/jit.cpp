@@ -195,8 +195,8 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
   const int M = S * P;
   auto acc = [&](int m) { return kJitAcc + m; };
   auto win = [&](int m, uint32_t k) { return jit_window(M, W, m) + (int)k; };
-  const int X = jit_x(M, W), Y = X + P, T = X + 2 * P;  // temporaries from T
-  auto row = [](uint32_t r, int s) { return kJitRow + 4 * (int)(r % 8) + s; };
+  const int X = jit_x(M, W), Y = X + P, T = X + 2 * P;  // the temporary (S = 1) at T
+  auto row = [](uint32_t r, int s) { return kJitRow + 4 * (int)(r % kJitRowBlock) + s; };
   const uint32_t n = output_varies ? n_rec : 0u;
 
   if (n == 0) {
@@ -215,12 +215,13 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
     const uint32_t* R = rec + 16 * (size_t)r;
     const uint32_t meta = R[0];
     if (meta & kRecFirst) {
-      // The bias rows of the first records of this record's block of 8 are loaded together (the
-      // rows of the records the interpreter reads them for), and waited for once.
+      // The bias rows of the first records of this record's block of kJitRowBlock are loaded
+      // together (the rows of the records the interpreter reads them for), and waited for once.
       bool wait = false;
-      if ((int64_t)(r / 8) != loaded_block) {
-        loaded_block = r / 8;
-        const uint32_t b0 = 8 * (r / 8), b1 = b0 + 8 < n ? b0 + 8 : n;
+      if ((int64_t)(r / kJitRowBlock) != loaded_block) {
+        loaded_block = r / kJitRowBlock;
+        const uint32_t b0 = kJitRowBlock * (r / kJitRowBlock);
+        const uint32_t b1 = b0 + kJitRowBlock < n ? b0 + kJitRowBlock : n;
         for (uint32_t q = b0; q < b1; ++q)
           if (rec[16 * (size_t)q] & kRecFirst) E.load_x4(row(q, 0), kJitBp, 16u * (1u + q));
         wait = true;
@@ -232,15 +233,15 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
         for (int j = 0; j < P; ++j) E.fmamk(acc(j), X + j, R[1], tb);
         for (int j = 0; j < P; ++j) E.vop2(kOpV2Fmac, "v_fmac_f32_e32", acc(j), Emitter::K(R[2]), Y + j);
       } else {
-        const int L = T, B = T + P;  // partial sums l_j, then the S bias copies
+        // the partial sums l_j live in the last source's accumulators (free at a node's start)
+        // until every source has added its bias to them
+        const int L = acc((S - 1) * P);
         for (int j = 0; j < P; ++j) E.vop2(kOpV2Mul, "v_mul_f32_e32", L + j, Emitter::K(R[1]), X + j);
         for (int j = 0; j < P; ++j) E.vop2(kOpV2Fmac, "v_fmac_f32_e32", L + j, Emitter::K(R[2]), Y + j);
         if (wait) E.wait_lgkm0();
         for (int s = 0; s < S; ++s)
-          E.vop1(kOpV1Mov, "v_mov_b32_e32", B + s, Emitter::Sg(row(r, s)), false);
-        for (int s = 0; s < S; ++s)
           for (int j = 0; j < P; ++j)
-            E.vop2(kOpV2Add, "v_add_f32_e32", acc(s * P + j), Emitter::V(B + s), L + j);
+            E.vop2(kOpV2Add, "v_add_f32_e32", acc(s * P + j), Emitter::Sg(row(r, s)), L + j);
       }
     }
     // edges, from record position n - 1 down to 0

@@ -148,12 +148,34 @@ __global__ void __launch_bounds__(kCompactWaves * kWave)
 // The interpreting discover kernel: one launch covers every part of a call.
 template <int MODE>
 __global__ void __launch_bounds__(256)
-    k_discover(const uint32_t* __restrict__ blob, const Group* __restrict__ groups,
+    k_discover(const uint32_t* __restrict__ geo, const uint32_t* __restrict__ blob,
+               const Group* __restrict__ groups,
                const float* __restrict__ bias_tab, uint64_t* __restrict__ status,
                uint32_t* __restrict__ err, uint32_t* __restrict__ parent, float* __restrict__ w4,
                int64_t* __restrict__ pair_count, float* __restrict__ raw, DiscoverScalars a) {
-  discover_body<MODE, false>(blob, groups, bias_tab, status, err, parent, w4, pair_count, raw, a,
-                             0ull);
+  discover_body<MODE, false>(geo, blob, groups, bias_tab, status, err, parent, w4, pair_count, raw,
+                             a, 0ull);
+}
+
+// The tile geometry table of a depth: row T (T >= 1, a level-aligned tile of 256 positions) holds
+// the corner term of its 16 x 16 block of cells (Eq. 1: (32 column + 1) 2^-level - 1, likewise for
+// the row), the level's cell size 2^-level, and the grid index of its first position. Row 0 (the
+// head tile, decoded lane by lane) is zero.
+__global__ void k_tile_geo(uint32_t* __restrict__ out, uint32_t rows) {
+  for (uint32_t T = blockIdx.x * blockDim.x + threadIdx.x; T < rows; T += gridDim.x * blockDim.x) {
+    uint32_t r[4] = {0u, 0u, 0u, 0u};
+    if (T > 0) {
+      TileGeo g;
+      tile_geo_set(g, T);
+      const float sc = pow2_neg((int)g.lvl);
+      r[0] = __float_as_uint(__builtin_fmaf((float)(32u * g.cx + 1u), sc, -1.0f));
+      r[1] = __float_as_uint(__builtin_fmaf((float)(32u * g.cy + 1u), sc, -1.0f));
+      r[2] = __float_as_uint(sc);
+      r[3] = (uint32_t)(level_offset(kFirstAlignedLevel) + (int64_t)(T - 1) * kTile);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) out[4 * (size_t)T + q] = r[q];
+  }
 }
 
 // ------------------------------------------------------------------------ bind kernel
@@ -333,6 +355,14 @@ extern "C" hipError_t emr_launch_grid(float* xy, int64_t n, hipStream_t s) {
   return hipGetLastError();
 }
 
+extern "C" hipError_t emr_launch_tile_geo(uint32_t* out, uint32_t rows, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  uint32_t blocks = (rows + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(emr::k_tile_geo, dim3(blocks), dim3(256), 0, s, out, rows);
+  return hipGetLastError();
+}
+
 extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
   if (a->n_members == 0) return hipSuccess;
   hipLaunchKernelGGL(emr::k_bind, dim3((a->n_members + emr::kBindWaves - 1) / emr::kBindWaves),
@@ -350,6 +380,7 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   if (per_cu <= 0) per_cu = 1;
   if (cus <= 0) cus = 1;
   if (a->n_parts == 0 || a->n_parts > (uint32_t)emr::kMaxParts) return hipErrorInvalidValue;
+  if (!a->geo || (uint64_t)a->tile_lo + a->tiles > a->geo_rows) return hipErrorInvalidValue;
   uint64_t groups = 0;
   for (uint32_t k = 0; k < a->n_parts; ++k) {
     const int S = (int)a->part_S[k], W = (int)a->part_W[k];
@@ -357,9 +388,13 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
       return hipErrorInvalidValue;
     groups += a->part_groups[k];
   }
-  // Chunks of 4 tiles when the launch has work for at least 4 such chunks per SIMD; else each
-  // chunk is one walk's worth of tiles, for parallelism.
-  const bool big = groups * a->tiles >= 16ull * 4ull * (uint64_t)cus;
+  // Chunk size: the largest of 16, 8 and 4 tiles that still gives every resident wave at least
+  // four chunks (fewer, longer chunks spend less per-chunk work; enough of them keep the waves
+  // balanced); else each chunk is one walk's worth of tiles, for parallelism.
+  const uint64_t waves = 4ull * (uint64_t)per_cu * (uint64_t)cus;
+  uint32_t target = 0;
+  for (uint32_t c : {emr::kChunkTilesMax, 8u, 4u})
+    if (target == 0 && groups * ((a->tiles + c - 1) / c) >= 4ull * waves) target = c;
   emr::DiscoverScalars sc{};
   sc.cap = a->cap;
   sc.n_pos = a->n_pos;
@@ -371,7 +406,7 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   for (uint32_t k = 0; k < a->n_parts; ++k) {
     const int S = (int)a->part_S[k], W = (int)a->part_W[k];
     const uint32_t tpw = (uint32_t)emr::positions_per_lane(S, W) / emr::kTileIters;
-    const uint32_t chunk = big ? 4u : tpw;
+    const uint32_t chunk = target > tpw ? target : tpw;  // at most kChunkTilesMax (tpw <= 4)
     const uint32_t cpg = (a->tiles + chunk - 1) / chunk;
     sc.part[k] = emr::DiscoverPart{(uint32_t)S, (uint32_t)W, a->part_group0[k],
                                    a->part_groups[k] * cpg, cpg, chunk};
@@ -382,6 +417,7 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   sc.depth = a->depth;
   sc.theta16 = 16.0f * a->theta;
   sc.code_bytes = 0;
+  sc.geo_rows = a->geo_rows;
   sc.blob_words = a->blob_words;
   sc.n_pairs = a->n_pairs;
   sc.bias_floats = (uint32_t)a->bias_floats;
@@ -425,6 +461,7 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
     if (stop && (e = hipEventRecord(stop, s)) != hipSuccess) return e;
     return hipSuccess;
   }
+  const uint32_t* geo = a->geo;
   const uint32_t* blob = a->blob;
   const emr::Group* grp = a->groups;
   const float* bias_tab = a->bias_tab;
@@ -436,10 +473,11 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
   float* raw = a->raw;
   if (start && (e = hipEventRecord(start, s)) != hipSuccess) return e;
   if constexpr (MODE == emr::kModeLookback) {
-    void* args[] = {&blob, &grp, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw, &sc};
+    void* args[] = {&geo, &blob, &grp, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw,
+                    &sc};
     e = hipLaunchCooperativeKernel((const void*)kern, dim3(grid), dim3(256), args, 0, s);
   } else {
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, blob, grp, bias_tab, status, err,
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, geo, blob, grp, bias_tab, status, err,
                        parent, w4, pair_count, raw, sc);
     e = hipGetLastError();
   }

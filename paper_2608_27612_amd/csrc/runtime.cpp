@@ -33,6 +33,7 @@ extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* paren
 extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
                                         const float* w4, int64_t cap, uint32_t n_pairs,
                                         uint32_t* out_parent, float* out_w4, hipStream_t s);
+extern "C" hipError_t emr_launch_tile_geo(uint32_t* out, uint32_t rows, hipStream_t s);
 extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t blocks, int per_cu,
                                          int cus, emr::DiscoverScalars* out, uint32_t* grid);
 // The compiled tier's template code object (jit_image.cpp).
@@ -505,6 +506,39 @@ emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspac
   return EMR_OK;
 }
 
+// The tile geometry table of a depth on the current device (k_tile_geo), built on first use and
+// kept for the life of the process (tiles_per_pair(depth) rows of 16 bytes: 5.6 MB at depth 13).
+emr_status tile_geo_table(int depth, const uint32_t** out, uint32_t* rows) {
+  static std::mutex mu;
+  static std::vector<std::pair<std::pair<int, int>, uint32_t*>> cache;  // (device, depth)
+  int dev = 0;
+  HIP_OR_FAIL(hipGetDevice(&dev));
+  const int64_t n = emr::tiles_per_pair(depth);
+  if (n > 0xFFFFFFFFll / 4) return fail(EMR_E_LIMIT, "depth %d has too many tiles", depth);
+  *rows = (uint32_t)n;
+  std::lock_guard<std::mutex> lock(mu);
+  for (const auto& e : cache)
+    if (e.first == std::make_pair(dev, depth)) {
+      *out = e.second;
+      return EMR_OK;
+    }
+  uint32_t* d = nullptr;
+  if (hipMalloc((void**)&d, (size_t)n * 16) != hipSuccess)
+    return fail(EMR_E_NOMEM, "tile geometry table of %lld rows", (long long)n);
+  StreamPool* sp = nullptr;
+  emr_status st = stream_pool(&sp);
+  if (st == EMR_OK && (emr_launch_tile_geo(d, (uint32_t)n, sp->aux[0]) != hipSuccess ||
+                       hipStreamSynchronize(sp->aux[0]) != hipSuccess))
+    st = fail(EMR_E_DEVICE, "building the tile geometry table failed");
+  if (st != EMR_OK) {
+    (void)hipFree(d);
+    return st;
+  }
+  cache.push_back({{dev, depth}, d});
+  *out = d;
+  return EMR_OK;
+}
+
 // ------------------------------------------------------------------ compiled tier
 std::atomic<int> g_jit_policy{EMR_JIT_AUTO};
 
@@ -681,6 +715,7 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
   sc.code_bytes = M.code_bytes;
   if (start) HIP_OR_FAIL(hipEventRecord(start, s));
   if (grid > 0) {
+    const uint32_t* geo = a.geo;
     const uint32_t* blob = a.blob;
     const emr::Group* grp = a.groups;
     const float* bias_tab = a.bias_tab;
@@ -690,7 +725,8 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
     float* w4 = a.w4;
     int64_t* pair_count = a.pair_count;
     float* raw = a.raw;
-    void* args[] = {&blob, &grp, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw, &sc};
+    void* args[] = {&geo, &blob, &grp, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw,
+                    &sc};
     if (mode == 2)  // look-back placement relies on every wave being resident
       HIP_OR_FAIL(hipModuleLaunchCooperativeKernel(M.fn[mode], grid, 1, 1, 256, 1, 1, 0, s, args));
     else
@@ -709,6 +745,9 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
   char* tables = nullptr;
   emr_status tst = plan_tables(P, &tables);
   if (tst != EMR_OK) return tst;
+  const uint32_t* geo_tab = nullptr;
+  uint32_t geo_rows = 0;
+  if ((tst = tile_geo_table(P.depth, &geo_tab, &geo_rows)) != EMR_OK) return tst;
   const int cus = device_cu_count();
   const int64_t parent_lo = emr::tile_parent_offset(tile_lo, P.depth);
   const int64_t range_parents = emr::tile_parent_offset(tile_lo + n_tiles, P.depth) - parent_lo;
@@ -735,6 +774,8 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
   for (size_t li = 0; li < P.launches.size(); ++li) {
     const Plan::Launch& L = P.launches[li];
     emr::DiscoverArgs a{};
+    a.geo = geo_tab;
+    a.geo_rows = geo_rows;
     a.blob = pop->d_blob;
     a.groups = jit ? P.jit->d_groups : (const emr::Group*)(tables + P.t_groups);
     a.bias_tab = (const float*)(ws + P.off_bias);

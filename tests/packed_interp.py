@@ -174,7 +174,7 @@ def emulate(listing, rows, x, y, M, W):
         a = [t.strip() for t in rest.split(",")] if rest else []
         if op == "s_load_dwordx4":
             base = int(a[0][2:].split(":")[0])
-            assert a[1] == "s[72:73]"
+            assert a[1] == "s[56:57]"
             off = int(a[2], 16) // 4
             for k in range(4):
                 S_[base + k] = float(rows[off + k])
@@ -182,7 +182,7 @@ def emulate(listing, rows, x, y, M, W):
         if op in ("s_waitcnt", "s_nop"):
             continue
         if op == "s_setpc_b64":
-            assert a[0] == "s[74:75]"
+            assert a[0] == "s[58:59]"
             break
         d = int(a[0][1:])
         if op == "v_mov_b32_e32":

@@ -100,7 +100,7 @@ def test_records_bit_identical_tabular(emr):
 def test_records_bit_identical_lookback_placement(emr):
     # a capacity below the worst case places records through the look-back scan
     genomes = W.population(5, 60, 20, 60)
-    records_both(emr, genomes, W.xor_sources(), 6, 0.03, cap=600)
+    records_both(emr, genomes, W.xor_sources(), 6, 0.03, cap=1300)
 
 
 def test_records_bit_identical_per_genome_sources(emr):

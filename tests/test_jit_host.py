@@ -97,7 +97,7 @@ def test_uniform_output_program_copies_row_zero():
     st, blob, desc, info, msg = PI.pack(g)
     assert st == 0 and not (int(desc[0][4]) & 1)
     words, listing = PI.compile_program(blob, desc[0], 3, 8, 4)
-    assert listing.splitlines()[0] == "s_load_dwordx4 s[40:43], s[72:73], 0x0"
+    assert listing.splitlines()[0] == "s_load_dwordx4 s[40:43], s[56:57], 0x0"
     rows = np.zeros(8)
     rows[:3] = [0.25, -1.5, 3.0]
     V = PI.emulate(listing, rows, np.zeros(8), np.zeros(8), 24, 4)
@@ -116,25 +116,25 @@ def test_transcendental_results_are_never_read_by_the_next_instruction():
                 dst = a.split()[1].rstrip(",")
                 assert not re.search(r"(?<![\w])-?%s\b" % dst, b.partition(" ")[2]), (a, b)
         # the caller reads the accumulators right after the return
-        assert lines[-1] == "s_setpc_b64 s[74:75]"
+        assert lines[-1] == "s_setpc_b64 s[58:59]"
         if any(l.startswith(TRANS) for l in lines):
             assert lines[-2] == "s_nop 1"
 
 
 def test_register_use_stays_inside_the_convention():
     """Only the accumulators, windows, positions and temporaries of the variant, and SGPRs
-    s[40:75]."""
+    s[40:59]."""
     for gi, blob, desc, d, S, P, Wn in programs(POPS[1]):
         M = S * P
         X = ((4 + M + 1) & ~1) + M * Wn
-        top = X + 2 * P + (P + S if S > 1 else 1)
+        top = X + 2 * P + (0 if S > 1 else 1)
         _, listing = PI.compile_program(blob, desc[d], S, P, Wn)
         for v in re.findall(r"\bv(\d+)\b", listing):
             assert 4 <= int(v) < top
         for s in re.findall(r"\bs(\d+)\b", listing):
-            assert 40 <= int(s) <= 75
+            assert 40 <= int(s) <= 59
         for a, b in re.findall(r"s\[(\d+):(\d+)\]", listing):
-            assert 40 <= int(a) and int(b) <= 75
+            assert 40 <= int(a) and int(b) <= 59
 
 
 def test_bad_variants_are_refused():
