@@ -16,7 +16,12 @@ Printed as one JSON line:
   valu_frac_step  the same algorithmic slots for the whole step over ms_per_step, against the
                same peak (every kernel, launch gap and host interaction of a step included)
   ms_per_gen   pack (host + upload) + discover + check, host clock: the per-generation cost of
-               discovery in an evolution loop
+               discovery in an evolution loop (a new population each generation, discovered once:
+               the default policy runs it through the interpreter); ms_per_gen_compiled the same
+               with the population's programs compiled first (compile + module load included)
+  compiled_tier  the timed steps' compiled programs (the default policy compiles a population's
+               programs on its second call, so the warm-up compiles them): count, machine-code
+               bytes, host compile and module-load times
   cpu_baseline the CPU oracle on a bounded, stated sample of the same workload
 """
 
@@ -147,29 +152,41 @@ def main():
     t1 = time.perf_counter()
     # the discover launch of each timed step, bracketed by its own event pair
     launch_slots = None
+    compiled = set()
     for rec in emr.emr_profile_read():
         assert rec["first"] and launch_slots in (None, rec["slots"])
         launch_slots = rec["slots"]
         launch_ms.append(rec["ms"])
+        compiled.add(rec["compiled"])
+    assert len(compiled) == 1, "the timed steps ran both tiers"
+    jit = emr.emr_jit_info(pop)
     assert len(launch_ms) == (args.steps + TIME_EVERY - 1) // TIME_EVERY
     emr.emr_profile_enable(False)
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = queries / (ms_per_step * 1e-3)
     records = int(res["pair_count"].clamp(max=res["pair_capacity"]).sum().item())
 
-    kernel_name = "k_discover<1>"  # the padded-record mode of the discover kernel
+    # the padded-record mode of the discover kernel, compiled programs or the interpreter
+    kernel_name = "emr_discover_jit_padded" if compiled == {True} else "k_discover<1>"
     avg_ms = float(np.mean(launch_ms))
     achieved = launch_slots / (avg_ms * 1e-3)
 
-    # ms per generation: pack + discover + check on the host clock
-    torch.cuda.synchronize()
-    g0 = time.perf_counter()
-    for _ in range(args.gens):
-        p = emr.emr_pack_population(genomes)
-        emr.emr_discover(p, sources, depth, theta32, res=res)
-        emr.emr_result_check(res)
-        del p
-    ms_per_gen = (time.perf_counter() - g0) * 1e3 / args.gens
+    # ms per generation: pack + discover + check on the host clock, for a new population each
+    # generation (one call per population: the default policy interprets it), and with the
+    # population's programs compiled first (pack + compile + load + discover + check)
+    def per_gen(policy):
+        emr.emr_set_jit(policy)
+        torch.cuda.synchronize()
+        g0 = time.perf_counter()
+        for _ in range(args.gens):
+            p = emr.emr_pack_population(genomes)
+            emr.emr_discover(p, sources, depth, theta32, res=res)
+            emr.emr_result_check(res)
+            del p
+        emr.emr_set_jit(emr.EMR_JIT_AUTO)
+        return (time.perf_counter() - g0) * 1e3 / args.gens
+    ms_per_gen = per_gen(emr.EMR_JIT_AUTO)
+    ms_per_gen_compiled = per_gen(emr.EMR_JIT_ALWAYS)
 
     line = {
         "metric": METRIC,
@@ -188,6 +205,9 @@ def main():
                    "depth": depth, "theta": theta, "queries_per_step": int(queries),
                    "records_per_step": records},
         "ms_per_gen": ms_per_gen,
+        "ms_per_gen_compiled": ms_per_gen_compiled,
+        "compiled_tier": {"programs": jit["programs"], "code_bytes": jit["code_bytes"],
+                          "compile_ms": jit["compile_ms"], "load_ms": jit["load_ms"]},
         "host_enqueue_ms": host_s * 1e3 / args.steps,
         "valu_frac_step": (slots / (ms_per_step * 1e-3)) / VALU_PEAK_SLOTS,
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_SLOTS / 1e12,

@@ -18,6 +18,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x32 __attribute__((ext_vector_type(32)));
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
 
 // ------------------------------------------------------------------------ position decode
 __device__ __forceinline__ uint32_t compact_even(uint32_t x) {  // bits 0,2,4,.. -> 0,1,2,..
@@ -287,10 +288,35 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
 
   Walker<S, P, W> R;
   JitCall<S, P, W> J;
+  // Compiled programs find the group's bias rows 1 .. 4 in their scalar registers: loaded once
+  // per chunk (the workspace keeps 16 floats of padding after the bias table, so the load stays
+  // inside it for the last group).
+  u32x16 rows;
+  if constexpr (JIT)
+    rows = *reinterpret_cast<const __attribute__((address_space(4))) u32x16*>(
+        d.bias + G.bias_off + 4u);
   // Padded placement: the chunk's record counts, source s and tile chunk_tile + k in lane
   // 16 s + k; they stay zero unless a walk keeps a cell, and go out with one store per chunk.
   uint32_t chunk_counts = 0;
+  // The geometry rows of the walk's tiles, loaded one walk ahead. The host sizes the table for
+  // the launch's range (emr_discover_setup); the row index is still bounded, and a walk past the
+  // range end reads the last row and keeps nothing.
+  uint32_t gnext[TPW][4];
+  auto load_geo = [&](uint32_t t) {
+#pragma unroll
+    for (int k = 0; k < TPW; ++k) {
+      cu32* gt = d.geo + 4u * min(a.tile_lo + t + (uint32_t)k, a.geo_rows - 1u);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) gnext[k][q] = gt[q];
+    }
+  };
+  load_geo(chunk_tile);
   for (uint32_t t0 = chunk_tile; t0 < chunk_end; t0 += TPW) {
+    uint32_t gcur[TPW][4];
+#pragma unroll
+    for (int k = 0; k < TPW; ++k)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) gcur[k][q] = gnext[k][q];
     // ---- geometry of the walk's tiles (t0 counts from the launch's first tile, tile_lo). The
     // pair's tile 0 holds the parents of levels 1..3 (21 of them; the positions decoded one by
     // one); every other tile 64 parents of one level, whose 256 children start at grid index p0,
@@ -318,12 +344,9 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
           py[4 * k + c4] = __builtin_fmaf((float)(2u * compact_even(mm >> 1) + 1u), sc, -1.0f);
         }
       } else {
-        // The host sizes the table for the launch's range (emr_discover_setup); the row index is
-        // still bounded, and a walk past the range end reads the last row and keeps nothing.
-        cu32* gt = d.geo + 4u * min(tile, a.geo_rows - 1u);
-        const float bx = __uint_as_float(gt[0]), by = __uint_as_float(gt[1]);
-        const float sc = __uint_as_float(gt[2]);
-        p0[k] = gt[3];
+        const float bx = __uint_as_float(gcur[k][0]), by = __uint_as_float(gcur[k][1]);
+        const float sc = __uint_as_float(gcur[k][2]);
+        p0[k] = gcur[k][3];
         vmask[k] = in_range ? ~0ull : 0ull;
 #pragma unroll
         for (int c4 = 0; c4 < 4; ++c4) {
@@ -338,9 +361,10 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
     // record and row are loaded while the current one is computed. A uniform output is the
     // constant of row 0 (its program has no records).
     // The output node's activation was applied by its record's tail (or the compiled program).
+    load_geo(t0 + TPW);  // the next walk's rows, while this one runs
     const float* w;
     if constexpr (JIT) {
-      J.call(code_base + G.code_off, (uint64_t)(d.bias + G.bias_off), px, py);
+      J.call(code_base + G.code_off, (uint64_t)(d.bias + G.bias_off), px, py, rows);
       w = J.acc;
     } else {
       R.def();

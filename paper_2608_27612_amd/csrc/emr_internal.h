@@ -197,9 +197,12 @@ constexpr int kModeRaw = 0, kModePadded = 1, kModeLookback = 2;
 //   v[kJitAcc + m]                    accumulator of instance m (the program's outputs)
 //   v[jit_window(M, W, m) + k]        slot k of instance m's value window (k < W)
 //   v[jit_x(M, W) + j], + P + j       the x and y of position j (read only)
-//   v[jit_x(M, W) + 2 P]              one bias copy (S = 1; for S > 1 the last source's
+//   v[jit_x(M, W) + 2 P ...]          jit_temps(S, P, W) bias copies (for S > 1 the last source's
 //                                     accumulators hold the partial sums)
-//   s[kJitRow .. kJitRow + 15]        bias rows of up to kJitRowBlock records (4 floats each)
+//   s[kJitRow .. kJitRow + 15]        bias rows 1 .. kJitRowBlock of the group (the rows of records
+//                                     0 .. 3), loaded by the caller once per chunk (in and out:
+//                                     a program that needs later rows loads them here, and then
+//                                     loads its first rows itself too)
 //   s[kJitBp, kJitBp + 1]             the group's bias rows (row 0 outputs of a program without
 //                                     records, row 1 + r the biases of the node starting at record r)
 //   s[kJitRet, kJitRet + 1]           the return address
@@ -212,7 +215,12 @@ constexpr int kJitRet = 58;
 constexpr uint32_t kJitTailPad = 1024;  // s_endpgm bytes kept after the last program
 EMR_HD constexpr int jit_window(int M, int W, int m) { return ((kJitAcc + M + 1) & ~1) + m * W; }
 EMR_HD constexpr int jit_x(int M, int W) { return jit_window(M, W, M); }
-EMR_HD constexpr int jit_temps(int S) { return S > 1 ? 0 : 1; }
+// Bias copies of a variant: one per source, where they fit below kJitTop (the highest register
+// any variant needs); a variant without them adds the biases from their SGPRs.
+constexpr int kJitTop = 148;
+EMR_HD constexpr int jit_temps(int S, int P, int W) {
+  return S == 1 ? 1 : (jit_x(S * P, W) + 2 * P + S <= kJitTop ? S : 0);
+}
 
 // Tiles of one chunk at most (a chunk's record counts are held one per lane, 16 per source).
 constexpr uint32_t kChunkTilesMax = 16;

@@ -285,14 +285,17 @@ def gen_walker(S, P, W):
 
 # The compiled tier's call convention (restated in emr_internal.h for the host code generator):
 # accumulators and value windows where the walker keeps them, the positions right after the
-# windows (x at XY .. XY + P - 1, y at XY + P ..), then the generated code's temporary (one bias
-# copy for S = 1; none for S > 1, whose partial sums use accumulators); s[40:55] bias rows,
-# s[56:57] the group's bias row base, s[58:59] the return address.
+# windows (x at XY .. XY + P - 1, y at XY + P ..), then the generated code's bias copies (one per
+# source where they fit below JIT_TOP; for S > 1 the partial sums use accumulators); s[40:55] the
+# group's first bias rows (loaded by the caller per chunk, in and out), s[56:57] the group's bias
+# row base, s[58:59] the return address.
 JIT_ROW, JIT_BP, JIT_RET = 40, 56, 58
+JIT_TOP = 148
 
 
-def jit_temps(S, P):
-    return 0 if S > 1 else 1
+def jit_temps(S, P, W):
+    M = S * P
+    return 1 if S == 1 else (S if base(M, M, W) + 2 * P + S <= JIT_TOP else 0)
 
 
 def gen_jitcall(S, P, W):
@@ -307,21 +310,22 @@ def gen_jitcall(S, P, W):
          ".Lret_%=:"]
     outs = ['"={v%d}"(acc[%d])' % (ACC + m, m) for m in range(M)]
     outs += ['"=&{v[%d:%d]}"(w%d)' % (base(M, m, W), base(M, m, W) + W - 1, m) for m in range(M)]
-    outs += ['"=&{v%d}"(t[%d])' % (tmp0 + k, k) for k in range(jit_temps(S, P))]
+    outs += ['"=&{v%d}"(t[%d])' % (tmp0 + k, k) for k in range(jit_temps(S, P, W))]
+    outs += ['"+{s[%d:%d]}"(rows)' % (JIT_ROW, JIT_ROW + 15)]
     ins = ['[tgt] "s"(target)', '"{s[%d:%d]}"(bp)' % (JIT_BP, JIT_BP + 1)]
     ins += ['"{v%d}"(x[%d]), "{v%d}"(y[%d])' % (xy + j, j, xy + P + j, j) for j in range(P)]
-    clob = ['"scc"'] + ['"s%d"' % r for r in range(JIT_ROW, JIT_BP)] + \
-        ['"s%d"' % JIT_RET, '"s%d"' % (JIT_RET + 1)]
+    clob = ['"scc"', '"s%d"' % JIT_RET, '"s%d"' % (JIT_RET + 1)]
     body = "\n".join('        "%s\\n"' % l for l in L)
     out = []
     out.append("template <> struct JitCall<%d, %d, %d> {" % (S, P, W))
     out.append("  float acc[%d];" % M)
-    out.append("  // Runs the compiled program at `target` for the P positions (x, y); bp: the group's bias rows.")
+    out.append("  // Runs the compiled program at `target` for the P positions (x, y); bp: the group's bias rows,")
+    out.append("  // rows: its rows 1 .. 4 (in and out, see the register convention).")
     out.append("  __device__ __forceinline__ void call(uint64_t target, uint64_t bp, const float* x, "
-               "const float* y) {")
+               "const float* y, u32x16& rows) {")
     out.append("    f32x%d %s;" % (W, ", ".join("w%d" % m for m in range(M))))
-    if jit_temps(S, P):
-        out.append("    float t[%d];" % jit_temps(S, P))
+    if jit_temps(S, P, W):
+        out.append("    float t[%d];" % jit_temps(S, P, W))
     out.append("    asm volatile(")
     out.append(body)
     out.append("        : %s" % ",\n          ".join(outs))

@@ -195,7 +195,7 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
   const int M = S * P;
   auto acc = [&](int m) { return kJitAcc + m; };
   auto win = [&](int m, uint32_t k) { return jit_window(M, W, m) + (int)k; };
-  const int X = jit_x(M, W), Y = X + P, T = X + 2 * P;  // the temporary (S = 1) at T
+  const int X = jit_x(M, W), Y = X + P, T = X + 2 * P;  // bias copies from T
   auto row = [](uint32_t r, int s) { return kJitRow + 4 * (int)(r % kJitRowBlock) + s; };
   const uint32_t n = output_varies ? n_rec : 0u;
 
@@ -210,7 +210,13 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
   }
 
   const uint32_t wmask = (uint32_t)W - 1u;
-  int64_t loaded_block = -1;
+  // The caller has loaded the rows of records 0 .. kJitRowBlock - 1 (block 0). A program with a
+  // node starting later loads those blocks over them, so it loads block 0 itself too: the next
+  // walk finds the registers as this one left them.
+  bool long_program = false;
+  for (uint32_t r = kJitRowBlock; r < n; ++r) long_program |= (rec[16 * (size_t)r] & kRecFirst) != 0;
+  int64_t loaded_block = long_program ? -1 : 0;
+  const int copies = jit_temps(S, P, W);
   for (uint32_t r = 0; r < n; ++r) {
     const uint32_t* R = rec + 16 * (size_t)r;
     const uint32_t meta = R[0];
@@ -239,9 +245,17 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
         for (int j = 0; j < P; ++j) E.vop2(kOpV2Mul, "v_mul_f32_e32", L + j, Emitter::K(R[1]), X + j);
         for (int j = 0; j < P; ++j) E.vop2(kOpV2Fmac, "v_fmac_f32_e32", L + j, Emitter::K(R[2]), Y + j);
         if (wait) E.wait_lgkm0();
-        for (int s = 0; s < S; ++s)
-          for (int j = 0; j < P; ++j)
-            E.vop2(kOpV2Add, "v_add_f32_e32", acc(s * P + j), Emitter::Sg(row(r, s)), L + j);
+        if (copies == S) {  // bias copies in VGPRs: the adds read vector operands only
+          for (int s = 0; s < S; ++s)
+            E.vop1(kOpV1Mov, "v_mov_b32_e32", T + s, Emitter::Sg(row(r, s)), false);
+          for (int s = 0; s < S; ++s)
+            for (int j = 0; j < P; ++j)
+              E.vop2(kOpV2Add, "v_add_f32_e32", acc(s * P + j), Emitter::V(T + s), L + j);
+        } else {
+          for (int s = 0; s < S; ++s)
+            for (int j = 0; j < P; ++j)
+              E.vop2(kOpV2Add, "v_add_f32_e32", acc(s * P + j), Emitter::Sg(row(r, s)), L + j);
+        }
       }
     }
     // edges, from record position n - 1 down to 0

@@ -376,7 +376,8 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
   P.off_status = 256;
   P.status_bytes = (size_t)P.n_pairs * P.tiles * 8;
   P.off_bias = align256(P.off_status + P.status_bytes);
-  P.total = align256(P.off_bias + P.bias_floats * sizeof(float));
+  // 16 floats of padding after the bias table: the compiled tier loads a group's rows 1 .. 4 at once
+  P.total = align256(P.off_bias + (P.bias_floats + 16) * sizeof(float));
   // tables
   P.t_groups = 0;
   P.t_members = align256(P.groups.size() * sizeof(emr::Group));

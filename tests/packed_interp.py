@@ -159,16 +159,20 @@ def _operand(tok, V, S_):
     return f32(i & 0xFFFFFFFF)
 
 
-def emulate(listing, rows, x, y, M, W):
+def emulate(listing, rows, x, y, M, W, stale_rows=False):
     """Executes a compiled program's listing on the host in float64 with exact transcendentals:
     `rows` are the group's bias rows (bias_rows), x and y the P positions. Returns the VGPR file
     (a dict). Reading a register that nothing wrote raises KeyError, as an interpreter that reads
-    an undefined slot would."""
+    an undefined slot would. With `stale_rows`, s[40:55] start out holding garbage instead of the
+    preloaded rows (what a program finds after a longer program of the same chunk ran)."""
     P = len(x)
     X = ((4 + M + 1) & ~1) + M * W
     V = {X + j: float(x[j]) for j in range(P)}
     V.update({X + P + j: float(y[j]) for j in range(P)})
-    S_ = {}
+    # on entry s[40:55] hold the group's bias rows 1 .. 4 (loaded by the caller once per chunk)
+    S_ = {40 + k: (float(rows[4 + k]) if 4 + k < len(rows) else 0.0) for k in range(16)}
+    if stale_rows:
+        S_ = {40 + k: float("nan") for k in range(16)}
     for line in listing.strip().split("\n"):
         op, _, rest = line.partition(" ")
         a = [t.strip() for t in rest.split(",")] if rest else []

@@ -203,7 +203,7 @@ def test_template_kernels_allocate_the_convention_registers(jit_asm):
     import sys
     sys.path.insert(0, os.path.join(ROOT, "paper_2608_27612_amd", "csrc"))
     import gen_regwin as G
-    top = max(G.base(S * P, S * P, W) + 2 * P + G.jit_temps(S, P) for S, P, W in G.VARIANTS)
+    top = max(G.base(S * P, S * P, W) + 2 * P + G.jit_temps(S, P, W) for S, P, W in G.VARIANTS)
     counts = re.findall(r"\.name:\s+(emr_discover_jit_\w+)\s*\n(?:.*\n)*?\s+\.vgpr_count:\s+(\d+)",
                         jit_asm)
     assert len(counts) == 3

@@ -90,6 +90,35 @@ def test_compiled_programs_compute_the_packed_programs():
     assert n > 10
 
 
+def test_programs_load_only_rows_the_caller_did_not_preload():
+    """A program whose nodes all start in records 0 .. 3 uses the preloaded rows and loads
+    nothing; a longer one loads every row it uses (so it runs right whatever s[40:55] hold)."""
+    rng = np.random.default_rng(9)
+    seen_long = seen_short = 0
+    for gi, blob, desc, d, S, P, Wn in programs(POPS[1] + POPS[0][:6]):
+        n_rec = int(desc[d][1])
+        if not (int(desc[d][4]) & 1) or n_rec == 0:
+            continue
+        var_off = int(desc[d][0])
+        firsts = [r for r in range(n_rec) if blob[var_off + 16 * r] & 16]
+        _, listing = PI.compile_program(blob, desc[d], S, P, Wn)
+        loads = [l for l in listing.splitlines() if l.startswith("s_load")]
+        if max(firsts) < 4:
+            assert not loads
+            seen_short += 1
+            continue
+        seen_long += 1
+        srcs = [(float(rng.uniform(-1, 1)), float(rng.uniform(-1, 1))) for _ in range(S)]
+        x, y = rng.uniform(-1, 1, P), rng.uniform(-1, 1, P)
+        V = PI.emulate(listing, PI.bias_rows(blob, desc, d, srcs), x, y, S * P, Wn,
+                       stale_rows=True)
+        for s, (sx, sy) in enumerate(srcs):
+            want, _ = PI.interpret(blob, desc, d, sx, sy, x, y)
+            got = np.array([V[4 + s * P + j] for j in range(P)])
+            assert np.allclose(got, want, rtol=1e-9, atol=1e-9)
+    assert seen_long > 0 and seen_short > 0
+
+
 def test_uniform_output_program_copies_row_zero():
     g = W.single_cppn(0, 3, 6)[0]
     # no enabled edge leaves x2 or y2: for outgoing queries the output is a per-source constant
@@ -127,7 +156,7 @@ def test_register_use_stays_inside_the_convention():
     for gi, blob, desc, d, S, P, Wn in programs(POPS[1]):
         M = S * P
         X = ((4 + M + 1) & ~1) + M * Wn
-        top = X + 2 * P + (0 if S > 1 else 1)
+        top = X + 2 * P + G.jit_temps(S, P, Wn)
         _, listing = PI.compile_program(blob, desc[d], S, P, Wn)
         for v in re.findall(r"\bv(\d+)\b", listing):
             assert 4 <= int(v) < top
