@@ -18,6 +18,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x32 __attribute__((ext_vector_type(32)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
 
 // ------------------------------------------------------------------------ position decode
@@ -361,12 +362,26 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
     // record and row are loaded while the current one is computed. A uniform output is the
     // constant of row 0 (its program has no records).
     // The output node's activation was applied by its record's tail (or the compiled program).
-    load_geo(t0 + TPW);  // the next walk's rows, while this one runs
+    // The next walk's geometry rows are loaded while this walk runs: by the call statement before
+    // it jumps to the program (the compiler waits for every pending scalar load before an asm
+    // statement, so a load issued ahead of it in C++ would be waited for at once), or before the
+    // interpreter's walk.
     const float* w;
     if constexpr (JIT) {
-      J.call(code_base + G.code_off, (uint64_t)(d.bias + G.bias_off), px, py, rows);
+      uint64_t next_rows[TPW];
+#pragma unroll
+      for (int k = 0; k < TPW; ++k)
+        next_rows[k] = (uint64_t)(d.geo + 4u * min(a.tile_lo + t0 + (uint32_t)(TPW + k),
+                                                   a.geo_rows - 1u));
+      u32x4 g[TPW];
+      J.call(code_base + G.code_off, (uint64_t)(d.bias + G.bias_off), px, py, rows, next_rows, g);
+#pragma unroll
+      for (int k = 0; k < TPW; ++k)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) gnext[k][q] = g[k][q];
       w = J.acc;
     } else {
+      load_geo(t0 + TPW);
       R.def();
       R.walk((uint64_t)(d.blob + G.var_off), (uint64_t)(d.bias + G.bias_off), n_rec, px, py);
       w = R.acc;
