@@ -77,22 +77,27 @@ class Emitter {
  public:
   Emitter(bool listing, Code* out) : want_(listing), out_(out) {}
 
-  // src0 operands: a VGPR, an SGPR, or a 32-bit constant
+  // src0 operands: a VGPR, an SGPR, or a 32-bit constant (their text is made for listings only)
   struct Src {
     uint32_t code;  // 9-bit operand code
-    uint32_t lit;   // literal dword when code == kSrcLiteral
+    uint32_t lit;   // the constant's bits (for a literal: the literal dword)
     int vgpr;       // the VGPR read, or -1
-    std::string text;
+    int sgpr;       // the SGPR read, or -1
   };
-  static Src V(int v) { return {256u + (uint32_t)v, 0, v, "v" + std::to_string(v)}; }
-  static Src Sg(int s) { return {(uint32_t)s, 0, -1, "s" + std::to_string(s)}; }
-  static Src K(uint32_t bits) { return {inline_code(bits), bits, -1, const_text(bits)}; }
+  static Src V(int v) { return {256u + (uint32_t)v, 0, v, -1}; }
+  static Src Sg(int s) { return {(uint32_t)s, 0, -1, s}; }
+  static Src K(uint32_t bits) { return {inline_code(bits), bits, -1, -1}; }
+  static std::string str(const Src& s) {
+    if (s.vgpr >= 0) return "v" + std::to_string(s.vgpr);
+    if (s.sgpr >= 0) return "s" + std::to_string(s.sgpr);
+    return const_text(s.lit);
+  }
 
   void vop2(uint32_t op, const char* name, int vdst, const Src& s0, int vsrc1, bool trans = false) {
     hazard(s0.vgpr, vsrc1, -1);
     put((op << 25) | ((uint32_t)vdst << 17) | ((uint32_t)vsrc1 << 9) | s0.code);
     if (s0.code == kSrcLiteral) put(s0.lit);
-    text("%s v%d, %s, v%d", name, vdst, s0.text.c_str(), vsrc1);
+    if (want_) text("%s v%d, %s, v%d", name, vdst, str(s0).c_str(), vsrc1);
     wrote(vdst, trans);
   }
   // v_fmamk_f32 vdst, src0, K, vsrc1: vdst = src0 * K + vsrc1
@@ -107,7 +112,7 @@ class Emitter {
     hazard(s0.vgpr, -1, -1);
     put(0x7E000000u | ((uint32_t)vdst << 17) | (op << 9) | s0.code);
     if (s0.code == kSrcLiteral) put(s0.lit);
-    text("%s v%d, %s", name, vdst, s0.text.c_str());
+    if (want_) text("%s v%d, %s", name, vdst, str(s0).c_str());
     wrote(vdst, trans);
   }
   // VOP3 with VGPR src0 and inline-constant or VGPR src1 / src2; neg: the NEG field
@@ -116,10 +121,10 @@ class Emitter {
     hazard(a.vgpr, b.vgpr, c ? c->vgpr : -1);
     put(0xD0000000u | (op << 16) | (uint32_t)vdst);
     put((neg << 29) | ((c ? c->code : 0u) << 18) | (b.code << 9) | a.code);
-    if (c)
-      text("%s v%d, %s, %s, %s", name, vdst, a.text.c_str(), b.text.c_str(), c->text.c_str());
-    else
-      text("%s v%d, %s, %s%s", name, vdst, a.text.c_str(), (neg & 2u) ? "-" : "", b.text.c_str());
+    if (want_ && c)
+      text("%s v%d, %s, %s, %s", name, vdst, str(a).c_str(), str(b).c_str(), str(*c).c_str());
+    else if (want_)
+      text("%s v%d, %s, %s%s", name, vdst, str(a).c_str(), (neg & 2u) ? "-" : "", str(b).c_str());
     wrote(vdst, false);
   }
   void load_x4(int sdata, int sbase, uint32_t offset) {
@@ -232,18 +237,51 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
           if (rec[16 * (size_t)q] & kRecFirst) E.load_x4(row(q, 0), kJitBp, 16u * (1u + q));
         wait = true;
       }
+      // A zero x or y weight adds nothing: its term is left out. (Positions are never 0 (odd
+      // multiples of 2^-level, minus 1), so every product kept is nonzero and the sums equal the
+      // interpreter's, which adds the zero terms; only a node bias of -0.0 would come out +0.0
+      // there.)
+      const bool has_x = R[1] != 0u && R[1] != 0x80000000u, has_y = R[2] != 0u && R[2] != 0x80000000u;
       if (S == 1) {
         if (wait) E.wait_lgkm0();
         const int tb = T;
-        E.vop1(kOpV1Mov, "v_mov_b32_e32", tb, Emitter::Sg(row(r, 0)), false);
-        for (int j = 0; j < P; ++j) E.fmamk(acc(j), X + j, R[1], tb);
-        for (int j = 0; j < P; ++j) E.vop2(kOpV2Fmac, "v_fmac_f32_e32", acc(j), Emitter::K(R[2]), Y + j);
+        if (!has_x && !has_y) {
+          for (int j = 0; j < P; ++j)
+            E.vop1(kOpV1Mov, "v_mov_b32_e32", acc(j), Emitter::Sg(row(r, 0)), false);
+        } else {
+          E.vop1(kOpV1Mov, "v_mov_b32_e32", tb, Emitter::Sg(row(r, 0)), false);
+          if (has_x)
+            for (int j = 0; j < P; ++j) E.fmamk(acc(j), X + j, R[1], tb);
+          else
+            for (int j = 0; j < P; ++j) E.fmamk(acc(j), Y + j, R[2], tb);
+          if (has_x && has_y)
+            for (int j = 0; j < P; ++j)
+              E.vop2(kOpV2Fmac, "v_fmac_f32_e32", acc(j), Emitter::K(R[2]), Y + j);
+        }
+      } else if (!has_x && !has_y) {
+        if (wait) E.wait_lgkm0();
+        if (copies == S) {
+          for (int s = 0; s < S; ++s)
+            E.vop1(kOpV1Mov, "v_mov_b32_e32", T + s, Emitter::Sg(row(r, s)), false);
+          for (int s = 0; s < S; ++s)
+            for (int j = 0; j < P; ++j)
+              E.vop1(kOpV1Mov, "v_mov_b32_e32", acc(s * P + j), Emitter::V(T + s), false);
+        } else {
+          for (int s = 0; s < S; ++s)
+            for (int j = 0; j < P; ++j)
+              E.vop1(kOpV1Mov, "v_mov_b32_e32", acc(s * P + j), Emitter::Sg(row(r, s)), false);
+        }
       } else {
         // the partial sums l_j live in the last source's accumulators (free at a node's start)
         // until every source has added its bias to them
         const int L = acc((S - 1) * P);
-        for (int j = 0; j < P; ++j) E.vop2(kOpV2Mul, "v_mul_f32_e32", L + j, Emitter::K(R[1]), X + j);
-        for (int j = 0; j < P; ++j) E.vop2(kOpV2Fmac, "v_fmac_f32_e32", L + j, Emitter::K(R[2]), Y + j);
+        if (has_x)
+          for (int j = 0; j < P; ++j) E.vop2(kOpV2Mul, "v_mul_f32_e32", L + j, Emitter::K(R[1]), X + j);
+        else
+          for (int j = 0; j < P; ++j) E.vop2(kOpV2Mul, "v_mul_f32_e32", L + j, Emitter::K(R[2]), Y + j);
+        if (has_x && has_y)
+          for (int j = 0; j < P; ++j)
+            E.vop2(kOpV2Fmac, "v_fmac_f32_e32", L + j, Emitter::K(R[2]), Y + j);
         if (wait) E.wait_lgkm0();
         if (copies == S) {  // bias copies in VGPRs: the adds read vector operands only
           for (int s = 0; s < S; ++s)
