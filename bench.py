@@ -43,8 +43,9 @@ VALU_PEAK_SLOTS = 157.3e12 / 2.0  # lane-slots per second (fp32 vector peak, FMA
 METRIC = "CPPN queries/sec incl. variance filter (% VALU peak); ms/gen pop1000 depth7"
 
 
-KERNEL_SOURCES = ["paper_2608_27612_amd/csrc/kernels.hip", "paper_2608_27612_amd/csrc/regwin_gen.h",
-                  "paper_2608_27612_amd/csrc/emr_internal.h"]
+KERNEL_SOURCES = ["paper_2608_27612_amd/csrc/kernels.hip", "paper_2608_27612_amd/csrc/discover.h",
+                  "paper_2608_27612_amd/csrc/jit.hip", "paper_2608_27612_amd/csrc/jit.cpp",
+                  "paper_2608_27612_amd/csrc/regwin_gen.h", "paper_2608_27612_amd/csrc/emr_internal.h"]
 
 
 def kernel_source_sha():
