@@ -103,6 +103,8 @@ def main():
     ap.add_argument("--gens", type=int, default=5, help="generations timed for ms_per_gen")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--jit", choices=["auto", "off", "always"], default="auto",
+                    help="compiled-tier policy for the timed steps (auto: the warm-up compiles)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one device-to-device copy of this size first (outside the timed "
                          "region), as a known-size reference for memory counters")
@@ -127,6 +129,8 @@ def main():
     theta32 = float(np.float32(theta))
     rT = args.transcendental_slots
 
+    policy = {"auto": emr.EMR_JIT_AUTO, "off": emr.EMR_JIT_OFF, "always": emr.EMR_JIT_ALWAYS}[args.jit]
+    emr.emr_set_jit(policy)
     pop = emr.emr_pack_population(genomes)
     res = emr.alloc_result(pop, sources, depth)
     slots, queries = emr.emr_discover_cost(pop, sources, depth, transcendental_slots=rT)
@@ -175,8 +179,8 @@ def main():
     # ms per generation: pack + discover + check on the host clock, for a new population each
     # generation (one call per population: the default policy interprets it), and with the
     # population's programs compiled first (pack + compile + load + discover + check)
-    def per_gen(policy):
-        emr.emr_set_jit(policy)
+    def per_gen(gen_policy):
+        emr.emr_set_jit(gen_policy)
         torch.cuda.synchronize()
         g0 = time.perf_counter()
         for _ in range(args.gens):
@@ -184,7 +188,7 @@ def main():
             emr.emr_discover(p, sources, depth, theta32, res=res)
             emr.emr_result_check(res)
             del p
-        emr.emr_set_jit(emr.EMR_JIT_AUTO)
+        emr.emr_set_jit(policy)
         return (time.perf_counter() - g0) * 1e3 / args.gens
     ms_per_gen = per_gen(emr.EMR_JIT_AUTO)
     ms_per_gen_compiled = per_gen(emr.EMR_JIT_ALWAYS)

@@ -497,36 +497,17 @@ __device__ __forceinline__ void discover_body(const uint32_t* __restrict__ geo_t
                     {(float)(4u * j_lo), (float)(4u * j_lo + 2u)}};
   const DiscoverPtrs d{(cu32*)geo_tab, (cu32*)blob, (cu32*)groups, (cf32*)bias_tab, status, err,
                        parent, w4, pair_count, raw};
-  // XCD-aware assignment: workgroups are dispatched round-robin over the chip's XCDs, each with
-  // its own L2. Group g of a part goes to the workgroups of XCD g mod X (X: the XCDs the grid
-  // covers), whose waves take its chunks in order, so a group's program, tables and records stay
-  // in one L2. Per XCD, chunks are listed part by part (costliest first), group by group, and
-  // its waves take them round-robin.
-  const uint32_t xcds = gridDim.x < kXcds ? gridDim.x : kXcds;
-  const uint32_t xcd = blockIdx.x % xcds;
-  const uint32_t wpb = blockDim.x / kWave;
-  const uint32_t waves_x = ((gridDim.x - xcd + xcds - 1) / xcds) * wpb;
-  const uint32_t wave = __builtin_amdgcn_readfirstlane((blockIdx.x / xcds) * wpb +
+  const uint32_t n_waves = gridDim.x * (blockDim.x / kWave);
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +
                                                        threadIdx.x / kWave);
-  for (uint32_t l = wave;; l += waves_x) {
-    // the local chunk's part, then the part-local chunk index of its group (the gl-th group of
-    // this XCD in the part) and chunk
-    uint32_t k = 0, ll = l;
-    bool found = false;
-    for (; k < a.n_parts; ++k) {
-      const uint32_t cpg = a.part[k].chunks_per_group;
-      const uint32_t groups = cpg ? a.part[k].n_chunks / cpg : 0u;
-      const uint32_t mine = groups > xcd ? (groups - 1u - xcd) / xcds + 1u : 0u;
-      if (ll < mine * cpg) {
-        found = true;
-        break;
-      }
-      ll -= mine * cpg;
+  for (uint32_t c = wave; c < a.n_chunks; c += n_waves) {
+    // the chunk's part, and its index within the part
+    uint32_t k = 0, cl = c;
+    while (k + 1 < a.n_parts && cl >= a.part[k].n_chunks) {
+      cl -= a.part[k].n_chunks;
+      ++k;
     }
-    if (!found) break;
     const DiscoverPart pt = a.part[k];
-    const uint32_t cl = (xcd + xcds * (ll / pt.chunks_per_group)) * pt.chunks_per_group +
-                        ll % pt.chunks_per_group;
     switch (pt.W * 4u + pt.S) {
       case 4 * 4 + 3: discover_chunk<3, 4, MODE, JIT>(cl, pt, a, d, geo, lane, code_base); break;
       case 4 * 4 + 2: discover_chunk<2, 4, MODE, JIT>(cl, pt, a, d, geo, lane, code_base); break;

@@ -224,9 +224,6 @@ EMR_HD constexpr int jit_temps(int S, int P, int W) {
 
 // Tiles of one chunk at most (a chunk's record counts are held one per lane, 16 per source).
 constexpr uint32_t kChunkTilesMax = 16;
-// XCDs of the chip (MI355X: 8 dies of 32 CUs, each with its own L2); workgroups are dispatched
-// round-robin over them.
-constexpr uint32_t kXcds = 8;
 
 struct DiscoverArgs {
   const uint32_t* geo;     // tile geometry table of the depth (k_tile_geo), geo_rows rows
