@@ -222,10 +222,53 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
   for (uint32_t r = kJitRowBlock; r < n; ++r) long_program |= (rec[16 * (size_t)r] & kRecFirst) != 0;
   int64_t loaded_block = long_program ? -1 : 0;
   const int copies = jit_temps(S, P, W);
+
+  // A linear node that stores its value sums straight into its destination slot (the
+  // interpreter sums in the accumulator and copies it there) when none of its own edges reads that
+  // slot: the same operations in the same order on other registers. Marked at the node's first
+  // record.
+  std::vector<uint8_t> in_place(n, 0);
+  {
+    bool started = false;
+    uint32_t first = 0, reads = 0;  // window slots the node's edges read (W <= 32)
+    for (uint32_t r = 0; r < n; ++r) {
+      const uint32_t meta = rec[16 * (size_t)r];
+      if (meta & kRecFirst) {
+        started = true;
+        first = r;
+        reads = 0;
+      }
+      uint32_t ne = (meta >> kRecEdgeShift) & 15u;
+      if (ne > kRecEdges) ne = kRecEdges;
+      for (uint32_t q = 0; q < ne; ++q) {
+        const uint32_t sw = q < 6 ? rec[16 * (size_t)r + 3] : rec[16 * (size_t)r + 4];
+        reads |= 1u << ((sw >> (kSlotBits * (q % 6))) & wmask);
+      }
+      uint32_t tail = meta & kRecTailMask;
+      if (tail > 13) tail = 13;
+      if (tail == 0 || tail == 13) continue;
+      const uint32_t dst = (meta >> kRecDstShift) & wmask;
+      if (started && tail == kRecTailStore + EMR_ACT_LINEAR && !((reads >> dst) & 1u))
+        in_place[first] = 1;
+      started = false;
+    }
+  }
+  bool inplace = false;
+  uint32_t node_dst = 0;
+  auto A = [&](int m) { return inplace ? win(m, node_dst) : acc(m); };  // the node's sum
+  // A node without x or y terms starts from its bias: folded into its first edge (one v_fmamk
+  // per instance, the fma the interpreter's move + v_fmac computes) when that edge is in the
+  // node's first record and the bias is in a VGPR (a copy per source, or one for S = 1).
+  bool fuse = false;
+  int bias_base = 0, bias_step = 0;  // instance m's bias in v[bias_base + (m / P) * bias_step]
   for (uint32_t r = 0; r < n; ++r) {
     const uint32_t* R = rec + 16 * (size_t)r;
     const uint32_t meta = R[0];
     if (meta & kRecFirst) {
+      inplace = in_place[r] != 0;
+      node_dst = (meta >> kRecDstShift) & wmask;
+      uint32_t ne0 = (meta >> kRecEdgeShift) & 15u;
+      if (ne0 > kRecEdges) ne0 = kRecEdges;
       // The bias rows of the first records of this record's block of kJitRowBlock are loaded
       // together (the rows of the records the interpreter reads them for), and waited for once.
       bool wait = false;
@@ -242,34 +285,46 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
       // interpreter's, which adds the zero terms; only a node bias of -0.0 would come out +0.0
       // there.)
       const bool has_x = R[1] != 0u && R[1] != 0x80000000u, has_y = R[2] != 0u && R[2] != 0x80000000u;
+      fuse = false;
       if (S == 1) {
         if (wait) E.wait_lgkm0();
         const int tb = T;
-        if (!has_x && !has_y) {
+        if (!has_x && !has_y && ne0 > 0) {
+          E.vop1(kOpV1Mov, "v_mov_b32_e32", tb, Emitter::Sg(row(r, 0)), false);
+          fuse = true;
+          bias_base = tb;
+          bias_step = 0;
+        } else if (!has_x && !has_y) {
           for (int j = 0; j < P; ++j)
-            E.vop1(kOpV1Mov, "v_mov_b32_e32", acc(j), Emitter::Sg(row(r, 0)), false);
+            E.vop1(kOpV1Mov, "v_mov_b32_e32", A(j), Emitter::Sg(row(r, 0)), false);
         } else {
           E.vop1(kOpV1Mov, "v_mov_b32_e32", tb, Emitter::Sg(row(r, 0)), false);
           if (has_x)
-            for (int j = 0; j < P; ++j) E.fmamk(acc(j), X + j, R[1], tb);
+            for (int j = 0; j < P; ++j) E.fmamk(A(j), X + j, R[1], tb);
           else
-            for (int j = 0; j < P; ++j) E.fmamk(acc(j), Y + j, R[2], tb);
+            for (int j = 0; j < P; ++j) E.fmamk(A(j), Y + j, R[2], tb);
           if (has_x && has_y)
             for (int j = 0; j < P; ++j)
-              E.vop2(kOpV2Fmac, "v_fmac_f32_e32", acc(j), Emitter::K(R[2]), Y + j);
+              E.vop2(kOpV2Fmac, "v_fmac_f32_e32", A(j), Emitter::K(R[2]), Y + j);
         }
       } else if (!has_x && !has_y) {
         if (wait) E.wait_lgkm0();
         if (copies == S) {
           for (int s = 0; s < S; ++s)
             E.vop1(kOpV1Mov, "v_mov_b32_e32", T + s, Emitter::Sg(row(r, s)), false);
-          for (int s = 0; s < S; ++s)
-            for (int j = 0; j < P; ++j)
-              E.vop1(kOpV1Mov, "v_mov_b32_e32", acc(s * P + j), Emitter::V(T + s), false);
+          if (ne0 > 0) {
+            fuse = true;
+            bias_base = T;
+            bias_step = 1;
+          } else {
+            for (int s = 0; s < S; ++s)
+              for (int j = 0; j < P; ++j)
+                E.vop1(kOpV1Mov, "v_mov_b32_e32", A(s * P + j), Emitter::V(T + s), false);
+          }
         } else {
           for (int s = 0; s < S; ++s)
             for (int j = 0; j < P; ++j)
-              E.vop1(kOpV1Mov, "v_mov_b32_e32", acc(s * P + j), Emitter::Sg(row(r, s)), false);
+              E.vop1(kOpV1Mov, "v_mov_b32_e32", A(s * P + j), Emitter::Sg(row(r, s)), false);
         }
       } else {
         // the partial sums l_j live in the last source's accumulators (free at a node's start)
@@ -288,11 +343,11 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
             E.vop1(kOpV1Mov, "v_mov_b32_e32", T + s, Emitter::Sg(row(r, s)), false);
           for (int s = 0; s < S; ++s)
             for (int j = 0; j < P; ++j)
-              E.vop2(kOpV2Add, "v_add_f32_e32", acc(s * P + j), Emitter::V(T + s), L + j);
+              E.vop2(kOpV2Add, "v_add_f32_e32", A(s * P + j), Emitter::V(T + s), L + j);
         } else {
           for (int s = 0; s < S; ++s)
             for (int j = 0; j < P; ++j)
-              E.vop2(kOpV2Add, "v_add_f32_e32", acc(s * P + j), Emitter::Sg(row(r, s)), L + j);
+              E.vop2(kOpV2Add, "v_add_f32_e32", A(s * P + j), Emitter::Sg(row(r, s)), L + j);
         }
       }
     }
@@ -303,7 +358,13 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
       const uint32_t sw = q < 6 ? R[3] : R[4];
       const uint32_t slot = (sw >> (kSlotBits * (q % 6))) & wmask;
       const Src w = Emitter::K(R[5 + q]);
-      for (int m = 0; m < M; ++m) E.vop2(kOpV2Fmac, "v_fmac_f32_e32", acc(m), w, win(m, slot));
+      if (fuse) {
+        for (int m = 0; m < M; ++m)
+          E.fmamk(A(m), win(m, slot), R[5 + q], bias_base + (m / P) * bias_step);
+        fuse = false;
+      } else {
+        for (int m = 0; m < M; ++m) E.vop2(kOpV2Fmac, "v_fmac_f32_e32", A(m), w, win(m, slot));
+      }
     }
     // tail
     uint32_t tail = meta & kRecTailMask;
@@ -318,7 +379,8 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
     };
     switch (act) {
       case EMR_ACT_LINEAR:
-        if (store) each([&](int m) { E.vop1(kOpV1Mov, "v_mov_b32_e32", D(m), Emitter::V(acc(m)), false); });
+        if (store && !inplace)
+          each([&](int m) { E.vop1(kOpV1Mov, "v_mov_b32_e32", D(m), Emitter::V(acc(m)), false); });
         break;
       case EMR_ACT_ABS:
         each([&](int m) { E.vop2(kOpV2And, "v_and_b32_e32", D(m), Emitter::K(0x7fffffffu), acc(m)); });

@@ -133,6 +133,88 @@ def test_uniform_output_program_copies_row_zero():
     assert [V[4 + m] for m in range(24)] == [0.25] * 8 + [-1.5] * 8 + [3.0] * 8
 
 
+
+def _writes(listing):
+    """(opcode, destination VGPR, source text) of every vector instruction in a listing."""
+    out = []
+    for line in listing.strip().split("\n"):
+        op, _, rest = line.partition(" ")
+        if op.startswith("v_"):
+            dst, _, srcs = rest.partition(",")
+            out.append((op, int(dst.strip()[1:]), srcs))
+    return out
+
+
+def test_nodes_without_position_terms_start_with_their_first_edge():
+    """A node's bias is folded into its first edge (v_fmamk): no accumulator is set by a move
+    and then summed into by v_fmac."""
+    fused = 0
+    for gi, blob, desc, d, S, P, Wn in programs(POPS[0] + POPS[1]):
+        _, listing = PI.compile_program(blob, desc[d], S, P, Wn)
+        last = {}
+        for op, dst, srcs in _writes(listing):
+            if op == "v_fmac_f32_e32":
+                assert last.get(dst) != "v_mov_b32_e32", (gi, d, S, P, Wn, dst)
+            fused += op == "v_fmamk_f32" and dst < 4 + S * P
+            last[dst] = op
+    assert fused > 0
+
+
+def _rec_slots(blob, off):
+    """(edge source slots, tail, destination slot) of the record at blob[off]."""
+    meta = int(blob[off])
+    ne = (meta >> 16) & 15
+    srcs = [(int(blob[off + 3 + e // 6]) >> (5 * (e % 6))) & 31 for e in range(ne)]
+    return srcs, meta & 15, (meta >> 8) & 31
+
+
+def _linear_store_counts(blob, desc, d):
+    """(linear nodes that store their value, those of them whose own edges read the slot they
+    store into) of one program."""
+    var_off, n_rec = int(desc[d][0]), int(desc[d][1])
+    n = clash = 0
+    reads = set()
+    for r in range(n_rec):
+        srcs, tail, dst = _rec_slots(blob, var_off + 16 * r)
+        if int(blob[var_off + 16 * r]) & 16:
+            reads = set()
+        reads |= set(srcs)
+        n += tail == 1
+        clash += tail == 1 and dst in reads
+    return n, clash
+
+
+def test_linear_nodes_sum_in_their_destination_slot():
+    """A linear node that stores its value sums in its destination slot (no copy from an
+    accumulator); one whose own edges read that slot (the packer reuses an input's slot when
+    the input dies at the node) keeps the accumulator and copies it; both compute the packed
+    program."""
+    rng = np.random.default_rng(13)
+    in_place = clashing = 0
+    for gi, blob, desc, d, S, P, Wn in programs(W.population(21, 60, 20, 60)):
+        if not (int(desc[d][4]) & 1):
+            continue
+        n_lin, n_clash = _linear_store_counts(blob, desc, d)
+        if n_lin == 0:
+            continue
+        M = S * P
+        _, listing = PI.compile_program(blob, desc[d], S, P, Wn)
+        copies = [w for w in _writes(listing)
+                  if w[0] == "v_mov_b32_e32" and re.fullmatch(r"\s*v(\d+)", w[2])
+                  and 4 <= int(w[2].strip()[1:]) < 4 + M]
+        assert len(copies) == M * n_clash, (gi, d, S, P, Wn)
+        srcs = [(float(rng.uniform(-1, 1)), float(rng.uniform(-1, 1))) for _ in range(S)]
+        x, y = rng.uniform(-1, 1, P), rng.uniform(-1, 1, P)
+        V = PI.emulate(listing, PI.bias_rows(blob, desc, d, srcs), x, y, M, Wn)
+        for s, (sx, sy) in enumerate(srcs):
+            want, _ = PI.interpret(blob, desc, d, sx, sy, x, y)
+            got = np.array([V[4 + s * P + j] for j in range(P)])
+            assert np.allclose(got, want, rtol=1e-9, atol=1e-9), (gi, d, S, P, Wn, s)
+        in_place += n_lin - n_clash
+        clashing += n_clash
+    assert in_place > 0 and clashing > 0, (in_place, clashing)
+
+
 TRANS = ("v_exp_f32", "v_rcp_f32", "v_sin_f32")
 
 
