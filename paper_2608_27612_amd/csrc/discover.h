@@ -299,19 +299,20 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
   // Padded placement: the chunk's record counts, source s and tile chunk_tile + k in lane
   // 16 s + k; they stay zero unless a walk keeps a cell, and go out with one store per chunk.
   uint32_t chunk_counts = 0;
-  // The geometry rows of the walk's tiles, loaded one walk ahead. The host sizes the table for
-  // the launch's range (emr_discover_setup); the row index is still bounded, and a walk past the
-  // range end reads the last row and keeps nothing.
+  // The geometry rows of the walk's tiles, loaded one walk ahead from gp (the rows of the next
+  // walk's tiles). The host sizes the table for the launch's range plus kGeoPadRows rows of
+  // padding (emr_discover_setup), which the last walks' loads reach; a walk past the range end
+  // keeps nothing.
   uint32_t gnext[TPW][4];
-  auto load_geo = [&](uint32_t t) {
+  cu32* gp = d.geo + 4u * (a.tile_lo + chunk_tile);
+  auto load_geo = [&]() {
 #pragma unroll
-    for (int k = 0; k < TPW; ++k) {
-      cu32* gt = d.geo + 4u * min(a.tile_lo + t + (uint32_t)k, a.geo_rows - 1u);
+    for (int k = 0; k < TPW; ++k)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) gnext[k][q] = gt[q];
-    }
+      for (int q = 0; q < 4; ++q) gnext[k][q] = gp[4 * k + q];
+    gp += 4 * TPW;
   };
-  load_geo(chunk_tile);
+  load_geo();
   for (uint32_t t0 = chunk_tile; t0 < chunk_end; t0 += TPW) {
     uint32_t gcur[TPW][4];
 #pragma unroll
@@ -368,20 +369,17 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
     // interpreter's walk.
     const float* w;
     if constexpr (JIT) {
-      uint64_t next_rows[TPW];
-#pragma unroll
-      for (int k = 0; k < TPW; ++k)
-        next_rows[k] = (uint64_t)(d.geo + 4u * min(a.tile_lo + t0 + (uint32_t)(TPW + k),
-                                                   a.geo_rows - 1u));
-      u32x4 g[TPW];
-      J.call(code_base + G.code_off, (uint64_t)(d.bias + G.bias_off), px, py, rows, next_rows, g);
+      typename JitCall<S, P, W>::Geo g;
+      J.call(code_base + G.code_off, (uint64_t)(d.bias + G.bias_off), px, py, rows, (uint64_t)gp,
+             g);
+      gp += 4 * TPW;
 #pragma unroll
       for (int k = 0; k < TPW; ++k)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) gnext[k][q] = g[k][q];
+        for (int q = 0; q < 4; ++q) gnext[k][q] = g[4 * k + q];
       w = J.acc;
     } else {
-      load_geo(t0 + TPW);
+      load_geo();
       R.def();
       R.walk((uint64_t)(d.blob + G.var_off), (uint64_t)(d.bias + G.bias_off), n_rec, px, py);
       w = R.acc;

@@ -179,7 +179,6 @@ struct DiscoverScalars {
   int32_t depth;
   float theta16;  // 16 theta
   uint32_t code_bytes;  // compiled tier: size of the code area (0 for the interpreter)
-  uint32_t geo_rows;    // rows of the tile geometry table (tiles per pair)
   uint32_t blob_words, n_pairs;
   uint32_t bias_floats;  // the host keeps the bias table below 2^32 floats
   uint32_t head_parents;  // parents in a pair's tile 0 (levels 1..3, or all levels of a shallower grid)
@@ -196,7 +195,11 @@ constexpr int kModeRaw = 0, kModePadded = 1, kModeLookback = 2;
 // kernel and the host code generator. For M = S P instances:
 //   v[kJitAcc + m]                    accumulator of instance m (the program's outputs)
 //   v[jit_window(M, W, m) + k]        slot k of instance m's value window (k < W)
-//   v[jit_x(M, W) + j], + P + j       the x and y of position j (read only)
+//   v[jit_xr(M, W, j)], v[jit_yr(...)] the x and y of position j (read only). Position
+//                                     4 k + c is child c of the lane's parent in tile k, whose
+//                                     x depends on c & 1 and y on c >> 1 only: each is held once,
+//                                     x at jit_x + 4 k + (c & 1), y at jit_x + P + 4 k + (c & 2)
+//                                     (the registers between are not part of the convention)
 //   v[jit_x(M, W) + 2 P ...]          jit_temps(S, P, W) bias copies (for S > 1 the last source's
 //                                     accumulators hold the partial sums)
 //   s[kJitRow .. kJitRow + 15]        bias rows 1 .. kJitRowBlock of the group (the rows of records
@@ -215,6 +218,10 @@ constexpr int kJitRet = 58;
 constexpr uint32_t kJitTailPad = 1024;  // s_endpgm bytes kept after the last program
 EMR_HD constexpr int jit_window(int M, int W, int m) { return ((kJitAcc + M + 1) & ~1) + m * W; }
 EMR_HD constexpr int jit_x(int M, int W) { return jit_window(M, W, M); }
+EMR_HD constexpr int jit_xr(int M, int W, int j) { return jit_x(M, W) + (j & ~3) + (j & 1); }
+EMR_HD constexpr int jit_yr(int M, int W, int P, int j) {
+  return jit_x(M, W) + P + (j & ~3) + (j & 2);
+}
 // Bias copies of a variant: one per source, where they fit below kJitTop (the highest register
 // any variant needs); a variant without them adds the biases from their SGPRs.
 constexpr int kJitTop = 148;
@@ -224,10 +231,13 @@ EMR_HD constexpr int jit_temps(int S, int P, int W) {
 
 // Tiles of one chunk at most (a chunk's record counts are held one per lane, 16 per source).
 constexpr uint32_t kChunkTilesMax = 16;
+// Rows of zeros after the last tile of the tile geometry table: a walk of TPW <= 4 tiles loads
+// the next walk's TPW rows, up to 2 TPW - 1 rows past its first tile, with no bound per load.
+constexpr uint32_t kGeoPadRows = 8;
 
 struct DiscoverArgs {
   const uint32_t* geo;     // tile geometry table of the depth (k_tile_geo), geo_rows rows
-  uint32_t geo_rows;
+  uint32_t geo_rows;       // with the kGeoPadRows rows of padding
   const uint32_t* blob;
   const Group* groups;     // the plan's group table (parts index into it)
   const float* bias_tab;

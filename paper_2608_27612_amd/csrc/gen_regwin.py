@@ -303,9 +303,10 @@ def gen_jitcall(S, P, W):
     xy = base(M, M, W)
     tmp0 = xy + 2 * P
     TPW = P // 4
-    # the next walk's tile geometry rows are loaded first, so they arrive while the program runs;
-    # the wait after the return point makes them safe to read (long done by then)
-    L = ["s_load_dwordx4 %%[g%d], %%[a%d], 0x0" % (k, k) for k in range(TPW)]
+    # the next walk's tile geometry rows (TPW consecutive rows of 4 words) are loaded first, with
+    # one load, so they arrive while the program runs; the wait after the return point makes them
+    # safe to read (long done by then)
+    L = ["s_load_dwordx%d %%[geo], %%[ga], 0x0" % (4 * TPW)]
     L += ["s_getpc_b64 s[%d:%d]" % (JIT_RET, JIT_RET + 1),
           ".Lcall_%=:",
           "s_add_u32 s%d, s%d, .Lret_%%= - .Lcall_%%=" % (JIT_RET, JIT_RET),
@@ -317,19 +318,22 @@ def gen_jitcall(S, P, W):
     outs += ['"=&{v[%d:%d]}"(w%d)' % (base(M, m, W), base(M, m, W) + W - 1, m) for m in range(M)]
     outs += ['"=&{v%d}"(t[%d])' % (tmp0 + k, k) for k in range(jit_temps(S, P, W))]
     outs += ['"+{s[%d:%d]}"(rows)' % (JIT_ROW, JIT_ROW + 15)]
-    outs += ['[g%d] "=&s"(geo[%d])' % (k, k) for k in range(TPW)]
-    ins = ['[tgt] "s"(target)', '"{s[%d:%d]}"(bp)' % (JIT_BP, JIT_BP + 1)]
-    ins += ['[a%d] "s"(geo_addr[%d])' % (k, k) for k in range(TPW)]
-    ins += ['"{v%d}"(x[%d]), "{v%d}"(y[%d])' % (xy + j, j, xy + P + j, j) for j in range(P)]
+    outs += ['[geo] "=&s"(geo)']
+    ins = ['[tgt] "s"(target)', '"{s[%d:%d]}"(bp)' % (JIT_BP, JIT_BP + 1), '[ga] "s"(geo_addr)']
+    # position 4 k + c: x depends on c & 1, y on c >> 1; each distinct value is passed once
+    ins += ['"{v%d}"(x[%d])' % (xy + j, j) for j in range(P) if j % 4 in (0, 1)]
+    ins += ['"{v%d}"(y[%d])' % (xy + P + j, j) for j in range(P) if j % 4 in (0, 2)]
     clob = ['"scc"', '"s%d"' % JIT_RET, '"s%d"' % (JIT_RET + 1)]
     body = "\n".join('        "%s\\n"' % l for l in L)
     out = []
     out.append("template <> struct JitCall<%d, %d, %d> {" % (S, P, W))
+    out.append("  typedef uint32_t Geo __attribute__((ext_vector_type(%d)));" % (4 * TPW))
     out.append("  float acc[%d];" % M)
     out.append("  // Runs the compiled program at `target` for the P positions (x, y); bp: the group's bias rows,")
-    out.append("  // rows: its rows 1 .. 4 (in and out, see the register convention); geo: the rows at geo_addr.")
+    out.append("  // rows: its rows 1 .. 4 (in and out, see the register convention); geo: the %d words at" % (4 * TPW))
+    out.append("  // geo_addr.")
     out.append("  __device__ __forceinline__ void call(uint64_t target, uint64_t bp, const float* x, "
-               "const float* y, u32x16& rows, const uint64_t* geo_addr, u32x4* geo) {")
+               "const float* y, u32x16& rows, uint64_t geo_addr, Geo& geo) {")
     out.append("    f32x%d %s;" % (W, ", ".join("w%d" % m for m in range(M))))
     if jit_temps(S, P, W):
         out.append("    float t[%d];" % jit_temps(S, P, W))

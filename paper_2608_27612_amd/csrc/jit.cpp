@@ -200,7 +200,10 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
   const int M = S * P;
   auto acc = [&](int m) { return kJitAcc + m; };
   auto win = [&](int m, uint32_t k) { return jit_window(M, W, m) + (int)k; };
-  const int X = jit_x(M, W), Y = X + P, T = X + 2 * P;  // bias copies from T
+  const int T = jit_x(M, W) + 2 * P;  // bias copies from T
+  // position j's x and y (the convention holds each distinct value of a tile once)
+  auto xr = [&](int j) { return jit_xr(M, W, j); };
+  auto yr = [&](int j) { return jit_yr(M, W, P, j); };
   auto row = [](uint32_t r, int s) { return kJitRow + 4 * (int)(r % kJitRowBlock) + s; };
   const uint32_t n = output_varies ? n_rec : 0u;
 
@@ -300,12 +303,12 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
         } else {
           E.vop1(kOpV1Mov, "v_mov_b32_e32", tb, Emitter::Sg(row(r, 0)), false);
           if (has_x)
-            for (int j = 0; j < P; ++j) E.fmamk(A(j), X + j, R[1], tb);
+            for (int j = 0; j < P; ++j) E.fmamk(A(j), xr(j), R[1], tb);
           else
-            for (int j = 0; j < P; ++j) E.fmamk(A(j), Y + j, R[2], tb);
+            for (int j = 0; j < P; ++j) E.fmamk(A(j), yr(j), R[2], tb);
           if (has_x && has_y)
             for (int j = 0; j < P; ++j)
-              E.vop2(kOpV2Fmac, "v_fmac_f32_e32", A(j), Emitter::K(R[2]), Y + j);
+              E.vop2(kOpV2Fmac, "v_fmac_f32_e32", A(j), Emitter::K(R[2]), yr(j));
         }
       } else if (!has_x && !has_y) {
         if (wait) E.wait_lgkm0();
@@ -328,27 +331,30 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
         }
       } else {
         // the partial sums l_j live in the last source's accumulators (free at a node's start)
-        // until every source has added its bias to them
+        // until every source has added its bias to them. With one position term, l_j has two
+        // distinct values per tile, computed once each: position j reads l at ls(j) <= j.
         const int L = acc((S - 1) * P);
-        if (has_x)
-          for (int j = 0; j < P; ++j) E.vop2(kOpV2Mul, "v_mul_f32_e32", L + j, Emitter::K(R[1]), X + j);
-        else
-          for (int j = 0; j < P; ++j) E.vop2(kOpV2Mul, "v_mul_f32_e32", L + j, Emitter::K(R[2]), Y + j);
+        auto ls = [&](int j) {
+          return L + (has_x && has_y ? j : has_x ? (j & ~3) + (j & 1) : (j & ~3) + (j & 2));
+        };
+        for (int j = 0; j < P; ++j)
+          if (ls(j) == L + j)
+            E.vop2(kOpV2Mul, "v_mul_f32_e32", L + j, Emitter::K(has_x ? R[1] : R[2]),
+                   has_x ? xr(j) : yr(j));
         if (has_x && has_y)
           for (int j = 0; j < P; ++j)
-            E.vop2(kOpV2Fmac, "v_fmac_f32_e32", L + j, Emitter::K(R[2]), Y + j);
+            E.vop2(kOpV2Fmac, "v_fmac_f32_e32", L + j, Emitter::K(R[2]), yr(j));
         if (wait) E.wait_lgkm0();
-        if (copies == S) {  // bias copies in VGPRs: the adds read vector operands only
+        if (copies == S)  // bias copies in VGPRs: the adds read vector operands only
           for (int s = 0; s < S; ++s)
             E.vop1(kOpV1Mov, "v_mov_b32_e32", T + s, Emitter::Sg(row(r, s)), false);
-          for (int s = 0; s < S; ++s)
-            for (int j = 0; j < P; ++j)
-              E.vop2(kOpV2Add, "v_add_f32_e32", A(s * P + j), Emitter::V(T + s), L + j);
-        } else {
-          for (int s = 0; s < S; ++s)
-            for (int j = 0; j < P; ++j)
-              E.vop2(kOpV2Add, "v_add_f32_e32", A(s * P + j), Emitter::Sg(row(r, s)), L + j);
-        }
+        // (the last source's sums overwrite l, in decreasing j: l at ls(j) <= j is read first)
+        for (int s = 0; s < S; ++s)
+          for (int jj = 0; jj < P; ++jj) {
+            const int j = s == S - 1 ? P - 1 - jj : jj;
+            const Src b = copies == S ? Emitter::V(T + s) : Emitter::Sg(row(r, s));
+            E.vop2(kOpV2Add, "v_add_f32_e32", A(s * P + j), b, ls(j));
+          }
       }
     }
     // edges, from record position n - 1 down to 0

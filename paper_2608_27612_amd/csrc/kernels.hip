@@ -160,11 +160,11 @@ __global__ void __launch_bounds__(256)
 // The tile geometry table of a depth: row T (T >= 1, a level-aligned tile of 256 positions) holds
 // the corner term of its 16 x 16 block of cells (Eq. 1: (32 column + 1) 2^-level - 1, likewise for
 // the row), the level's cell size 2^-level, and the grid index of its first position. Row 0 (the
-// head tile, decoded lane by lane) is zero.
-__global__ void k_tile_geo(uint32_t* __restrict__ out, uint32_t rows) {
+// head tile, decoded lane by lane) and the rows from `tiles` to `rows` (padding) are zero.
+__global__ void k_tile_geo(uint32_t* __restrict__ out, uint32_t tiles, uint32_t rows) {
   for (uint32_t T = blockIdx.x * blockDim.x + threadIdx.x; T < rows; T += gridDim.x * blockDim.x) {
-    uint32_t r[4] = {0u, 0u, 0u, 0u};
-    if (T > 0) {
+    uint32_t r[4] = {0u, 0u, 0u, 0u};  // tile 0 (decoded per position) and the padding rows
+    if (T > 0 && T < tiles) {
       TileGeo g;
       tile_geo_set(g, T);
       const float sc = pow2_neg((int)g.lvl);
@@ -355,11 +355,12 @@ extern "C" hipError_t emr_launch_grid(float* xy, int64_t n, hipStream_t s) {
   return hipGetLastError();
 }
 
-extern "C" hipError_t emr_launch_tile_geo(uint32_t* out, uint32_t rows, hipStream_t s) {
+extern "C" hipError_t emr_launch_tile_geo(uint32_t* out, uint32_t tiles, uint32_t rows,
+                                          hipStream_t s) {
   if (rows == 0) return hipSuccess;
   uint32_t blocks = (rows + 255) / 256;
   if (blocks > 65536) blocks = 65536;
-  hipLaunchKernelGGL(emr::k_tile_geo, dim3(blocks), dim3(256), 0, s, out, rows);
+  hipLaunchKernelGGL(emr::k_tile_geo, dim3(blocks), dim3(256), 0, s, out, tiles, rows);
   return hipGetLastError();
 }
 
@@ -380,7 +381,8 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   if (per_cu <= 0) per_cu = 1;
   if (cus <= 0) cus = 1;
   if (a->n_parts == 0 || a->n_parts > (uint32_t)emr::kMaxParts) return hipErrorInvalidValue;
-  if (!a->geo || (uint64_t)a->tile_lo + a->tiles > a->geo_rows) return hipErrorInvalidValue;
+  if (!a->geo || (uint64_t)a->tile_lo + a->tiles + emr::kGeoPadRows > a->geo_rows)
+    return hipErrorInvalidValue;
   uint64_t groups = 0;
   for (uint32_t k = 0; k < a->n_parts; ++k) {
     const int S = (int)a->part_S[k], W = (int)a->part_W[k];
@@ -417,7 +419,6 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   sc.depth = a->depth;
   sc.theta16 = 16.0f * a->theta;
   sc.code_bytes = 0;
-  sc.geo_rows = a->geo_rows;
   sc.blob_words = a->blob_words;
   sc.n_pairs = a->n_pairs;
   sc.bias_floats = (uint32_t)a->bias_floats;

@@ -33,7 +33,8 @@ extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* paren
 extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
                                         const float* w4, int64_t cap, uint32_t n_pairs,
                                         uint32_t* out_parent, float* out_w4, hipStream_t s);
-extern "C" hipError_t emr_launch_tile_geo(uint32_t* out, uint32_t rows, hipStream_t s);
+extern "C" hipError_t emr_launch_tile_geo(uint32_t* out, uint32_t tiles, uint32_t rows,
+                                          hipStream_t s);
 extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t blocks, int per_cu,
                                          int cus, emr::DiscoverScalars* out, uint32_t* grid);
 // The compiled tier's template code object (jit_image.cpp).
@@ -508,13 +509,14 @@ emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspac
 }
 
 // The tile geometry table of a depth on the current device (k_tile_geo), built on first use and
-// kept for the life of the process (tiles_per_pair(depth) rows of 16 bytes: 5.6 MB at depth 13).
+// kept for the life of the process (tiles_per_pair(depth) + kGeoPadRows rows of 16 bytes: 5.6 MB
+// at depth 13).
 emr_status tile_geo_table(int depth, const uint32_t** out, uint32_t* rows) {
   static std::mutex mu;
   static std::vector<std::pair<std::pair<int, int>, uint32_t*>> cache;  // (device, depth)
   int dev = 0;
   HIP_OR_FAIL(hipGetDevice(&dev));
-  const int64_t n = emr::tiles_per_pair(depth);
+  const int64_t tiles = emr::tiles_per_pair(depth), n = tiles + emr::kGeoPadRows;
   if (n > 0xFFFFFFFFll / 4) return fail(EMR_E_LIMIT, "depth %d has too many tiles", depth);
   *rows = (uint32_t)n;
   std::lock_guard<std::mutex> lock(mu);
@@ -528,7 +530,7 @@ emr_status tile_geo_table(int depth, const uint32_t** out, uint32_t* rows) {
     return fail(EMR_E_NOMEM, "tile geometry table of %lld rows", (long long)n);
   StreamPool* sp = nullptr;
   emr_status st = stream_pool(&sp);
-  if (st == EMR_OK && (emr_launch_tile_geo(d, (uint32_t)n, sp->aux[0]) != hipSuccess ||
+  if (st == EMR_OK && (emr_launch_tile_geo(d, (uint32_t)tiles, (uint32_t)n, sp->aux[0]) != hipSuccess ||
                        hipStreamSynchronize(sp->aux[0]) != hipSuccess))
     st = fail(EMR_E_DEVICE, "building the tile geometry table failed");
   if (st != EMR_OK) {

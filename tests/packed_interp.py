@@ -159,16 +159,31 @@ def _operand(tok, V, S_):
     return f32(i & 0xFFFFFFFF)
 
 
+def positions(rng, P):
+    """P positions in sibling quads (x of child c depends on c & 1, y on c >> 1), as a lane holds
+    them."""
+    x0, y0 = rng.uniform(-1, 1, (2, P // 4, 2))
+    c = np.arange(P) % 4
+    q = np.arange(P) // 4
+    return x0[q, c & 1], y0[q, c >> 1]
+
+
 def emulate(listing, rows, x, y, M, W, stale_rows=False):
     """Executes a compiled program's listing on the host in float64 with exact transcendentals:
-    `rows` are the group's bias rows (bias_rows), x and y the P positions. Returns the VGPR file
-    (a dict). Reading a register that nothing wrote raises KeyError, as an interpreter that reads
-    an undefined slot would. With `stale_rows`, s[40:55] start out holding garbage instead of the
+    `rows` are the group's bias rows (bias_rows), x and y the P positions (sibling quads, as
+    `positions` makes them). Returns the VGPR file (a dict). Reading a register that nothing
+    wrote raises KeyError, as an interpreter that reads an undefined slot would; only the
+    registers of the convention hold positions (x of child c of quad k at X + 4 k + (c & 1), y at
+    X + P + 4 k + (c & 2)). With `stale_rows`, s[40:55] start out holding garbage instead of the
     preloaded rows (what a program finds after a longer program of the same chunk ran)."""
     P = len(x)
     X = ((4 + M + 1) & ~1) + M * W
-    V = {X + j: float(x[j]) for j in range(P)}
-    V.update({X + P + j: float(y[j]) for j in range(P)})
+    V = {}
+    for j in range(P):
+        xj, yj = X + (j & ~3) + (j & 1), X + P + (j & ~3) + (j & 2)
+        assert V.setdefault(xj, float(x[j])) == float(x[j]), "not a sibling quad"
+        assert V.setdefault(yj, float(y[j])) == float(y[j]), "not a sibling quad"
+
     # on entry s[40:55] hold the group's bias rows 1 .. 4 (loaded by the caller once per chunk)
     S_ = {40 + k: (float(rows[4 + k]) if 4 + k < len(rows) else 0.0) for k in range(16)}
     if stale_rows:

@@ -78,8 +78,7 @@ def test_compiled_programs_compute_the_packed_programs():
     for gi, blob, desc, d, S, P, Wn in programs(POPS[0] + POPS[1][:2]):
         M = S * P
         srcs = [(float(rng.uniform(-1, 1)), float(rng.uniform(-1, 1))) for _ in range(S)]
-        x = rng.uniform(-1, 1, P)
-        y = rng.uniform(-1, 1, P)
+        x, y = PI.positions(rng, P)
         words, listing = PI.compile_program(blob, desc[d], S, P, Wn)
         V = PI.emulate(listing, PI.bias_rows(blob, desc, d, srcs), x, y, M, Wn)
         for s, (sx, sy) in enumerate(srcs):
@@ -109,7 +108,7 @@ def test_programs_load_only_rows_the_caller_did_not_preload():
             continue
         seen_long += 1
         srcs = [(float(rng.uniform(-1, 1)), float(rng.uniform(-1, 1))) for _ in range(S)]
-        x, y = rng.uniform(-1, 1, P), rng.uniform(-1, 1, P)
+        x, y = PI.positions(rng, P)
         V = PI.emulate(listing, PI.bias_rows(blob, desc, d, srcs), x, y, S * P, Wn,
                        stale_rows=True)
         for s, (sx, sy) in enumerate(srcs):
@@ -204,7 +203,7 @@ def test_linear_nodes_sum_in_their_destination_slot():
                   and 4 <= int(w[2].strip()[1:]) < 4 + M]
         assert len(copies) == M * n_clash, (gi, d, S, P, Wn)
         srcs = [(float(rng.uniform(-1, 1)), float(rng.uniform(-1, 1))) for _ in range(S)]
-        x, y = rng.uniform(-1, 1, P), rng.uniform(-1, 1, P)
+        x, y = PI.positions(rng, P)
         V = PI.emulate(listing, PI.bias_rows(blob, desc, d, srcs), x, y, M, Wn)
         for s, (sx, sy) in enumerate(srcs):
             want, _ = PI.interpret(blob, desc, d, sx, sy, x, y)
@@ -233,15 +232,20 @@ def test_transcendental_results_are_never_read_by_the_next_instruction():
 
 
 def test_register_use_stays_inside_the_convention():
-    """Only the accumulators, windows, positions and temporaries of the variant, and SGPRs
-    s[40:59]."""
-    for gi, blob, desc, d, S, P, Wn in programs(POPS[1]):
+    """Only the accumulators, windows, positions (read only, at the registers of the
+    convention) and temporaries of the variant, and SGPRs s[40:59]."""
+    for gi, blob, desc, d, S, P, Wn in programs(POPS[1] + POPS[0][:4]):
         M = S * P
         X = ((4 + M + 1) & ~1) + M * Wn
         top = X + 2 * P + G.jit_temps(S, P, Wn)
+        pos = {X + (j & ~3) + (j & 1) for j in range(P)} | {X + P + (j & ~3) + (j & 2)
+                                                             for j in range(P)}
         _, listing = PI.compile_program(blob, desc[d], S, P, Wn)
         for v in re.findall(r"\bv(\d+)\b", listing):
             assert 4 <= int(v) < top
+            assert not X <= int(v) < X + 2 * P or int(v) in pos, (gi, d, S, P, Wn, v)
+        for op, dst, srcs in _writes(listing):
+            assert not X <= dst < X + 2 * P, (gi, d, S, P, Wn, op, dst)
         for s in re.findall(r"\bs(\d+)\b", listing):
             assert 40 <= int(s) <= 59
         for a, b in re.findall(r"s\[(\d+):(\d+)\]", listing):
