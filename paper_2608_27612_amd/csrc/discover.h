@@ -222,6 +222,17 @@ __device__ __forceinline__ void store_chunk_counts(const DiscoverPtrs& d, const 
   for (int s = 0; s < S; ++s)
     if ((lane >> 4) == (uint32_t)s && chunk_tile + k < chunk_end)
       d.status[(int64_t)G.pair[s] * a.tiles + chunk_tile + k] = (uint64_t)counts;
+  // A chunk (a whole number of chunks fills a group of 64 tiles) that kept a cell marks its
+  // group, so that the compaction of a long range visits only the groups with records.
+  if (a.tiles > kNzMinGroups * kWave) {
+    const uint64_t kept = ballot(counts != 0u);
+    const uint32_t g = chunk_tile / kWave;
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+      if (lane == 0 && ((kept >> (16 * s)) & 0xFFFFull) != 0ull)
+        atomicOr((unsigned long long*)(a.nz + (int64_t)G.pair[s] * a.nz_words + g / 64u),
+                 1ull << (g % 64u));
+  }
 }
 
 // One chunk (chunk_tiles consecutive tiles of one group) of a part with S sources per walk. A lane

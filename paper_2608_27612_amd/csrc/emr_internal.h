@@ -179,6 +179,10 @@ struct DiscoverScalars {
   int32_t depth;
   float theta16;  // 16 theta
   uint32_t code_bytes;  // compiled tier: size of the code area (0 for the interpreter)
+  // Padded placement over more than 2 groups of 64 tiles: bit g % 64 of nz[pair * nz_words +
+  // g / 64] marks a group g of the range that kept a cell (k_compact visits only those).
+  uint64_t* nz;
+  uint32_t nz_words;
   uint32_t blob_words, n_pairs;
   uint32_t bias_floats;  // the host keeps the bias table below 2^32 floats
   uint32_t head_parents;  // parents in a pair's tile 0 (levels 1..3, or all levels of a shallower grid)
@@ -231,6 +235,10 @@ EMR_HD constexpr int jit_temps(int S, int P, int W) {
 
 // Tiles of one chunk at most (a chunk's record counts are held one per lane, 16 per source).
 constexpr uint32_t kChunkTilesMax = 16;
+// Group marks of the padded placement: a range of more than kNzMinGroups groups of 64 tiles has
+// nz_words(tiles) words of marks per pair, one bit per group.
+constexpr uint32_t kNzMinGroups = 2;
+EMR_HD constexpr uint32_t nz_words(uint32_t tiles) { return ((tiles + 63u) / 64u + 63u) / 64u; }
 // Rows of zeros after the last tile of the tile geometry table: a walk of TPW <= 4 tiles loads
 // the next walk's TPW rows, up to 2 TPW - 1 rows past its first tile, with no bound per load.
 constexpr uint32_t kGeoPadRows = 8;
@@ -242,6 +250,7 @@ struct DiscoverArgs {
   const Group* groups;     // the plan's group table (parts index into it)
   const float* bias_tab;
   uint64_t* status;        // [n_pairs_total * tiles]
+  uint64_t* nz;            // padded placement: group marks (DiscoverScalars::nz)
   uint32_t* err;           // device error flags
   uint32_t* parent;
   float* w4;
@@ -275,6 +284,8 @@ struct BindArgs {
   uint32_t n_sources;
   uint32_t blob_words;
   uint64_t bias_floats;
+  uint64_t* nz;            // the compaction's group marks, cleared by the bind kernel
+  uint32_t nz_words;
 };
 
 }  // namespace emr

@@ -66,37 +66,45 @@ __device__ __forceinline__ uint32_t tile_parent_offset(uint32_t T) {
 }
 
 // Compaction of one pair by one wave, once every tile of the range has left its records at the
-// tile's own slots and its count in counts[pair * tiles + t]: scans the counts, 64 tiles at a time,
-// and moves the records down to their final, contiguous place, then writes the pair's count and
-// returns it.
+// tile's own slots and its count in counts[pair * tiles + t]. The tiles go in groups of 64 in
+// increasing order: a group's counts are scanned and its records moved down to their final,
+// contiguous place. A range of more than two groups visits only the groups whose bit the discover
+// kernel set in the pair's words of `nz` (a group that kept nothing has no records to move), and
+// clears those words for the next range. Writes the pair's count and returns it.
 __device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
                                  float* __restrict__ w4, int64_t* __restrict__ pair_count,
-                                 int64_t cap, uint32_t tile_lo, uint32_t tiles, uint32_t pair,
-                                 uint32_t head_slots, uint32_t lane) {
+                                 uint64_t* __restrict__ nz, int64_t cap, uint32_t tile_lo,
+                                 uint32_t tiles, uint32_t pair, uint32_t head_slots,
+                                 uint32_t lane) {
   const uint32_t parent_lo = tile_parent_offset(tile_lo);
   const uint64_t* row = counts + (int64_t)pair * tiles;
   const int64_t region = (int64_t)pair * cap;
+  const uint32_t n_groups = (tiles + kWave - 1) / kWave;
   uint32_t running = 0;
-  for (uint32_t t0 = 0; t0 < tiles; t0 += kWave) {
-    // a tile holds at most its own slot count (64, or the head tile's parents)
-    const uint32_t t_lane = t0 + lane;
+  // lane's tile count in group g (a tile holds at most its own slot count: 64, or the head
+  // tile's parents)
+  auto load_count = [&](uint32_t g) -> uint32_t {
+    const uint32_t t_lane = g * kWave + lane;
     const uint32_t slots = tile_lo + t_lane == 0 ? head_slots : (uint32_t)(kTile / 4);
-    const uint32_t c = t_lane < tiles ? min((uint32_t)row[t_lane], slots) : 0u;
+    return t_lane < tiles ? min((uint32_t)row[t_lane], slots) : 0u;
+  };
+  auto group = [&](uint32_t g, uint32_t c) {
+    const uint32_t t0 = g * kWave;
     // inclusive scan over the wave, bit-sliced: c < 128, so the counts of the lanes below are
     // the sum over bits b of 2^b times the number of lanes below with bit b set (mbcnt)
     uint32_t incl = c;
 #pragma unroll
     for (int b = 0; b < 7; ++b) incl += mbcnt64(ballot((c >> b) & 1u)) << b;
-    // These tiles' records in batches of 64, lane l moving the batch's l-th record: its tile is
+    // The group's records in batches of 64, lane l moving the batch's l-th record: its tile is
     // the one (among the tiles with records) whose scan range holds it. A batch's loads all come
     // before its stores, and no record moves up, so a batch never overwrites a later batch's
     // records before they are read.
     const uint32_t total = __builtin_amdgcn_readlane(incl, kWave - 1);
-    const uint64_t nz = ballot(c != 0u);
+    const uint64_t has = ballot(c != 0u);
     for (uint32_t b = 0; b < total; b += kWave) {
-      const uint32_t q = b + lane;  // the record's rank among these tiles' records
+      const uint32_t q = b + lane;  // the record's rank among the group's records
       uint32_t src = running + q;
-      for (uint64_t m = nz; m != 0ull; m &= m - 1ull) {
+      for (uint64_t m = has; m != 0ull; m &= m - 1ull) {
         const uint32_t i = (uint32_t)__builtin_ctzll(m);
         const uint32_t hi = __builtin_amdgcn_readlane(incl, i);
         const uint32_t lo = hi - __builtin_amdgcn_readlane(c, i);
@@ -111,6 +119,45 @@ __device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* 
       }
     }
     running += total;
+  };
+  if (n_groups <= kNzMinGroups) {
+    // both groups' counts are requested before either is scanned
+    const uint32_t c0 = load_count(0), c1 = n_groups > 1 ? load_count(1) : 0u;
+    if (n_groups > 0) group(0, c0);
+    if (n_groups > 1) group(1, c1);
+  } else {
+    const uint32_t n_words = nz_words(tiles);
+    uint64_t* words = nz + (int64_t)pair * n_words;
+    for (uint32_t w0 = 0; w0 < n_words; w0 += kWave) {
+      const bool mine = w0 + lane < n_words;
+      const uint64_t bits = mine ? words[w0 + lane] : 0ull;
+      if (mine && bits != 0ull) words[w0 + lane] = 0ull;
+      // the marked groups of these words in increasing order (all values wave-uniform); each
+      // group's counts are requested before the previous group is compacted
+      uint64_t lanes = ballot(bits != 0ull), bw = 0ull;
+      uint32_t i = 0;
+      auto next = [&]() -> uint32_t {  // the next marked group, or ~0u
+        while (bw == 0ull) {
+          if (lanes == 0ull) return 0xFFFFFFFFu;
+          i = (uint32_t)__builtin_ctzll(lanes);
+          lanes &= lanes - 1ull;
+          bw = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(bits >> 32), i) << 32) |
+               __builtin_amdgcn_readlane((uint32_t)bits, i);
+        }
+        const uint32_t j = (uint32_t)__builtin_ctzll(bw);
+        bw &= bw - 1ull;
+        return (w0 + i) * kWave + j;
+      };
+      uint32_t g = next();
+      uint32_t c = g < n_groups ? load_count(g) : 0u;
+      while (g != 0xFFFFFFFFu) {
+        const uint32_t g2 = next();
+        const uint32_t c2 = g2 < n_groups ? load_count(g2) : 0u;
+        if (g < n_groups) group(g, c);
+        g = g2;
+        c = c2;
+      }
+    }
   }
   if (lane == 0) pair_count[pair] = running;
   return running;
@@ -124,8 +171,8 @@ constexpr int kCompactWaves = 4;
 __global__ void __launch_bounds__(kCompactWaves * kWave)
     k_compact(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
               float* __restrict__ w4, int64_t* __restrict__ pair_count,
-              uint32_t* __restrict__ max_count, int64_t cap, uint32_t tile_lo, uint32_t tiles,
-              uint32_t n_pairs, uint32_t head_slots) {
+              uint32_t* __restrict__ max_count, uint64_t* __restrict__ nz, int64_t cap,
+              uint32_t tile_lo, uint32_t tiles, uint32_t n_pairs, uint32_t head_slots) {
   __shared__ uint32_t wave_max[kCompactWaves];
   const uint32_t lane = lane_id();
   const uint32_t wv = threadIdx.x / kWave;
@@ -133,8 +180,8 @@ __global__ void __launch_bounds__(kCompactWaves * kWave)
   uint32_t my_max = 0;
   for (uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * kCompactWaves + wv);
        pair < n_pairs; pair += n_waves) {
-    my_max = max(my_max, compact_pair(counts, parent, w4, pair_count, cap, tile_lo, tiles, pair,
-                                      head_slots, lane));
+    my_max = max(my_max, compact_pair(counts, parent, w4, pair_count, nz, cap, tile_lo, tiles,
+                                      pair, head_slots, lane));
   }
   if (lane == 0) wave_max[wv] = my_max;
   __syncthreads();
@@ -191,9 +238,13 @@ __global__ void __launch_bounds__(kBindWaves * kWave)
     k_bind(const uint32_t* __restrict__ blob, const ProgDesc* __restrict__ desc,
            const Member* __restrict__ members, const float* __restrict__ src_xy,
            float* __restrict__ bias_tab, uint32_t* __restrict__ err, uint32_t n_members,
-           uint32_t n_desc, uint32_t n_sources, uint32_t blob_words, uint64_t bias_floats) {
+           uint32_t n_desc, uint32_t n_sources, uint32_t blob_words, uint64_t bias_floats,
+           uint64_t* __restrict__ nz, uint32_t nz_words) {
   __shared__ float U_all[kBindWaves][kMaxU];
   __shared__ uint32_t prog_all[kBindWaves][kBindProgWords];
+  // the compaction's group marks start out clear (the discover kernel sets them)
+  for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < nz_words; k += gridDim.x * blockDim.x)
+    nz[k] = 0ull;
   const uint32_t lane = lane_id();
   const uint32_t wv = threadIdx.x / kWave;
   const uint32_t i = __builtin_amdgcn_readfirstlane(blockIdx.x * kBindWaves + wv);
@@ -369,7 +420,7 @@ extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
   hipLaunchKernelGGL(emr::k_bind, dim3((a->n_members + emr::kBindWaves - 1) / emr::kBindWaves),
                      dim3(emr::kBindWaves * emr::kWave), 0, s, a->blob, a->desc,
                      a->members, a->src_xy, a->bias_tab, a->err, a->n_members, a->n_desc,
-                     a->n_sources, a->blob_words, a->bias_floats);
+                     a->n_sources, a->blob_words, a->bias_floats, a->nz, a->nz_words);
   return hipGetLastError();
 }
 
@@ -419,6 +470,8 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   sc.depth = a->depth;
   sc.theta16 = 16.0f * a->theta;
   sc.code_bytes = 0;
+  sc.nz = a->nz;
+  sc.nz_words = emr::nz_words(a->tiles);
   sc.blob_words = a->blob_words;
   sc.n_pairs = a->n_pairs;
   sc.bias_floats = (uint32_t)a->bias_floats;
@@ -512,14 +565,14 @@ extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* p
 }
 
 extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
-                                         int64_t* pair_count, uint32_t* max_count, int64_t cap,
-                                         uint32_t tile_lo, uint32_t tiles, uint32_t n_pairs,
-                                         uint32_t head_slots, hipStream_t s) {
+                                         int64_t* pair_count, uint32_t* max_count, uint64_t* nz,
+                                         int64_t cap, uint32_t tile_lo, uint32_t tiles,
+                                         uint32_t n_pairs, uint32_t head_slots, hipStream_t s) {
   if (n_pairs == 0) return hipSuccess;
   uint32_t blocks = (n_pairs + emr::kCompactWaves - 1) / emr::kCompactWaves;
-  if (blocks > 1024) blocks = 1024;  // waves loop over pairs beyond this
+  if (blocks > 8192) blocks = 8192;  // waves loop over pairs beyond this
   hipLaunchKernelGGL(emr::k_compact, dim3(blocks), dim3(emr::kCompactWaves * emr::kWave), 0, s,
-                     counts, parent, w4, pair_count, max_count, cap, tile_lo, tiles, n_pairs,
+                     counts, parent, w4, pair_count, max_count, nz, cap, tile_lo, tiles, n_pairs,
                      head_slots);
   return hipGetLastError();
 }

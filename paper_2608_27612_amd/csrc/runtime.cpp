@@ -27,9 +27,9 @@ extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s);
 extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int mode, uint32_t blocks,
                                           hipStream_t s, hipEvent_t start, hipEvent_t stop);
 extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
-                                         int64_t* pair_count, uint32_t* max_count, int64_t cap,
-                                         uint32_t tile_lo, uint32_t tiles, uint32_t n_pairs,
-                                         uint32_t head_slots, hipStream_t s);
+                                         int64_t* pair_count, uint32_t* max_count, uint64_t* nz,
+                                         int64_t cap, uint32_t tile_lo, uint32_t tiles,
+                                         uint32_t n_pairs, uint32_t head_slots, hipStream_t s);
 extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
                                         const float* w4, int64_t cap, uint32_t n_pairs,
                                         uint32_t* out_parent, float* out_w4, hipStream_t s);
@@ -243,6 +243,7 @@ struct Plan {
   size_t off_status = 0;
   size_t off_bias = 0, total = 0;
   size_t status_bytes = 0;  // cleared before a call only for look-back placement
+  size_t off_nz = 0, nz_bytes = 0;  // the compaction's group marks (cleared by k_bind)
 };
 
 emr_status build_plan(const emr_population* pop, const emr_source* sources, int32_t n_sources,
@@ -376,7 +377,9 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
   P.off_err = 0;
   P.off_status = 256;
   P.status_bytes = (size_t)P.n_pairs * P.tiles * 8;
-  P.off_bias = align256(P.off_status + P.status_bytes);
+  P.off_nz = align256(P.off_status + P.status_bytes);
+  P.nz_bytes = (size_t)P.n_pairs * emr::nz_words((uint32_t)P.tiles) * 8;
+  P.off_bias = align256(P.off_nz + P.nz_bytes);
   // 16 floats of padding after the bias table: the compiled tier loads a group's rows 1 .. 4 at once
   P.total = align256(P.off_bias + (P.bias_floats + 16) * sizeof(float));
   // tables
@@ -504,6 +507,8 @@ emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspac
   b.n_sources = (uint32_t)(P.src_xy.size() / 2);
   b.blob_words = (uint32_t)pop->blob_words;
   b.bias_floats = P.bias_floats;
+  b.nz = (uint64_t*)(ws + P.off_nz);
+  b.nz_words = (uint32_t)(P.nz_bytes / 8);
   HIP_OR_FAIL(emr_launch_bind(&b, s));
   return EMR_OK;
 }
@@ -530,8 +535,9 @@ emr_status tile_geo_table(int depth, const uint32_t** out, uint32_t* rows) {
     return fail(EMR_E_NOMEM, "tile geometry table of %lld rows", (long long)n);
   StreamPool* sp = nullptr;
   emr_status st = stream_pool(&sp);
-  if (st == EMR_OK && (emr_launch_tile_geo(d, (uint32_t)tiles, (uint32_t)n, sp->aux[0]) != hipSuccess ||
-                       hipStreamSynchronize(sp->aux[0]) != hipSuccess))
+  if (st == EMR_OK &&
+      (emr_launch_tile_geo(d, (uint32_t)tiles, (uint32_t)n, sp->aux[0]) != hipSuccess ||
+       hipStreamSynchronize(sp->aux[0]) != hipSuccess))
     st = fail(EMR_E_DEVICE, "building the tile geometry table failed");
   if (st != EMR_OK) {
     (void)hipFree(d);
@@ -783,6 +789,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
     a.groups = jit ? P.jit->d_groups : (const emr::Group*)(tables + P.t_groups);
     a.bias_tab = (const float*)(ws + P.off_bias);
     a.status = (uint64_t*)(ws + P.off_status);
+    a.nz = (uint64_t*)(ws + P.off_nz);
     a.err = (uint32_t*)(ws + P.off_err);
     a.parent = out ? out->parent : nullptr;
     a.w4 = out ? out->w4 : nullptr;
@@ -835,7 +842,8 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
   if (padded && P.n_pairs > 0)
     HIP_OR_FAIL(emr_launch_compact(
         (const uint64_t*)(ws + P.off_status), out->parent, out->w4, out->pair_count,
-        (uint32_t*)(ws + P.off_err) + 1, out->pair_capacity, (uint32_t)tile_lo, (uint32_t)n_tiles,
+        (uint32_t*)(ws + P.off_err) + 1, (uint64_t*)(ws + P.off_nz), out->pair_capacity,
+        (uint32_t)tile_lo, (uint32_t)n_tiles,
         (uint32_t)P.n_pairs,
         (uint32_t)(P.depth < emr::kFirstAlignedLevel ? emr::n_parents(P.depth)
                                                      : emr::level_offset(emr::kFirstAlignedLevel) / 4),

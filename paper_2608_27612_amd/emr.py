@@ -230,11 +230,21 @@ def emr_pack_population(genomes, layout: str = "flat") -> Population:
 
 # ----------------------------------------------------------------------------- discovery
 
+# numpy records with emr_source's layout (12 bytes: float x, float y, int32 dir)
+SOURCE_DTYPE = np.dtype([("x", "<f4"), ("y", "<f4"), ("dir", "<i4")])
+_NO_SOURCE = np.zeros(1, SOURCE_DTYPE)
+
+
 def _sources(sources):
-    arr = (emr_source * max(1, len(sources)))()
-    for i, s in enumerate(sources):
-        arr[i] = emr_source(float(s["x"]), float(s["y"]), int(s["dir"]))
-    return arr
+    """The sources as a contiguous array of emr_source records: an array of SOURCE_DTYPE is
+    passed as it is (no per-call conversion); anything else indexable by "x", "y", "dir" is
+    converted. Keep the returned array alive until the call that gets its address returns."""
+    if isinstance(sources, np.ndarray) and sources.dtype == SOURCE_DTYPE:
+        arr = sources if sources.flags.c_contiguous else np.ascontiguousarray(sources)
+    else:
+        arr = np.array([(float(s["x"]), float(s["y"]), int(s["dir"])) for s in sources],
+                       dtype=SOURCE_DTYPE)
+    return arr if len(arr) else _NO_SOURCE
 
 
 def _offsets(src_offsets):
@@ -250,7 +260,8 @@ def n_pairs_of(pop: Population, sources, src_offsets=None) -> int:
 def emr_workspace_bytes(pop: Population, sources, depth: int, src_offsets=None) -> int:
     offs = _offsets(src_offsets)
     b = C.c_int64()
-    _check(lib().emr_workspace_bytes(pop.handle, _sources(sources), len(sources),
+    src = _sources(sources)
+    _check(lib().emr_workspace_bytes(pop.handle, src.ctypes.data, len(sources),
                                      None if offs is None else offs.ctypes.data,
                                      0 if offs is not None else len(sources), depth, C.byref(b)))
     return b.value
@@ -291,7 +302,8 @@ def emr_discover(pop: Population, sources, depth: int, theta: float, res=None, s
     offs = _offsets(src_offsets)
     out = _result_struct(res)
     res["_struct"] = out
-    _check(lib().emr_discover(pop.handle, _sources(sources), len(sources),
+    src = _sources(sources)
+    _check(lib().emr_discover(pop.handle, src.ctypes.data, len(sources),
                               None if offs is None else offs.ctypes.data,
                               0 if offs is not None else len(sources), depth,
                               C.c_float(theta), C.byref(out), _stream_ptr(stream)))
@@ -315,7 +327,8 @@ def emr_eval_raw(pop: Population, sources, depth: int, src_offsets=None, stream=
     ws_bytes = emr_workspace_bytes(pop, sources, depth, src_offsets)
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
     offs = _offsets(src_offsets)
-    _check(lib().emr_eval_raw(pop.handle, _sources(sources), len(sources),
+    src = _sources(sources)
+    _check(lib().emr_eval_raw(pop.handle, src.ctypes.data, len(sources),
                               None if offs is None else offs.ctypes.data,
                               0 if offs is not None else len(sources), depth,
                               C.c_void_p(out.data_ptr() if out.numel() else 0),
@@ -328,7 +341,8 @@ def emr_discover_cost(pop: Population, sources, depth: int, src_offsets=None,
     """(algorithmic VALU slots, queries) of one discover call under the cost model."""
     offs = _offsets(src_offsets)
     slots, queries = C.c_double(), C.c_double()
-    _check(lib().emr_discover_cost(pop.handle, _sources(sources), len(sources),
+    src = _sources(sources)
+    _check(lib().emr_discover_cost(pop.handle, src.ctypes.data, len(sources),
                                    None if offs is None else offs.ctypes.data,
                                    0 if offs is not None else len(sources), depth,
                                    float(transcendental_slots), C.byref(slots), C.byref(queries)))
@@ -423,7 +437,8 @@ def emr_discover_stream(pop: Population, sources, depth: int, theta: float, sink
 
     cb = SINK(_sink)
     nxt = C.c_int64(start)
-    st = lib().emr_discover_stream(pop.handle, _sources(sources), len(sources),
+    src = _sources(sources)
+    st = lib().emr_discover_stream(pop.handle, src.ctypes.data, len(sources),
                                    None if offs is None else offs.ctypes.data,
                                    0 if offs is not None else len(sources), depth,
                                    C.c_float(theta), chunk_positions, start, cb, None,

@@ -63,7 +63,7 @@ def test_discover_rejects_null_population():
     L = emr.lib()
     res = emr.emr_result()
     src = emr._sources(W.xor_sources())
-    st = L.emr_discover(None, src, 4, None, 4, 5, C.c_float(0.03), C.byref(res), None)
+    st = L.emr_discover(None, src.ctypes.data, 4, None, 4, 5, C.c_float(0.03), C.byref(res), None)
     assert st == emr.EMR_E_INVAL
     assert b"population" in L.emr_last_error()
     st = L.emr_build_grids(-3, None, None)

@@ -327,6 +327,37 @@ def test_config2_xor_pop1000_full(emr, D):
     assert st["records"] > 0
 
 
+
+def test_compaction_over_many_tile_groups_sparse(emr):
+    """Depth 8 (342 tiles per pair: the compaction visits only the groups of 64 tiles that the
+    discover kernel marked), a population against the oracle."""
+    genomes = W.population(31, 24, 20, 60)
+    st = check_discover(emr, genomes, W.xor_sources(), 8, 0.03)
+    assert st["records"] > 0
+
+
+def test_compaction_over_many_tile_groups_dense(emr):
+    """Depth 8 with theta < 0: every group of every pair is marked and every cell kept, so the
+    records of each pair are its raw outputs in parent order, bit for bit; a second call on the
+    same result (marks cleared and set again) gives the same records."""
+    genomes = W.population(32, 3, 20, 60)
+    sources = W.xor_sources()
+    D = 8
+    Q = oracle.n_parents(D)
+    pop = emr.emr_pack_population(genomes)
+    raw = emr.emr_eval_raw(pop, sources, D).cpu().numpy()
+    res = emr.alloc_result(pop, sources, D)
+    for call in range(2):
+        emr.emr_discover(pop, sources, D, -1.0, res=res)
+        assert emr.emr_result_check(res) == Q
+        counts, recs = emr.records_to_host(res)
+        assert np.all(counts == Q)
+        for r in range(len(counts)):
+            gp, gw = recs[r]
+            assert np.array_equal(gp, np.arange(Q)), (call, r)
+            assert np.array_equal(gw.reshape(-1).view(np.uint32), raw[r].view(np.uint32)), (call, r)
+
+
 def test_config3_tabular_pop150_full(emr):
     """The tabular workload: 150 genomes (up to 40 hidden nodes, 120 edges) x 33 sources at depth
     6, every pair."""
