@@ -96,8 +96,8 @@ def cpu_baseline(genomes, sources, depth, theta32, target_s):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="xor_pop1000_d7")
     ap.add_argument("--transcendental-slots", type=float, default=4.0)
     ap.add_argument("--gens", type=int, default=5, help="generations timed for ms_per_gen")

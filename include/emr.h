@@ -178,11 +178,14 @@ emr_status emr_discover(const emr_population* pop, const emr_source* sources, in
                         const int32_t* src_offsets, int32_t n_shared, int32_t depth, float theta,
                         const emr_result* out, void* stream);
 
-/* Synchronizes `stream`, then reports EMR_E_CAPACITY if any pair_count exceeds pair_capacity
- * (*max_count receives the largest count, so a retry can size the regions), or EMR_E_DEVICE if
- * the kernel flagged an internal error. n_pairs is the number of pairs of the discover call.
- * The flags and the largest count are read from the workspace of `out` (the discover call
- * leaves them there); without a workspace the counts themselves are read. */
+/* Waits for the latest discover (or raw-output) call made with out's workspace on the current
+ * device, then reports EMR_E_CAPACITY if any pair_count exceeds pair_capacity (*max_count
+ * receives the largest count, so a retry can size the regions), or EMR_E_DEVICE if a kernel
+ * flagged an internal error. n_pairs is the number of pairs of the call; `stream` is not used
+ * (the call's own completion is waited for, not the stream's later work). A call's flags live in
+ * a library-owned ring of 256 slots per device, written by the call's last kernel straight to
+ * pinned memory: a result is checked before 255 further calls on its device, and EMR_E_INVAL
+ * reports a workspace with no call to check. */
 emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max_count,
                             void* stream);
 

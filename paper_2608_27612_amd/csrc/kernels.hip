@@ -163,6 +163,19 @@ __device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* 
   return running;
 }
 
+// The call's last kernel: its flags (error bits in flags[0], largest pair count in flags[1],
+// raised with device-scope atomics by the call's other kernels; zero when the call starts) go to
+// its pinned host words and are cleared for the slot's next call.
+__global__ void k_finalize(uint32_t* flags, uint32_t* host) {
+  if (blockIdx.x != 0 || threadIdx.x != 0) return;
+  const uint32_t e = __hip_atomic_load(flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint32_t m = __hip_atomic_load(flags + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  host[0] = e;
+  host[1] = m;
+  __hip_atomic_store(flags, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(flags + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Each wave takes pairs pair = wave, wave + n_waves, ...: compacts them once every discover launch
 // of the range has finished, and the workgroup's largest count is raised into *max_count with one
 // atomic.
@@ -574,5 +587,10 @@ extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* paren
   hipLaunchKernelGGL(emr::k_compact, dim3(blocks), dim3(emr::kCompactWaves * emr::kWave), 0, s,
                      counts, parent, w4, pair_count, max_count, nz, cap, tile_lo, tiles, n_pairs,
                      head_slots);
+  return hipGetLastError();
+}
+
+extern "C" hipError_t emr_launch_finalize(uint32_t* flags, uint32_t* host, hipStream_t s) {
+  hipLaunchKernelGGL(emr::k_finalize, dim3(1), dim3(64), 0, s, flags, host);
   return hipGetLastError();
 }

@@ -30,6 +30,7 @@ extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* paren
                                          int64_t* pair_count, uint32_t* max_count, uint64_t* nz,
                                          int64_t cap, uint32_t tile_lo, uint32_t tiles,
                                          uint32_t n_pairs, uint32_t head_slots, hipStream_t s);
+extern "C" hipError_t emr_launch_finalize(uint32_t* flags, uint32_t* host, hipStream_t s);
 extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
                                         const float* w4, int64_t cap, uint32_t n_pairs,
                                         uint32_t* out_parent, float* out_w4, hipStream_t s);
@@ -170,20 +171,22 @@ struct JitModule {
   int per_cu[3] = {1, 1, 1};  // workgroups per CU of each
   uint32_t code_bytes = 0;    // size of the code area
   emr::Group* d_groups = nullptr;  // the plan's group table with the code offsets
-  hipEvent_t last = nullptr;  // recorded after every launch from the module
   size_t programs = 0, program_bytes = 0, image_bytes = 0;
   double compile_ms = 0.0, load_ms = 0.0;
   JitModule() = default;
   JitModule(const JitModule&) = delete;
   JitModule& operator=(const JitModule&) = delete;
   ~JitModule() {
-    // nothing queued may still run the module's code or read its tables
-    if (last) {
-      (void)hipEventSynchronize(last);
-      (void)hipEventDestroy(last);
-    }
+    // Nothing queued may still run the module's code or read its tables, so the device drains
+    // first (a module goes only when its plan is replaced or its population freed).
+    if (!mod && !d_groups) return;
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    if (device >= 0 && cur != device) (void)hipSetDevice(device);
+    (void)hipDeviceSynchronize();
     if (d_groups) (void)hipFree(d_groups);
     if (mod) (void)hipModuleUnload(mod);
+    if (device >= 0 && cur >= 0 && cur != device) (void)hipSetDevice(cur);
   }
 };
 
@@ -224,7 +227,7 @@ struct Plan {
   Plan(const Plan&) = delete;
   Plan& operator=(const Plan&) = delete;
   ~Plan() {
-    jit.reset();  // waits for the compiled tier's last launch
+    jit.reset();  // drains the device before the compiled tier's module goes
     if (d_tables) (void)hipFree(d_tables);
   }
   // The compiled tier (jit_use): built at most once per plan, under jit_mu.
@@ -239,7 +242,6 @@ struct Plan {
   bool key_has_offs = false;
   int32_t key_n_shared = 0;
   // Workspace layout (bytes from the workspace start).
-  size_t off_err = 0;      // 64 words: [0] error flags, [1] largest pair count (saturating)
   size_t off_status = 0;
   size_t off_bias = 0, total = 0;
   size_t status_bytes = 0;  // cleared before a call only for look-back placement
@@ -374,8 +376,7 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
   }
 
   // workspace: flags, tile status words, bias rows
-  P.off_err = 0;
-  P.off_status = 256;
+  P.off_status = 0;
   P.status_bytes = (size_t)P.n_pairs * P.tiles * 8;
   P.off_nz = align256(P.off_status + P.status_bytes);
   P.nz_bytes = (size_t)P.n_pairs * emr::nz_words((uint32_t)P.tiles) * 8;
@@ -461,26 +462,113 @@ emr_status plan_tables(const Plan& P, char** out) {
   return EMR_OK;
 }
 
-// 256 zero bytes in pinned memory (clears a workspace's flags with one async copy).
-emr_status zero_block(const void** out) {
-  static void* z = nullptr;
-  static std::mutex mu;
-  std::lock_guard<std::mutex> lock(mu);
-  if (!z) {
-    if (hipHostMalloc(&z, 256, hipHostMallocDefault) != hipSuccess) {
-      z = nullptr;
-      return fail(EMR_E_NOMEM, "pinned zero block");
+// ------------------------------------------------------------------ call flags
+// Each call's kernels raise their error bits (word 0) and largest pair count (word 1) into a slot
+// of a library-owned ring in device memory. A slot is zero when a call takes it; the call's last
+// kernel, k_finalize, writes the words to the slot's pinned host words and clears them again. So
+// no copy of the flags goes either way, and the caller's workspace keeps no state from one call
+// to the next.
+constexpr int kFlagSlots = 256;
+constexpr int kSlotWords = 16;  // [0] errors, [1] largest count
+
+struct FlagRing {
+  uint32_t* dev = nullptr;
+  uint32_t* host = nullptr;      // pinned (host view)
+  uint32_t* host_dev = nullptr;  // the same words, device view
+  hipEvent_t done[kFlagSlots] = {};
+  const void* ws[kFlagSlots] = {};  // workspace of the slot's last call (NULL: nothing to check)
+  uint64_t seq[kFlagSlots] = {};    // order of the calls
+  bool pending[kFlagSlots] = {};    // done[k] is recorded after the slot's last call
+  bool dirty[kFlagSlots] = {};      // a call failed after taking the slot: cleared before reuse
+  int next = 0;
+  uint64_t calls = 0;
+};
+std::mutex g_ring_mu;
+std::vector<std::pair<int, FlagRing*>> g_rings;  // one per device, kept for the process
+
+// The ring of the current device (g_ring_mu held).
+emr_status flag_ring(FlagRing** out) {
+  int dev = 0;
+  HIP_OR_FAIL(hipGetDevice(&dev));
+  for (const auto& e : g_rings)
+    if (e.first == dev) {
+      *out = e.second;
+      return EMR_OK;
     }
-    std::memset(z, 0, 256);
+  std::unique_ptr<FlagRing> R(new FlagRing());
+  const size_t bytes = (size_t)kFlagSlots * kSlotWords * 4;
+  if (hipMalloc((void**)&R->dev, bytes) != hipSuccess) return fail(EMR_E_NOMEM, "flag slots");
+  if (hipMemset(R->dev, 0, bytes) != hipSuccess ||
+      hipHostMalloc((void**)&R->host, bytes, hipHostMallocDefault) != hipSuccess) {
+    (void)hipFree(R->dev);
+    return fail(EMR_E_NOMEM, "flag slots");
   }
-  *out = z;
+  std::memset(R->host, 0, bytes);
+  if (hipHostGetDevicePointer((void**)&R->host_dev, R->host, 0) != hipSuccess)
+    return fail(EMR_E_DEVICE, "device view of the pinned flag words");
+  for (int k = 0; k < kFlagSlots; ++k)
+    HIP_OR_FAIL(hipEventCreateWithFlags(&R->done[k], hipEventDisableTiming));
+  g_rings.push_back({dev, R.get()});
+  *out = R.release();
   return EMR_OK;
 }
 
-// Clears the workspace's flags (and its tile status words when the look-back placement needs
-// them) and runs the bind kernel over the plan's tables.
+// One call's slot: taken before its first kernel, given back after its last (or on failure).
+struct CallFlags {
+  FlagRing* ring = nullptr;
+  int slot = -1;
+  uint32_t* dev = nullptr;       // the device words the kernels raise into
+  uint32_t* host = nullptr;      // the pinned words (host view)
+  uint32_t* host_dev = nullptr;  // the pinned words (device view)
+  hipStream_t s = nullptr;
+  const void* ws = nullptr;
+  bool ok = false;  // the call's last kernel is enqueued
+  CallFlags() = default;
+  CallFlags(const CallFlags&) = delete;
+  CallFlags& operator=(const CallFlags&) = delete;
+  ~CallFlags() {
+    if (!ring) return;
+    std::lock_guard<std::mutex> lock(g_ring_mu);
+    // the slot's next user waits for whatever this call enqueued
+    ring->pending[slot] = hipEventRecord(ring->done[slot], s) == hipSuccess;
+    ring->ws[slot] = ok ? ws : nullptr;
+    ring->seq[slot] = ++ring->calls;
+    ring->dirty[slot] = !ok;
+  }
+};
+
+emr_status take_flags(const void* workspace, hipStream_t s, CallFlags* f) {
+  std::lock_guard<std::mutex> lock(g_ring_mu);
+  FlagRing* R = nullptr;
+  emr_status st = flag_ring(&R);
+  if (st != EMR_OK) return st;
+  const int k = R->next;
+  R->next = (k + 1) % kFlagSlots;
+  // the slot's previous call (kFlagSlots calls ago) must have finished with its words
+  if (R->pending[k]) HIP_OR_FAIL(hipEventSynchronize(R->done[k]));
+  R->pending[k] = false;
+  R->ws[k] = nullptr;
+  f->ring = R;
+  f->slot = k;
+  f->dev = R->dev + (size_t)k * kSlotWords;
+  f->host = R->host + (size_t)k * kSlotWords;
+  f->host_dev = R->host_dev + (size_t)k * kSlotWords;
+  f->s = s;
+  f->ws = workspace;
+  f->host[0] = 0u;
+  f->host[1] = 0u;
+  if (R->dirty[k]) {
+    HIP_OR_FAIL(emr_launch_fill(f->dev, kSlotWords, 0u, s));
+    R->dirty[k] = false;
+  }
+  return EMR_OK;
+}
+
+// Clears the workspace's tile status words when the look-back placement needs them, and runs the
+// bind kernel over the plan's tables.
 emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspace,
-                        int64_t workspace_bytes, hipStream_t s, bool clear_status) {
+                        int64_t workspace_bytes, hipStream_t s, bool clear_status,
+                        uint32_t* flags) {
   if (!workspace || workspace_bytes < (int64_t)P.total)
     return fail(EMR_E_INVAL, "workspace of %lld bytes is smaller than the %zu needed",
                 (long long)workspace_bytes, P.total);
@@ -489,9 +577,6 @@ emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspac
   char* tables = nullptr;
   emr_status st = plan_tables(P, &tables);
   if (st != EMR_OK) return st;
-  const void* zeros = nullptr;
-  if ((st = zero_block(&zeros)) != EMR_OK) return st;
-  HIP_OR_FAIL(hipMemcpyAsync(ws + P.off_err, zeros, 256, hipMemcpyHostToDevice, s));
   if (clear_status)
     HIP_OR_FAIL(emr_launch_fill(ws + P.off_status, (int64_t)(P.status_bytes / 4), 0u, s));
 
@@ -501,7 +586,7 @@ emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspac
   b.members = (const emr::Member*)(tables + P.t_members);
   b.src_xy = (const float*)(tables + P.t_srcxy);
   b.bias_tab = (float*)(ws + P.off_bias);
-  b.err = (uint32_t*)(ws + P.off_err);
+  b.err = flags;
   b.n_members = (uint32_t)P.members.size();
   b.n_desc = (uint32_t)pop->desc.size();
   b.n_sources = (uint32_t)(P.src_xy.size() / 2);
@@ -653,7 +738,6 @@ emr_status jit_build(const emr_population* pop, const Plan& P, std::unique_ptr<J
     HIP_OR_FAIL(hipMemcpy(M->d_groups, groups.data(), groups.size() * sizeof(emr::Group),
                           hipMemcpyHostToDevice));
   }
-  HIP_OR_FAIL(hipEventCreateWithFlags(&M->last, hipEventDisableTiming));
   const auto t2 = clock::now();
   M->programs = jobs.size();
   M->program_bytes = bytes;
@@ -742,14 +826,15 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
       HIP_OR_FAIL(hipModuleLaunchKernel(M.fn[mode], grid, 1, 1, 256, 1, 1, 0, s, args, nullptr));
   }
   if (stop) HIP_OR_FAIL(hipEventRecord(stop, s));
-  HIP_OR_FAIL(hipEventRecord(M.last, s));
   return EMR_OK;
 }
 
-// jit: run the plan's compiled programs (jit_use said so) instead of the interpreter.
+// jit: run the plan's compiled programs (jit_use said so) instead of the interpreter. With
+// `finalize`, k_finalize then hands the call's flags to their pinned words.
 emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
                         const emr_result* out, float* raw, void* workspace, hipStream_t s,
-                        int64_t tile_lo, int64_t n_tiles, bool jit) {
+                        int64_t tile_lo, int64_t n_tiles, bool jit, const CallFlags& f,
+                        bool finalize) {
   char* ws = (char*)workspace;
   char* tables = nullptr;
   emr_status tst = plan_tables(P, &tables);
@@ -790,7 +875,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
     a.bias_tab = (const float*)(ws + P.off_bias);
     a.status = (uint64_t*)(ws + P.off_status);
     a.nz = (uint64_t*)(ws + P.off_nz);
-    a.err = (uint32_t*)(ws + P.off_err);
+    a.err = f.dev;
     a.parent = out ? out->parent : nullptr;
     a.w4 = out ? out->w4 : nullptr;
     a.pair_count = out ? out->pair_count : nullptr;
@@ -841,51 +926,32 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
   if (timed_call) prof.calls++;
   if (padded && P.n_pairs > 0)
     HIP_OR_FAIL(emr_launch_compact(
-        (const uint64_t*)(ws + P.off_status), out->parent, out->w4, out->pair_count,
-        (uint32_t*)(ws + P.off_err) + 1, (uint64_t*)(ws + P.off_nz), out->pair_capacity,
-        (uint32_t)tile_lo, (uint32_t)n_tiles,
-        (uint32_t)P.n_pairs,
+        (const uint64_t*)(ws + P.off_status), out->parent, out->w4, out->pair_count, f.dev + 1,
+        (uint64_t*)(ws + P.off_nz), out->pair_capacity, (uint32_t)tile_lo,
+        (uint32_t)n_tiles, (uint32_t)P.n_pairs,
         (uint32_t)(P.depth < emr::kFirstAlignedLevel ? emr::n_parents(P.depth)
                                                      : emr::level_offset(emr::kFirstAlignedLevel) / 4),
         s));
+  if (finalize) HIP_OR_FAIL(emr_launch_finalize(f.dev, f.host_dev, s));
   return EMR_OK;
 }
 
-// The last call's flags (error bits, largest pair count), copied to pinned memory on its stream
-// so that emr_result_check on the same workspace only waits for them.
-struct FlagReadback {
-  uint32_t* host = nullptr;
-  hipEvent_t done = nullptr;
-  const void* ws = nullptr;
-};
-thread_local FlagReadback g_flags;
-
-emr_status queue_flags_readback(void* workspace, hipStream_t s) {
-  FlagReadback& f = g_flags;
-  f.ws = nullptr;
-  if (!f.host && hipHostMalloc((void**)&f.host, 64, hipHostMallocDefault) != hipSuccess) {
-    f.host = nullptr;
-    return EMR_OK;  // the check then reads the workspace itself
-  }
-  if (!f.done) HIP_OR_FAIL(hipEventCreateWithFlags(&f.done, hipEventDisableTiming));
-  HIP_OR_FAIL(hipMemcpyAsync(f.host, workspace, 8, hipMemcpyDeviceToHost, s));
-  HIP_OR_FAIL(hipEventRecord(f.done, s));
-  f.ws = workspace;
-  return EMR_OK;
-}
-
-// Enqueue a whole call: prepare, then every tile of every pair.
+// Enqueue a whole call: take a flag slot, prepare, then every tile of every pair.
 emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const emr_result* out,
                     float* raw, void* workspace, int64_t workspace_bytes, hipStream_t s) {
   const bool lookback = out && !raw && out->pair_capacity < emr::n_parents(P.depth);
-  emr_status st = prepare_plan(pop, P, workspace, workspace_bytes, s, lookback);
+  CallFlags f;
+  emr_status st = take_flags(workspace, s, &f);
+  if (st != EMR_OK) return st;
+  st = prepare_plan(pop, P, workspace, workspace_bytes, s, lookback, f.dev);
   if (st != EMR_OK) return st;
   bool jit = false;
   st = jit_use(pop, P, plan_slots(P), &jit);
   if (st != EMR_OK) return st;
-  st = launch_range(pop, P, theta, out, raw, workspace, s, 0, P.tiles, jit);
+  st = launch_range(pop, P, theta, out, raw, workspace, s, 0, P.tiles, jit, f, true);
   if (st != EMR_OK) return st;
-  return queue_flags_readback(workspace, s);
+  f.ok = true;
+  return EMR_OK;
 }
 
 }  // namespace
@@ -1139,25 +1205,30 @@ emr_status emr_discover(const emr_population* pop, const emr_source* sources, in
 
 emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max_count,
                             void* stream) {
+  (void)stream;
   if (!out || n_pairs < 0) return fail(EMR_E_INVAL, "bad arguments");
-  HIP_OR_FAIL(hipStreamSynchronize((hipStream_t)stream));
-  // Workspace words 0 and 1: the error flags and the largest pair count of the call.
-  uint32_t w2[2] = {0, 0};
-  int64_t mx = 0;
-  if (out->workspace && g_flags.ws == out->workspace) {
-    HIP_OR_FAIL(hipEventSynchronize(g_flags.done));
-    w2[0] = g_flags.host[0];
-    w2[1] = g_flags.host[1];
-    mx = w2[1];
-  } else if (out->workspace) {
-    HIP_OR_FAIL(hipMemcpy(w2, out->workspace, 8, hipMemcpyDeviceToHost));
-    mx = w2[1];
-  } else if (n_pairs > 0) {
-    std::vector<int64_t> cnt((size_t)n_pairs);
-    HIP_OR_FAIL(hipMemcpy(cnt.data(), out->pair_count, (size_t)n_pairs * 8, hipMemcpyDeviceToHost));
-    for (int64_t c : cnt) mx = std::max(mx, c);
+  // the flag slot of the latest call with this result's workspace
+  hipEvent_t ev = nullptr;
+  const uint32_t* host = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_ring_mu);
+    FlagRing* R = nullptr;
+    emr_status st = flag_ring(&R);
+    if (st != EMR_OK) return st;
+    uint64_t latest = 0;
+    for (int k = 0; k < kFlagSlots; ++k)
+      if (out->workspace && R->ws[k] == out->workspace && R->seq[k] > latest) {
+        latest = R->seq[k];
+        ev = R->done[k];
+        host = R->host + (size_t)k * kSlotWords;
+      }
   }
-  const uint32_t err = w2[0];
+  if (!ev)
+    return fail(EMR_E_INVAL, "no call with this workspace among the last %d calls on this device",
+                kFlagSlots);
+  HIP_OR_FAIL(hipEventSynchronize(ev));
+  const uint32_t err = host[0];
+  const int64_t mx = host[1];
   if (max_count) *max_count = mx;
   if (err)
     return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (1: look-back wait bound, 2: a "
@@ -1379,7 +1450,10 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
       return fail(EMR_E_NOMEM, "pinned counts of a streamed call");
   }
 
-  st = prepare_plan(pop, P, R.ws, (int64_t)P.total, R.s, false);
+  CallFlags f;  // the chunks raise into its words, handed over once at the end
+  st = take_flags(nullptr, R.s, &f);
+  if (st != EMR_OK) return st;
+  st = prepare_plan(pop, P, R.ws, (int64_t)P.total, R.s, false, f.dev);
   if (st != EMR_OK) return st;
   emr_result chunk_out{R.pad_parent, R.pad_w4, cap, R.counts, R.ws, (int64_t)P.total};
   bool jit = false;
@@ -1392,7 +1466,8 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     const int b = (int)(c & 1);
     if (R.copy_pending[b]) HIP_OR_FAIL(hipStreamWaitEvent(R.s, R.ev_copy[b], 0));
     const int64_t tile_lo = c * tpc, n = std::min<int64_t>(tpc, P.tiles - tile_lo);
-    emr_status e = launch_range(pop, P, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n, jit);
+    emr_status e =
+        launch_range(pop, P, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n, jit, f, false);
     if (e != EMR_OK) return e;
     HIP_OR_FAIL(emr_launch_gather(R.counts, R.pad_parent, R.pad_w4, cap, (uint32_t)n_pairs,
                                   R.g_parent[b], R.g_w4[b], R.s));
@@ -1453,9 +1528,10 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     }
     if (next) *next = (c + 1) * n_pairs;
   }
+  HIP_OR_FAIL(emr_launch_finalize(f.dev, f.host_dev, R.s));
   HIP_OR_FAIL(hipStreamSynchronize(R.s));
-  uint32_t err = 0;
-  HIP_OR_FAIL(hipMemcpy(&err, R.ws, 4, hipMemcpyDeviceToHost));
+  f.ok = true;
+  const uint32_t err = f.host[0];
   if (err)
     return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (2: a table entry out of range)",
                 err);
