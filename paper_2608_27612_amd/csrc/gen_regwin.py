@@ -306,14 +306,11 @@ def gen_jitcall(S, P, W):
     # the next walk's tile geometry rows (TPW consecutive rows of 4 words) are loaded first, with
     # one load, so they arrive while the program runs; the wait after the return point makes them
     # safe to read (long done by then)
-    L = ["s_load_dwordx%d %%[geo], %%[ga], 0x0" % (4 * TPW)]
-    L += ["s_getpc_b64 s[%d:%d]" % (JIT_RET, JIT_RET + 1),
-          ".Lcall_%=:",
-          "s_add_u32 s%d, s%d, .Lret_%%= - .Lcall_%%=" % (JIT_RET, JIT_RET),
-          "s_addc_u32 s%d, s%d, 0" % (JIT_RET + 1, JIT_RET + 1),
-          "s_setpc_b64 %[tgt]",
-          ".Lret_%=:",
-          "s_waitcnt lgkmcnt(0)"]
+    # s_swappc_b64 jumps to the program and leaves the address of the next instruction (where the
+    # program returns to) in s[JIT_RET:JIT_RET+1]
+    L = ["s_load_dwordx%d %%[geo], %%[ga], 0x0" % (4 * TPW),
+         "s_swappc_b64 s[%d:%d], %%[tgt]" % (JIT_RET, JIT_RET + 1),
+         "s_waitcnt lgkmcnt(0)"]
     outs = ['"={v%d}"(acc[%d])' % (ACC + m, m) for m in range(M)]
     outs += ['"=&{v[%d:%d]}"(w%d)' % (base(M, m, W), base(M, m, W) + W - 1, m) for m in range(M)]
     outs += ['"=&{v%d}"(t[%d])' % (tmp0 + k, k) for k in range(jit_temps(S, P, W))]

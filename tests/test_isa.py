@@ -184,7 +184,7 @@ def test_template_does_not_carry_scc_across_calls(jit_asm):
     lines = jit_asm.splitlines()
     calls = 0
     for i, line in enumerate(lines):
-        if "s_setpc_b64" not in line.split(";")[0]:
+        if "s_swappc_b64" not in line.split(";")[0]:
             continue
         calls += 1
         for k in range(i + 1, min(i + 80, len(lines))):
