@@ -239,7 +239,11 @@ emr_status emr_eval_raw(const emr_population* pop, const emr_source* sources, in
                         void* workspace, int64_t workspace_bytes, void* stream);
 
 /* Algorithmic VALU work of one emr_discover call under the cost model documented with the
- * benchmark: total lane-operation slots (*slots) and number of queries (*queries). Host only. */
+ * benchmark: total lane-operation slots (*slots) and number of queries (*queries). Per query of a
+ * (genome, direction) program: one slot per position-dependent edge, the activations' slots
+ * (transcendental instructions weighted by transcendental_slots) and 2.5 for the variance; a
+ * program whose output does not depend on the position costs 0 (its outputs are per-source
+ * constants and their variance is exactly zero). Host only. */
 emr_status emr_discover_cost(const emr_population* pop, const emr_source* sources,
                              int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
                              int32_t depth, double transcendental_slots, double* slots,

@@ -118,14 +118,19 @@ thread_local Profiler g_prof;
 // edge, the activation costs (transcendental instructions weighted by rT), and 2.5 for the
 // variance and threshold share of a query.
 // The cost is base + rT * trans: query_base() is the part without transcendentals, query_trans()
-// their count per query.
+// their count per query. A program whose output does not depend on the position costs nothing
+// per query: its output is the source's constant (folded once by the bind kernel, like every
+// position-independent node) and the variance of a constant is exactly zero, so the kernels
+// evaluate and test nothing for it.
 double query_base(const emr::GenomeInfo& inf) {
+  if (!inf.out_varying) return 0.0;
   const double other[6] = {0.0, 1.0, 2.0, 1.0, 1.0, 1.0};
   double c = inf.fma_xy + inf.fma_node + 2.5;
   for (int a = 0; a < 6; ++a) c += inf.act_count[a] * other[a];
   return c;
 }
 double query_trans(const emr::GenomeInfo& inf) {
+  if (!inf.out_varying) return 0.0;
   const double trans[6] = {0.0, 2.0, 2.0, 1.0, 1.0, 0.0};
   double c = 0.0;
   for (int a = 0; a < 6; ++a) c += inf.act_count[a] * trans[a];
