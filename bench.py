@@ -17,8 +17,9 @@ Printed as one JSON line:
                same peak (every kernel, launch gap and host interaction of a step included)
   ms_per_gen   pack (host + upload) + discover + check, host clock: the per-generation cost of
                discovery in an evolution loop (a new population each generation, discovered once:
-               the default policy runs it through the interpreter); ms_per_gen_compiled the same
-               with the population's programs compiled first (compile + module load included)
+               the default policy runs it through the interpreter), from genomes held as the C
+               ABI's concatenated arrays; ms_per_gen_compiled the same with the population's
+               programs compiled first (compile + module load included)
   compiled_tier  the timed steps' compiled programs (the default policy compiles a population's
                programs on its second call, so the warm-up compiles them): count, machine-code
                bytes, host compile and module-load times
@@ -178,13 +179,18 @@ def main():
 
     # ms per generation: pack + discover + check on the host clock, for a new population each
     # generation (one call per population: the default policy interprets it), and with the
-    # population's programs compiled first (pack + compile + load + discover + check)
+    # population's programs compiled first (pack + compile + load + discover + check). The
+    # genomes arrive as the C ABI's concatenated arrays (emr_pack_population_flat), as an
+    # evolution loop would hold them; turning this script's list of dicts into those arrays is
+    # part of generating the genomes, outside the timing.
+    flat = emr.flat_genomes(genomes)
+
     def per_gen(gen_policy):
         emr.emr_set_jit(gen_policy)
         torch.cuda.synchronize()
         g0 = time.perf_counter()
         for _ in range(args.gens):
-            p = emr.emr_pack_population(genomes)
+            p = emr.emr_pack_population(flat)
             emr.emr_discover(p, sources, depth, theta32, res=res)
             emr.emr_result_check(res)
             del p

@@ -205,12 +205,15 @@ def flat_genomes(genomes):
 
 
 def emr_pack_population(genomes, layout: str = "flat") -> Population:
-    """Validate and pack genomes (list of dicts, see workloads.py) into device program tables,
-    through emr_pack_population_flat (layout "flat") or emr_pack_population ("structs")."""
+    """Validate and pack genomes into device program tables: a list of dicts (see workloads.py),
+    through emr_pack_population_flat (layout "flat") or emr_pack_population ("structs"), or the
+    concatenated arrays of flat_genomes (a dict; passed as they are)."""
     handle = C.c_void_p()
     bad = C.c_int32(-1)
+    if isinstance(genomes, dict):
+        layout = "flat"
     if layout == "flat":
-        f = flat_genomes(genomes)
+        f = genomes if isinstance(genomes, dict) else flat_genomes(genomes)
         d = lambda a: a.ctypes.data if len(a) else None  # noqa: E731
         st = lib().emr_pack_population_flat(f["n"], f["node_off"].ctypes.data, d(f["kind"]),
                                             d(f["act"]), d(f["bias"]), f["edge_off"].ctypes.data,
@@ -225,7 +228,7 @@ def emr_pack_population(genomes, layout: str = "flat") -> Population:
         err.bad_index = bad.value
         raise err
     del keep
-    return Population(handle, len(genomes))
+    return Population(handle, int(f["n"]) if layout == "flat" else len(genomes))
 
 
 # ----------------------------------------------------------------------------- discovery
