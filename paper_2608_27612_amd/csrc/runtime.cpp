@@ -569,11 +569,11 @@ emr_status take_flags(const void* workspace, hipStream_t s, CallFlags* f) {
   return EMR_OK;
 }
 
-// Clears the workspace's tile status words when the look-back placement needs them, and runs the
-// bind kernel over the plan's tables.
+// Clears the workspace's tile status words when the look-back placement needs them, and fills
+// the bind kernel's arguments over the plan's tables (*b: launched by the caller).
 emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspace,
                         int64_t workspace_bytes, hipStream_t s, bool clear_status,
-                        uint32_t* flags) {
+                        uint32_t* flags, emr::BindArgs* bind) {
   if (!workspace || workspace_bytes < (int64_t)P.total)
     return fail(EMR_E_INVAL, "workspace of %lld bytes is smaller than the %zu needed",
                 (long long)workspace_bytes, P.total);
@@ -599,7 +599,7 @@ emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspac
   b.bias_floats = P.bias_floats;
   b.nz = (uint64_t*)(ws + P.off_nz);
   b.nz_words = (uint32_t)(P.nz_bytes / 8);
-  HIP_OR_FAIL(emr_launch_bind(&b, s));
+  *bind = b;
   return EMR_OK;
 }
 
@@ -836,10 +836,12 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
 
 // jit: run the plan's compiled programs (jit_use said so) instead of the interpreter. With
 // `finalize`, k_finalize then hands the call's flags to their pinned words.
+// With `bind`, the bind kernel goes right before the first discover launch, once every argument
+// of that launch is ready on the host (so the GPU does not wait for host work between them).
 emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
                         const emr_result* out, float* raw, void* workspace, hipStream_t s,
                         int64_t tile_lo, int64_t n_tiles, bool jit, const CallFlags& f,
-                        bool finalize) {
+                        bool finalize, const emr::BindArgs* bind) {
   char* ws = (char*)workspace;
   char* tables = nullptr;
   emr_status tst = plan_tables(P, &tables);
@@ -907,6 +909,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
     const bool timed = li < n_timed;
     hipEvent_t e0 = timed ? prof.events[2 * (rec0 + li)] : nullptr;
     hipEvent_t e1 = timed ? prof.events[2 * (rec0 + li) + 1] : nullptr;
+    if (li == 0 && bind) HIP_OR_FAIL(emr_launch_bind(bind, s));
     if (jit) {
       emr_status js = jit_launch(P, a, mode, blocks, s, e0, e1);
       if (js != EMR_OK) return js;
@@ -948,12 +951,15 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
   CallFlags f;
   emr_status st = take_flags(workspace, s, &f);
   if (st != EMR_OK) return st;
-  st = prepare_plan(pop, P, workspace, workspace_bytes, s, lookback, f.dev);
+  emr::BindArgs bind{};
+  st = prepare_plan(pop, P, workspace, workspace_bytes, s, lookback, f.dev, &bind);
   if (st != EMR_OK) return st;
   bool jit = false;
   st = jit_use(pop, P, plan_slots(P), &jit);
   if (st != EMR_OK) return st;
-  st = launch_range(pop, P, theta, out, raw, workspace, s, 0, P.tiles, jit, f, true);
+  if (P.launches.empty()) HIP_OR_FAIL(emr_launch_bind(&bind, s));  // (no discover launch)
+  st = launch_range(pop, P, theta, out, raw, workspace, s, 0, P.tiles, jit, f, true,
+                    P.launches.empty() ? nullptr : &bind);
   if (st != EMR_OK) return st;
   f.ok = true;
   return EMR_OK;
@@ -1458,8 +1464,10 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
   CallFlags f;  // the chunks raise into its words, handed over once at the end
   st = take_flags(nullptr, R.s, &f);
   if (st != EMR_OK) return st;
-  st = prepare_plan(pop, P, R.ws, (int64_t)P.total, R.s, false, f.dev);
+  emr::BindArgs bind{};
+  st = prepare_plan(pop, P, R.ws, (int64_t)P.total, R.s, false, f.dev, &bind);
   if (st != EMR_OK) return st;
+  HIP_OR_FAIL(emr_launch_bind(&bind, R.s));
   emr_result chunk_out{R.pad_parent, R.pad_w4, cap, R.counts, R.ws, (int64_t)P.total};
   bool jit = false;
   st = jit_use(pop, P, plan_slots(P) * (double)(total - start) / (double)total, &jit);
@@ -1472,7 +1480,8 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     if (R.copy_pending[b]) HIP_OR_FAIL(hipStreamWaitEvent(R.s, R.ev_copy[b], 0));
     const int64_t tile_lo = c * tpc, n = std::min<int64_t>(tpc, P.tiles - tile_lo);
     emr_status e =
-        launch_range(pop, P, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n, jit, f, false);
+        launch_range(pop, P, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n, jit, f, false,
+                     nullptr);
     if (e != EMR_OK) return e;
     HIP_OR_FAIL(emr_launch_gather(R.counts, R.pad_parent, R.pad_w4, cap, (uint32_t)n_pairs,
                                   R.g_parent[b], R.g_w4[b], R.s));

@@ -242,6 +242,32 @@ def test_capacity_overflow_is_reported(emr):
     np.testing.assert_array_equal(recs[0][0], np.arange(10))
 
 
+
+def test_result_checks_wait_for_their_own_call(emr):
+    """Each call's flags live in a slot of their own: two calls on two results enqueued back to
+    back are checked afterwards, each against its own largest count (one overflows, the other
+    does not), and a workspace with no call to check is refused."""
+    genomes, sources, D, _ = W.workload("single_d5")
+    pop = emr.emr_pack_population(genomes)
+    res_all = emr.emr_discover(pop, sources, D, -1.0)               # every cell kept
+    res_few = emr.emr_discover(pop, sources, D, -1.0, pair_capacity=10)
+    res_none = emr.emr_discover(pop, sources, D, 1e30)             # nothing kept
+    assert emr.emr_result_check(res_all) == oracle.n_parents(D)
+    with pytest.raises(emr.EmrError) as e:
+        emr.emr_result_check(res_few)
+    assert e.value.status == emr.EMR_E_CAPACITY
+    assert emr.emr_result_check(res_none) == 0
+    # checked again later (no call in between on these results): the same answers
+    assert emr.emr_result_check(res_all) == oracle.n_parents(D)
+    import torch
+    other = dict(res_all)
+    other.pop("_struct", None)
+    other["workspace"] = torch.empty_like(res_all["workspace"])
+    with pytest.raises(emr.EmrError) as e:
+        emr.emr_result_check(other)
+    assert e.value.status == emr.EMR_E_INVAL
+
+
 def test_lookback_placement_matches_padded_placement(emr):
     """A pair capacity below Q(D) switches record placement to the look-back scan; both
     placements must give identical records."""
