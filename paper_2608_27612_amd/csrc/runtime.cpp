@@ -1353,8 +1353,14 @@ namespace {
 // Device and pinned buffers of one emr_discover_stream call. The destructor drains both streams
 // before freeing, so an early return (an error, or a sink that stops the run) never frees memory
 // a queued kernel or copy still uses.
-struct StreamRun {
-  hipStream_t s = nullptr, side = nullptr;
+// The buffers, side stream and events of one streamed call. A call takes an idle set of its
+// device from a process-wide cache (or a new one), grows what is too small, and gives the set back
+// when it is done with it, so repeated streamed calls allocate nothing (a set is kept until the
+// process ends: at most the largest call's buffers per concurrent streamed call).
+struct StreamSet {
+  int device = -1;
+  hipStream_t side = nullptr;
+  hipEvent_t ev_count[2] = {}, ev_copy[2] = {};
   void* ws = nullptr;
   uint32_t* pad_parent = nullptr;   // padded per-pair regions of the current chunk
   float* pad_w4 = nullptr;
@@ -1365,28 +1371,51 @@ struct StreamRun {
   uint32_t* stage_parent[2] = {};   // pinned staging of the gathered records
   float* stage_w4[2] = {};
   int64_t stage_cap[2] = {0, 0};
-  hipEvent_t ev_count[2] = {}, ev_copy[2] = {};
-  bool copy_pending[2] = {false, false};
+  int64_t ws_bytes = 0, pad_records = 0, count_pairs = 0, g_records = 0, counts_h_pairs = 0;
+};
+std::mutex g_stream_sets_mu;
+std::vector<StreamSet*> g_stream_sets;  // idle sets
 
+struct StreamRun : StreamSet {
+  hipStream_t s = nullptr;
+  bool copy_pending[2] = {false, false};
+  StreamRun() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return;
+    std::lock_guard<std::mutex> lock(g_stream_sets_mu);
+    for (size_t k = 0; k < g_stream_sets.size(); ++k)
+      if (g_stream_sets[k]->device == dev) {
+        static_cast<StreamSet&>(*this) = *g_stream_sets[k];
+        delete g_stream_sets[k];
+        g_stream_sets.erase(g_stream_sets.begin() + (ptrdiff_t)k);
+        return;
+      }
+    device = dev;
+  }
   ~StreamRun() {
+    // nothing queued may still use the set when the next call takes it
     if (s) (void)hipStreamSynchronize(s);
     if (side) (void)hipStreamSynchronize(side);
-    for (int b = 0; b < 2; ++b) {
-      if (g_parent[b]) (void)hipFree(g_parent[b]);
-      if (g_w4[b]) (void)hipFree(g_w4[b]);
-      if (counts_h[b]) (void)hipHostFree(counts_h[b]);
-      if (stage_parent[b]) (void)hipHostFree(stage_parent[b]);
-      if (stage_w4[b]) (void)hipHostFree(stage_w4[b]);
-      if (ev_count[b]) (void)hipEventDestroy(ev_count[b]);
-      if (ev_copy[b]) (void)hipEventDestroy(ev_copy[b]);
-    }
-    if (ws) (void)hipFree(ws);
-    if (pad_parent) (void)hipFree(pad_parent);
-    if (pad_w4) (void)hipFree(pad_w4);
-    if (counts) (void)hipFree(counts);
-    if (side) (void)hipStreamDestroy(side);
+    std::lock_guard<std::mutex> lock(g_stream_sets_mu);
+    g_stream_sets.push_back(new StreamSet(static_cast<const StreamSet&>(*this)));
   }
 };
+
+// Device buffer *p of at least `bytes` (256 or more), keeping the current one when it is large
+// enough; *have is its size.
+bool reserve_device(void** p, int64_t* have, int64_t bytes) {
+  bytes = std::max<int64_t>(bytes, 256);
+  if (*p && *have >= bytes) return true;
+  if (*p) (void)hipFree(*p);
+  *p = nullptr;
+  *have = 0;
+  if (hipMalloc(p, (size_t)bytes) != hipSuccess) {
+    *p = nullptr;
+    return false;
+  }
+  *have = bytes;
+  return true;
+}
 
 // Largest device footprint of one streamed call's record buffers (padded + two gathered sets).
 constexpr int64_t kStreamBufferLimit = int64_t(48) << 30;
@@ -1438,27 +1467,51 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
 
   StreamRun R;
   R.s = (hipStream_t)stream;
-  HIP_OR_FAIL(hipStreamCreateWithFlags(&R.side, hipStreamNonBlocking));
+  if (!R.side) HIP_OR_FAIL(hipStreamCreateWithFlags(&R.side, hipStreamNonBlocking));
   for (int b = 0; b < 2; ++b) {
-    HIP_OR_FAIL(hipEventCreateWithFlags(&R.ev_count[b], hipEventDisableTiming));
-    HIP_OR_FAIL(hipEventCreateWithFlags(&R.ev_copy[b], hipEventDisableTiming));
+    if (!R.ev_count[b]) HIP_OR_FAIL(hipEventCreateWithFlags(&R.ev_count[b], hipEventDisableTiming));
+    if (!R.ev_copy[b]) HIP_OR_FAIL(hipEventCreateWithFlags(&R.ev_copy[b], hipEventDisableTiming));
   }
-  auto dmalloc = [](void** p, int64_t bytes) {
-    return hipMalloc(p, (size_t)std::max<int64_t>(bytes, 256));
-  };
-  if (dmalloc(&R.ws, (int64_t)P.total) != hipSuccess ||
-      dmalloc((void**)&R.pad_parent, n_pairs * cap * 4) != hipSuccess ||
-      dmalloc((void**)&R.pad_w4, n_pairs * cap * 16) != hipSuccess ||
-      dmalloc((void**)&R.counts, n_pairs * 8) != hipSuccess)
+  // record buffers by the records they hold (parents, then float4 outputs: sized together)
+  const int64_t records = n_pairs * cap;
+  int64_t have = 0;
+  bool ok = reserve_device(&R.ws, &R.ws_bytes, (int64_t)P.total);
+  if (ok && R.pad_records < records) {
+    have = R.pad_records * 4;
+    ok = reserve_device((void**)&R.pad_parent, &have, records * 4);
+    have = R.pad_records * 16;
+    ok = ok && reserve_device((void**)&R.pad_w4, &have, records * 16);
+    R.pad_records = ok ? records : 0;
+  }
+  if (ok && R.count_pairs < n_pairs) {
+    have = R.count_pairs * 8;
+    ok = reserve_device((void**)&R.counts, &have, n_pairs * 8);
+    R.count_pairs = ok ? n_pairs : 0;
+  }
+  if (!ok)
     return fail(EMR_E_NOMEM, "device buffers of a streamed call (%lld bytes per record set)",
                 (long long)set_bytes);
-  for (int b = 0; b < 2; ++b) {
-    if (dmalloc((void**)&R.g_parent[b], n_pairs * cap * 4) != hipSuccess ||
-        dmalloc((void**)&R.g_w4[b], n_pairs * cap * 16) != hipSuccess)
-      return fail(EMR_E_NOMEM, "gather buffers of a streamed call");
-    if (hipHostMalloc((void**)&R.counts_h[b], (size_t)std::max<int64_t>(n_pairs, 1) * 8,
-                      hipHostMallocDefault) != hipSuccess)
-      return fail(EMR_E_NOMEM, "pinned counts of a streamed call");
+  if (R.g_records < records) {
+    for (int b = 0; b < 2 && ok; ++b) {
+      have = R.g_records * 4;
+      ok = reserve_device((void**)&R.g_parent[b], &have, records * 4);
+      have = R.g_records * 16;
+      ok = ok && reserve_device((void**)&R.g_w4[b], &have, records * 16);
+    }
+    R.g_records = ok ? records : 0;
+    if (!ok) return fail(EMR_E_NOMEM, "gather buffers of a streamed call");
+  }
+  if (R.counts_h_pairs < std::max<int64_t>(n_pairs, 1)) {
+    for (int b = 0; b < 2; ++b) {
+      if (R.counts_h[b]) (void)hipHostFree(R.counts_h[b]);
+      R.counts_h[b] = nullptr;
+    }
+    R.counts_h_pairs = 0;
+    for (int b = 0; b < 2; ++b)
+      if (hipHostMalloc((void**)&R.counts_h[b], (size_t)std::max<int64_t>(n_pairs, 1) * 8,
+                        hipHostMallocDefault) != hipSuccess)
+        return fail(EMR_E_NOMEM, "pinned counts of a streamed call");
+    R.counts_h_pairs = std::max<int64_t>(n_pairs, 1);
   }
 
   CallFlags f;  // the chunks raise into its words, handed over once at the end
