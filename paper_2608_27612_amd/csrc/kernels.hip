@@ -178,14 +178,16 @@ __global__ void k_finalize(uint32_t* flags, uint32_t* host) {
 
 // Each wave takes pairs pair = wave, wave + n_waves, ...: compacts them once every discover launch
 // of the range has finished, and the workgroup's largest count is raised into *max_count with one
-// atomic.
+// atomic. A pair with skip[pair] set (its groups were left out of the launch: they keep nothing)
+// gets a count of 0 without its tile counts being read.
 constexpr int kCompactWaves = 4;
 
 __global__ void __launch_bounds__(kCompactWaves * kWave)
     k_compact(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
               float* __restrict__ w4, int64_t* __restrict__ pair_count,
-              uint32_t* __restrict__ max_count, uint64_t* __restrict__ nz, int64_t cap,
-              uint32_t tile_lo, uint32_t tiles, uint32_t n_pairs, uint32_t head_slots) {
+              uint32_t* __restrict__ max_count, uint64_t* __restrict__ nz,
+              const uint8_t* __restrict__ skip, int64_t cap, uint32_t tile_lo, uint32_t tiles,
+              uint32_t n_pairs, uint32_t head_slots) {
   __shared__ uint32_t wave_max[kCompactWaves];
   const uint32_t lane = lane_id();
   const uint32_t wv = threadIdx.x / kWave;
@@ -193,6 +195,10 @@ __global__ void __launch_bounds__(kCompactWaves * kWave)
   uint32_t my_max = 0;
   for (uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * kCompactWaves + wv);
        pair < n_pairs; pair += n_waves) {
+    if (skip && skip[pair]) {
+      if (lane == 0) pair_count[pair] = 0;
+      continue;
+    }
     my_max = max(my_max, compact_pair(counts, parent, w4, pair_count, nz, cap, tile_lo, tiles,
                                       pair, head_slots, lane));
   }
@@ -579,14 +585,15 @@ extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* p
 
 extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
                                          int64_t* pair_count, uint32_t* max_count, uint64_t* nz,
-                                         int64_t cap, uint32_t tile_lo, uint32_t tiles,
-                                         uint32_t n_pairs, uint32_t head_slots, hipStream_t s) {
+                                         const uint8_t* skip, int64_t cap, uint32_t tile_lo,
+                                         uint32_t tiles, uint32_t n_pairs, uint32_t head_slots,
+                                         hipStream_t s) {
   if (n_pairs == 0) return hipSuccess;
   uint32_t blocks = (n_pairs + emr::kCompactWaves - 1) / emr::kCompactWaves;
   if (blocks > 8192) blocks = 8192;  // waves loop over pairs beyond this
   hipLaunchKernelGGL(emr::k_compact, dim3(blocks), dim3(emr::kCompactWaves * emr::kWave), 0, s,
-                     counts, parent, w4, pair_count, max_count, nz, cap, tile_lo, tiles, n_pairs,
-                     head_slots);
+                     counts, parent, w4, pair_count, max_count, nz, skip, cap, tile_lo, tiles,
+                     n_pairs, head_slots);
   return hipGetLastError();
 }
 

@@ -28,8 +28,9 @@ extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int mode, 
                                           hipStream_t s, hipEvent_t start, hipEvent_t stop);
 extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
                                          int64_t* pair_count, uint32_t* max_count, uint64_t* nz,
-                                         int64_t cap, uint32_t tile_lo, uint32_t tiles,
-                                         uint32_t n_pairs, uint32_t head_slots, hipStream_t s);
+                                         const uint8_t* skip, int64_t cap, uint32_t tile_lo,
+                                         uint32_t tiles, uint32_t n_pairs, uint32_t head_slots,
+                                         hipStream_t s);
 extern "C" hipError_t emr_launch_finalize(uint32_t* flags, uint32_t* host, hipStream_t s);
 extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
                                         const float* w4, int64_t cap, uint32_t n_pairs,
@@ -204,6 +205,8 @@ struct Plan {
     int S, window;
     uint32_t first, count;
     double cost;  // summed per-query cost of its groups' programs (launch order)
+    uint32_t varying;  // its first `varying` groups have a position-dependent output (the rest,
+                       // the cheapest, do not)
   };
   // The discover launch of a call: its buckets (one per sources per walk and register window),
   // costliest first.
@@ -223,9 +226,10 @@ struct Plan {
   std::vector<float> src_xy;
   uint64_t bias_floats = 0;
   // The plan's tables (groups at t_groups, members at t_members, source coordinates at
-  // t_srcxy): a host image, and its device copy, uploaded on first use and freed with the plan.
+  // t_srcxy, one byte per pair at t_uniform: 1 when the pair's output does not depend on the
+  // position): a host image, and its device copy, uploaded on first use and freed with the plan.
   std::vector<char> img;
-  size_t t_groups = 0, t_members = 0, t_srcxy = 0;
+  size_t t_groups = 0, t_members = 0, t_srcxy = 0, t_uniform = 0;
   mutable std::mutex dev_mu;
   mutable char* d_tables = nullptr;
   Plan() = default;
@@ -338,8 +342,9 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
   for (size_t i = 0; i < tmp.size(); ++i) {
     TmpGroup& t = tmp[i];
     if (P.buckets.empty() || P.buckets.back().S != t.S || P.buckets.back().window != t.window)
-      P.buckets.push_back({t.S, t.window, (uint32_t)i, 0, 0.0});
+      P.buckets.push_back({t.S, t.window, (uint32_t)i, 0, 0.0, 0});
     P.buckets.back().count++;
+    if (t.g.flags & 1u) P.buckets.back().varying = P.buckets.back().count;
     P.buckets.back().cost += t.S * cost[t.desc];
     t.g.bias_off = (uint32_t)bias;
     P.group_member0.push_back((uint32_t)P.members.size());
@@ -392,7 +397,11 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
   P.t_groups = 0;
   P.t_members = align256(P.groups.size() * sizeof(emr::Group));
   P.t_srcxy = align256(P.t_members + P.members.size() * sizeof(emr::Member));
-  P.img.assign(align256(P.t_srcxy + P.src_xy.size() * sizeof(float)) + 256, 0);
+  P.t_uniform = align256(P.t_srcxy + P.src_xy.size() * sizeof(float));
+  P.img.assign(align256(P.t_uniform + (size_t)P.n_pairs) + 256, 0);
+  for (const emr::Group& g : P.groups)
+    if (!(g.flags & 1u))
+      for (int s = 0; s < emr::kMaxGroup; ++s) P.img[P.t_uniform + g.pair[s]] = 1;
   if (!P.groups.empty())
     std::memcpy(P.img.data() + P.t_groups, P.groups.data(), P.groups.size() * sizeof(emr::Group));
   if (!P.members.empty())
@@ -856,6 +865,10 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
   // compacted afterwards; a smaller capacity places them through the look-back scan instead.
   const bool padded = out && out->pair_capacity >= range_parents;
   const int mode = raw ? 0 : (padded ? 1 : 2);
+  // With theta >= 0 a position-independent output keeps no cell (its variance is exactly 0): the
+  // padded placement leaves those groups (the last of each part) out of the launch, and the
+  // compaction gives their pairs no records without reading their counts.
+  const bool skip_uniform = padded && !(0.0f > theta);
   if (mode == 2 && (tile_lo != 0 || n_tiles != P.tiles))
     return fail(EMR_E_INVAL, "a tile range needs pair_capacity >= its %lld parents",
                 (long long)range_parents);
@@ -895,7 +908,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
       a.part_S[k] = (uint32_t)bk.S;
       a.part_W[k] = (uint32_t)bk.window;
       a.part_group0[k] = bk.first;
-      a.part_groups[k] = bk.count;
+      a.part_groups[k] = skip_uniform ? bk.varying : bk.count;
     }
     a.tile_lo = (uint32_t)tile_lo;
     a.parent_lo = (uint32_t)parent_lo;
@@ -935,7 +948,9 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
   if (padded && P.n_pairs > 0)
     HIP_OR_FAIL(emr_launch_compact(
         (const uint64_t*)(ws + P.off_status), out->parent, out->w4, out->pair_count, f.dev + 1,
-        (uint64_t*)(ws + P.off_nz), out->pair_capacity, (uint32_t)tile_lo,
+        (uint64_t*)(ws + P.off_nz),
+        skip_uniform ? (const uint8_t*)(tables + P.t_uniform) : nullptr, out->pair_capacity,
+        (uint32_t)tile_lo,
         (uint32_t)n_tiles, (uint32_t)P.n_pairs,
         (uint32_t)(P.depth < emr::kFirstAlignedLevel ? emr::n_parents(P.depth)
                                                      : emr::level_offset(emr::kFirstAlignedLevel) / 4),
