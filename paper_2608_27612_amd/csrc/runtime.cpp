@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <atomic>
 #include <chrono>
+#include <condition_variable>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -65,6 +66,87 @@ emr_status fail(emr_status st, const char* fmt, ...) {
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Compute units of the current device, queried once per device.
+// Host worker threads for the library's parallel host work (packing, the compiled tier's
+// translation), started on first use and kept for the process: run(n, f) calls f(0) .. f(n - 1)
+// on the workers and the calling thread and returns when every call has returned. One job runs at
+// a time (concurrent callers queue).
+class WorkerPool {
+ public:
+  static WorkerPool& get() {
+    static WorkerPool p;
+    return p;
+  }
+  int size() const { return (int)workers_.size() + 1; }
+  void run(int n, const std::function<void(int)>& f) {
+    if (n <= 1 || workers_.empty()) {
+      for (int i = 0; i < n; ++i) f(i);
+      return;
+    }
+    std::lock_guard<std::mutex> one_job(job_mu_);
+    {
+      std::lock_guard<std::mutex> l(mu_);
+      fn_ = &f;
+      next_ = 0;
+      n_ = n;
+      done_ = 0;
+      ++gen_;
+    }
+    cv_.notify_all();
+    take();
+    std::unique_lock<std::mutex> l(mu_);
+    done_cv_.wait(l, [&] { return done_ == n_; });
+    fn_ = nullptr;
+  }
+  ~WorkerPool() {
+    {
+      std::lock_guard<std::mutex> l(mu_);
+      stop_ = true;
+    }
+    cv_.notify_all();
+    for (auto& t : workers_) t.join();
+  }
+
+ private:
+  WorkerPool() {
+    const int hw = (int)std::max(1u, std::thread::hardware_concurrency());
+    for (int i = 1; i < std::min(hw, 16); ++i) workers_.emplace_back([this] { loop(); });
+  }
+  void take() {
+    for (;;) {
+      const std::function<void(int)>* fn;
+      int i;
+      {
+        std::lock_guard<std::mutex> l(mu_);
+        if (!fn_ || next_ >= n_) return;
+        fn = fn_;
+        i = next_++;
+      }
+      (*fn)(i);
+      std::lock_guard<std::mutex> l(mu_);
+      if (++done_ == n_) done_cv_.notify_all();
+    }
+  }
+  void loop() {
+    uint64_t seen = 0;
+    for (;;) {
+      {
+        std::unique_lock<std::mutex> l(mu_);
+        cv_.wait(l, [&] { return stop_ || gen_ != seen; });
+        if (stop_) return;
+        seen = gen_;
+      }
+      take();
+    }
+  }
+  std::vector<std::thread> workers_;
+  std::mutex job_mu_, mu_;
+  std::condition_variable cv_, done_cv_;
+  const std::function<void(int)>* fn_ = nullptr;
+  int next_ = 0, n_ = 0, done_ = 0;
+  uint64_t gen_ = 0;
+  bool stop_ = false;
+};
+
 int device_cu_count() {
   static std::atomic<int> cached[64];
   int dev = 0, cus = 0;
@@ -701,16 +783,11 @@ emr_status jit_build(const emr_population* pop, const Plan& P, std::unique_ptr<J
                                         &errs[j]);
     }
   };
-  const int hw = (int)std::max(1u, std::thread::hardware_concurrency());
-  const int n_threads = (int)std::max<size_t>(1, std::min<size_t>({(size_t)hw, 16, jobs.size() / 64}));
-  if (n_threads == 1) {
-    work(0, jobs.size());
-  } else {
-    std::vector<std::thread> pool;
-    for (int t = 0; t < n_threads; ++t)
-      pool.emplace_back(work, jobs.size() * t / n_threads, jobs.size() * (t + 1) / n_threads);
-    for (auto& th : pool) th.join();
-  }
+  const int n_threads = (int)std::max<size_t>(
+      1, std::min<size_t>({(size_t)WorkerPool::get().size(), 16, jobs.size() / 64}));
+  WorkerPool::get().run(n_threads, [&](int t) {
+    work(jobs.size() * t / n_threads, jobs.size() * (t + 1) / n_threads);
+  });
   std::vector<uint32_t> offs(jobs.size());
   size_t bytes = 0;
   for (size_t j = 0; j < jobs.size(); ++j) {
@@ -1016,8 +1093,7 @@ emr_status pack_and_upload(int32_t n, const std::function<emr_genome(int32_t)>& 
                            emr_population** out, int32_t* bad_index) {
   std::vector<emr::ProgDesc> desc(2 * (size_t)n);
   std::vector<emr::GenomeInfo> info(2 * (size_t)n);
-  const int hw = (int)std::max(1u, std::thread::hardware_concurrency());
-  const int n_threads = std::max(1, std::min({hw, 16, n / 32}));
+  const int n_threads = std::max(1, std::min({WorkerPool::get().size(), 16, n / 32}));
   struct Part {
     std::vector<uint32_t> words;
     int32_t bad = -1;
@@ -1048,13 +1124,7 @@ emr_status pack_and_upload(int32_t n, const std::function<emr_genome(int32_t)>& 
     }
     while (p.words.size() % emr::kRecWords) p.words.push_back(0u);  // keep bases aligned
   };
-  if (n_threads == 1) {
-    work(0);
-  } else {
-    std::vector<std::thread> pool;
-    for (int t = 0; t < n_threads; ++t) pool.emplace_back(work, t);
-    for (auto& th : pool) th.join();
-  }
+  WorkerPool::get().run(n_threads, work);
   for (const Part& p : parts)
     if (p.bad >= 0) {  // the parts cover increasing genome ranges: the first is the lowest
       if (bad_index) *bad_index = p.bad;
