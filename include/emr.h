@@ -158,9 +158,11 @@ typedef struct {
 } emr_result;
 
 /* Device scratch (bytes) needed by emr_discover / emr_eval_raw for this population, these
- * sources (host) and this depth: flags, tile status words and the folded per-(genome, source)
- * biases. Host only. (The grouping tables of a call live with the population: it keeps those of
- * its last sources and depth on the device, and a call with different ones replaces them.) */
+ * sources (host) and this depth: tile status words, the compaction's tile-group marks and the
+ * folded per-(genome, source) biases. The library keeps no state in it from one call to the next
+ * (a call's error flags and largest count live in a library-owned slot, see emr_result_check).
+ * Host only. (The grouping tables of a call live with the population: it keeps those of its last
+ * sources and depth on the device, and a call with different ones replaces them.) */
 emr_status emr_workspace_bytes(const emr_population* pop, const emr_source* sources,
                                int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
                                int32_t depth, int64_t* bytes);
@@ -219,9 +221,11 @@ emr_status emr_stream_chunks(int32_t depth, int64_t chunk_positions, int64_t* n_
  * (0 for a full run; deliveries below it are skipped), and *next (may be NULL) receives the
  * cursor to resume from: n_chunks * n_pairs after a complete run, or, when the sink returns
  * nonzero, the cursor of the delivery it refused (status EMR_E_ABORTED). Returns when done.
- * Device memory: the library allocates the workspace and three record buffers of
- * n_pairs * min(64 chunk_positions / 256, Q(D)) records (20 bytes each) for the call and frees
- * them before returning; EMR_E_LIMIT if they would exceed 48 GiB (use smaller chunks).
+ * Device memory: the library needs a workspace and three record buffers of
+ * n_pairs * min(64 chunk_positions / 256, Q(D)) records (20 bytes each), plus pinned staging, a
+ * side stream and events; it keeps them after the call for the next streamed call on the device
+ * (grown when a call needs more, held until the process ends); EMR_E_LIMIT if the record buffers
+ * would exceed 48 GiB (use smaller chunks).
  * Errors: EMR_E_INVAL for bad arguments (checked before any GPU work), EMR_E_NOMEM, EMR_E_DEVICE
  * (also when a kernel flagged an internal error), EMR_E_ABORTED.
  */
