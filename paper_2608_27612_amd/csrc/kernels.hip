@@ -121,10 +121,45 @@ __device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* 
     running += total;
   };
   if (n_groups <= kNzMinGroups) {
-    // both groups' counts are requested before either is scanned
+    // Both groups' counts are requested at once, and both groups' records move in one sequence
+    // of batches (rank q < total0 in group 0, else rank q - total0 in group 1), so a pair with
+    // few records waits for one round of record loads. Ranks ascend with the source slots and
+    // every record moves down, as within one group.
     const uint32_t c0 = load_count(0), c1 = n_groups > 1 ? load_count(1) : 0u;
-    if (n_groups > 0) group(0, c0);
-    if (n_groups > 1) group(1, c1);
+    auto scan = [&](uint32_t c) {
+      uint32_t incl = c;
+#pragma unroll
+      for (int b = 0; b < 7; ++b) incl += mbcnt64(ballot((c >> b) & 1u)) << b;
+      return incl;
+    };
+    const uint32_t incl0 = scan(c0), incl1 = scan(c1);
+    const uint32_t total0 = __builtin_amdgcn_readlane(incl0, kWave - 1);
+    const uint32_t total = total0 + __builtin_amdgcn_readlane(incl1, kWave - 1);
+    const uint64_t has0 = ballot(c0 != 0u), has1 = ballot(c1 != 0u);
+    for (uint32_t b = 0; b < total; b += kWave) {
+      const uint32_t q = b + lane, q1 = q - total0;  // (q1 wraps above every range for q < total0)
+      uint32_t src = q;
+      for (uint64_t m = has0; m != 0ull; m &= m - 1ull) {
+        const uint32_t i = (uint32_t)__builtin_ctzll(m);
+        const uint32_t hi = __builtin_amdgcn_readlane(incl0, i);
+        const uint32_t lo = hi - __builtin_amdgcn_readlane(c0, i);
+        if (q >= lo && q < hi) src = tile_parent_offset(tile_lo + i) - parent_lo + (q - lo);
+      }
+      for (uint64_t m = has1; m != 0ull; m &= m - 1ull) {
+        const uint32_t i = (uint32_t)__builtin_ctzll(m);
+        const uint32_t hi = __builtin_amdgcn_readlane(incl1, i);
+        const uint32_t lo = hi - __builtin_amdgcn_readlane(c1, i);
+        if (q1 >= lo && q1 < hi)
+          src = tile_parent_offset(tile_lo + kWave + i) - parent_lo + (q1 - lo);
+      }
+      if (q < total && src != q) {
+        const uint32_t pv = parent[region + src];
+        const float4 wv = reinterpret_cast<const float4*>(w4)[region + src];
+        parent[region + q] = pv;
+        reinterpret_cast<float4*>(w4)[region + q] = wv;
+      }
+    }
+    running = total;
   } else {
     const uint32_t n_words = nz_words(tiles);
     uint64_t* words = nz + (int64_t)pair * n_words;
