@@ -10,7 +10,7 @@ Genome layout (one genome = a dict of numpy arrays):
   node  5+H       the output node (kind 6)
   kind  u8[n]     node role
   act   u8[n]     activation id (0 linear, 1 sigmoid, 2 tanh, 3 gaussian, 4 sine, 5 abs)
-  bias  f32[n]    per-node bias (0 in every generated genome)
+  bias  f32[n]    per-node bias (0 unless drawn, see `biases` below)
   src, dst i32[e] edge endpoints (node ids)
   w     f32[e]    edge weights
   enabled u8[e]   1 = enabled
@@ -22,7 +22,10 @@ genomes are available, so seeded random DAGs of the same size classes stand in f
     rank(u) < rank(v) (inputs rank first, the output last); there are 5(H+1) + H(H-1)/2 + H;
   * E distinct candidates are drawn uniformly without replacement, in random order;
   * weights are clip(N(0, 1), -3, 3) rounded to float32; activations are uniform over the six
-    ids for hidden and output nodes; biases are 0; every edge is enabled.
+    ids for hidden and output nodes; every edge is enabled;
+  * biases are 0, or, when asked for (`biases=True`, test populations that exercise the bias
+    terms), clip(N(0, 1), -3, 3) rounded to float32 for every hidden and output node, drawn after
+    the genome's other values.
 """
 
 from __future__ import annotations
@@ -57,7 +60,8 @@ def _candidate_edges(h: int, rank: np.ndarray):
     return cand
 
 
-def random_genome(rng: np.random.Generator, n_hidden: int, n_edges: int) -> dict:
+def random_genome(rng: np.random.Generator, n_hidden: int, n_edges: int,
+                  biases: bool = False) -> dict:
     """One random CPPN genome following the module recipe."""
     h = int(n_hidden)
     n = 5 + h + 1
@@ -71,10 +75,13 @@ def random_genome(rng: np.random.Generator, n_hidden: int, n_edges: int) -> dict
     kind = np.array([0, 1, 2, 3, 4] + [KIND_HIDDEN] * h + [KIND_OUTPUT], dtype=np.uint8)
     act = np.zeros(n, dtype=np.uint8)
     act[5:] = rng.integers(0, N_ACT, size=h + 1)
+    bias = np.zeros(n, dtype=np.float32)
+    if biases:
+        bias[5:] = np.clip(rng.standard_normal(h + 1), -3.0, 3.0).astype(np.float32)
     return {
         "kind": kind,
         "act": act,
-        "bias": np.zeros(n, dtype=np.float32),
+        "bias": bias,
         "src": src,
         "dst": dst,
         "w": w,
@@ -102,14 +109,14 @@ def depends_on(genome: dict, roles) -> bool:
     return out in seen
 
 
-def population(seed: int, n: int, h_max: int, e_max: int) -> list:
+def population(seed: int, n: int, h_max: int, e_max: int, biases: bool = False) -> list:
     """n genomes with H ~ U{0..h_max} and E ~ U{1..min(e_max, C(H))}, drawn in index order."""
     rng = np.random.default_rng(seed)
     pop = []
     for _ in range(n):
         h = int(rng.integers(0, h_max + 1))
         e = int(rng.integers(1, min(e_max, n_candidates(h)) + 1))
-        pop.append(random_genome(rng, h, e))
+        pop.append(random_genome(rng, h, e, biases))
     return pop
 
 

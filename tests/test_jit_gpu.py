@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 from paper_2608_27612_amd import workloads as W
-from tests.test_parity_gpu import check_discover
+from tests.test_parity_gpu import check_discover, check_raw
 
 pytestmark = pytest.mark.gpu
 
@@ -177,3 +177,36 @@ def test_auto_policy_compiles_on_the_second_call(emr):
     assert np.array_equal(first[0], second[0])
     for a, b in zip(first[1], second[1]):
         assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_biased_population_both_tiers(emr):
+    """Nonzero node biases: raw outputs of both tiers bit-identical and within tolerance of the
+    oracle; records of both tiers against the oracle."""
+    genomes = W.population(53, 120, 20, 60, biases=True)
+    sources = W.xor_sources()
+    a, b = raw_both(emr, genomes, sources, 5)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    for policy in (emr.EMR_JIT_OFF, emr.EMR_JIT_ALWAYS):
+        emr.emr_set_jit(policy)
+        check_raw(emr, genomes, sources, 5)
+        pop = emr.emr_pack_population(genomes)
+        check_discover(emr, genomes, sources, 6, 0.03, pop=pop)
+        assert emr.emr_jit_info(pop)["state"] == (1 if policy == emr.EMR_JIT_ALWAYS else 0)
+
+
+@pytest.mark.parametrize("act", range(6))
+def test_biased_node_of_each_activation_both_tiers(emr, act):
+    # hidden h = act(3 x2 - 2 y2 + 0.5 + 0.7) with a uniform node u = act(x1 + 0.4) feeding it,
+    # output = linear(2 h + x2 - 1.25): a bias reaches every activation in both kinds of node
+    g = {"kind": np.array([0, 1, 2, 3, 4, 6, 5, 5], np.uint8),
+         "act": np.array([0] * 5 + [0, act, act], np.uint8),
+         "bias": np.array([0, 0, 0, 0, 0, -1.25, 0.7, 0.4], np.float32),
+         "src": np.array([2, 3, 4, 6, 2, 0, 7], np.int32),
+         "dst": np.array([6, 6, 6, 5, 5, 7, 6], np.int32),
+         "w": np.array([3.0, -2.0, 0.5, 2.0, 1.0, 1.0, 0.75], np.float32),
+         "enabled": np.ones(7, np.uint8)}
+    a, b = raw_both(emr, [g], W.xor_sources(), 5)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    for policy in (emr.EMR_JIT_OFF, emr.EMR_JIT_ALWAYS):
+        emr.emr_set_jit(policy)
+        check_raw(emr, [g], W.xor_sources(), 5)

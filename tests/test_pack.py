@@ -52,6 +52,27 @@ def test_packed_programs_match_oracle_population(seed):
         _check_genome(g)
 
 
+@pytest.mark.parametrize("seed", range(3))
+def test_packed_programs_match_oracle_with_biases(seed):
+    # nonzero node biases on every hidden and output node: a varying node's bias is folded per
+    # source into its first record's bias row (scaled by its activation's input gain), a uniform
+    # node's bias stays in the uniform program, and a uniform output keeps its own
+    for g in W.population(100 + seed, 40, 20, 60, biases=True):
+        assert np.any(g["bias"] != 0)
+        _check_genome(g)
+
+
+@pytest.mark.parametrize("act", range(6))
+def test_packed_biased_node_of_each_activation(act):
+    # hidden h = act(3 x2 - 2 y2 + 0.5 + bias 0.7), output = linear(2 h + x2 - 1.25); and a uniform
+    # node u = act(x1 + 0.4) feeding h, so both kinds of node carry a bias into each activation
+    g = mk([0, 1, 2, 3, 4, 6, 5, 5], [0] * 5 + [0, act, act],
+           [(2, 6, 3.0), (3, 6, -2.0), (4, 6, 0.5), (6, 5, 2.0), (2, 5, 1.0), (0, 7, 1.0),
+            (7, 6, 0.75)])
+    g["bias"] = np.array([0, 0, 0, 0, 0, -1.25, 0.7, 0.4], np.float32)
+    _check_genome(g)
+
+
 def test_packed_programs_match_oracle_large_genomes():
     for g in W.population(11, 12, 40, 120):
         _check_genome(g, D=3)

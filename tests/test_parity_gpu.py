@@ -322,27 +322,46 @@ def test_direction_duality_bit_exact(emr):
 
 # ------------------------------------------------------------------------------- full size
 
-def test_full_size_xor_pop1000_depth7_sampled(emr):
-    """The benchmark's workload and launch: 1000 genomes x 4 sources at depth 7, one discover
-    call; the oracle recomputes a deterministic sample of whole pairs."""
-    genomes, sources, D, theta = W.workload("xor_pop1000_d7")
-    theta32 = float(np.float32(theta))
-    pop = emr.emr_pack_population(genomes)
-    res = emr.emr_discover(pop, sources, D, theta32)
-    emr.emr_result_check(res)
-    counts, recs = emr.records_to_host(res)
-    rng = np.random.default_rng(123)
-    sample = sorted(rng.choice(len(counts), size=16, replace=False).tolist())
-    for r in sample:
-        g, s = genomes[r // 4], sources[r % 4]
-        o = oracle.discover([g], [s], D, theta32)
-        gp, gw = recs[r]
-        if counts[r] == o["pair_count"][0] and np.array_equal(gp, o["parent"]):
-            assert close(gw, o["w4"]).all(), r
-        else:
-            diff = np.setxor1d(gp, o["parent"])
-            _, dvar = oracle.eval_parents(g, s, diff)
-            assert np.all(np.abs(dvar - theta32) <= BAND), (r, diff[:5], dvar[:5])
+@pytest.mark.parametrize("policy", ["always", "off"])
+def test_full_size_xor_pop1000_depth7_all_pairs(emr, policy):
+    """The benchmark's workload and launch: 1000 genomes x 4 sources at depth 7 in one call, under
+    the compiled tier (what the timed steps run) and under the interpreter, every pair and every
+    record against the oracle."""
+    emr.emr_set_jit(emr.EMR_JIT_ALWAYS if policy == "always" else emr.EMR_JIT_OFF)
+    try:
+        genomes, sources, D, theta = W.workload("xor_pop1000_d7")
+        pop = emr.emr_pack_population(genomes)
+        st = check_discover(emr, genomes, sources, D, theta, pop=pop)
+        assert st["records"] > 0
+        assert emr.emr_jit_info(pop)["state"] == (1 if policy == "always" else 0)
+    finally:
+        emr.emr_set_jit(emr.EMR_JIT_AUTO)
+
+
+def test_full_size_depth8_compiled(emr):
+    """Depth 8 (87,380 positions per source, the paper's depth-7 grid) under the compiled tier:
+    200 genomes of the XOR population recipe x 4 sources, every pair against the oracle."""
+    emr.emr_set_jit(emr.EMR_JIT_ALWAYS)
+    try:
+        genomes = W.population(0, 200, 20, 60)
+        pop = emr.emr_pack_population(genomes)
+        st = check_discover(emr, genomes, W.xor_sources(), 8, 0.03, pop=pop)
+        assert st["records"] > 0
+        assert emr.emr_jit_info(pop)["state"] == 1
+    finally:
+        emr.emr_set_jit(emr.EMR_JIT_AUTO)
+
+
+def test_raw_population_with_biases(emr):
+    """Nonzero node biases (hidden and output nodes): raw outputs against the oracle."""
+    genomes = W.population(51, 60, 20, 60, biases=True)
+    check_raw(emr, genomes, W.xor_sources(), 5)
+
+
+def test_discover_population_with_biases(emr):
+    genomes = W.population(52, 150, 20, 60, biases=True)
+    st = check_discover(emr, genomes, W.xor_sources(), 6, 0.03)
+    assert st["records"] > 0
 
 
 @pytest.mark.parametrize("D", [5, 6])
@@ -393,11 +412,10 @@ def test_config3_tabular_pop150_full(emr):
 
 
 def test_config4_recurrent_depth10_two_phases(emr):
-    """The recurrent workload at depth 10 on its first 6 genomes: phase 1 (the XOR sources) in
-    full against the oracle; hidden-to-hidden sources built from each side's own phase-1 output
-    agree; phase 2 (per-genome CSR sources, one per discovered hidden node) on sampled pairs."""
+    """The recurrent workload at depth 10: phase 1 (the XOR sources, all 100 genomes) against the
+    oracle; hidden-to-hidden sources built from each side's own phase-1 output agree; phase 2
+    (per-genome CSR sources, one per discovered hidden node) on 64 sampled pairs."""
     genomes, sources, D, theta = W.workload("recurrent_pop100")
-    genomes = genomes[:6]
     theta32 = float(np.float32(theta))
     pop = emr.emr_pack_population(genomes)
     res = emr.emr_discover(pop, sources, D, theta32)
@@ -414,15 +432,17 @@ def test_config4_recurrent_depth10_two_phases(emr):
             diff = np.setxor1d(gp, o["parent"][lo:hi])
             _, dvar = oracle.eval_parents(g, s, diff)
             assert np.all(np.abs(dvar - theta32) <= BAND)
+            common, gi, oi = np.intersect1d(gp, o["parent"][lo:hi], return_indices=True)
+            assert close(gw[gi], o["w4"][lo:hi][oi]).all(), r
         else:
-            assert close(gw, o["w4"][lo:hi]).all()
+            assert close(gw, o["w4"][lo:hi]).all(), r
     hs_o, offs_o = oracle.hidden_sources(o, len(genomes), sources, D)
     hs_g, offs_g = emr.hidden_sources(counts, recs, sources, D, len(genomes))
     if same:
         np.testing.assert_array_equal(offs_g, offs_o)
         np.testing.assert_array_equal(hs_g["x"], hs_o["x"].astype(np.float32))
         np.testing.assert_array_equal(hs_g["y"], hs_o["y"].astype(np.float32))
-    assert offs_o[-1] > 0
+    assert offs_o[-1] >= 64
     # phase 2 on the oracle's sources: records per pair are few, so regions of 8192 (look-back
     # placement) suffice; an overflow would be reported and retried at the reported size
     cap = 8192
@@ -436,17 +456,23 @@ def test_config4_recurrent_depth10_two_phases(emr):
         emr.emr_result_check(res2)
     counts2, recs2 = emr.records_to_host(res2)
     rng = np.random.default_rng(4)
-    for r in sorted(rng.choice(len(counts2), size=min(8, len(counts2)), replace=False).tolist()):
-        g = genomes[int(np.searchsorted(offs_o, r, side="right") - 1)]
-        s = hs_o[r]
-        oo = oracle.discover([g], [s], D, theta32)
+    sample = np.sort(rng.choice(len(counts2), size=64, replace=False))
+    # the sampled pairs as one oracle call: each sampled source with its own genome
+    owner = np.searchsorted(offs_o, sample, side="right") - 1
+    sub_offs = np.zeros(len(genomes) + 1, np.int32)
+    np.add.at(sub_offs, owner + 1, 1)
+    sub_offs = np.cumsum(sub_offs).astype(np.int32)
+    oo = oracle.discover(genomes, hs_o[sample], D, theta32, src_offsets=sub_offs)
+    for k, r in enumerate(sample):
+        lo, hi = oo["pair_offset"][k], oo["pair_offset"][k + 1]
+        op, ow = oo["parent"][lo:hi], oo["w4"][lo:hi]
         gp, gw = recs2[r]
         assert counts2[r] <= cap
-        if np.array_equal(gp, oo["parent"]):
-            assert close(gw, oo["w4"]).all(), r
+        if np.array_equal(gp, op):
+            assert close(gw, ow).all(), r
         else:
-            diff = np.setxor1d(gp, oo["parent"])
-            _, dvar = oracle.eval_parents(g, s, diff)
+            diff = np.setxor1d(gp, op)
+            _, dvar = oracle.eval_parents(genomes[owner[k]], hs_o[r], diff)
             assert np.all(np.abs(dvar - theta32) <= BAND), (r, diff[:5], dvar[:5])
 
 

@@ -7,6 +7,7 @@ import pytest
 
 import oracle
 from paper_2608_27612_amd import workloads as W
+from tests.test_parity_gpu import close
 
 pytestmark = pytest.mark.gpu
 
@@ -164,7 +165,7 @@ def test_stream_deep_single_depth9_matches_oracle(emr):
             _, dvar = oracle.eval_parents(genomes[0], sources[r], diff)
             assert np.all(np.abs(dvar - theta32) <= BAND), (r, diff[:5], dvar[:5])
         common, gi, oi = np.intersect1d(p, op, return_indices=True)
-        np.testing.assert_allclose(w[gi], ow[oi], rtol=1e-5, atol=1e-5)
+        assert close(w[gi], ow[oi]).all(), r
 
 
 def test_stream_deep_single_depth13_sampled(emr):
@@ -201,7 +202,7 @@ def test_stream_deep_single_depth13_sampled(emr):
             w = np.concatenate([b for _, b in samples[r]])
             ow, ovar = oracle.eval_parents(genomes[0], sources[r], p)
             assert np.all(ovar > theta32 - BAND)
-            np.testing.assert_allclose(w, ow, rtol=1e-5, atol=1e-5)
+            assert close(w, ow).all(), r
         cand = np.unique(rng.integers(0, Q, size=4000)).astype(np.uint32)
         _, cvar = oracle.eval_parents(genomes[0], sources[r], cand)
         delivered = np.isin(cand, allp)
