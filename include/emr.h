@@ -242,6 +242,33 @@ emr_status emr_eval_raw(const emr_population* pop, const emr_source* sources, in
                         const int32_t* src_offsets, int32_t n_shared, int32_t depth, float* out_dev,
                         void* workspace, int64_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------ allocation-free raw outputs
+ * For callers that cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation. */
+
+/* Size of the library's allocation-free scratch: a static array in the library's code object, one
+ * copy per device the library runs on, held until the process ends. */
+#define EMR_NOALLOC_SCRATCH_BYTES (32 << 20)
+
+/*
+ * emr_eval_raw without allocating: the same outputs (out_dev[r * N(D) + p], device, caller-owned,
+ * n_pairs * N(D) floats), computed by the interpreter (the compiled tier loads a module, so it is
+ * never used here), with every device buffer besides out_dev and err_dev in the scratch: the
+ * call's tables, the depth's tile geometry and the workspace. The call makes no device, pinned or
+ * host-registered allocation and loads no module; the only host memory it keeps is its plan,
+ * held by the population (one per distinct sources and depth used this way).
+ * err_dev: device, caller-owned, one word; the call's first kernel clears it and its kernels raise
+ * error bits into it (2: a table entry out of range, the affected outputs left unwritten), to be
+ * read after the stream's work completes.
+ * Errors: EMR_E_INVAL for bad arguments; EMR_E_LIMIT when the call's tables, tile geometry and
+ * workspace exceed EMR_NOALLOC_SCRATCH_BYTES (checked before anything is enqueued); EMR_E_DEVICE.
+ * Every call on a device shares that device's scratch and leaves its last contents there: calls
+ * that overlap in time on one device (other streams, other threads) race and must not be made.
+ */
+emr_status emr_eval_raw_noalloc(const emr_population* pop, const emr_source* sources,
+                                int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                                int32_t depth, float* out_dev, uint32_t* err_dev, void* stream);
+
 /* Algorithmic VALU work of one emr_discover call under the cost model documented with the
  * benchmark: total lane-operation slots (*slots) and number of queries (*queries). Per query of a
  * (genome, direction) program: one slot per position-dependent edge, the activations' slots

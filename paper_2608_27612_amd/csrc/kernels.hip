@@ -14,6 +14,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/emr.h"
 #include "emr_internal.h"
 #include "discover.h"
@@ -439,7 +441,35 @@ __global__ void k_grid(float* xy, int64_t n) {
   }
 }
 
+// ------------------------------------------------------------------------ allocation-free scratch
+// The device memory of emr_eval_raw_noalloc: a fixed array in the library's code object, so the
+// loader places one copy on every device the library runs on and nothing is allocated per call.
+// Host code never passes this name to a kernel (on the host it is only a stand-in for the
+// symbol); it passes the device address emr_noalloc_scratch looks up.
+static __device__ __align__(256) uint8_t scratch[EMR_NOALLOC_SCRATCH_BYTES];
+
 }  // namespace emr
+
+// The current device's address of the allocation-free scratch (EMR_NOALLOC_SCRATCH_BYTES bytes),
+// looked up with that device current on its first use and kept per device.
+extern "C" hipError_t emr_noalloc_scratch(void** out) {
+  static std::mutex mu;
+  static void* addr[256] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 256) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(emr::scratch));
+    if (e != hipSuccess) return e;
+    if (!p || ((uintptr_t)p & 255) != 0) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
 
 // ------------------------------------------------------------------------ launchers
 // Called by the host runtime (runtime.cpp); each returns the hipError_t of its launch.

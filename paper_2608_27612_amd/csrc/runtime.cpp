@@ -38,6 +38,7 @@ extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* p
                                         uint32_t* out_parent, float* out_w4, hipStream_t s);
 extern "C" hipError_t emr_launch_tile_geo(uint32_t* out, uint32_t tiles, uint32_t rows,
                                           hipStream_t s);
+extern "C" hipError_t emr_noalloc_scratch(void** out);
 extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t blocks, int per_cu,
                                          int cus, emr::DiscoverScalars* out, uint32_t* grid);
 // The compiled tier's template code object (jit_image.cpp).
@@ -240,6 +241,10 @@ struct emr_population {
   // The plan of the last call (see plan_for): calls with the same sources and depth reuse it.
   mutable std::mutex plan_mu;
   mutable std::shared_ptr<const Plan> plan;
+  // The plans of emr_eval_raw_noalloc calls (host memory only: they never get device tables or a
+  // compiled tier), one per distinct sources and depth, kept with the population so that a table
+  // image stays valid while its copy is in flight.
+  mutable std::vector<std::shared_ptr<const Plan>> noalloc_plans;
 };
 
 namespace {
@@ -660,19 +665,25 @@ emr_status take_flags(const void* workspace, hipStream_t s, CallFlags* f) {
   return EMR_OK;
 }
 
+// Where a call's kernels find the plan's tables and the depth's tile geometry: the plan's own
+// device copies (plan_tables, tile_geo_table), or copies in the allocation-free scratch.
+struct CallTables {
+  const char* tables = nullptr;
+  const uint32_t* geo = nullptr;
+  uint32_t geo_rows = 0;
+};
+
 // Clears the workspace's tile status words when the look-back placement needs them, and fills
 // the bind kernel's arguments over the plan's tables (*b: launched by the caller).
-emr_status prepare_plan(const emr_population* pop, const Plan& P, void* workspace,
-                        int64_t workspace_bytes, hipStream_t s, bool clear_status,
-                        uint32_t* flags, emr::BindArgs* bind) {
+emr_status prepare_plan(const emr_population* pop, const Plan& P, const CallTables& T,
+                        void* workspace, int64_t workspace_bytes, hipStream_t s,
+                        bool clear_status, uint32_t* flags, emr::BindArgs* bind) {
   if (!workspace || workspace_bytes < (int64_t)P.total)
     return fail(EMR_E_INVAL, "workspace of %lld bytes is smaller than the %zu needed",
                 (long long)workspace_bytes, P.total);
   if (((uintptr_t)workspace & 255) != 0) return fail(EMR_E_INVAL, "workspace not 256-byte aligned");
   char* ws = (char*)workspace;
-  char* tables = nullptr;
-  emr_status st = plan_tables(P, &tables);
-  if (st != EMR_OK) return st;
+  const char* tables = T.tables;
   if (clear_status)
     HIP_OR_FAIL(emr_launch_fill(ws + P.off_status, (int64_t)(P.status_bytes / 4), 0u, s));
 
@@ -924,17 +935,19 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
 // `finalize`, k_finalize then hands the call's flags to their pinned words.
 // With `bind`, the bind kernel goes right before the first discover launch, once every argument
 // of that launch is ready on the host (so the GPU does not wait for host work between them).
-emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
-                        const emr_result* out, float* raw, void* workspace, hipStream_t s,
-                        int64_t tile_lo, int64_t n_tiles, bool jit, const CallFlags& f,
-                        bool finalize, const emr::BindArgs* bind) {
+// flags: the call's device flag words (error bits, largest count); flags_host: their pinned words
+// (device view) for k_finalize.
+// timing: the thread's launch profiling applies to this call (off for the allocation-free call,
+// whose events would be created on first use).
+emr_status launch_range(const emr_population* pop, const Plan& P, const CallTables& T,
+                        float theta, const emr_result* out, float* raw, void* workspace,
+                        hipStream_t s, int64_t tile_lo, int64_t n_tiles, bool jit,
+                        uint32_t* flags, uint32_t* flags_host, bool finalize,
+                        const emr::BindArgs* bind, bool timing = true) {
   char* ws = (char*)workspace;
-  char* tables = nullptr;
-  emr_status tst = plan_tables(P, &tables);
-  if (tst != EMR_OK) return tst;
-  const uint32_t* geo_tab = nullptr;
-  uint32_t geo_rows = 0;
-  if ((tst = tile_geo_table(P.depth, &geo_tab, &geo_rows)) != EMR_OK) return tst;
+  const char* tables = T.tables;
+  const uint32_t* geo_tab = T.geo;
+  const uint32_t geo_rows = T.geo_rows;
   const int cus = device_cu_count();
   const int64_t parent_lo = emr::tile_parent_offset(tile_lo, P.depth);
   const int64_t range_parents = emr::tile_parent_offset(tile_lo + n_tiles, P.depth) - parent_lo;
@@ -951,7 +964,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
                 (long long)range_parents);
   Profiler& prof = g_prof;
   const size_t rec0 = prof.recs.size();
-  const bool timed_call = prof.on && prof.seen++ % prof.every == 0;
+  const bool timed_call = timing && prof.on && prof.seen++ % prof.every == 0;
   const size_t n_timed = timed_call ? (prof.first_only ? 1 : P.launches.size()) : 0;
   while (prof.events.size() < 2 * (rec0 + n_timed)) {
     hipEvent_t e;
@@ -972,7 +985,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
     a.bias_tab = (const float*)(ws + P.off_bias);
     a.status = (uint64_t*)(ws + P.off_status);
     a.nz = (uint64_t*)(ws + P.off_nz);
-    a.err = f.dev;
+    a.err = flags;
     a.parent = out ? out->parent : nullptr;
     a.w4 = out ? out->w4 : nullptr;
     a.pair_count = out ? out->pair_count : nullptr;
@@ -1024,7 +1037,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
   if (timed_call) prof.calls++;
   if (padded && P.n_pairs > 0)
     HIP_OR_FAIL(emr_launch_compact(
-        (const uint64_t*)(ws + P.off_status), out->parent, out->w4, out->pair_count, f.dev + 1,
+        (const uint64_t*)(ws + P.off_status), out->parent, out->w4, out->pair_count, flags + 1,
         (uint64_t*)(ws + P.off_nz),
         skip_uniform ? (const uint8_t*)(tables + P.t_uniform) : nullptr, out->pair_capacity,
         (uint32_t)tile_lo,
@@ -1032,25 +1045,38 @@ emr_status launch_range(const emr_population* pop, const Plan& P, float theta,
         (uint32_t)(P.depth < emr::kFirstAlignedLevel ? emr::n_parents(P.depth)
                                                      : emr::level_offset(emr::kFirstAlignedLevel) / 4),
         s));
-  if (finalize) HIP_OR_FAIL(emr_launch_finalize(f.dev, f.host_dev, s));
+  if (finalize) HIP_OR_FAIL(emr_launch_finalize(flags, flags_host, s));
   return EMR_OK;
+}
+
+// The plan's own device tables and the depth's tile geometry table (allocated on first use).
+emr_status call_tables(const Plan& P, CallTables* T) {
+  char* tables = nullptr;
+  emr_status st = plan_tables(P, &tables);
+  if (st != EMR_OK) return st;
+  T->tables = tables;
+  return tile_geo_table(P.depth, &T->geo, &T->geo_rows);
 }
 
 // Enqueue a whole call: take a flag slot, prepare, then every tile of every pair.
 emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const emr_result* out,
                     float* raw, void* workspace, int64_t workspace_bytes, hipStream_t s) {
   const bool lookback = out && !raw && out->pair_capacity < emr::n_parents(P.depth);
+  CallTables T;
+  emr_status st = call_tables(P, &T);
+  if (st != EMR_OK) return st;
   CallFlags f;
-  emr_status st = take_flags(workspace, s, &f);
+  st = take_flags(workspace, s, &f);
   if (st != EMR_OK) return st;
   emr::BindArgs bind{};
-  st = prepare_plan(pop, P, workspace, workspace_bytes, s, lookback, f.dev, &bind);
+  st = prepare_plan(pop, P, T, workspace, workspace_bytes, s, lookback, f.dev, &bind);
   if (st != EMR_OK) return st;
   bool jit = false;
   st = jit_use(pop, P, plan_slots(P), &jit);
   if (st != EMR_OK) return st;
   if (P.launches.empty()) HIP_OR_FAIL(emr_launch_bind(&bind, s));  // (no discover launch)
-  st = launch_range(pop, P, theta, out, raw, workspace, s, 0, P.tiles, jit, f, true,
+  st = launch_range(pop, P, T, theta, out, raw, workspace, s, 0, P.tiles, jit, f.dev, f.host_dev,
+                    true,
                     P.launches.empty() ? nullptr : &bind);
   if (st != EMR_OK) return st;
   f.ok = true;
@@ -1347,6 +1373,63 @@ emr_status emr_eval_raw(const emr_population* pop, const emr_source* sources, in
   return run_plan(pop, P, 0.0f, nullptr, out_dev, workspace, workspace_bytes, (hipStream_t)stream);
 }
 
+emr_status emr_eval_raw_noalloc(const emr_population* pop, const emr_source* sources,
+                                int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                                int32_t depth, float* out_dev, uint32_t* err_dev, void* stream) {
+  if (!pop) return fail(EMR_E_INVAL, "population is NULL");
+  if (!err_dev) return fail(EMR_E_INVAL, "err_dev is NULL");
+  // The plan: one of the population's host-only plans, built on first use for these arguments.
+  std::shared_ptr<const Plan> plan;
+  {
+    std::lock_guard<std::mutex> lock(pop->plan_mu);
+    for (const auto& q : pop->noalloc_plans)
+      if ((n_sources == 0 || sources) && n_sources >= 0 &&
+          plan_matches(*q, sources, n_sources, src_offsets, n_shared, depth, pop->n_genomes)) {
+        plan = q;
+        break;
+      }
+  }
+  if (!plan) {
+    auto P = std::make_shared<Plan>();
+    emr_status st = build_plan(pop, sources, n_sources, src_offsets, n_shared, depth, P.get());
+    if (st != EMR_OK) return st;
+    std::lock_guard<std::mutex> lock(pop->plan_mu);
+    pop->noalloc_plans.push_back(P);
+    plan = P;
+  }
+  const Plan& P = *plan;
+  if (P.n_pairs > 0 && emr::n_positions(depth) > 0 && !out_dev)
+    return fail(EMR_E_INVAL, "out_dev is NULL");
+  // Scratch layout: the plan's tables, the tile geometry rows, then the workspace.
+  const int64_t geo_rows = P.tiles + emr::kGeoPadRows;
+  const size_t off_geo = align256(P.img.size());
+  const size_t off_ws = align256(off_geo + (size_t)geo_rows * 16);
+  const size_t need = off_ws + P.total;
+  if (need > (size_t)EMR_NOALLOC_SCRATCH_BYTES)
+    return fail(EMR_E_LIMIT, "the call needs %zu bytes of scratch; the allocation-free scratch "
+                "holds %d", need, EMR_NOALLOC_SCRATCH_BYTES);
+  void* base = nullptr;
+  HIP_OR_FAIL(emr_noalloc_scratch(&base));
+  char* scr = (char*)base;
+  const hipStream_t s = (hipStream_t)stream;
+  CallTables T;
+  T.tables = scr;
+  T.geo = (const uint32_t*)(scr + off_geo);
+  T.geo_rows = (uint32_t)geo_rows;
+  char* ws = scr + off_ws;
+  // The call's first kernel clears the caller's error word; then the tables and the geometry.
+  HIP_OR_FAIL(emr_launch_fill(err_dev, 1, 0u, s));
+  HIP_OR_FAIL(hipMemcpyAsync(scr, P.img.data(), P.img.size(), hipMemcpyHostToDevice, s));
+  HIP_OR_FAIL(emr_launch_tile_geo((uint32_t*)(scr + off_geo), (uint32_t)P.tiles,
+                                  (uint32_t)geo_rows, s));
+  emr::BindArgs bind{};
+  emr_status st = prepare_plan(pop, P, T, ws, (int64_t)P.total, s, false, err_dev, &bind);
+  if (st != EMR_OK) return st;
+  if (P.launches.empty()) HIP_OR_FAIL(emr_launch_bind(&bind, s));  // (no discover launch)
+  return launch_range(pop, P, T, 0.0f, nullptr, out_dev, ws, s, 0, P.tiles, false, err_dev,
+                      nullptr, false, P.launches.empty() ? nullptr : &bind, false);
+}
+
 emr_status emr_discover_cost(const emr_population* pop, const emr_source* sources,
                              int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
                              int32_t depth, double transcendental_slots, double* slots,
@@ -1599,11 +1682,14 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     R.counts_h_pairs = std::max<int64_t>(n_pairs, 1);
   }
 
+  CallTables T;
+  st = call_tables(P, &T);
+  if (st != EMR_OK) return st;
   CallFlags f;  // the chunks raise into its words, handed over once at the end
   st = take_flags(nullptr, R.s, &f);
   if (st != EMR_OK) return st;
   emr::BindArgs bind{};
-  st = prepare_plan(pop, P, R.ws, (int64_t)P.total, R.s, false, f.dev, &bind);
+  st = prepare_plan(pop, P, T, R.ws, (int64_t)P.total, R.s, false, f.dev, &bind);
   if (st != EMR_OK) return st;
   HIP_OR_FAIL(emr_launch_bind(&bind, R.s));
   emr_result chunk_out{R.pad_parent, R.pad_w4, cap, R.counts, R.ws, (int64_t)P.total};
@@ -1618,8 +1704,8 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     if (R.copy_pending[b]) HIP_OR_FAIL(hipStreamWaitEvent(R.s, R.ev_copy[b], 0));
     const int64_t tile_lo = c * tpc, n = std::min<int64_t>(tpc, P.tiles - tile_lo);
     emr_status e =
-        launch_range(pop, P, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n, jit, f, false,
-                     nullptr);
+        launch_range(pop, P, T, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n, jit, f.dev,
+                     f.host_dev, false, nullptr);
     if (e != EMR_OK) return e;
     HIP_OR_FAIL(emr_launch_gather(R.counts, R.pad_parent, R.pad_w4, cap, (uint32_t)n_pairs,
                                   R.g_parent[b], R.g_w4[b], R.s));

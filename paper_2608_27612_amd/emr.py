@@ -26,8 +26,9 @@ ABI_FUNCTIONS = [
     "emr_free_population", "emr_population_info", "emr_workspace_bytes", "emr_discover",
     "emr_result_check", "emr_eval_raw", "emr_discover_cost", "emr_profile_enable",
     "emr_profile_read", "emr_stream_chunks", "emr_discover_stream", "emr_pack_population_flat",
-    "emr_set_jit", "emr_jit_info",
+    "emr_set_jit", "emr_jit_info", "emr_eval_raw_noalloc",
 ]
+EMR_NOALLOC_SCRATCH_BYTES = 32 << 20
 EMR_JIT_OFF, EMR_JIT_AUTO, EMR_JIT_ALWAYS = 0, 1, 2
 
 
@@ -95,6 +96,7 @@ def lib():
             "emr_pack_population_flat": (I32, [I32, P, P, P, P, P, P, P, P, P, P, P]),
             "emr_discover_stream": (I32, [P, P, I32, P, I32, I32, F32, I64, I64, SINK, P, P, P]),
             "emr_set_jit": (I32, [I32]),
+            "emr_eval_raw_noalloc": (I32, [P, P, I32, P, I32, I32, P, P, P]),
             "emr_jit_info": (I32, [P, P, P, P, P, P]),
         }
         for name, (res, args) in sig.items():
@@ -337,6 +339,19 @@ def emr_eval_raw(pop: Population, sources, depth: int, src_offsets=None, stream=
                               C.c_void_p(out.data_ptr() if out.numel() else 0),
                               C.c_void_p(ws.data_ptr()), ws.numel(), _stream_ptr(stream)))
     return out
+
+
+def emr_eval_raw_noalloc(pop: Population, sources, depth: int, out, err, src_offsets=None,
+                         stream=None):
+    """emr_eval_raw_noalloc into caller-owned device tensors: out float32 [n_pairs, N(D)] and err
+    (one int32 / uint32 word, cleared by the call, error bits after the stream's work)."""
+    offs = _offsets(src_offsets)
+    src = _sources(sources)
+    _check(lib().emr_eval_raw_noalloc(pop.handle, src.ctypes.data, len(sources),
+                                      None if offs is None else offs.ctypes.data,
+                                      0 if offs is not None else len(sources), depth,
+                                      C.c_void_p(out.data_ptr() if out.numel() else 0),
+                                      C.c_void_p(err.data_ptr()), _stream_ptr(stream)))
 
 
 def emr_discover_cost(pop: Population, sources, depth: int, src_offsets=None,
