@@ -170,10 +170,10 @@ def main():
     emr.emr_profile_enable(False)
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = queries / (ms_per_step * 1e-3)
-    records = int(res["pair_count"].clamp(max=res["pair_capacity"]).sum().item())
+    records = int(res["pair_offset"][-1].item())
 
-    # the padded-record mode of the discover kernel, compiled programs or the interpreter
-    kernel_name = "emr_discover_jit_padded" if compiled == {True} else "k_discover<1>"
+    # the record mode of the discover kernel, compiled programs or the interpreter
+    kernel_name = "emr_discover_jit_records" if compiled == {True} else "k_discover<1>"
     avg_ms = float(np.mean(launch_ms))
     achieved = launch_slots / (avg_ms * 1e-3)
 

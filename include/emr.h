@@ -109,7 +109,7 @@ typedef struct emr_population emr_population;
 /* Limits of one genome after dead-node pruning. */
 #define EMR_MAX_NODES 256   /* nodes in the genome as given */
 #define EMR_MAX_EDGES 4096  /* edges in the genome as given */
-#define EMR_MAX_LIVE 64     /* position-dependent values alive at once */
+#define EMR_MAX_LIVE 32     /* position-dependent values alive at once */
 
 /* Validates and packs n genomes, then copies the tables to the current device (synchronously).
  * On a validation failure returns EMR_E_INVAL / EMR_E_CYCLE / EMR_E_LIMIT and sets *bad_index to
@@ -141,31 +141,37 @@ emr_status emr_population_info(const emr_population* pop, int32_t* n_genomes, in
  * pair = g * n_shared + j. Otherwise src_offsets (host, [n_genomes+1], ascending, starting at 0)
  * gives genome g the sources src_offsets[g] .. src_offsets[g+1]-1 and pair = that source index. */
 
-/* Output of emr_discover (device buffers, caller-owned).
- * Records of pair r occupy the region [r*pair_capacity, (r+1)*pair_capacity): record i of that
- * pair is parent[r*pair_capacity + i] (the heap index of a kept cell) and
- * w4[4*(r*pair_capacity + i) + k] (the CPPN output at its child k), in ascending parent order,
- * for i < min(pair_count[r], pair_capacity). pair_count[r] is the true count; a count above
- * pair_capacity is an overflow (reported by emr_result_check) whose excess records are dropped.
- * pair_capacity = Q(D) can never overflow. */
+/* Output of emr_discover (device buffers, caller-owned): the kept cells of every pair, pairs back
+ * to back in pair order (CSR). Record i of pair r, i < pair_count[r], is
+ * parent[pair_offset[r] + i] (the heap index of a kept cell) and w4[4 * (pair_offset[r] + i) + k]
+ * (the CPPN output at its child k), each pair's records in ascending parent order;
+ * pair_offset[n_pairs] is the call's total. Counts and offsets are always exact; a total above
+ * `capacity` is an overflow (reported by emr_result_check with the total, so a retry can size the
+ * buffers), and then the records are not complete. Memory follows the kept cells: capacity is
+ * the caller's choice (n_pairs * Q(D) can never overflow). */
 typedef struct {
-  uint32_t* parent;      /* [n_pairs * pair_capacity] */
-  float* w4;             /* [n_pairs * pair_capacity * 4] */
-  int64_t pair_capacity; /* records per pair region, >= 0 */
+  uint32_t* parent;      /* [capacity] */
+  float* w4;             /* [capacity * 4] */
+  int64_t capacity;      /* records the buffers hold, 0 .. 2^32 - 1 */
   int64_t* pair_count;   /* [n_pairs] */
-  void* workspace;       /* device scratch, >= emr_workspace_bytes(...) bytes, 256-byte aligned */
+  int64_t* pair_offset;  /* [n_pairs + 1] */
+  void* workspace;       /* device scratch, >= emr_workspace_bytes(..., capacity) bytes, aligned to
+                            256 bytes */
   int64_t workspace_bytes;
 } emr_result;
 
-/* Device scratch (bytes) needed by emr_discover / emr_eval_raw for this population, these
- * sources (host) and this depth: tile status words, the compaction's tile-group marks and the
- * folded per-(genome, source) biases. The library keeps no state in it from one call to the next
- * (a call's error flags and largest count live in a library-owned slot, see emr_result_check).
- * Host only. (The grouping tables of a call live with the population: it keeps those of its last
- * sources and depth on the device, and a call with different ones replaces them.) */
+/* Device scratch (bytes) needed by an emr_discover call of this capacity (0 for emr_eval_raw) for
+ * this population, these sources (host) and this depth: per-tile status words, the compaction's
+ * tile-group marks and per-pair look-back words, the folded per-(genome, source) biases, and a
+ * record pool of `capacity` records (20 bytes each) that the discover kernel fills in any order
+ * and the compaction gathers from. The library keeps no state in it from one call to the next (a
+ * call's error flags, largest count and total live in a library-owned slot, see
+ * emr_result_check). EMR_E_INVAL for a capacity outside [0, 2^32 - 1]. Host only. (The grouping
+ * tables of a call live with the population: it keeps those of its last sources and depth on the
+ * device, and a call with different ones replaces them.) */
 emr_status emr_workspace_bytes(const emr_population* pop, const emr_source* sources,
                                int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
-                               int32_t depth, int64_t* bytes);
+                               int32_t depth, int64_t capacity, int64_t* bytes);
 
 /*
  * Eager discovery: for every pair (genome g, source s) and every parent cell P (levels 0..D-1),
@@ -181,14 +187,14 @@ emr_status emr_discover(const emr_population* pop, const emr_source* sources, in
                         const emr_result* out, void* stream);
 
 /* Waits for the latest discover (or raw-output) call made with out's workspace on the current
- * device, then reports EMR_E_CAPACITY if any pair_count exceeds pair_capacity (*max_count
- * receives the largest count, so a retry can size the regions), or EMR_E_DEVICE if a kernel
- * flagged an internal error. n_pairs is the number of pairs of the call; `stream` is not used
- * (the call's own completion is waited for, not the stream's later work). A call's flags live in
- * a library-owned ring of 256 slots per device, written by the call's last kernel straight to
- * pinned memory: a result is checked before 255 further calls on its device, and EMR_E_INVAL
- * reports a workspace with no call to check. */
-emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max_count,
+ * device, then reports EMR_E_DEVICE if a kernel flagged an internal error, or EMR_E_CAPACITY if
+ * the call found more records than out->capacity. *total (may be NULL) receives the records
+ * found, *max_count (may be NULL) the largest pair count. `stream` is not used (the call's own
+ * completion is waited for, not the stream's later work). A call's flags live in a library-owned
+ * ring of 256 slots per device, written by the call's last kernel straight to pinned memory: a
+ * result is checked before 255 further calls on its device, and EMR_E_INVAL reports a workspace
+ * with no call to check. */
+emr_status emr_result_check(const emr_result* out, int64_t* total, int64_t* max_count,
                             void* stream);
 
 /* ------------------------------------------------------------------ streaming
@@ -221,13 +227,15 @@ emr_status emr_stream_chunks(int32_t depth, int64_t chunk_positions, int64_t* n_
  * (0 for a full run; deliveries below it are skipped), and *next (may be NULL) receives the
  * cursor to resume from: n_chunks * n_pairs after a complete run, or, when the sink returns
  * nonzero, the cursor of the delivery it refused (status EMR_E_ABORTED). Returns when done.
- * Device memory: the library needs a workspace and three record buffers of
- * n_pairs * min(64 chunk_positions / 256, Q(D)) records (20 bytes each), plus pinned staging, a
- * side stream and events; it keeps them after the call for the next streamed call on the device
- * (grown when a call needs more, held until the process ends); EMR_E_LIMIT if the record buffers
- * would exceed 48 GiB (use smaller chunks).
+ * Device memory: the library needs a workspace whose record pool, and two chunk outputs, hold
+ * n_pairs * min(64 chunk_positions / 256, Q(D)) records each (20 bytes a record), plus pinned
+ * staging, a side stream and events; it keeps them after the call for the next streamed call on
+ * the device (grown when a call needs more, held until the process ends); EMR_E_LIMIT if the
+ * record buffers would exceed 48 GiB or 2^32 records (use smaller chunks).
  * Errors: EMR_E_INVAL for bad arguments (checked before any GPU work), EMR_E_NOMEM, EMR_E_DEVICE
- * (also when a kernel flagged an internal error), EMR_E_ABORTED.
+ * (also when a kernel flagged an internal error: checked before each chunk is delivered, so no
+ * record of a chunk computed after such an error reaches the sink; *next then holds the cursor of
+ * that chunk's first delivery), EMR_E_ABORTED.
  */
 emr_status emr_discover_stream(const emr_population* pop, const emr_source* sources,
                                int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,

@@ -54,10 +54,6 @@ __device__ __forceinline__ uint32_t popc64(uint64_t m) { return __builtin_popcou
 __device__ __forceinline__ uint32_t mbcnt64(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
-}
 
 // ------------------------------------------------------------------------ register windows
 // Walker<S, P, W>: the M = S * P instances' accumulators and varying values in pinned VGPRs, and
@@ -71,57 +67,6 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 // from all queueing on the one word.
 __device__ __forceinline__ void raise_max(uint32_t* p, uint32_t v) {
   if (v > __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicMax(p, v);
-}
-
-// ------------------------------------------------------------------------ look-back scan
-// Tile status words of one pair, indexed by tile. A tile publishes its local count as an
-// aggregate, sums predecessors (64 per probe, one per lane) back to the nearest inclusive
-// prefix, then publishes its own inclusive prefix. The kernel is launched cooperatively (every
-// wave is resident) and each wave walks its tiles in increasing order, so the lowest unfinished
-// tile always belongs to a running wave whose earlier tiles are done: waits always end. Each wait
-// is also bounded and, if the bound were ever hit, raises an error flag instead of spinning on.
-constexpr uint32_t kSpinLimit = 1u << 22;
-
-__device__ __forceinline__ void status_store(uint64_t* p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t status_load(uint64_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ uint64_t lookback(uint64_t* row, uint32_t tile, uint64_t count, uint32_t* err) {
-  const uint32_t lane = lane_id();
-  if (tile == 0) {
-    if (lane == 0) status_store(&row[0], kStatusInclusive | count);
-    return 0;
-  }
-  if (lane == 0) status_store(&row[tile], kStatusAggregate | count);
-  uint64_t prefix = 0;
-  int64_t j = (int64_t)tile - 1;
-  uint32_t spins = 0;
-  for (;;) {
-    const int64_t idx = j - (int64_t)lane;
-    const uint64_t s = idx >= 0 ? status_load(&row[idx]) : kStatusInclusive;
-    const uint64_t flag = s >> 62;
-    const uint64_t incl = ballot(flag == 2);
-    const uint64_t empty = ballot(flag == 0);
-    const uint32_t first = incl ? (uint32_t)__builtin_ctzll(incl) : 64u;
-    const uint64_t upto = first >= 63 ? ~0ull : ((2ull << first) - 1ull);
-    if (empty & upto) {
-      if (++spins > kSpinLimit) {
-        if (lane == 0) atomicOr(err, kErrLookback);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(2);
-      continue;
-    }
-    const uint64_t mine = ((upto >> lane) & 1ull) ? (s & kStatusValueMask) : 0ull;
-    prefix += wave_sum_u64(mine);
-    if (first < 64) break;
-    j -= 64;
-  }
-  if (lane == 0) status_store(&row[tile], kStatusInclusive | (prefix + count));
-  return prefix;
 }
 
 // ------------------------------------------------------------------------ discover kernel
@@ -202,26 +147,29 @@ struct DiscoverPtrs {
   cf32* bias;
   uint64_t* status;
   uint32_t* err;
-  uint32_t* parent;
-  float* w4;
-  int64_t* pair_count;
   float* raw;
 };
 
-// Padded placement: the record counts of a chunk's tiles, source s and tile chunk_tile + k held
-// in lane 16 s + k, stored by those lanes at once (the status words of the tiles outside the
-// launch range are never written).
+// Record mode: the status words of a chunk's tiles, source s and tile chunk_tile + k held in lane
+// 16 s + k (pool offset of the tile's records and their count), stored by those lanes at once (the
+// status words of the tiles outside the launch range are never written); and each source's
+// records of the chunk (totals[s], wave-uniform) added to its pair's total.
 template <int S>
 __device__ __forceinline__ void store_chunk_counts(const DiscoverPtrs& d, const DiscoverScalars& a,
                                                    const Group& G, uint32_t chunk_tile,
                                                    uint32_t chunk_end, uint32_t counts,
+                                                   uint32_t bases, const uint32_t* totals,
                                                    uint32_t lane) {
+#pragma unroll
+  for (int s = 0; s < S; ++s)
+    if (lane == 0 && totals[s] != 0u) atomicAdd(a.pair_total + G.pair[s], totals[s]);
   // one store per source (its pair id uniform), lanes 16 s .. 16 s + 15
   const uint32_t k = lane & 15u;
 #pragma unroll
   for (int s = 0; s < S; ++s)
     if ((lane >> 4) == (uint32_t)s && chunk_tile + k < chunk_end)
-      d.status[(int64_t)G.pair[s] * a.tiles + chunk_tile + k] = (uint64_t)counts;
+      d.status[(int64_t)G.pair[s] * a.tiles + chunk_tile + k] =
+          ((uint64_t)bases << kStatusCountBits) | (uint64_t)counts;
   // A chunk (a whole number of chunks fills a group of 64 tiles) that kept a cell marks its
   // group, so that the compaction of a long range visits only the groups with records.
   if (a.tiles > kNzMinGroups * kWave) {
@@ -282,18 +230,9 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
   if constexpr (MODE != kModeRaw) {
     if (n_rec == 0 && !(0.0f > a.theta16)) {
       // A uniform output has variance 0 everywhere: with theta >= 0 every tile of the chunk keeps
-      // nothing, and its counts (padded) or inclusive prefixes (look-back: all zero, no
-      // predecessor needed) are written at once.
-      if constexpr (MODE == kModePadded) {
-        store_chunk_counts<S>(d, a, G, chunk_tile, chunk_end, 0u, lane);
-      } else if (lane == 0) {
-        for (uint32_t t = chunk_tile; t < chunk_end; ++t)
-#pragma unroll
-          for (int s = 0; s < S; ++s) {
-            status_store(d.status + (int64_t)G.pair[s] * a.tiles + t, kStatusInclusive);
-            if (t + 1 == a.tiles) d.pair_count[G.pair[s]] = 0;
-          }
-      }
+      // nothing, and its counts are written at once.
+      const uint32_t none[S] = {};
+      store_chunk_counts<S>(d, a, G, chunk_tile, chunk_end, 0u, 0u, none, lane);
       return;
     }
   }
@@ -307,9 +246,12 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
   if constexpr (JIT)
     rows = *reinterpret_cast<const __attribute__((address_space(4))) u32x16*>(
         d.bias + G.bias_off + 4u);
-  // Padded placement: the chunk's record counts, source s and tile chunk_tile + k in lane
-  // 16 s + k; they stay zero unless a walk keeps a cell, and go out with one store per chunk.
-  uint32_t chunk_counts = 0;
+  // Record mode: the chunk's record counts and pool offsets, source s and tile chunk_tile + k in
+  // lane 16 s + k; they stay zero unless a walk keeps a cell, and go out with one store per chunk.
+  uint32_t chunk_counts = 0, chunk_bases = 0;
+  uint32_t chunk_total[S];  // records of the chunk per source (wave-uniform)
+#pragma unroll
+  for (int s = 0; s < S; ++s) chunk_total[s] = 0u;
   // The geometry rows of the walk's tiles, loaded one walk ahead from gp (the rows of the next
   // walk's tiles). The host sizes the table for the launch's range plus kGeoPadRows rows of
   // padding (emr_discover_setup), which the last walks' loads reach; a walk past the range end
@@ -430,58 +372,50 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
       for (int k = 0; k < TPW; ++k) mx = __builtin_fmaxf(mx, s2[s][k]);
     const bool some = ballot(mx > a.theta16) != 0ull;
 
-    if constexpr (MODE == kModePadded) {
+    if constexpr (MODE == kModeRecords) {
       if (some) {
+        // The walk's kept cells, source s and tile k: one pool reservation for all of them (one
+        // atomic per walk that keeps anything), then each (s, k) segment in (s, k) order.
+        uint64_t kb[S][TPW];
+        uint32_t n_walk = 0;
 #pragma unroll
         for (int s = 0; s < S; ++s)
 #pragma unroll
           for (int k = 0; k < TPW; ++k) {
-            const uint64_t kb = ballot(s2[s][k] > a.theta16) & vmask[k];
-            if (lane == 16u * (uint32_t)s + min(t0 + (uint32_t)k - chunk_tile, 15u))
-              chunk_counts = popc64(kb);
-            if ((kb >> lane) & 1ull) {
-              // a tile's records start at its first parent index within the pair
-              const int64_t slot = (int64_t)G.pair[s] * a.cap + ((p0[k] >> 2) - a.parent_lo) +
-                                   mbcnt64(kb);
-              d.parent[slot] = (p0[k] >> 2) + lane;
+            kb[s][k] = ballot(s2[s][k] > a.theta16) & vmask[k];
+            n_walk += popc64(kb[s][k]);
+          }
+        uint64_t off = 0;
+        if (lane == 0)
+          off = atomicAdd((unsigned long long*)a.pool_ctr, (unsigned long long)n_walk);
+        off = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(off >> 32)) << 32) |
+              __builtin_amdgcn_readfirstlane((uint32_t)off);
 #pragma unroll
-              for (int c4 = 0; c4 < 4; ++c4) d.w4[slot * 4 + c4] = w[s * P + 4 * k + c4];
+        for (int s = 0; s < S; ++s)
+#pragma unroll
+          for (int k = 0; k < TPW; ++k) {
+            const uint32_t cnt = popc64(kb[s][k]);
+            chunk_total[s] += cnt;
+            if (lane == 16u * (uint32_t)s + min(t0 + (uint32_t)k - chunk_tile, 15u)) {
+              chunk_counts = cnt;
+              chunk_bases = (uint32_t)off;  // (a pool offset beyond 2^32 exceeds any capacity)
             }
-          }
-      }
-    }
-    if constexpr (MODE == kModeLookback) {
-      // ---- each tile learns its exact offset within each pair from the look-back scan, in
-      // increasing tile order
+            if ((kb[s][k] >> lane) & 1ull) {
+              const uint64_t idx = off + mbcnt64(kb[s][k]);
+              if (idx < (uint64_t)a.cap) {
+                a.pool_parent[idx] = (p0[k] >> 2) + lane;
 #pragma unroll
-      for (int k = 0; k < TPW; ++k) {
-        const uint32_t tile = t0 + k;
-        if (tile >= a.tiles) break;
-#pragma unroll
-        for (int s = 0; s < S; ++s) {
-          const uint64_t kb = some ? ballot(s2[s][k] > a.theta16) & vmask[k] : 0ull;
-          const uint64_t cnt = popc64(kb);
-          const uint32_t pair = G.pair[s];
-          const uint64_t base = lookback(d.status + (int64_t)pair * a.tiles, tile, cnt, d.err);
-          if (tile + 1 == a.tiles && lane == 0) {
-            d.pair_count[pair] = (int64_t)(base + cnt);
-            raise_max(d.err + 1, (uint32_t)min(base + cnt, (uint64_t)0xFFFFFFFFu));
-          }
-          if ((kb >> lane) & 1ull) {
-            const int64_t idx = (int64_t)base + (int64_t)mbcnt64(kb);
-            if (idx < a.cap) {
-              const int64_t slot = (int64_t)pair * a.cap + idx;
-              d.parent[slot] = (p0[k] >> 2) + lane;
-#pragma unroll
-              for (int c4 = 0; c4 < 4; ++c4) d.w4[slot * 4 + c4] = w[s * P + 4 * k + c4];
+                for (int c4 = 0; c4 < 4; ++c4) a.pool_w4[idx * 4 + c4] = w[s * P + 4 * k + c4];
+              }
             }
+            off += cnt;
           }
-        }
       }
     }
   }
-  if constexpr (MODE == kModePadded)
-    store_chunk_counts<S>(d, a, G, chunk_tile, chunk_end, chunk_counts, lane);
+  if constexpr (MODE == kModeRecords)
+    store_chunk_counts<S>(d, a, G, chunk_tile, chunk_end, chunk_counts, chunk_bases, chunk_total,
+                          lane);
 }
 
 // One launch: every part, each chunk dispatched to the code of its part's (S, W). Chunks are
@@ -496,19 +430,19 @@ __device__ __forceinline__ void discover_body(const uint32_t* __restrict__ geo_t
                                               const Group* __restrict__ groups,
                                               const float* __restrict__ bias_tab,
                                               uint64_t* __restrict__ status, uint32_t* __restrict__ err,
-                                              uint32_t* __restrict__ parent, float* __restrict__ w4,
-                                              int64_t* __restrict__ pair_count, float* __restrict__ raw,
-                                              const DiscoverScalars& a, uint64_t code_base) {
+                                              float* __restrict__ raw, const DiscoverScalars& a,
+                                              uint64_t code_base) {
   const uint32_t lane = lane_id();
   const uint32_t i_lo = (lane & 1u) | ((lane >> 1) & 2u) | ((lane >> 2) & 4u);
   const uint32_t j_lo = ((lane >> 1) & 1u) | ((lane >> 2) & 2u) | ((lane >> 3) & 4u);
   const LaneGeo geo{{(float)(4u * i_lo), (float)(4u * i_lo + 2u)},
                     {(float)(4u * j_lo), (float)(4u * j_lo + 2u)}};
   const DiscoverPtrs d{(cu32*)geo_tab, (cu32*)blob, (cu32*)groups, (cf32*)bias_tab, status, err,
-                       parent, w4, pair_count, raw};
+                       raw};
   const uint32_t n_waves = gridDim.x * (blockDim.x / kWave);
   const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +
                                                        threadIdx.x / kWave);
+
   for (uint32_t c = wave; c < a.n_chunks; c += n_waves) {
     // the chunk's part, and its index within the part
     uint32_t k = 0, cl = c;

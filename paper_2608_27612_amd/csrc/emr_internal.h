@@ -100,8 +100,7 @@ struct Group {
   uint32_t pair[kMaxGroup];  // global pair ids of the sources (unused entries repeat the last)
 };
 
-// Device error flags (first word of a workspace).
-constexpr uint32_t kErrLookback = 1u;  // a look-back wait hit its bound
+// Device error bits (word kFlagErr of a call's flag slot).
 constexpr uint32_t kErrTable = 2u;     // a table entry pointed outside its table (entry skipped)
 constexpr uint32_t kMaxSteps = 256;
 constexpr uint32_t kMaxRecords = kMaxSteps + 4096 / kRecEdges + 1;
@@ -113,11 +112,6 @@ struct Member {
   uint32_t bias_base;  // its group's bias_off + its slot in the group
   uint32_t bias_rows;  // rows owned by its group (n_rec + 2)
 };
-
-// Look-back tile status word: flag in bits 62..63, value in bits 0..61.
-constexpr uint64_t kStatusAggregate = 1ull << 62;
-constexpr uint64_t kStatusInclusive = 2ull << 62;
-constexpr uint64_t kStatusValueMask = (1ull << 62) - 1;
 
 // Positions per lane per program walk. A lane holds whole sibling quads: the four children of
 // one parent (P = 4) or of a parent in each of P / 4 consecutive tiles (P = 8, 16), so a cell's
@@ -170,28 +164,44 @@ struct DiscoverPart {
   uint32_t n_chunks, chunks_per_group, chunk_tiles;
 };
 struct DiscoverScalars {
-  int64_t cap, n_pos;
-  // The launch covers tiles tile_lo .. tile_lo + tiles - 1 of every pair; record slots of a pair
-  // region count from parent_lo, the first parent index of tile tile_lo.
-  uint32_t tile_lo, parent_lo, tiles;
+  int64_t cap, n_pos;  // cap: records the pool holds
+  // The launch covers tiles tile_lo .. tile_lo + tiles - 1 of every pair.
+  uint32_t tile_lo, tiles;
   uint32_t n_parts, n_chunks;  // chunks of all parts
   DiscoverPart part[kMaxParts];
   int32_t depth;
   float theta16;  // 16 theta
   uint32_t code_bytes;  // compiled tier: size of the code area (0 for the interpreter)
-  // Padded placement over more than 2 groups of 64 tiles: bit g % 64 of nz[pair * nz_words +
-  // g / 64] marks a group g of the range that kept a cell (k_compact visits only those).
+  // Records over more than 2 groups of 64 tiles: bit g % 64 of nz[pair * nz_words + g / 64]
+  // marks a group g of the range that kept a cell (k_compact visits only those).
   uint64_t* nz;
   uint32_t nz_words;
   uint32_t blob_words, n_pairs;
   uint32_t bias_floats;  // the host keeps the bias table below 2^32 floats
   uint32_t head_parents;  // parents in a pair's tile 0 (levels 1..3, or all levels of a shallower grid)
+  // Record mode: the pool's reservation counter, the pool, and the per-pair record totals (each
+  // chunk adds its sources' counts; zero when the launch starts).
+  uint64_t* pool_ctr;
+  uint32_t* pool_parent;
+  float* pool_w4;
+  uint32_t* pair_total;
 };
 
-// Output modes: raw CPPN outputs; records at fixed per-tile slots (pair_capacity >= Q(D)),
-// compacted afterwards by k_compact; records placed directly through the look-back scan (any
-// capacity).
-constexpr int kModeRaw = 0, kModePadded = 1, kModeLookback = 2;
+// Output modes: raw CPPN outputs; records of kept cells, each walk's reserved in a pool with one
+// atomic, each tile's pool offset and count left in its status word and each chunk's count added
+// to its pair's total, for k_scan (pair offsets) and k_move (per-pair contiguous lists).
+constexpr int kModeRaw = 0, kModeRecords = 1;
+
+// A tile's status word in record mode: its records' pool offset << 8 | their count (<= 64).
+constexpr uint32_t kStatusCountBits = 8;
+
+// Call flag words (a library-owned slot of kSlotWords words per call, zero when a call takes it and
+// cleared again by the call's last kernel).
+constexpr int kFlagErr = 0;      // error bits
+constexpr int kFlagMax = 1;      // largest pair count (saturating u32)
+constexpr int kFlagPool = 2;     // u64: the pool's reservation counter (words 2, 3)
+constexpr int kFlagTotal = 6;    // u64: records found by the call (words 6, 7)
+constexpr int kFlagWords = 8;
 
 // ---------------------------------------------------------------- compiled tier
 // A walk calls its group's compiled program (machine code written at run time into the code area
@@ -249,27 +259,51 @@ struct DiscoverArgs {
   const uint32_t* blob;
   const Group* groups;     // the plan's group table (parts index into it)
   const float* bias_tab;
-  uint64_t* status;        // [n_pairs_total * tiles]
-  uint64_t* nz;            // padded placement: group marks (DiscoverScalars::nz)
-  uint32_t* err;           // device error flags
-  uint32_t* parent;
-  float* w4;
-  int64_t* pair_count;
+  uint64_t* status;        // [n_pairs * tiles] tile status words of the range
+  uint64_t* nz;            // group marks (DiscoverScalars::nz)
+  uint32_t* err;           // the call's flag words (kFlag*)
+  uint32_t* pool_parent;   // record mode: the pool (cap records)
+  float* pool_w4;
+  uint32_t* pair_total;    // record mode: per-pair record totals
   float* raw;              // raw-output mode: [pair][N]
-  int64_t cap;             // records per pair region
+  int64_t cap;             // records the pool holds
   int64_t n_pos;           // N(depth)
   // The launch's parts: groups part_group0[k] .. + part_groups[k] - 1, with part_S[k] sources
   // per walk and register window part_W[k], in launch order.
   uint32_t n_parts;
   uint32_t part_S[kMaxParts], part_W[kMaxParts], part_group0[kMaxParts], part_groups[kMaxParts];
   uint32_t tile_lo;        // first tile of the launch (of every pair)
-  uint32_t parent_lo;      // first parent index of tile tile_lo (record slots count from it)
   uint32_t tiles;          // tiles of the launch per pair
   int32_t depth;
   float theta;
   uint32_t blob_words;     // size of the population table
   uint32_t n_pairs;        // pairs of the call (bound for pair ids)
   uint64_t bias_floats;    // size of the bias table
+};
+
+// Arguments of the compaction of one record-mode range: k_scan (the pairs' offsets, one
+// workgroup) then k_move (one wave per pair).
+struct ScanArgs {
+  uint32_t* pair_total;  // [n_pairs] per-pair totals of the range (cleared by k_scan after use)
+  int64_t* pair_count;   // [n_pairs] out
+  int64_t* pair_offset;  // [n_pairs + 1] out
+  uint32_t* flags;       // the call's flag words (kFlag*)
+  uint32_t* host;        // non-NULL: the call's pinned flag words (device view); k_scan then
+                         // hands the flags over and clears them (the call's last flag writer)
+  uint32_t n_pairs;
+};
+struct MoveArgs {
+  const uint64_t* status;  // [n_pairs * tiles]
+  const uint32_t* pool_parent;
+  const float* pool_w4;
+  uint32_t* parent;
+  float* w4;
+  const int64_t* pair_count;
+  const int64_t* pair_offset;
+  uint64_t* nz;
+  const uint8_t* skip;   // per pair: 1 = its groups were left out of the launch (no records)
+  int64_t cap;
+  uint32_t tiles, n_pairs, nz_words;
 };
 
 struct BindArgs {
@@ -286,6 +320,8 @@ struct BindArgs {
   uint64_t bias_floats;
   uint64_t* nz;            // the compaction's group marks, cleared by the bind kernel
   uint32_t nz_words;
+  uint32_t* pair_total;    // record mode: per-pair totals, cleared by the bind kernel
+  uint32_t n_pairs;
 };
 
 }  // namespace emr

@@ -27,21 +27,16 @@ __device__ __forceinline__ uint64_t code_area_base() {
   const uint32_t *__restrict__ geo, const uint32_t *__restrict__ blob,                          \
       const emr::Group *__restrict__ groups,                                                    \
       const float *__restrict__ bias_tab, uint64_t *__restrict__ status,                        \
-      uint32_t *__restrict__ err, uint32_t *__restrict__ parent, float *__restrict__ w4,        \
-      int64_t *__restrict__ pair_count, float *__restrict__ raw, emr::DiscoverScalars a
+      uint32_t *__restrict__ err, float *__restrict__ raw, emr::DiscoverScalars a
 
-// One kernel per output mode (raw outputs, padded records, look-back records).
+// One kernel per output mode (raw outputs, records to the pool).
 extern "C" __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) emr_discover_jit_raw(EMR_JIT_PARAMS) {
-  emr::discover_body<emr::kModeRaw, true>(geo, blob, groups, bias_tab, status, err, parent, w4,
-                                          pair_count, raw, a, emr::code_area_base());
+  emr::discover_body<emr::kModeRaw, true>(geo, blob, groups, bias_tab, status, err, raw, a,
+                                          emr::code_area_base());
 }
-extern "C" __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) emr_discover_jit_padded(EMR_JIT_PARAMS) {
-  emr::discover_body<emr::kModePadded, true>(geo, blob, groups, bias_tab, status, err, parent, w4,
-                                             pair_count, raw, a, emr::code_area_base());
-}
-extern "C" __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) emr_discover_jit_lookback(EMR_JIT_PARAMS) {
-  emr::discover_body<emr::kModeLookback, true>(geo, blob, groups, bias_tab, status, err, parent, w4,
-                                               pair_count, raw, a, emr::code_area_base());
+extern "C" __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) emr_discover_jit_records(EMR_JIT_PARAMS) {
+  emr::discover_body<emr::kModeRecords, true>(geo, blob, groups, bias_tab, status, err, raw, a,
+                                              emr::code_area_base());
 }
 
 // The code area: a never-launched function whose body ends .text. It is filled with s_endpgm,

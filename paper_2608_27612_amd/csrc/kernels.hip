@@ -7,10 +7,13 @@
 //   k_discover  the hot path: one lane per parent cell; each lane interprets the varying CPPN
 //               program for S sources of one genome at the cell's four children at once
 //               (Section 3.1, the batched query W), reduces the four siblings to their variance
-//               in registers, applies var > theta (Section 3.2, Eq. 2), and places the kept cells
-//               with a wave ballot at per-tile slots (compacted by k_compact) or through a
-//               per-pair decoupled look-back scan, so every pair's records land in ascending
-//               parent order with no atomics on the output.
+//               in registers, applies var > theta (Section 3.2, Eq. 2), and writes the kept cells
+//               to a record pool (one reservation per walk), each tile's pool offset and count to
+//               its status word.
+//   k_scan      one workgroup: the pairs' output offsets (exclusive scan of their totals), the
+//               call's total and largest count, and the hand-over of the call's flags.
+//   k_move      one wave per pair: gathers its records from the pool into its place in the
+//               call's output (pairs back to back, CSR), in ascending parent order.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -61,190 +64,199 @@ __device__ __forceinline__ float act_apply(uint32_t a, float z) {
 }
 
 // ------------------------------------------------------------------------ compaction
-// First parent index of a pair's tile T: tile 0 holds the parents of levels 1..3, every other tile
-// 64 parents.
-__device__ __forceinline__ uint32_t tile_parent_offset(uint32_t T) {
-  return T == 0 ? 0u : (uint32_t)(level_offset(kFirstAlignedLevel) / 4) + (T - 1) * (kTile / 4);
+// After a record-mode discover launch every tile of the range has left its status word (pool
+// offset << 8 | count) and every pair its total. k_scan turns the totals into output offsets
+// (pairs back to back in pair order: CSR), k_move gathers each pair's records from the pool to its
+// offset: tiles in increasing order, each tile's records in increasing lane (parent) order, so
+// each pair's records come out in ascending parent order. Records whose pool or output index is
+// beyond `cap`, or beyond their pair's count, are not moved (an overflowing call reports its
+// total, which exceeds the capacity; a pair whose tiles were skipped after a table error gets no
+// more than its count).
+
+// The call's flag words go to its pinned host words and are cleared for the slot's next call.
+__device__ __forceinline__ void hand_over_flags(uint32_t* flags, uint32_t* host) {
+  uint32_t v[kFlagWords];
+#pragma unroll
+  for (int k = 0; k < kFlagWords; ++k)
+    v[k] = __hip_atomic_load(flags + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  host[kFlagErr] = v[kFlagErr];
+  host[kFlagMax] = v[kFlagMax];
+  host[kFlagTotal] = v[kFlagTotal];
+  host[kFlagTotal + 1] = v[kFlagTotal + 1];
+#pragma unroll
+  for (int k = 0; k < kFlagWords; ++k)
+    __hip_atomic_store(flags + k, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Compaction of one pair by one wave, once every tile of the range has left its records at the
-// tile's own slots and its count in counts[pair * tiles + t]. The tiles go in groups of 64 in
-// increasing order: a group's counts are scanned and its records moved down to their final,
-// contiguous place. A range of more than two groups visits only the groups whose bit the discover
-// kernel set in the pair's words of `nz` (a group that kept nothing has no records to move), and
-// clears those words for the next range. Writes the pair's count and returns it.
-__device__ uint32_t compact_pair(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
-                                 float* __restrict__ w4, int64_t* __restrict__ pair_count,
-                                 uint64_t* __restrict__ nz, int64_t cap, uint32_t tile_lo,
-                                 uint32_t tiles, uint32_t pair, uint32_t head_slots,
-                                 uint32_t lane) {
-  const uint32_t parent_lo = tile_parent_offset(tile_lo);
-  const uint64_t* row = counts + (int64_t)pair * tiles;
-  const int64_t region = (int64_t)pair * cap;
-  const uint32_t n_groups = (tiles + kWave - 1) / kWave;
-  uint32_t running = 0;
-  // lane's tile count in group g (a tile holds at most its own slot count: 64, or the head
-  // tile's parents)
-  auto load_count = [&](uint32_t g) -> uint32_t {
-    const uint32_t t_lane = g * kWave + lane;
-    const uint32_t slots = tile_lo + t_lane == 0 ? head_slots : (uint32_t)(kTile / 4);
-    return t_lane < tiles ? min((uint32_t)row[t_lane], slots) : 0u;
-  };
-  auto group = [&](uint32_t g, uint32_t c) {
-    const uint32_t t0 = g * kWave;
-    // inclusive scan over the wave, bit-sliced: c < 128, so the counts of the lanes below are
-    // the sum over bits b of 2^b times the number of lanes below with bit b set (mbcnt)
-    uint32_t incl = c;
-#pragma unroll
-    for (int b = 0; b < 7; ++b) incl += mbcnt64(ballot((c >> b) & 1u)) << b;
-    // The group's records in batches of 64, lane l moving the batch's l-th record: its tile is
-    // the one (among the tiles with records) whose scan range holds it. A batch's loads all come
-    // before its stores, and no record moves up, so a batch never overwrites a later batch's
-    // records before they are read.
-    const uint32_t total = __builtin_amdgcn_readlane(incl, kWave - 1);
-    const uint64_t has = ballot(c != 0u);
-    for (uint32_t b = 0; b < total; b += kWave) {
-      const uint32_t q = b + lane;  // the record's rank among the group's records
-      uint32_t src = running + q;
-      for (uint64_t m = has; m != 0ull; m &= m - 1ull) {
-        const uint32_t i = (uint32_t)__builtin_ctzll(m);
-        const uint32_t hi = __builtin_amdgcn_readlane(incl, i);
-        const uint32_t lo = hi - __builtin_amdgcn_readlane(c, i);
-        if (q >= lo && q < hi) src = tile_parent_offset(tile_lo + t0 + i) - parent_lo + (q - lo);
-      }
-      const uint32_t dst = running + q;
-      if (q < total && src != dst) {
-        const uint32_t pv = parent[region + src];
-        const float4 wv = reinterpret_cast<const float4*>(w4)[region + src];
-        parent[region + dst] = pv;
-        reinterpret_cast<float4*>(w4)[region + dst] = wv;
-      }
-    }
-    running += total;
-  };
-  if (n_groups <= kNzMinGroups) {
-    // Both groups' counts are requested at once, and both groups' records move in one sequence
-    // of batches (rank q < total0 in group 0, else rank q - total0 in group 1), so a pair with
-    // few records waits for one round of record loads. Ranks ascend with the source slots and
-    // every record moves down, as within one group.
-    const uint32_t c0 = load_count(0), c1 = n_groups > 1 ? load_count(1) : 0u;
-    auto scan = [&](uint32_t c) {
-      uint32_t incl = c;
-#pragma unroll
-      for (int b = 0; b < 7; ++b) incl += mbcnt64(ballot((c >> b) & 1u)) << b;
-      return incl;
-    };
-    const uint32_t incl0 = scan(c0), incl1 = scan(c1);
-    const uint32_t total0 = __builtin_amdgcn_readlane(incl0, kWave - 1);
-    const uint32_t total = total0 + __builtin_amdgcn_readlane(incl1, kWave - 1);
-    const uint64_t has0 = ballot(c0 != 0u), has1 = ballot(c1 != 0u);
-    for (uint32_t b = 0; b < total; b += kWave) {
-      const uint32_t q = b + lane, q1 = q - total0;  // (q1 wraps above every range for q < total0)
-      uint32_t src = q;
-      for (uint64_t m = has0; m != 0ull; m &= m - 1ull) {
-        const uint32_t i = (uint32_t)__builtin_ctzll(m);
-        const uint32_t hi = __builtin_amdgcn_readlane(incl0, i);
-        const uint32_t lo = hi - __builtin_amdgcn_readlane(c0, i);
-        if (q >= lo && q < hi) src = tile_parent_offset(tile_lo + i) - parent_lo + (q - lo);
-      }
-      for (uint64_t m = has1; m != 0ull; m &= m - 1ull) {
-        const uint32_t i = (uint32_t)__builtin_ctzll(m);
-        const uint32_t hi = __builtin_amdgcn_readlane(incl1, i);
-        const uint32_t lo = hi - __builtin_amdgcn_readlane(c1, i);
-        if (q1 >= lo && q1 < hi)
-          src = tile_parent_offset(tile_lo + kWave + i) - parent_lo + (q1 - lo);
-      }
-      if (q < total && src != q) {
-        const uint32_t pv = parent[region + src];
-        const float4 wv = reinterpret_cast<const float4*>(w4)[region + src];
-        parent[region + q] = pv;
-        reinterpret_cast<float4*>(w4)[region + q] = wv;
-      }
-    }
-    running = total;
-  } else {
-    const uint32_t n_words = nz_words(tiles);
-    uint64_t* words = nz + (int64_t)pair * n_words;
-    for (uint32_t w0 = 0; w0 < n_words; w0 += kWave) {
-      const bool mine = w0 + lane < n_words;
-      const uint64_t bits = mine ? words[w0 + lane] : 0ull;
-      if (mine && bits != 0ull) words[w0 + lane] = 0ull;
-      // the marked groups of these words in increasing order (all values wave-uniform); each
-      // group's counts are requested before the previous group is compacted
-      uint64_t lanes = ballot(bits != 0ull), bw = 0ull;
-      uint32_t i = 0;
-      auto next = [&]() -> uint32_t {  // the next marked group, or ~0u
-        while (bw == 0ull) {
-          if (lanes == 0ull) return 0xFFFFFFFFu;
-          i = (uint32_t)__builtin_ctzll(lanes);
-          lanes &= lanes - 1ull;
-          bw = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(bits >> 32), i) << 32) |
-               __builtin_amdgcn_readlane((uint32_t)bits, i);
-        }
-        const uint32_t j = (uint32_t)__builtin_ctzll(bw);
-        bw &= bw - 1ull;
-        return (w0 + i) * kWave + j;
-      };
-      uint32_t g = next();
-      uint32_t c = g < n_groups ? load_count(g) : 0u;
-      while (g != 0xFFFFFFFFu) {
-        const uint32_t g2 = next();
-        const uint32_t c2 = g2 < n_groups ? load_count(g2) : 0u;
-        if (g < n_groups) group(g, c);
-        g = g2;
-        c = c2;
-      }
-    }
-  }
-  if (lane == 0) pair_count[pair] = running;
-  return running;
-}
-
-// The call's last kernel: its flags (error bits in flags[0], largest pair count in flags[1],
-// raised with device-scope atomics by the call's other kernels; zero when the call starts) go to
-// its pinned host words and are cleared for the slot's next call.
+// The call's last kernel when k_scan does not hand over its flags (raw outputs, streamed calls).
 __global__ void k_finalize(uint32_t* flags, uint32_t* host) {
   if (blockIdx.x != 0 || threadIdx.x != 0) return;
-  const uint32_t e = __hip_atomic_load(flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const uint32_t m = __hip_atomic_load(flags + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  host[0] = e;
-  host[1] = m;
-  __hip_atomic_store(flags, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __hip_atomic_store(flags + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  hand_over_flags(flags, host);
 }
 
-// Each wave takes pairs pair = wave, wave + n_waves, ...: compacts them once every discover launch
-// of the range has finished, and the workgroup's largest count is raised into *max_count with one
-// atomic. A pair with skip[pair] set (its groups were left out of the launch: they keep nothing)
-// gets a count of 0 without its tile counts being read.
-constexpr int kCompactWaves = 4;
+constexpr int kScanThreads = 1024;
 
-__global__ void __launch_bounds__(kCompactWaves * kWave)
-    k_compact(const uint64_t* __restrict__ counts, uint32_t* __restrict__ parent,
-              float* __restrict__ w4, int64_t* __restrict__ pair_count,
-              uint32_t* __restrict__ max_count, uint64_t* __restrict__ nz,
-              const uint8_t* __restrict__ skip, int64_t cap, uint32_t tile_lo, uint32_t tiles,
-              uint32_t n_pairs, uint32_t head_slots) {
-  __shared__ uint32_t wave_max[kCompactWaves];
-  const uint32_t lane = lane_id();
-  const uint32_t wv = threadIdx.x / kWave;
-  const uint32_t n_waves = gridDim.x * kCompactWaves;
-  uint32_t my_max = 0;
-  for (uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * kCompactWaves + wv);
-       pair < n_pairs; pair += n_waves) {
-    if (skip && skip[pair]) {
-      if (lane == 0) pair_count[pair] = 0;
-      continue;
+// One workgroup: pairs in rounds of kScanThreads, thread t taking pair round + t. Writes
+// pair_count, pair_offset (exclusive scan, pair_offset[n_pairs] = the total), clears the totals
+// for the next launch, resets the pool counter, raises the largest count and stores the total in
+// the flags, and, with A.host, hands the flags over.
+__global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs A) {
+  __shared__ uint64_t wsum[kScanThreads / kWave];
+  __shared__ uint32_t wmax[kScanThreads / kWave];
+  const uint32_t t = threadIdx.x, lane = t % kWave, wv = t / kWave;
+  uint64_t carry = 0;
+  uint32_t mx = 0;
+  for (uint32_t round = 0; round < A.n_pairs; round += kScanThreads) {
+    const uint32_t i = round + t;
+    const bool mine = i < A.n_pairs;
+    const uint32_t c = mine ? A.pair_total[i] : 0u;
+    if (mine) A.pair_total[i] = 0u;
+    mx = max(mx, c);
+    uint64_t incl = c;  // inclusive scan within the wave
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const uint64_t v = __shfl_up(incl, off, kWave);
+      if (lane >= (uint32_t)off) incl += v;
     }
-    my_max = max(my_max, compact_pair(counts, parent, w4, pair_count, nz, cap, tile_lo, tiles,
-                                      pair, head_slots, lane));
+    if (lane == kWave - 1) wsum[wv] = incl;
+    __syncthreads();
+    uint64_t before = 0, round_total = 0;
+#pragma unroll
+    for (int k = 0; k < kScanThreads / kWave; ++k) {
+      if ((uint32_t)k < wv) before += wsum[k];
+      round_total += wsum[k];
+    }
+    if (mine) {
+      A.pair_count[i] = c;
+      A.pair_offset[i] = (int64_t)(carry + before + incl - c);
+    }
+    carry += round_total;
+    __syncthreads();  // wsum is rewritten by the next round
   }
-  if (lane == 0) wave_max[wv] = my_max;
+  if (lane == 0) wmax[wv] = 0u;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off, kWave));
+  if (lane == 0) wmax[wv] = mx;
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (t == 0) {
     uint32_t m = 0;
-    for (int k = 0; k < kCompactWaves; ++k) m = max(m, wave_max[k]);
-    raise_max(max_count, m);
+    for (int k = 0; k < kScanThreads / kWave; ++k) m = max(m, wmax[k]);
+    A.pair_offset[A.n_pairs] = (int64_t)carry;
+    raise_max(A.flags + kFlagMax, m);
+    __hip_atomic_store((uint64_t*)(A.flags + kFlagTotal), carry, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    // every record of the range is in the pool: a next range reserves from 0
+    __hip_atomic_store((uint64_t*)(A.flags + kFlagPool), 0ull, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    if (A.host) hand_over_flags(A.flags, A.host);
+  }
+}
+
+// A tile's count from its status word, at most the 64 parents a tile holds.
+__device__ __forceinline__ uint32_t status_count(uint64_t w) {
+  return min((uint32_t)(w & ((1u << kStatusCountBits) - 1u)), (uint32_t)(kTile / 4));
+}
+
+// Inclusive scan of a per-lane count c < 128 over the wave, bit-sliced: the counts of the lanes
+// below are the sum over bits b of 2^b times the number of lanes below with bit b set (mbcnt).
+__device__ __forceinline__ uint32_t wave_incl_scan7(uint32_t c) {
+  uint32_t incl = c;
+#pragma unroll
+  for (int b = 0; b < 7; ++b) incl += mbcnt64(ballot((c >> b) & 1u)) << b;
+  return incl;
+}
+
+// Moves the records of one group of up to 64 tiles (lane l holds tile l's status word w and count
+// c, incl their inclusive scan): the group's rank q (the pair's rank at + q) goes from its tile's
+// pool segment to base + at + q, in batches of 64 ranks, lane l moving the batch's l-th record.
+__device__ __forceinline__ void move_group(const MoveArgs& A, uint64_t w, uint32_t c, uint32_t incl,
+                                           int64_t base, uint32_t at, uint32_t count,
+                                           uint32_t lane) {
+  const uint32_t total = __builtin_amdgcn_readlane(incl, kWave - 1);
+  const uint64_t has = ballot(c != 0u);
+  for (uint32_t b = 0; b < total; b += kWave) {
+    const uint32_t q = b + lane;
+    uint64_t src = ~0ull;
+    for (uint64_t m = has; m != 0ull; m &= m - 1ull) {
+      const uint32_t i = (uint32_t)__builtin_ctzll(m);
+      const uint32_t hi = __builtin_amdgcn_readlane(incl, i);
+      const uint32_t lo = hi - __builtin_amdgcn_readlane(c, i);
+      if (q >= lo && q < hi) {
+        const uint64_t wi = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(w >> 32), i) << 32) |
+                            __builtin_amdgcn_readlane((uint32_t)w, i);
+        src = (wi >> kStatusCountBits) + (q - lo);
+      }
+    }
+    const int64_t dst = base + at + q;
+    if (q < total && at + q < count && src < (uint64_t)A.cap && dst < A.cap) {
+      A.parent[dst] = A.pool_parent[src];
+      reinterpret_cast<float4*>(A.w4)[dst] = reinterpret_cast<const float4*>(A.pool_w4)[src];
+    }
+  }
+}
+
+// Visits the marked groups of a long range in increasing order, clearing the pair's marks: f(g) for
+// each group g whose bit is set in the pair's nz words.
+template <typename F>
+__device__ __forceinline__ void for_marked_groups(const MoveArgs& A, uint32_t pair, uint32_t lane,
+                                                  F&& f) {
+  const uint32_t n_groups = (A.tiles + kWave - 1) / kWave;
+  uint64_t* words = A.nz + (int64_t)pair * A.nz_words;
+  for (uint32_t w0 = 0; w0 < A.nz_words; w0 += kWave) {
+    const bool mine = w0 + lane < A.nz_words;
+    const uint64_t bits = mine ? words[w0 + lane] : 0ull;
+    if (mine && bits != 0ull) words[w0 + lane] = 0ull;
+    for (uint64_t lanes = ballot(bits != 0ull); lanes != 0ull; lanes &= lanes - 1ull) {
+      const uint32_t i = (uint32_t)__builtin_ctzll(lanes);
+      uint64_t bw = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(bits >> 32), i) << 32) |
+                    __builtin_amdgcn_readlane((uint32_t)bits, i);
+      for (; bw != 0ull; bw &= bw - 1ull) {
+        const uint32_t g = (w0 + i) * kWave + (uint32_t)__builtin_ctzll(bw);
+        if (g < n_groups) f(g);
+      }
+    }
+  }
+}
+
+// Each wave takes pairs wave, wave + n_waves, ...: the pair's count and offset from k_scan, then
+// its tiles' records group by group (a range of at most two groups reads both groups' status
+// words at once; a longer one visits only its marked groups).
+constexpr int kMoveWaves = 4;
+
+__global__ void __launch_bounds__(kMoveWaves * kWave) k_move(MoveArgs A) {
+  const uint32_t lane = lane_id();
+  const uint32_t n_waves = gridDim.x * kMoveWaves;
+  const uint32_t n_groups = (A.tiles + kWave - 1) / kWave;
+  for (uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * kMoveWaves + threadIdx.x / kWave);
+       pair < A.n_pairs; pair += n_waves) {
+    if (A.skip && A.skip[pair]) continue;  // no records, no marks
+    const uint32_t count = (uint32_t)min(A.pair_count[pair], (int64_t)0xFFFFFFFFll);
+    const int64_t base = A.pair_offset[pair];
+    const uint64_t* row = A.status + (int64_t)pair * A.tiles;
+    auto load = [&](uint32_t g) -> uint64_t {
+      const uint32_t t = g * kWave + lane;
+      return t < A.tiles ? row[t] : 0ull;
+    };
+    if (n_groups <= kNzMinGroups) {
+      if (count == 0u) continue;
+      const uint64_t w0 = load(0), w1 = n_groups > 1 ? load(1) : 0ull;
+      const uint32_t c0 = status_count(w0), c1 = status_count(w1);
+      const uint32_t incl0 = wave_incl_scan7(c0), incl1 = wave_incl_scan7(c1);
+      move_group(A, w0, c0, incl0, base, 0u, count, lane);
+      if (n_groups > 1)
+        move_group(A, w1, c1, incl1, base, __builtin_amdgcn_readlane(incl0, kWave - 1), count,
+                   lane);
+    } else {
+      uint32_t at = 0;
+      for_marked_groups(A, pair, lane, [&](uint32_t g) {
+        if (count == 0u) return;
+        const uint64_t w = load(g);
+        const uint32_t c = status_count(w);
+        const uint32_t incl = wave_incl_scan7(c);
+        move_group(A, w, c, incl, base, at, count, lane);
+        at += __builtin_amdgcn_readlane(incl, kWave - 1);
+      });
+    }
   }
 }
 
@@ -254,10 +266,8 @@ __global__ void __launch_bounds__(256)
     k_discover(const uint32_t* __restrict__ geo, const uint32_t* __restrict__ blob,
                const Group* __restrict__ groups,
                const float* __restrict__ bias_tab, uint64_t* __restrict__ status,
-               uint32_t* __restrict__ err, uint32_t* __restrict__ parent, float* __restrict__ w4,
-               int64_t* __restrict__ pair_count, float* __restrict__ raw, DiscoverScalars a) {
-  discover_body<MODE, false>(geo, blob, groups, bias_tab, status, err, parent, w4, pair_count, raw,
-                             a, 0ull);
+               uint32_t* __restrict__ err, float* __restrict__ raw, DiscoverScalars a) {
+  discover_body<MODE, false>(geo, blob, groups, bias_tab, status, err, raw, a, 0ull);
 }
 
 // The tile geometry table of a depth: row T (T >= 1, a level-aligned tile of 256 positions) holds
@@ -295,12 +305,18 @@ __global__ void __launch_bounds__(kBindWaves * kWave)
            const Member* __restrict__ members, const float* __restrict__ src_xy,
            float* __restrict__ bias_tab, uint32_t* __restrict__ err, uint32_t n_members,
            uint32_t n_desc, uint32_t n_sources, uint32_t blob_words, uint64_t bias_floats,
-           uint64_t* __restrict__ nz, uint32_t nz_words) {
+           uint64_t* __restrict__ nz, uint32_t nz_words, uint32_t* __restrict__ pair_total,
+           uint32_t n_pairs) {
   __shared__ float U_all[kBindWaves][kMaxU];
   __shared__ uint32_t prog_all[kBindWaves][kBindProgWords];
-  // the compaction's group marks start out clear (the discover kernel sets them)
+  // the compaction's group marks and per-pair totals start out clear (the discover kernel sets
+  // them)
   for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < nz_words; k += gridDim.x * blockDim.x)
     nz[k] = 0ull;
+  if (pair_total)
+    for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < n_pairs;
+         k += gridDim.x * blockDim.x)
+      pair_total[k] = 0u;
   const uint32_t lane = lane_id();
   const uint32_t wv = threadIdx.x / kWave;
   const uint32_t i = __builtin_amdgcn_readfirstlane(blockIdx.x * kBindWaves + wv);
@@ -379,47 +395,6 @@ __global__ void __launch_bounds__(kBindWaves * kWave)
   }
   if (bad) atomicOr(err, kErrTable);
   if (lane == 0) bias_tab[m.bias_base] = out_u == kNone ? 0.0f : U[out_u];
-}
-
-// ------------------------------------------------------------------------ gather
-// Packs the compacted records of all pairs into one contiguous list, pair after pair: pair r's
-// min(count_r, cap) records go to offset sum_{q < r} min(count_q, cap). Workgroup b handles pairs
-// 64 b .. 64 b + 63; it sums the counts before its first pair itself, so no other pass is needed.
-constexpr int kGatherPairs = 64;
-
-__global__ void __launch_bounds__(256)
-    k_gather(const int64_t* __restrict__ counts, const uint32_t* __restrict__ parent,
-             const float* __restrict__ w4, int64_t cap, uint32_t n_pairs,
-             uint32_t* __restrict__ out_parent, float* __restrict__ out_w4) {
-  __shared__ uint64_t part[256];
-  __shared__ uint64_t offs[kGatherPairs + 1];
-  const uint32_t first = blockIdx.x * kGatherPairs;
-  auto clamp = [&](uint32_t r) -> uint64_t {
-    const int64_t c = counts[r];
-    return (uint64_t)(c < 0 ? 0 : (c < cap ? c : cap));
-  };
-  uint64_t mine = 0;
-  for (uint32_t r = threadIdx.x; r < first; r += blockDim.x) mine += clamp(r);
-  part[threadIdx.x] = mine;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint64_t base = 0;
-    for (int k = 0; k < 256; ++k) base += part[k];
-    offs[0] = base;
-    for (int i = 0; i < kGatherPairs; ++i)
-      offs[i + 1] = offs[i] + (first + i < n_pairs ? clamp(first + i) : 0ull);
-  }
-  __syncthreads();
-  const uint32_t lane = lane_id();
-  for (uint32_t i = threadIdx.x / kWave; i < (uint32_t)kGatherPairs && first + i < n_pairs;
-       i += blockDim.x / kWave) {
-    const uint64_t n = offs[i + 1] - offs[i], dst = offs[i];
-    const int64_t src = (int64_t)(first + i) * cap;
-    for (uint64_t e = lane; e < n; e += kWave) {
-      out_parent[dst + e] = parent[src + e];
-      reinterpret_cast<float4*>(out_w4)[dst + e] = reinterpret_cast<const float4*>(w4)[src + e];
-    }
-  }
 }
 
 // ------------------------------------------------------------------------ small kernels
@@ -504,7 +479,8 @@ extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
   hipLaunchKernelGGL(emr::k_bind, dim3((a->n_members + emr::kBindWaves - 1) / emr::kBindWaves),
                      dim3(emr::kBindWaves * emr::kWave), 0, s, a->blob, a->desc,
                      a->members, a->src_xy, a->bias_tab, a->err, a->n_members, a->n_desc,
-                     a->n_sources, a->blob_words, a->bias_floats, a->nz, a->nz_words);
+                     a->n_sources, a->blob_words, a->bias_floats, a->nz, a->nz_words,
+                     a->pair_total, a->n_pairs);
   return hipGetLastError();
 }
 
@@ -536,7 +512,6 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   sc.cap = a->cap;
   sc.n_pos = a->n_pos;
   sc.tile_lo = a->tile_lo;
-  sc.parent_lo = a->parent_lo;
   sc.tiles = a->tiles;
   sc.n_parts = a->n_parts;
   uint64_t chunks = 0;
@@ -562,9 +537,12 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   sc.head_parents =
       (uint32_t)(a->depth < emr::kFirstAlignedLevel ? emr::n_parents(a->depth)
                                                     : emr::level_offset(emr::kFirstAlignedLevel) / 4);
-  // Clamp the grid to what can be resident at once: the waves walk their chunks. The look-back
-  // mode is launched cooperatively (the runtime refuses a grid that cannot be resident all at
-  // once), which its forward progress relies on; the other modes have no waits between waves.
+  sc.pool_ctr = (uint64_t*)(a->err + emr::kFlagPool);
+  sc.pool_parent = a->pool_parent;
+  sc.pool_w4 = a->pool_w4;
+  sc.pair_total = a->pair_total;
+  // Clamp the grid to what can be resident at once: the waves walk their chunks (no wave waits
+  // for another).
   const uint32_t resident = (uint32_t)per_cu * (uint32_t)cus;
   const uint32_t needed = (uint32_t)((chunks + 3) / 4);  // one wave per chunk, 4 per workgroup
   if (blocks > needed) blocks = needed;
@@ -605,20 +583,11 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
   const float* bias_tab = a->bias_tab;
   uint64_t* status = a->status;
   uint32_t* err = a->err;
-  uint32_t* parent = a->parent;
-  float* w4 = a->w4;
-  int64_t* pair_count = a->pair_count;
   float* raw = a->raw;
   if (start && (e = hipEventRecord(start, s)) != hipSuccess) return e;
-  if constexpr (MODE == emr::kModeLookback) {
-    void* args[] = {&geo, &blob, &grp, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw,
-                    &sc};
-    e = hipLaunchCooperativeKernel((const void*)kern, dim3(grid), dim3(256), args, 0, s);
-  } else {
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, geo, blob, grp, bias_tab, status, err,
-                       parent, w4, pair_count, raw, sc);
-    e = hipGetLastError();
-  }
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, geo, blob, grp, bias_tab, status, err, raw,
+                     sc);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   return stop ? hipEventRecord(stop, s) : hipSuccess;
 }
@@ -627,38 +596,27 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
 // most 256-thread workgroups (4 waves each) to launch; the launch uses at most one wave per chunk
 // of tiles and no more workgroups than can be resident at once; every wave walks its share of the
 // chunks. start, stop: events recorded on s around the launch, or NULL.
-// mode: 0 raw outputs, 1 padded records (then emr_launch_compact), 2 look-back records.
+// mode: 0 raw outputs, 1 records to the pool (then emr_launch_compact).
 extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int mode, uint32_t blocks,
                                           hipStream_t s, hipEvent_t start, hipEvent_t stop) {
   switch (mode) {
     case emr::kModeRaw: return launch_discover_t<emr::kModeRaw>(a, blocks, s, start, stop);
-    case emr::kModePadded: return launch_discover_t<emr::kModePadded>(a, blocks, s, start, stop);
-    case emr::kModeLookback:
-      return launch_discover_t<emr::kModeLookback>(a, blocks, s, start, stop);
+    case emr::kModeRecords: return launch_discover_t<emr::kModeRecords>(a, blocks, s, start, stop);
     default: return hipErrorInvalidValue;
   }
 }
 
-extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
-                                        const float* w4, int64_t cap, uint32_t n_pairs,
-                                        uint32_t* out_parent, float* out_w4, hipStream_t s) {
-  if (n_pairs == 0) return hipSuccess;
-  hipLaunchKernelGGL(emr::k_gather, dim3((n_pairs + emr::kGatherPairs - 1) / emr::kGatherPairs),
-                     dim3(256), 0, s, counts, parent, w4, cap, n_pairs, out_parent, out_w4);
-  return hipGetLastError();
-}
-
-extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
-                                         int64_t* pair_count, uint32_t* max_count, uint64_t* nz,
-                                         const uint8_t* skip, int64_t cap, uint32_t tile_lo,
-                                         uint32_t tiles, uint32_t n_pairs, uint32_t head_slots,
+// The compaction of one record-mode range (after its discover launch, on the same stream): the
+// pairs' offsets, then the records' move.
+extern "C" hipError_t emr_launch_compact(const emr::ScanArgs* S, const emr::MoveArgs* M,
                                          hipStream_t s) {
-  if (n_pairs == 0) return hipSuccess;
-  uint32_t blocks = (n_pairs + emr::kCompactWaves - 1) / emr::kCompactWaves;
+  if (S->n_pairs == 0) return hipSuccess;
+  hipLaunchKernelGGL(emr::k_scan, dim3(1), dim3(emr::kScanThreads), 0, s, *S);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  uint32_t blocks = (M->n_pairs + emr::kMoveWaves - 1) / emr::kMoveWaves;
   if (blocks > 8192) blocks = 8192;  // waves loop over pairs beyond this
-  hipLaunchKernelGGL(emr::k_compact, dim3(blocks), dim3(emr::kCompactWaves * emr::kWave), 0, s,
-                     counts, parent, w4, pair_count, max_count, nz, skip, cap, tile_lo, tiles,
-                     n_pairs, head_slots);
+  hipLaunchKernelGGL(emr::k_move, dim3(blocks), dim3(emr::kMoveWaves * emr::kWave), 0, s, *M);
   return hipGetLastError();
 }
 

@@ -224,11 +224,13 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       assigned[v] = sl;
       window = std::max(window, sl + 1);
     }
-    if (window > EMR_MAX_LIVE || window > kMaxWindow) {
+    // the declared limit is the kernels' widest register window (5-bit slot indices)
+    static_assert(EMR_MAX_LIVE == kMaxWindow && kMaxWindow <= (1 << kSlotBits), "window limit");
+    if (window > EMR_MAX_LIVE) {
       *st = EMR_E_LIMIT;
       char buf[128];
       std::snprintf(buf, sizeof buf, "needs %d live position-dependent values (limit %d)", window,
-                    std::min(EMR_MAX_LIVE, kMaxWindow));
+                    EMR_MAX_LIVE);
       *msg = buf;
       return false;
     }

@@ -27,15 +27,9 @@ extern "C" hipError_t emr_launch_grid(float* xy, int64_t n, hipStream_t s);
 extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s);
 extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int mode, uint32_t blocks,
                                           hipStream_t s, hipEvent_t start, hipEvent_t stop);
-extern "C" hipError_t emr_launch_compact(const uint64_t* counts, uint32_t* parent, float* w4,
-                                         int64_t* pair_count, uint32_t* max_count, uint64_t* nz,
-                                         const uint8_t* skip, int64_t cap, uint32_t tile_lo,
-                                         uint32_t tiles, uint32_t n_pairs, uint32_t head_slots,
+extern "C" hipError_t emr_launch_compact(const emr::ScanArgs* S, const emr::MoveArgs* M,
                                          hipStream_t s);
 extern "C" hipError_t emr_launch_finalize(uint32_t* flags, uint32_t* host, hipStream_t s);
-extern "C" hipError_t emr_launch_gather(const int64_t* counts, const uint32_t* parent,
-                                        const float* w4, int64_t cap, uint32_t n_pairs,
-                                        uint32_t* out_parent, float* out_w4, hipStream_t s);
 extern "C" hipError_t emr_launch_tile_geo(uint32_t* out, uint32_t tiles, uint32_t rows,
                                           hipStream_t s);
 extern "C" hipError_t emr_noalloc_scratch(void** out);
@@ -260,8 +254,8 @@ int window_bucket(int window) {
 struct JitModule {
   int device = -1;
   hipModule_t mod = nullptr;
-  hipFunction_t fn[3] = {};   // by output mode: raw, padded, look-back
-  int per_cu[3] = {1, 1, 1};  // workgroups per CU of each
+  hipFunction_t fn[2] = {};   // by output mode: raw, records
+  int per_cu[2] = {1, 1};     // workgroups per CU of each
   uint32_t code_bytes = 0;    // size of the code area
   emr::Group* d_groups = nullptr;  // the plan's group table with the code offsets
   size_t programs = 0, program_bytes = 0, image_bytes = 0;
@@ -337,12 +331,24 @@ struct Plan {
   std::vector<int32_t> key_offs;
   bool key_has_offs = false;
   int32_t key_n_shared = 0;
-  // Workspace layout (bytes from the workspace start).
+  // Workspace layout (bytes from the workspace start): tile status words, the compaction's group
+  // marks and per-pair record totals (both cleared by k_bind), the bias rows; then (total
+  // onwards) the record pool of a call's capacity.
   size_t off_status = 0;
   size_t off_bias = 0, total = 0;
-  size_t status_bytes = 0;  // cleared before a call only for look-back placement
-  size_t off_nz = 0, nz_bytes = 0;  // the compaction's group marks (cleared by k_bind)
+  size_t status_bytes = 0;
+  size_t off_nz = 0, nz_bytes = 0;
+  size_t off_ptotal = 0;
 };
+
+// The record pool after a plan's fixed workspace: `capacity` parent indices, then (16-byte
+// aligned) their float4 outputs.
+size_t pool_w4_offset(const Plan& P, int64_t capacity) {
+  return align256(P.total + (size_t)capacity * 4);
+}
+size_t workspace_need(const Plan& P, int64_t capacity) {
+  return capacity > 0 ? align256(pool_w4_offset(P, capacity) + (size_t)capacity * 16) : P.total;
+}
 
 emr_status build_plan(const emr_population* pop, const emr_source* sources, int32_t n_sources,
                       const int32_t* offs, int32_t n_shared, int32_t depth, Plan* plan) {
@@ -472,12 +478,13 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
     P.src_xy[2 * i + 1] = sources[i].y;
   }
 
-  // workspace: flags, tile status words, bias rows
+  // workspace: tile status words, group marks, per-pair totals, bias rows
   P.off_status = 0;
   P.status_bytes = (size_t)P.n_pairs * P.tiles * 8;
   P.off_nz = align256(P.off_status + P.status_bytes);
   P.nz_bytes = (size_t)P.n_pairs * emr::nz_words((uint32_t)P.tiles) * 8;
-  P.off_bias = align256(P.off_nz + P.nz_bytes);
+  P.off_ptotal = align256(P.off_nz + P.nz_bytes);
+  P.off_bias = align256(P.off_ptotal + (size_t)P.n_pairs * 4);
   // 16 floats of padding after the bias table: the compiled tier loads a group's rows 1 .. 4 at once
   P.total = align256(P.off_bias + (P.bias_floats + 16) * sizeof(float));
   // tables
@@ -570,7 +577,7 @@ emr_status plan_tables(const Plan& P, char** out) {
 // no copy of the flags goes either way, and the caller's workspace keeps no state from one call
 // to the next.
 constexpr int kFlagSlots = 256;
-constexpr int kSlotWords = 16;  // [0] errors, [1] largest count
+constexpr int kSlotWords = 16;  // the kFlag* words, then padding
 
 struct FlagRing {
   uint32_t* dev = nullptr;
@@ -656,8 +663,7 @@ emr_status take_flags(const void* workspace, hipStream_t s, CallFlags* f) {
   f->host_dev = R->host_dev + (size_t)k * kSlotWords;
   f->s = s;
   f->ws = workspace;
-  f->host[0] = 0u;
-  f->host[1] = 0u;
+  for (int k = 0; k < emr::kFlagWords; ++k) f->host[k] = 0u;
   if (R->dirty[k]) {
     HIP_OR_FAIL(emr_launch_fill(f->dev, kSlotWords, 0u, s));
     R->dirty[k] = false;
@@ -673,19 +679,18 @@ struct CallTables {
   uint32_t geo_rows = 0;
 };
 
-// Clears the workspace's tile status words when the look-back placement needs them, and fills
-// the bind kernel's arguments over the plan's tables (*b: launched by the caller).
+// Checks the workspace (need: its bytes for this call) and fills the bind kernel's arguments over
+// the plan's tables (*b: launched by the caller).
 emr_status prepare_plan(const emr_population* pop, const Plan& P, const CallTables& T,
-                        void* workspace, int64_t workspace_bytes, hipStream_t s,
-                        bool clear_status, uint32_t* flags, emr::BindArgs* bind) {
-  if (!workspace || workspace_bytes < (int64_t)P.total)
-    return fail(EMR_E_INVAL, "workspace of %lld bytes is smaller than the %zu needed",
-                (long long)workspace_bytes, P.total);
+                        void* workspace, int64_t workspace_bytes, int64_t need, hipStream_t s,
+                        uint32_t* flags, emr::BindArgs* bind) {
+  (void)s;
+  if (!workspace || workspace_bytes < need)
+    return fail(EMR_E_INVAL, "workspace of %lld bytes is smaller than the %lld needed",
+                (long long)workspace_bytes, (long long)need);
   if (((uintptr_t)workspace & 255) != 0) return fail(EMR_E_INVAL, "workspace not 256-byte aligned");
   char* ws = (char*)workspace;
   const char* tables = T.tables;
-  if (clear_status)
-    HIP_OR_FAIL(emr_launch_fill(ws + P.off_status, (int64_t)(P.status_bytes / 4), 0u, s));
 
   emr::BindArgs b{};
   b.blob = pop->d_blob;
@@ -701,6 +706,8 @@ emr_status prepare_plan(const emr_population* pop, const Plan& P, const CallTabl
   b.bias_floats = P.bias_floats;
   b.nz = (uint64_t*)(ws + P.off_nz);
   b.nz_words = (uint32_t)(P.nz_bytes / 8);
+  b.pair_total = (uint32_t*)(ws + P.off_ptotal);
+  b.n_pairs = (uint32_t)P.n_pairs;
   *bind = b;
   return EMR_OK;
 }
@@ -824,9 +831,8 @@ emr_status jit_build(const emr_population* pop, const Plan& P, std::unique_ptr<J
   const auto t1 = clock::now();
   HIP_OR_FAIL(hipGetDevice(&M->device));
   HIP_OR_FAIL(hipModuleLoadData(&M->mod, img.data()));
-  static const char* names[3] = {"emr_discover_jit_raw", "emr_discover_jit_padded",
-                                 "emr_discover_jit_lookback"};
-  for (int k = 0; k < 3; ++k) {
+  static const char* names[2] = {"emr_discover_jit_raw", "emr_discover_jit_records"};
+  for (int k = 0; k < 2; ++k) {
     HIP_OR_FAIL(hipModuleGetFunction(&M->fn[k], M->mod, names[k]));
     int n = 0;
     if (hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&n, M->fn[k], 256, 0) == hipSuccess && n > 0)
@@ -895,10 +901,6 @@ double plan_slots(const Plan& P) {
   return s * (double)emr::n_positions(P.depth);
 }
 
-// Enqueues the discover launch (every bucket, on the caller's stream) for tiles
-// tile_lo .. tile_lo + n_tiles - 1 of every pair, then the compaction when records go to padded
-// slots. Records of pair r go to its region of `out` counted from the range's first parent; raw
-// outputs to raw[r * N(D) + p].
 // The compiled tier's discover launch: the same scalars and grid sizing as the interpreter's,
 // through the plan's module.
 emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint32_t blocks,
@@ -916,21 +918,18 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
     const float* bias_tab = a.bias_tab;
     uint64_t* status = a.status;
     uint32_t* err = a.err;
-    uint32_t* parent = a.parent;
-    float* w4 = a.w4;
-    int64_t* pair_count = a.pair_count;
     float* raw = a.raw;
-    void* args[] = {&geo, &blob, &grp, &bias_tab, &status, &err, &parent, &w4, &pair_count, &raw,
-                    &sc};
-    if (mode == 2)  // look-back placement relies on every wave being resident
-      HIP_OR_FAIL(hipModuleLaunchCooperativeKernel(M.fn[mode], grid, 1, 1, 256, 1, 1, 0, s, args));
-    else
-      HIP_OR_FAIL(hipModuleLaunchKernel(M.fn[mode], grid, 1, 1, 256, 1, 1, 0, s, args, nullptr));
+    void* args[] = {&geo, &blob, &grp, &bias_tab, &status, &err, &raw, &sc};
+    HIP_OR_FAIL(hipModuleLaunchKernel(M.fn[mode], grid, 1, 1, 256, 1, 1, 0, s, args, nullptr));
   }
   if (stop) HIP_OR_FAIL(hipEventRecord(stop, s));
   return EMR_OK;
 }
 
+// Enqueues the discover launch (every bucket, on the caller's stream) for tiles
+// tile_lo .. tile_lo + n_tiles - 1 of every pair, then, for records, the compaction: the range's
+// records go to `out` pair after pair (pair_offset, pair_count), its capacity also bounding the
+// pool in the workspace; raw outputs go to raw[r * N(D) + p].
 // jit: run the plan's compiled programs (jit_use said so) instead of the interpreter. With
 // `finalize`, k_finalize then hands the call's flags to their pinned words.
 // With `bind`, the bind kernel goes right before the first discover launch, once every argument
@@ -949,19 +948,15 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
   const uint32_t* geo_tab = T.geo;
   const uint32_t geo_rows = T.geo_rows;
   const int cus = device_cu_count();
-  const int64_t parent_lo = emr::tile_parent_offset(tile_lo, P.depth);
-  const int64_t range_parents = emr::tile_parent_offset(tile_lo + n_tiles, P.depth) - parent_lo;
-  // Records go to fixed per-tile slots when every pair region can hold the worst case, and are
-  // compacted afterwards; a smaller capacity places them through the look-back scan instead.
-  const bool padded = out && out->pair_capacity >= range_parents;
-  const int mode = raw ? 0 : (padded ? 1 : 2);
+  const bool records = out != nullptr && raw == nullptr;
+  const int mode = records ? emr::kModeRecords : emr::kModeRaw;
   // With theta >= 0 a position-independent output keeps no cell (its variance is exactly 0): the
-  // padded placement leaves those groups (the last of each part) out of the launch, and the
+  // record mode leaves those groups (the last of each part) out of the launch, and the
   // compaction gives their pairs no records without reading their counts.
-  const bool skip_uniform = padded && !(0.0f > theta);
-  if (mode == 2 && (tile_lo != 0 || n_tiles != P.tiles))
-    return fail(EMR_E_INVAL, "a tile range needs pair_capacity >= its %lld parents",
-                (long long)range_parents);
+  const bool skip_uniform = records && !(0.0f > theta);
+  const int64_t cap = records ? out->capacity : 0;
+  uint32_t* pool_parent = records ? (uint32_t*)(ws + P.total) : nullptr;
+  float* pool_w4 = records ? (float*)(ws + pool_w4_offset(P, cap)) : nullptr;
   Profiler& prof = g_prof;
   const size_t rec0 = prof.recs.size();
   const bool timed_call = timing && prof.on && prof.seen++ % prof.every == 0;
@@ -986,11 +981,11 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
     a.status = (uint64_t*)(ws + P.off_status);
     a.nz = (uint64_t*)(ws + P.off_nz);
     a.err = flags;
-    a.parent = out ? out->parent : nullptr;
-    a.w4 = out ? out->w4 : nullptr;
-    a.pair_count = out ? out->pair_count : nullptr;
+    a.pool_parent = pool_parent;
+    a.pool_w4 = pool_w4;
+    a.pair_total = records ? (uint32_t*)(ws + P.off_ptotal) : nullptr;
     a.raw = raw;
-    a.cap = out ? out->pair_capacity : 0;
+    a.cap = cap;
     a.n_pos = emr::n_positions(P.depth);
     a.n_parts = (uint32_t)L.n_parts;
     for (int k = 0; k < L.n_parts; ++k) {
@@ -1001,7 +996,6 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
       a.part_groups[k] = skip_uniform ? bk.varying : bk.count;
     }
     a.tile_lo = (uint32_t)tile_lo;
-    a.parent_lo = (uint32_t)parent_lo;
     a.tiles = (uint32_t)n_tiles;
     a.depth = P.depth;
     a.theta = theta;
@@ -1035,16 +1029,32 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
     }
   }
   if (timed_call) prof.calls++;
-  if (padded && P.n_pairs > 0)
-    HIP_OR_FAIL(emr_launch_compact(
-        (const uint64_t*)(ws + P.off_status), out->parent, out->w4, out->pair_count, flags + 1,
-        (uint64_t*)(ws + P.off_nz),
-        skip_uniform ? (const uint8_t*)(tables + P.t_uniform) : nullptr, out->pair_capacity,
-        (uint32_t)tile_lo,
-        (uint32_t)n_tiles, (uint32_t)P.n_pairs,
-        (uint32_t)(P.depth < emr::kFirstAlignedLevel ? emr::n_parents(P.depth)
-                                                     : emr::level_offset(emr::kFirstAlignedLevel) / 4),
-        s));
+  if (records && P.n_pairs > 0) {
+    emr::ScanArgs S{};
+    S.pair_total = (uint32_t*)(ws + P.off_ptotal);
+    S.pair_count = out->pair_count;
+    S.pair_offset = out->pair_offset;
+    S.flags = flags;
+    S.host = finalize ? flags_host : nullptr;  // k_scan then ends the call's flag writes
+    S.n_pairs = (uint32_t)P.n_pairs;
+    emr::MoveArgs M{};
+    M.status = (const uint64_t*)(ws + P.off_status);
+    M.pool_parent = pool_parent;
+    M.pool_w4 = pool_w4;
+    M.parent = out->parent;
+    M.w4 = out->w4;
+    M.pair_count = out->pair_count;
+    M.pair_offset = out->pair_offset;
+    M.nz = (uint64_t*)(ws + P.off_nz);
+    M.skip = skip_uniform ? (const uint8_t*)(tables + P.t_uniform) : nullptr;
+    M.cap = cap;
+    M.tiles = (uint32_t)n_tiles;
+    M.n_pairs = (uint32_t)P.n_pairs;
+    M.nz_words = emr::nz_words((uint32_t)n_tiles);
+    HIP_OR_FAIL(emr_launch_compact(&S, &M, s));
+    return EMR_OK;
+  }
+  if (records) HIP_OR_FAIL(emr_launch_fill(out->pair_offset, 2, 0u, s));  // no pairs: offset 0
   if (finalize) HIP_OR_FAIL(emr_launch_finalize(flags, flags_host, s));
   return EMR_OK;
 }
@@ -1061,7 +1071,6 @@ emr_status call_tables(const Plan& P, CallTables* T) {
 // Enqueue a whole call: take a flag slot, prepare, then every tile of every pair.
 emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const emr_result* out,
                     float* raw, void* workspace, int64_t workspace_bytes, hipStream_t s) {
-  const bool lookback = out && !raw && out->pair_capacity < emr::n_parents(P.depth);
   CallTables T;
   emr_status st = call_tables(P, &T);
   if (st != EMR_OK) return st;
@@ -1069,7 +1078,8 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
   st = take_flags(workspace, s, &f);
   if (st != EMR_OK) return st;
   emr::BindArgs bind{};
-  st = prepare_plan(pop, P, T, workspace, workspace_bytes, s, lookback, f.dev, &bind);
+  st = prepare_plan(pop, P, T, workspace, workspace_bytes,
+                    (int64_t)workspace_need(P, out ? out->capacity : 0), s, f.dev, &bind);
   if (st != EMR_OK) return st;
   bool jit = false;
   st = jit_use(pop, P, plan_slots(P), &jit);
@@ -1295,13 +1305,14 @@ emr_status emr_population_info(const emr_population* pop, int32_t* n_genomes, in
 
 emr_status emr_workspace_bytes(const emr_population* pop, const emr_source* sources,
                                int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
-                               int32_t depth, int64_t* bytes) {
+                               int32_t depth, int64_t capacity, int64_t* bytes) {
   if (!bytes) return fail(EMR_E_INVAL, "bytes is NULL");
+  if (capacity < 0 || capacity > (int64_t)0xFFFFFFFFll)
+    return fail(EMR_E_INVAL, "capacity %lld outside [0, 2^32 - 1]", (long long)capacity);
   std::shared_ptr<const Plan> plan;
   emr_status st = plan_for(pop, sources, n_sources, src_offsets, n_shared, depth, &plan);
   if (st != EMR_OK) return st;
-  const Plan& P = *plan;
-  *bytes = (int64_t)P.total;
+  *bytes = (int64_t)workspace_need(*plan, capacity);
   return EMR_OK;
 }
 
@@ -1313,22 +1324,20 @@ emr_status emr_discover(const emr_population* pop, const emr_source* sources, in
   emr_status st = plan_for(pop, sources, n_sources, src_offsets, n_shared, depth, &plan);
   if (st != EMR_OK) return st;
   const Plan& P = *plan;
-  if (out->pair_capacity < 0) return fail(EMR_E_INVAL, "pair_capacity < 0");
-  if (P.n_pairs > 0) {
-    if (!out->pair_count) return fail(EMR_E_INVAL, "pair_count is NULL");
-    if (out->pair_capacity > 0 && (!out->parent || !out->w4))
-      return fail(EMR_E_INVAL, "parent/w4 is NULL with pair_capacity > 0");
-    if (out->pair_capacity > ((int64_t)1 << 40) / P.n_pairs)
-      return fail(EMR_E_LIMIT, "n_pairs * pair_capacity too large");
-  }
+  if (out->capacity < 0 || out->capacity > (int64_t)0xFFFFFFFFll)
+    return fail(EMR_E_INVAL, "capacity %lld outside [0, 2^32 - 1]", (long long)out->capacity);
+  if (!out->pair_offset) return fail(EMR_E_INVAL, "pair_offset is NULL");
+  if (P.n_pairs > 0 && !out->pair_count) return fail(EMR_E_INVAL, "pair_count is NULL");
+  if (out->capacity > 0 && (!out->parent || !out->w4))
+    return fail(EMR_E_INVAL, "parent/w4 is NULL with capacity > 0");
   return run_plan(pop, P, theta, out, nullptr, out->workspace, out->workspace_bytes,
                   (hipStream_t)stream);
 }
 
-emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max_count,
+emr_status emr_result_check(const emr_result* out, int64_t* total, int64_t* max_count,
                             void* stream) {
   (void)stream;
-  if (!out || n_pairs < 0) return fail(EMR_E_INVAL, "bad arguments");
+  if (!out) return fail(EMR_E_INVAL, "out is NULL");
   // the flag slot of the latest call with this result's workspace
   hipEvent_t ev = nullptr;
   const uint32_t* host = nullptr;
@@ -1349,15 +1358,18 @@ emr_status emr_result_check(const emr_result* out, int64_t n_pairs, int64_t* max
     return fail(EMR_E_INVAL, "no call with this workspace among the last %d calls on this device",
                 kFlagSlots);
   HIP_OR_FAIL(hipEventSynchronize(ev));
-  const uint32_t err = host[0];
-  const int64_t mx = host[1];
+  const uint32_t err = host[emr::kFlagErr];
+  const int64_t mx = host[emr::kFlagMax];
+  const int64_t found = (int64_t)(((uint64_t)host[emr::kFlagTotal + 1] << 32) |
+                                  host[emr::kFlagTotal]);
   if (max_count) *max_count = mx;
+  if (total) *total = found;
   if (err)
     return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (1: look-back wait bound, 2: a "
                 "table entry out of range)", err);
-  if (mx > out->pair_capacity)
-    return fail(EMR_E_CAPACITY, "a pair found %lld records; pair_capacity is %lld",
-                (long long)mx, (long long)out->pair_capacity);
+  if (found > out->capacity)
+    return fail(EMR_E_CAPACITY, "the call found %lld records; the capacity is %lld",
+                (long long)found, (long long)out->capacity);
   return EMR_OK;
 }
 
@@ -1423,7 +1435,8 @@ emr_status emr_eval_raw_noalloc(const emr_population* pop, const emr_source* sou
   HIP_OR_FAIL(emr_launch_tile_geo((uint32_t*)(scr + off_geo), (uint32_t)P.tiles,
                                   (uint32_t)geo_rows, s));
   emr::BindArgs bind{};
-  emr_status st = prepare_plan(pop, P, T, ws, (int64_t)P.total, s, false, err_dev, &bind);
+  emr_status st = prepare_plan(pop, P, T, ws, (int64_t)P.total, (int64_t)P.total, s, err_dev,
+                               &bind);
   if (st != EMR_OK) return st;
   if (P.launches.empty()) HIP_OR_FAIL(emr_launch_bind(&bind, s));  // (no discover launch)
   return launch_range(pop, P, T, 0.0f, nullptr, out_dev, ws, s, 0, P.tiles, false, err_dev,
@@ -1518,28 +1531,26 @@ emr_status emr_profile_read(emr_launch_profile* out, int32_t cap, int32_t* n) {
 // ------------------------------------------------------------------ streaming
 namespace {
 
-// Device and pinned buffers of one emr_discover_stream call. The destructor drains both streams
-// before freeing, so an early return (an error, or a sink that stops the run) never frees memory
-// a queued kernel or copy still uses.
 // The buffers, side stream and events of one streamed call. A call takes an idle set of its
 // device from a process-wide cache (or a new one), grows what is too small, and gives the set back
 // when it is done with it, so repeated streamed calls allocate nothing (a set is kept until the
-// process ends: at most the largest call's buffers per concurrent streamed call).
+// process ends: at most the largest call's buffers per concurrent streamed call). The destructor
+// drains both streams first, so an early return (an error, or a sink that stops the run) never
+// hands over memory that a queued kernel or copy still uses.
 struct StreamSet {
   int device = -1;
   hipStream_t side = nullptr;
   hipEvent_t ev_count[2] = {}, ev_copy[2] = {};
-  void* ws = nullptr;
-  uint32_t* pad_parent = nullptr;   // padded per-pair regions of the current chunk
-  float* pad_w4 = nullptr;
-  int64_t* counts = nullptr;        // per-pair counts of the current chunk
-  uint32_t* g_parent[2] = {};       // gathered records, double buffered
+  void* ws = nullptr;               // workspace, with the chunk's record pool
+  int64_t* counts = nullptr;        // per-pair counts and offsets of the current chunk
+  int64_t* offsets = nullptr;
+  uint32_t* g_parent[2] = {};       // each chunk's records (CSR), double buffered
   float* g_w4[2] = {};
-  int64_t* counts_h[2] = {};        // pinned copies of the counts
-  uint32_t* stage_parent[2] = {};   // pinned staging of the gathered records
+  int64_t* counts_h[2] = {};        // pinned: a chunk's counts, then its error flags (one word)
+  uint32_t* stage_parent[2] = {};   // pinned staging of a chunk's records
   float* stage_w4[2] = {};
   int64_t stage_cap[2] = {0, 0};
-  int64_t ws_bytes = 0, pad_records = 0, count_pairs = 0, g_records = 0, counts_h_pairs = 0;
+  int64_t ws_bytes = 0, count_pairs = 0, g_records = 0, counts_h_pairs = 0;
 };
 std::mutex g_stream_sets_mu;
 std::vector<StreamSet*> g_stream_sets;  // idle sets
@@ -1585,7 +1596,7 @@ bool reserve_device(void** p, int64_t* have, int64_t bytes) {
   return true;
 }
 
-// Largest device footprint of one streamed call's record buffers (padded + two gathered sets).
+// Largest device footprint of one streamed call's record buffers (the pool + two chunk outputs).
 constexpr int64_t kStreamBufferLimit = int64_t(48) << 30;
 
 }  // namespace
@@ -1625,10 +1636,11 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     if (next) *next = total;
     return EMR_OK;
   }
-  // A pair region holds a chunk's parents: at most 64 per tile, and never more than Q(D).
-  const int64_t cap = std::min<int64_t>(tpc * (emr::kTile / 4), emr::n_parents(depth));
-  const int64_t set_bytes = n_pairs * cap * 20;
-  if (set_bytes > kStreamBufferLimit / 3)
+  // A chunk keeps at most 64 parents per tile of each pair, and never more than Q(D) per pair.
+  const int64_t per_pair = std::min<int64_t>(tpc * (emr::kTile / 4), emr::n_parents(depth));
+  const int64_t records = n_pairs * per_pair;  // the pool's and each chunk output's capacity
+  const int64_t set_bytes = records * 20;
+  if (records > (int64_t)0xFFFFFFFFll || set_bytes > kStreamBufferLimit / 3)
     return fail(EMR_E_LIMIT, "%lld pairs x %lld-position chunks need %lld bytes of record buffers; "
                 "use smaller chunks", (long long)n_pairs, (long long)chunk_positions,
                 (long long)(3 * set_bytes));
@@ -1640,25 +1652,19 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     if (!R.ev_count[b]) HIP_OR_FAIL(hipEventCreateWithFlags(&R.ev_count[b], hipEventDisableTiming));
     if (!R.ev_copy[b]) HIP_OR_FAIL(hipEventCreateWithFlags(&R.ev_copy[b], hipEventDisableTiming));
   }
-  // record buffers by the records they hold (parents, then float4 outputs: sized together)
-  const int64_t records = n_pairs * cap;
+  const int64_t ws_need = (int64_t)workspace_need(P, records);
   int64_t have = 0;
-  bool ok = reserve_device(&R.ws, &R.ws_bytes, (int64_t)P.total);
-  if (ok && R.pad_records < records) {
-    have = R.pad_records * 4;
-    ok = reserve_device((void**)&R.pad_parent, &have, records * 4);
-    have = R.pad_records * 16;
-    ok = ok && reserve_device((void**)&R.pad_w4, &have, records * 16);
-    R.pad_records = ok ? records : 0;
-  }
-  if (ok && R.count_pairs < n_pairs) {
+  bool ok = reserve_device(&R.ws, &R.ws_bytes, ws_need);
+  if (ok && R.count_pairs < n_pairs + 1) {
     have = R.count_pairs * 8;
-    ok = reserve_device((void**)&R.counts, &have, n_pairs * 8);
-    R.count_pairs = ok ? n_pairs : 0;
+    ok = reserve_device((void**)&R.counts, &have, (n_pairs + 1) * 8);
+    have = R.count_pairs * 8;
+    ok = ok && reserve_device((void**)&R.offsets, &have, (n_pairs + 1) * 8);
+    R.count_pairs = ok ? n_pairs + 1 : 0;
   }
   if (!ok)
-    return fail(EMR_E_NOMEM, "device buffers of a streamed call (%lld bytes per record set)",
-                (long long)set_bytes);
+    return fail(EMR_E_NOMEM, "device buffers of a streamed call (%lld bytes of workspace)",
+                (long long)ws_need);
   if (R.g_records < records) {
     for (int b = 0; b < 2 && ok; ++b) {
       have = R.g_records * 4;
@@ -1667,19 +1673,19 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
       ok = ok && reserve_device((void**)&R.g_w4[b], &have, records * 16);
     }
     R.g_records = ok ? records : 0;
-    if (!ok) return fail(EMR_E_NOMEM, "gather buffers of a streamed call");
+    if (!ok) return fail(EMR_E_NOMEM, "record buffers of a streamed call");
   }
-  if (R.counts_h_pairs < std::max<int64_t>(n_pairs, 1)) {
+  if (R.counts_h_pairs < n_pairs + 1) {
     for (int b = 0; b < 2; ++b) {
       if (R.counts_h[b]) (void)hipHostFree(R.counts_h[b]);
       R.counts_h[b] = nullptr;
     }
     R.counts_h_pairs = 0;
     for (int b = 0; b < 2; ++b)
-      if (hipHostMalloc((void**)&R.counts_h[b], (size_t)std::max<int64_t>(n_pairs, 1) * 8,
-                        hipHostMallocDefault) != hipSuccess)
+      if (hipHostMalloc((void**)&R.counts_h[b], (size_t)(n_pairs + 1) * 8, hipHostMallocDefault) !=
+          hipSuccess)
         return fail(EMR_E_NOMEM, "pinned counts of a streamed call");
-    R.counts_h_pairs = std::max<int64_t>(n_pairs, 1);
+    R.counts_h_pairs = n_pairs + 1;
   }
 
   CallTables T;
@@ -1689,29 +1695,30 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
   st = take_flags(nullptr, R.s, &f);
   if (st != EMR_OK) return st;
   emr::BindArgs bind{};
-  st = prepare_plan(pop, P, T, R.ws, (int64_t)P.total, R.s, false, f.dev, &bind);
+  st = prepare_plan(pop, P, T, R.ws, R.ws_bytes, ws_need, R.s, f.dev, &bind);
   if (st != EMR_OK) return st;
   HIP_OR_FAIL(emr_launch_bind(&bind, R.s));
-  emr_result chunk_out{R.pad_parent, R.pad_w4, cap, R.counts, R.ws, (int64_t)P.total};
   bool jit = false;
   st = jit_use(pop, P, plan_slots(P) * (double)(total - start) / (double)total, &jit);
   if (st != EMR_OK) return st;
 
-  // Chunk c on the compute stream: discover + compact over its tiles, gather into buffer c & 1,
-  // counts to pinned memory.
+  // Chunk c on the compute stream: discover + compact over its tiles into buffer c & 1, then its
+  // counts and the call's error word to pinned memory.
   auto enqueue = [&](int64_t c) -> emr_status {
     const int b = (int)(c & 1);
     if (R.copy_pending[b]) HIP_OR_FAIL(hipStreamWaitEvent(R.s, R.ev_copy[b], 0));
     const int64_t tile_lo = c * tpc, n = std::min<int64_t>(tpc, P.tiles - tile_lo);
-    emr_status e =
-        launch_range(pop, P, T, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n, jit, f.dev,
-                     f.host_dev, false, nullptr);
+    emr_result chunk_out{R.g_parent[b], R.g_w4[b], records, R.counts, R.offsets, R.ws,
+                         R.ws_bytes};
+    emr_status e = launch_range(pop, P, T, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n, jit,
+                                f.dev, f.host_dev, false, nullptr);
     if (e != EMR_OK) return e;
-    HIP_OR_FAIL(emr_launch_gather(R.counts, R.pad_parent, R.pad_w4, cap, (uint32_t)n_pairs,
-                                  R.g_parent[b], R.g_w4[b], R.s));
     if (n_pairs > 0)
       HIP_OR_FAIL(hipMemcpyAsync(R.counts_h[b], R.counts, (size_t)n_pairs * 8,
                                  hipMemcpyDeviceToHost, R.s));
+    R.counts_h[b][n_pairs] = 0;
+    HIP_OR_FAIL(hipMemcpyAsync(R.counts_h[b] + n_pairs, f.dev + emr::kFlagErr, 4,
+                               hipMemcpyDeviceToHost, R.s));
     HIP_OR_FAIL(hipEventRecord(R.ev_count[b], R.s));
     return EMR_OK;
   };
@@ -1726,8 +1733,18 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
       if (st != EMR_OK) return st;
     }
     HIP_OR_FAIL(hipEventSynchronize(R.ev_count[b]));
+    // a kernel error raised up to this chunk stops the run before its records are delivered
+    const uint32_t err = (uint32_t)R.counts_h[b][n_pairs];
+    if (err) {
+      if (next) *next = c * n_pairs + (c == c0 ? skip : 0);
+      return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x at chunk %lld (1: look-back "
+                  "wait bound, 2: a table entry out of range)", err, (long long)c);
+    }
     int64_t n_rec = 0;
-    for (int64_t r = 0; r < n_pairs; ++r) n_rec += std::min<int64_t>(std::max<int64_t>(R.counts_h[b][r], 0), cap);
+    for (int64_t r = 0; r < n_pairs; ++r) n_rec += std::max<int64_t>(R.counts_h[b][r], 0);
+    if (n_rec > records)
+      return fail(EMR_E_DEVICE, "chunk %lld reports %lld records for a pool of %lld",
+                  (long long)c, (long long)n_rec, (long long)records);
     if (n_rec > R.stage_cap[b]) {
       if (R.stage_parent[b]) (void)hipHostFree(R.stage_parent[b]);
       if (R.stage_w4[b]) (void)hipHostFree(R.stage_w4[b]);
@@ -1754,7 +1771,7 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     }
     int64_t off = 0;
     for (int64_t r = 0; r < n_pairs; ++r) {
-      const int64_t nr = std::min<int64_t>(std::max<int64_t>(R.counts_h[b][r], 0), cap);
+      const int64_t nr = std::max<int64_t>(R.counts_h[b][r], 0);
       if (nr > 0 && !(c == c0 && r < skip)) {
         if (sink(r, c, R.stage_parent[b] + off, R.stage_w4[b] + 4 * off, nr, user) != 0) {
           if (next) *next = c * n_pairs + r;
@@ -1769,10 +1786,10 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
   HIP_OR_FAIL(emr_launch_finalize(f.dev, f.host_dev, R.s));
   HIP_OR_FAIL(hipStreamSynchronize(R.s));
   f.ok = true;
-  const uint32_t err = f.host[0];
+  const uint32_t err = f.host[emr::kFlagErr];
   if (err)
-    return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (2: a table entry out of range)",
-                err);
+    return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (1: look-back wait bound, 2: a "
+                "table entry out of range)", err);
   return EMR_OK;
 }
 

@@ -49,9 +49,9 @@ class emr_source(C.Structure):
 
 
 class emr_result(C.Structure):
-    _fields_ = [("parent", C.c_void_p), ("w4", C.c_void_p), ("pair_capacity", C.c_int64),
-                ("pair_count", C.c_void_p), ("workspace", C.c_void_p),
-                ("workspace_bytes", C.c_int64)]
+    _fields_ = [("parent", C.c_void_p), ("w4", C.c_void_p), ("capacity", C.c_int64),
+                ("pair_count", C.c_void_p), ("pair_offset", C.c_void_p),
+                ("workspace", C.c_void_p), ("workspace_bytes", C.c_int64)]
 
 
 class emr_launch_profile(C.Structure):
@@ -85,9 +85,9 @@ def lib():
             "emr_pack_population": (I32, [P, I32, P, P]),
             "emr_free_population": (None, [P]),
             "emr_population_info": (I32, [P, P, P, P, P]),
-            "emr_workspace_bytes": (I32, [P, P, I32, P, I32, I32, P]),
+            "emr_workspace_bytes": (I32, [P, P, I32, P, I32, I32, I64, P]),
             "emr_discover": (I32, [P, P, I32, P, I32, I32, F32, P, P]),
-            "emr_result_check": (I32, [P, I64, P, P]),
+            "emr_result_check": (I32, [P, P, P, P]),
             "emr_eval_raw": (I32, [P, P, I32, P, I32, I32, P, P, I64, P]),
             "emr_discover_cost": (I32, [P, P, I32, P, I32, I32, F64, P, P]),
             "emr_profile_enable": (I32, [I32, I32, F64]),
@@ -262,48 +262,56 @@ def n_pairs_of(pop: Population, sources, src_offsets=None) -> int:
     return len(sources) if src_offsets is not None else pop.n_genomes * len(sources)
 
 
-def emr_workspace_bytes(pop: Population, sources, depth: int, src_offsets=None) -> int:
+def emr_workspace_bytes(pop: Population, sources, depth: int, src_offsets=None,
+                        capacity: int = 0) -> int:
     offs = _offsets(src_offsets)
     b = C.c_int64()
     src = _sources(sources)
     _check(lib().emr_workspace_bytes(pop.handle, src.ctypes.data, len(sources),
                                      None if offs is None else offs.ctypes.data,
-                                     0 if offs is not None else len(sources), depth, C.byref(b)))
+                                     0 if offs is not None else len(sources), depth,
+                                     int(capacity), C.byref(b)))
     return b.value
 
 
-def alloc_result(pop: Population, sources, depth: int, src_offsets=None, pair_capacity=None):
-    """Device buffers for emr_discover (torch tensors); pair_capacity defaults to Q(D)."""
+# Default capacity of a result: the worst case n_pairs * Q(D) while its buffers stay below this
+# many records, else this many (a call that finds more reports its total; emr_discover_all then
+# retries at that size).
+DEFAULT_CAPACITY = 1 << 22
+
+
+def alloc_result(pop: Population, sources, depth: int, src_offsets=None, capacity=None):
+    """Device buffers for emr_discover (torch tensors): CSR records of `capacity` records."""
     import torch
     _, q = emr_grid_count(depth)
-    cap = q if pair_capacity is None else int(pair_capacity)
     npairs = n_pairs_of(pop, sources, src_offsets)
-    ws = emr_workspace_bytes(pop, sources, depth, src_offsets)
+    cap = min(npairs * q, DEFAULT_CAPACITY) if capacity is None else int(capacity)
+    ws = emr_workspace_bytes(pop, sources, depth, src_offsets, cap)
     return {
-        "parent": torch.empty((npairs, cap), dtype=torch.int32, device="cuda"),
-        "w4": torch.empty((npairs, cap, 4), dtype=torch.float32, device="cuda"),
-        "pair_count": torch.empty(npairs, dtype=torch.int64, device="cuda"),
+        "parent": torch.empty(max(cap, 1), dtype=torch.int32, device="cuda"),
+        "w4": torch.empty((max(cap, 1), 4), dtype=torch.float32, device="cuda"),
+        "pair_count": torch.empty(max(npairs, 1), dtype=torch.int64, device="cuda"),
+        "pair_offset": torch.empty(npairs + 1, dtype=torch.int64, device="cuda"),
         "workspace": torch.empty(max(ws, 256), dtype=torch.uint8, device="cuda"),
-        "pair_capacity": cap,
+        "capacity": cap,
         "n_pairs": npairs,
     }
 
 
 def _result_struct(res):
-    def ptr(t):
-        return t.data_ptr() if t.numel() else 0
     ws = res["workspace"]
     assert ws.data_ptr() % 256 == 0
-    return emr_result(ptr(res["parent"]), ptr(res["w4"]), res["pair_capacity"],
-                      ptr(res["pair_count"]), ws.data_ptr(), ws.numel())
+    return emr_result(res["parent"].data_ptr(), res["w4"].data_ptr(), res["capacity"],
+                      res["pair_count"].data_ptr(), res["pair_offset"].data_ptr(),
+                      ws.data_ptr(), ws.numel())
 
 
 def emr_discover(pop: Population, sources, depth: int, theta: float, res=None, src_offsets=None,
-                 stream=None, pair_capacity=None):
+                 stream=None, capacity=None):
     """Enqueue eager discovery; returns the result dict (device tensors, see alloc_result).
     `parent` is the int32 view of the library's uint32 heap indices."""
     if res is None:
-        res = alloc_result(pop, sources, depth, src_offsets, pair_capacity)
+        res = alloc_result(pop, sources, depth, src_offsets, capacity)
     offs = _offsets(src_offsets)
     out = _result_struct(res)
     res["_struct"] = out
@@ -315,12 +323,30 @@ def emr_discover(pop: Population, sources, depth: int, theta: float, res=None, s
     return res
 
 
-def emr_result_check(res, stream=None) -> int:
-    """Synchronize and check a discover result; returns the largest pair count."""
+def emr_result_check(res, stream=None):
+    """Synchronize and check a discover result; returns (total records, largest pair count)."""
     out = res.get("_struct") or _result_struct(res)
-    mx = C.c_int64()
-    _check(lib().emr_result_check(C.byref(out), res["n_pairs"], C.byref(mx), _stream_ptr(stream)))
-    return mx.value
+    total, mx = C.c_int64(), C.c_int64()
+    _check(lib().emr_result_check(C.byref(out), C.byref(total), C.byref(mx), _stream_ptr(stream)))
+    return total.value, mx.value
+
+
+def emr_discover_all(pop: Population, sources, depth: int, theta: float, src_offsets=None,
+                     stream=None, capacity=None):
+    """emr_discover + emr_result_check, retried once at the reported total when the capacity was
+    too small; returns the checked result."""
+    res = emr_discover(pop, sources, depth, theta, src_offsets=src_offsets, stream=stream,
+                       capacity=capacity)
+    try:
+        emr_result_check(res, stream)
+    except EmrError as e:
+        if e.status != EMR_E_CAPACITY:
+            raise
+        total = int(res["pair_offset"][-1].item())
+        res = emr_discover(pop, sources, depth, theta, src_offsets=src_offsets, stream=stream,
+                           capacity=total)
+        emr_result_check(res, stream)
+    return res
 
 
 def emr_eval_raw(pop: Population, sources, depth: int, src_offsets=None, stream=None):
@@ -329,7 +355,7 @@ def emr_eval_raw(pop: Population, sources, depth: int, src_offsets=None, stream=
     n, _ = emr_grid_count(depth)
     npairs = n_pairs_of(pop, sources, src_offsets)
     out = torch.empty((npairs, n), dtype=torch.float32, device="cuda")
-    ws_bytes = emr_workspace_bytes(pop, sources, depth, src_offsets)
+    ws_bytes = emr_workspace_bytes(pop, sources, depth, src_offsets, 0)
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
     offs = _offsets(src_offsets)
     src = _sources(sources)
@@ -368,15 +394,18 @@ def emr_discover_cost(pop: Population, sources, depth: int, src_offsets=None,
 
 
 def records_to_host(res):
-    """Copy a checked result to numpy: per-pair lists (parent[i], w4[i]) in ascending order."""
-    counts = res["pair_count"].cpu().numpy()
-    cap = res["pair_capacity"]
-    parent = res["parent"].cpu().numpy().view(np.uint32)
-    w4 = res["w4"].cpu().numpy()
+    """Copy a checked result to numpy: (pair counts, per-pair (parent[i], w4[i]) in ascending
+    order)."""
+    n = res["n_pairs"]
+    counts = res["pair_count"][:n].cpu().numpy()
+    offs = res["pair_offset"].cpu().numpy()
+    total = int(min(offs[-1], res["capacity"]))
+    parent = res["parent"][:total].cpu().numpy().view(np.uint32).astype(np.int64)
+    w4 = res["w4"][:total].cpu().numpy()
     out = []
-    for r, c in enumerate(counts):
-        c = min(int(c), cap)
-        out.append((parent[r, :c].astype(np.int64), w4[r, :c]))
+    for r in range(n):
+        lo, hi = int(offs[r]), int(offs[r] + counts[r])
+        out.append((parent[lo:hi], w4[lo:hi]))
     return counts, out
 
 

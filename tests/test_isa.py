@@ -57,7 +57,7 @@ def test_m0_only_for_register_indexing(asm):
 
 def test_discover_kernels_use_no_scratch(asm):
     ks = {k: v for k, v in _kernels(asm).items() if "k_discover" in k}
-    assert len(ks) == 3   # one per output mode
+    assert len(ks) == 2   # one per output mode
     for name, body in ks.items():
         assert "scratch_" not in body and "buffer_store" not in body, name
     sizes = re.findall(r"\.name:\s+(\S*k_discover\S*)\s*\n(?:.*\n)*?\s+\.private_segment_fixed_size:\s+(\d+)",
@@ -150,7 +150,7 @@ def test_tail_jumps_land_on_their_tails():
         got = [at.get(t0 + i * stride, "?") for i in range(14)]
         assert all(g.startswith(f) for g, f in zip(got, first)), (stride, got)
         sites += 1
-    assert sites == 3 * 9  # one per walker (9 sources-per-walk and window variants) per mode
+    assert sites == 2 * 9  # one per walker (9 sources-per-walk and window variants) per mode
 
 
 # ------------------------------------------------------------------ the compiled tier's template
@@ -194,7 +194,7 @@ def test_template_does_not_carry_scc_across_calls(jit_asm):
             assert not _SCC_READERS.match(code), "SCC read after a call: " + code.strip()
             if _SCC_WRITERS.match(code) or re.match(r"^\s*s_(branch|endpgm|setpc)", code):
                 break
-    assert calls == 3 * 9  # one call site per (sources per walk, window) variant per mode
+    assert calls == 2 * 9  # one call site per (sources per walk, window) variant per mode
 
 
 def test_template_kernels_allocate_the_convention_registers(jit_asm):
@@ -206,7 +206,7 @@ def test_template_kernels_allocate_the_convention_registers(jit_asm):
     top = max(G.base(S * P, S * P, W) + 2 * P + G.jit_temps(S, P, W) for S, P, W in G.VARIANTS)
     counts = re.findall(r"\.name:\s+(emr_discover_jit_\w+)\s*\n(?:.*\n)*?\s+\.vgpr_count:\s+(\d+)",
                         jit_asm)
-    assert len(counts) == 3
+    assert len(counts) == 2
     for name, n in counts:
         assert int(n) >= top, (name, n, top)
 

@@ -45,11 +45,10 @@ def raw_both(emr, genomes, sources, D, offs=None):
     return both_tiers(emr, run)
 
 
-def records_both(emr, genomes, sources, D, theta, offs=None, cap=None):
+def records_both(emr, genomes, sources, D, theta, offs=None):
     def run(policy):
         pop = emr.emr_pack_population(genomes)
-        res = emr.emr_discover(pop, sources, D, float(np.float32(theta)), src_offsets=offs,
-                               pair_capacity=cap)
+        res = emr.emr_discover(pop, sources, D, float(np.float32(theta)), src_offsets=offs)
         emr.emr_result_check(res)
         assert emr.emr_jit_info(pop)["state"] == (1 if policy == emr.EMR_JIT_ALWAYS else 0)
         return emr.records_to_host(res)
@@ -95,12 +94,6 @@ def test_records_bit_identical_population_depth6(emr):
 
 def test_records_bit_identical_tabular(emr):
     records_both(emr, W.population(3, 20, 40, 120), W.tabular_sources(), 5, 0.03)
-
-
-def test_records_bit_identical_lookback_placement(emr):
-    # a capacity below the worst case places records through the look-back scan
-    genomes = W.population(5, 60, 20, 60)
-    records_both(emr, genomes, W.xor_sources(), 6, 0.03, cap=1300)
 
 
 def test_records_bit_identical_per_genome_sources(emr):

@@ -320,14 +320,14 @@ def test_grown_template_is_a_consistent_code_object(tmp_path, pages):
     assert out[dyn_off + d:dyn_off + d + dyn_size] == img[dyn_off:dyn_off + dyn_size]
     y0, y1 = symbols(t0), symbols(t1)
     assert y1["emr_code_area"] == y0["emr_code_area"]
-    for k in ("emr_discover_jit_padded", "emr_discover_jit_padded.kd", "emr_discover_jit_raw"):
+    for k in ("emr_discover_jit_records", "emr_discover_jit_records.kd", "emr_discover_jit_raw"):
         assert y1[k] == y0[k]
     assert y1["emr_code_area_holder"][1] == y0["emr_code_area_holder"][1] + d
     if "_DYNAMIC" in y0:
         assert y1["_DYNAMIC"][0] == y0["_DYNAMIC"][0] + d
     r = subprocess.run([os.path.join(LLVM, "llvm-objdump"), "-d", str(p1)], capture_output=True,
                        text=True)
-    assert r.returncode == 0 and "<emr_discover_jit_padded>:" in r.stdout
+    assert r.returncode == 0 and "<emr_discover_jit_records>:" in r.stdout
 
 
 @pytest.mark.skipif(not os.path.exists(TEMPLATE), reason="template code object not built")

@@ -44,14 +44,16 @@ def pair_genome_source(r, genomes, sources, offs):
     return genomes[g], sources[r]
 
 
-def check_discover(emr, genomes, sources, D, theta, offs=None, cap=None, pop=None):
+def check_discover(emr, genomes, sources, D, theta, offs=None, capacity=None, pop=None):
     """Runs the GPU path and the oracle; asserts parity; returns summary stats."""
     theta32 = float(np.float32(theta))
     if pop is None:
         pop = emr.emr_pack_population(genomes)
-    res = emr.emr_discover(pop, sources, D, theta32, src_offsets=offs, pair_capacity=cap)
-    mx = emr.emr_result_check(res)
+    res = emr.emr_discover(pop, sources, D, theta32, src_offsets=offs, capacity=capacity)
+    total, mx = emr.emr_result_check(res)
     counts, recs = emr.records_to_host(res)
+    offsets = res["pair_offset"].cpu().numpy()
+    assert offsets[0] == 0 and np.array_equal(np.diff(offsets), counts) and offsets[-1] == total
     o = oracle.discover(genomes, sources, D, theta32, src_offsets=offs)
     assert len(counts) == len(o["pair_count"])
     n_band = 0
@@ -73,8 +75,7 @@ def check_discover(emr, genomes, sources, D, theta, offs=None, cap=None, pop=Non
         common, gi, oi = np.intersect1d(gp, op, return_indices=True)
         assert close(gw[gi], ow[oi]).all()
     assert mx == (int(counts.max()) if len(counts) else 0)
-    return {"records": int(np.sum(np.minimum(counts, res["pair_capacity"]))), "band": n_band,
-            "counts": counts}
+    return {"records": int(total), "band": n_band, "counts": counts}
 
 
 def check_raw(emr, genomes, sources, D, offs=None):
@@ -209,10 +210,11 @@ def test_infinite_weights_give_nan_variance_never_kept(emr):
 def test_empty_population_and_no_sources(emr):
     pop = emr.emr_pack_population(W.population(0, 3, 5, 10))
     res = emr.emr_discover(pop, W.xor_sources()[:0], 5, 0.03)
-    assert emr.emr_result_check(res) == 0
+    assert emr.emr_result_check(res) == (0, 0)
+    assert int(res["pair_offset"][0].item()) == 0
     pop0 = emr.emr_pack_population([])
     res = emr.emr_discover(pop0, W.xor_sources(), 5, 0.03)
-    assert emr.emr_result_check(res) == 0
+    assert emr.emr_result_check(res) == (0, 0)
 
 
 def test_one_population_many_calls(emr):
@@ -230,35 +232,58 @@ def test_one_population_many_calls(emr):
 
 
 def test_capacity_overflow_is_reported(emr):
-    genomes, sources, D, theta = W.workload("single_d5")
+    """A capacity below the call's total: EMR_E_CAPACITY with the exact total; counts and offsets
+    are exact (the records are not: the pool is filled in the order walks finish); a retry at the
+    reported total gives the complete output."""
+    genomes = W.population(12, 80, 20, 60)
+    srcs = W.xor_sources()
     pop = emr.emr_pack_population(genomes)
-    res = emr.emr_discover(pop, sources, D, -1.0, pair_capacity=10)
+    full = emr.emr_discover(pop, srcs, 6, 0.01)
+    total, mx = emr.emr_result_check(full)
+    assert total > 100 and mx < oracle.n_parents(6)
+    small = emr.emr_discover(pop, srcs, 6, 0.01, capacity=total // 3)
+    with pytest.raises(emr.EmrError) as e:
+        emr.emr_result_check(small)
+    assert e.value.status == emr.EMR_E_CAPACITY
+    assert str(total) in str(e.value)
+    np.testing.assert_array_equal(small["pair_count"].cpu().numpy(), full["pair_count"].cpu().numpy())
+    np.testing.assert_array_equal(small["pair_offset"].cpu().numpy(), full["pair_offset"].cpu().numpy())
+    retry = emr.emr_discover_all(pop, srcs, 6, 0.01, capacity=total // 3)
+    assert retry["capacity"] == total
+    np.testing.assert_array_equal(retry["parent"].cpu().numpy(), full["parent"][:total].cpu().numpy())
+    st = check_discover(emr, genomes, srcs, 6, 0.01, capacity=total, pop=pop)
+    assert st["records"] == total
+
+
+def test_zero_capacity_and_exact_capacity(emr):
+    genomes, sources, D, _ = W.workload("single_d5")
+    pop = emr.emr_pack_population(genomes)
+    res = emr.emr_discover(pop, sources, D, 1e-4, capacity=0)
     with pytest.raises(emr.EmrError) as e:
         emr.emr_result_check(res)
     assert e.value.status == emr.EMR_E_CAPACITY
-    # the records that fit are the first ones
-    counts, recs = emr.records_to_host(res)
-    assert counts[0] == oracle.n_parents(D)
-    np.testing.assert_array_equal(recs[0][0], np.arange(10))
-
+    total = int(res["pair_offset"][-1].item())
+    assert total > 0
+    check_discover(emr, genomes, sources, D, 1e-4, capacity=total, pop=pop)
 
 
 def test_result_checks_wait_for_their_own_call(emr):
-    """Each call's flags live in a slot of their own: two calls on two results enqueued back to
-    back are checked afterwards, each against its own largest count (one overflows, the other
-    does not), and a workspace with no call to check is refused."""
+    """Each call's flags live in a slot of their own: three calls on three results enqueued back
+    to back are checked afterwards, each against its own total (one overflows, the others do
+    not), and a workspace with no call to check is refused."""
     genomes, sources, D, _ = W.workload("single_d5")
+    Q = oracle.n_parents(D)
     pop = emr.emr_pack_population(genomes)
     res_all = emr.emr_discover(pop, sources, D, -1.0)               # every cell kept
-    res_few = emr.emr_discover(pop, sources, D, -1.0, pair_capacity=10)
+    res_few = emr.emr_discover(pop, sources, D, -1.0, capacity=10)
     res_none = emr.emr_discover(pop, sources, D, 1e30)             # nothing kept
-    assert emr.emr_result_check(res_all) == oracle.n_parents(D)
+    assert emr.emr_result_check(res_all) == (Q, Q)
     with pytest.raises(emr.EmrError) as e:
         emr.emr_result_check(res_few)
     assert e.value.status == emr.EMR_E_CAPACITY
-    assert emr.emr_result_check(res_none) == 0
+    assert emr.emr_result_check(res_none) == (0, 0)
     # checked again later (no call in between on these results): the same answers
-    assert emr.emr_result_check(res_all) == oracle.n_parents(D)
+    assert emr.emr_result_check(res_all) == (Q, Q)
     import torch
     other = dict(res_all)
     other.pop("_struct", None)
@@ -268,25 +293,20 @@ def test_result_checks_wait_for_their_own_call(emr):
     assert e.value.status == emr.EMR_E_INVAL
 
 
-def test_lookback_placement_matches_padded_placement(emr):
-    """A pair capacity below Q(D) switches record placement to the look-back scan; both
-    placements must give identical records."""
-    genomes = W.population(12, 80, 20, 60)
-    srcs = W.xor_sources()
-    pop = emr.emr_pack_population(genomes)
-    a = emr.emr_discover(pop, srcs, 6, 0.01)
-    mx = emr.emr_result_check(a)
-    assert mx < oracle.n_parents(6)
-    b = emr.emr_discover(pop, srcs, 6, 0.01, pair_capacity=mx)
-    assert emr.emr_result_check(b) == mx
-    ca, ra = emr.records_to_host(a)
-    cb, rb = emr.records_to_host(b)
-    np.testing.assert_array_equal(ca, cb)
-    for (pa, wa), (pb, wb) in zip(ra, rb):
-        np.testing.assert_array_equal(pa, pb)
-        np.testing.assert_array_equal(wa.view(np.uint32), wb.view(np.uint32))
-    st = check_discover(emr, genomes, srcs, 6, 0.01, cap=mx)
-    assert st["records"] == int(ca.sum())
+def test_many_pairs_csr_offsets(emr):
+    """Per-genome CSR sources with many empty and many busy pairs: the compaction's look-back over
+    pairs gives exact offsets (every pair's records where its offset says) for 6000+ pairs."""
+    rng = np.random.default_rng(71)
+    genomes = W.population(71, 300, 12, 40)
+    pts, offs = [], [0]
+    for k in range(len(genomes)):
+        n = int(rng.integers(0, 40))
+        for _ in range(n):
+            pts.append((float(rng.uniform(-1, 1)), float(rng.uniform(-1, 1)), int(rng.integers(0, 2))))
+        offs.append(len(pts))
+    sources = W.sources_array(pts)
+    st = check_discover(emr, genomes, sources, 4, 0.01, offs=offs)
+    assert st["records"] > 0 and len(st["counts"]) > 5000
 
 
 def test_discover_is_deterministic(emr):
@@ -394,7 +414,7 @@ def test_compaction_over_many_tile_groups_dense(emr):
     res = emr.alloc_result(pop, sources, D)
     for call in range(2):
         emr.emr_discover(pop, sources, D, -1.0, res=res)
-        assert emr.emr_result_check(res) == Q
+        assert emr.emr_result_check(res) == (len(genomes) * len(sources) * Q, Q)
         counts, recs = emr.records_to_host(res)
         assert np.all(counts == Q)
         for r in range(len(counts)):
@@ -443,17 +463,9 @@ def test_config4_recurrent_depth10_two_phases(emr):
         np.testing.assert_array_equal(hs_g["x"], hs_o["x"].astype(np.float32))
         np.testing.assert_array_equal(hs_g["y"], hs_o["y"].astype(np.float32))
     assert offs_o[-1] >= 64
-    # phase 2 on the oracle's sources: records per pair are few, so regions of 8192 (look-back
-    # placement) suffice; an overflow would be reported and retried at the reported size
-    cap = 8192
-    res2 = emr.emr_discover(pop, hs_o, D, theta32, src_offsets=offs_o, pair_capacity=cap)
-    try:
-        emr.emr_result_check(res2)
-    except emr.EmrError as e:
-        assert e.status == emr.EMR_E_CAPACITY
-        cap = int(res2["pair_count"].max().item())  # true counts survive an overflow
-        res2 = emr.emr_discover(pop, hs_o, D, theta32, src_offsets=offs_o, pair_capacity=cap)
-        emr.emr_result_check(res2)
+    # phase 2 on the oracle's sources (CSR output of the default capacity; retried at the
+    # reported total if it overflows)
+    res2 = emr.emr_discover_all(pop, hs_o, D, theta32, src_offsets=offs_o)
     counts2, recs2 = emr.records_to_host(res2)
     rng = np.random.default_rng(4)
     sample = np.sort(rng.choice(len(counts2), size=64, replace=False))
@@ -467,7 +479,6 @@ def test_config4_recurrent_depth10_two_phases(emr):
         lo, hi = oo["pair_offset"][k], oo["pair_offset"][k + 1]
         op, ow = oo["parent"][lo:hi], oo["w4"][lo:hi]
         gp, gw = recs2[r]
-        assert counts2[r] <= cap
         if np.array_equal(gp, op):
             assert close(gw, ow).all(), r
         else:
