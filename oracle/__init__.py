@@ -220,6 +220,57 @@ def max_threads() -> int:
     return int(lib().orc_max_threads())
 
 
+def _pair_sources(sources, n_genomes: int, src_offsets=None):
+    """(genome of each pair, source index of each pair) for the two pair layouts: shared sources
+    (pair = g * n_shared + j) or per-genome CSR sources (pair = source index)."""
+    if src_offsets is None:
+        n_src = len(sources)
+        pairs = np.arange(n_genomes * n_src)
+        return pairs // max(n_src, 1), pairs % max(n_src, 1)
+    offs = np.asarray(src_offsets, np.int64)
+    pairs = np.arange(int(offs[-1]))
+    return np.searchsorted(offs, pairs, side="right") - 1, pairs
+
+
+def hidden_cells(records, n_genomes: int, sources, src_offsets=None, exclude=None):
+    """The hidden nodes a discovery found (Section 2, Phase 1 feeding Phase 2): per genome, the
+    heap indices 4P+1 .. 4P+4 of the children of every kept parent P of its outgoing pairs, as a
+    set (deduplicated), minus the cells in exclude[g] (the nodes found before, when the hidden-to-
+    hidden step is iterated). Returns a list of ascending int64 arrays, one per genome."""
+    gen, src = _pair_sources(sources, n_genomes, src_offsets)
+    out = []
+    for g in range(n_genomes):
+        kids = []
+        for r in np.nonzero(gen == g)[0]:
+            if int(sources[int(src[r])]["dir"]) != 0:
+                continue
+            lo, hi = records["pair_offset"][r], records["pair_offset"][r + 1]
+            P = np.asarray(records["parent"][lo:hi], np.int64)
+            kids.append((4 * P[:, None] + np.arange(1, 5)[None, :]).ravel())
+        cells = np.unique(np.concatenate(kids)) if kids else np.zeros(0, np.int64)
+        if exclude is not None and len(exclude[g]):
+            cells = np.setdiff1d(cells, np.asarray(exclude[g], np.int64))
+        out.append(cells)
+    return out
+
+
+def sources_at_cells(cells_per_genome, depth: int):
+    """Outgoing sources at the centres of the given heap cells, per genome: (sources, offsets) in
+    the CSR layout of discover's src_offsets."""
+    xy = grid(depth)
+    offs = [0]
+    parts = []
+    for cells in cells_per_genome:
+        parts.append(np.asarray(cells, np.int64))
+        offs.append(offs[-1] + len(cells))
+    src = np.zeros(offs[-1], dtype=[("x", "<f4"), ("y", "<f4"), ("dir", "<i4")])
+    if offs[-1]:
+        idx = np.concatenate(parts) - 1  # heap cell F sits at grid index F - 1
+        src["x"] = xy[idx, 0]
+        src["y"] = xy[idx, 1]
+    return src, np.array(offs, np.int32)
+
+
 def hidden_sources(records, genomes_sources, sources, depth: int):
     """Sources of the hidden-to-hidden phase, from this oracle's own phase-1 output (the reading of
     'from every discovered hidden node' used for the recurrent substrate): for each genome, the
@@ -230,25 +281,85 @@ def hidden_sources(records, genomes_sources, sources, depth: int):
     Returns (sources array, offsets[n_genomes + 1]) in the layout of discover's src_offsets;
     the sources of a genome are ordered by heap index.
     """
-    n_src = len(sources)
+    return sources_at_cells(hidden_cells(records, genomes_sources, sources), depth)
+
+
+def chain_filter(records, depth: int):
+    """Eq. 2 read literally on a parent-rule result: a kept parent stays only if its own parent
+    was kept by the same rule, recursively up to the root (active at depth 0, then active[d] =
+    active[d-1] of the parent and its variance test). Records are per pair in ascending heap
+    order, i.e. level by level, so one pass in that order decides every cell after its parent.
+    Returns a records dict of the same form (pair_count, pair_offset, parent, w4, var)."""
+    counts = np.asarray(records["pair_count"], np.int64)
+    offs = np.asarray(records["pair_offset"], np.int64)
+    keep = np.zeros(int(offs[-1]), bool)
+    for r in range(len(counts)):
+        kept = set()
+        for i in range(int(offs[r]), int(offs[r + 1])):
+            P = int(records["parent"][i])
+            if P == 0 or (P - 1) // 4 in kept:
+                kept.add(P)
+                keep[i] = True
+    new_counts = np.array([int(np.sum(keep[offs[r]:offs[r + 1]])) for r in range(len(counts))],
+                          np.int64)
+    new_offs = np.zeros(len(counts) + 1, np.int64)
+    np.cumsum(new_counts, out=new_offs[1:])
+    out = {"pair_count": new_counts, "pair_offset": new_offs,
+           "parent": np.asarray(records["parent"])[keep], "w4": np.asarray(records["w4"])[keep]}
+    if "var" in records:
+        out["var"] = np.asarray(records["var"])[keep]
+    return out
+
+
+# Connection types (Section 4, the connection type taxonomy): from the source and target node's y
+# coordinates; a self-loop is a connection from a node to itself.
+CONN_FORWARD, CONN_BACKWARD, CONN_LATERAL, CONN_SELF = 1, 2, 4, 8
+
+
+def connection_type(sx, sy, tx, ty) -> int:
+    """Self when source and target are the same node (same position), else forward (y_s < y_t),
+    backward (y_s > y_t) or lateral (y_s = y_t)."""
+    if sx == tx and sy == ty:
+        return CONN_SELF
+    if sy < ty:
+        return CONN_FORWARD
+    if sy > ty:
+        return CONN_BACKWARD
+    return CONN_LATERAL
+
+
+def express(records, sources, depth: int, type_mask: int, w_min: float, n_genomes=None,
+            src_offsets=None):
+    """The connections a discovery expresses: every child C = 4P+k (k = 1..4) of a kept parent P
+    of pair (genome, source s) is a connection with the CPPN output at C as its weight. An outgoing
+    source s connects s -> C, an incoming one C -> s (Section 3.1: the query direction). A
+    connection is expressed when its type (Section 4) is in type_mask and its weight magnitude
+    exceeds w_min (Section 3.3: the weight magnitude filter, 0.1 in the paper). The weights are
+    the records' values as given (pass the float32 outputs the kernels produced to compare the
+    filters exactly). Returns dict(pair_count, pair_offset, cell (heap index of C), w)."""
+    offs = np.asarray(records["pair_offset"], np.int64)
+    n_pairs = len(offs) - 1
+    if n_genomes is None:
+        n_genomes = n_pairs // max(len(sources), 1) if src_offsets is None else len(src_offsets) - 1
+    _, src = _pair_sources(sources, n_genomes, src_offsets)
     xy = grid(depth)
-    out_x, out_y, offs = [], [], [0]
-    for g in range(genomes_sources):
-        kids = []
-        for j in range(n_src):
-            if int(sources[j]["dir"]) != 0:
-                continue
-            r = g * n_src + j
-            lo, hi = records["pair_offset"][r], records["pair_offset"][r + 1]
-            P = records["parent"][lo:hi].astype(np.int64)
-            # heap cell F sits at grid index F - 1: the children 4P+1..4P+4 at 4P..4P+3
-            kids.append((4 * P[:, None] + np.arange(4)[None, :]).ravel())
-        idx = np.unique(np.concatenate(kids)) if kids else np.zeros(0, np.int64)
-        out_x.append(xy[idx, 0])
-        out_y.append(xy[idx, 1])
-        offs.append(offs[-1] + len(idx))
-    src = np.zeros(offs[-1], dtype=[("x", "<f4"), ("y", "<f4"), ("dir", "<i4")])
-    if offs[-1]:
-        src["x"] = np.concatenate(out_x)
-        src["y"] = np.concatenate(out_y)
-    return src, np.array(offs, np.int32)
+    counts = np.zeros(n_pairs, np.int64)
+    cells, ws = [], []
+    for r in range(n_pairs):
+        s = sources[int(src[r])]
+        sx, sy, d = float(s["x"]), float(s["y"]), int(s["dir"])
+        for i in range(int(offs[r]), int(offs[r + 1])):
+            P = int(records["parent"][i])
+            for k in range(4):
+                C = 4 * P + 1 + k
+                cx, cy = float(xy[C - 1, 0]), float(xy[C - 1, 1])
+                t = connection_type(sx, sy, cx, cy) if d == 0 else connection_type(cx, cy, sx, sy)
+                w = float(records["w4"][i][k])
+                if (t & type_mask) and abs(w) > w_min:
+                    cells.append(C)
+                    ws.append(w)
+                    counts[r] += 1
+    pair_offset = np.zeros(n_pairs + 1, np.int64)
+    np.cumsum(counts, out=pair_offset[1:])
+    return {"pair_count": counts, "pair_offset": pair_offset,
+            "cell": np.array(cells, np.int64), "w": np.array(ws, np.float64)}

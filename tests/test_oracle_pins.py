@@ -367,3 +367,123 @@ def test_hidden_sources_are_children_of_kept_cells():
     got = set(zip(hs["x"].tolist(), hs["y"].tolist()))
     assert got == {(float(a), float(b)) for a, b in want}
     assert len(hs) == len(want) and np.all(hs["dir"] == 0)
+
+
+# ---------------------------------------------------------------- Eq. 2 read literally, on records
+
+def test_chain_filter_equals_the_literal_chain_rule():
+    """Filtering a parent-rule result by Eq. 2's ancestor condition (chain_filter, on records) and
+    evaluating Eq. 2 directly (the oracle's CHAIN mode, one recursion per cell) give the same
+    records; and by the lazy-equivalence pin above both equal ES-HyperNEAT's division."""
+    removed = 0
+    for seed in range(4):
+        genomes = W.population(300 + seed, 6, 10, 30)
+        srcs = W.xor_sources()
+        theta = float(np.float32(0.02))
+        eager = oracle.discover(genomes, srcs, 6, theta, oracle.PARENT)
+        chain = oracle.discover(genomes, srcs, 6, theta, oracle.CHAIN)
+        got = oracle.chain_filter(eager, 6)
+        np.testing.assert_array_equal(got["pair_count"], chain["pair_count"])
+        np.testing.assert_array_equal(got["parent"], chain["parent"])
+        np.testing.assert_array_equal(got["w4"], chain["w4"])
+        removed += len(eager["parent"]) - len(got["parent"])
+    assert removed > 0  # the rule removes cells in these populations
+
+
+def test_chain_filter_closed_form_linear_cppn():
+    # out = x2 (linear): the children of a level-k parent have variance 1/4^(k+1), so the kept
+    # parents are every cell of levels 0..K*-1: each one's ancestors are kept too, and the chain
+    # rule removes nothing. out = sin(2 pi x2) fails at the root (its children sit on zeros of the
+    # sine) but keeps cells further down: the chain rule removes all of them.
+    g = linear_cppn(1.0, 0.0, 0.0)
+    s = src_(0.0, -1.0)
+    rec = oracle.discover([g], [s], 5, 0.03)
+    np.testing.assert_array_equal(oracle.chain_filter(rec, 5)["parent"], rec["parent"])
+    g2 = mk(INPUTS + [6, 5], [0] * 5 + [LIN, SINE], [(6, 5, 1.0), (2, 6, 2 * math.pi)])
+    rec2 = oracle.discover([g2], [s], 5, 0.3)
+    assert rec2["pair_count"][0] > 0 and 0 not in set(rec2["parent"].tolist())
+    assert oracle.chain_filter(rec2, 5)["pair_count"][0] == 0  # the root failed: nothing below
+
+
+# ---------------------------------------------------------------- hidden nodes (Phase 2 sources)
+
+@pytest.mark.parametrize("a,b,n_cells", [(1.0, 0.0, 20), (3.0, 3.0, 340)])
+def test_hidden_cells_closed_form_linear_cppn(a, b, n_cells):
+    """out = a x2 + b y2 keeps every cell of levels 0..K*-1 for every outgoing source (the output
+    does not depend on the source), so the hidden nodes are every cell of levels 1..K*: heap
+    indices 1 .. N(K*), each once although three sources found it; excluding them leaves none."""
+    g = linear_cppn(a, b, 0.0)
+    srcs = W.xor_sources()
+    rec = oracle.discover([g], srcs, 6, 0.03)
+    cells = oracle.hidden_cells(rec, 1, srcs)
+    np.testing.assert_array_equal(cells[0], np.arange(1, n_cells + 1))
+    again = oracle.hidden_cells(rec, 1, srcs, exclude=cells)
+    assert len(again[0]) == 0
+    hs, offs = oracle.hidden_sources(rec, 1, srcs, 6)
+    xy = oracle.grid(6)
+    np.testing.assert_array_equal(hs["x"], xy[:n_cells, 0].astype(np.float32))
+    np.testing.assert_array_equal(offs, [0, n_cells])
+
+
+def test_hidden_cells_ignore_incoming_pairs():
+    # an incoming source's kept cells connect hidden nodes to an output: they add no hidden node
+    g = linear_cppn(1.0, 0.0, 0.0)
+    only_in = W.sources_array([(0.0, 1.0, 1)])
+    g_in = mk(INPUTS + [6], [0] * 5 + [LIN], [(0, 5, 1.0)])  # out = x1: varies for incoming
+    rec = oracle.discover([g_in], only_in, 5, 0.03)
+    assert rec["pair_count"][0] > 0
+    assert len(oracle.hidden_cells(rec, 1, only_in)[0]) == 0
+    del g
+
+
+# ---------------------------------------------------------------- connection types and |w| filter
+
+def test_connection_types_closed_form():
+    """A source at the level-1 cell (-1/2, -1/2) under out = x2 (every cell of levels 1..2 is a
+    target, 20 of them): 1 self-loop (the cell itself), 1 lateral (the other level-1 cell of its
+    row y = -1/2: cells of other levels never share a y), 14 forward (y > -1/2: 2 at level 1,
+    12 at level 2) and 4 backward (the level-2 row y = -3/4)."""
+    g = linear_cppn(1.0, 0.0, 0.0)
+    s = W.sources_array([(-0.5, -0.5, 0)])
+    rec = oracle.discover([g], s, 5, 0.03)
+    assert rec["pair_count"][0] == 5  # parents of levels 0..1
+    F, B, L, S = (oracle.CONN_FORWARD, oracle.CONN_BACKWARD, oracle.CONN_LATERAL, oracle.CONN_SELF)
+    count = lambda m: int(oracle.express(rec, s, 5, m, -1.0)["pair_count"][0])  # noqa: E731
+    assert (count(S), count(L), count(F), count(B)) == (1, 1, 14, 4)
+    assert count(F | B | L | S) == 20
+    e = oracle.express(rec, s, 5, S, -1.0)
+    assert e["cell"][0] == 1  # heap cell 1 is the level-1 cell at (-1/2, -1/2)
+
+
+def test_weight_filter_closed_form():
+    # out = x2: the weight of target C is its x; |x| > 0.3 keeps the 4 level-1 cells (|x| = 1/2)
+    # and the 8 level-2 cells with |x| = 3/4; the filter is strict
+    g = linear_cppn(1.0, 0.0, 0.0)
+    s = src_(0.0, -1.0)
+    rec = oracle.discover([g], [s], 5, 0.03)
+    allt = oracle.CONN_FORWARD | oracle.CONN_BACKWARD | oracle.CONN_LATERAL | oracle.CONN_SELF
+    assert oracle.express(rec, [s], 5, allt, 0.3)["pair_count"][0] == 12
+    assert oracle.express(rec, [s], 5, allt, 0.5)["pair_count"][0] == 8
+    assert oracle.express(rec, [s], 5, allt, 0.75)["pair_count"][0] == 0
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_connection_types_partition_and_input_layers_are_forward(seed):
+    """The four types split every connection exactly once; with a zero-width filter every child of
+    every record is a connection; the XOR inputs (y = -1) and output (y = 1) only ever make forward
+    connections (grid cells lie strictly between)."""
+    genomes = W.population(400 + seed, 8, 12, 40)
+    srcs = W.xor_sources()
+    rec = oracle.discover(genomes, srcs, 5, 0.01)
+    masks = [oracle.CONN_FORWARD, oracle.CONN_BACKWARD, oracle.CONN_LATERAL, oracle.CONN_SELF]
+    per = [oracle.express(rec, srcs, 5, m, -1.0) for m in masks]
+    total = sum(int(e["pair_offset"][-1]) for e in per)
+    assert total == 4 * len(rec["parent"])
+    assert int(per[0]["pair_offset"][-1]) == total
+    # a hidden-to-hidden style call: sources at cell centres see all four types
+    cells = oracle.hidden_cells(rec, len(genomes), srcs)
+    hs, offs = oracle.sources_at_cells(cells, 5)
+    rec2 = oracle.discover(genomes, hs, 5, 0.01, src_offsets=offs)
+    per2 = [int(oracle.express(rec2, hs, 5, m, -1.0, src_offsets=offs)["pair_offset"][-1])
+            for m in masks]
+    assert sum(per2) == 4 * len(rec2["parent"])
