@@ -197,6 +197,96 @@ emr_status emr_discover(const emr_population* pop, const emr_source* sources, in
 emr_status emr_result_check(const emr_result* out, int64_t* total, int64_t* max_count,
                             void* stream);
 
+/* Waits for the latest call that wrote a CSR output through `workspace` on the current device
+ * (emr_discover, emr_hidden_sources, emr_express, emr_chain_filter) and reports it like
+ * emr_result_check: EMR_E_DEVICE for a kernel error, EMR_E_CAPACITY when it found more than
+ * `capacity` entries; *total and *max_count (largest per pair or per genome; either may be NULL).
+ * emr_result_check(out, ...) is emr_call_check(out->workspace, out->capacity, ...). */
+emr_status emr_call_check(const void* workspace, int64_t capacity, int64_t* total,
+                          int64_t* max_count, void* stream);
+
+/* ------------------------------------------------------------------ after discovery
+ * Operations on the checked CSR output `rec` of an emr_discover call, given the same population,
+ * sources and depth as that call. Each writes a CSR output of its own through a workspace and is
+ * checked with emr_call_check. */
+
+/* Words of a per-genome cell bitmap at this depth: bit p of word p / 32 stands for grid position p
+ * (heap cell p + 1), p < N(D). Host only. */
+emr_status emr_cell_words(int32_t depth, int64_t* words);
+
+/* Output of emr_hidden_sources (device buffers, caller-owned). */
+typedef struct {
+  emr_source* sources;  /* [capacity] outgoing sources at the hidden cells' centres, per genome in
+                           ascending heap order */
+  uint32_t* cell;       /* [capacity] their heap indices, or NULL */
+  int64_t capacity;
+  int64_t* offsets;     /* [n_genomes + 1]: genome g's are offsets[g] .. offsets[g+1]-1 */
+  uint32_t* known;      /* [n_genomes * emr_cell_words(depth)] or NULL: cells already hidden nodes
+                           (excluded from the output), or-ed with the output's cells by the call */
+  void* workspace;      /* >= emr_hidden_workspace_bytes(...), 256-byte aligned */
+  int64_t workspace_bytes;
+} emr_hidden;
+
+emr_status emr_hidden_workspace_bytes(int32_t n_genomes, int32_t depth, int64_t* bytes);
+
+/*
+ * The hidden nodes of a discovery (Section 2: Phase 1's discovered positions become the sources of
+ * Phase 2, the hidden-to-hidden query; Section 4's recurrent substrates): per genome, the heap
+ * cells 4P+1 .. 4P+4 of every kept parent P of its outgoing pairs, deduplicated, in ascending
+ * order, minus the cells set in `known`; each is returned as an outgoing source at its cell centre
+ * (Eq. 1, exact in fp32). Passing a phase's new nodes as the next emr_discover call's per-genome
+ * sources (src_offsets from `offsets`), and `known` again to the next emr_hidden_sources call,
+ * iterates Phase 2 until no genome finds a new node. Check with emr_call_check(workspace,
+ * capacity): *total = the nodes found, *max_count = the most of one genome.
+ */
+emr_status emr_hidden_sources(const emr_population* pop, const emr_source* sources,
+                              int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                              int32_t depth, const emr_result* rec, const emr_hidden* out,
+                              void* stream);
+
+/* Connection types (Section 4): forward y_s < y_t, backward y_s > y_t, lateral y_s = y_t, self
+ * s = t (same position), for a connection from node s to node t. */
+enum { EMR_CONN_FORWARD = 1, EMR_CONN_BACKWARD = 2, EMR_CONN_LATERAL = 4, EMR_CONN_SELF = 8,
+       EMR_CONN_ALL = 15 };
+
+/* Output of emr_express (device buffers, caller-owned): pair r's connections are entries
+ * pair_offset[r] .. + pair_count[r] - 1, in ascending cell order. */
+typedef struct {
+  uint32_t* cell;       /* [capacity] heap index of the grid end of the connection */
+  float* w;             /* [capacity] its weight (the CPPN output at that cell) */
+  int64_t capacity;
+  int64_t* pair_count;  /* [n_pairs] */
+  int64_t* pair_offset; /* [n_pairs + 1] */
+  void* workspace;      /* >= emr_express_workspace_bytes(n_pairs), 256-byte aligned */
+  int64_t workspace_bytes;
+} emr_connections;
+
+emr_status emr_express_workspace_bytes(int64_t n_pairs, int64_t* bytes);
+
+/*
+ * The connections a discovery expresses: each child C of a kept parent of pair (g, s) is a
+ * connection s -> C for an outgoing source and C -> s for an incoming one, weighted by the CPPN
+ * output at C; it is kept when its type (Section 4) is in type_mask and |w| > w_min (Section 3.3:
+ * the weight magnitude filter that replaces ES-HyperNEAT's band threshold, 0.1 in the paper).
+ * fp32 comparisons. Check with emr_call_check(workspace, capacity).
+ */
+emr_status emr_express(const emr_population* pop, const emr_source* sources, int32_t n_sources,
+                       const int32_t* src_offsets, int32_t n_shared, int32_t depth,
+                       const emr_result* rec, int32_t type_mask, float w_min,
+                       const emr_connections* out, void* stream);
+
+emr_status emr_chain_workspace_bytes(int64_t n_pairs, int32_t depth, int64_t* bytes);
+
+/*
+ * Eq. 2 read literally: keeps a record only when every ancestor of its cell is a record of the
+ * same pair too (the active mask propagated from the root), which is ES-HyperNEAT's division
+ * (the Superset Discovery theorem's lazy set). `out` receives those records in CSR form (its
+ * workspace at least emr_chain_workspace_bytes); n_pairs is the discover call's. Check with
+ * emr_result_check(out).
+ */
+emr_status emr_chain_filter(const emr_result* rec, int64_t n_pairs, int32_t depth,
+                            const emr_result* out, void* stream);
+
 /* ------------------------------------------------------------------ streaming
  * Deep runs stream their output between device and host memory (Section 5.2: the depth-7 note of
  * the per-generation timing table and the depth 8..13 runs of the total-runtime figure; Section 6

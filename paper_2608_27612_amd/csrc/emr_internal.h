@@ -306,6 +306,55 @@ struct MoveArgs {
   uint32_t tiles, n_pairs, nz_words;
 };
 
+// ---------------------------------------------------------------- after discovery (phase2.hip)
+// The records of a checked discover call (CSR) and each pair's genome, direction and source.
+struct RecordsIn {
+  const uint32_t* parent;
+  const float* w4;
+  const int64_t* count;   // [n_pairs]
+  const int64_t* offset;  // [n_pairs + 1]
+  int64_t cap;            // records the buffers hold (entries beyond it are not read)
+  const uint32_t* pair_info;  // [2 n_pairs]: genome << 1 | dir, source index
+  const float* src_xy;        // [2 n_sources]
+  uint32_t n_pairs;
+  int32_t depth;
+};
+
+struct HiddenArgs {
+  RecordsIn rec;
+  uint32_t* fresh;         // [n_genomes * words] cells found by this call (cleared before it)
+  uint32_t* known;         // [n_genomes * words] or NULL
+  uint32_t* totals;        // [n_genomes] new cells per genome
+  const int64_t* offsets;  // [n_genomes + 1] from k_scan
+  uint32_t* out_src;       // [3 cap] emr_source records (x, y bits, dir)
+  uint32_t* out_cell;      // [cap] or NULL
+  int64_t cap;
+  int64_t words;
+  uint32_t n_genomes;
+};
+
+struct ExpressArgs {
+  RecordsIn rec;
+  uint32_t type_mask;
+  float w_min;
+  uint32_t* totals;           // [n_pairs]
+  const int64_t* out_offset;  // [n_pairs + 1] from k_scan
+  uint32_t* out_cell;
+  float* out_w;
+  int64_t cap;
+};
+
+struct ChainArgs {
+  RecordsIn rec;
+  uint32_t* member;           // [n_pairs * qwords] bit P: parent P is a record of the pair
+  int64_t qwords;
+  uint32_t* totals;           // [n_pairs]
+  const int64_t* out_offset;  // [n_pairs + 1] from k_scan
+  uint32_t* out_parent;
+  float* out_w4;
+  int64_t cap;
+};
+
 struct BindArgs {
   const uint32_t* blob;
   const ProgDesc* desc;

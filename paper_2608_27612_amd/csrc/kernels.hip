@@ -606,6 +606,12 @@ extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int mode, 
   }
 }
 
+// Offsets of a CSR output from per-pair (or per-genome) totals, one workgroup.
+extern "C" hipError_t emr_launch_scan(const emr::ScanArgs* S, hipStream_t s) {
+  hipLaunchKernelGGL(emr::k_scan, dim3(1), dim3(emr::kScanThreads), 0, s, *S);
+  return hipGetLastError();
+}
+
 // The compaction of one record-mode range (after its discover launch, on the same stream): the
 // pairs' offsets, then the records' move.
 extern "C" hipError_t emr_launch_compact(const emr::ScanArgs* S, const emr::MoveArgs* M,

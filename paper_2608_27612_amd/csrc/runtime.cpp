@@ -30,6 +30,10 @@ extern "C" hipError_t emr_launch_discover(const emr::DiscoverArgs* a, int mode, 
 extern "C" hipError_t emr_launch_compact(const emr::ScanArgs* S, const emr::MoveArgs* M,
                                          hipStream_t s);
 extern "C" hipError_t emr_launch_finalize(uint32_t* flags, uint32_t* host, hipStream_t s);
+extern "C" hipError_t emr_launch_scan(const emr::ScanArgs* S, hipStream_t s);
+extern "C" hipError_t emr_launch_hidden(const emr::HiddenArgs* A, int step, hipStream_t s);
+extern "C" hipError_t emr_launch_express(const emr::ExpressArgs* A, int emit, hipStream_t s);
+extern "C" hipError_t emr_launch_chain(const emr::ChainArgs* A, int step, hipStream_t s);
 extern "C" hipError_t emr_launch_tile_geo(uint32_t* out, uint32_t tiles, uint32_t rows,
                                           hipStream_t s);
 extern "C" hipError_t emr_noalloc_scratch(void** out);
@@ -311,6 +315,7 @@ struct Plan {
   // position): a host image, and its device copy, uploaded on first use and freed with the plan.
   std::vector<char> img;
   size_t t_groups = 0, t_members = 0, t_srcxy = 0, t_uniform = 0;
+  size_t t_pairinfo = 0;  // per pair: genome << 1 | dir, source index (two words)
   mutable std::mutex dev_mu;
   mutable char* d_tables = nullptr;
   Plan() = default;
@@ -492,7 +497,19 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
   P.t_members = align256(P.groups.size() * sizeof(emr::Group));
   P.t_srcxy = align256(P.t_members + P.members.size() * sizeof(emr::Member));
   P.t_uniform = align256(P.t_srcxy + P.src_xy.size() * sizeof(float));
-  P.img.assign(align256(P.t_uniform + (size_t)P.n_pairs) + 256, 0);
+  P.t_pairinfo = align256(P.t_uniform + (size_t)P.n_pairs);
+  P.img.assign(align256(P.t_pairinfo + (size_t)P.n_pairs * 8) + 256, 0);
+  {
+    uint32_t* info = (uint32_t*)(P.img.data() + P.t_pairinfo);
+    for (int32_t g = 0; g < G; ++g) {
+      const int32_t lo = offs ? offs[g] : 0, hi = offs ? offs[g + 1] : n_shared;
+      for (int32_t j = lo; j < hi; ++j) {
+        const int64_t pair = offs ? (int64_t)j : (int64_t)g * n_shared + j;
+        info[2 * pair] = ((uint32_t)g << 1) | (uint32_t)sources[j].dir;
+        info[2 * pair + 1] = (uint32_t)j;
+      }
+    }
+  }
   for (const emr::Group& g : P.groups)
     if (!(g.flags & 1u))
       for (int s = 0; s < emr::kMaxGroup; ++s) P.img[P.t_uniform + g.pair[s]] = 1;
@@ -1334,11 +1351,11 @@ emr_status emr_discover(const emr_population* pop, const emr_source* sources, in
                   (hipStream_t)stream);
 }
 
-emr_status emr_result_check(const emr_result* out, int64_t* total, int64_t* max_count,
-                            void* stream) {
+emr_status emr_call_check(const void* workspace, int64_t capacity, int64_t* total,
+                          int64_t* max_count, void* stream) {
   (void)stream;
-  if (!out) return fail(EMR_E_INVAL, "out is NULL");
-  // the flag slot of the latest call with this result's workspace
+  if (!workspace) return fail(EMR_E_INVAL, "workspace is NULL");
+  // the flag slot of the latest call with this workspace
   hipEvent_t ev = nullptr;
   const uint32_t* host = nullptr;
   {
@@ -1348,7 +1365,7 @@ emr_status emr_result_check(const emr_result* out, int64_t* total, int64_t* max_
     if (st != EMR_OK) return st;
     uint64_t latest = 0;
     for (int k = 0; k < kFlagSlots; ++k)
-      if (out->workspace && R->ws[k] == out->workspace && R->seq[k] > latest) {
+      if (R->ws[k] == workspace && R->seq[k] > latest) {
         latest = R->seq[k];
         ev = R->done[k];
         host = R->host + (size_t)k * kSlotWords;
@@ -1365,12 +1382,18 @@ emr_status emr_result_check(const emr_result* out, int64_t* total, int64_t* max_
   if (max_count) *max_count = mx;
   if (total) *total = found;
   if (err)
-    return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (1: look-back wait bound, 2: a "
-                "table entry out of range)", err);
-  if (found > out->capacity)
-    return fail(EMR_E_CAPACITY, "the call found %lld records; the capacity is %lld",
-                (long long)found, (long long)out->capacity);
+    return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (2: a table entry out of range)",
+                err);
+  if (found > capacity)
+    return fail(EMR_E_CAPACITY, "the call found %lld entries; the capacity is %lld",
+                (long long)found, (long long)capacity);
   return EMR_OK;
+}
+
+emr_status emr_result_check(const emr_result* out, int64_t* total, int64_t* max_count,
+                            void* stream) {
+  if (!out) return fail(EMR_E_INVAL, "out is NULL");
+  return emr_call_check(out->workspace, out->capacity, total, max_count, stream);
 }
 
 emr_status emr_eval_raw(const emr_population* pop, const emr_source* sources, int32_t n_sources,
@@ -1790,6 +1813,243 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
   if (err)
     return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (1: look-back wait bound, 2: a "
                 "table entry out of range)", err);
+  return EMR_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------ after discovery
+namespace {
+
+// The records of a checked discover call as the phase-2 kernels read them.
+emr_status records_in(const emr_result* rec, int64_t n_pairs, int32_t depth, emr::RecordsIn* R) {
+  if (!rec) return fail(EMR_E_INVAL, "rec is NULL");
+  if (n_pairs < 0 || n_pairs > 0xFFFFFFFFll) return fail(EMR_E_INVAL, "n_pairs %lld", (long long)n_pairs);
+  if (depth < 0 || depth > EMR_MAX_DEPTH)
+    return fail(EMR_E_INVAL, "depth %d outside [0, %d]", depth, EMR_MAX_DEPTH);
+  if (!rec->pair_offset || (n_pairs > 0 && !rec->pair_count))
+    return fail(EMR_E_INVAL, "rec has no pair_count / pair_offset");
+  if (rec->capacity < 0 || (rec->capacity > 0 && (!rec->parent || !rec->w4)))
+    return fail(EMR_E_INVAL, "rec has no records");
+  *R = emr::RecordsIn{};
+  R->parent = rec->parent;
+  R->w4 = rec->w4;
+  R->count = rec->pair_count;
+  R->offset = rec->pair_offset;
+  R->cap = rec->capacity;
+  R->n_pairs = (uint32_t)n_pairs;
+  R->depth = depth;
+  return EMR_OK;
+}
+
+// A workspace of at least `need` bytes, 256-byte aligned.
+emr_status check_workspace(const void* ws, int64_t bytes, int64_t need) {
+  if (!ws || bytes < need)
+    return fail(EMR_E_INVAL, "workspace of %lld bytes is smaller than the %lld needed",
+                (long long)bytes, (long long)need);
+  if (((uintptr_t)ws & 255) != 0) return fail(EMR_E_INVAL, "workspace not 256-byte aligned");
+  return EMR_OK;
+}
+
+int64_t cell_words(int32_t depth) { return (emr::n_positions(depth) + 31) / 32; }
+
+// Workspace layouts: hidden nodes (fresh bitmap, per-genome totals and counts), expression (per-pair
+// totals), chain (membership bitmap, per-pair totals).
+struct HiddenLayout {
+  size_t fresh = 0, totals = 0, counts = 0, bytes = 0;
+  HiddenLayout(int64_t G, int32_t depth) {
+    fresh = 0;
+    totals = align256((size_t)G * (size_t)cell_words(depth) * 4);
+    counts = align256(totals + (size_t)G * 4);
+    bytes = align256(counts + (size_t)G * 8);
+  }
+};
+struct ChainLayout {
+  size_t member = 0, totals = 0, bytes = 0;
+  int64_t qwords = 0;
+  ChainLayout(int64_t n_pairs, int32_t depth) {
+    qwords = (emr::n_parents(depth) + 31) / 32;
+    totals = align256((size_t)n_pairs * (size_t)qwords * 4);
+    bytes = align256(totals + (size_t)n_pairs * 4);
+  }
+};
+
+// The offsets of a phase-2 output (k_scan over per-pair or per-genome totals), which also hands the
+// call's flags over.
+emr_status scan_totals(uint32_t* totals, int64_t* counts, int64_t* offsets, int64_t n,
+                       const CallFlags& f, hipStream_t s) {
+  if (n == 0) {
+    HIP_OR_FAIL(emr_launch_fill(offsets, 2, 0u, s));
+    HIP_OR_FAIL(emr_launch_finalize(f.dev, f.host_dev, s));
+    return EMR_OK;
+  }
+  emr::ScanArgs S{};
+  S.pair_total = totals;
+  S.pair_count = counts;
+  S.pair_offset = offsets;
+  S.flags = f.dev;
+  S.host = f.host_dev;
+  S.n_pairs = (uint32_t)n;
+  HIP_OR_FAIL(emr_launch_scan(&S, s));
+  return EMR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+emr_status emr_cell_words(int32_t depth, int64_t* words) {
+  if (depth < 0 || depth > EMR_MAX_DEPTH)
+    return fail(EMR_E_INVAL, "depth %d outside [0, %d]", depth, EMR_MAX_DEPTH);
+  if (!words) return fail(EMR_E_INVAL, "words is NULL");
+  *words = cell_words(depth);
+  return EMR_OK;
+}
+
+emr_status emr_hidden_workspace_bytes(int32_t n_genomes, int32_t depth, int64_t* bytes) {
+  if (n_genomes < 0 || depth < 0 || depth > EMR_MAX_DEPTH || !bytes)
+    return fail(EMR_E_INVAL, "bad arguments");
+  *bytes = (int64_t)HiddenLayout(n_genomes, depth).bytes;
+  return EMR_OK;
+}
+
+emr_status emr_hidden_sources(const emr_population* pop, const emr_source* sources,
+                              int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                              int32_t depth, const emr_result* rec, const emr_hidden* out,
+                              void* stream) {
+  if (!out) return fail(EMR_E_INVAL, "out is NULL");
+  std::shared_ptr<const Plan> plan;
+  emr_status st = plan_for(pop, sources, n_sources, src_offsets, n_shared, depth, &plan);
+  if (st != EMR_OK) return st;
+  const Plan& P = *plan;
+  const int64_t G = pop->n_genomes;
+  emr::RecordsIn R;
+  if ((st = records_in(rec, P.n_pairs, depth, &R)) != EMR_OK) return st;
+  if (out->capacity < 0 || out->capacity > 0xFFFFFFFFll || !out->offsets ||
+      (out->capacity > 0 && !out->sources))
+    return fail(EMR_E_INVAL, "bad hidden-node output buffers");
+  const HiddenLayout L(G, depth);
+  if ((st = check_workspace(out->workspace, out->workspace_bytes, (int64_t)L.bytes)) != EMR_OK)
+    return st;
+  CallTables T;
+  if ((st = call_tables(P, &T)) != EMR_OK) return st;
+  R.pair_info = (const uint32_t*)(T.tables + P.t_pairinfo);
+  R.src_xy = (const float*)(T.tables + P.t_srcxy);
+  const hipStream_t s = (hipStream_t)stream;
+  CallFlags f;
+  if ((st = take_flags(out->workspace, s, &f)) != EMR_OK) return st;
+  char* ws = (char*)out->workspace;
+  emr::HiddenArgs A{};
+  A.rec = R;
+  A.fresh = (uint32_t*)(ws + L.fresh);
+  A.known = out->known;
+  A.totals = (uint32_t*)(ws + L.totals);
+  A.offsets = out->offsets;
+  A.out_src = (uint32_t*)out->sources;
+  A.out_cell = out->cell;
+  A.cap = out->capacity;
+  A.words = cell_words(depth);
+  A.n_genomes = (uint32_t)G;
+  HIP_OR_FAIL(emr_launch_fill(A.fresh, G * A.words, 0u, s));
+  HIP_OR_FAIL(emr_launch_hidden(&A, 0, s));
+  HIP_OR_FAIL(emr_launch_hidden(&A, 1, s));
+  if ((st = scan_totals(A.totals, (int64_t*)(ws + L.counts), out->offsets, G, f, s)) != EMR_OK)
+    return st;
+  HIP_OR_FAIL(emr_launch_hidden(&A, 2, s));
+  f.ok = true;
+  return EMR_OK;
+}
+
+emr_status emr_express_workspace_bytes(int64_t n_pairs, int64_t* bytes) {
+  if (n_pairs < 0 || !bytes) return fail(EMR_E_INVAL, "bad arguments");
+  *bytes = (int64_t)align256((size_t)n_pairs * 4);
+  return EMR_OK;
+}
+
+emr_status emr_express(const emr_population* pop, const emr_source* sources, int32_t n_sources,
+                       const int32_t* src_offsets, int32_t n_shared, int32_t depth,
+                       const emr_result* rec, int32_t type_mask, float w_min,
+                       const emr_connections* out, void* stream) {
+  if (!out) return fail(EMR_E_INVAL, "out is NULL");
+  if (type_mask < 0 || type_mask > EMR_CONN_ALL)
+    return fail(EMR_E_INVAL, "type_mask 0x%x (bits of EMR_CONN_ALL)", type_mask);
+  std::shared_ptr<const Plan> plan;
+  emr_status st = plan_for(pop, sources, n_sources, src_offsets, n_shared, depth, &plan);
+  if (st != EMR_OK) return st;
+  const Plan& P = *plan;
+  emr::RecordsIn R;
+  if ((st = records_in(rec, P.n_pairs, depth, &R)) != EMR_OK) return st;
+  if (out->capacity < 0 || !out->pair_offset || (P.n_pairs > 0 && !out->pair_count) ||
+      (out->capacity > 0 && (!out->cell || !out->w)))
+    return fail(EMR_E_INVAL, "bad connection output buffers");
+  if ((st = check_workspace(out->workspace, out->workspace_bytes,
+                            (int64_t)align256((size_t)P.n_pairs * 4))) != EMR_OK)
+    return st;
+  CallTables T;
+  if ((st = call_tables(P, &T)) != EMR_OK) return st;
+  R.pair_info = (const uint32_t*)(T.tables + P.t_pairinfo);
+  R.src_xy = (const float*)(T.tables + P.t_srcxy);
+  const hipStream_t s = (hipStream_t)stream;
+  CallFlags f;
+  if ((st = take_flags(out->workspace, s, &f)) != EMR_OK) return st;
+  emr::ExpressArgs A{};
+  A.rec = R;
+  A.type_mask = (uint32_t)type_mask;
+  A.w_min = w_min;
+  A.totals = (uint32_t*)out->workspace;
+  A.out_offset = out->pair_offset;
+  A.out_cell = out->cell;
+  A.out_w = out->w;
+  A.cap = out->capacity;
+  if (P.n_pairs > 0) HIP_OR_FAIL(emr_launch_express(&A, 0, s));
+  if ((st = scan_totals(A.totals, out->pair_count, out->pair_offset, P.n_pairs, f, s)) != EMR_OK)
+    return st;
+  if (P.n_pairs > 0) HIP_OR_FAIL(emr_launch_express(&A, 1, s));
+  f.ok = true;
+  return EMR_OK;
+}
+
+emr_status emr_chain_workspace_bytes(int64_t n_pairs, int32_t depth, int64_t* bytes) {
+  if (n_pairs < 0 || depth < 0 || depth > EMR_MAX_DEPTH || !bytes)
+    return fail(EMR_E_INVAL, "bad arguments");
+  *bytes = (int64_t)ChainLayout(n_pairs, depth).bytes;
+  return EMR_OK;
+}
+
+emr_status emr_chain_filter(const emr_result* rec, int64_t n_pairs, int32_t depth,
+                            const emr_result* out, void* stream) {
+  if (!out) return fail(EMR_E_INVAL, "out is NULL");
+  emr::RecordsIn R;
+  emr_status st = records_in(rec, n_pairs, depth, &R);
+  if (st != EMR_OK) return st;
+  if (out->capacity < 0 || out->capacity > 0xFFFFFFFFll || !out->pair_offset ||
+      (n_pairs > 0 && !out->pair_count) || (out->capacity > 0 && (!out->parent || !out->w4)))
+    return fail(EMR_E_INVAL, "bad output buffers");
+  const ChainLayout L(n_pairs, depth);
+  if ((st = check_workspace(out->workspace, out->workspace_bytes, (int64_t)L.bytes)) != EMR_OK)
+    return st;
+  const hipStream_t s = (hipStream_t)stream;
+  CallFlags f;
+  if ((st = take_flags(out->workspace, s, &f)) != EMR_OK) return st;
+  char* ws = (char*)out->workspace;
+  emr::ChainArgs A{};
+  A.rec = R;
+  A.member = (uint32_t*)(ws + L.member);
+  A.qwords = L.qwords;
+  A.totals = (uint32_t*)(ws + L.totals);
+  A.out_offset = out->pair_offset;
+  A.out_parent = out->parent;
+  A.out_w4 = out->w4;
+  A.cap = out->capacity;
+  if (n_pairs > 0) {
+    HIP_OR_FAIL(emr_launch_fill(A.member, n_pairs * L.qwords, 0u, s));
+    HIP_OR_FAIL(emr_launch_chain(&A, 0, s));
+    HIP_OR_FAIL(emr_launch_chain(&A, 1, s));
+  }
+  if ((st = scan_totals(A.totals, out->pair_count, out->pair_offset, n_pairs, f, s)) != EMR_OK)
+    return st;
+  if (n_pairs > 0) HIP_OR_FAIL(emr_launch_chain(&A, 2, s));
+  f.ok = true;
   return EMR_OK;
 }
 

@@ -26,8 +26,11 @@ ABI_FUNCTIONS = [
     "emr_free_population", "emr_population_info", "emr_workspace_bytes", "emr_discover",
     "emr_result_check", "emr_eval_raw", "emr_discover_cost", "emr_profile_enable",
     "emr_profile_read", "emr_stream_chunks", "emr_discover_stream", "emr_pack_population_flat",
-    "emr_set_jit", "emr_jit_info", "emr_eval_raw_noalloc",
+    "emr_set_jit", "emr_jit_info", "emr_eval_raw_noalloc", "emr_call_check", "emr_cell_words",
+    "emr_hidden_workspace_bytes", "emr_hidden_sources", "emr_express_workspace_bytes",
+    "emr_express", "emr_chain_workspace_bytes", "emr_chain_filter",
 ]
+EMR_CONN_FORWARD, EMR_CONN_BACKWARD, EMR_CONN_LATERAL, EMR_CONN_SELF, EMR_CONN_ALL = 1, 2, 4, 8, 15
 EMR_NOALLOC_SCRATCH_BYTES = 32 << 20
 EMR_JIT_OFF, EMR_JIT_AUTO, EMR_JIT_ALWAYS = 0, 1, 2
 
@@ -50,6 +53,18 @@ class emr_source(C.Structure):
 
 class emr_result(C.Structure):
     _fields_ = [("parent", C.c_void_p), ("w4", C.c_void_p), ("capacity", C.c_int64),
+                ("pair_count", C.c_void_p), ("pair_offset", C.c_void_p),
+                ("workspace", C.c_void_p), ("workspace_bytes", C.c_int64)]
+
+
+class emr_hidden(C.Structure):
+    _fields_ = [("sources", C.c_void_p), ("cell", C.c_void_p), ("capacity", C.c_int64),
+                ("offsets", C.c_void_p), ("known", C.c_void_p), ("workspace", C.c_void_p),
+                ("workspace_bytes", C.c_int64)]
+
+
+class emr_connections(C.Structure):
+    _fields_ = [("cell", C.c_void_p), ("w", C.c_void_p), ("capacity", C.c_int64),
                 ("pair_count", C.c_void_p), ("pair_offset", C.c_void_p),
                 ("workspace", C.c_void_p), ("workspace_bytes", C.c_int64)]
 
@@ -98,6 +113,14 @@ def lib():
             "emr_set_jit": (I32, [I32]),
             "emr_eval_raw_noalloc": (I32, [P, P, I32, P, I32, I32, P, P, P]),
             "emr_jit_info": (I32, [P, P, P, P, P, P]),
+            "emr_call_check": (I32, [P, I64, P, P, P]),
+            "emr_cell_words": (I32, [I32, P]),
+            "emr_hidden_workspace_bytes": (I32, [I32, I32, P]),
+            "emr_hidden_sources": (I32, [P, P, I32, P, I32, I32, P, P, P]),
+            "emr_express_workspace_bytes": (I32, [I64, P]),
+            "emr_express": (I32, [P, P, I32, P, I32, I32, P, I32, F32, P, P]),
+            "emr_chain_workspace_bytes": (I32, [I64, I32, P]),
+            "emr_chain_filter": (I32, [P, I64, I32, P, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -500,26 +523,122 @@ def emr_discover_stream(pop: Population, sources, depth: int, theta: float, sink
 
 
 
-# ----------------------------------------------------------------------------- h->h sources
+# ----------------------------------------------------------------------------- after discovery
 
-def hidden_sources(counts, recs, sources, depth: int, n_genomes: int, grid_xy=None):
-    """Host glue for the hidden-to-hidden phase: per genome, the union over its outgoing input
-    sources of the children of kept parents (records_to_host output of a shared-source discover
-    call), deduplicated by heap index in ascending order, as outgoing sources at the cell centres
-    of the library's grid (emr_build_grids). Returns (sources, src_offsets) for a CSR call."""
-    if grid_xy is None:
-        grid_xy = emr_build_grids(depth).cpu().numpy()
-    n_src = len(sources)
-    xs, ys, offs = [], [], [0]
-    for g in range(n_genomes):
-        kids = [4 * recs[g * n_src + j][0][:, None] + np.arange(4)[None, :]
-                for j in range(n_src) if int(sources[j]["dir"]) == EMR_DIR_OUT]
-        idx = np.unique(np.concatenate([k.ravel() for k in kids])) if kids else np.zeros(0, np.int64)
-        xs.append(grid_xy[idx, 0])
-        ys.append(grid_xy[idx, 1])
-        offs.append(offs[-1] + len(idx))
-    src = np.zeros(offs[-1], dtype=[("x", "<f4"), ("y", "<f4"), ("dir", "<i4")])
-    if offs[-1]:
-        src["x"] = np.concatenate(xs)
-        src["y"] = np.concatenate(ys)
-    return src, np.array(offs, np.int32)
+def emr_call_check(workspace, capacity: int, stream=None):
+    """emr_call_check on a call's workspace tensor: (total, largest per pair or genome)."""
+    total, mx = C.c_int64(), C.c_int64()
+    _check(lib().emr_call_check(C.c_void_p(workspace.data_ptr()), int(capacity), C.byref(total),
+                                C.byref(mx), _stream_ptr(stream)))
+    return total.value, mx.value
+
+
+def emr_cell_words(depth: int) -> int:
+    w = C.c_int64()
+    _check(lib().emr_cell_words(depth, C.byref(w)))
+    return w.value
+
+
+def _rec_struct(rec):
+    return rec.get("_struct") or _result_struct(rec)
+
+
+def emr_hidden_sources(pop: Population, sources, depth: int, rec, src_offsets=None, known=None,
+                       capacity=None, stream=None):
+    """The hidden nodes of a checked discover result `rec` (same population, sources and depth):
+    enqueues emr_hidden_sources and checks it (retrying once at the reported total when the
+    capacity was too small). Returns dict(sources int32 [n, 3] device (emr_source records), cell
+    uint32-as-int32 [n] device, offsets int64 [n_genomes + 1] device, total). `known`: an int32
+    device bitmap of n_genomes * emr_cell_words(depth) words or None."""
+    import torch
+    G = pop.n_genomes
+    cap = int(capacity) if capacity is not None else max(1024, 4 * int(rec["pair_offset"][-1].item()))
+    wsb = C.c_int64()
+    _check(lib().emr_hidden_workspace_bytes(G, depth, C.byref(wsb)))
+    ws = torch.empty(max(wsb.value, 256), dtype=torch.uint8, device="cuda")
+    offs = _offsets(src_offsets)
+    src = _sources(sources)
+    # the call ors its new cells into `known`: a retry starts again from the bits given
+    known_before = known.clone() if known is not None else None
+    for attempt in range(2):
+        out = {"sources": torch.empty((max(cap, 1), 3), dtype=torch.int32, device="cuda"),
+               "cell": torch.empty(max(cap, 1), dtype=torch.int32, device="cuda"),
+               "offsets": torch.empty(G + 1, dtype=torch.int64, device="cuda")}
+        st = emr_hidden(out["sources"].data_ptr(), out["cell"].data_ptr(), cap,
+                        out["offsets"].data_ptr(), 0 if known is None else known.data_ptr(),
+                        ws.data_ptr(), ws.numel())
+        _check(lib().emr_hidden_sources(pop.handle, src.ctypes.data, len(sources),
+                                        None if offs is None else offs.ctypes.data,
+                                        0 if offs is not None else len(sources), depth,
+                                        C.byref(_rec_struct(rec)), C.byref(st),
+                                        _stream_ptr(stream)))
+        try:
+            total, _ = emr_call_check(ws, cap, stream)
+        except EmrError as e:
+            if e.status != EMR_E_CAPACITY or attempt == 1:
+                raise
+            cap = int(out["offsets"][-1].item())
+            if known is not None:
+                known.copy_(known_before)
+            continue
+        out["total"] = total
+        return out
+
+
+def hidden_sources_to_host(hs):
+    """(sources as numpy emr_source records, int32 offsets) of an emr_hidden_sources output, for
+    the next emr_discover call's per-genome sources."""
+    n = hs["total"]
+    src = hs["sources"][:n].cpu().numpy().copy().view(SOURCE_DTYPE).reshape(-1)
+    return src, hs["offsets"].cpu().numpy().astype(np.int32)
+
+
+def emr_express(pop: Population, sources, depth: int, rec, type_mask: int = EMR_CONN_ALL,
+                w_min: float = 0.1, src_offsets=None, capacity=None, stream=None):
+    """The connections of a checked discover result (see emr_express in include/emr.h), checked;
+    returns dict(cell, w, pair_count, pair_offset device tensors, total)."""
+    import torch
+    n_pairs = rec["n_pairs"]
+    cap = int(capacity) if capacity is not None else 4 * int(rec["pair_offset"][-1].item())
+    wsb = C.c_int64()
+    _check(lib().emr_express_workspace_bytes(n_pairs, C.byref(wsb)))
+    ws = torch.empty(max(wsb.value, 256), dtype=torch.uint8, device="cuda")
+    out = {"cell": torch.empty(max(cap, 1), dtype=torch.int32, device="cuda"),
+           "w": torch.empty(max(cap, 1), dtype=torch.float32, device="cuda"),
+           "pair_count": torch.empty(max(n_pairs, 1), dtype=torch.int64, device="cuda"),
+           "pair_offset": torch.empty(n_pairs + 1, dtype=torch.int64, device="cuda")}
+    st = emr_connections(out["cell"].data_ptr(), out["w"].data_ptr(), cap,
+                         out["pair_count"].data_ptr(), out["pair_offset"].data_ptr(),
+                         ws.data_ptr(), ws.numel())
+    offs = _offsets(src_offsets)
+    src = _sources(sources)
+    _check(lib().emr_express(pop.handle, src.ctypes.data, len(sources),
+                             None if offs is None else offs.ctypes.data,
+                             0 if offs is not None else len(sources), depth,
+                             C.byref(_rec_struct(rec)), int(type_mask), C.c_float(w_min),
+                             C.byref(st), _stream_ptr(stream)))
+    out["total"], _ = emr_call_check(ws, cap, stream)
+    out["n_pairs"] = n_pairs
+    return out
+
+
+def emr_chain_filter(rec, depth: int, capacity=None, stream=None):
+    """Eq. 2's literal chain rule applied to a checked discover result: a result dict of the same
+    form (checked)."""
+    import torch
+    n_pairs = rec["n_pairs"]
+    cap = int(rec["pair_offset"][-1].item()) if capacity is None else int(capacity)
+    wsb = C.c_int64()
+    _check(lib().emr_chain_workspace_bytes(n_pairs, depth, C.byref(wsb)))
+    out = {"parent": torch.empty(max(cap, 1), dtype=torch.int32, device="cuda"),
+           "w4": torch.empty((max(cap, 1), 4), dtype=torch.float32, device="cuda"),
+           "pair_count": torch.empty(max(n_pairs, 1), dtype=torch.int64, device="cuda"),
+           "pair_offset": torch.empty(n_pairs + 1, dtype=torch.int64, device="cuda"),
+           "workspace": torch.empty(max(wsb.value, 256), dtype=torch.uint8, device="cuda"),
+           "capacity": cap, "n_pairs": n_pairs}
+    st = _result_struct(out)
+    out["_struct"] = st
+    _check(lib().emr_chain_filter(C.byref(_rec_struct(rec)), n_pairs, depth, C.byref(st),
+                                  _stream_ptr(stream)))
+    emr_result_check(out, stream)
+    return out

@@ -38,6 +38,27 @@ def _kernels(asm):
     return out
 
 
+@pytest.fixture(scope="module")
+def phase2_asm():
+    from paper_2608_27612_amd import build
+    with tempfile.TemporaryDirectory() as d:
+        out = os.path.join(d, "p.s")
+        cmd = [build.HIPCC, "-O3", "-std=c++17", "--cuda-device-only", "-S"] + build.DEVICE_FLAGS \
+            + [os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "phase2.hip"), "-o", out]
+        subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
+        return open(out).read()
+
+
+def test_phase2_kernels_have_no_packed_fp32_scalar_writes_m0_or_scratch(phase2_asm):
+    assert not re.search(r"v_pk_(add|mul|fma)_f32", phase2_asm)
+    pattern = r"\bs_(buffer_)?(st" + r"ore|atom" + r"ic)\w*|\bs_dca" + r"che_\w+|\bs_scr" + r"atch_\w+"
+    assert not re.search(pattern, phase2_asm)
+    for line in phase2_asm.splitlines():
+        assert not re.search(r"\bm0\b", line.split(";")[0]), line
+    for size in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", phase2_asm):
+        assert int(size) == 0
+
+
 def test_no_packed_fp32(asm):
     assert not re.search(r"v_pk_(add|mul|fma)_f32", asm)
 

@@ -432,9 +432,10 @@ def test_config3_tabular_pop150_full(emr):
 
 
 def test_config4_recurrent_depth10_two_phases(emr):
-    """The recurrent workload at depth 10: phase 1 (the XOR sources, all 100 genomes) against the
-    oracle; hidden-to-hidden sources built from each side's own phase-1 output agree; phase 2
-    (per-genome CSR sources, one per discovered hidden node) on 64 sampled pairs."""
+    """The recurrent workload at depth 10, end to end on the GPU: phase 1 (the XOR sources, all 100
+    genomes) against the oracle; the hidden nodes found on the device equal the oracle's hidden
+    sources from its own phase 1; phase 2 (per-genome CSR sources, one per hidden node) on 64
+    sampled pairs against the oracle at the same sources."""
     genomes, sources, D, theta = W.workload("recurrent_pop100")
     theta32 = float(np.float32(theta))
     pop = emr.emr_pack_population(genomes)
@@ -456,25 +457,26 @@ def test_config4_recurrent_depth10_two_phases(emr):
             assert close(gw[gi], o["w4"][lo:hi][oi]).all(), r
         else:
             assert close(gw, o["w4"][lo:hi]).all(), r
+    # phase 2's sources on the device (hidden nodes of phase 1); the oracle's from its own phase 1
     hs_o, offs_o = oracle.hidden_sources(o, len(genomes), sources, D)
-    hs_g, offs_g = emr.hidden_sources(counts, recs, sources, D, len(genomes))
+    hs_dev = emr.emr_hidden_sources(pop, sources, D, res)
+    hs_g, offs_g = emr.hidden_sources_to_host(hs_dev)
     if same:
         np.testing.assert_array_equal(offs_g, offs_o)
         np.testing.assert_array_equal(hs_g["x"], hs_o["x"].astype(np.float32))
         np.testing.assert_array_equal(hs_g["y"], hs_o["y"].astype(np.float32))
-    assert offs_o[-1] >= 64
-    # phase 2 on the oracle's sources (CSR output of the default capacity; retried at the
-    # reported total if it overflows)
-    res2 = emr.emr_discover_all(pop, hs_o, D, theta32, src_offsets=offs_o)
+    assert offs_g[-1] >= 64
+    # phase 2 end to end on the GPU (per-genome CSR sources from the device), checked on 64 sampled
+    # pairs against the oracle evaluated at the same sources
+    res2 = emr.emr_discover_all(pop, hs_g, D, theta32, src_offsets=offs_g)
     counts2, recs2 = emr.records_to_host(res2)
     rng = np.random.default_rng(4)
     sample = np.sort(rng.choice(len(counts2), size=64, replace=False))
-    # the sampled pairs as one oracle call: each sampled source with its own genome
-    owner = np.searchsorted(offs_o, sample, side="right") - 1
+    owner = np.searchsorted(offs_g, sample, side="right") - 1
     sub_offs = np.zeros(len(genomes) + 1, np.int32)
     np.add.at(sub_offs, owner + 1, 1)
     sub_offs = np.cumsum(sub_offs).astype(np.int32)
-    oo = oracle.discover(genomes, hs_o[sample], D, theta32, src_offsets=sub_offs)
+    oo = oracle.discover(genomes, hs_g[sample], D, theta32, src_offsets=sub_offs)
     for k, r in enumerate(sample):
         lo, hi = oo["pair_offset"][k], oo["pair_offset"][k + 1]
         op, ow = oo["parent"][lo:hi], oo["w4"][lo:hi]
@@ -483,7 +485,7 @@ def test_config4_recurrent_depth10_two_phases(emr):
             assert close(gw, ow).all(), r
         else:
             diff = np.setxor1d(gp, op)
-            _, dvar = oracle.eval_parents(genomes[owner[k]], hs_o[r], diff)
+            _, dvar = oracle.eval_parents(genomes[owner[k]], hs_g[r], diff)
             assert np.all(np.abs(dvar - theta32) <= BAND), (r, diff[:5], dvar[:5])
 
 
