@@ -367,10 +367,6 @@ struct BindArgs {
   uint32_t n_sources;
   uint32_t blob_words;
   uint64_t bias_floats;
-  uint64_t* nz;            // the compaction's group marks, cleared by the bind kernel
-  uint32_t nz_words;
-  uint32_t* pair_total;    // record mode: per-pair totals, cleared by the bind kernel
-  uint32_t n_pairs;
 };
 
 }  // namespace emr

@@ -95,24 +95,32 @@ __global__ void k_finalize(uint32_t* flags, uint32_t* host) {
 }
 
 constexpr int kScanThreads = 1024;
+constexpr int kScanPer = 4;  // consecutive pairs per thread and round
 
-// One workgroup: pairs in rounds of kScanThreads, thread t taking pair round + t. Writes
-// pair_count, pair_offset (exclusive scan, pair_offset[n_pairs] = the total), clears the totals
-// for the next launch, resets the pool counter, raises the largest count and stores the total in
-// the flags, and, with A.host, hands the flags over.
+// One workgroup: pairs in rounds of kScanThreads * kScanPer, thread t taking the kScanPer pairs
+// from round + kScanPer t (their loads issued together). Writes pair_count, pair_offset
+// (exclusive scan, pair_offset[n_pairs] = the total), clears the totals for the next launch,
+// resets the pool counter, raises the largest count and stores the total in the flags, and, with
+// A.host, hands the flags over.
 __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs A) {
   __shared__ uint64_t wsum[kScanThreads / kWave];
   __shared__ uint32_t wmax[kScanThreads / kWave];
   const uint32_t t = threadIdx.x, lane = t % kWave, wv = t / kWave;
   uint64_t carry = 0;
   uint32_t mx = 0;
-  for (uint32_t round = 0; round < A.n_pairs; round += kScanThreads) {
-    const uint32_t i = round + t;
-    const bool mine = i < A.n_pairs;
-    const uint32_t c = mine ? A.pair_total[i] : 0u;
-    if (mine) A.pair_total[i] = 0u;
-    mx = max(mx, c);
-    uint64_t incl = c;  // inclusive scan within the wave
+  for (uint32_t round = 0; round < A.n_pairs; round += kScanThreads * kScanPer) {
+    const uint32_t i0 = round + t * kScanPer;
+    uint32_t c[kScanPer];
+#pragma unroll
+    for (int k = 0; k < kScanPer; ++k) c[k] = i0 + k < A.n_pairs ? A.pair_total[i0 + k] : 0u;
+    uint32_t mine = 0;
+#pragma unroll
+    for (int k = 0; k < kScanPer; ++k) {
+      if (i0 + k < A.n_pairs) A.pair_total[i0 + k] = 0u;
+      mine += c[k];
+      mx = max(mx, c[k]);
+    }
+    uint64_t incl = mine;  // inclusive scan of the threads' sums within the wave
 #pragma unroll
     for (int off = 1; off < kWave; off <<= 1) {
       const uint64_t v = __shfl_up(incl, off, kWave);
@@ -126,14 +134,17 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs A) {
       if ((uint32_t)k < wv) before += wsum[k];
       round_total += wsum[k];
     }
-    if (mine) {
-      A.pair_count[i] = c;
-      A.pair_offset[i] = (int64_t)(carry + before + incl - c);
-    }
+    uint64_t at = carry + before + incl - mine;
+#pragma unroll
+    for (int k = 0; k < kScanPer; ++k)
+      if (i0 + k < A.n_pairs) {
+        A.pair_count[i0 + k] = c[k];
+        A.pair_offset[i0 + k] = (int64_t)at;
+        at += c[k];
+      }
     carry += round_total;
     __syncthreads();  // wsum is rewritten by the next round
   }
-  if (lane == 0) wmax[wv] = 0u;
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off, kWave));
   if (lane == 0) wmax[wv] = mx;
@@ -304,19 +315,9 @@ __global__ void __launch_bounds__(kBindWaves * kWave)
     k_bind(const uint32_t* __restrict__ blob, const ProgDesc* __restrict__ desc,
            const Member* __restrict__ members, const float* __restrict__ src_xy,
            float* __restrict__ bias_tab, uint32_t* __restrict__ err, uint32_t n_members,
-           uint32_t n_desc, uint32_t n_sources, uint32_t blob_words, uint64_t bias_floats,
-           uint64_t* __restrict__ nz, uint32_t nz_words, uint32_t* __restrict__ pair_total,
-           uint32_t n_pairs) {
+           uint32_t n_desc, uint32_t n_sources, uint32_t blob_words, uint64_t bias_floats) {
   __shared__ float U_all[kBindWaves][kMaxU];
   __shared__ uint32_t prog_all[kBindWaves][kBindProgWords];
-  // the compaction's group marks and per-pair totals start out clear (the discover kernel sets
-  // them)
-  for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < nz_words; k += gridDim.x * blockDim.x)
-    nz[k] = 0ull;
-  if (pair_total)
-    for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < n_pairs;
-         k += gridDim.x * blockDim.x)
-      pair_total[k] = 0u;
   const uint32_t lane = lane_id();
   const uint32_t wv = threadIdx.x / kWave;
   const uint32_t i = __builtin_amdgcn_readfirstlane(blockIdx.x * kBindWaves + wv);
@@ -479,8 +480,7 @@ extern "C" hipError_t emr_launch_bind(const emr::BindArgs* a, hipStream_t s) {
   hipLaunchKernelGGL(emr::k_bind, dim3((a->n_members + emr::kBindWaves - 1) / emr::kBindWaves),
                      dim3(emr::kBindWaves * emr::kWave), 0, s, a->blob, a->desc,
                      a->members, a->src_xy, a->bias_tab, a->err, a->n_members, a->n_desc,
-                     a->n_sources, a->blob_words, a->bias_floats, a->nz, a->nz_words,
-                     a->pair_total, a->n_pairs);
+                     a->n_sources, a->blob_words, a->bias_floats);
   return hipGetLastError();
 }
 

@@ -318,12 +318,16 @@ struct Plan {
   size_t t_pairinfo = 0;  // per pair: genome << 1 | dir, source index (two words)
   mutable std::mutex dev_mu;
   mutable char* d_tables = nullptr;
+  // The bias rows of the plan's groups (the bind kernel's output: every position-independent
+  // contribution per (genome, source)), computed on the device once, on first use (dev_mu).
+  mutable float* d_bias = nullptr;
   Plan() = default;
   Plan(const Plan&) = delete;
   Plan& operator=(const Plan&) = delete;
   ~Plan() {
     jit.reset();  // drains the device before the compiled tier's module goes
     if (d_tables) (void)hipFree(d_tables);
+    if (d_bias) (void)hipFree(d_bias);
   }
   // The compiled tier (jit_use): built at most once per plan, under jit_mu.
   mutable std::mutex jit_mu;
@@ -337,13 +341,17 @@ struct Plan {
   bool key_has_offs = false;
   int32_t key_n_shared = 0;
   // Workspace layout (bytes from the workspace start): tile status words, the compaction's group
-  // marks and per-pair record totals (both cleared by k_bind), the bias rows; then (total
-  // onwards) the record pool of a call's capacity.
+  // marks and per-pair record totals (cleared before each record call: clear_words words from
+  // off_nz); then (total onwards) the record pool of a call's capacity.
   size_t off_status = 0;
-  size_t off_bias = 0, total = 0;
+  size_t total = 0;
   size_t status_bytes = 0;
   size_t off_nz = 0, nz_bytes = 0;
   size_t off_ptotal = 0;
+  int64_t clear_words = 0;
+  // Floats of a bias table: the groups' rows plus 16 floats of padding (the compiled tier loads a
+  // group's rows 1 .. 4 at once).
+  size_t bias_table_floats() const { return (size_t)bias_floats + 16; }
 };
 
 // The record pool after a plan's fixed workspace: `capacity` parent indices, then (16-byte
@@ -483,15 +491,14 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
     P.src_xy[2 * i + 1] = sources[i].y;
   }
 
-  // workspace: tile status words, group marks, per-pair totals, bias rows
+  // workspace: tile status words, group marks, per-pair totals
   P.off_status = 0;
   P.status_bytes = (size_t)P.n_pairs * P.tiles * 8;
   P.off_nz = align256(P.off_status + P.status_bytes);
   P.nz_bytes = (size_t)P.n_pairs * emr::nz_words((uint32_t)P.tiles) * 8;
   P.off_ptotal = align256(P.off_nz + P.nz_bytes);
-  P.off_bias = align256(P.off_ptotal + (size_t)P.n_pairs * 4);
-  // 16 floats of padding after the bias table: the compiled tier loads a group's rows 1 .. 4 at once
-  P.total = align256(P.off_bias + (P.bias_floats + 16) * sizeof(float));
+  P.total = align256(P.off_ptotal + (size_t)P.n_pairs * 4);
+  P.clear_words = (int64_t)((P.off_ptotal + (size_t)P.n_pairs * 4 - P.off_nz + 3) / 4);
   // tables
   P.t_groups = 0;
   P.t_members = align256(P.groups.size() * sizeof(emr::Group));
@@ -688,44 +695,75 @@ emr_status take_flags(const void* workspace, hipStream_t s, CallFlags* f) {
   return EMR_OK;
 }
 
-// Where a call's kernels find the plan's tables and the depth's tile geometry: the plan's own
-// device copies (plan_tables, tile_geo_table), or copies in the allocation-free scratch.
+// Where a call's kernels find the plan's tables, the depth's tile geometry and the bias rows: the
+// plan's own device copies (call_tables), or copies in the allocation-free scratch.
 struct CallTables {
   const char* tables = nullptr;
   const uint32_t* geo = nullptr;
   uint32_t geo_rows = 0;
+  const float* bias = nullptr;
 };
 
-// Checks the workspace (need: its bytes for this call) and fills the bind kernel's arguments over
-// the plan's tables (*b: launched by the caller).
-emr_status prepare_plan(const emr_population* pop, const Plan& P, const CallTables& T,
-                        void* workspace, int64_t workspace_bytes, int64_t need, hipStream_t s,
-                        uint32_t* flags, emr::BindArgs* bind) {
-  (void)s;
-  if (!workspace || workspace_bytes < need)
-    return fail(EMR_E_INVAL, "workspace of %lld bytes is smaller than the %lld needed",
-                (long long)workspace_bytes, (long long)need);
-  if (((uintptr_t)workspace & 255) != 0) return fail(EMR_E_INVAL, "workspace not 256-byte aligned");
-  char* ws = (char*)workspace;
-  const char* tables = T.tables;
-
+// The bind kernel's arguments over the plan's tables: bias rows to `bias` (bias_table_floats()),
+// table errors raised into *err.
+emr::BindArgs bind_args(const emr_population* pop, const Plan& P, const char* tables, float* bias,
+                        uint32_t* err) {
   emr::BindArgs b{};
   b.blob = pop->d_blob;
   b.desc = pop->d_desc;
   b.members = (const emr::Member*)(tables + P.t_members);
   b.src_xy = (const float*)(tables + P.t_srcxy);
-  b.bias_tab = (float*)(ws + P.off_bias);
-  b.err = flags;
+  b.bias_tab = bias;
+  b.err = err;
   b.n_members = (uint32_t)P.members.size();
   b.n_desc = (uint32_t)pop->desc.size();
   b.n_sources = (uint32_t)(P.src_xy.size() / 2);
   b.blob_words = (uint32_t)pop->blob_words;
   b.bias_floats = P.bias_floats;
-  b.nz = (uint64_t*)(ws + P.off_nz);
-  b.nz_words = (uint32_t)(P.nz_bytes / 8);
-  b.pair_total = (uint32_t*)(ws + P.off_ptotal);
-  b.n_pairs = (uint32_t)P.n_pairs;
-  *bind = b;
+  return b;
+}
+
+// The plan's bias rows on the device, computed on first use by the bind kernel on the library's
+// stream and waited for (a table error found then fails the call that needed them).
+emr_status plan_bias(const emr_population* pop, const Plan& P, const char* tables,
+                     const float** out) {
+  std::lock_guard<std::mutex> lock(P.dev_mu);
+  if (!P.d_bias) {
+    const size_t n = P.bias_table_floats();
+    float* d = nullptr;
+    if (hipMalloc((void**)&d, (n + 64) * sizeof(float)) != hipSuccess)
+      return fail(EMR_E_NOMEM, "bias rows of %zu floats", n);
+    uint32_t* err = (uint32_t*)(d + n);  // one word after the rows and their padding
+    StreamPool* sp = nullptr;
+    emr_status st = stream_pool(&sp);
+    uint32_t host_err = 0;
+    if (st == EMR_OK) {
+      const emr::BindArgs b = bind_args(pop, P, tables, d, err);
+      if (emr_launch_fill(d, (int64_t)n + 1, 0u, sp->aux[0]) != hipSuccess ||
+          emr_launch_bind(&b, sp->aux[0]) != hipSuccess ||
+          hipMemcpyAsync(&host_err, err, 4, hipMemcpyDeviceToHost, sp->aux[0]) != hipSuccess ||
+          hipStreamSynchronize(sp->aux[0]) != hipSuccess)
+        st = fail(EMR_E_DEVICE, "computing the bias rows failed");
+      else if (host_err)
+        st = fail(EMR_E_DEVICE, "the bind kernel reported error flags 0x%x (2: a table entry out "
+                  "of range)", host_err);
+    }
+    if (st != EMR_OK) {
+      (void)hipFree(d);
+      return st;
+    }
+    P.d_bias = d;
+  }
+  *out = P.d_bias;
+  return EMR_OK;
+}
+
+// A call's workspace: at least `need` bytes, 256-byte aligned.
+emr_status check_call_workspace(const void* workspace, int64_t workspace_bytes, int64_t need) {
+  if (!workspace || workspace_bytes < need)
+    return fail(EMR_E_INVAL, "workspace of %lld bytes is smaller than the %lld needed",
+                (long long)workspace_bytes, (long long)need);
+  if (((uintptr_t)workspace & 255) != 0) return fail(EMR_E_INVAL, "workspace not 256-byte aligned");
   return EMR_OK;
 }
 
@@ -949,8 +987,8 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
 // pool in the workspace; raw outputs go to raw[r * N(D) + p].
 // jit: run the plan's compiled programs (jit_use said so) instead of the interpreter. With
 // `finalize`, k_finalize then hands the call's flags to their pinned words.
-// With `bind`, the bind kernel goes right before the first discover launch, once every argument
-// of that launch is ready on the host (so the GPU does not wait for host work between them).
+// With `clear` (record mode), the workspace's group marks and per-pair totals are cleared right
+// before the discover launch, once every argument of that launch is ready on the host.
 // flags: the call's device flag words (error bits, largest count); flags_host: their pinned words
 // (device view) for k_finalize.
 // timing: the thread's launch profiling applies to this call (off for the allocation-free call,
@@ -958,8 +996,8 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
 emr_status launch_range(const emr_population* pop, const Plan& P, const CallTables& T,
                         float theta, const emr_result* out, float* raw, void* workspace,
                         hipStream_t s, int64_t tile_lo, int64_t n_tiles, bool jit,
-                        uint32_t* flags, uint32_t* flags_host, bool finalize,
-                        const emr::BindArgs* bind, bool timing = true) {
+                        uint32_t* flags, uint32_t* flags_host, bool finalize, bool clear,
+                        bool timing = true) {
   char* ws = (char*)workspace;
   const char* tables = T.tables;
   const uint32_t* geo_tab = T.geo;
@@ -994,7 +1032,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
     a.geo_rows = geo_rows;
     a.blob = pop->d_blob;
     a.groups = jit ? P.jit->d_groups : (const emr::Group*)(tables + P.t_groups);
-    a.bias_tab = (const float*)(ws + P.off_bias);
+    a.bias_tab = T.bias;
     a.status = (uint64_t*)(ws + P.off_status);
     a.nz = (uint64_t*)(ws + P.off_nz);
     a.err = flags;
@@ -1023,7 +1061,8 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
     const bool timed = li < n_timed;
     hipEvent_t e0 = timed ? prof.events[2 * (rec0 + li)] : nullptr;
     hipEvent_t e1 = timed ? prof.events[2 * (rec0 + li) + 1] : nullptr;
-    if (li == 0 && bind) HIP_OR_FAIL(emr_launch_bind(bind, s));
+    if (li == 0 && clear && records)
+      HIP_OR_FAIL(emr_launch_fill(ws + P.off_nz, P.clear_words, 0u, s));
     if (jit) {
       emr_status js = jit_launch(P, a, mode, blocks, s, e0, e1);
       if (js != EMR_OK) return js;
@@ -1046,6 +1085,8 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
     }
   }
   if (timed_call) prof.calls++;
+  if (clear && records && P.launches.empty())
+    HIP_OR_FAIL(emr_launch_fill(ws + P.off_nz, P.clear_words, 0u, s));
   if (records && P.n_pairs > 0) {
     emr::ScanArgs S{};
     S.pair_total = (uint32_t*)(ws + P.off_ptotal);
@@ -1076,35 +1117,31 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
   return EMR_OK;
 }
 
-// The plan's own device tables and the depth's tile geometry table (allocated on first use).
-emr_status call_tables(const Plan& P, CallTables* T) {
+// The plan's own device tables and bias rows and the depth's tile geometry table (each made on
+// first use).
+emr_status call_tables(const emr_population* pop, const Plan& P, CallTables* T) {
   char* tables = nullptr;
   emr_status st = plan_tables(P, &tables);
   if (st != EMR_OK) return st;
   T->tables = tables;
+  if ((st = plan_bias(pop, P, tables, &T->bias)) != EMR_OK) return st;
   return tile_geo_table(P.depth, &T->geo, &T->geo_rows);
 }
 
-// Enqueue a whole call: take a flag slot, prepare, then every tile of every pair.
+// Enqueue a whole call: take a flag slot, then every tile of every pair.
 emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const emr_result* out,
                     float* raw, void* workspace, int64_t workspace_bytes, hipStream_t s) {
+  emr_status st = check_call_workspace(workspace, workspace_bytes,
+                                       (int64_t)workspace_need(P, out ? out->capacity : 0));
+  if (st != EMR_OK) return st;
   CallTables T;
-  emr_status st = call_tables(P, &T);
-  if (st != EMR_OK) return st;
+  if ((st = call_tables(pop, P, &T)) != EMR_OK) return st;
   CallFlags f;
-  st = take_flags(workspace, s, &f);
-  if (st != EMR_OK) return st;
-  emr::BindArgs bind{};
-  st = prepare_plan(pop, P, T, workspace, workspace_bytes,
-                    (int64_t)workspace_need(P, out ? out->capacity : 0), s, f.dev, &bind);
-  if (st != EMR_OK) return st;
+  if ((st = take_flags(workspace, s, &f)) != EMR_OK) return st;
   bool jit = false;
-  st = jit_use(pop, P, plan_slots(P), &jit);
-  if (st != EMR_OK) return st;
-  if (P.launches.empty()) HIP_OR_FAIL(emr_launch_bind(&bind, s));  // (no discover launch)
+  if ((st = jit_use(pop, P, plan_slots(P), &jit)) != EMR_OK) return st;
   st = launch_range(pop, P, T, theta, out, raw, workspace, s, 0, P.tiles, jit, f.dev, f.host_dev,
-                    true,
-                    P.launches.empty() ? nullptr : &bind);
+                    true, true);
   if (st != EMR_OK) return st;
   f.ok = true;
   return EMR_OK;
@@ -1435,10 +1472,11 @@ emr_status emr_eval_raw_noalloc(const emr_population* pop, const emr_source* sou
   const Plan& P = *plan;
   if (P.n_pairs > 0 && emr::n_positions(depth) > 0 && !out_dev)
     return fail(EMR_E_INVAL, "out_dev is NULL");
-  // Scratch layout: the plan's tables, the tile geometry rows, then the workspace.
+  // Scratch layout: the plan's tables, the tile geometry rows, the bias rows, then the workspace.
   const int64_t geo_rows = P.tiles + emr::kGeoPadRows;
   const size_t off_geo = align256(P.img.size());
-  const size_t off_ws = align256(off_geo + (size_t)geo_rows * 16);
+  const size_t off_bias = align256(off_geo + (size_t)geo_rows * 16);
+  const size_t off_ws = align256(off_bias + P.bias_table_floats() * sizeof(float));
   const size_t need = off_ws + P.total;
   if (need > (size_t)EMR_NOALLOC_SCRATCH_BYTES)
     return fail(EMR_E_LIMIT, "the call needs %zu bytes of scratch; the allocation-free scratch "
@@ -1451,19 +1489,18 @@ emr_status emr_eval_raw_noalloc(const emr_population* pop, const emr_source* sou
   T.tables = scr;
   T.geo = (const uint32_t*)(scr + off_geo);
   T.geo_rows = (uint32_t)geo_rows;
+  T.bias = (const float*)(scr + off_bias);
   char* ws = scr + off_ws;
-  // The call's first kernel clears the caller's error word; then the tables and the geometry.
+  // The call's first kernel clears the caller's error word; then the tables, the geometry and the
+  // bias rows (the bind kernel, each call: they live in the shared scratch).
   HIP_OR_FAIL(emr_launch_fill(err_dev, 1, 0u, s));
   HIP_OR_FAIL(hipMemcpyAsync(scr, P.img.data(), P.img.size(), hipMemcpyHostToDevice, s));
   HIP_OR_FAIL(emr_launch_tile_geo((uint32_t*)(scr + off_geo), (uint32_t)P.tiles,
                                   (uint32_t)geo_rows, s));
-  emr::BindArgs bind{};
-  emr_status st = prepare_plan(pop, P, T, ws, (int64_t)P.total, (int64_t)P.total, s, err_dev,
-                               &bind);
-  if (st != EMR_OK) return st;
-  if (P.launches.empty()) HIP_OR_FAIL(emr_launch_bind(&bind, s));  // (no discover launch)
+  const emr::BindArgs bind = bind_args(pop, P, scr, (float*)(scr + off_bias), err_dev);
+  HIP_OR_FAIL(emr_launch_bind(&bind, s));
   return launch_range(pop, P, T, 0.0f, nullptr, out_dev, ws, s, 0, P.tiles, false, err_dev,
-                      nullptr, false, P.launches.empty() ? nullptr : &bind, false);
+                      nullptr, false, false, false);
 }
 
 emr_status emr_discover_cost(const emr_population* pop, const emr_source* sources,
@@ -1712,15 +1749,12 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
   }
 
   CallTables T;
-  st = call_tables(P, &T);
+  st = call_tables(pop, P, &T);
   if (st != EMR_OK) return st;
+  if ((st = check_call_workspace(R.ws, R.ws_bytes, ws_need)) != EMR_OK) return st;
   CallFlags f;  // the chunks raise into its words, handed over once at the end
   st = take_flags(nullptr, R.s, &f);
   if (st != EMR_OK) return st;
-  emr::BindArgs bind{};
-  st = prepare_plan(pop, P, T, R.ws, R.ws_bytes, ws_need, R.s, f.dev, &bind);
-  if (st != EMR_OK) return st;
-  HIP_OR_FAIL(emr_launch_bind(&bind, R.s));
   bool jit = false;
   st = jit_use(pop, P, plan_slots(P) * (double)(total - start) / (double)total, &jit);
   if (st != EMR_OK) return st;
@@ -1734,7 +1768,7 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     emr_result chunk_out{R.g_parent[b], R.g_w4[b], records, R.counts, R.offsets, R.ws,
                          R.ws_bytes};
     emr_status e = launch_range(pop, P, T, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n, jit,
-                                f.dev, f.host_dev, false, nullptr);
+                                f.dev, f.host_dev, false, true);
     if (e != EMR_OK) return e;
     if (n_pairs > 0)
       HIP_OR_FAIL(hipMemcpyAsync(R.counts_h[b], R.counts, (size_t)n_pairs * 8,
@@ -1932,7 +1966,7 @@ emr_status emr_hidden_sources(const emr_population* pop, const emr_source* sourc
   if ((st = check_workspace(out->workspace, out->workspace_bytes, (int64_t)L.bytes)) != EMR_OK)
     return st;
   CallTables T;
-  if ((st = call_tables(P, &T)) != EMR_OK) return st;
+  if ((st = call_tables(pop, P, &T)) != EMR_OK) return st;
   R.pair_info = (const uint32_t*)(T.tables + P.t_pairinfo);
   R.src_xy = (const float*)(T.tables + P.t_srcxy);
   const hipStream_t s = (hipStream_t)stream;
@@ -1986,7 +2020,7 @@ emr_status emr_express(const emr_population* pop, const emr_source* sources, int
                             (int64_t)align256((size_t)P.n_pairs * 4))) != EMR_OK)
     return st;
   CallTables T;
-  if ((st = call_tables(P, &T)) != EMR_OK) return st;
+  if ((st = call_tables(pop, P, &T)) != EMR_OK) return st;
   R.pair_info = (const uint32_t*)(T.tables + P.t_pairinfo);
   R.src_xy = (const float*)(T.tables + P.t_srcxy);
   const hipStream_t s = (hipStream_t)stream;
