@@ -12,7 +12,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libemr.so")
 JIT_CO = os.path.join(HERE, "libemr_jit.co")
-SOURCES = ["kernels.hip", "phase2.hip", "runtime.cpp", "pack.cpp", "jit.cpp", "jit_image.cpp"]
+SOURCES = ["kernels.hip", "phase2.hip", "runtime.cpp", "pack.cpp", "sched.cpp", "jit.cpp",
+           "jit_image.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # No packed-FP32 instructions anywhere in the device code.
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -418,10 +418,12 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
                           lane);
 }
 
-// One launch: every part, each chunk dispatched to the code of its part's (S, W). Chunks are
-// handed out round-robin over the waves: chunk c goes to wave c mod n_waves. A group's chunks go
-// to consecutive waves, so a pair's tiles are computed concurrently, and each wave visits its
-// tiles in increasing order.
+// One launch: every part, each chunk dispatched to the code of its part's (S, W). A workgroup
+// (one CU) owns a share of the chunks: the entries of its list when the launch has a schedule
+// (lists balanced across CUs by the host's cost model, costliest chunk first), else chunks
+// b, b + n_wg, ... (round-robin); its waves take them in that order, one at a time, from a
+// counter in LDS. Chunks are independent: each writes its own tiles' status words, records and raw
+// outputs, and adds to counters, so neither their order nor their wave matters for the result.
 // (The body of the discover kernels: k_discover below runs the interpreter, the template code
 // object's kernels the compiled programs.)
 template <int MODE, bool JIT>
@@ -439,11 +441,45 @@ __device__ __forceinline__ void discover_body(const uint32_t* __restrict__ geo_t
                     {(float)(4u * j_lo), (float)(4u * j_lo + 2u)}};
   const DiscoverPtrs d{(cu32*)geo_tab, (cu32*)blob, (cu32*)groups, (cf32*)bias_tab, status, err,
                        raw};
-  const uint32_t n_waves = gridDim.x * (blockDim.x / kWave);
-  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) +
-                                                       threadIdx.x / kWave);
-
-  for (uint32_t c = wave; c < a.n_chunks; c += n_waves) {
+  const uint32_t n_wg = gridDim.x, wg = blockIdx.x;
+  // the workgroup's next share entry; one barrier before any wave takes one
+  __shared__ uint32_t next;
+  if (threadIdx.x == 0) next = 0u;
+  __syncthreads();
+  // (the launcher accepts a schedule only when it was made for this grid: sched_lists == n_wg,
+  // so row wg and its sched_stride entries lie inside the table)
+  const bool listed = a.sched != nullptr;
+  for (;;) {
+    // The wave's share entry: every lane adds to `next`, lane 0 one and the others zero, so lane
+    // 0 reads the entry it took. (One asm statement: as a lane-0 branch around an atomicAdd the
+    // compiler keeps values live across the loop in a way that spills.)
+    uint32_t e, one, addr;
+    asm volatile(
+        "v_mbcnt_lo_u32_b32 %1, -1, 0\n\t"
+        "v_cmp_eq_u32_e32 vcc, 0, %1\n\t"
+        "v_cndmask_b32_e64 %1, 0, 1, vcc\n\t"
+        "v_mov_b32 %2, %3\n\t"
+        "ds_add_rtn_u32 %0, %2, %1\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=v"(e), "=&v"(one), "=&v"(addr)
+        : "s"((uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)&next)
+        : "vcc", "memory");
+    e = __builtin_amdgcn_readfirstlane(e);
+    uint32_t c;
+    if (listed) {
+      if (e >= a.sched_stride) break;
+      c = __builtin_amdgcn_readfirstlane(a.sched[wg * a.sched_stride + e]);
+      if (c == kNoChunk) break;
+      if (c >= a.n_chunks) {
+        if (lane == 0) atomicOr(err, kErrTable);
+        break;
+      }
+    } else {
+      // (each wave takes one entry past the share's end at most, so c < n_chunks + 13 n_wg,
+      // which does not wrap with n_chunks < 2^31)
+      c = wg + e * n_wg;
+      if (c >= a.n_chunks) break;
+    }
     // the chunk's part, and its index within the part
     uint32_t k = 0, cl = c;
     while (k + 1 < a.n_parts && cl >= a.part[k].n_chunks) {

@@ -185,7 +185,21 @@ struct DiscoverScalars {
   uint32_t* pool_parent;
   float* pool_w4;
   uint32_t* pair_total;
+  // The workgroups' chunk lists, or NULL for round-robin chunks (chunk c to workgroup c mod
+  // workgroups): workgroup b's waves take chunks sched[b * sched_stride + j], j = 0, 1, ..., up to
+  // the first kNoChunk. The lists were made for exactly sched_lists workgroups (the launch's grid);
+  // sched_stride is a multiple of 64.
+  const uint32_t* sched;
+  uint32_t sched_stride, sched_lists;
 };
+constexpr uint32_t kNoChunk = 0xFFFFFFFFu;
+
+// A discover workgroup fills one CU: 3 waves on each of its 4 SIMDs (the kernels' register budget
+// allows 3), taking their workgroup's chunks one at a time from a counter in LDS. A SIMD issues
+// for its oldest wave first, so waves of one workgroup progress at different speeds; taking chunks
+// as they free up keeps every wave busy until the CU's share runs out.
+constexpr int kDiscoverWaves = 12;
+constexpr int kDiscoverThreads = kDiscoverWaves * kWave;
 
 // Output modes: raw CPPN outputs; records of kept cells, each walk's reserved in a pool with one
 // atomic, each tile's pool offset and count left in its status word and each chunk's count added
@@ -279,6 +293,8 @@ struct DiscoverArgs {
   uint32_t blob_words;     // size of the population table
   uint32_t n_pairs;        // pairs of the call (bound for pair ids)
   uint64_t bias_floats;    // size of the bias table
+  const uint32_t* sched;   // the workgroups' chunk lists (DiscoverScalars::sched), or NULL
+  uint32_t sched_stride, sched_lists;
 };
 
 // Arguments of the compaction of one record-mode range: k_scan (the pairs' offsets, one

@@ -30,11 +30,11 @@ __device__ __forceinline__ uint64_t code_area_base() {
       uint32_t *__restrict__ err, float *__restrict__ raw, emr::DiscoverScalars a
 
 // One kernel per output mode (raw outputs, records to the pool).
-extern "C" __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) emr_discover_jit_raw(EMR_JIT_PARAMS) {
+extern "C" __global__ void __launch_bounds__(emr::kDiscoverThreads) emr_discover_jit_raw(EMR_JIT_PARAMS) {
   emr::discover_body<emr::kModeRaw, true>(geo, blob, groups, bias_tab, status, err, raw, a,
                                           emr::code_area_base());
 }
-extern "C" __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) emr_discover_jit_records(EMR_JIT_PARAMS) {
+extern "C" __global__ void __launch_bounds__(emr::kDiscoverThreads) emr_discover_jit_records(EMR_JIT_PARAMS) {
   emr::discover_body<emr::kModeRecords, true>(geo, blob, groups, bias_tab, status, err, raw, a,
                                               emr::code_area_base());
 }

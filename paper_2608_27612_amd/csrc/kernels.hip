@@ -273,7 +273,7 @@ __global__ void __launch_bounds__(kMoveWaves * kWave) k_move(MoveArgs A) {
 
 // The interpreting discover kernel: one launch covers every part of a call.
 template <int MODE>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(kDiscoverThreads)
     k_discover(const uint32_t* __restrict__ geo, const uint32_t* __restrict__ blob,
                const Group* __restrict__ groups,
                const float* __restrict__ bias_tab, uint64_t* __restrict__ status,
@@ -504,7 +504,7 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   // Chunk size: the largest of 16, 8 and 4 tiles that still gives every resident wave at least
   // four chunks (fewer, longer chunks spend less per-chunk work; enough of them keep the waves
   // balanced); else each chunk is one walk's worth of tiles, for parallelism.
-  const uint64_t waves = 4ull * (uint64_t)per_cu * (uint64_t)cus;
+  const uint64_t waves = (uint64_t)emr::kDiscoverWaves * (uint64_t)per_cu * (uint64_t)cus;
   uint32_t target = 0;
   for (uint32_t c : {emr::kChunkTilesMax, 8u, 4u})
     if (target == 0 && groups * ((a->tiles + c - 1) / c) >= 4ull * waves) target = c;
@@ -524,7 +524,8 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
                                    a->part_groups[k] * cpg, cpg, chunk};
     chunks += (uint64_t)a->part_groups[k] * cpg;
   }
-  if (chunks > 0xFFFFFFFFull) return hipErrorInvalidValue;
+  // (a workgroup's chunk index then stays below 2^32 when it steps past its last chunk)
+  if (chunks > 0x7FFFFFFFull) return hipErrorInvalidValue;
   sc.n_chunks = (uint32_t)chunks;
   sc.depth = a->depth;
   sc.theta16 = 16.0f * a->theta;
@@ -541,15 +542,37 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   sc.pool_parent = a->pool_parent;
   sc.pool_w4 = a->pool_w4;
   sc.pair_total = a->pair_total;
-  // Clamp the grid to what can be resident at once: the waves walk their chunks (no wave waits
-  // for another).
+  // Clamp the grid to what can be resident at once (the waves take their chunks; none waits for
+  // another), and to one workgroup per chunk (few chunks: spread over as many CUs).
   const uint32_t resident = (uint32_t)per_cu * (uint32_t)cus;
-  const uint32_t needed = (uint32_t)((chunks + 3) / 4);  // one wave per chunk, 4 per workgroup
-  if (blocks > needed) blocks = needed;
+  if (blocks > chunks) blocks = (uint32_t)chunks;
   if (blocks > resident) blocks = resident;
+  // A schedule is made for one grid: it must be this launch's.
+  if (a->sched != nullptr) {
+    if (a->sched_lists != blocks || a->sched_stride == 0u || a->sched_stride % emr::kWave != 0u)
+      return hipErrorInvalidValue;
+    sc.sched = a->sched;
+    sc.sched_stride = a->sched_stride;
+    sc.sched_lists = a->sched_lists;
+  }
   *out = sc;
   *grid = blocks;
   return hipSuccess;
+}
+
+// Workgroups of the interpreter's discover kernel (mode 0 raw, 1 records) that fit on one CU.
+extern "C" int emr_discover_per_cu(int mode) {
+  auto occ = [](auto kern) {
+    int n = 0;
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, emr::kDiscoverThreads, 0) ==
+                   hipSuccess &&
+               n > 0
+               ? n
+               : 1;
+  };
+  static const int per_cu[2] = {occ(emr::k_discover<emr::kModeRaw>),
+                                occ(emr::k_discover<emr::kModeRecords>)};
+  return per_cu[mode == emr::kModeRecords ? 1 : 0];
 }
 
 template <int MODE>
@@ -561,13 +584,7 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
     return e;
-  // Workgroups of this kernel that fit on one CU (a property of the compiled kernel).
-  static const int per_cu = [&] {
-    int n = 0;
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, 256, 0) == hipSuccess && n > 0
-               ? n
-               : 1;
-  }();
+  const int per_cu = emr_discover_per_cu(MODE);
   emr::DiscoverScalars sc{};
   uint32_t grid = 0;
   if ((e = emr_discover_setup(a, blocks, per_cu, cus, &sc, &grid)) != hipSuccess) return e;
@@ -585,7 +602,7 @@ static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks,
   uint32_t* err = a->err;
   float* raw = a->raw;
   if (start && (e = hipEventRecord(start, s)) != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, geo, blob, grp, bias_tab, status, err, raw,
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(emr::kDiscoverThreads), 0, s, geo, blob, grp, bias_tab, status, err, raw,
                      sc);
   e = hipGetLastError();
   if (e != hipSuccess) return e;

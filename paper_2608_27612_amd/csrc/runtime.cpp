@@ -20,6 +20,7 @@
 #include "emr_internal.h"
 #include "jit.h"
 #include "pack.h"
+#include "sched.h"
 
 // Launchers (kernels.hip).
 extern "C" hipError_t emr_launch_fill(void* p, int64_t n_words, uint32_t value, hipStream_t s);
@@ -37,6 +38,7 @@ extern "C" hipError_t emr_launch_chain(const emr::ChainArgs* A, int step, hipStr
 extern "C" hipError_t emr_launch_tile_geo(uint32_t* out, uint32_t tiles, uint32_t rows,
                                           hipStream_t s);
 extern "C" hipError_t emr_noalloc_scratch(void** out);
+extern "C" int emr_discover_per_cu(int mode);
 extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t blocks, int per_cu,
                                          int cus, emr::DiscoverScalars* out, uint32_t* grid);
 // The compiled tier's template code object (jit_image.cpp).
@@ -145,6 +147,19 @@ class WorkerPool {
   uint64_t gen_ = 0;
   bool stop_ = false;
 };
+
+// The current device's XCDs (each with its own L2), 1 when unknown.
+int device_xcd_count() {
+  static std::atomic<int> cached[64];
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 1;
+  if (dev >= 0 && dev < 64 && cached[dev].load(std::memory_order_relaxed) > 0)
+    return cached[dev].load(std::memory_order_relaxed);
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess || n <= 0)
+    n = 1;
+  if (dev >= 0 && dev < 64) cached[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
 
 int device_cu_count() {
   static std::atomic<int> cached[64];
@@ -321,6 +336,18 @@ struct Plan {
   // The bias rows of the plan's groups (the bind kernel's output: every position-independent
   // contribution per (genome, source)), computed on the device once, on first use (dev_mu).
   mutable float* d_bias = nullptr;
+  // Per group: cost-model slots of one query of one of its sources (the launch schedules' chunk
+  // costs).
+  std::vector<float> group_cost;
+  // The waves' chunk lists of the plan's launches (plan_schedule), one per launch shape, on the
+  // device (dev_mu).
+  struct Sched {
+    uint32_t grid, tiles, n_parts;
+    emr::DiscoverPart part[emr::kMaxParts];
+    uint32_t* d;
+    uint32_t stride;
+  };
+  mutable std::vector<Sched> scheds;
   Plan() = default;
   Plan(const Plan&) = delete;
   Plan& operator=(const Plan&) = delete;
@@ -328,6 +355,7 @@ struct Plan {
     jit.reset();  // drains the device before the compiled tier's module goes
     if (d_tables) (void)hipFree(d_tables);
     if (d_bias) (void)hipFree(d_bias);
+    for (const Sched& x : scheds) (void)hipFree(x.d);
   }
   // The compiled tier (jit_use): built at most once per plan, under jit_mu.
   mutable std::mutex jit_mu;
@@ -459,6 +487,7 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
       P.members.push_back({t.desc, t.src[s], (uint32_t)(bias + s), rows});
     bias += 4ull * rows;
     P.groups.push_back(t.g);
+    P.group_cost.push_back((float)cost[t.desc]);
   }
   if (bias > 0xFFFFFFFFull) return fail(EMR_E_LIMIT, "bias table too large");
   // Part order within the launch: the costliest bucket first (its chunks are handed out first).
@@ -591,6 +620,88 @@ emr_status plan_tables(const Plan& P, char** out) {
     P.d_tables = d;
   }
   *out = P.d_tables;
+  return EMR_OK;
+}
+
+// Chunk cost estimates for the schedule, in lane-slots: the queries' cost-model slots (one tile is
+// kTile / kWave positions per lane, for each source of the walk), plus per walk (positions, the
+// variance, records) and per chunk (the group's tables) overheads. A position-independent group
+// (a record-less walk) costs about one output row per query.
+constexpr double kSchedWalkSlots = 40.0, kSchedChunkSlots = 200.0, kSchedUniformQuery = 2.5;
+constexpr size_t kMaxScheds = 16;            // launch shapes a plan keeps lists for
+constexpr uint64_t kSchedMaxChunks = 1u << 22;
+constexpr uint64_t kSchedMaxBytes = 64u << 20;
+
+// The waves' chunk lists of a discover launch with scalars sc on `grid` workgroups, made and
+// uploaded on first use of that launch shape (the plan keeps them until it goes). *d is NULL when
+// the launch runs round-robin instead: no chunks, beyond the bounds above, or cost estimates the
+// scheduler refuses (not finite).
+emr_status plan_schedule(const Plan& P, const emr::DiscoverScalars& sc, uint32_t grid,
+                         const uint32_t** d, uint32_t* stride) {
+  *d = nullptr;
+  *stride = 0;
+  if (grid == 0 || sc.n_chunks == 0 || sc.n_chunks > kSchedMaxChunks) return EMR_OK;
+  std::lock_guard<std::mutex> lock(P.dev_mu);
+  for (const Plan::Sched& x : P.scheds)
+    if (x.grid == grid && x.tiles == sc.tiles && x.n_parts == sc.n_parts &&
+        std::memcmp(x.part, sc.part, sizeof(emr::DiscoverPart) * sc.n_parts) == 0) {
+      *d = x.d;
+      *stride = x.stride;
+      return EMR_OK;
+    }
+  if (P.scheds.size() >= kMaxScheds) return EMR_OK;
+  std::vector<float> cost;
+  std::vector<uint32_t> key;  // each chunk's group: a group's chunks share one XCD
+  cost.reserve(sc.n_chunks);
+  key.reserve(sc.n_chunks);
+  for (uint32_t k = 0; k < sc.n_parts; ++k) {
+    const emr::DiscoverPart& pt = sc.part[k];
+    const double tpw = (double)(emr::positions_per_lane((int)pt.S, (int)pt.W) / emr::kTileIters);
+    for (uint32_t cl = 0; cl < pt.n_chunks; ++cl) {
+      const uint64_t gi = (uint64_t)pt.group0 + cl / pt.chunks_per_group;
+      const uint32_t t0 = (cl % pt.chunks_per_group) * pt.chunk_tiles;
+      if (gi >= P.groups.size() || t0 >= sc.tiles) return EMR_OK;  // not this plan's launch
+      const double nt = (double)std::min(pt.chunk_tiles, sc.tiles - t0);
+      const double q = (P.groups[gi].flags & 1u) ? (double)P.group_cost[gi] : kSchedUniformQuery;
+      cost.push_back((float)(pt.S * q * nt * (emr::kTile / emr::kWave) +
+                             nt / tpw * kSchedWalkSlots + kSchedChunkSlots));
+      key.push_back((uint32_t)gi);
+    }
+  }
+  if (cost.size() != sc.n_chunks) return EMR_OK;
+  std::vector<uint32_t> table;
+  uint32_t st = 0;
+  // one list per workgroup (a CU); workgroups go to the XCDs round-robin (from a starting XCD
+  // that changes between launches), so workgroups b with equal b % xcds share an XCD
+  const uint32_t xcds = (uint32_t)device_xcd_count();
+  if (!emr::lpt_schedule(cost.data(), key.data(), (uint32_t)P.groups.size(), sc.n_chunks, grid,
+                         1u, grid >= xcds ? xcds : 1u, &table, &st) ||
+      table.size() * sizeof(uint32_t) > kSchedMaxBytes)
+    return EMR_OK;
+  uint32_t* dev = nullptr;
+  if (hipMalloc((void**)&dev, table.size() * sizeof(uint32_t)) != hipSuccess)
+    return fail(EMR_E_NOMEM, "chunk schedule of %zu bytes", table.size() * sizeof(uint32_t));
+  StreamPool* sp = nullptr;
+  emr_status rs = stream_pool(&sp);
+  if (rs == EMR_OK &&
+      (hipMemcpyAsync(dev, table.data(), table.size() * sizeof(uint32_t), hipMemcpyHostToDevice,
+                      sp->aux[0]) != hipSuccess ||
+       hipStreamSynchronize(sp->aux[0]) != hipSuccess))
+    rs = fail(EMR_E_DEVICE, "upload of the chunk schedule failed");
+  if (rs != EMR_OK) {
+    (void)hipFree(dev);
+    return rs;
+  }
+  Plan::Sched x{};
+  x.grid = grid;
+  x.tiles = sc.tiles;
+  x.n_parts = sc.n_parts;
+  std::memcpy(x.part, sc.part, sizeof(emr::DiscoverPart) * sc.n_parts);
+  x.d = dev;
+  x.stride = st;
+  P.scheds.push_back(x);
+  *d = dev;
+  *stride = st;
   return EMR_OK;
 }
 
@@ -890,7 +1001,9 @@ emr_status jit_build(const emr_population* pop, const Plan& P, std::unique_ptr<J
   for (int k = 0; k < 2; ++k) {
     HIP_OR_FAIL(hipModuleGetFunction(&M->fn[k], M->mod, names[k]));
     int n = 0;
-    if (hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&n, M->fn[k], 256, 0) == hipSuccess && n > 0)
+    if (hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&n, M->fn[k], emr::kDiscoverThreads, 0) ==
+            hipSuccess &&
+        n > 0)
       M->per_cu[k] = n;
   }
   M->code_bytes = (uint32_t)area;
@@ -975,7 +1088,8 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
     uint32_t* err = a.err;
     float* raw = a.raw;
     void* args[] = {&geo, &blob, &grp, &bias_tab, &status, &err, &raw, &sc};
-    HIP_OR_FAIL(hipModuleLaunchKernel(M.fn[mode], grid, 1, 1, 256, 1, 1, 0, s, args, nullptr));
+    HIP_OR_FAIL(hipModuleLaunchKernel(M.fn[mode], grid, 1, 1, emr::kDiscoverThreads, 1, 1, 0, s, args,
+                                      nullptr));
   }
   if (stop) HIP_OR_FAIL(hipEventRecord(stop, s));
   return EMR_OK;
@@ -991,13 +1105,16 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
 // before the discover launch, once every argument of that launch is ready on the host.
 // flags: the call's device flag words (error bits, largest count); flags_host: their pinned words
 // (device view) for k_finalize.
-// timing: the thread's launch profiling applies to this call (off for the allocation-free call,
-// whose events would be created on first use).
+// may_alloc: the call may allocate on first use: the thread's launch profiling (its events) and
+// the launch's chunk schedule apply (off for the allocation-free call, which runs its chunks
+// round-robin). A launch gets its waves' chunk lists once its plan runs again (a second call) or
+// runs in several ranges (a streamed call): placing the chunks of a plan used once would cost its
+// single call more than the balance saves.
 emr_status launch_range(const emr_population* pop, const Plan& P, const CallTables& T,
                         float theta, const emr_result* out, float* raw, void* workspace,
                         hipStream_t s, int64_t tile_lo, int64_t n_tiles, bool jit,
                         uint32_t* flags, uint32_t* flags_host, bool finalize, bool clear,
-                        bool timing = true) {
+                        bool may_alloc = true) {
   char* ws = (char*)workspace;
   const char* tables = T.tables;
   const uint32_t* geo_tab = T.geo;
@@ -1014,7 +1131,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
   float* pool_w4 = records ? (float*)(ws + pool_w4_offset(P, cap)) : nullptr;
   Profiler& prof = g_prof;
   const size_t rec0 = prof.recs.size();
-  const bool timed_call = timing && prof.on && prof.seen++ % prof.every == 0;
+  const bool timed_call = may_alloc && prof.on && prof.seen++ % prof.every == 0;
   const size_t n_timed = timed_call ? (prof.first_only ? 1 : P.launches.size()) : 0;
   while (prof.events.size() < 2 * (rec0 + n_timed)) {
     hipEvent_t e;
@@ -1058,6 +1175,22 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
     a.n_pairs = (uint32_t)P.n_pairs;
     a.bias_floats = P.bias_floats;
     const uint32_t blocks = (uint32_t)cus * 16;  // the launcher sizes the grid below this
+    if (may_alloc && (P.calls.load() >= 2 || n_tiles < P.tiles)) {
+      // the launch's grid and chunks, as its launcher will size them, for the waves' lists
+      emr::DiscoverScalars sc{};
+      uint32_t grid = 0;
+      const int per_cu = jit ? P.jit->per_cu[mode] : emr_discover_per_cu(mode);
+      HIP_OR_FAIL(emr_discover_setup(&a, blocks, per_cu, cus, &sc, &grid));
+      const uint32_t* sched = nullptr;
+      uint32_t stride = 0;
+      emr_status ss = plan_schedule(P, sc, grid, &sched, &stride);
+      if (ss != EMR_OK) return ss;
+      if (sched) {
+        a.sched = sched;
+        a.sched_stride = stride;
+        a.sched_lists = grid;
+      }
+    }
     const bool timed = li < n_timed;
     hipEvent_t e0 = timed ? prof.events[2 * (rec0 + li)] : nullptr;
     hipEvent_t e1 = timed ? prof.events[2 * (rec0 + li) + 1] : nullptr;
