@@ -442,13 +442,19 @@ __device__ __forceinline__ void discover_body(const uint32_t* __restrict__ geo_t
   const DiscoverPtrs d{(cu32*)geo_tab, (cu32*)blob, (cu32*)groups, (cf32*)bias_tab, status, err,
                        raw};
   const uint32_t n_wg = gridDim.x, wg = blockIdx.x;
-  // the workgroup's next share entry; one barrier before any wave takes one
-  __shared__ uint32_t next;
-  if (threadIdx.x == 0) next = 0u;
-  __syncthreads();
   // (the launcher accepts a schedule only when it was made for this grid: sched_lists == n_wg,
-  // so row wg and its sched_stride entries lie inside the table)
-  const bool listed = a.sched != nullptr;
+  // so row wg and its sched_stride entries lie inside the table; the interpreter, which runs the
+  // calls without lists, leaves the list path out)
+  const bool listed = JIT && a.sched != nullptr;
+  // The workgroup's next share entry, and its list (at most kListLds entries), copied to LDS (a
+  // wave then takes a chunk with two LDS accesses); one barrier before any wave takes one.
+  __shared__ uint32_t next;
+  __shared__ uint32_t list[kListLds];
+  if (threadIdx.x == 0) next = 0u;
+  if (listed)
+    for (uint32_t i = threadIdx.x; i < a.sched_stride; i += blockDim.x)
+      list[i] = a.sched[wg * a.sched_stride + i];
+  __syncthreads();
   for (;;) {
     // The wave's share entry: every lane adds to `next`, lane 0 one and the others zero, so lane
     // 0 reads the entry it took. (One asm statement: as a lane-0 branch around an atomicAdd the
@@ -465,26 +471,30 @@ __device__ __forceinline__ void discover_body(const uint32_t* __restrict__ geo_t
         : "s"((uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)&next)
         : "vcc", "memory");
     e = __builtin_amdgcn_readfirstlane(e);
-    uint32_t c;
+    // the chunk, as a list entry: its part << kEntryPartShift | its index in the part
+    uint32_t entry;
     if (listed) {
       if (e >= a.sched_stride) break;
-      c = __builtin_amdgcn_readfirstlane(a.sched[wg * a.sched_stride + e]);
-      if (c == kNoChunk) break;
-      if (c >= a.n_chunks) {
-        if (lane == 0) atomicOr(err, kErrTable);
-        break;
-      }
+      entry = __builtin_amdgcn_readfirstlane(list[e]);
+      if (entry == kNoChunk) break;
     } else {
       // (each wave takes one entry past the share's end at most, so c < n_chunks + 13 n_wg,
       // which does not wrap with n_chunks < 2^31)
-      c = wg + e * n_wg;
+      uint32_t c = wg + e * n_wg;
       if (c >= a.n_chunks) break;
+      uint32_t p = 0;
+      while (p + 1 < a.n_parts && c >= a.part[p].n_chunks) {
+        c -= a.part[p].n_chunks;
+        ++p;
+      }
+      entry = p << kEntryPartShift | c;  // (setup bounds an unlisted part below 2^24 chunks)
     }
-    // the chunk's part, and its index within the part
-    uint32_t k = 0, cl = c;
-    while (k + 1 < a.n_parts && cl >= a.part[k].n_chunks) {
-      cl -= a.part[k].n_chunks;
-      ++k;
+    // (the launcher checked every listed entry's index against its part when it made the lists;
+    // a round-robin entry's index is inside its part by the scan)
+    const uint32_t k = entry >> kEntryPartShift, cl = entry & ((1u << kEntryPartShift) - 1u);
+    if (k >= a.n_parts) {
+      if (lane == 0) atomicOr(err, kErrTable);
+      break;
     }
     const DiscoverPart pt = a.part[k];
     switch (pt.W * 4u + pt.S) {

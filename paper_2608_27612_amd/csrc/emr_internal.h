@@ -25,7 +25,10 @@ constexpr int kWindows[] = {4, 8, 16, 32};
 constexpr int kMaxWindow = 32;
 // Sources evaluated together by one lane (same genome, same direction).
 constexpr int kMaxGroup = 4;
-constexpr int kMaxParts = 9;  // (sources per walk, register window) variants of a launch
+// Parts of a launch: one per (sources per walk, register window) variant present (9 at most),
+// each split at most 5 ways by chunk size (16 .. 1 tiles) when the launch has a schedule.
+constexpr int kMaxBuckets = 9;
+constexpr int kMaxParts = 5 * kMaxBuckets;
 // Register budget of the value windows: S sources x P positions x W slots <= 128 VGPRs per lane.
 constexpr int kWindowRegs = 128;
 // Positions per wave iteration and iterations per tile.
@@ -156,8 +159,8 @@ EMR_HD inline int64_t tile_parent_offset(int64_t T, int depth) {
 
 
 // ---------------------------------------------------------------- discover launch scalars
-// One launch covers every group of a call, in up to kMaxParts parts: the groups with S sources
-// per walk and register window W, one part per (S, W) present (costliest part first). The
+// One launch covers every group of a call, in up to kMaxParts parts: runs of groups with S
+// sources per walk and register window W, each with one chunk size (costliest part first). The
 // launch's chunks are those of its parts, one after the other.
 struct DiscoverPart {
   uint32_t S, W, group0;                     // sources per walk, window; the part's first group
@@ -185,14 +188,17 @@ struct DiscoverScalars {
   uint32_t* pool_parent;
   float* pool_w4;
   uint32_t* pair_total;
-  // The workgroups' chunk lists, or NULL for round-robin chunks (chunk c to workgroup c mod
-  // workgroups): workgroup b's waves take chunks sched[b * sched_stride + j], j = 0, 1, ..., up to
-  // the first kNoChunk. The lists were made for exactly sched_lists workgroups (the launch's grid);
-  // sched_stride is a multiple of 64.
+  // The workgroups' chunk lists, or NULL for round-robin chunks (chunk c of the launch to
+  // workgroup c mod workgroups): workgroup b's waves take the entries sched[b * sched_stride + j],
+  // j = 0, 1, ..., up to the first kNoChunk, each naming a chunk as its part << kEntryPartShift |
+  // its index in the part. The lists were made for exactly sched_lists workgroups (the launch's
+  // grid); sched_stride is a multiple of 64, at most kListLds.
   const uint32_t* sched;
   uint32_t sched_stride, sched_lists;
 };
 constexpr uint32_t kNoChunk = 0xFFFFFFFFu;
+constexpr uint32_t kEntryPartShift = 24;  // a listed part holds fewer than 2^24 chunks
+static_assert(kMaxParts < (1 << (32 - kEntryPartShift)) - 1, "part ids of list entries");
 
 // A discover workgroup fills one CU: 3 waves on each of its 4 SIMDs (the kernels' register budget
 // allows 3), taking their workgroup's chunks one at a time from a counter in LDS. A SIMD issues
@@ -200,6 +206,7 @@ constexpr uint32_t kNoChunk = 0xFFFFFFFFu;
 // as they free up keeps every wave busy until the CU's share runs out.
 constexpr int kDiscoverWaves = 12;
 constexpr int kDiscoverThreads = kDiscoverWaves * kWave;
+constexpr uint32_t kListLds = 2048;  // the longest list: a discover workgroup holds it in LDS
 
 // Output modes: raw CPPN outputs; records of kept cells, each walk's reserved in a pool with one
 // atomic, each tile's pool offset and count left in its status word and each chunk's count added
@@ -286,6 +293,9 @@ struct DiscoverArgs {
   // per walk and register window part_W[k], in launch order.
   uint32_t n_parts;
   uint32_t part_S[kMaxParts], part_W[kMaxParts], part_group0[kMaxParts], part_groups[kMaxParts];
+  // the part's chunk size in tiles: a power of two from one walk's tiles to kChunkTilesMax, or 0
+  // for the launcher's rule
+  uint32_t part_chunk[kMaxParts];
   uint32_t tile_lo;        // first tile of the launch (of every pair)
   uint32_t tiles;          // tiles of the launch per pair
   int32_t depth;

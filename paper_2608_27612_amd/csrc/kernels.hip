@@ -518,8 +518,16 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   for (uint32_t k = 0; k < a->n_parts; ++k) {
     const int S = (int)a->part_S[k], W = (int)a->part_W[k];
     const uint32_t tpw = (uint32_t)emr::positions_per_lane(S, W) / emr::kTileIters;
-    const uint32_t chunk = target > tpw ? target : tpw;  // at most kChunkTilesMax (tpw <= 4)
+    uint32_t chunk = target > tpw ? target : tpw;  // at most kChunkTilesMax (tpw <= 4)
+    if (a->part_chunk[k] != 0u) {
+      chunk = a->part_chunk[k];
+      if (chunk < tpw || chunk > emr::kChunkTilesMax || (chunk & (chunk - 1u)) != 0u)
+        return hipErrorInvalidValue;
+    }
     const uint32_t cpg = (a->tiles + chunk - 1) / chunk;
+    // (a part's chunk index fits a list entry's index field)
+    if ((uint64_t)a->part_groups[k] * cpg >= (1ull << emr::kEntryPartShift))
+      return hipErrorInvalidValue;
     sc.part[k] = emr::DiscoverPart{(uint32_t)S, (uint32_t)W, a->part_group0[k],
                                    a->part_groups[k] * cpg, cpg, chunk};
     chunks += (uint64_t)a->part_groups[k] * cpg;
@@ -547,9 +555,11 @@ extern "C" hipError_t emr_discover_setup(const emr::DiscoverArgs* a, uint32_t bl
   const uint32_t resident = (uint32_t)per_cu * (uint32_t)cus;
   if (blocks > chunks) blocks = (uint32_t)chunks;
   if (blocks > resident) blocks = resident;
-  // A schedule is made for one grid: it must be this launch's.
+  // A schedule is made for one grid: it must be this launch's. (Only the compiled tier's
+  // kernels read it; the interpreter's launcher refuses one.)
   if (a->sched != nullptr) {
-    if (a->sched_lists != blocks || a->sched_stride == 0u || a->sched_stride % emr::kWave != 0u)
+    if (a->sched_lists != blocks || a->sched_stride == 0u || a->sched_stride % emr::kWave != 0u ||
+        a->sched_stride > emr::kListLds)
       return hipErrorInvalidValue;
     sc.sched = a->sched;
     sc.sched_stride = a->sched_stride;
@@ -579,6 +589,7 @@ template <int MODE>
 static hipError_t launch_discover_t(const emr::DiscoverArgs* a, uint32_t blocks, hipStream_t s,
                                     hipEvent_t start, hipEvent_t stop) {
   auto kern = emr::k_discover<MODE>;
+  if (a->sched != nullptr) return hipErrorInvalidValue;  // the interpreter runs round-robin
   int dev = 0, cus = 0;
   hipError_t e;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;

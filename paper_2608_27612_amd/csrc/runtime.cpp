@@ -312,7 +312,7 @@ struct Plan {
   // costliest first.
   struct Launch {
     int n_parts;
-    int part[emr::kMaxParts];  // bucket indices
+    int part[emr::kMaxBuckets];  // bucket indices
     double cost;
     // per position of the range, over all the launch's queries: cost-model slots without
     // transcendentals, transcendental instructions, and queries (sources)
@@ -494,7 +494,7 @@ emr_status build_plan(const emr_population* pop, const emr_source* sources, int3
   std::stable_sort(P.buckets.begin(), P.buckets.end(),
                    [](const Plan::Bucket& a, const Plan::Bucket& b) { return a.cost > b.cost; });
   // One launch with every bucket as a part, in cost order.
-  if ((int)P.buckets.size() > emr::kMaxParts) return fail(EMR_E_LIMIT, "too many buckets");
+  if ((int)P.buckets.size() > emr::kMaxBuckets) return fail(EMR_E_LIMIT, "too many buckets");
   if (!P.buckets.empty()) {
     Plan::Launch L{};
     for (size_t bi = 0; bi < P.buckets.size(); ++bi) {
@@ -628,6 +628,15 @@ emr_status plan_tables(const Plan& P, char** out) {
 // variance, records) and per chunk (the group's tables) overheads. A position-independent group
 // (a record-less walk) costs about one output row per query.
 constexpr double kSchedWalkSlots = 40.0, kSchedChunkSlots = 200.0, kSchedUniformQuery = 2.5;
+// A scheduled launch's chunks are sized so that none costs more than this share of a wave's mean
+// load: the costliest chunks, taken first, end well before the launch does.
+constexpr double kChunkCostShare = 0.5;
+
+// Estimated cost of a chunk of nt tiles of group gi (sources per walk S, tiles per walk tpw).
+double chunk_cost(const Plan& P, uint64_t gi, uint32_t S, double tpw, double nt) {
+  const double q = (P.groups[gi].flags & 1u) ? (double)P.group_cost[gi] : kSchedUniformQuery;
+  return S * q * nt * (emr::kTile / emr::kWave) + nt / tpw * kSchedWalkSlots + kSchedChunkSlots;
+}
 constexpr size_t kMaxScheds = 16;            // launch shapes a plan keeps lists for
 constexpr uint64_t kSchedMaxChunks = 1u << 22;
 constexpr uint64_t kSchedMaxBytes = 64u << 20;
@@ -651,21 +660,23 @@ emr_status plan_schedule(const Plan& P, const emr::DiscoverScalars& sc, uint32_t
     }
   if (P.scheds.size() >= kMaxScheds) return EMR_OK;
   std::vector<float> cost;
-  std::vector<uint32_t> key;  // each chunk's group: a group's chunks share one XCD
+  std::vector<uint32_t> key;    // each chunk's group: a group's chunks share one XCD
+  std::vector<uint32_t> entry;  // each chunk's list entry: part << kEntryPartShift | index
   cost.reserve(sc.n_chunks);
   key.reserve(sc.n_chunks);
+  entry.reserve(sc.n_chunks);
   for (uint32_t k = 0; k < sc.n_parts; ++k) {
     const emr::DiscoverPart& pt = sc.part[k];
+    if (pt.n_chunks >= (1u << emr::kEntryPartShift)) return EMR_OK;
     const double tpw = (double)(emr::positions_per_lane((int)pt.S, (int)pt.W) / emr::kTileIters);
     for (uint32_t cl = 0; cl < pt.n_chunks; ++cl) {
       const uint64_t gi = (uint64_t)pt.group0 + cl / pt.chunks_per_group;
       const uint32_t t0 = (cl % pt.chunks_per_group) * pt.chunk_tiles;
       if (gi >= P.groups.size() || t0 >= sc.tiles) return EMR_OK;  // not this plan's launch
       const double nt = (double)std::min(pt.chunk_tiles, sc.tiles - t0);
-      const double q = (P.groups[gi].flags & 1u) ? (double)P.group_cost[gi] : kSchedUniformQuery;
-      cost.push_back((float)(pt.S * q * nt * (emr::kTile / emr::kWave) +
-                             nt / tpw * kSchedWalkSlots + kSchedChunkSlots));
+      cost.push_back((float)chunk_cost(P, gi, pt.S, tpw, nt));
       key.push_back((uint32_t)gi);
+      entry.push_back(k << emr::kEntryPartShift | cl);
     }
   }
   if (cost.size() != sc.n_chunks) return EMR_OK;
@@ -676,8 +687,17 @@ emr_status plan_schedule(const Plan& P, const emr::DiscoverScalars& sc, uint32_t
   const uint32_t xcds = (uint32_t)device_xcd_count();
   if (!emr::lpt_schedule(cost.data(), key.data(), (uint32_t)P.groups.size(), sc.n_chunks, grid,
                          1u, grid >= xcds ? xcds : 1u, &table, &st) ||
-      table.size() * sizeof(uint32_t) > kSchedMaxBytes)
+      st > emr::kListLds || table.size() * sizeof(uint32_t) > kSchedMaxBytes)
     return EMR_OK;
+  // every entry names a part of the launch and a chunk inside it (the kernel relies on it)
+  for (uint32_t& t : table) {
+    if (t == emr::kNoChunk) continue;
+    if (t >= entry.size()) return fail(EMR_E_LIMIT, "chunk schedule: bad chunk %u", t);
+    t = entry[t];
+    const uint32_t k = t >> emr::kEntryPartShift, cl = t & ((1u << emr::kEntryPartShift) - 1u);
+    if (k >= sc.n_parts || cl >= sc.part[k].n_chunks)
+      return fail(EMR_E_LIMIT, "chunk schedule: entry %u outside its part", t);
+  }
   uint32_t* dev = nullptr;
   if (hipMalloc((void**)&dev, table.size() * sizeof(uint32_t)) != hipSuccess)
     return fail(EMR_E_NOMEM, "chunk schedule of %zu bytes", table.size() * sizeof(uint32_t));
@@ -1095,6 +1115,51 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
   return EMR_OK;
 }
 
+// The parts of a scheduled launch: each bucket of L (its groups in decreasing cost) split into
+// runs of groups that share a chunk size, the largest power of two of at most kChunkTilesMax
+// tiles (and at least one walk's) whose chunk costs no more than kChunkCostShare of a wave's mean
+// load over `waves` waves. False (a is left for the caller) when the launch has no groups.
+bool split_parts(const Plan& P, const Plan::Launch& L, bool skip_uniform, int64_t n_tiles,
+                 double waves, emr::DiscoverArgs* a) {
+  double total = 0.0;  // the launch's queries and walks (per-chunk costs aside)
+  for (int k = 0; k < L.n_parts; ++k) {
+    const Plan::Bucket& bk = P.buckets[(size_t)L.part[k]];
+    const uint32_t n = skip_uniform ? bk.varying : bk.count;
+    const double tpw = (double)(emr::positions_per_lane(bk.S, bk.window) / emr::kTileIters);
+    for (uint32_t g = 0; g < n; ++g)
+      total += chunk_cost(P, bk.first + g, (uint32_t)bk.S, tpw, (double)n_tiles) - kSchedChunkSlots;
+  }
+  if (total <= 0.0 || waves <= 0.0) return false;
+  const double limit = kChunkCostShare * total / waves;
+  uint32_t np = 0;
+  for (int k = 0; k < L.n_parts; ++k) {
+    const Plan::Bucket& bk = P.buckets[(size_t)L.part[k]];
+    const uint32_t n = skip_uniform ? bk.varying : bk.count;
+    const uint32_t tpw = (uint32_t)emr::positions_per_lane(bk.S, bk.window) / emr::kTileIters;
+    auto size_of = [&](uint32_t g) {
+      for (uint32_t t = emr::kChunkTilesMax; t > tpw; t /= 2)
+        if (chunk_cost(P, bk.first + g, (uint32_t)bk.S, (double)tpw, (double)t) <= limit) return t;
+      return tpw;
+    };
+    for (uint32_t g = 0; g < n;) {
+      const uint32_t t = size_of(g);
+      uint32_t h = g + 1;
+      while (h < n && size_of(h) == t) ++h;
+      if (np == (uint32_t)emr::kMaxParts) return false;
+      a->part_S[np] = (uint32_t)bk.S;
+      a->part_W[np] = (uint32_t)bk.window;
+      a->part_group0[np] = bk.first + g;
+      a->part_groups[np] = h - g;
+      a->part_chunk[np] = t;
+      ++np;
+      g = h;
+    }
+  }
+  if (np == 0) return false;
+  a->n_parts = np;
+  return true;
+}
+
 // Enqueues the discover launch (every bucket, on the caller's stream) for tiles
 // tile_lo .. tile_lo + n_tiles - 1 of every pair, then, for records, the compaction: the range's
 // records go to `out` pair after pair (pair_offset, pair_count), its capacity also bounding the
@@ -1107,9 +1172,10 @@ emr_status jit_launch(const Plan& P, const emr::DiscoverArgs& a, int mode, uint3
 // (device view) for k_finalize.
 // may_alloc: the call may allocate on first use: the thread's launch profiling (its events) and
 // the launch's chunk schedule apply (off for the allocation-free call, which runs its chunks
-// round-robin). A launch gets its waves' chunk lists once its plan runs again (a second call) or
-// runs in several ranges (a streamed call): placing the chunks of a plan used once would cost its
-// single call more than the balance saves.
+// round-robin). A compiled-tier launch gets its workgroups' chunk lists once its plan runs again
+// (a second call) or runs in several ranges (a streamed call): placing the chunks of a plan used
+// once would cost its single call more than the balance saves. Interpreted launches run
+// round-robin.
 emr_status launch_range(const emr_population* pop, const Plan& P, const CallTables& T,
                         float theta, const emr_result* out, float* raw, void* workspace,
                         hipStream_t s, int64_t tile_lo, int64_t n_tiles, bool jit,
@@ -1159,13 +1225,19 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
     a.raw = raw;
     a.cap = cap;
     a.n_pos = emr::n_positions(P.depth);
-    a.n_parts = (uint32_t)L.n_parts;
-    for (int k = 0; k < L.n_parts; ++k) {
-      const Plan::Bucket& bk = P.buckets[(size_t)L.part[k]];
-      a.part_S[k] = (uint32_t)bk.S;
-      a.part_W[k] = (uint32_t)bk.window;
-      a.part_group0[k] = bk.first;
-      a.part_groups[k] = skip_uniform ? bk.varying : bk.count;
+    const bool scheduled = may_alloc && jit && (P.calls.load() >= 2 || n_tiles < P.tiles);
+    const int per_cu = jit ? P.jit->per_cu[mode] : emr_discover_per_cu(mode);
+    if (!scheduled || !split_parts(P, L, skip_uniform, n_tiles,
+                                   (double)emr::kDiscoverWaves * per_cu * cus, &a)) {
+      a.n_parts = (uint32_t)L.n_parts;
+      for (int k = 0; k < L.n_parts; ++k) {
+        const Plan::Bucket& bk = P.buckets[(size_t)L.part[k]];
+        a.part_S[k] = (uint32_t)bk.S;
+        a.part_W[k] = (uint32_t)bk.window;
+        a.part_group0[k] = bk.first;
+        a.part_groups[k] = skip_uniform ? bk.varying : bk.count;
+        a.part_chunk[k] = 0;  // the launcher's rule
+      }
     }
     a.tile_lo = (uint32_t)tile_lo;
     a.tiles = (uint32_t)n_tiles;
@@ -1175,11 +1247,10 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
     a.n_pairs = (uint32_t)P.n_pairs;
     a.bias_floats = P.bias_floats;
     const uint32_t blocks = (uint32_t)cus * 16;  // the launcher sizes the grid below this
-    if (may_alloc && (P.calls.load() >= 2 || n_tiles < P.tiles)) {
-      // the launch's grid and chunks, as its launcher will size them, for the waves' lists
+    if (scheduled) {
+      // the launch's grid and chunks, as its launcher will size them, for the workgroups' lists
       emr::DiscoverScalars sc{};
       uint32_t grid = 0;
-      const int per_cu = jit ? P.jit->per_cu[mode] : emr_discover_per_cu(mode);
       HIP_OR_FAIL(emr_discover_setup(&a, blocks, per_cu, cus, &sc, &grid));
       const uint32_t* sched = nullptr;
       uint32_t stride = 0;
