@@ -420,6 +420,9 @@ typedef struct {
   double slots;
   float ms;
   int32_t compiled; /* 1: the launch ran compiled programs, 0: the interpreter */
+  int32_t listed;   /* 1: its workgroups took their chunks from the plan's balanced lists (a
+                       compiled plan's later calls), 0: from round-robin shares */
+  int32_t parts;    /* runs of groups with one chunk size the launch was split into */
 } emr_launch_profile;
 
 /* Sets per-launch event timing for the calling thread's later calls and drops the records held:

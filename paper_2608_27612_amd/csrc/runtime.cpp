@@ -1285,6 +1285,8 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
       r.slots = npos * (L.slots_base + prof.rT * L.slots_trans);
       r.queries = (int64_t)(npos * L.sources);
       r.compiled = jit ? 1 : 0;
+      r.listed = a.sched != nullptr ? 1 : 0;
+      r.parts = (int32_t)a.n_parts;
       prof.recs.push_back(r);
     }
   }

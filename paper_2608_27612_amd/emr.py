@@ -72,7 +72,8 @@ class emr_connections(C.Structure):
 class emr_launch_profile(C.Structure):
     _fields_ = [("group_size", C.c_int32), ("window", C.c_int32), ("positions", C.c_int32),
                 ("call", C.c_int32), ("tiles", C.c_int64), ("queries", C.c_int64),
-                ("slots", C.c_double), ("ms", C.c_float), ("compiled", C.c_int32)]
+                ("slots", C.c_double), ("ms", C.c_float), ("compiled", C.c_int32),
+                ("listed", C.c_int32), ("parts", C.c_int32)]
 
 
 _lib = None
@@ -452,7 +453,7 @@ def emr_profile_read():
     for i, r in enumerate(arr[:n.value]):
         out.append({"S": r.group_size, "W": r.window, "P": r.positions, "call": r.call,
                     "tiles": r.tiles, "queries": r.queries, "slots": r.slots, "ms": r.ms,
-                    "compiled": bool(r.compiled),
+                    "compiled": bool(r.compiled), "listed": bool(r.listed), "parts": r.parts,
                     "first": i == 0 or arr[i - 1].call != r.call})
     return out
 

@@ -44,14 +44,25 @@ def pair_genome_source(r, genomes, sources, offs):
     return genomes[g], sources[r]
 
 
-def check_discover(emr, genomes, sources, D, theta, offs=None, capacity=None, pop=None):
-    """Runs the GPU path and the oracle; asserts parity; returns summary stats."""
+def check_discover(emr, genomes, sources, D, theta, offs=None, capacity=None, pop=None, calls=1):
+    """Runs the GPU path and the oracle; asserts parity; returns summary stats. With calls > 1 the
+    same plan runs that many times (a compiled plan's later calls take their chunks from balanced
+    lists): every call's result must equal the first bit for bit, and the last is checked."""
     theta32 = float(np.float32(theta))
     if pop is None:
         pop = emr.emr_pack_population(genomes)
-    res = emr.emr_discover(pop, sources, D, theta32, src_offsets=offs, capacity=capacity)
-    total, mx = emr.emr_result_check(res)
-    counts, recs = emr.records_to_host(res)
+    first = None
+    for _ in range(calls):
+        res = emr.emr_discover(pop, sources, D, theta32, src_offsets=offs, capacity=capacity)
+        total, mx = emr.emr_result_check(res)
+        counts, recs = emr.records_to_host(res)
+        if first is None:
+            first = (total, mx, counts, recs)
+            continue
+        assert (total, mx) == first[:2] and np.array_equal(counts, first[2])
+        for (ga, wa), (gb, wb) in zip(recs, first[3]):
+            np.testing.assert_array_equal(ga, gb)
+            np.testing.assert_array_equal(wa.view(np.uint32), wb.view(np.uint32))
     offsets = res["pair_offset"].cpu().numpy()
     assert offsets[0] == 0 and np.array_equal(np.diff(offsets), counts) and offsets[-1] == total
     o = oracle.discover(genomes, sources, D, theta32, src_offsets=offs)
@@ -348,13 +359,18 @@ def test_full_size_xor_pop1000_depth7_all_pairs(emr, policy):
     the compiled tier (what the timed steps run) and under the interpreter, every pair and every
     record against the oracle."""
     emr.emr_set_jit(emr.EMR_JIT_ALWAYS if policy == "always" else emr.EMR_JIT_OFF)
+    emr.emr_profile_enable(True)
     try:
         genomes, sources, D, theta = W.workload("xor_pop1000_d7")
         pop = emr.emr_pack_population(genomes)
-        st = check_discover(emr, genomes, sources, D, theta, pop=pop)
+        st = check_discover(emr, genomes, sources, D, theta, pop=pop, calls=2)
         assert st["records"] > 0
         assert emr.emr_jit_info(pop)["state"] == (1 if policy == "always" else 0)
+        launches = emr.emr_profile_read()
+        assert [r["listed"] for r in launches] == ([False, True] if policy == "always" else
+                                                    [False, False])
     finally:
+        emr.emr_profile_enable(False)
         emr.emr_set_jit(emr.EMR_JIT_AUTO)
 
 
@@ -365,7 +381,7 @@ def test_full_size_depth8_compiled(emr):
     try:
         genomes = W.population(0, 200, 20, 60)
         pop = emr.emr_pack_population(genomes)
-        st = check_discover(emr, genomes, W.xor_sources(), 8, 0.03, pop=pop)
+        st = check_discover(emr, genomes, W.xor_sources(), 8, 0.03, pop=pop, calls=2)
         assert st["records"] > 0
         assert emr.emr_jit_info(pop)["state"] == 1
     finally:
