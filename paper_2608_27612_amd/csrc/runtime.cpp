@@ -348,6 +348,18 @@ struct Plan {
     uint32_t stride;
   };
   mutable std::vector<Sched> scheds;
+  // Split parts of the plan's scheduled launches (cached_split_parts), one per launch shape.
+  struct Split {
+    bool skip_uniform;
+    int64_t n_tiles;
+    double waves;
+    bool ok;
+    uint32_t n_parts;
+    uint32_t S[emr::kMaxParts], W[emr::kMaxParts], group0[emr::kMaxParts],
+        groups[emr::kMaxParts], chunk[emr::kMaxParts];
+  };
+  mutable std::mutex split_mu;
+  mutable std::vector<Split> splits;
   Plan() = default;
   Plan(const Plan&) = delete;
   Plan& operator=(const Plan&) = delete;
@@ -1160,6 +1172,45 @@ bool split_parts(const Plan& P, const Plan::Launch& L, bool skip_uniform, int64_
   return true;
 }
 
+// split_parts, remembered per launch shape (a plan's repeated calls split the same way).
+constexpr size_t kMaxSplits = 8;
+bool cached_split_parts(const Plan& P, const Plan::Launch& L, bool skip_uniform, int64_t n_tiles,
+                        double waves, emr::DiscoverArgs* a) {
+  std::lock_guard<std::mutex> lock(P.split_mu);
+  const Plan::Split* hit = nullptr;
+  for (const Plan::Split& x : P.splits)
+    if (x.skip_uniform == skip_uniform && x.n_tiles == n_tiles && x.waves == waves) hit = &x;
+  if (!hit) {
+    Plan::Split x{};
+    x.skip_uniform = skip_uniform;
+    x.n_tiles = n_tiles;
+    x.waves = waves;
+    emr::DiscoverArgs t{};
+    x.ok = split_parts(P, L, skip_uniform, n_tiles, waves, &t);
+    x.n_parts = x.ok ? t.n_parts : 0u;
+    for (uint32_t k = 0; k < x.n_parts; ++k) {
+      x.S[k] = t.part_S[k];
+      x.W[k] = t.part_W[k];
+      x.group0[k] = t.part_group0[k];
+      x.groups[k] = t.part_groups[k];
+      x.chunk[k] = t.part_chunk[k];
+    }
+    if (P.splits.size() >= kMaxSplits) P.splits.erase(P.splits.begin());
+    P.splits.push_back(x);
+    hit = &P.splits.back();
+  }
+  if (!hit->ok) return false;
+  a->n_parts = hit->n_parts;
+  for (uint32_t k = 0; k < hit->n_parts; ++k) {
+    a->part_S[k] = hit->S[k];
+    a->part_W[k] = hit->W[k];
+    a->part_group0[k] = hit->group0[k];
+    a->part_groups[k] = hit->groups[k];
+    a->part_chunk[k] = hit->chunk[k];
+  }
+  return true;
+}
+
 // Enqueues the discover launch (every bucket, on the caller's stream) for tiles
 // tile_lo .. tile_lo + n_tiles - 1 of every pair, then, for records, the compaction: the range's
 // records go to `out` pair after pair (pair_offset, pair_count), its capacity also bounding the
@@ -1227,8 +1278,8 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
     a.n_pos = emr::n_positions(P.depth);
     const bool scheduled = may_alloc && jit && (P.calls.load() >= 2 || n_tiles < P.tiles);
     const int per_cu = jit ? P.jit->per_cu[mode] : emr_discover_per_cu(mode);
-    if (!scheduled || !split_parts(P, L, skip_uniform, n_tiles,
-                                   (double)emr::kDiscoverWaves * per_cu * cus, &a)) {
+    if (!scheduled || !cached_split_parts(P, L, skip_uniform, n_tiles,
+                                          (double)emr::kDiscoverWaves * per_cu * cus, &a)) {
       a.n_parts = (uint32_t)L.n_parts;
       for (int k = 0; k < L.n_parts; ++k) {
         const Plan::Bucket& bk = P.buckets[(size_t)L.part[k]];
