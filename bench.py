@@ -1,18 +1,23 @@
 #!/usr/bin/env python3
 """Benchmark of eager multi-resolution substrate discovery on one MI355X.
 
-One step = one emr_discover call over the whole workload (bind the sources, query every
-(genome, source, position), variance filter, ordered compaction) plus emr_result_check (the
-synchronizing count check). The packed population is resident in HBM before timing starts.
-Printed as one JSON line:
+One step = one emr_discover call over the whole workload (the sources' bias rows are the plan's,
+every (genome, source, position) is queried, the variance filter is applied and the kept cells are
+compacted per pair) plus emr_result_check (the synchronizing count check). The packed population
+is resident in HBM before timing starts. Printed as one JSON line:
 
   value        CPPN queries per second over the timed steps (host clock, synchronized)
+  evaluated_queries_per_s  the same for the queries of position-dependent pairs only (a pair
+               whose CPPN output does not depend on the position is answered by its per-source
+               constant, exactly, without a per-position evaluation)
   roofline     the discover kernel (one launch per step, every query of the step):
                algorithmic VALU lane-slots (cost model of emr_discover_cost: one slot per fp32
                FMA / add / mul, transcendentals weighted by their measured 1/4 rate) / its
                HIP-event duration (an event pair around the launch in every 4th timed step), against
                the chip's fp32 vector peak: 157.3 TFLOP/s = 78.64 T lane-slots/s (an FMA is one
-               slot, two flops)
+               slot, two flops); flops / frac_flops: the useful floating-point operations (2 per
+               multiply-add, 1 per other operation) over the same duration, against 157.3 TFLOP/s;
+               hbm_write_gbps: the kept records' 20 bytes each over the same duration
   valu_frac_step  the same algorithmic slots for the whole step over ms_per_step, against the
                same peak (every kernel, launch gap and host interaction of a step included)
   ms_per_gen   pack (host + upload) + discover + check, host clock: the per-generation cost of
@@ -23,7 +28,11 @@ Printed as one JSON line:
   compiled_tier  the timed steps' compiled programs (the default policy compiles a population's
                programs on its second call, so the warm-up compiles them): count, machine-code
                bytes, host compile and module-load times
-  cpu_baseline the CPU oracle on a bounded, stated sample of the same workload
+  sub          the other measured workloads, each with the same per-step figures: the population
+               at depth 8, the tabular population (33 sources, depth 6) and the single deep CPPN
+               streamed at depth 13 (emr_discover_stream, one step = one streamed call)
+  cpu_baseline the CPU oracle on a bounded, stated sample of the same workload, the host CPU, the
+               oracle's one-thread rates on three small workloads, and a sample of every sub workload
 """
 
 from __future__ import annotations
@@ -41,6 +50,8 @@ sys.path.insert(0, ROOT)
 
 TIME_EVERY = 4  # steps per timed discover launch
 VALU_PEAK_SLOTS = 157.3e12 / 2.0  # lane-slots per second (fp32 vector peak, FMA = 2 flops)
+FLOP_PEAK = 157.3e12
+RECORD_BYTES = 20  # a kept cell: parent index (4 bytes) + its four children's outputs (16 bytes)
 METRIC = "CPPN queries/sec incl. variance filter (% VALU peak); ms/gen pop1000 depth7"
 
 
@@ -77,10 +88,120 @@ def profiled_traffic(kernel, workload):
     return None
 
 
-def cpu_baseline(genomes, sources, depth, theta32, target_s):
-    """The oracle, as it stands, on the first n genomes (all sources) sized to ~target_s."""
-    import oracle
-    n = min(4, len(genomes))
+def roofline(work, kernel_ms_per_step, records, kernel, workload):
+    """The discover kernel's roofline entry for a step of `work` taking kernel_ms_per_step."""
+    t = kernel_ms_per_step * 1e-3
+    achieved = work["slots"] / t
+    flops = work["flops"] / t
+    return {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_SLOTS / 1e12,
+            "unit": "TOP/s", "frac": achieved / VALU_PEAK_SLOTS,
+            "flops": flops / 1e12, "frac_flops": flops / FLOP_PEAK,
+            "hbm_write_gbps": RECORD_BYTES * records / t / 1e9,
+            "traffic": profiled_traffic(kernel, workload), "kernel": kernel,
+            "kernel_ms": kernel_ms_per_step}
+
+
+def timed_steps(emr, torch, step, steps, warmup, rT):
+    """Runs `step` warmup + steps times; the timed steps time their discover launches with a HIP
+    event pair in every TIME_EVERY-th step (the first, then every TIME_EVERY-th). Returns
+    (ms per step on the host clock, the launches' summed ms per timed step, launch records)."""
+    for _ in range(warmup):
+        step()
+    emr.emr_profile_enable(True, rT, every=TIME_EVERY)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    recs = emr.emr_profile_read()
+    emr.emr_profile_enable(False)
+    per_call = {}
+    for r in recs:
+        per_call[r["call"]] = per_call.get(r["call"], 0.0) + r["ms"]
+    assert len(per_call) == (steps + TIME_EVERY - 1) // TIME_EVERY
+    return (t1 - t0) * 1e3 / steps, float(np.mean(list(per_call.values()))), recs
+
+
+def measure_call(emr, torch, name, steps, warmup, rT):
+    """A workload discovered with emr_discover + emr_result_check per step."""
+    from paper_2608_27612_amd import workloads as W
+    genomes, sources, depth, theta = W.workload(name)
+    theta32 = float(np.float32(theta))
+    pop = emr.emr_pack_population(genomes)
+    res = emr.alloc_result(pop, sources, depth)
+    work = emr.emr_discover_work(pop, sources, depth, transcendental_slots=rT)
+
+    def step():
+        emr.emr_discover(pop, sources, depth, theta32, res=res)
+        emr.emr_result_check(res)
+    ms, kms, recs = timed_steps(emr, torch, step, steps, warmup, rT)
+    compiled = {r["compiled"] for r in recs}
+    assert len(compiled) == 1, "the timed steps ran both tiers"
+    kernel = "emr_discover_jit_records" if compiled == {True} else "k_discover<1>"
+    records = int(res["pair_offset"][-1].item())
+    out = {"workload": name, "genomes": len(genomes), "sources": len(sources), "depth": depth,
+           "theta": theta, "steps": steps, "ms_per_step": ms,
+           "queries_per_step": int(work["queries"]), "records_per_step": records,
+           "queries_per_s": work["queries"] / (ms * 1e-3),
+           "evaluated_queries_per_s": work["evaluated"] / (ms * 1e-3),
+           "listed": all(r["listed"] for r in recs),
+           "roofline": roofline(work, kms, records, kernel, name)}
+    return out, (pop, res, genomes, sources, depth, theta32, work)
+
+
+def measure_stream(emr, torch, name, steps, warmup, rT):
+    """A workload discovered with emr_discover_stream (records counted by the sink) per step."""
+    from paper_2608_27612_amd import workloads as W
+    genomes, sources, depth, theta = W.workload(name)
+    theta32 = float(np.float32(theta))
+    pop = emr.emr_pack_population(genomes)
+    work = emr.emr_discover_work(pop, sources, depth, transcendental_slots=rT)
+    kept = [0]
+
+    def sink(pair, chunk, parent, w4):
+        kept[0] += len(parent)
+
+    def step():
+        kept[0] = 0
+        emr.emr_discover_stream(pop, sources, depth, theta32, sink)
+    for _ in range(warmup):
+        step()
+    emr.emr_profile_enable(True, rT, every=1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    recs = emr.emr_profile_read()
+    emr.emr_profile_enable(False)
+    ms = (t1 - t0) * 1e3 / steps
+    kms = sum(r["ms"] for r in recs) / steps  # every chunk's launch of a call
+    kernel = "emr_discover_jit_records" if all(r["compiled"] for r in recs) else "k_discover<1>"
+    return {"workload": name + " (streamed)", "genomes": len(genomes), "sources": len(sources),
+            "depth": depth, "theta": theta, "steps": steps, "ms_per_step": ms,
+            "launches_per_step": len(recs) // steps,
+            "queries_per_step": int(work["queries"]), "records_per_step": kept[0],
+            "queries_per_s": work["queries"] / (ms * 1e-3),
+            "evaluated_queries_per_s": work["evaluated"] / (ms * 1e-3),
+            "roofline": roofline(work, kms, kept[0], kernel, name)}, (genomes, sources, depth,
+                                                                        theta32)
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_rate(oracle, genomes, sources, depth, theta32, target_s, n0=2):
+    """The oracle as it stands on the first n genomes (all sources), n sized to ~target_s."""
+    n = min(n0, len(genomes))
     t0 = time.perf_counter()
     oracle.discover(genomes[:n], sources, depth, theta32)
     t = time.perf_counter() - t0
@@ -89,9 +210,49 @@ def cpu_baseline(genomes, sources, depth, theta32, target_s):
     oracle.discover(genomes[:n], sources, depth, theta32)
     t = time.perf_counter() - t0
     q = n * len(sources) * oracle.n_positions(depth)
-    return {"value": q / t, "unit": "queries/s", "cores": oracle.max_threads(), "kind": "oracle",
+    return {"value": q / t, "unit": "queries/s",
             "sample": "first %d of %d genomes x %d sources at depth %d (%d queries, %.1f s)"
                       % (n, len(genomes), len(sources), depth, q, t)}
+
+
+def cpu_baseline(genomes, sources, depth, theta32, target_s, sub_inputs, sub_target_s):
+    """The oracle, as it stands: the main workload's sample with every thread, then one-thread
+    rates on three small workloads, then a sample of every sub workload."""
+    import oracle
+    from paper_2608_27612_amd import workloads as W
+    threads = oracle.max_threads()
+    out = oracle_rate(oracle, genomes, sources, depth, theta32, target_s, n0=4)
+    out.update({"cores": threads, "kind": "oracle", "cpu_model": cpu_model()})
+    oracle.set_threads(1)
+    try:
+        one = {}
+        for name in ("single_d5", "xor_pop1000_d5", "tabular_pop150"):
+            g, s, d, th = W.workload(name)
+            r = oracle_rate(oracle, g, s, d, float(np.float32(th)), sub_target_s, n0=1)
+            one[name] = {"value": r["value"], "sample": r["sample"]}
+        out["one_thread"] = one
+    finally:
+        oracle.set_threads(threads)
+    subs = {}
+    for name, inp in sub_inputs.items():
+        g, s, d, th = inp
+        if len(g) == 1 and d >= 11:
+            # one deep CPPN: a random sample of its parents (each gives 4 queries)
+            Q = oracle.n_parents(d)
+            rng = np.random.default_rng(0)
+            parents = np.sort(rng.choice(Q, size=min(Q, 1 << 18), replace=False)).astype(np.int64)
+            t0 = time.perf_counter()
+            for src in s:
+                oracle.eval_parents(g[0], src, parents)
+            t = time.perf_counter() - t0
+            q = 4 * len(parents) * len(s)
+            subs[name] = {"value": q / t, "unit": "queries/s",
+                          "sample": "%d random parents of %d x %d sources at depth %d (%d queries, "
+                                    "%.1f s)" % (len(parents), Q, len(s), d, q, t)}
+        else:
+            subs[name] = oracle_rate(oracle, g, s, d, th, sub_target_s, n0=1)
+    out["workloads"] = subs
+    return out
 
 
 def main():
@@ -104,6 +265,7 @@ def main():
     ap.add_argument("--gens", type=int, default=5, help="generations timed for ms_per_gen")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sub", action="store_true", help="the main workload only")
     ap.add_argument("--jit", choices=["auto", "off", "always"], default="auto",
                     help="compiled-tier policy for the timed steps (auto: the warm-up compiles)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -116,7 +278,7 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2608_27612_amd import emr, workloads as W
+    from paper_2608_27612_amd import emr
 
     torch.cuda.set_device(0)
     if args.copy_calibration_mib > 0:
@@ -126,56 +288,14 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    genomes, sources, depth, theta = W.workload(args.workload)
-    theta32 = float(np.float32(theta))
     rT = args.transcendental_slots
-
     policy = {"auto": emr.EMR_JIT_AUTO, "off": emr.EMR_JIT_OFF, "always": emr.EMR_JIT_ALWAYS}[args.jit]
     emr.emr_set_jit(policy)
-    pop = emr.emr_pack_population(genomes)
-    res = emr.alloc_result(pop, sources, depth)
-    slots, queries = emr.emr_discover_cost(pop, sources, depth, transcendental_slots=rT)
 
-    for _ in range(args.warmup):
-        emr.emr_discover(pop, sources, depth, theta32, res=res)
-        emr.emr_result_check(res)
-
-    # The timed steps time the call's discover launch (one per call, every (sources per walk,
-    # window) part of the workload) with a HIP event pair on the call's stream, in one step of
-    # every TIME_EVERY (the first, then every TIME_EVERY-th), so that the events' own cost stays
-    # off most steps.
-    emr.emr_profile_enable("first", rT, every=TIME_EVERY)
-    launch_ms = []
-    host_s = 0.0
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        h0 = time.perf_counter()
-        emr.emr_discover(pop, sources, depth, theta32, res=res)
-        host_s += time.perf_counter() - h0
-        emr.emr_result_check(res)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    # the discover launch of each timed step, bracketed by its own event pair
-    launch_slots = None
-    compiled = set()
-    for rec in emr.emr_profile_read():
-        assert rec["first"] and launch_slots in (None, rec["slots"])
-        launch_slots = rec["slots"]
-        launch_ms.append(rec["ms"])
-        compiled.add(rec["compiled"])
-    assert len(compiled) == 1, "the timed steps ran both tiers"
+    main_line, (pop, res, genomes, sources, depth, theta32, work) = measure_call(
+        emr, torch, args.workload, args.steps, args.warmup, rT)
     jit = emr.emr_jit_info(pop)
-    assert len(launch_ms) == (args.steps + TIME_EVERY - 1) // TIME_EVERY
-    emr.emr_profile_enable(False)
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    value = queries / (ms_per_step * 1e-3)
-    records = int(res["pair_offset"][-1].item())
-
-    # the record mode of the discover kernel, compiled programs or the interpreter
-    kernel_name = "emr_discover_jit_records" if compiled == {True} else "k_discover<1>"
-    avg_ms = float(np.mean(launch_ms))
-    achieved = launch_slots / (avg_ms * 1e-3)
+    ms_per_step = main_line["ms_per_step"]
 
     # ms per generation: pack + discover + check on the host clock, for a new population each
     # generation (one call per population: the default policy interprets it), and with the
@@ -199,9 +319,22 @@ def main():
     ms_per_gen = per_gen(emr.EMR_JIT_AUTO)
     ms_per_gen_compiled = per_gen(emr.EMR_JIT_ALWAYS)
 
+    subs, sub_inputs = [], {}
+    if not args.no_sub:
+        from paper_2608_27612_amd import workloads as W
+        for name, steps in (("xor_pop1000_d8", 40), ("tabular_pop150", 100)):
+            if name == args.workload:
+                continue
+            line, inp = measure_call(emr, torch, name, steps, 5, rT)
+            subs.append(line)
+            sub_inputs[name] = (inp[2], inp[3], inp[4], inp[5])
+        line, inp = measure_stream(emr, torch, "deep_single", 3, 1, rT)
+        subs.append(line)
+        sub_inputs["deep_single"] = inp
+
     line = {
         "metric": METRIC,
-        "value": value,
+        "value": main_line["queries_per_s"],
         "unit": "queries/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -212,23 +345,23 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": args.workload, "genomes": len(genomes), "sources": len(sources),
-                   "depth": depth, "theta": theta, "queries_per_step": int(queries),
-                   "records_per_step": records},
+        "config": {"workload": args.workload, "genomes": main_line["genomes"],
+                   "sources": main_line["sources"], "depth": main_line["depth"],
+                   "theta": main_line["theta"], "queries_per_step": main_line["queries_per_step"],
+                   "records_per_step": main_line["records_per_step"]},
+        "evaluated_queries_per_s": main_line["evaluated_queries_per_s"],
         "ms_per_gen": ms_per_gen,
         "ms_per_gen_compiled": ms_per_gen_compiled,
         "compiled_tier": {"programs": jit["programs"], "code_bytes": jit["code_bytes"],
-                          "compile_ms": jit["compile_ms"], "load_ms": jit["load_ms"]},
-        "host_enqueue_ms": host_s * 1e3 / args.steps,
-        "valu_frac_step": (slots / (ms_per_step * 1e-3)) / VALU_PEAK_SLOTS,
-        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_SLOTS / 1e12,
-                     "unit": "TOP/s", "frac": achieved / VALU_PEAK_SLOTS,
-                     "traffic": profiled_traffic(kernel_name, args.workload),
-                     "kernel": kernel_name, "kernel_ms": avg_ms,
-                     "transcendental_slots": rT},
+                          "compile_ms": jit["compile_ms"], "load_ms": jit["load_ms"],
+                          "listed": main_line["listed"]},
+        "valu_frac_step": (work["slots"] / (ms_per_step * 1e-3)) / VALU_PEAK_SLOTS,
+        "roofline": dict(main_line["roofline"], transcendental_slots=rT),
+        "sub": subs,
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(genomes, sources, depth, theta32, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(genomes, sources, depth, theta32, args.cpu_seconds,
+                                            sub_inputs, min(3.0, args.cpu_seconds))
     print(json.dumps(line), flush=True)
 
 

@@ -372,11 +372,15 @@ emr_status emr_eval_raw_noalloc(const emr_population* pop, const emr_source* sou
  * (genome, direction) program: one slot per position-dependent edge, the activations' slots
  * (transcendental instructions weighted by transcendental_slots) and 2.5 for the variance; a
  * program whose output does not depend on the position costs 0 (its outputs are per-source
- * constants and their variance is exactly zero). Host only. */
+ * constants and their variance is exactly zero). *evaluated: the queries of the pairs whose output
+ * depends on the position (the others are answered by their per-source constant); *flops: useful
+ * floating-point operations, 2 per position-dependent edge (a multiply-add), 1 per other
+ * activation operation and per transcendental, 2.5 per query for the variance. Any output pointer
+ * may be NULL. Host only. */
 emr_status emr_discover_cost(const emr_population* pop, const emr_source* sources,
                              int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
                              int32_t depth, double transcendental_slots, double* slots,
-                             double* queries);
+                             double* queries, double* evaluated, double* flops);
 
 /* ------------------------------------------------------------------ compiled tier */
 

@@ -74,6 +74,8 @@ def lib():
                                C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
                                C.POINTER(C.c_int64)]
         L.orc_max_threads.restype = C.c_int
+        L.orc_set_threads.restype = None
+        L.orc_set_threads.argtypes = [C.c_int]
         _lib = L
     return _lib
 
@@ -218,6 +220,11 @@ def lazy(g: dict, source, depth: int, theta: float):
 
 def max_threads() -> int:
     return int(lib().orc_max_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads the oracle's later calls may use (timing harness only)."""
+    lib().orc_set_threads(int(n))
 
 
 def _pair_sources(sources, n_genomes: int, src_offsets=None):

@@ -392,6 +392,15 @@ int64_t orc_lazy(const orc_genome* g, const orc_source* s, int depth, double the
   return found;
 }
 
+/* Harness control, no arithmetic: the OpenMP threads later calls may use (n >= 1). */
+void orc_set_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 int orc_max_threads(void) {
 #ifdef _OPENMP
   return omp_get_max_threads();

@@ -236,6 +236,13 @@ double query_trans(const emr::GenomeInfo& inf) {
 double query_slots(const emr::GenomeInfo& inf, double rT) {
   return query_base(inf) + rT * query_trans(inf);
 }
+// Useful floating-point operations per query: a multiply-add per position-dependent edge counts
+// 2, every other activation operation and each transcendental 1, the variance 2.5.
+double query_flops(const emr::GenomeInfo& inf) {
+  if (!inf.out_varying) return 0.0;
+  return 2.0 * (inf.fma_xy + inf.fma_node) + (query_base(inf) - inf.fma_xy - inf.fma_node - 2.5) +
+         query_trans(inf) + 2.5;
+}
 
 }  // namespace
 
@@ -1763,16 +1770,25 @@ emr_status emr_eval_raw_noalloc(const emr_population* pop, const emr_source* sou
 emr_status emr_discover_cost(const emr_population* pop, const emr_source* sources,
                              int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
                              int32_t depth, double transcendental_slots, double* slots,
-                             double* queries) {
+                             double* queries, double* evaluated, double* flops) {
   std::shared_ptr<const Plan> plan;
   emr_status st = plan_for(pop, sources, n_sources, src_offsets, n_shared, depth, &plan);
   if (st != EMR_OK) return st;
   const Plan& P = *plan;
   const double npos = (double)emr::n_positions(depth);
-  double total = 0.0;
-  for (const emr::Member& m : P.members) total += query_slots(pop->info[m.desc], transcendental_slots) * npos;
+  double total = 0.0, varying = 0.0, fl = 0.0;
+  for (const emr::Member& m : P.members) {
+    const emr::GenomeInfo& inf = pop->info[m.desc];
+    total += query_slots(inf, transcendental_slots) * npos;
+    if (inf.out_varying) {
+      varying += npos;
+      fl += query_flops(inf) * npos;
+    }
+  }
   if (slots) *slots = total;
   if (queries) *queries = (double)P.n_pairs * npos;
+  if (evaluated) *evaluated = varying;
+  if (flops) *flops = fl;
   return EMR_OK;
 }
 

@@ -105,7 +105,7 @@ def lib():
             "emr_discover": (I32, [P, P, I32, P, I32, I32, F32, P, P]),
             "emr_result_check": (I32, [P, P, P, P]),
             "emr_eval_raw": (I32, [P, P, I32, P, I32, I32, P, P, I64, P]),
-            "emr_discover_cost": (I32, [P, P, I32, P, I32, I32, F64, P, P]),
+            "emr_discover_cost": (I32, [P, P, I32, P, I32, I32, F64, P, P, P, P]),
             "emr_profile_enable": (I32, [I32, I32, F64]),
             "emr_profile_read": (I32, [P, I32, P]),
             "emr_stream_chunks": (I32, [I32, I64, P]),
@@ -404,17 +404,28 @@ def emr_eval_raw_noalloc(pop: Population, sources, depth: int, out, err, src_off
                                       C.c_void_p(err.data_ptr()), _stream_ptr(stream)))
 
 
-def emr_discover_cost(pop: Population, sources, depth: int, src_offsets=None,
+def emr_discover_work(pop: Population, sources, depth: int, src_offsets=None,
                       transcendental_slots: float = 4.0):
-    """(algorithmic VALU slots, queries) of one discover call under the cost model."""
+    """The algorithmic work of one discover call: {"slots": VALU slots under the cost model,
+    "queries": all queries, "evaluated": queries of position-dependent pairs, "flops": useful
+    floating-point operations}."""
     offs = _offsets(src_offsets)
-    slots, queries = C.c_double(), C.c_double()
+    slots, queries, evaluated, flops = C.c_double(), C.c_double(), C.c_double(), C.c_double()
     src = _sources(sources)
     _check(lib().emr_discover_cost(pop.handle, src.ctypes.data, len(sources),
                                    None if offs is None else offs.ctypes.data,
                                    0 if offs is not None else len(sources), depth,
-                                   float(transcendental_slots), C.byref(slots), C.byref(queries)))
-    return slots.value, queries.value
+                                   float(transcendental_slots), C.byref(slots), C.byref(queries),
+                                   C.byref(evaluated), C.byref(flops)))
+    return {"slots": slots.value, "queries": queries.value, "evaluated": evaluated.value,
+            "flops": flops.value}
+
+
+def emr_discover_cost(pop: Population, sources, depth: int, src_offsets=None,
+                      transcendental_slots: float = 4.0):
+    """(algorithmic VALU slots, queries) of one discover call under the cost model."""
+    w = emr_discover_work(pop, sources, depth, src_offsets, transcendental_slots)
+    return w["slots"], w["queries"]
 
 
 def records_to_host(res):
