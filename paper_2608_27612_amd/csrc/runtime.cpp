@@ -20,6 +20,7 @@
 #include "emr_internal.h"
 #include "jit.h"
 #include "pack.h"
+#include "plan.h"
 #include "sched.h"
 
 // Launchers (kernels.hip).
@@ -64,7 +65,7 @@ emr_status fail(emr_status st, const char* fmt, ...) {
     if (e_ != hipSuccess) return fail(EMR_E_DEVICE, "%s: %s", #call, hipGetErrorString(e_)); \
   } while (0)
 
-inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+using emr::align256;
 
 // Compute units of the current device, queried once per device.
 // Host worker threads for the library's parallel host work (packing, the compiled tier's
@@ -211,38 +212,10 @@ struct Profiler {
 };
 thread_local Profiler g_prof;
 
-// Algorithmic VALU slots per query of one (genome, direction) program: one per position-dependent
-// edge, the activation costs (transcendental instructions weighted by rT), and 2.5 for the
-// variance and threshold share of a query.
-// The cost is base + rT * trans: query_base() is the part without transcendentals, query_trans()
-// their count per query. A program whose output does not depend on the position costs nothing
-// per query: its output is the source's constant (folded once by the bind kernel, like every
-// position-independent node) and the variance of a constant is exactly zero, so the kernels
-// evaluate and test nothing for it.
-double query_base(const emr::GenomeInfo& inf) {
-  if (!inf.out_varying) return 0.0;
-  const double other[6] = {0.0, 1.0, 2.0, 1.0, 1.0, 1.0};
-  double c = inf.fma_xy + inf.fma_node + 2.5;
-  for (int a = 0; a < 6; ++a) c += inf.act_count[a] * other[a];
-  return c;
-}
-double query_trans(const emr::GenomeInfo& inf) {
-  if (!inf.out_varying) return 0.0;
-  const double trans[6] = {0.0, 2.0, 2.0, 1.0, 1.0, 0.0};
-  double c = 0.0;
-  for (int a = 0; a < 6; ++a) c += inf.act_count[a] * trans[a];
-  return c;
-}
-double query_slots(const emr::GenomeInfo& inf, double rT) {
-  return query_base(inf) + rT * query_trans(inf);
-}
-// Useful floating-point operations per query: a multiply-add per position-dependent edge counts
-// 2, every other activation operation and each transcendental 1, the variance 2.5.
-double query_flops(const emr::GenomeInfo& inf) {
-  if (!inf.out_varying) return 0.0;
-  return 2.0 * (inf.fma_xy + inf.fma_node) + (query_base(inf) - inf.fma_xy - inf.fma_node - 2.5) +
-         query_trans(inf) + 2.5;
-}
+using emr::query_base;
+using emr::query_trans;
+using emr::query_slots;
+using emr::query_flops;
 
 }  // namespace
 
@@ -269,11 +242,7 @@ struct emr_population {
 
 namespace {
 
-int window_bucket(int window) {
-  for (int w : emr::kWindows)
-    if (window <= w) return w;
-  return -1;
-}
+using emr::window_bucket;
 
 // The compiled tier of one plan: its groups' programs translated to machine code, written into the
 // code area of a copy of the template code object, loaded as a module on one device.
@@ -303,51 +272,17 @@ struct JitModule {
   }
 };
 
-// Everything one discover / raw-eval call needs besides the population.
-struct Plan {
-  int depth = 0;
-  int64_t n_pairs = 0;
-  int64_t tiles = 0;
-  struct Bucket {
-    int S, window;
-    uint32_t first, count;
-    double cost;  // summed per-query cost of its groups' programs (launch order)
-    uint32_t varying;  // its first `varying` groups have a position-dependent output (the rest,
-                       // the cheapest, do not)
-  };
-  // The discover launch of a call: its buckets (one per sources per walk and register window),
-  // costliest first.
-  struct Launch {
-    int n_parts;
-    int part[emr::kMaxBuckets];  // bucket indices
-    double cost;
-    // per position of the range, over all the launch's queries: cost-model slots without
-    // transcendentals, transcendental instructions, and queries (sources)
-    double slots_base, slots_trans, sources;
-  };
-  std::vector<emr::Group> groups;
-  std::vector<Bucket> buckets;
-  std::vector<Launch> launches;  // one (none without groups)
-  std::vector<emr::Member> members;
-  std::vector<uint32_t> group_member0;  // index of each group's first member
-  std::vector<float> src_xy;
-  uint64_t bias_floats = 0;
-  // The plan's tables (groups at t_groups, members at t_members, source coordinates at
-  // t_srcxy, one byte per pair at t_uniform: 1 when the pair's output does not depend on the
-  // position): a host image, and its device copy, uploaded on first use and freed with the plan.
-  std::vector<char> img;
-  size_t t_groups = 0, t_members = 0, t_srcxy = 0, t_uniform = 0;
-  size_t t_pairinfo = 0;  // per pair: genome << 1 | dir, source index (two words)
+// Everything one discover / raw-eval call needs besides the population: the host-built tables
+// (emr::PlanTables) and their device copies, schedules and compiled tier.
+struct Plan : emr::PlanTables {
   mutable std::mutex dev_mu;
+  // The tables' device copy, uploaded on first use and freed with the plan.
   mutable char* d_tables = nullptr;
   // The bias rows of the plan's groups (the bind kernel's output: every position-independent
   // contribution per (genome, source)), computed on the device once, on first use (dev_mu).
   mutable float* d_bias = nullptr;
-  // Per group: cost-model slots of one query of one of its sources (the launch schedules' chunk
-  // costs).
-  std::vector<float> group_cost;
-  // The waves' chunk lists of the plan's launches (plan_schedule), one per launch shape, on the
-  // device (dev_mu).
+  // The workgroups' chunk lists of the plan's launches (plan_schedule), one per launch shape, on
+  // the device (dev_mu).
   struct Sched {
     uint32_t grid, tiles, n_parts;
     emr::DiscoverPart part[emr::kMaxParts];
@@ -382,23 +317,6 @@ struct Plan {
   mutable int jit_state = 0;  // 0 not built, 1 ready, -1 failed (reason in jit_error)
   mutable std::string jit_error;
   mutable std::atomic<int> calls{0};  // calls that ran this plan
-  // What the plan was built for (exact copies, compared on reuse).
-  std::vector<emr_source> key_sources;
-  std::vector<int32_t> key_offs;
-  bool key_has_offs = false;
-  int32_t key_n_shared = 0;
-  // Workspace layout (bytes from the workspace start): tile status words, the compaction's group
-  // marks and per-pair record totals (cleared before each record call: clear_words words from
-  // off_nz); then (total onwards) the record pool of a call's capacity.
-  size_t off_status = 0;
-  size_t total = 0;
-  size_t status_bytes = 0;
-  size_t off_nz = 0, nz_bytes = 0;
-  size_t off_ptotal = 0;
-  int64_t clear_words = 0;
-  // Floats of a bias table: the groups' rows plus 16 floats of padding (the compiled tier loads a
-  // group's rows 1 .. 4 at once).
-  size_t bias_table_floats() const { return (size_t)bias_floats + 16; }
 };
 
 // The record pool after a plan's fixed workspace: `capacity` parent indices, then (16-byte
@@ -413,172 +331,13 @@ size_t workspace_need(const Plan& P, int64_t capacity) {
 emr_status build_plan(const emr_population* pop, const emr_source* sources, int32_t n_sources,
                       const int32_t* offs, int32_t n_shared, int32_t depth, Plan* plan) {
   if (!pop) return fail(EMR_E_INVAL, "population is NULL");
-  if (depth < 0 || depth > EMR_MAX_DEPTH)
-    return fail(EMR_E_INVAL, "depth %d outside [0, %d]", depth, EMR_MAX_DEPTH);
-  if (n_sources < 0 || (n_sources > 0 && !sources)) return fail(EMR_E_INVAL, "bad sources");
-  const int32_t G = pop->n_genomes;
-  if (offs) {
-    if (offs[0] != 0) return fail(EMR_E_INVAL, "src_offsets[0] must be 0");
-    for (int32_t g = 0; g < G; ++g)
-      if (offs[g + 1] < offs[g]) return fail(EMR_E_INVAL, "src_offsets not ascending at %d", g);
-    if (offs[G] != n_sources)
-      return fail(EMR_E_INVAL, "src_offsets[n_genomes]=%d but n_sources=%d", offs[G], n_sources);
-  } else {
-    if (n_shared < 0 || n_shared != n_sources)
-      return fail(EMR_E_INVAL, "n_shared=%d must equal n_sources=%d", n_shared, n_sources);
-  }
-  for (int32_t i = 0; i < n_sources; ++i)
-    if (sources[i].dir != EMR_DIR_OUT && sources[i].dir != EMR_DIR_IN)
-      return fail(EMR_E_INVAL, "source %d has direction %d", i, sources[i].dir);
-
-  Plan& P = *plan;  // a freshly made plan
-  P.depth = depth;
-  P.n_pairs = offs ? (int64_t)n_sources : (int64_t)G * n_shared;
-  P.tiles = emr::tiles_per_pair(depth);
-  if (P.n_pairs > 0xFFFFFFFFll) return fail(EMR_E_LIMIT, "too many pairs");
-
-  // Group each genome's sources by direction, in source order, into sets of <= max_group(window).
-  struct TmpGroup {
-    emr::Group g;
-    int S, window;
-    uint32_t desc;
-    uint32_t src[emr::kMaxGroup];
-  };
-  std::vector<TmpGroup> tmp;
-  for (int32_t g = 0; g < G; ++g) {
-    const int32_t lo = offs ? offs[g] : 0, hi = offs ? offs[g + 1] : n_shared;
-    for (int dir = 0; dir < 2; ++dir) {
-      const uint32_t di = 2u * (uint32_t)g + (uint32_t)dir;
-      const emr::ProgDesc& d = pop->desc[di];
-      const int wb = window_bucket(pop->info[di].window);
-      if (wb < 0) return fail(EMR_E_LIMIT, "genome %d needs a value window of %d", g, pop->info[di].window);
-      const int gmax = emr::max_group(wb);
-      TmpGroup cur{};
-      int n = 0;
-      auto flush = [&]() {
-        if (n == 0) return;
-        cur.S = n;
-        cur.window = wb;
-        cur.desc = di;
-        for (int s = n; s < emr::kMaxGroup; ++s) cur.g.pair[s] = cur.g.pair[n - 1];
-        cur.g.var_off = d.var_off;
-        cur.g.n_rec = d.n_rec;
-        cur.g.n_steps = d.n_steps;
-        cur.g.flags = d.flags;
-        tmp.push_back(cur);
-        cur = TmpGroup{};
-        n = 0;
-      };
-      for (int32_t j = lo; j < hi; ++j) {
-        if (sources[j].dir != dir) continue;
-        const int64_t pair = offs ? (int64_t)j : (int64_t)g * n_shared + j;
-        cur.g.pair[n] = (uint32_t)pair;
-        cur.src[n] = (uint32_t)j;
-        if (++n == gmax) flush();
-      }
-      flush();
-    }
-  }
-  // Order groups by bucket; assign bias-table offsets and members.
-  // Within a bucket, the most expensive programs come first: waves take tiles round-robin, so the
-  // cheap tiles end up in the last rounds and even out the tail. Output order does not depend on
-  // this order (each pair has its own region and scan row).
-  std::vector<double> cost(2 * (size_t)G);
-  for (size_t i = 0; i < cost.size(); ++i) cost[i] = query_slots(pop->info[i], 4.0);
-  std::stable_sort(tmp.begin(), tmp.end(), [&](const TmpGroup& a, const TmpGroup& b) {
-    if (a.S != b.S) return a.S < b.S;
-    if (a.window != b.window) return a.window < b.window;
-    return cost[a.desc] > cost[b.desc];
-  });
-  P.groups.reserve(tmp.size());
-  uint64_t bias = 0;
-  for (size_t i = 0; i < tmp.size(); ++i) {
-    TmpGroup& t = tmp[i];
-    if (P.buckets.empty() || P.buckets.back().S != t.S || P.buckets.back().window != t.window)
-      P.buckets.push_back({t.S, t.window, (uint32_t)i, 0, 0.0, 0});
-    P.buckets.back().count++;
-    if (t.g.flags & 1u) P.buckets.back().varying = P.buckets.back().count;
-    P.buckets.back().cost += t.S * cost[t.desc];
-    t.g.bias_off = (uint32_t)bias;
-    P.group_member0.push_back((uint32_t)P.members.size());
-    const uint32_t rows = t.g.n_rec + 2;  // output row, one per record at most, prefetch row
-    for (int s = 0; s < t.S; ++s)
-      P.members.push_back({t.desc, t.src[s], (uint32_t)(bias + s), rows});
-    bias += 4ull * rows;
-    P.groups.push_back(t.g);
-    P.group_cost.push_back((float)cost[t.desc]);
-  }
-  if (bias > 0xFFFFFFFFull) return fail(EMR_E_LIMIT, "bias table too large");
-  // Part order within the launch: the costliest bucket first (its chunks are handed out first).
-  std::stable_sort(P.buckets.begin(), P.buckets.end(),
-                   [](const Plan::Bucket& a, const Plan::Bucket& b) { return a.cost > b.cost; });
-  // One launch with every bucket as a part, in cost order.
-  if ((int)P.buckets.size() > emr::kMaxBuckets) return fail(EMR_E_LIMIT, "too many buckets");
-  if (!P.buckets.empty()) {
-    Plan::Launch L{};
-    for (size_t bi = 0; bi < P.buckets.size(); ++bi) {
-      const Plan::Bucket& b = P.buckets[bi];
-      L.part[L.n_parts++] = (int)bi;
-      L.cost += b.cost;
-      for (uint32_t g = 0; g < b.count; ++g) {
-        const emr::GenomeInfo& inf = pop->info[P.members[P.group_member0[b.first + g]].desc];
-        L.slots_base += b.S * query_base(inf);
-        L.slots_trans += b.S * query_trans(inf);
-      }
-      L.sources += (double)b.S * b.count;
-    }
-    P.launches.push_back(L);
-  }
-  for (const auto& b : P.buckets)
-    if ((uint64_t)b.count * (uint64_t)P.tiles > 0xFFFFFFFFull)
-      return fail(EMR_E_LIMIT, "too many tiles in one launch");
-  P.bias_floats = bias;
-  P.src_xy.resize(2 * (size_t)n_sources);
-  for (int32_t i = 0; i < n_sources; ++i) {
-    P.src_xy[2 * i] = sources[i].x;
-    P.src_xy[2 * i + 1] = sources[i].y;
-  }
-
-  // workspace: tile status words, group marks, per-pair totals
-  P.off_status = 0;
-  P.status_bytes = (size_t)P.n_pairs * P.tiles * 8;
-  P.off_nz = align256(P.off_status + P.status_bytes);
-  P.nz_bytes = (size_t)P.n_pairs * emr::nz_words((uint32_t)P.tiles) * 8;
-  P.off_ptotal = align256(P.off_nz + P.nz_bytes);
-  P.total = align256(P.off_ptotal + (size_t)P.n_pairs * 4);
-  P.clear_words = (int64_t)((P.off_ptotal + (size_t)P.n_pairs * 4 - P.off_nz + 3) / 4);
-  // tables
-  P.t_groups = 0;
-  P.t_members = align256(P.groups.size() * sizeof(emr::Group));
-  P.t_srcxy = align256(P.t_members + P.members.size() * sizeof(emr::Member));
-  P.t_uniform = align256(P.t_srcxy + P.src_xy.size() * sizeof(float));
-  P.t_pairinfo = align256(P.t_uniform + (size_t)P.n_pairs);
-  P.img.assign(align256(P.t_pairinfo + (size_t)P.n_pairs * 8) + 256, 0);
-  {
-    uint32_t* info = (uint32_t*)(P.img.data() + P.t_pairinfo);
-    for (int32_t g = 0; g < G; ++g) {
-      const int32_t lo = offs ? offs[g] : 0, hi = offs ? offs[g + 1] : n_shared;
-      for (int32_t j = lo; j < hi; ++j) {
-        const int64_t pair = offs ? (int64_t)j : (int64_t)g * n_shared + j;
-        info[2 * pair] = ((uint32_t)g << 1) | (uint32_t)sources[j].dir;
-        info[2 * pair + 1] = (uint32_t)j;
-      }
-    }
-  }
-  for (const emr::Group& g : P.groups)
-    if (!(g.flags & 1u))
-      for (int s = 0; s < emr::kMaxGroup; ++s) P.img[P.t_uniform + g.pair[s]] = 1;
-  if (!P.groups.empty())
-    std::memcpy(P.img.data() + P.t_groups, P.groups.data(), P.groups.size() * sizeof(emr::Group));
-  if (!P.members.empty())
-    std::memcpy(P.img.data() + P.t_members, P.members.data(),
-                P.members.size() * sizeof(emr::Member));
-  if (!P.src_xy.empty())
-    std::memcpy(P.img.data() + P.t_srcxy, P.src_xy.data(), P.src_xy.size() * sizeof(float));
-  P.key_sources.assign(sources, sources + n_sources);
-  P.key_has_offs = offs != nullptr;
-  if (offs) P.key_offs.assign(offs, offs + G + 1);
-  P.key_n_shared = n_shared;
+  std::string msg;
+  emr_status st = emr::build_plan_tables(pop->desc.data(), pop->info.data(), pop->n_genomes,
+                                         sources, n_sources, offs, n_shared, depth, plan, &msg);
+  if (st != EMR_OK) return fail(st, "%s", msg.c_str());
+  // every offset the kernels take from the tables, checked before any of them is uploaded
+  if (!emr::check_plan_tables(*plan, pop->desc.data(), pop->blob_words, &msg))
+    return fail(EMR_E_LIMIT, "the call's tables failed their bounds check: %s", msg.c_str());
   return EMR_OK;
 }
 
@@ -1440,68 +1199,30 @@ emr_status emr_build_grids(int32_t depth, float* xy_dev, void* stream) {
 
 namespace {
 
-// Packs genomes on host threads (each thread a contiguous range into its own word vector, then
-// the vectors are concatenated and their genomes' descriptors moved by the vector's base), and
-// uploads the tables through pinned staging. *bad_index receives the lowest failing genome.
+// Packs genomes on host threads (emr::pack_genomes: each thread a contiguous range into its own
+// word vector, then the vectors concatenated and their genomes' descriptors moved by the vector's
+// base), and uploads the tables through pinned staging. *bad_index receives the lowest failing
+// genome.
 emr_status pack_and_upload(int32_t n, const std::function<emr_genome(int32_t)>& genome_at,
                            emr_population** out, int32_t* bad_index) {
-  std::vector<emr::ProgDesc> desc(2 * (size_t)n);
-  std::vector<emr::GenomeInfo> info(2 * (size_t)n);
+  std::vector<emr::ProgDesc> desc;
+  std::vector<emr::GenomeInfo> info;
+  std::vector<uint32_t> words;
   const int n_threads = std::max(1, std::min({WorkerPool::get().size(), 16, n / 32}));
-  struct Part {
-    std::vector<uint32_t> words;
-    int32_t bad = -1;
-    emr_status st = EMR_OK;
-    std::string msg;
-  };
-  std::vector<Part> parts((size_t)n_threads);
-  auto work = [&](int t) {
-    const int32_t lo = (int32_t)((int64_t)n * t / n_threads);
-    const int32_t hi = (int32_t)((int64_t)n * (t + 1) / n_threads);
-    Part& p = parts[(size_t)t];
-    for (int32_t g = lo; g < hi; ++g) {
-      emr_status st = EMR_OK;
-      std::string msg;
-      if (!emr::pack_genome(genome_at(g), p.words, &desc[2 * (size_t)g], &info[2 * (size_t)g], &st,
-                            &msg)) {
-        p.bad = g;
-        p.st = st;
-        p.msg = msg;
-        return;
-      }
-      if (p.words.size() > 0xF0000000ull) {
-        p.bad = g;
-        p.st = EMR_E_LIMIT;
-        p.msg = "population too large";
-        return;
-      }
-    }
-    while (p.words.size() % emr::kRecWords) p.words.push_back(0u);  // keep bases aligned
-  };
-  WorkerPool::get().run(n_threads, work);
-  for (const Part& p : parts)
-    if (p.bad >= 0) {  // the parts cover increasing genome ranges: the first is the lowest
-      if (bad_index) *bad_index = p.bad;
-      return fail(p.st, "genome %d: %s", p.bad, p.msg.c_str());
-    }
-  // concatenate, moving each part's descriptors by its base
-  size_t total = 16;  // the kernels may read a few words past a program's end
-  for (const Part& p : parts) total += p.words.size();
-  if (total > 0xF0000000ull) return fail(EMR_E_LIMIT, "population too large");
+  std::string msg;
+  int32_t bad = -1;
+  emr_status pst = emr::pack_genomes(
+      n, genome_at, n_threads,
+      [](int k, const std::function<void(int)>& f) { WorkerPool::get().run(k, f); }, &desc, &info,
+      &words, &bad, &msg);
+  if (pst != EMR_OK) {
+    if (bad_index && bad >= 0) *bad_index = bad;
+    return fail(pst, "%s", msg.c_str());
+  }
+  const size_t total = words.size();
   emr_population* pop = new (std::nothrow) emr_population;
   if (!pop) return fail(EMR_E_NOMEM, "host allocation failed");
   std::unique_ptr<emr_population, void (*)(emr_population*)> guard(pop, emr_free_population);
-  size_t base = 0;
-  for (int t = 0; t < n_threads; ++t) {
-    const int32_t lo = (int32_t)((int64_t)n * t / n_threads);
-    const int32_t hi = (int32_t)((int64_t)n * (t + 1) / n_threads);
-    for (size_t d = 2 * (size_t)lo; d < 2 * (size_t)hi; ++d) {
-      desc[d].var_off += (uint32_t)base;
-      desc[d].uni_off += (uint32_t)base;
-      desc[d].uni_end += (uint32_t)base;
-    }
-    base += parts[(size_t)t].words.size();
-  }
   pop->n_genomes = n;
   pop->desc = std::move(desc);
   pop->info = std::move(info);
@@ -1526,12 +1247,7 @@ emr_status pack_and_upload(int32_t n, const std::function<emr_genome(int32_t)>& 
       return fail(EMR_E_NOMEM, "pinned upload staging of %zu bytes failed", want);
     up_size = want;
   }
-  pop->h_blob.assign(total, 0u);
-  size_t off = 0;
-  for (const Part& p : parts) {
-    std::copy(p.words.begin(), p.words.end(), pop->h_blob.begin() + (ptrdiff_t)off);
-    off += p.words.size();
-  }
+  pop->h_blob = std::move(words);
   char* img = (char*)up_buf;
   std::memcpy(img, pop->h_blob.data(), blob_bytes);
   std::memcpy(img + blob_bytes, pop->desc.data(), pop->desc.size() * sizeof(emr::ProgDesc));

@@ -16,7 +16,9 @@ ROOT = os.path.dirname(HERE)
 SHIM_SRC = os.path.join(HERE, "shim", "pack_shim.cpp")
 PACK_SRC = os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "pack.cpp")
 JIT_SRC = os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "jit.cpp")
-JIT_DEPS = [os.path.join(ROOT, "paper_2608_27612_amd", "csrc", f) for f in ("jit.h", "emr_internal.h", "pack.h")]
+PLAN_SRC = os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "plan.cpp")
+JIT_DEPS = [os.path.join(ROOT, "paper_2608_27612_amd", "csrc", f)
+            for f in ("jit.h", "emr_internal.h", "pack.h", "plan.h")]
 SHIM_LIB = os.path.join(HERE, "shim", "libpackshim.so")
 
 _lib = None
@@ -25,7 +27,7 @@ _lib = None
 def shim():
     global _lib
     if _lib is None:
-        srcs = [SHIM_SRC, PACK_SRC, JIT_SRC]
+        srcs = [SHIM_SRC, PACK_SRC, JIT_SRC, PLAN_SRC]
         if (not os.path.exists(SHIM_LIB)
                 or max(os.path.getmtime(s) for s in srcs + JIT_DEPS) > os.path.getmtime(SHIM_LIB)):
             tmp = SHIM_LIB + ".tmp%d" % os.getpid()
@@ -43,6 +45,10 @@ def shim():
         L.shim_grow.restype = C.c_int
         L.shim_grow.argtypes = [C.c_void_p, C.c_int64, C.c_int64, C.c_int64, C.c_void_p, C.c_int64,
                                 C.POINTER(C.c_int64), C.POINTER(C.c_int64), C.c_char_p, C.c_int]
+        L.shim_plan_check.restype = C.c_int
+        L.shim_plan_check.argtypes = [C.c_void_p, C.c_int32, C.c_int, C.c_void_p, C.c_int32,
+                                      C.c_void_p, C.c_int32, C.c_int32, C.c_int,
+                                      C.POINTER(C.c_int64), C.c_char_p, C.c_int]
         _lib = L
     return _lib
 

@@ -75,3 +75,74 @@ extern "C" int shim_grow(const uint8_t* img, int64_t n, int64_t area_bytes, int6
   std::memcpy(out, o.data(), o.size());
   return 0;
 }
+
+// A population's packing and a call's plan, built on the host exactly as the library builds them
+// (packing in n_parts ranges, as threads do), then checked with the library's table check. With
+// plant > 0 one entry is made wrong before the check (1: a group's bias rows past the table, 2: a
+// group's pair past the call, 3: a member's source past the sources, 4: a descriptor's records
+// past the program words, 5: one pair in two groups, 6: the workspace totals over the pool).
+// Returns 0 when the tables check out, 1 when the check refuses them, else the build's status;
+// stats[0..4]: groups, members, bias floats, program words, buckets.
+#include "../../paper_2608_27612_amd/csrc/plan.h"
+
+extern "C" int shim_plan_check(const emr_genome* genomes, int32_t n_genomes, int n_parts,
+                               const emr_source* sources, int32_t n_sources, const int32_t* offs,
+                               int32_t n_shared, int32_t depth, int plant, int64_t* stats,
+                               char* msg, int msg_cap) {
+  auto put = [&](const std::string& m) {
+    std::strncpy(msg, m.c_str(), (size_t)msg_cap - 1);
+    msg[msg_cap - 1] = 0;
+  };
+  std::vector<emr::ProgDesc> desc;
+  std::vector<emr::GenomeInfo> info;
+  std::vector<uint32_t> words;
+  std::string m;
+  int32_t bad = -1;
+  emr_status st = emr::pack_genomes(
+      n_genomes, [&](int32_t g) { return genomes[g]; }, n_parts,
+      [](int k, const std::function<void(int)>& f) {
+        for (int t = 0; t < k; ++t) f(t);
+      },
+      &desc, &info, &words, &bad, &m);
+  if (st != EMR_OK) {
+    put(m);
+    return (int)st;
+  }
+  emr::PlanTables P;
+  st = emr::build_plan_tables(desc.data(), info.data(), n_genomes, sources, n_sources, offs,
+                              n_shared, depth, &P, &m);
+  if (st != EMR_OK) {
+    put(m);
+    return (int)st;
+  }
+  stats[0] = (int64_t)P.groups.size();
+  stats[1] = (int64_t)P.members.size();
+  stats[2] = (int64_t)P.bias_floats;
+  stats[3] = (int64_t)words.size();
+  stats[4] = (int64_t)P.buckets.size();
+  if (plant > 0 && P.groups.empty()) {
+    put("nothing to plant in");
+    return 2;
+  }
+  switch (plant) {
+    case 1: P.groups.back().bias_off = (uint32_t)P.bias_floats; break;
+    case 2: P.groups[0].pair[0] = (uint32_t)P.n_pairs; break;
+    case 3: P.members.back().source = (uint32_t)n_sources; break;
+    case 4: desc[P.members[0].desc].var_off = (uint32_t)words.size(); break;
+    case 5:
+      if (P.groups.size() < 2) {
+        put("one group only");
+        return 2;
+      }
+      P.groups[1].pair[0] = P.groups[0].pair[0];
+      break;
+    case 6: P.total = P.off_ptotal; break;
+    default: break;
+  }
+  if (!emr::check_plan_tables(P, desc.data(), words.size(), &m)) {
+    put(m);
+    return 1;
+  }
+  put("ok");
+  return 0;
+}
