@@ -316,6 +316,9 @@ struct ScanArgs {
   uint32_t* flags;       // the call's flag words (kFlag*)
   uint32_t* host;        // non-NULL: the call's pinned flag words (device view); k_scan then
                          // hands the flags over and clears them (the call's last flag writer)
+  int64_t* host_counts;  // non-NULL: pinned words (device view) that also get the counts, and at
+                         // [n_pairs] the call's error bits (a streamed chunk's check before its
+                         // delivery)
   uint32_t n_pairs;
 };
 struct MoveArgs {

@@ -139,6 +139,7 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs A) {
     for (int k = 0; k < kScanPer; ++k)
       if (i0 + k < A.n_pairs) {
         A.pair_count[i0 + k] = c[k];
+        if (A.host_counts) A.host_counts[i0 + k] = c[k];
         A.pair_offset[i0 + k] = (int64_t)at;
         at += c[k];
       }
@@ -153,6 +154,9 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs A) {
     uint32_t m = 0;
     for (int k = 0; k < kScanThreads / kWave; ++k) m = max(m, wmax[k]);
     A.pair_offset[A.n_pairs] = (int64_t)carry;
+    if (A.host_counts)
+      A.host_counts[A.n_pairs] =
+          __hip_atomic_load(A.flags + kFlagErr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     raise_max(A.flags + kFlagMax, m);
     __hip_atomic_store((uint64_t*)(A.flags + kFlagTotal), carry, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);

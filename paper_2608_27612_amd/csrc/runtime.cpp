@@ -997,7 +997,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
                         float theta, const emr_result* out, float* raw, void* workspace,
                         hipStream_t s, int64_t tile_lo, int64_t n_tiles, bool jit,
                         uint32_t* flags, uint32_t* flags_host, bool finalize, bool clear,
-                        bool may_alloc = true) {
+                        bool may_alloc = true, int64_t* host_counts = nullptr) {
   char* ws = (char*)workspace;
   const char* tables = T.tables;
   const uint32_t* geo_tab = T.geo;
@@ -1117,6 +1117,7 @@ emr_status launch_range(const emr_population* pop, const Plan& P, const CallTabl
     S.pair_offset = out->pair_offset;
     S.flags = flags;
     S.host = finalize ? flags_host : nullptr;  // k_scan then ends the call's flag writes
+    S.host_counts = host_counts;
     S.n_pairs = (uint32_t)P.n_pairs;
     emr::MoveArgs M{};
     M.status = (const uint64_t*)(ws + P.off_status);
@@ -1596,6 +1597,7 @@ struct StreamSet {
   uint32_t* g_parent[2] = {};       // each chunk's records (CSR), double buffered
   float* g_w4[2] = {};
   int64_t* counts_h[2] = {};        // pinned: a chunk's counts, then its error flags (one word)
+  int64_t* counts_h_dev[2] = {};    // the same words, device view (k_scan writes them)
   uint32_t* stage_parent[2] = {};   // pinned staging of a chunk's records
   float* stage_w4[2] = {};
   int64_t stage_cap[2] = {0, 0};
@@ -1728,11 +1730,13 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     for (int b = 0; b < 2; ++b) {
       if (R.counts_h[b]) (void)hipHostFree(R.counts_h[b]);
       R.counts_h[b] = nullptr;
+      R.counts_h_dev[b] = nullptr;
     }
     R.counts_h_pairs = 0;
     for (int b = 0; b < 2; ++b)
       if (hipHostMalloc((void**)&R.counts_h[b], (size_t)(n_pairs + 1) * 8, hipHostMallocDefault) !=
-          hipSuccess)
+              hipSuccess ||
+          hipHostGetDevicePointer((void**)&R.counts_h_dev[b], R.counts_h[b], 0) != hipSuccess)
         return fail(EMR_E_NOMEM, "pinned counts of a streamed call");
     R.counts_h_pairs = n_pairs + 1;
   }
@@ -1756,15 +1760,10 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     const int64_t tile_lo = c * tpc, n = std::min<int64_t>(tpc, P.tiles - tile_lo);
     emr_result chunk_out{R.g_parent[b], R.g_w4[b], records, R.counts, R.offsets, R.ws,
                          R.ws_bytes};
+    // k_scan also writes the chunk's counts and the call's error bits to the pinned words
     emr_status e = launch_range(pop, P, T, theta, &chunk_out, nullptr, R.ws, R.s, tile_lo, n, jit,
-                                f.dev, f.host_dev, false, true);
+                                f.dev, f.host_dev, false, true, true, R.counts_h_dev[b]);
     if (e != EMR_OK) return e;
-    if (n_pairs > 0)
-      HIP_OR_FAIL(hipMemcpyAsync(R.counts_h[b], R.counts, (size_t)n_pairs * 8,
-                                 hipMemcpyDeviceToHost, R.s));
-    R.counts_h[b][n_pairs] = 0;
-    HIP_OR_FAIL(hipMemcpyAsync(R.counts_h[b] + n_pairs, f.dev + emr::kFlagErr, 4,
-                               hipMemcpyDeviceToHost, R.s));
     HIP_OR_FAIL(hipEventRecord(R.ev_count[b], R.s));
     return EMR_OK;
   };

@@ -26,6 +26,8 @@ namespace emr {
 namespace {
 
 using Slot = std::pair<double, uint32_t>;  // (load, index): the least load, then the lowest index
+// Domains are used only when no key holds more than this share of a domain's mean load.
+constexpr double kMaxKeyShare = 0.1;
 using MinHeap = std::priority_queue<Slot, std::vector<Slot>, std::greater<Slot>>;
 
 // Chunks `order` (already in decreasing cost) onto the waves `ws`, appending to lists[w].
@@ -79,6 +81,15 @@ bool lpt_schedule(const float* cost, const uint32_t* key, uint32_t n_keys, uint3
       if (total[k] > 0.0) korder.push_back(k);
     std::stable_sort(korder.begin(), korder.end(),
                      [&](uint32_t a, uint32_t b) { return total[a] > total[b]; });
+    // Keys too large to balance over the domains (a call with few groups) would leave domains
+    // idle: then the chunks are placed over all waves as one domain.
+    double sum = 0.0, biggest = 0.0;
+    for (uint32_t k : korder) {
+      sum += total[k];
+      biggest = std::max(biggest, total[k]);
+    }
+    if (biggest > kMaxKeyShare * sum / domains)
+      return lpt_schedule(cost, key, n_keys, n, waves, domain_waves, 1u, table, stride);
     std::vector<uint32_t> dom(n_keys, 0u);
     std::vector<double> load(domains, 0.0);
     for (uint32_t k : korder) {

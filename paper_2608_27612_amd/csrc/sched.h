@@ -11,7 +11,8 @@ namespace emr {
 //  - the waves form `domains` domains: wave w belongs to domain (w / domain_waves) % domains;
 //  - chunks with the same key[c] (< n_keys) all go to one domain: keys in order of decreasing
 //    total cost (equal totals by key), each to the domain with the least load per wave so far
-//    (equal: the lowest domain);
+//    (equal: the lowest domain); when a key holds more than a tenth of a domain's mean load (few
+//    keys), the domains could not be balanced and all waves form one domain instead;
 //  - within a domain (or over all waves when domains <= 1), chunks in order of decreasing cost
 //    (equal costs by index), each to the wave with the least load so far (equal: the lowest wave).
 // The result is a table of `waves` rows of *stride entries (stride a multiple of 64, at least 64):

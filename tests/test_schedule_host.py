@@ -86,7 +86,7 @@ def test_domains_keep_keys_together_and_balance():
     # follow the one-level rule over its own waves
     rng = np.random.default_rng(11)
     n_groups, per = 400, 11
-    gcost = rng.lognormal(3.0, 1.0, n_groups)
+    gcost = rng.lognormal(3.0, 0.4, n_groups)  # no group above a tenth of a domain's load
     key = np.repeat(np.arange(n_groups), per)
     cost = (np.repeat(gcost, per) * rng.uniform(0.9, 1.1, key.size)).astype(np.float32)
     waves = 4 * 96
@@ -121,3 +121,18 @@ def test_schedule_rejects_bad_input():
     assert lpt(np.array([1.0, np.nan]), 2)[0] == -1
     assert lpt(np.array([1.0, -1.0]), 2)[0] == -1
     assert lpt(np.array([1.0, np.inf]), 2)[0] == -1
+
+
+def test_few_large_keys_use_all_waves():
+    # 4 keys (a call with 4 groups) over 8 domains: one domain per key would idle half the waves,
+    # so the placement uses every wave (the one-level rule)
+    rng = np.random.default_rng(21)
+    key = np.repeat(np.arange(4), 500)
+    cost = rng.uniform(90, 110, key.size).astype(np.float32)
+    waves = 4 * 64
+    rc, t = lpt(cost, waves, key, 4, 8)
+    assert rc == 0
+    assert (t[:, 0] != NO_CHUNK).all()  # every wave has work
+    want = brute_lpt(cost, waves)
+    for w in range(waves):
+        assert [int(c) for c in t[w] if c != NO_CHUNK] == want[w]
