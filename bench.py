@@ -29,8 +29,10 @@ is resident in HBM before timing starts. Printed as one JSON line:
                programs on its second call, so the warm-up compiles them): count, machine-code
                bytes, host compile and module-load times
   sub          the other measured workloads, each with the same per-step figures: the population
-               at depth 8, the tabular population (33 sources, depth 6) and the single deep CPPN
-               streamed at depth 13 (emr_discover_stream, one step = one streamed call)
+               at depth 8, the tabular population (33 sources, depth 6), the single deep CPPN
+               streamed at depth 13 (emr_discover_stream, one step = one streamed call), and
+               the same CPPN at depth 14 streamed to a record file on disk (one step = open,
+               streamed call, flush, sync and close)
   cpu_baseline the CPU oracle on a bounded, stated sample of the same workload, the host CPU, the
                oracle's one-thread rates on three small workloads, and a sample of every sub workload
 """
@@ -41,6 +43,7 @@ import argparse
 import json
 import os
 import sys
+import tempfile
 import time
 
 import numpy as np
@@ -150,11 +153,14 @@ def measure_call(emr, torch, name, steps, warmup, rT):
     return out, (pop, res, genomes, sources, depth, theta32, work)
 
 
-def measure_stream(emr, torch, name, steps, warmup, rT):
-    """A workload discovered with emr_discover_stream (records counted by the sink) per step. (The
-    default policy compiles a plan's programs on its second call: the warm-up covers that.)"""
+def measure_stream(emr, torch, name, steps, warmup, rT, depth=None, to_disk=None):
+    """A workload discovered with emr_discover_stream per step: records counted by a Python sink,
+    or, with to_disk (a directory), written to a record file there by the library's file sink
+    (open, stream, flush, sync and close inside the step). (The default policy compiles a plan's
+    programs on its second call: the warm-up covers that.)"""
     from paper_2608_27612_amd import workloads as W
-    genomes, sources, depth, theta = W.workload(name)
+    genomes, sources, wl_depth, theta = W.workload(name)
+    depth = wl_depth if depth is None else depth
     theta32 = float(np.float32(theta))
     pop = emr.emr_pack_population(genomes)
     work = emr.emr_discover_work(pop, sources, depth, transcendental_slots=rT)
@@ -165,7 +171,15 @@ def measure_stream(emr, torch, name, steps, warmup, rT):
 
     def step():
         kept[0] = 0
-        emr.emr_discover_stream(pop, sources, depth, theta32, sink)
+        if to_disk is None:
+            emr.emr_discover_stream(pop, sources, depth, theta32, sink)
+            return
+        path = os.path.join(to_disk, "%s_d%d.rec" % (name, depth))
+        f = emr.RecordFile(path, len(genomes) * len(sources))
+        try:
+            emr.emr_discover_stream(pop, sources, depth, theta32, f)
+        finally:
+            kept[0] = f.close()[0]
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
@@ -184,7 +198,9 @@ def measure_stream(emr, torch, name, steps, warmup, rT):
     emr.emr_profile_enable(False)
     kms = sum(r["ms"] for r in recs) / steps  # every chunk's launch of a call
     kernel = "emr_discover_jit_records" if all(r["compiled"] for r in recs) else "k_discover<1>"
-    return {"workload": name + " (streamed)", "genomes": len(genomes), "sources": len(sources),
+    label = name if depth == wl_depth else "%s_d%d" % (name, depth)
+    label += " (streamed)" if to_disk is None else " (streamed to disk)"
+    return {"workload": label, "genomes": len(genomes), "sources": len(sources),
             "depth": depth, "theta": theta, "steps": steps, "ms_per_step": ms,
             "launches_per_step": len(recs) // steps,
             "queries_per_step": int(work["queries"]), "records_per_step": kept[0],
@@ -336,6 +352,10 @@ def main():
         line, inp = measure_stream(emr, torch, "deep_single", 5, 3, rT)
         subs.append(line)
         sub_inputs["deep_single"] = inp
+        with tempfile.TemporaryDirectory() as tmp:
+            line, inp = measure_stream(emr, torch, "deep_single", 3, 2, rT, depth=14, to_disk=tmp)
+        subs.append(line)
+        sub_inputs["deep_single_d14"] = inp
 
     line = {
         "metric": METRIC,

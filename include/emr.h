@@ -44,7 +44,8 @@ typedef enum {
   EMR_E_NOMEM = -4,    /* host or device allocation failed */
   EMR_E_CAPACITY = -5, /* some pair found more records than the output region holds */
   EMR_E_DEVICE = -6,   /* a HIP runtime call failed, or no gfx950 device */
-  EMR_E_ABORTED = -7   /* a streaming sink asked to stop */
+  EMR_E_ABORTED = -7,  /* a streaming sink asked to stop */
+  EMR_E_IO = -8        /* a file could not be read or written */
 } emr_status;
 
 /* Message for the calling thread's last failed call ("" if none). */
@@ -331,6 +332,37 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
                                int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
                                int32_t depth, float theta, int64_t chunk_positions, int64_t start,
                                emr_sink sink, void* user, int64_t* next, void* stream);
+
+/* ------------------------------------------------------------------ record files
+ * A sink that writes a streamed run to a file, so the output of a deep run is bounded by the disk
+ * rather than by host memory (Section 6: the depth-13 substrates streamed from disk), and a run
+ * that stopped resumes where the file ends. Host only; one handle serves one run at a time.
+ *
+ * File layout (little-endian): a 32-byte header {char magic[8] = "EMRRECv1", int64 n_pairs,
+ * int64 0, int64 0}; then one block per delivery, in increasing cursor order:
+ * {int64 pair, int64 chunk, int64 n (>= 1)}, uint32 parent[n], float w4[4 n] (as delivered). */
+typedef struct emr_record_file emr_record_file;
+
+/* Opens `path` for a run over n_pairs pairs (the streamed call's: genomes x shared sources, or
+ * the total of the per-genome sources). resume = 0 creates or truncates the file. resume = 1 keeps
+ * an existing file's whole deliveries (a trailing partial block, left by a run that died while
+ * writing, is cut off) and sets *cursor (may be NULL) to the cursor after the last one: pass it
+ * as emr_discover_stream's `start`; a missing file is created (*cursor = 0). buffer_bytes is the
+ * host write buffer (0: 8 MiB; at most 2^30). *out receives the handle.
+ * EMR_E_INVAL (bad arguments, not a record file, another n_pairs, malformed blocks), EMR_E_IO. */
+emr_status emr_record_file_open(const char* path, int64_t n_pairs, int32_t resume,
+                                int64_t buffer_bytes, emr_record_file** out, int64_t* cursor);
+
+/* The emr_sink that appends a delivery to the file; `user` is the handle. Refuses (returns 1) a
+ * delivery whose cursor precedes the file's end, a malformed delivery, and every delivery after a
+ * failed write or a refusal; the reason is reported by emr_record_file_close. */
+int32_t emr_record_file_sink(int64_t pair, int64_t chunk, const uint32_t* parent, const float* w4,
+                             int64_t n_records, void* user);
+
+/* Flushes, syncs and closes the file and frees the handle (always). *records and *next (either
+ * may be NULL) receive the records in the file and the cursor after its last delivery.
+ * EMR_E_IO when a write failed, EMR_E_INVAL when a delivery was refused, else EMR_OK. */
+emr_status emr_record_file_close(emr_record_file* file, int64_t* records, int64_t* next);
 
 /*
  * Raw CPPN outputs (debug and parity): out_dev[r * N(D) + p] = CPPN output of pair r at grid

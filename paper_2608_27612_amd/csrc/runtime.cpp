@@ -1173,6 +1173,14 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
 
 }  // namespace
 
+namespace emr {
+// Sets the calling thread's last error from other host modules of the library.
+emr_status set_error(emr_status st, const std::string& msg) {
+  g_err = msg;
+  return st;
+}
+}  // namespace emr
+
 extern "C" {
 
 const char* emr_last_error(void) { return g_err.c_str(); }

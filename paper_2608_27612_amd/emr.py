@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libemr.so")
 
 EMR_OK, EMR_E_INVAL, EMR_E_CYCLE, EMR_E_LIMIT, EMR_E_NOMEM, EMR_E_CAPACITY, EMR_E_DEVICE, \
-    EMR_E_ABORTED = 0, -1, -2, -3, -4, -5, -6, -7
+    EMR_E_ABORTED, EMR_E_IO = 0, -1, -2, -3, -4, -5, -6, -7, -8
 EMR_DIR_OUT, EMR_DIR_IN = 0, 1
 EMR_MAX_DEPTH = 15
 
@@ -28,7 +28,8 @@ ABI_FUNCTIONS = [
     "emr_profile_read", "emr_stream_chunks", "emr_discover_stream", "emr_pack_population_flat",
     "emr_set_jit", "emr_jit_info", "emr_eval_raw_noalloc", "emr_call_check", "emr_cell_words",
     "emr_hidden_workspace_bytes", "emr_hidden_sources", "emr_express_workspace_bytes",
-    "emr_express", "emr_chain_workspace_bytes", "emr_chain_filter",
+    "emr_express", "emr_chain_workspace_bytes", "emr_chain_filter", "emr_record_file_open",
+    "emr_record_file_sink", "emr_record_file_close",
 ]
 EMR_CONN_FORWARD, EMR_CONN_BACKWARD, EMR_CONN_LATERAL, EMR_CONN_SELF, EMR_CONN_ALL = 1, 2, 4, 8, 15
 EMR_NOALLOC_SCRATCH_BYTES = 32 << 20
@@ -122,6 +123,9 @@ def lib():
             "emr_express": (I32, [P, P, I32, P, I32, I32, P, I32, F32, P, P]),
             "emr_chain_workspace_bytes": (I32, [I64, I32, P]),
             "emr_chain_filter": (I32, [P, I64, I32, P, P]),
+            "emr_record_file_open": (I32, [C.c_char_p, I64, I32, I64, P, P]),
+            "emr_record_file_sink": (I32, [I64, I64, P, P, I64, P]),
+            "emr_record_file_close": (I32, [P, P, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -498,13 +502,61 @@ def emr_stream_chunks(depth: int, chunk_positions: int = 1 << 24) -> int:
     return n.value
 
 
+class RecordFile:
+    """A record file opened by emr_record_file_open; pass it as emr_discover_stream's sink to
+    write the run to disk. `cursor` is where a resumed run starts (0 for a new file)."""
+
+    def __init__(self, path: str, n_pairs: int, resume: bool = False, buffer_bytes: int = 0):
+        h, cur = C.c_void_p(), C.c_int64()
+        _check(lib().emr_record_file_open(os.fsencode(path), n_pairs, int(bool(resume)),
+                                          buffer_bytes, C.byref(h), C.byref(cur)))
+        self.handle, self.cursor, self.path = h, cur.value, path
+
+    def close(self):
+        """Closes the file: (records in the file, cursor after its last delivery)."""
+        if self.handle is None:
+            raise ValueError("record file already closed")
+        recs, nxt = C.c_int64(), C.c_int64()
+        h, self.handle = self.handle, None
+        _check(lib().emr_record_file_close(h, C.byref(recs), C.byref(nxt)))
+        return recs.value, nxt.value
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        if self.handle is not None:
+            self.close()
+
+
+def read_record_file(path: str):
+    """Reads a record file (layout in include/emr.h): (n_pairs, [(pair, chunk, parent uint32 [n],
+    w4 float32 [n, 4]), ...]) in file order. A trailing partial block is ignored."""
+    data = np.fromfile(path, dtype=np.uint8)
+    if len(data) < 32 or bytes(data[:8]) != b"EMRRECv1":
+        raise ValueError("%s is not a record file" % path)
+    n_pairs = int(data[8:16].view(np.int64)[0])
+    blocks, pos = [], 32
+    while pos + 24 <= len(data):
+        pair, chunk, n = (int(v) for v in data[pos:pos + 24].view(np.int64))
+        end = pos + 24 + 20 * n
+        if n < 1 or end > len(data):
+            break
+        parent = data[pos + 24:pos + 24 + 4 * n].view(np.uint32).copy()
+        w4 = data[pos + 24 + 4 * n:end].view(np.float32).reshape(n, 4).copy()
+        blocks.append((pair, chunk, parent, w4))
+        pos = end
+    return n_pairs, blocks
+
+
 def emr_discover_stream(pop: Population, sources, depth: int, theta: float, sink,
                         chunk_positions: int = 1 << 24, start: int = 0, src_offsets=None,
                         stream=None) -> int:
     """Streamed eager discovery. `sink(pair, chunk, parent, w4)` receives numpy copies of each
     (chunk, pair) delivery (parent uint32 [n], w4 float32 [n, 4]) and returns True/None to go on,
-    False to stop. Returns the cursor after the run; a stop raises EmrError(EMR_E_ABORTED) whose
-    `next_cursor` is the refused delivery's cursor (see emr_discover_stream in include/emr.h)."""
+    False to stop; or `sink` is a RecordFile, whose C sink writes the deliveries to its file.
+    Returns the cursor after the run; a stop raises EmrError(EMR_E_ABORTED) whose `next_cursor` is
+    the refused delivery's cursor (see emr_discover_stream in include/emr.h)."""
     offs = _offsets(src_offsets)
     errors = []
 
@@ -517,13 +569,18 @@ def emr_discover_stream(pop: Population, sources, depth: int, theta: float, sink
             errors.append(e)
             return 1
 
-    cb = SINK(_sink)
+    if isinstance(sink, RecordFile):
+        if sink.handle is None:
+            raise ValueError("record file is closed")
+        cb, user = SINK(("emr_record_file_sink", lib())), sink.handle
+    else:
+        cb, user = SINK(_sink), None
     nxt = C.c_int64(start)
     src = _sources(sources)
     st = lib().emr_discover_stream(pop.handle, src.ctypes.data, len(sources),
                                    None if offs is None else offs.ctypes.data,
                                    0 if offs is not None else len(sources), depth,
-                                   C.c_float(theta), chunk_positions, start, cb, None,
+                                   C.c_float(theta), chunk_positions, start, cb, user,
                                    C.byref(nxt), _stream_ptr(stream))
     if errors:
         raise errors[0]

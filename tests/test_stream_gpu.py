@@ -168,6 +168,32 @@ def test_stream_deep_single_depth9_matches_oracle(emr):
         assert close(w[gi], ow[oi]).all(), r
 
 
+def check_deep_against_oracle(genome, sources, D, theta32, parents, samples, rng):
+    """Per pair: the delivered parents (a list of ascending arrays) are increasing across
+    deliveries and at most Q(D); the sampled records (parent, w4) match the oracle evaluated cell
+    by cell and pass theta; random parents are delivered exactly when the oracle's variance is
+    above theta (outside the band around it). Returns the records delivered."""
+    Q = oracle.n_parents(D)
+    kept_total = 0
+    for r in range(len(sources)):
+        allp = np.concatenate(parents[r]) if parents[r] else np.zeros(0, np.uint32)
+        assert np.all(np.diff(allp.astype(np.int64)) > 0)
+        assert len(allp) <= Q and (len(allp) == 0 or int(allp[-1]) < Q)
+        if samples[r]:
+            p = np.concatenate([a for a, _ in samples[r]])
+            w = np.concatenate([b for _, b in samples[r]])
+            ow, ovar = oracle.eval_parents(genome, sources[r], p)
+            assert np.all(ovar > theta32 - BAND)
+            assert close(w, ow).all(), r
+        cand = np.unique(rng.integers(0, Q, size=4000)).astype(np.uint32)
+        _, cvar = oracle.eval_parents(genome, sources[r], cand)
+        delivered = np.isin(cand, allp)
+        assert np.all(delivered[cvar > theta32 + BAND])
+        assert not np.any(delivered[cvar < theta32 - BAND])
+        kept_total += len(allp)
+    return kept_total
+
+
 def test_stream_deep_single_depth13_sampled(emr):
     """The depth-13 streamed run (one CPPN with 30 hidden nodes and 90 edges, 4 sources, 358M
     queries, chunks of 2^24 positions): every delivery is well formed, sampled kept records match
@@ -182,9 +208,6 @@ def test_stream_deep_single_depth13_sampled(emr):
     samples = {r: [] for r in range(len(sources))}
 
     def sink(pair, chunk, parent, w4):
-        assert np.all(np.diff(parent.astype(np.int64)) > 0)
-        if parents[pair]:
-            assert parent[0] > parents[pair][-1][-1]
         parents[pair].append(parent)
         take = rng.choice(len(parent), size=min(40, len(parent)), replace=False)
         samples[pair].append((parent[take], w4[take]))
@@ -192,21 +215,72 @@ def test_stream_deep_single_depth13_sampled(emr):
 
     nxt = emr.emr_discover_stream(pop, sources, D, theta32, sink, chunk_positions=1 << 24)
     assert nxt == emr.emr_stream_chunks(D, 1 << 24) * len(sources)
-    Q = oracle.n_parents(D)
-    kept_total = 0
-    for r in range(len(sources)):
-        allp = np.concatenate(parents[r]) if parents[r] else np.zeros(0, np.uint32)
-        assert len(allp) <= Q
-        if samples[r]:
-            p = np.concatenate([a for a, _ in samples[r]])
-            w = np.concatenate([b for _, b in samples[r]])
-            ow, ovar = oracle.eval_parents(genomes[0], sources[r], p)
-            assert np.all(ovar > theta32 - BAND)
-            assert close(w, ow).all(), r
-        cand = np.unique(rng.integers(0, Q, size=4000)).astype(np.uint32)
-        _, cvar = oracle.eval_parents(genomes[0], sources[r], cand)
-        delivered = np.isin(cand, allp)
-        assert np.all(delivered[cvar > theta32 + BAND])
-        assert not np.any(delivered[cvar < theta32 - BAND])
-        kept_total += len(allp)
-    assert kept_total > 0
+    assert check_deep_against_oracle(genomes[0], sources, D, theta32, parents, samples, rng) > 0
+
+
+def test_stream_to_record_file_and_resume(emr, tmp_path):
+    """A run written by the record-file sink holds exactly the deliveries a Python sink receives;
+    a file cut inside a block (a run that died while writing) resumes at its last whole delivery,
+    and the resumed run completes the same file byte for byte."""
+    genomes = W.population(35, 40, 20, 60)
+    sources = W.xor_sources()
+    D, theta, chunk = 7, float(np.float32(0.02)), 256 * 16
+    pop = emr.emr_pack_population(genomes)
+    n_pairs = len(genomes) * len(sources)
+    got, order, total = collect(emr, pop, sources, D, theta, chunk)
+    path = str(tmp_path / "run.rec")
+    with emr.RecordFile(path, n_pairs) as f:
+        assert emr.emr_discover_stream(pop, sources, D, theta, f, chunk_positions=chunk) == total
+    n, blocks = emr.read_record_file(path)
+    assert n == n_pairs
+    assert [(c, r) for r, c, _, _ in blocks] == order
+    seen = {}
+    for r, c, p, w in blocks:
+        k = seen.get(r, 0)
+        c0, p0, w0 = got[r][k]
+        assert c == c0
+        np.testing.assert_array_equal(p, p0)
+        np.testing.assert_array_equal(w, w0)
+        seen[r] = k + 1
+    full = open(path, "rb").read()
+    cut_block = len(blocks) // 2
+    start = 32 + sum(24 + 20 * len(b[2]) for b in blocks[:cut_block])
+    with open(path, "r+b") as fh:
+        fh.truncate(start + 24 + 8)
+    f = emr.RecordFile(path, n_pairs, resume=True)
+    r_, c_ = blocks[cut_block - 1][0], blocks[cut_block - 1][1]
+    assert f.cursor == c_ * n_pairs + r_ + 1
+    assert emr.emr_discover_stream(pop, sources, D, theta, f, chunk_positions=chunk,
+                                   start=f.cursor) == total
+    recs, nxt = f.close()
+    assert open(path, "rb").read() == full
+    assert recs == sum(len(b[2]) for b in blocks)
+    # resuming a complete file delivers nothing more
+    with emr.RecordFile(path, n_pairs, resume=True) as f:
+        assert emr.emr_discover_stream(pop, sources, D, theta, f, chunk_positions=chunk,
+                                       start=f.cursor) == total
+    assert open(path, "rb").read() == full
+
+
+def test_stream_deep_single_depth14_to_disk(emr, tmp_path):
+    """The same CPPN and sources at depth 14 (358M positions per source: the paper's depth-13
+    substrate; 1.43G queries) streamed to a record file on disk in chunks of 2^24 positions, then
+    read back and checked against the oracle on sampled records and sampled parents."""
+    genomes, sources, _, theta = W.workload("deep_single")
+    D = 14
+    theta32 = float(np.float32(theta))
+    pop = emr.emr_pack_population(genomes)
+    path = str(tmp_path / "d14.rec")
+    with emr.RecordFile(path, len(sources)) as f:
+        nxt = emr.emr_discover_stream(pop, sources, D, theta32, f, chunk_positions=1 << 24)
+    assert nxt == emr.emr_stream_chunks(D, 1 << 24) * len(sources)
+    n, blocks = emr.read_record_file(path)
+    assert n == len(sources)
+    rng = np.random.default_rng(14)
+    parents = {r: [] for r in range(len(sources))}
+    samples = {r: [] for r in range(len(sources))}
+    for r, c, p, w in blocks:
+        parents[r].append(p)
+        take = rng.choice(len(p), size=min(40, len(p)), replace=False)
+        samples[r].append((p[take], w[take]))
+    assert check_deep_against_oracle(genomes[0], sources, D, theta32, parents, samples, rng) > 0
