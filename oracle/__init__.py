@@ -370,3 +370,175 @@ def express(records, sources, depth: int, type_mask: int, w_min: float, n_genome
     np.cumsum(counts, out=pair_offset[1:])
     return {"pair_count": counts, "pair_offset": pair_offset,
             "cell": np.array(cells, np.int64), "w": np.array(ws, np.float64)}
+
+
+# ----------------------------------------------------------------------------- networks
+# The networks the experiments evaluate (Section 5: XOR over its four input patterns), built from
+# the discovered substrate. The paper does not spell out this construction; the oracle follows
+# ES-HyperNEAT's: substrate nodes plus the hidden nodes of Phase 1 and the hidden-to-hidden
+# phase, connected by the expressed connections, then cut down to the nodes that lie on a path
+# from an input to an output, and activated synchronously for a fixed number of steps with the
+# sigmoid on every non-input node.
+
+def sigmoid(z):
+    """1 / (1 + e^-z), elementwise, float64."""
+    z = np.asarray(z, np.float64)
+    out = np.empty_like(z)
+    pos = z >= 0
+    out[pos] = 1.0 / (1.0 + np.exp(-z[pos]))
+    ez = np.exp(z[~pos])
+    out[~pos] = ez / (1.0 + ez)
+    return out
+
+
+def network_phases(genomes, substrate, depth: int, theta: float, iterations: int):
+    """Phase 1 on the substrate sources, then up to `iterations` hidden-to-hidden phases, each
+    querying the hidden nodes the previous phase found (and only those) as outgoing sources; it
+    stops early when no genome found a new node. Returns (phases, known): phases[k] =
+    dict(records, sources, src_offsets, cells) (cells: per genome the hidden cells queried in
+    phase k, None for the substrate phase), known[g] = every hidden cell of genome g, ascending
+    (the children of the kept parents of every outgoing pair of every phase)."""
+    G = len(genomes)
+    rec = discover(genomes, substrate, depth, theta)
+    phases = [{"records": rec, "sources": substrate, "src_offsets": None, "cells": None}]
+    new = hidden_cells(rec, G, substrate)
+    known = [c.copy() for c in new]
+    for _ in range(iterations):
+        if not any(len(c) for c in new):
+            break
+        src, offs = sources_at_cells(new, depth)
+        rec = discover(genomes, src, depth, theta, src_offsets=offs)
+        phases.append({"records": rec, "sources": src, "src_offsets": offs, "cells": new})
+        new = hidden_cells(rec, G, src, offs, exclude=known)
+        known = [np.union1d(k, n) for k, n in zip(known, new)]
+    return phases, known
+
+
+def reachable(n_nodes: int, edges, seeds):
+    """Boolean mask of the nodes reachable from `seeds` along the directed (u, v) edges."""
+    adj = [[] for _ in range(n_nodes)]
+    for u, v in edges:
+        adj[u].append(v)
+    seen = np.zeros(n_nodes, bool)
+    stack = list(seeds)
+    for s in stack:
+        seen[s] = True
+    while stack:
+        u = stack.pop()
+        for v in adj[u]:
+            if not seen[v]:
+                seen[v] = True
+                stack.append(v)
+    return seen
+
+
+def prune(n_nodes: int, inputs, outputs, edges):
+    """(node mask, edge mask): a node stays when it is an input or an output, or when it can be
+    reached from an input and can reach an output; an edge u -> v stays when u can be reached from
+    an input and v can reach an output (so it lies on an input-to-output path)."""
+    fwd = reachable(n_nodes, edges, inputs)
+    bwd = reachable(n_nodes, [(v, u) for u, v in edges], outputs)
+    node = fwd & bwd
+    node[list(inputs)] = True
+    node[list(outputs)] = True
+    emask = np.array([bool(fwd[u] and bwd[v]) for u, v in edges], bool)
+    return node, emask
+
+
+def assemble(n_genomes: int, substrate, depth: int, phases, known, type_mask: int, w_min: float):
+    """The pruned networks. Per genome, before pruning: node j < n_sub is substrate source j, node
+    n_sub + i is the hidden cell known[g][i]; every connection the phases express (express(), with
+    type_mask and w_min) is an edge between the source's node (a substrate node in phase 0, the
+    queried hidden cell's node later) and the grid cell's node, in the connection's direction; a
+    connection whose grid cell is not a hidden node (an incoming source's cell that no outgoing
+    pair reached) is dropped. Then prune(). Returns per genome dict(cells: the kept hidden cells
+    ascending (node n_sub + i is cells[i]), src, dst, w: the kept edges with the kept nodes'
+    numbers, in the order phase, pair, cell)."""
+    n_sub = len(substrate)
+    inputs = [j for j in range(n_sub) if int(substrate[j]["dir"]) == 0]
+    outputs = [j for j in range(n_sub) if int(substrate[j]["dir"]) != 0]
+    raw = [[] for _ in range(n_genomes)]
+    for ph in phases:
+        offs = ph["src_offsets"]
+        conn = express(ph["records"], ph["sources"], depth, type_mask, w_min, n_genomes, offs)
+        gen, src = _pair_sources(ph["sources"], n_genomes, offs)
+        for r in range(len(conn["pair_count"])):
+            g, j = int(gen[r]), int(src[r])
+            if ph["cells"] is None:
+                s_node, d = j, int(substrate[j]["dir"])
+            else:
+                cell = int(ph["cells"][g][j - int(offs[g])])
+                s_node, d = n_sub + int(np.searchsorted(known[g], cell)), 0
+            for i in range(int(conn["pair_offset"][r]), int(conn["pair_offset"][r + 1])):
+                c = int(conn["cell"][i])
+                pos = int(np.searchsorted(known[g], c))
+                if pos == len(known[g]) or int(known[g][pos]) != c:
+                    continue
+                c_node = n_sub + pos
+                raw[g].append((s_node, c_node, float(conn["w"][i])) if d == 0
+                              else (c_node, s_node, float(conn["w"][i])))
+    nets = []
+    for g in range(n_genomes):
+        n = n_sub + len(known[g])
+        edges = [(u, v) for u, v, _ in raw[g]]
+        node, emask = prune(n, inputs, outputs, edges)
+        new_id = np.cumsum(node) - 1
+        e = [(int(new_id[u]), int(new_id[v]), w) for (u, v, w), k in zip(raw[g], emask) if k]
+        nets.append({"cells": np.asarray(known[g], np.int64)[node[n_sub:]],
+                     "src": np.array([x[0] for x in e], np.int64),
+                     "dst": np.array([x[1] for x in e], np.int64),
+                     "w": np.array([x[2] for x in e], np.float64)})
+    return nets
+
+
+def build_networks(genomes, substrate, depth: int, theta: float, type_mask: int, w_min: float,
+                   iterations: int):
+    """network_phases() then assemble(), all from this oracle's own float64 discovery."""
+    phases, known = network_phases(genomes, substrate, depth, theta, iterations)
+    return assemble(len(genomes), substrate, depth, phases, known, type_mask, w_min)
+
+
+def activate(net, substrate, inputs, steps: int):
+    """Outputs [n_patterns, n_outputs] of one network after `steps` synchronous updates: the input
+    nodes (the outgoing substrate sources, in order) hold the pattern's values throughout, every
+    other node starts at 0 and takes sigmoid(sum of w * the source node's previous value) at each
+    step."""
+    n_sub = len(substrate)
+    inputs = np.atleast_2d(np.asarray(inputs, np.float64))
+    ins = [j for j in range(n_sub) if int(substrate[j]["dir"]) == 0]
+    outs = [j for j in range(n_sub) if int(substrate[j]["dir"]) != 0]
+    n = n_sub + len(net["cells"])
+    s = np.zeros((len(inputs), n))
+    s[:, ins] = inputs
+    for _ in range(steps):
+        z = np.zeros_like(s)
+        for u, v, w in zip(net["src"], net["dst"], net["w"]):
+            z[:, v] += w * s[:, u]
+        s = sigmoid(z)
+        s[:, ins] = inputs
+    return s[:, outs]
+
+
+XOR_TARGETS = np.array([0.0, 1.0, 1.0, 0.0])
+
+
+def xor_patterns(n_inputs: int, bias_input=None) -> np.ndarray:
+    """The four XOR patterns (a, b) = (0,0), (0,1), (1,0), (1,1) as input values in input order:
+    a and b are the first and second input other than `bias_input` (the bias input, held at 1;
+    None when there is none)."""
+    ab = np.array([[0, 0], [0, 1], [1, 0], [1, 1]], np.float64)
+    if n_inputs != 2 + (bias_input is not None):
+        raise ValueError("XOR needs inputs a, b and at most one bias input")
+    out = np.ones((4, n_inputs))
+    cols = [j for j in range(n_inputs) if j != bias_input]
+    out[:, cols] = ab
+    return out
+
+
+def xor_fitness(net, substrate, steps: int, bias_input=None) -> float:
+    """1 - the mean squared error of the single output over the four XOR patterns."""
+    n_in = sum(1 for s in substrate if int(s["dir"]) == 0)
+    out = activate(net, substrate, xor_patterns(n_in, bias_input), steps)
+    if out.shape[1] != 1:
+        raise ValueError("XOR needs one output")
+    return float(1.0 - np.mean((out[:, 0] - XOR_TARGETS) ** 2))
