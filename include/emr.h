@@ -364,6 +364,104 @@ int32_t emr_record_file_sink(int64_t pair, int64_t chunk, const uint32_t* parent
  * EMR_E_IO when a write failed, EMR_E_INVAL when a delivery was refused, else EMR_OK. */
 emr_status emr_record_file_close(emr_record_file* file, int64_t* records, int64_t* next);
 
+/* ------------------------------------------------------------------ networks
+ * The networks the experiments evaluate (Section 5: XOR over its four input patterns), built from
+ * each genome's discovered substrate, and their activation. The paper names the parts (Phase 1,
+ * the hidden-to-hidden phase of Section 2 and the connection types of Section 4's configurations)
+ * without spelling out the assembly; the library builds it as ES-HyperNEAT does:
+ *   - phase 0 is emr_discover on the substrate sources; its hidden nodes are the children of the
+ *     kept parents of the outgoing pairs (emr_hidden_sources);
+ *   - each further phase (at most `iterations`) queries, per genome, the hidden nodes the previous
+ *     phase found and no earlier phase had, as outgoing sources at their cell centres, and adds the
+ *     children of its kept parents that are new; it stops early when no genome finds one;
+ *   - every phase's connections are expressed with type_mask and w_min (emr_express); each is an
+ *     edge between the source's node and the grid cell's node, in the connection's direction; a
+ *     connection to a cell that is not a hidden node (an incoming source's cell that no outgoing
+ *     query reached) is dropped;
+ *   - a hidden node is kept when an input reaches it and it reaches an output; an edge u -> v when
+ *     an input reaches u and v reaches an output. Substrate nodes are always kept.
+ * Node numbers per genome: the substrate sources in substrate order (inputs are the outgoing
+ * sources, outputs the incoming ones), then the kept hidden nodes in ascending heap cell order.
+ * Activation is synchronous: input nodes hold the pattern's values, every other node starts at 0
+ * and at each step takes sigmoid(sum of w * the source node's previous value) = 1/(1+e^-z),
+ * over its incoming edges in the order phase, pair, cell. fp32. */
+typedef struct emr_networks emr_networks;
+
+#define EMR_SUBSTRATE_NODE 0xFFFFFFFFu /* node_cell of a substrate node */
+
+/* Builds the networks of every genome of `pop` for the substrate (host, n_substrate sources with
+ * at least one input and one output) at this depth and theta; type_mask (EMR_CONN_*, 1..15) and
+ * w_min filter the connections; iterations (0..64) bounds the hidden-to-hidden phases (0: the
+ * feedforward configuration without them). Runs on `stream` and synchronizes with it; *out
+ * receives a handle owning every device buffer below (free with emr_free_networks). The
+ * population's grouping tables are replaced by those of the last phase (emr_discover's rule).
+ * EMR_E_INVAL, EMR_E_LIMIT (more than 2^32 - 2 nodes), EMR_E_NOMEM, EMR_E_DEVICE, or any status of
+ * the discovery calls it makes. */
+emr_status emr_build_networks(const emr_population* pop, const emr_source* substrate,
+                              int32_t n_substrate, int32_t depth, float theta, int32_t type_mask,
+                              float w_min, int32_t iterations, emr_networks** out, void* stream);
+
+/* The networks (device pointers owned by the handle, valid until emr_free_networks). Genome g's
+ * nodes are node_offset[g] .. node_offset[g+1] - 1; node i's incoming edges are
+ * in_offset[i] .. in_offset[i+1] - 1, with in_src the source's node index (counted over all
+ * genomes) and in_w the weight. known: the hidden cells of every phase before pruning, a
+ * bitmap of known_words words per genome (bit p stands for heap cell p + 1). */
+typedef struct {
+  int32_t n_genomes, n_substrate, n_inputs, n_outputs, depth, phases;
+  int64_t nodes, edges;
+  const int64_t* node_offset; /* [n_genomes + 1] */
+  const uint32_t* node_cell;  /* [nodes]: heap cell, EMR_SUBSTRATE_NODE for substrate nodes */
+  const int64_t* in_offset;   /* [nodes + 1] */
+  const uint32_t* in_src;     /* [edges] */
+  const float* in_w;          /* [edges] */
+  const uint32_t* known;      /* [n_genomes * known_words] */
+  int64_t known_words;
+} emr_network_info;
+emr_status emr_networks_info(const emr_networks* net, emr_network_info* info);
+
+/* One phase of a build (0 .. phases - 1), for inspection: its sources (host, owned by the handle:
+ * the substrate for phase 0, else per genome the queried hidden nodes at src_offsets, with their
+ * heap cells in src_cell on the device), its checked discovery (CSR over n_pairs pairs: parent,
+ * w4, pair_offset, `records` in all) and its expressed connections (conn_cell, conn_w,
+ * conn_offset, `connections` in all). Device pointers owned by the handle. */
+typedef struct {
+  const emr_source* sources;
+  int32_t n_sources;
+  const int32_t* src_offsets; /* NULL for phase 0 */
+  const uint32_t* src_cell;   /* NULL for phase 0 */
+  int64_t n_pairs;
+  const uint32_t* parent;
+  const float* w4;
+  const int64_t* pair_offset;
+  int64_t records;
+  const uint32_t* conn_cell;
+  const float* conn_w;
+  const int64_t* conn_offset;
+  int64_t connections;
+} emr_network_phase;
+emr_status emr_networks_phase(const emr_networks* net, int32_t phase, emr_network_phase* out);
+
+/* Activates every network for n_patterns (1..65536) input patterns (host, [n_patterns][n_inputs]
+ * in input order, read during the call) for `steps` (0..2^20) synchronous steps and writes the
+ * outputs (device, caller-owned, [n_genomes][n_patterns][n_outputs]). Enqueued on `stream` (the
+ * device the networks were built on must be current). The handle's state buffers serve one call at
+ * a time: calls on one handle must be ordered on one stream. */
+emr_status emr_activate(const emr_networks* net, const float* inputs, int32_t n_patterns,
+                        int32_t steps, float* outputs, void* stream);
+
+/* XOR fitness of every network (device, caller-owned, [n_genomes]): 1 - the mean squared error of
+ * the single output over (a, b) = (0,0), (0,1), (1,0), (1,1) with targets 0, 1, 1, 0, after
+ * `steps` steps; a and b are the first and second input other than bias_input, the input held at
+ * 1 (-1: none). Needs one output and two inputs besides the bias. Enqueued like emr_activate. */
+emr_status emr_xor_fitness(const emr_networks* net, int32_t bias_input, int32_t steps,
+                           float* fitness, void* stream);
+
+void emr_free_networks(emr_networks* net);
+
+/* Copies `bytes` of device memory (such as the buffers the info calls above point to) to host
+ * memory after the work already on `stream`; returns when the copy is done. */
+emr_status emr_copy_to_host(void* host, const void* device, int64_t bytes, void* stream);
+
 /*
  * Raw CPPN outputs (debug and parity): out_dev[r * N(D) + p] = CPPN output of pair r at grid
  * position p (device, caller-owned, n_pairs * N(D) floats). Same arithmetic as emr_discover.

@@ -1,0 +1,134 @@
+// Arguments of the network kernels (network.hip), shared with their host driver (networks.cpp).
+//
+// Numbering. Before pruning, genome g has raw nodes 0 .. n_sub - 1 (its substrate sources, in
+// substrate order) and n_sub + i for the i-th set bit of its hidden-cell bitmap (ascending grid
+// position); raw node j of genome g is entry raw_node[g] + j of the per-node arrays. Its raw edges
+// (one per expressed connection of every phase, genome by genome, each genome's phases in order,
+// each phase's pairs in order, each pair's connections in cell order) are entries
+// raw_edge[g] .. raw_edge[g + 1] - 1 of eu/ev/ew, holding raw node numbers (kNoNode: the grid end
+// is not a hidden node, the edge is dropped). After pruning, the kept nodes of genome g are
+// renumbered in raw order (substrate nodes first, all kept) as entries node_offset[g] + k of the
+// network arrays, and the kept edges are grouped by destination (CSR, in_offset), each group in
+// raw order.
+#pragma once
+#include <stdint.h>
+
+namespace emr {
+
+constexpr uint32_t kNoNode = 0xFFFFFFFFu;
+constexpr int kNetThreads = 256;
+
+// Error bits of the network kernels.
+constexpr uint32_t kNetErrIndex = 1u;   // an index outside its table (a host bug; never expected)
+constexpr uint32_t kNetErrPasses = 2u;  // pruning did not settle within its bound
+
+struct NetRankArgs {
+  const uint32_t* known;  // [n_genomes * words] hidden-cell bitmaps
+  uint32_t* rank;         // [n_genomes * words] set bits of the genome's earlier words
+  uint32_t* hidden;       // [n_genomes] set bits per genome
+  int64_t words;
+  uint32_t n_genomes;
+};
+
+struct NetEdgeArgs {
+  // one phase's expressed connections (CSR over its pairs)
+  const int64_t* conn_offset;  // [n_pairs + 1]
+  const uint32_t* conn_cell;
+  const float* conn_w;
+  int64_t n_pairs;
+  int64_t total;               // conn_offset[n_pairs]
+  // the phase's pairs: shared substrate sources (src_offsets == NULL: pair = g * n_sub + j) or
+  // per-genome hidden sources (pair = source index, genome g owns src_offsets[g] .. [g + 1] - 1,
+  // source r sits at heap cell src_cell[r])
+  const int64_t* src_offsets;  // [n_genomes + 1] or NULL
+  const uint32_t* src_cell;    // [n_sources] or NULL
+  const uint8_t* sub_dir;      // [n_sub] 0: input (outgoing queries), 1: output (incoming)
+  uint32_t n_sub;
+  uint32_t n_genomes;
+  const uint32_t* known;
+  const uint32_t* rank;
+  int64_t words;
+  const int64_t* seg;          // [n_genomes] raw edge index of genome g's first edge of this phase
+  const int64_t* raw_edge;     // [n_genomes + 1]
+  uint32_t* eu;
+  uint32_t* ev;
+  float* ew;
+  uint32_t* err;
+};
+
+struct NetPruneArgs {
+  const uint8_t* sub_dir;
+  const int64_t* raw_node;  // [n_genomes + 1]
+  const int64_t* raw_edge;  // [n_genomes + 1]
+  const uint32_t* eu;
+  const uint32_t* ev;
+  uint8_t* fwd;             // [raw nodes] reachable from an input
+  uint8_t* bwd;             // [raw nodes] reaches an output
+  uint32_t* in_deg;         // [raw nodes] kept edges into the node
+  uint32_t* kept_nodes;     // [n_genomes] kept hidden nodes
+  uint32_t* kept_edges;     // [n_genomes]
+  uint32_t* err;
+  uint32_t n_sub;
+  uint32_t n_genomes;
+};
+
+struct NetNodeArgs {
+  const uint32_t* known;
+  const uint32_t* rank;
+  int64_t words;
+  const int64_t* raw_node;
+  const uint8_t* fwd;
+  const uint8_t* bwd;
+  const uint32_t* in_deg;
+  const int64_t* node_offset;  // [n_genomes + 1] kept nodes
+  const int64_t* edge_offset;  // [n_genomes + 1] kept edges
+  uint32_t* new_id;            // [raw nodes] kept number within the genome, or kNoNode
+  uint32_t* node_cell;         // [nodes] heap cell, kNoNode for substrate nodes
+  int64_t* in_offset;          // [nodes + 1]
+  uint32_t* err;
+  uint32_t n_sub;
+  uint32_t n_genomes;
+};
+
+struct NetPlaceArgs {
+  const int64_t* raw_node;
+  const int64_t* raw_edge;
+  const int64_t* node_offset;
+  const uint32_t* eu;
+  const uint32_t* ev;
+  const float* ew;
+  const uint8_t* fwd;
+  const uint8_t* bwd;
+  const uint32_t* new_id;
+  const int64_t* in_offset;
+  uint32_t* cursor;            // [nodes], zero before the launch
+  uint32_t* in_src;            // [edges] global node index of the source
+  float* in_w;                 // [edges]
+  int64_t edges;
+  uint32_t* err;
+  uint32_t n_genomes;
+};
+
+struct NetForwardArgs {
+  const int64_t* node_offset;
+  const int64_t* in_offset;
+  const uint32_t* in_src;
+  const float* in_w;
+  const int32_t* in_slot;   // [n_sub] input number of a substrate node, or -1
+  const int32_t* out_slot;  // [n_sub] output number, or -1
+  const float* patterns;    // [n_patterns * n_inputs]
+  const float* targets;     // [n_patterns] or NULL (fitness: one output)
+  float* state;             // [2 * pblocks * nodes * 4]
+  float* outputs;           // [n_genomes * n_patterns * n_outputs] or NULL
+  float* fitness;           // [n_genomes] or NULL
+  int64_t nodes;
+  uint32_t n_genomes;
+  uint32_t n_sub;
+  uint32_t n_inputs;
+  uint32_t n_outputs;
+  uint32_t n_patterns;
+  uint32_t pblocks;         // pattern blocks of 4
+  uint32_t steps;
+};
+
+}  // namespace emr

@@ -29,7 +29,9 @@ ABI_FUNCTIONS = [
     "emr_set_jit", "emr_jit_info", "emr_eval_raw_noalloc", "emr_call_check", "emr_cell_words",
     "emr_hidden_workspace_bytes", "emr_hidden_sources", "emr_express_workspace_bytes",
     "emr_express", "emr_chain_workspace_bytes", "emr_chain_filter", "emr_record_file_open",
-    "emr_record_file_sink", "emr_record_file_close",
+    "emr_record_file_sink", "emr_record_file_close", "emr_build_networks", "emr_networks_info",
+    "emr_networks_phase", "emr_activate", "emr_xor_fitness", "emr_free_networks",
+    "emr_copy_to_host",
 ]
 EMR_CONN_FORWARD, EMR_CONN_BACKWARD, EMR_CONN_LATERAL, EMR_CONN_SELF, EMR_CONN_ALL = 1, 2, 4, 8, 15
 EMR_NOALLOC_SCRATCH_BYTES = 32 << 20
@@ -75,6 +77,22 @@ class emr_launch_profile(C.Structure):
                 ("call", C.c_int32), ("tiles", C.c_int64), ("queries", C.c_int64),
                 ("slots", C.c_double), ("ms", C.c_float), ("compiled", C.c_int32),
                 ("listed", C.c_int32), ("parts", C.c_int32)]
+
+
+class emr_network_info(C.Structure):
+    _fields_ = [("n_genomes", C.c_int32), ("n_substrate", C.c_int32), ("n_inputs", C.c_int32),
+                ("n_outputs", C.c_int32), ("depth", C.c_int32), ("phases", C.c_int32),
+                ("nodes", C.c_int64), ("edges", C.c_int64), ("node_offset", C.c_void_p),
+                ("node_cell", C.c_void_p), ("in_offset", C.c_void_p), ("in_src", C.c_void_p),
+                ("in_w", C.c_void_p), ("known", C.c_void_p), ("known_words", C.c_int64)]
+
+
+class emr_network_phase(C.Structure):
+    _fields_ = [("sources", C.c_void_p), ("n_sources", C.c_int32), ("src_offsets", C.c_void_p),
+                ("src_cell", C.c_void_p), ("n_pairs", C.c_int64), ("parent", C.c_void_p),
+                ("w4", C.c_void_p), ("pair_offset", C.c_void_p), ("records", C.c_int64),
+                ("conn_cell", C.c_void_p), ("conn_w", C.c_void_p), ("conn_offset", C.c_void_p),
+                ("connections", C.c_int64)]
 
 
 _lib = None
@@ -126,6 +144,13 @@ def lib():
             "emr_record_file_open": (I32, [C.c_char_p, I64, I32, I64, P, P]),
             "emr_record_file_sink": (I32, [I64, I64, P, P, I64, P]),
             "emr_record_file_close": (I32, [P, P, P]),
+            "emr_build_networks": (I32, [P, P, I32, I32, F32, I32, F32, I32, P, P]),
+            "emr_networks_info": (I32, [P, P]),
+            "emr_networks_phase": (I32, [P, I32, P]),
+            "emr_activate": (I32, [P, P, I32, I32, P, P]),
+            "emr_xor_fitness": (I32, [P, I32, I32, P, P]),
+            "emr_free_networks": (None, [P]),
+            "emr_copy_to_host": (I32, [P, P, I64, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -711,3 +736,121 @@ def emr_chain_filter(rec, depth: int, capacity=None, stream=None):
                                   _stream_ptr(stream)))
     emr_result_check(out, stream)
     return out
+
+
+# ----------------------------------------------------------------------------- networks
+
+def _dev_to_host(ptr, n, dtype, stream=None):
+    """n elements of dtype from a library-owned device pointer (emr_copy_to_host)."""
+    out = np.empty(max(int(n), 0), dtype=dtype)
+    if n > 0:
+        _check(lib().emr_copy_to_host(out.ctypes.data, C.c_void_p(ptr), out.nbytes,
+                                      _stream_ptr(stream)))
+    return out
+
+
+class Networks:
+    """The networks of a population (owns the library's emr_networks handle)."""
+
+    def __init__(self, handle):
+        self.handle = handle
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.emr_free_networks(self.handle)
+            self.handle = None
+
+    def info(self) -> emr_network_info:
+        i = emr_network_info()
+        _check(lib().emr_networks_info(self.handle, C.byref(i)))
+        return i
+
+    def to_host(self, stream=None):
+        """Per genome dict(cells: kept hidden cells ascending, src, dst, w: the edges with the
+        genome's node numbers, grouped by destination in the library's order)."""
+        i = self.info()
+        G = i.n_genomes
+        node_off = _dev_to_host(i.node_offset, G + 1, np.int64, stream)
+        cell = _dev_to_host(i.node_cell, i.nodes, np.uint32, stream)
+        in_off = _dev_to_host(i.in_offset, i.nodes + 1, np.int64, stream)
+        src = _dev_to_host(i.in_src, i.edges, np.uint32, stream).astype(np.int64)
+        w = _dev_to_host(i.in_w, i.edges, np.float32, stream)
+        nets = []
+        for g in range(G):
+            a, b = int(node_off[g]), int(node_off[g + 1])
+            e0, e1 = int(in_off[a]), int(in_off[b])
+            dst = np.repeat(np.arange(b - a, dtype=np.int64), np.diff(in_off[a:b + 1]))
+            nets.append({"cells": cell[a + i.n_substrate:b].astype(np.int64),
+                         "substrate_cells": cell[a:a + i.n_substrate],
+                         "src": src[e0:e1] - a, "dst": dst, "w": w[e0:e1]})
+        return nets
+
+    def known_cells(self, stream=None):
+        """Per genome the hidden cells of every phase before pruning (ascending heap indices)."""
+        i = self.info()
+        bits = _dev_to_host(i.known, i.n_genomes * i.known_words, np.uint32, stream)
+        bits = bits.reshape(i.n_genomes, i.known_words)
+        return [np.nonzero(np.unpackbits(bits[g].view(np.uint8), bitorder="little"))[0] + 1
+                for g in range(i.n_genomes)]
+
+    def phase(self, k: int, stream=None):
+        """Phase k on the host: dict(sources, src_offsets, src_cell, records (the oracle's records
+        layout: pair_count, pair_offset, parent, w4), conn (pair_count, pair_offset, cell, w))."""
+        ph = emr_network_phase()
+        _check(lib().emr_networks_phase(self.handle, k, C.byref(ph)))
+        G = self.info().n_genomes
+        src = np.ctypeslib.as_array(C.cast(ph.sources, C.POINTER(C.c_uint8)),
+                                    shape=(ph.n_sources * SOURCE_DTYPE.itemsize,))
+        src = src.view(SOURCE_DTYPE).copy()
+        offs = None
+        if ph.src_offsets:
+            offs = np.ctypeslib.as_array(C.cast(ph.src_offsets, C.POINTER(C.c_int32)),
+                                         shape=(G + 1,)).copy()
+        rec_off = _dev_to_host(ph.pair_offset, ph.n_pairs + 1, np.int64, stream)
+        records = {"pair_offset": rec_off, "pair_count": np.diff(rec_off),
+                   "parent": _dev_to_host(ph.parent, ph.records, np.uint32, stream).astype(np.int64),
+                   "w4": _dev_to_host(ph.w4, 4 * ph.records, np.float32, stream).reshape(-1, 4)}
+        c_off = _dev_to_host(ph.conn_offset, ph.n_pairs + 1, np.int64, stream)
+        conn = {"pair_offset": c_off, "pair_count": np.diff(c_off),
+                "cell": _dev_to_host(ph.conn_cell, ph.connections, np.uint32, stream).astype(np.int64),
+                "w": _dev_to_host(ph.conn_w, ph.connections, np.float32, stream)}
+        cells = None
+        if ph.src_cell:
+            cells = _dev_to_host(ph.src_cell, ph.n_sources, np.uint32, stream).astype(np.int64)
+        return {"sources": src, "src_offsets": offs, "src_cell": cells, "records": records,
+                "conn": conn}
+
+    def activate(self, inputs, steps: int, stream=None):
+        """Outputs [n_genomes, n_patterns, n_outputs] (numpy) of emr_activate."""
+        import torch
+        i = self.info()
+        x = np.ascontiguousarray(inputs, dtype=np.float32).reshape(-1, i.n_inputs)
+        out = torch.empty(max(1, i.n_genomes * len(x) * i.n_outputs), dtype=torch.float32,
+                          device="cuda")
+        _check(lib().emr_activate(self.handle, x.ctypes.data, len(x), steps,
+                                  C.c_void_p(out.data_ptr()), _stream_ptr(stream)))
+        return out[:i.n_genomes * len(x) * i.n_outputs].cpu().numpy().reshape(
+            i.n_genomes, len(x), i.n_outputs)
+
+    def xor_fitness(self, bias_input: int, steps: int, out=None, stream=None):
+        """emr_xor_fitness into `out` (a float32 device tensor of n_genomes, allocated when None);
+        returns the tensor (not synchronized)."""
+        import torch
+        G = self.info().n_genomes
+        if out is None:
+            out = torch.empty(G, dtype=torch.float32, device="cuda")
+        _check(lib().emr_xor_fitness(self.handle, -1 if bias_input is None else int(bias_input),
+                                     steps, C.c_void_p(out.data_ptr()), _stream_ptr(stream)))
+        return out
+
+
+def emr_build_networks(pop: Population, substrate, depth: int, theta: float, type_mask: int,
+                       w_min: float, iterations: int, stream=None) -> Networks:
+    """emr_build_networks (synchronizing) on a packed population and a substrate (shared
+    sources: inputs outgoing, outputs incoming)."""
+    src = _sources(substrate)
+    h = C.c_void_p()
+    _check(lib().emr_build_networks(pop.handle, src.ctypes.data, len(substrate), depth,
+                                    C.c_float(theta), type_mask, C.c_float(w_min), iterations,
+                                    C.byref(h), _stream_ptr(stream)))
+    return Networks(h)

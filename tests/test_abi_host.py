@@ -100,3 +100,21 @@ def test_stream_chunk_count_and_argument_errors():
     st = L.emr_discover_stream(None, None, 0, None, 0, 7, C.c_float(0.03), 256, 0,
                                C.cast(None, emr.SINK), None, None, None)
     assert st == emr.EMR_E_INVAL
+
+
+def test_network_calls_refuse_null_arguments():
+    """Checked on the host before any device work."""
+    L = emr.lib()
+    h = C.c_void_p()
+    subs = W.xor_sources()
+    assert L.emr_build_networks(None, subs.ctypes.data, 4, 5, C.c_float(0.02), 1, C.c_float(0.1), 1,
+                                C.byref(h), None) == emr.EMR_E_INVAL
+    assert L.emr_build_networks(None, subs.ctypes.data, 4, 5, C.c_float(0.02), 1, C.c_float(0.1), 1,
+                                None, None) == emr.EMR_E_INVAL
+    assert L.emr_activate(None, None, 4, 1, None, None) == emr.EMR_E_INVAL
+    assert L.emr_xor_fitness(None, 1, 1, None, None) == emr.EMR_E_INVAL
+    assert L.emr_networks_info(None, None) == emr.EMR_E_INVAL
+    assert L.emr_networks_phase(None, 0, None) == emr.EMR_E_INVAL
+    assert L.emr_copy_to_host(None, None, -1, None) == emr.EMR_E_INVAL
+    assert L.emr_copy_to_host(None, None, 0, None) == emr.EMR_OK
+    L.emr_free_networks(None)

@@ -38,13 +38,14 @@ def _kernels(asm):
     return out
 
 
-@pytest.fixture(scope="module")
-def phase2_asm():
+@pytest.fixture(scope="module", params=["phase2.hip", "network.hip"])
+def phase2_asm(request):
+    """The kernels after discovery: Phase 2 and connections, and the network kernels."""
     from paper_2608_27612_amd import build
     with tempfile.TemporaryDirectory() as d:
         out = os.path.join(d, "p.s")
         cmd = [build.HIPCC, "-O3", "-std=c++17", "--cuda-device-only", "-S"] + build.DEVICE_FLAGS \
-            + [os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "phase2.hip"), "-o", out]
+            + [os.path.join(ROOT, "paper_2608_27612_amd", "csrc", request.param), "-o", out]
         subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
         return open(out).read()
 
