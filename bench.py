@@ -25,6 +25,11 @@ is resident in HBM before timing starts. Printed as one JSON line:
                the default policy runs it through the interpreter), from genomes held as the C
                ABI's concatenated arrays; ms_per_gen_compiled the same with the population's
                programs compiled first (compile + module load included)
+  generation   per-generation cost with the networks (the paper's per-generation quantity minus
+               NEAT's reproduction): pack + discovery of the substrate's sources and one
+               hidden-to-hidden phase + expression (forward, |w| > 0.1) + network assembly and
+               pruning + XOR fitness of every network, at depth 7 and depth 8 (the paper's
+               "depth 7"), host clock, with its parts
   compiled_tier  the timed steps' compiled programs (the default policy compiles a population's
                programs on its second call, so the warm-up compiles them): count, machine-code
                bytes, host compile and module-load times
@@ -210,6 +215,50 @@ def measure_stream(emr, torch, name, steps, warmup, rT, depth=None, to_disk=None
                                                                         theta32)
 
 
+GEN_TYPES = 1          # connection types of a generation's networks: forward ...
+GEN_ITERATIONS = 1     # ... plus one hidden-to-hidden phase (the h->h configuration)
+GEN_W_MIN = 0.1        # expression's weight filter
+GEN_STEPS = 4          # synchronous activation steps of the XOR evaluation
+
+
+def measure_generation(emr, torch, flat, sources, depth, theta32, gens):
+    """A generation as the paper's per-generation timing counts it, minus NEAT's reproduction: a
+    fresh population packed, its substrates discovered (the substrate's sources, then one
+    hidden-to-hidden phase), connections expressed (forward, |w| > 0.1), the networks assembled
+    and pruned, and all of them evaluated on XOR's four patterns (synchronous activation). Host
+    clock, synchronized; the default compiled-tier policy (a fresh population is interpreted)."""
+    emr.emr_set_jit(emr.EMR_JIT_AUTO)
+    fit = None
+    parts = {"pack": 0.0, "networks": 0.0, "fitness": 0.0}
+    hidden = edges = 0
+    torch.cuda.synchronize()
+    g0 = time.perf_counter()
+    for _ in range(gens):
+        t0 = time.perf_counter()
+        p = emr.emr_pack_population(flat)
+        t1 = time.perf_counter()
+        net = emr.emr_build_networks(p, sources, depth, theta32, GEN_TYPES, GEN_W_MIN,
+                                     GEN_ITERATIONS)
+        t2 = time.perf_counter()
+        fit = net.xor_fitness(1, GEN_STEPS, out=fit)
+        torch.cuda.synchronize()
+        t3 = time.perf_counter()
+        parts["pack"] += t1 - t0
+        parts["networks"] += t2 - t1
+        parts["fitness"] += t3 - t2
+        i = net.info()
+        hidden, edges = int(i.nodes - i.n_genomes * i.n_substrate), int(i.edges)
+        del net, p
+    ms = (time.perf_counter() - g0) * 1e3 / gens
+    f = fit.cpu().numpy()
+    return {"workload": "xor_pop1000_d%d" % depth, "depth": depth, "gens": gens,
+            "ms_per_gen": ms, "ms_parts": {k: v * 1e3 / gens for k, v in parts.items()},
+            "types": "forward + hidden-to-hidden", "iterations": GEN_ITERATIONS,
+            "w_min": GEN_W_MIN, "activation_steps": GEN_STEPS,
+            "kept_hidden_nodes": hidden, "edges": edges,
+            "fitness_mean": float(f.mean()), "fitness_max": float(f.max())}
+
+
 def cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -339,6 +388,13 @@ def main():
         return (time.perf_counter() - g0) * 1e3 / args.gens
     ms_per_gen = per_gen(emr.EMR_JIT_AUTO)
     ms_per_gen_compiled = per_gen(emr.EMR_JIT_ALWAYS)
+    generation = [measure_generation(emr, torch, flat, sources, depth, theta32, args.gens)]
+    if not args.no_sub and args.workload.startswith("xor_pop1000"):
+        from paper_2608_27612_amd import workloads as W
+        g8, s8, d8, t8 = W.workload("xor_pop1000_d8")
+        generation.append(measure_generation(emr, torch, emr.flat_genomes(g8), s8, d8,
+                                             float(np.float32(t8)), max(1, args.gens // 2)))
+    emr.emr_set_jit(policy)
 
     subs, sub_inputs = [], {}
     if not args.no_sub:
@@ -377,6 +433,7 @@ def main():
         "evaluated_queries_per_s": main_line["evaluated_queries_per_s"],
         "ms_per_gen": ms_per_gen,
         "ms_per_gen_compiled": ms_per_gen_compiled,
+        "generation": generation,
         "compiled_tier": {"programs": jit["programs"], "code_bytes": jit["code_bytes"],
                           "compile_ms": jit["compile_ms"], "load_ms": jit["load_ms"],
                           "listed": main_line["listed"]},

@@ -382,9 +382,12 @@ emr_status emr_record_file_close(emr_record_file* file, int64_t* records, int64_
  *     an input reaches u and v reaches an output. Substrate nodes are always kept.
  * Node numbers per genome: the substrate sources in substrate order (inputs are the outgoing
  * sources, outputs the incoming ones), then the kept hidden nodes in ascending heap cell order.
+ * A node's incoming edges are listed in the order phase, pair, cell.
  * Activation is synchronous: input nodes hold the pattern's values, every other node starts at 0
- * and at each step takes sigmoid(sum of w * the source node's previous value) = 1/(1+e^-z),
- * over its incoming edges in the order phase, pair, cell. fp32. */
+ * and at each step takes sigmoid(sum of w * the source node's previous value) = 1/(1+e^-z) over
+ * its incoming edges, in fp32: edge k of the node's list goes to partial sum k mod 64 (an fmaf
+ * chain in list order), and the 64 partial sums are added in a fixed butterfly, so every run
+ * gives the same bits. Each step is one launch on the stream. */
 typedef struct emr_networks emr_networks;
 
 #define EMR_SUBSTRATE_NODE 0xFFFFFFFFu /* node_cell of a substrate node */

@@ -13,12 +13,12 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libemr.so")
 JIT_CO = os.path.join(HERE, "libemr_jit.co")
 SOURCES = ["kernels.hip", "phase2.hip", "runtime.cpp", "pack.cpp", "plan.cpp", "sched.cpp",
-           "jit.cpp", "jit_image.cpp", "record_file.cpp", "network.hip",
+           "jit.cpp", "jit_image.cpp", "record_file.cpp", "network.hip", "net_sort.hip",
            "networks.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-# No packed-FP32 instructions anywhere in the device code. Atomics stay as written: every atomic on
-# one address here is issued by a single lane, so the compiler's rewrite of wave-wide atomics (a
-# loop over the active lanes) would only add code.
+# No packed-FP32 instructions anywhere in the device code. Atomics stay as written: in the discover
+# path every atomic on one address is issued by a single lane, so the compiler's rewrite of
+# wave-wide atomics (a loop over the active lanes) would only add code.
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                 "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]
 

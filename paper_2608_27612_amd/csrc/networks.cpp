@@ -7,8 +7,10 @@
 // cell in a per-genome bitmap) and expressed connections (emr_express); then each hidden-to-hidden
 // phase queries the previous phase's new hidden nodes, up to the requested number of phases or
 // until no genome finds a new one. The network kernels (network.hip) then number the nodes, map
-// every expressed connection to an edge, prune to the input-to-output paths and group each kept
-// node's incoming edges. Every step synchronizes with the host where it needs a count.
+// every expressed connection to an edge, prune to the input-to-output paths (passes over every
+// edge of the population until one changes nothing) and group each kept node's incoming edges (a
+// stable sort of the edges by destination). Every step synchronizes with the host where it needs
+// a count.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -26,6 +28,9 @@ namespace emr {
 emr_status set_error(emr_status st, const std::string& msg);
 }
 extern "C" hipError_t emr_launch_net(int step, const void* args, int64_t work, hipStream_t s);
+extern "C" hipError_t emr_net_sort(void* tmp, size_t* bytes, const uint32_t* kin, uint32_t* kout,
+                                   const uint32_t* vin, uint32_t* vout, uint32_t n, int bits,
+                                   hipStream_t s);
 
 namespace {
 
@@ -138,7 +143,8 @@ struct emr_networks {
   std::vector<int32_t> slots;  // in_slot[n_sub], then out_slot[n_sub]
   std::vector<std::unique_ptr<Phase>> phases;
   Dev known;
-  Dev node_offset, node_cell, in_offset, in_src, in_w, d_slots;
+  Dev node_offset, node_cell, node_in, in_offset, in_src, in_w, d_slots;
+  Dev d_out_node;  // [n_out] substrate index of output o
   int64_t nodes = 0, edges = 0;
   Dev state, patterns;
   // pinned staging of an activation's patterns and targets, and the event of its last copy
@@ -272,8 +278,10 @@ emr_status assemble(Build& B) {
   Dev rank, hidden, err;
   NET_TRY(alloc(rank, (size_t)G * (size_t)N.words * 4, "bitmap ranks"));
   NET_TRY(alloc(hidden, (size_t)G * 4, "hidden counts"));
-  NET_TRY(alloc(err, 4, "error word"));
-  NET_HIP(hipMemsetAsync(err.p, 0, 4, s));
+  NET_TRY(alloc(err, 8, "error and pass words"));
+  NET_HIP(hipMemsetAsync(err.p, 0, 8, s));
+  uint32_t* d_err = err.as<uint32_t>();
+  uint32_t* d_changed = d_err + 1;
   emr::NetRankArgs ra{N.known.as<uint32_t>(), rank.as<uint32_t>(), hidden.as<uint32_t>(), N.words,
                       G};
   NET_HIP(emr_launch_net(0, &ra, 0, s));
@@ -305,9 +313,11 @@ emr_status assemble(Build& B) {
     raw_edge[g + 1] = e;
   }
   const int64_t n_raw = raw_node[G], e_raw = raw_edge[G];
-  for (uint32_t g = 0; g < G; ++g)
-    if (raw_node[g + 1] - raw_node[g] >= (int64_t)emr::kNoNode)
-      return failf(EMR_E_LIMIT, "networks: genome %u has too many nodes", g);
+  // raw node and edge numbers are u32 (kNoNode, the largest, marks a dropped edge)
+  if (n_raw >= (int64_t)emr::kNoNode)
+    return failf(EMR_E_LIMIT, "networks: %lld raw nodes (at most 2^32 - 2)", (long long)n_raw);
+  if (e_raw >= (int64_t)emr::kNoNode)
+    return failf(EMR_E_LIMIT, "networks: %lld raw edges (at most 2^32 - 2)", (long long)e_raw);
   Dev d_raw_node, d_raw_edge, d_dir, eu, ev, ew, fwd, bwd, in_deg, kept_n, kept_e;
   std::vector<Dev> d_seg(K);
   NET_TRY(alloc(d_raw_node, (size_t)(G + 1) * 8, "node offsets"));
@@ -346,17 +356,34 @@ emr_status assemble(Build& B) {
     ea.words = N.words;
     ea.seg = d_seg[k].as<int64_t>();
     ea.raw_edge = d_raw_edge.as<int64_t>();
+    ea.raw_node = d_raw_node.as<int64_t>();
     ea.eu = eu.as<uint32_t>();
     ea.ev = ev.as<uint32_t>();
     ea.ew = ew.as<float>();
-    ea.err = err.as<uint32_t>();
+    ea.err = d_err;
     NET_HIP(emr_launch_net(1, &ea, 0, s));
   }
-  emr::NetPruneArgs pa{d_dir.as<uint8_t>(), d_raw_node.as<int64_t>(), d_raw_edge.as<int64_t>(),
-                       eu.as<uint32_t>(), ev.as<uint32_t>(), fwd.as<uint8_t>(), bwd.as<uint8_t>(),
-                       in_deg.as<uint32_t>(), kept_n.as<uint32_t>(), kept_e.as<uint32_t>(),
-                       err.as<uint32_t>(), (uint32_t)N.n_sub, G};
-  NET_HIP(emr_launch_net(2, &pa, 0, s));
+  // pruning: flags, then passes over every edge until one changes nothing
+  emr::NetFlagArgs fa{d_dir.as<uint8_t>(), d_raw_node.as<int64_t>(), fwd.as<uint8_t>(),
+                      bwd.as<uint8_t>(), in_deg.as<uint32_t>(), kept_n.as<uint32_t>(),
+                      kept_e.as<uint32_t>(), (uint32_t)N.n_sub, G};
+  NET_HIP(emr_launch_net(2, &fa, 0, s));
+  emr::NetReachArgs rr{eu.as<uint32_t>(), ev.as<uint32_t>(), fwd.as<uint8_t>(), bwd.as<uint8_t>(),
+                       in_deg.as<uint32_t>(), d_changed, e_raw, n_raw};
+  // a pass that changes something sets at least one more flag: 2 n_raw passes bound the loop
+  const int64_t max_pass = 2 * n_raw + 2;
+  for (int64_t pass = 0;; ++pass) {
+    if (pass > max_pass)
+      return failf(EMR_E_DEVICE, "networks: pruning did not settle in %lld passes",
+                   (long long)max_pass);
+    NET_HIP(hipMemsetAsync(d_changed, 0, 4, s));
+    NET_HIP(emr_launch_net(3, &rr, 0, s));
+    uint32_t ch = 0;
+    NET_TRY(to_host(&ch, d_changed, 4, s));
+    if (ch == 0) break;
+  }
+  NET_HIP(emr_launch_net(4, &rr, 0, s));
+  NET_HIP(emr_launch_net(5, &fa, 0, s));
   std::vector<uint32_t> kn(G), ke(G);
   NET_TRY(to_host(kn.data(), kept_n.p, (size_t)G * 4, s));
   NET_TRY(to_host(ke.data(), kept_e.p, (size_t)G * 4, s));
@@ -369,32 +396,59 @@ emr_status assemble(Build& B) {
   N.edges = edge_off[G];
   if (N.nodes >= (int64_t)emr::kNoNode)
     return failf(EMR_E_LIMIT, "networks: %lld nodes in all (at most 2^32 - 2)", (long long)N.nodes);
-  Dev d_edge_off, new_id, cursor;
+  if (N.edges > e_raw)
+    return failf(EMR_E_DEVICE, "networks: %lld kept edges of %lld", (long long)N.edges,
+                 (long long)e_raw);
+  Dev d_edge_off, gid;
   NET_TRY(alloc(N.node_offset, (size_t)(G + 1) * 8, "network node offsets"));
   NET_TRY(alloc(d_edge_off, (size_t)(G + 1) * 8, "network edge offsets"));
   NET_TRY(alloc(N.node_cell, (size_t)N.nodes * 4, "network nodes"));
+  NET_TRY(alloc(N.node_in, (size_t)N.nodes * 4, "network input numbers"));
   NET_TRY(alloc(N.in_offset, (size_t)(N.nodes + 1) * 8, "network edge offsets"));
   NET_TRY(alloc(N.in_src, (size_t)N.edges * 4, "network edges"));
   NET_TRY(alloc(N.in_w, (size_t)N.edges * 4, "network edges"));
-  NET_TRY(alloc(new_id, (size_t)n_raw * 4, "node numbers"));
-  NET_TRY(alloc(cursor, (size_t)N.nodes * 4, "edge cursors"));
+  NET_TRY(alloc(gid, (size_t)n_raw * 4, "node numbers"));
   NET_TRY(to_device(N.node_offset.p, node_off.data(), node_off.size() * 8, s));
   NET_TRY(to_device(d_edge_off.p, edge_off.data(), edge_off.size() * 8, s));
-  NET_HIP(hipMemsetAsync(cursor.p, 0, (size_t)N.nodes * 4, s));
   emr::NetNodeArgs na{N.known.as<uint32_t>(), rank.as<uint32_t>(), N.words,
                       d_raw_node.as<int64_t>(), fwd.as<uint8_t>(), bwd.as<uint8_t>(),
-                      in_deg.as<uint32_t>(), N.node_offset.as<int64_t>(),
-                      d_edge_off.as<int64_t>(), new_id.as<uint32_t>(), N.node_cell.as<uint32_t>(),
-                      N.in_offset.as<int64_t>(), err.as<uint32_t>(), (uint32_t)N.n_sub, G};
-  NET_HIP(emr_launch_net(3, &na, 0, s));
-  emr::NetPlaceArgs pl{d_raw_node.as<int64_t>(), d_raw_edge.as<int64_t>(),
-                       N.node_offset.as<int64_t>(), eu.as<uint32_t>(), ev.as<uint32_t>(),
-                       ew.as<float>(), fwd.as<uint8_t>(), bwd.as<uint8_t>(), new_id.as<uint32_t>(),
-                       N.in_offset.as<int64_t>(), cursor.as<uint32_t>(), N.in_src.as<uint32_t>(),
-                       N.in_w.as<float>(), N.edges, err.as<uint32_t>(), G};
-  NET_HIP(emr_launch_net(4, &pl, 0, s));
+                      in_deg.as<uint32_t>(), N.d_slots.as<int32_t>(),
+                      N.node_offset.as<int64_t>(), d_edge_off.as<int64_t>(), gid.as<uint32_t>(),
+                      N.node_cell.as<uint32_t>(), N.node_in.as<int32_t>(),
+                      N.in_offset.as<int64_t>(), d_err, (uint32_t)N.n_sub, G};
+  NET_HIP(emr_launch_net(6, &na, 0, s));
+  // kept edges grouped by destination, each group in raw order: a stable sort by destination
+  if (N.edges > 0) {
+    Dev keys, vals, skeys, svals, tmp;
+    NET_TRY(alloc(keys, (size_t)e_raw * 4, "edge keys"));
+    NET_TRY(alloc(vals, (size_t)e_raw * 4, "edge keys"));
+    NET_TRY(alloc(skeys, (size_t)e_raw * 4, "edge keys"));
+    NET_TRY(alloc(svals, (size_t)e_raw * 4, "edge keys"));
+    emr::NetKeyArgs ka{eu.as<uint32_t>(), ev.as<uint32_t>(), fwd.as<uint8_t>(), bwd.as<uint8_t>(),
+                       gid.as<uint32_t>(), keys.as<uint32_t>(), vals.as<uint32_t>(), e_raw, n_raw,
+                       (uint32_t)N.nodes, d_err};
+    NET_HIP(emr_launch_net(7, &ka, 0, s));
+    int bits = 1;
+    while (bits < 32 && ((uint64_t)1 << bits) <= (uint64_t)N.nodes) ++bits;  // keys <= nodes
+    size_t tb = 0;
+    NET_HIP(emr_net_sort(nullptr, &tb, keys.as<uint32_t>(), skeys.as<uint32_t>(),
+                         vals.as<uint32_t>(), svals.as<uint32_t>(), (uint32_t)e_raw, bits, s));
+    NET_TRY(alloc(tmp, tb, "sort storage"));
+    NET_HIP(emr_net_sort(tmp.p, &tb, keys.as<uint32_t>(), skeys.as<uint32_t>(),
+                         vals.as<uint32_t>(), svals.as<uint32_t>(), (uint32_t)e_raw, bits, s));
+    emr::NetGatherArgs ga{skeys.as<uint32_t>(), svals.as<uint32_t>(), eu.as<uint32_t>(),
+                          ew.as<float>(), gid.as<uint32_t>(), N.in_offset.as<int64_t>(),
+                          N.in_src.as<uint32_t>(), N.in_w.as<float>(), N.edges, e_raw, n_raw,
+                          N.nodes, d_err};
+    NET_HIP(emr_launch_net(8, &ga, 0, s));
+    uint32_t e = 0;
+    NET_TRY(to_host(&e, d_err, 4, s));  // (the sort's buffers are released after this sync)
+    if (e != 0)
+      return failf(EMR_E_DEVICE, "networks: a network kernel flagged an internal error (0x%x)", e);
+    return EMR_OK;
+  }
   uint32_t e = 0;
-  NET_TRY(to_host(&e, err.p, 4, s));
+  NET_TRY(to_host(&e, d_err, 4, s));
   if (e != 0)
     return failf(EMR_E_DEVICE, "networks: a network kernel flagged an internal error (0x%x)", e);
   return EMR_OK;
@@ -409,10 +463,11 @@ emr_status run_forward(const emr_networks* N, const float* patterns, int32_t n_p
   if (dev != N->device)
     return failf(EMR_E_INVAL, "networks: built on device %d, current device is %d", N->device, dev);
   const int64_t pblocks = (n_patterns + 3) / 4;
-  const int64_t work = (int64_t)N->n_genomes * pblocks;
-  if (work > 0x7FFFFFFF) return failf(EMR_E_LIMIT, "networks: too many genomes x patterns");
-  const size_t state_bytes = (size_t)2 * (size_t)pblocks * (size_t)(N->nodes ? N->nodes : 1) * 16;
-  if (M.state.bytes < state_bytes) NET_TRY(alloc(M.state, state_bytes, "node states"));
+  if (pblocks * (N->nodes ? N->nodes : 1) > ((int64_t)1 << 40))
+    return failf(EMR_E_LIMIT, "networks: too many nodes x patterns");
+  // two state buffers of [pblocks][nodes] float4
+  const size_t half = (size_t)pblocks * (size_t)(N->nodes ? N->nodes : 1) * 16;
+  if (M.state.bytes < 2 * half) NET_TRY(alloc(M.state, 2 * half, "node states"));
   // patterns, then targets, staged in pinned memory and copied on the stream; the staging is
   // rewritten only after the previous call's copy has completed
   const size_t pat_bytes = (size_t)n_patterns * (size_t)N->n_in * 4;
@@ -438,27 +493,30 @@ emr_status run_forward(const emr_networks* N, const float* patterns, int32_t n_p
   NET_HIP(hipMemcpyAsync(M.patterns.p, M.pin, need, hipMemcpyHostToDevice, s));
   NET_HIP(hipEventRecord(M.pin_done, s));
   M.pin_pending = true;
-  emr::NetForwardArgs A{};
-  A.node_offset = N->node_offset.as<int64_t>();
-  A.in_offset = N->in_offset.as<int64_t>();
-  A.in_src = N->in_src.as<uint32_t>();
-  A.in_w = N->in_w.as<float>();
-  A.in_slot = N->d_slots.as<int32_t>();
-  A.out_slot = N->d_slots.as<int32_t>() + N->n_sub;
-  A.patterns = M.patterns.as<float>();
-  A.targets = targets ? reinterpret_cast<const float*>(M.patterns.as<char>() + pat_bytes) : nullptr;
-  A.state = M.state.as<float>();
-  A.outputs = outputs;
-  A.fitness = fitness;
-  A.nodes = N->nodes;
-  A.n_genomes = (uint32_t)N->n_genomes;
-  A.n_sub = (uint32_t)N->n_sub;
-  A.n_inputs = (uint32_t)N->n_in;
-  A.n_outputs = (uint32_t)N->n_out;
-  A.n_patterns = (uint32_t)n_patterns;
-  A.pblocks = (uint32_t)pblocks;
-  A.steps = (uint32_t)steps;
-  NET_HIP(emr_launch_net(5, &A, work, s));
+  float* buf[2] = {M.state.as<float>(), reinterpret_cast<float*>(M.state.as<char>() + half)};
+  emr::NetStateArgs sa{N->node_in.as<int32_t>(), M.patterns.as<float>(), buf[0], N->nodes,
+                       (uint32_t)N->n_in, (uint32_t)n_patterns, (uint32_t)pblocks};
+  NET_HIP(emr_launch_net(9, &sa, 0, s));
+  int cur = 0;
+  for (int32_t t = 0; t < steps; ++t, cur ^= 1) {
+    emr::NetStepArgs st{N->node_in.as<int32_t>(), N->in_offset.as<int64_t>(),
+                        N->in_src.as<uint32_t>(), N->in_w.as<float>(), buf[cur], buf[cur ^ 1],
+                        N->nodes, (uint32_t)pblocks};
+    NET_HIP(emr_launch_net(10, &st, 0, s));
+  }
+  emr::NetOutArgs oa{};
+  oa.node_offset = N->node_offset.as<int64_t>();
+  oa.out_node = N->d_out_node.as<int32_t>();
+  oa.state = buf[cur];
+  oa.targets = targets ? reinterpret_cast<const float*>(M.patterns.as<char>() + pat_bytes) : nullptr;
+  oa.outputs = outputs;
+  oa.fitness = fitness;
+  oa.nodes = N->nodes;
+  oa.n_genomes = (uint32_t)N->n_genomes;
+  oa.n_outputs = (uint32_t)N->n_out;
+  oa.n_patterns = (uint32_t)n_patterns;
+  oa.pblocks = (uint32_t)pblocks;
+  NET_HIP(emr_launch_net(11, &oa, 0, s));
   return EMR_OK;
 }
 
@@ -515,6 +573,11 @@ emr_status emr_build_networks(const emr_population* pop, const emr_source* subst
   NET_HIP(hipMemsetAsync(N.known.p, 0, N.known.bytes, B.s));
   NET_TRY(alloc(N.d_slots, N.slots.size() * 4, "substrate slots"));
   NET_TRY(to_device(N.d_slots.p, N.slots.data(), N.slots.size() * 4, B.s));
+  std::vector<int32_t> out_node((size_t)N.n_out);
+  for (int32_t j = 0; j < n_substrate; ++j)
+    if (N.slots[(size_t)n_substrate + j] >= 0) out_node[(size_t)N.slots[(size_t)n_substrate + j]] = j;
+  NET_TRY(alloc(N.d_out_node, out_node.size() * 4, "output nodes"));
+  NET_TRY(to_device(N.d_out_node.p, out_node.data(), out_node.size() * 4, B.s));
 
   N.phases.push_back(std::make_unique<Phase>());
   N.phases[0]->sources = N.substrate;

@@ -50,6 +50,22 @@ def phase2_asm(request):
         return open(out).read()
 
 
+def test_sort_kernels_have_no_packed_fp32_or_scalar_writes():
+    """The library sort behind network assembly (a generic library kernel: its register and
+    scratch use is its own) holds no packed FP32 arithmetic and no scalar-memory writes."""
+    from paper_2608_27612_amd import build
+    with tempfile.TemporaryDirectory() as d:
+        out = os.path.join(d, "s.s")
+        cmd = [build.HIPCC, "-O3", "-std=c++17", "--cuda-device-only", "-S"] + build.DEVICE_FLAGS \
+            + [os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "net_sort.hip"), "-o", out]
+        subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
+        text = open(out).read()
+    assert "radix" in text
+    assert not re.search(r"v_pk_(add|mul|fma)_f32", text)
+    pattern = r"\bs_(buffer_)?(st" + r"ore|atom" + r"ic)\w*|\bs_dca" + r"che_\w+|\bs_scr" + r"atch_\w+"
+    assert not re.search(pattern, text)
+
+
 def test_phase2_kernels_have_no_packed_fp32_scalar_writes_m0_or_scratch(phase2_asm):
     assert not re.search(r"v_pk_(add|mul|fma)_f32", phase2_asm)
     pattern = r"\bs_(buffer_)?(st" + r"ore|atom" + r"ic)\w*|\bs_dca" + r"che_\w+|\bs_scr" + r"atch_\w+"
