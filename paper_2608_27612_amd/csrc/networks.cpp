@@ -17,7 +17,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <memory>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -54,40 +56,166 @@ emr_status failf(emr_status st, const char* fmt, ...) {
     if (s_ != EMR_OK) return s_;   \
   } while (0)
 
-// A device allocation owned by the networks handle.
+// Device memory of the network builds, kept for reuse: a build allocates and frees dozens of
+// buffers whose sizes change little from one generation to the next, and a hipMalloc / hipFree
+// pair costs about 0.1 ms. A freed buffer enters its device's cache with an event recorded on the
+// stream that used it (no event when the caller has already waited for that work) and is handed
+// out again once that event has completed, to a request of at most its size and more than half
+// of it. At most kCacheBytes stay cached per device; a buffer beyond that is freed. Cached memory
+// is held until the process ends.
+constexpr size_t kCacheBytes = size_t(8) << 30;
+
+struct CacheEntry {
+  void* p;
+  hipEvent_t ev;  // nullptr: idle
+};
+struct DevCache {
+  std::mutex mu;
+  std::map<int, std::multimap<size_t, CacheEntry>> blocks;
+  std::map<int, size_t> held;
+  std::vector<hipEvent_t> spare;
+};
+DevCache& dev_cache() {
+  static DevCache* c = new DevCache;  // (never destroyed: cached buffers live as long as the process)
+  return *c;
+}
+
+// A cached buffer of at least `bytes` on device `dev` whose last use has completed, or nullptr.
+void* cache_take(int dev, size_t bytes, size_t* cap) {
+  DevCache& C = dev_cache();
+  std::lock_guard<std::mutex> lk(C.mu);
+  auto& m = C.blocks[dev];
+  for (auto it = m.lower_bound(bytes); it != m.end() && it->first / 2 < bytes; ++it) {
+    if (it->second.ev) {
+      const hipError_t q = hipEventQuery(it->second.ev);
+      if (q != hipSuccess) {
+        (void)hipGetLastError();  // (not ready is no error of the caller's)
+        continue;
+      }
+      C.spare.push_back(it->second.ev);
+    }
+    void* p = it->second.p;
+    *cap = it->first;
+    C.held[dev] -= it->first;
+    m.erase(it);
+    return p;
+  }
+  return nullptr;
+}
+
+// Frees every cached buffer of `dev` (waiting for the last use of each).
+void cache_flush(int dev) {
+  DevCache& C = dev_cache();
+  std::lock_guard<std::mutex> lk(C.mu);
+  auto& m = C.blocks[dev];
+  for (auto& kv : m) {
+    if (kv.second.ev) {
+      (void)hipEventSynchronize(kv.second.ev);
+      C.spare.push_back(kv.second.ev);
+    }
+    (void)hipFree(kv.second.p);
+  }
+  m.clear();
+  C.held[dev] = 0;
+}
+
+// Returns a buffer to the cache; `s` is the stream of its last use, or nullptr with `idle` when
+// that use is known to have completed.
+void cache_give(int dev, void* p, size_t cap, hipStream_t s, bool idle) {
+  DevCache& C = dev_cache();
+  std::unique_lock<std::mutex> lk(C.mu);
+  if (C.held[dev] + cap > kCacheBytes) {
+    lk.unlock();
+    (void)hipFree(p);  // (waits for the device's outstanding work)
+    return;
+  }
+  hipEvent_t ev = nullptr;
+  if (!idle) {
+    if (!C.spare.empty()) {
+      ev = C.spare.back();
+      C.spare.pop_back();
+    } else if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) {
+      (void)hipGetLastError();
+      lk.unlock();
+      (void)hipFree(p);
+      return;
+    }
+    if (hipEventRecord(ev, s) != hipSuccess) {
+      (void)hipGetLastError();
+      C.spare.push_back(ev);
+      lk.unlock();
+      (void)hipFree(p);
+      return;
+    }
+  }
+  C.blocks[dev].emplace(cap, CacheEntry{p, ev});
+  C.held[dev] += cap;
+}
+
+// A device allocation of a build or of the networks handle, from the cache.
 struct Dev {
   void* p = nullptr;
-  size_t bytes = 0;
+  size_t bytes = 0;   // asked for
+  size_t cap = 0;     // the buffer's size
+  int dev = 0;
+  hipStream_t s = nullptr;  // the stream its users run on
   Dev() = default;
   Dev(const Dev&) = delete;
   Dev& operator=(const Dev&) = delete;
   ~Dev() { reset(); }
-  void reset() {
-    if (p) (void)hipFree(p);
-    p = nullptr;
-    bytes = 0;
-  }
+  // Back to the cache, usable once the work queued on `s` so far has completed.
+  void reset() { release(false); }
+  // Back to the cache when the caller has waited for every use of the buffer.
+  void reset_idle() { release(true); }
   void take(Dev& o) {
     reset();
     p = o.p;
     bytes = o.bytes;
+    cap = o.cap;
+    dev = o.dev;
+    s = o.s;
     o.p = nullptr;
-    o.bytes = 0;
+    o.bytes = o.cap = 0;
   }
   template <class T>
   T* as() const {
     return static_cast<T*>(p);
   }
+
+ private:
+  void release(bool idle) {
+    if (p) cache_give(dev, p, cap, s, idle);
+    p = nullptr;
+    bytes = cap = 0;
+  }
 };
 
-emr_status alloc(Dev& d, size_t bytes, const char* what) {
+emr_status alloc(Dev& d, size_t bytes, const char* what, hipStream_t s) {
   d.reset();
-  if (hipMalloc(&d.p, bytes ? bytes : 256) != hipSuccess) {
-    d.p = nullptr;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
     (void)hipGetLastError();
-    return failf(EMR_E_NOMEM, "networks: cannot allocate %zu bytes for %s", bytes, what);
+    return failf(EMR_E_DEVICE, "networks: no current device");
   }
+  const size_t want = bytes ? (bytes + 255) & ~size_t(255) : 256;
+  size_t cap = 0;
+  void* p = cache_take(dev, want, &cap);
+  if (!p) {
+    cap = want;
+    if (hipMalloc(&p, want) != hipSuccess) {
+      (void)hipGetLastError();
+      cache_flush(dev);
+      if (hipMalloc(&p, want) != hipSuccess) {
+        (void)hipGetLastError();
+        return failf(EMR_E_NOMEM, "networks: cannot allocate %zu bytes for %s", bytes, what);
+      }
+    }
+  }
+  d.p = p;
   d.bytes = bytes;
+  d.cap = cap;
+  d.dev = dev;
+  d.s = s;
   return EMR_OK;
 }
 
@@ -116,6 +244,12 @@ struct Phase {
   Dev src_cell;   // [sources] heap cells of the queried hidden nodes
   Dev src_offs;   // [n_genomes + 1] int64 copy of offs
   Dev ws;         // the discovery's workspace, released after the phase
+
+  void release_idle() {
+    for (Dev* d : {&parent, &w4, &rcount, &roffset, &cell, &w, &ccount, &coffset, &src_cell,
+                   &src_offs, &ws})
+      d->reset_idle();
+  }
 
   bool shared() const { return offs.empty(); }
   const int32_t* offs_ptr() const { return offs.empty() ? nullptr : offs.data(); }
@@ -152,12 +286,25 @@ struct emr_networks {
   size_t pin_bytes = 0;
   hipEvent_t pin_done = nullptr;
   bool pin_pending = false;
+  // the end of the last activation (its outputs written)
+  hipEvent_t done = nullptr;
+  bool done_pending = false;
+  // The build synchronized with its stream before the handle was returned (or, failing, before
+  // the handle was destroyed), and the last activation is waited for here: every buffer is idle.
   ~emr_networks() {
+    if (done) {
+      if (done_pending) (void)hipEventSynchronize(done);
+      (void)hipEventDestroy(done);
+    }
     if (pin_done) {
       if (pin_pending) (void)hipEventSynchronize(pin_done);
       (void)hipEventDestroy(pin_done);
     }
     if (pin) (void)hipHostFree(pin);
+    for (auto& ph : phases) ph->release_idle();
+    for (Dev* d : {&known, &node_offset, &node_cell, &node_in, &in_offset, &in_src, &in_w,
+                   &d_slots, &d_out_node, &state, &patterns})
+      d->reset_idle();
   }
 };
 
@@ -178,19 +325,21 @@ emr_status discover_phase(Build& B, Phase& P) {
   const emr_source* src = P.sources.data();
   const int32_t n = (int32_t)P.sources.size();
   P.n_pairs = P.shared() ? (int64_t)N.n_genomes * n : P.offs[N.n_genomes];
-  NET_TRY(alloc(P.rcount, (size_t)P.n_pairs * 8, "pair counts"));
-  NET_TRY(alloc(P.roffset, (size_t)(P.n_pairs + 1) * 8, "pair offsets"));
+  NET_TRY(alloc(P.rcount, (size_t)P.n_pairs * 8, "pair counts", B.s));
+  NET_TRY(alloc(P.roffset, (size_t)(P.n_pairs + 1) * 8, "pair offsets", B.s));
   int64_t n_pos = 0, Q = 0;
   NET_TRY(emr_grid_count(N.depth, &n_pos, &Q));
+  // A first guess of 16M records (320 MB) holds the kept cells of every workload measured here,
+  // so the retry (which runs the phase's discovery a second time) stays the exception.
   int64_t cap = P.n_pairs * Q;
-  if (cap > (int64_t)1 << 20) cap = (int64_t)1 << 20;
+  if (cap > (int64_t)1 << 24) cap = (int64_t)1 << 24;
   if (cap < 1) cap = 1;
   for (int attempt = 0;; ++attempt) {
     int64_t wsb = 0;
     NET_TRY(emr_workspace_bytes(B.pop, src, n, P.offs_ptr(), P.n_shared(), N.depth, cap, &wsb));
-    NET_TRY(alloc(P.ws, (size_t)wsb, "discover workspace"));
-    NET_TRY(alloc(P.parent, (size_t)cap * 4, "records"));
-    NET_TRY(alloc(P.w4, (size_t)cap * 16, "records"));
+    NET_TRY(alloc(P.ws, (size_t)wsb, "discover workspace", B.s));
+    NET_TRY(alloc(P.parent, (size_t)cap * 4, "records", B.s));
+    NET_TRY(alloc(P.w4, (size_t)cap * 16, "records", B.s));
     P.rcap = cap;
     const emr_result r = P.result();
     NET_TRY(emr_discover(B.pop, src, n, P.offs_ptr(), P.n_shared(), N.depth, B.theta, &r, B.s));
@@ -213,10 +362,10 @@ emr_status hidden_phase(Build& B, Phase& P, Phase* next, int64_t* n_new) {
   int64_t hb = 0;
   NET_TRY(emr_hidden_workspace_bytes(N.n_genomes, N.depth, &hb));
   Dev hws, hsrc, hcell, hoff;
-  NET_TRY(alloc(hws, (size_t)hb, "hidden-node workspace"));
-  NET_TRY(alloc(hsrc, (size_t)cap * sizeof(emr_source), "hidden sources"));
-  NET_TRY(alloc(hcell, (size_t)cap * 4, "hidden cells"));
-  NET_TRY(alloc(hoff, (size_t)(N.n_genomes + 1) * 8, "hidden offsets"));
+  NET_TRY(alloc(hws, (size_t)hb, "hidden-node workspace", B.s));
+  NET_TRY(alloc(hsrc, (size_t)cap * sizeof(emr_source), "hidden sources", B.s));
+  NET_TRY(alloc(hcell, (size_t)cap * 4, "hidden cells", B.s));
+  NET_TRY(alloc(hoff, (size_t)(N.n_genomes + 1) * 8, "hidden offsets", B.s));
   emr_hidden h;
   h.sources = hsrc.as<emr_source>();
   h.cell = hcell.as<uint32_t>();
@@ -251,11 +400,11 @@ emr_status express_phase(Build& B, Phase& P) {
   int64_t eb = 0;
   NET_TRY(emr_express_workspace_bytes(P.n_pairs, &eb));
   Dev cws;
-  NET_TRY(alloc(cws, (size_t)eb, "connection workspace"));
-  NET_TRY(alloc(P.cell, (size_t)P.ccap * 4, "connections"));
-  NET_TRY(alloc(P.w, (size_t)P.ccap * 4, "connections"));
-  NET_TRY(alloc(P.ccount, (size_t)P.n_pairs * 8, "connection counts"));
-  NET_TRY(alloc(P.coffset, (size_t)(P.n_pairs + 1) * 8, "connection offsets"));
+  NET_TRY(alloc(cws, (size_t)eb, "connection workspace", B.s));
+  NET_TRY(alloc(P.cell, (size_t)P.ccap * 4, "connections", B.s));
+  NET_TRY(alloc(P.w, (size_t)P.ccap * 4, "connections", B.s));
+  NET_TRY(alloc(P.ccount, (size_t)P.n_pairs * 8, "connection counts", B.s));
+  NET_TRY(alloc(P.coffset, (size_t)(P.n_pairs + 1) * 8, "connection offsets", B.s));
   emr_connections c;
   c.cell = P.cell.as<uint32_t>();
   c.w = P.w.as<float>();
@@ -276,9 +425,9 @@ emr_status assemble(Build& B) {
   const uint32_t G = (uint32_t)N.n_genomes;
   const hipStream_t s = B.s;
   Dev rank, hidden, err;
-  NET_TRY(alloc(rank, (size_t)G * (size_t)N.words * 4, "bitmap ranks"));
-  NET_TRY(alloc(hidden, (size_t)G * 4, "hidden counts"));
-  NET_TRY(alloc(err, 8, "error and pass words"));
+  NET_TRY(alloc(rank, (size_t)G * (size_t)N.words * 4, "bitmap ranks", s));
+  NET_TRY(alloc(hidden, (size_t)G * 4, "hidden counts", s));
+  NET_TRY(alloc(err, 8, "error and pass words", s));
   NET_HIP(hipMemsetAsync(err.p, 0, 8, s));
   uint32_t* d_err = err.as<uint32_t>();
   uint32_t* d_changed = d_err + 1;
@@ -320,17 +469,17 @@ emr_status assemble(Build& B) {
     return failf(EMR_E_LIMIT, "networks: %lld raw edges (at most 2^32 - 2)", (long long)e_raw);
   Dev d_raw_node, d_raw_edge, d_dir, eu, ev, ew, fwd, bwd, in_deg, kept_n, kept_e;
   std::vector<Dev> d_seg(K);
-  NET_TRY(alloc(d_raw_node, (size_t)(G + 1) * 8, "node offsets"));
-  NET_TRY(alloc(d_raw_edge, (size_t)(G + 1) * 8, "edge offsets"));
-  NET_TRY(alloc(d_dir, (size_t)N.n_sub, "substrate directions"));
-  NET_TRY(alloc(eu, (size_t)e_raw * 4, "edges"));
-  NET_TRY(alloc(ev, (size_t)e_raw * 4, "edges"));
-  NET_TRY(alloc(ew, (size_t)e_raw * 4, "edges"));
-  NET_TRY(alloc(fwd, (size_t)n_raw, "node flags"));
-  NET_TRY(alloc(bwd, (size_t)n_raw, "node flags"));
-  NET_TRY(alloc(in_deg, (size_t)n_raw * 4, "in-degrees"));
-  NET_TRY(alloc(kept_n, (size_t)G * 4, "kept counts"));
-  NET_TRY(alloc(kept_e, (size_t)G * 4, "kept counts"));
+  NET_TRY(alloc(d_raw_node, (size_t)(G + 1) * 8, "node offsets", s));
+  NET_TRY(alloc(d_raw_edge, (size_t)(G + 1) * 8, "edge offsets", s));
+  NET_TRY(alloc(d_dir, (size_t)N.n_sub, "substrate directions", s));
+  NET_TRY(alloc(eu, (size_t)e_raw * 4, "edges", s));
+  NET_TRY(alloc(ev, (size_t)e_raw * 4, "edges", s));
+  NET_TRY(alloc(ew, (size_t)e_raw * 4, "edges", s));
+  NET_TRY(alloc(fwd, (size_t)n_raw, "node flags", s));
+  NET_TRY(alloc(bwd, (size_t)n_raw, "node flags", s));
+  NET_TRY(alloc(in_deg, (size_t)n_raw * 4, "in-degrees", s));
+  NET_TRY(alloc(kept_n, (size_t)G * 4, "kept counts", s));
+  NET_TRY(alloc(kept_e, (size_t)G * 4, "kept counts", s));
   std::vector<uint8_t> dir(N.n_sub);
   for (int32_t j = 0; j < N.n_sub; ++j) dir[j] = N.substrate[j].dir == EMR_DIR_OUT ? 0 : 1;
   NET_TRY(to_device(d_raw_node.p, raw_node.data(), raw_node.size() * 8, s));
@@ -338,7 +487,7 @@ emr_status assemble(Build& B) {
   NET_TRY(to_device(d_dir.p, dir.data(), dir.size(), s));
   for (size_t k = 0; k < K; ++k) {
     Phase& P = *N.phases[k];
-    NET_TRY(alloc(d_seg[k], (size_t)G * 8, "phase segments"));
+    NET_TRY(alloc(d_seg[k], (size_t)G * 8, "phase segments", s));
     NET_TRY(to_device(d_seg[k].p, seg[k].data(), (size_t)G * 8, s));
     emr::NetEdgeArgs ea{};
     ea.conn_offset = P.coffset.as<int64_t>();
@@ -400,14 +549,14 @@ emr_status assemble(Build& B) {
     return failf(EMR_E_DEVICE, "networks: %lld kept edges of %lld", (long long)N.edges,
                  (long long)e_raw);
   Dev d_edge_off, gid;
-  NET_TRY(alloc(N.node_offset, (size_t)(G + 1) * 8, "network node offsets"));
-  NET_TRY(alloc(d_edge_off, (size_t)(G + 1) * 8, "network edge offsets"));
-  NET_TRY(alloc(N.node_cell, (size_t)N.nodes * 4, "network nodes"));
-  NET_TRY(alloc(N.node_in, (size_t)N.nodes * 4, "network input numbers"));
-  NET_TRY(alloc(N.in_offset, (size_t)(N.nodes + 1) * 8, "network edge offsets"));
-  NET_TRY(alloc(N.in_src, (size_t)N.edges * 4, "network edges"));
-  NET_TRY(alloc(N.in_w, (size_t)N.edges * 4, "network edges"));
-  NET_TRY(alloc(gid, (size_t)n_raw * 4, "node numbers"));
+  NET_TRY(alloc(N.node_offset, (size_t)(G + 1) * 8, "network node offsets", s));
+  NET_TRY(alloc(d_edge_off, (size_t)(G + 1) * 8, "network edge offsets", s));
+  NET_TRY(alloc(N.node_cell, (size_t)N.nodes * 4, "network nodes", s));
+  NET_TRY(alloc(N.node_in, (size_t)N.nodes * 4, "network input numbers", s));
+  NET_TRY(alloc(N.in_offset, (size_t)(N.nodes + 1) * 8, "network edge offsets", s));
+  NET_TRY(alloc(N.in_src, (size_t)N.edges * 4, "network edges", s));
+  NET_TRY(alloc(N.in_w, (size_t)N.edges * 4, "network edges", s));
+  NET_TRY(alloc(gid, (size_t)n_raw * 4, "node numbers", s));
   NET_TRY(to_device(N.node_offset.p, node_off.data(), node_off.size() * 8, s));
   NET_TRY(to_device(d_edge_off.p, edge_off.data(), edge_off.size() * 8, s));
   emr::NetNodeArgs na{N.known.as<uint32_t>(), rank.as<uint32_t>(), N.words,
@@ -420,10 +569,10 @@ emr_status assemble(Build& B) {
   // kept edges grouped by destination, each group in raw order: a stable sort by destination
   if (N.edges > 0) {
     Dev keys, vals, skeys, svals, tmp;
-    NET_TRY(alloc(keys, (size_t)e_raw * 4, "edge keys"));
-    NET_TRY(alloc(vals, (size_t)e_raw * 4, "edge keys"));
-    NET_TRY(alloc(skeys, (size_t)e_raw * 4, "edge keys"));
-    NET_TRY(alloc(svals, (size_t)e_raw * 4, "edge keys"));
+    NET_TRY(alloc(keys, (size_t)e_raw * 4, "edge keys", s));
+    NET_TRY(alloc(vals, (size_t)e_raw * 4, "edge keys", s));
+    NET_TRY(alloc(skeys, (size_t)e_raw * 4, "edge keys", s));
+    NET_TRY(alloc(svals, (size_t)e_raw * 4, "edge keys", s));
     emr::NetKeyArgs ka{eu.as<uint32_t>(), ev.as<uint32_t>(), fwd.as<uint8_t>(), bwd.as<uint8_t>(),
                        gid.as<uint32_t>(), keys.as<uint32_t>(), vals.as<uint32_t>(), e_raw, n_raw,
                        (uint32_t)N.nodes, d_err};
@@ -433,7 +582,7 @@ emr_status assemble(Build& B) {
     size_t tb = 0;
     NET_HIP(emr_net_sort(nullptr, &tb, keys.as<uint32_t>(), skeys.as<uint32_t>(),
                          vals.as<uint32_t>(), svals.as<uint32_t>(), (uint32_t)e_raw, bits, s));
-    NET_TRY(alloc(tmp, tb, "sort storage"));
+    NET_TRY(alloc(tmp, tb, "sort storage", s));
     NET_HIP(emr_net_sort(tmp.p, &tb, keys.as<uint32_t>(), skeys.as<uint32_t>(),
                          vals.as<uint32_t>(), svals.as<uint32_t>(), (uint32_t)e_raw, bits, s));
     emr::NetGatherArgs ga{skeys.as<uint32_t>(), svals.as<uint32_t>(), eu.as<uint32_t>(),
@@ -467,7 +616,7 @@ emr_status run_forward(const emr_networks* N, const float* patterns, int32_t n_p
     return failf(EMR_E_LIMIT, "networks: too many nodes x patterns");
   // two state buffers of [pblocks][nodes] float4
   const size_t half = (size_t)pblocks * (size_t)(N->nodes ? N->nodes : 1) * 16;
-  if (M.state.bytes < 2 * half) NET_TRY(alloc(M.state, 2 * half, "node states"));
+  if (M.state.bytes < 2 * half) NET_TRY(alloc(M.state, 2 * half, "node states", s));
   // patterns, then targets, staged in pinned memory and copied on the stream; the staging is
   // rewritten only after the previous call's copy has completed
   const size_t pat_bytes = (size_t)n_patterns * (size_t)N->n_in * 4;
@@ -487,7 +636,7 @@ emr_status run_forward(const emr_networks* N, const float* patterns, int32_t n_p
     }
     M.pin_bytes = need ? need : 16;
   }
-  if (M.patterns.bytes < need || !M.patterns.p) NET_TRY(alloc(M.patterns, need, "input patterns"));
+  if (M.patterns.bytes < need || !M.patterns.p) NET_TRY(alloc(M.patterns, need, "input patterns", s));
   std::memcpy(M.pin, patterns, pat_bytes);
   if (tgt_bytes) std::memcpy(static_cast<char*>(M.pin) + pat_bytes, targets, tgt_bytes);
   NET_HIP(hipMemcpyAsync(M.patterns.p, M.pin, need, hipMemcpyHostToDevice, s));
@@ -517,6 +666,41 @@ emr_status run_forward(const emr_networks* N, const float* patterns, int32_t n_p
   oa.n_patterns = (uint32_t)n_patterns;
   oa.pblocks = (uint32_t)pblocks;
   NET_HIP(emr_launch_net(11, &oa, 0, s));
+  if (!M.done) NET_HIP(hipEventCreateWithFlags(&M.done, hipEventDisableTiming));
+  NET_HIP(hipEventRecord(M.done, s));
+  M.done_pending = true;
+  return EMR_OK;
+}
+
+// Every phase and the assembly; synchronizes with the stream at the end.
+emr_status build_all(Build& B, int32_t n_substrate, int32_t iterations) {
+  emr_networks& N = *B.net;
+  NET_TRY(alloc(N.known, (size_t)N.n_genomes * (size_t)N.words * 4, "hidden-cell bitmaps", B.s));
+  NET_HIP(hipMemsetAsync(N.known.p, 0, N.known.bytes, B.s));
+  NET_TRY(alloc(N.d_slots, N.slots.size() * 4, "substrate slots", B.s));
+  NET_TRY(to_device(N.d_slots.p, N.slots.data(), N.slots.size() * 4, B.s));
+  std::vector<int32_t> out_node((size_t)N.n_out);
+  for (int32_t j = 0; j < n_substrate; ++j)
+    if (N.slots[(size_t)n_substrate + j] >= 0) out_node[(size_t)N.slots[(size_t)n_substrate + j]] = j;
+  NET_TRY(alloc(N.d_out_node, out_node.size() * 4, "output nodes", B.s));
+  NET_TRY(to_device(N.d_out_node.p, out_node.data(), out_node.size() * 4, B.s));
+
+  N.phases.push_back(std::make_unique<Phase>());
+  N.phases[0]->sources = N.substrate;
+  for (int32_t it = 0;; ++it) {
+    Phase& P = *N.phases.back();
+    NET_TRY(discover_phase(B, P));
+    const bool more = it < iterations;
+    auto next = more ? std::make_unique<Phase>() : nullptr;
+    int64_t n_new = 0;
+    NET_TRY(hidden_phase(B, P, next.get(), &n_new));
+    NET_TRY(express_phase(B, P));
+    P.ws.reset();
+    if (!more || n_new == 0) break;
+    N.phases.push_back(std::move(next));
+  }
+  NET_TRY(assemble(B));
+  NET_HIP(hipStreamSynchronize(B.s));
   return EMR_OK;
 }
 
@@ -569,32 +753,12 @@ emr_status emr_build_networks(const emr_population* pop, const emr_source* subst
   NET_HIP(hipGetDevice(&N.device));
   NET_TRY(emr_cell_words(depth, &N.words));
   Build B{pop, &N, theta, type_mask, w_min, (hipStream_t)stream};
-  NET_TRY(alloc(N.known, (size_t)N.n_genomes * (size_t)N.words * 4, "hidden-cell bitmaps"));
-  NET_HIP(hipMemsetAsync(N.known.p, 0, N.known.bytes, B.s));
-  NET_TRY(alloc(N.d_slots, N.slots.size() * 4, "substrate slots"));
-  NET_TRY(to_device(N.d_slots.p, N.slots.data(), N.slots.size() * 4, B.s));
-  std::vector<int32_t> out_node((size_t)N.n_out);
-  for (int32_t j = 0; j < n_substrate; ++j)
-    if (N.slots[(size_t)n_substrate + j] >= 0) out_node[(size_t)N.slots[(size_t)n_substrate + j]] = j;
-  NET_TRY(alloc(N.d_out_node, out_node.size() * 4, "output nodes"));
-  NET_TRY(to_device(N.d_out_node.p, out_node.data(), out_node.size() * 4, B.s));
-
-  N.phases.push_back(std::make_unique<Phase>());
-  N.phases[0]->sources = N.substrate;
-  for (int32_t it = 0;; ++it) {
-    Phase& P = *N.phases.back();
-    NET_TRY(discover_phase(B, P));
-    const bool more = it < iterations;
-    auto next = more ? std::make_unique<Phase>() : nullptr;
-    int64_t n_new = 0;
-    NET_TRY(hidden_phase(B, P, next.get(), &n_new));
-    NET_TRY(express_phase(B, P));
-    P.ws.reset();
-    if (!more || n_new == 0) break;
-    N.phases.push_back(std::move(next));
+  const emr_status st = build_all(B, n_substrate, iterations);
+  // after a failure, nothing queued may still use the buffers the handle gives back
+  if (st != EMR_OK) {
+    (void)hipStreamSynchronize(B.s);
+    return st;
   }
-  NET_TRY(assemble(B));
-  NET_HIP(hipStreamSynchronize(B.s));
   *out = net.release();
   return EMR_OK;
 }

@@ -55,7 +55,11 @@ __global__ void __launch_bounds__(256) k_hidden_mark(HiddenArgs A) {
     for (int64_t i = lo + lane; i < hi; i += kWave) {
       const uint32_t P = A.rec.parent[i];
       if ((int64_t)P >= Q) continue;
-      atomicOr(bits + P / 8u, 0xFu << (4u * (P % 8u)));  // grid positions 4P .. 4P+3
+      // grid positions 4P .. 4P+3; the many pairs of one genome mostly mark cells already marked,
+      // so a plain read first keeps them from queueing atomics on the same words
+      const uint32_t m = 0xFu << (4u * (P % 8u));
+      if ((__hip_atomic_load(bits + P / 8u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & m) != m)
+        atomicOr(bits + P / 8u, m);
     }
   }
 }
