@@ -372,6 +372,60 @@ def express(records, sources, depth: int, type_mask: int, w_min: float, n_genome
             "cell": np.array(cells, np.int64), "w": np.array(ws, np.float64)}
 
 
+def band_values(conn, genomes, sources, depth: int, src_offsets=None, neighbours=False):
+    """ES-HyperNEAT's band value of every expressed connection. Theorem 1 names a band threshold
+    beside the variance threshold and leaves its definition to ES-HyperNEAT, whose pruning step
+    keeps a point only when its weight stands out from its neighbours' on both sides along x or
+    along y. Here, for connection (pair r, cell C, weight w): C is the centre (x, y) of a level-l
+    cell of side d = 2^(1 - l) (its parent's half-width), and the pair's CPPN is queried, in the
+    pair's direction, at the four same-level neighbour centres (x - d, y), (x + d, y), (x, y - d),
+    (x, y + d); with dl, dr, dd, du the absolute differences between w and those four outputs,
+    band = max(min(dl, dr), min(dd, du)) (min and max ignore a NaN operand). conn: the CSR layout
+    of express() (pair_offset, cell, w; w as given). float64. Returns the band per connection, and
+    with neighbours=True also the [n, 4] neighbour outputs (left, right, down, up)."""
+    offs = np.asarray(conn["pair_offset"], np.int64)
+    n_pairs = len(offs) - 1
+    n_genomes = len(genomes)
+    gen, src = _pair_sources(sources, n_genomes, src_offsets)
+    assert len(gen) == n_pairs
+    n = int(offs[-1])
+    band = np.zeros(n, np.float64)
+    nb = np.zeros((n, 4), np.float64)
+    steps = np.array([[-1.0, 0.0], [1.0, 0.0], [0.0, -1.0], [0.0, 1.0]])
+    for r in range(n_pairs):
+        lo, hi = int(offs[r]), int(offs[r + 1])
+        if hi == lo:
+            continue
+        s = sources[int(src[r])]
+        sx, sy, d = float(s["x"]), float(s["y"]), int(s["dir"])
+        pts = []
+        for i in range(lo, hi):
+            x, y, lv = cell(int(conn["cell"][i]))
+            side = 2.0 * 0.5 ** lv
+            for k in range(4):
+                px, py = x + side * steps[k, 0], y + side * steps[k, 1]
+                pts.append((sx, sy, px, py, 1.0) if d == 0 else (px, py, sx, sy, 1.0))
+        vals = eval_points(genomes[int(gen[r])], np.array(pts)).reshape(-1, 4)
+        w = np.asarray(conn["w"][lo:hi], np.float64)[:, None]
+        dist = np.abs(w - vals)
+        band[lo:hi] = np.fmax(np.fmin(dist[:, 0], dist[:, 1]), np.fmin(dist[:, 2], dist[:, 3]))
+        nb[lo:hi] = vals
+    return (band, nb) if neighbours else band
+
+
+def band_filter(conn, band, theta_band: float):
+    """The connections whose band exceeds theta_band (strict; a NaN band never does), in their
+    order: dict(pair_count, pair_offset, cell, w) like express()."""
+    offs = np.asarray(conn["pair_offset"], np.int64)
+    keep = np.asarray(band) > theta_band
+    counts = np.array([int(keep[offs[r]:offs[r + 1]].sum()) for r in range(len(offs) - 1)],
+                      np.int64)
+    pair_offset = np.zeros(len(offs), np.int64)
+    np.cumsum(counts, out=pair_offset[1:])
+    return {"pair_count": counts, "pair_offset": pair_offset,
+            "cell": np.asarray(conn["cell"])[keep], "w": np.asarray(conn["w"])[keep]}
+
+
 # ----------------------------------------------------------------------------- networks
 # The networks the experiments evaluate (Section 5: XOR over its four input patterns), built from
 # the discovered substrate. The paper does not spell out this construction; the oracle follows
