@@ -199,7 +199,8 @@ emr_status emr_result_check(const emr_result* out, int64_t* total, int64_t* max_
                             void* stream);
 
 /* Waits for the latest call that wrote a CSR output through `workspace` on the current device
- * (emr_discover, emr_hidden_sources, emr_express, emr_chain_filter) and reports it like
+ * (emr_discover, emr_hidden_sources, emr_express, emr_chain_filter, emr_band_values,
+ * emr_band_filter) and reports it like
  * emr_result_check: EMR_E_DEVICE for a kernel error, EMR_E_CAPACITY when it found more than
  * `capacity` entries; *total and *max_count (largest per pair or per genome; either may be NULL).
  * emr_result_check(out, ...) is emr_call_check(out->workspace, out->capacity, ...). */
@@ -275,6 +276,38 @@ emr_status emr_express(const emr_population* pop, const emr_source* sources, int
                        const int32_t* src_offsets, int32_t n_shared, int32_t depth,
                        const emr_result* rec, int32_t type_mask, float w_min,
                        const emr_connections* out, void* stream);
+
+/* Workspace of emr_band_values: a 16-byte program entry per pair. Host only. */
+emr_status emr_band_workspace_bytes(int64_t n_pairs, int64_t* bytes);
+
+/*
+ * ES-HyperNEAT's band values of expressed connections (Theorem 1 names a band threshold beside the
+ * variance threshold and leaves it to ES-HyperNEAT, whose pruning step keeps a point whose weight
+ * stands out from its neighbours' on both sides along x or along y). For connection i of `conn`
+ * (the CSR output of emr_express for the same population, sources and depth: pair r, heap cell C
+ * with centre (x, y) at level l, weight w): the pair's CPPN at the same-level neighbour centres
+ * (x - d, y), (x + d, y), (x, y - d), (x, y + d), d = 2^(1-l) (exact in fp32), and
+ *   band[i] = max(min(|w - left|, |w - right|), min(|w - down|, |w - up|))
+ * in fp32 (fminf / fmaxf: a NaN operand is ignored). band: device, caller-owned, [conn->capacity]
+ * (entries past the connections are not written). conn->pair_count and conn->workspace are not
+ * used. `workspace` (device, >= emr_band_workspace_bytes(n_pairs), 256-byte aligned) holds the
+ * pairs' program entries. Enqueued on `stream`; check with emr_call_check(workspace, 0):
+ * EMR_E_DEVICE when a connection names no cell of the grid (its band is not written).
+ */
+emr_status emr_band_values(const emr_population* pop, const emr_source* sources,
+                           int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                           int32_t depth, const emr_connections* conn, float* band,
+                           void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * The band filter: the connections of `in` (n_pairs pairs, the layout of emr_express) whose band
+ * value (emr_band_values, device [in->capacity]) exceeds theta_band (strict; a NaN band never
+ * does), in their order, to `out` (its workspace at least emr_express_workspace_bytes(n_pairs)).
+ * theta_band < 0 keeps every connection with a band value that is not NaN. EMR_E_INVAL for a NaN
+ * theta_band. Check with emr_call_check(out->workspace, out->capacity).
+ */
+emr_status emr_band_filter(const emr_connections* in, const float* band, int64_t n_pairs,
+                           float theta_band, const emr_connections* out, void* stream);
 
 emr_status emr_chain_workspace_bytes(int64_t n_pairs, int32_t depth, int64_t* bytes);
 

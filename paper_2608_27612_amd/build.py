@@ -13,7 +13,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libemr.so")
 JIT_CO = os.path.join(HERE, "libemr_jit.co")
 SOURCES = ["kernels.hip", "phase2.hip", "runtime.cpp", "pack.cpp", "plan.cpp", "sched.cpp",
-           "jit.cpp", "jit_image.cpp", "record_file.cpp", "network.hip", "net_sort.hip",
+           "jit.cpp", "jit_image.cpp", "record_file.cpp", "network.hip", "net_sort.hip", "band.hip",
            "networks.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # No packed-FP32 instructions anywhere in the device code. Atomics stay as written: in the discover

@@ -6,12 +6,14 @@
 //     their cell centres (Eq. 1);
 //   connections (Section 4's types, Section 3.3's weight filter): each child of a kept parent as a
 //     connection, kept by its type and weight magnitude;
-//   Eq. 2 read literally: a record stays when every ancestor of its cell is a record of the pair.
+//   Eq. 2 read literally: a record stays when every ancestor of its cell is a record of the pair;
+//   the band filter: the connections whose band value (band.hip) exceeds a threshold.
 // Each output is CSR (k_scan in kernels.hip turns per-pair or per-genome totals into offsets).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "../../include/emr.h"
+#include "band.h"
 #include "discover.h"
 #include "emr_internal.h"
 
@@ -205,6 +207,35 @@ __global__ void __launch_bounds__(256) k_express(ExpressArgs A) {
   }
 }
 
+// ------------------------------------------------------------------------ band filter
+// Per pair (one wave): the connections with band > theta_band (strict; a NaN band never passes),
+// counted, then emitted in order at the pair's offset.
+template <bool EMIT>
+__global__ void __launch_bounds__(256) k_band_select(BandSelectArgs A) {
+  const uint32_t lane = lane_id();
+  FOR_EACH_PAIR_WAVE(pair, A.n_pairs) {
+    int64_t lo = A.in_offset[pair], hi = A.in_offset[pair + 1];
+    lo = lo < 0 ? 0 : (lo > A.in_cap ? A.in_cap : lo);
+    hi = hi > A.in_cap ? A.in_cap : (hi < lo ? lo : hi);
+    uint32_t total = 0;
+    const int64_t base = EMIT ? A.out_offset[pair] : 0;
+    for (int64_t b = lo; b < hi; b += kWave) {
+      const int64_t i = b + lane;
+      const bool keep = i < hi && A.band[i] > A.theta_band;
+      const uint64_t m = ballot(keep);
+      if constexpr (EMIT) {
+        const int64_t at = base + total + mbcnt64(m);
+        if (keep && at < A.out_cap) {
+          A.out_cell[at] = A.in_cell[i];
+          A.out_w[at] = A.in_w[i];
+        }
+      }
+      total += popc64(m);
+    }
+    if (!EMIT && lane == 0) A.totals[pair] = total;
+  }
+}
+
 // ------------------------------------------------------------------------ Eq. 2 chain rule
 __global__ void __launch_bounds__(256) k_chain_mark(ChainArgs A) {
   const uint32_t lane = lane_id();
@@ -283,6 +314,15 @@ extern "C" hipError_t emr_launch_express(const emr::ExpressArgs* A, int emit, hi
     hipLaunchKernelGGL(emr::k_express<true>, dim3(wave_blocks(A->rec.n_pairs)), dim3(256), 0, s, *A);
   else
     hipLaunchKernelGGL(emr::k_express<false>, dim3(wave_blocks(A->rec.n_pairs)), dim3(256), 0, s, *A);
+  return hipGetLastError();
+}
+
+extern "C" hipError_t emr_launch_band_select(const emr::BandSelectArgs* A, int emit,
+                                              hipStream_t s) {
+  if (emit)
+    hipLaunchKernelGGL(emr::k_band_select<true>, dim3(wave_blocks(A->n_pairs)), dim3(256), 0, s, *A);
+  else
+    hipLaunchKernelGGL(emr::k_band_select<false>, dim3(wave_blocks(A->n_pairs)), dim3(256), 0, s, *A);
   return hipGetLastError();
 }
 

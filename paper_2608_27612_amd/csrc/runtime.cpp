@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <atomic>
 #include <chrono>
+#include <cmath>
 #include <condition_variable>
 #include <cstdarg>
 #include <cstdio>
@@ -17,6 +18,7 @@
 #include <vector>
 
 #include "../../include/emr.h"
+#include "band.h"
 #include "emr_internal.h"
 #include "jit.h"
 #include "pack.h"
@@ -36,6 +38,9 @@ extern "C" hipError_t emr_launch_scan(const emr::ScanArgs* S, hipStream_t s);
 extern "C" hipError_t emr_launch_hidden(const emr::HiddenArgs* A, int step, hipStream_t s);
 extern "C" hipError_t emr_launch_express(const emr::ExpressArgs* A, int emit, hipStream_t s);
 extern "C" hipError_t emr_launch_chain(const emr::ChainArgs* A, int step, hipStream_t s);
+extern "C" hipError_t emr_launch_band(const emr::BandArgs* A, hipStream_t s);
+extern "C" hipError_t emr_launch_band_select(const emr::BandSelectArgs* A, int emit,
+                                              hipStream_t s);
 extern "C" hipError_t emr_launch_tile_geo(uint32_t* out, uint32_t tiles, uint32_t rows,
                                           hipStream_t s);
 extern "C" hipError_t emr_noalloc_scratch(void** out);
@@ -2035,6 +2040,109 @@ emr_status emr_express(const emr_population* pop, const emr_source* sources, int
   if ((st = scan_totals(A.totals, out->pair_count, out->pair_offset, P.n_pairs, f, s)) != EMR_OK)
     return st;
   if (P.n_pairs > 0) HIP_OR_FAIL(emr_launch_express(&A, 1, s));
+  f.ok = true;
+  return EMR_OK;
+}
+
+emr_status emr_band_workspace_bytes(int64_t n_pairs, int64_t* bytes) {
+  if (n_pairs < 0 || !bytes) return fail(EMR_E_INVAL, "bad arguments");
+  *bytes = (int64_t)align256((size_t)n_pairs * sizeof(emr::BandPair));
+  return EMR_OK;
+}
+
+emr_status emr_band_values(const emr_population* pop, const emr_source* sources,
+                           int32_t n_sources, const int32_t* src_offsets, int32_t n_shared,
+                           int32_t depth, const emr_connections* conn, float* band,
+                           void* workspace, int64_t workspace_bytes, void* stream) {
+  if (!conn) return fail(EMR_E_INVAL, "conn is NULL");
+  std::shared_ptr<const Plan> plan;
+  emr_status st = plan_for(pop, sources, n_sources, src_offsets, n_shared, depth, &plan);
+  if (st != EMR_OK) return st;
+  const Plan& P = *plan;
+  if (P.n_pairs > 0xFFFFFFFFll) return fail(EMR_E_LIMIT, "%lld pairs", (long long)P.n_pairs);
+  if (conn->capacity < 0 || !conn->pair_offset ||
+      (conn->capacity > 0 && (!conn->cell || !conn->w || !band)))
+    return fail(EMR_E_INVAL, "bad connection buffers");
+  if ((st = check_workspace(workspace, workspace_bytes,
+                            (int64_t)align256((size_t)P.n_pairs * sizeof(emr::BandPair)))) != EMR_OK)
+    return st;
+  // each pair's program, window and bias rows, from the group that holds it
+  std::vector<emr::BandPair> bp((size_t)P.n_pairs, emr::BandPair{0u, 0u, 0u, 0u});
+  for (const auto& bk : P.buckets)
+    for (uint32_t gi = bk.first; gi < bk.first + bk.count; ++gi) {
+      const emr::Group& G = P.groups[gi];
+      for (int k = 0; k < bk.S; ++k) {
+        const uint32_t pair = G.pair[k];
+        if ((int64_t)pair >= P.n_pairs) return fail(EMR_E_DEVICE, "plan: pair %u", pair);
+        if (k > 0 && pair == G.pair[k - 1]) break;  // (an unused slot repeats the last pair)
+        bp[pair] = emr::BandPair{G.var_off, (G.flags & 1u) ? G.n_rec : 0u, (uint32_t)bk.window,
+                                 G.bias_off + (uint32_t)k};
+      }
+    }
+  CallTables T;
+  if ((st = call_tables(pop, P, &T)) != EMR_OK) return st;
+  const hipStream_t s = (hipStream_t)stream;
+  CallFlags f;
+  if ((st = take_flags(workspace, s, &f)) != EMR_OK) return st;
+  if (P.n_pairs > 0) {
+    HIP_OR_FAIL(hipMemcpyAsync(workspace, bp.data(), bp.size() * sizeof(emr::BandPair),
+                               hipMemcpyHostToDevice, s));
+    HIP_OR_FAIL(hipStreamSynchronize(s));  // (bp is a host temporary)
+    emr::BandArgs A{};
+    A.blob = pop->d_blob;
+    A.bias = T.bias;
+    A.pairs = (const emr::BandPair*)workspace;
+    A.conn_offset = conn->pair_offset;
+    A.conn_cell = conn->cell;
+    A.conn_w = conn->w;
+    A.band = band;
+    A.err = f.dev + emr::kFlagErr;
+    A.cap = conn->capacity;
+    A.n_pairs = (uint32_t)P.n_pairs;
+    A.depth = depth;
+    A.blob_words = (uint32_t)pop->blob_words;
+    A.bias_floats = (uint32_t)P.bias_table_floats();
+    HIP_OR_FAIL(emr_launch_band(&A, s));
+  }
+  HIP_OR_FAIL(emr_launch_finalize(f.dev, f.host_dev, s));
+  f.ok = true;
+  return EMR_OK;
+}
+
+emr_status emr_band_filter(const emr_connections* in, const float* band, int64_t n_pairs,
+                           float theta_band, const emr_connections* out, void* stream) {
+  if (!in || !out) return fail(EMR_E_INVAL, "in or out is NULL");
+  if (n_pairs < 0 || n_pairs > 0xFFFFFFFFll) return fail(EMR_E_INVAL, "n_pairs %lld", (long long)n_pairs);
+  if (std::isnan(theta_band)) return fail(EMR_E_INVAL, "theta_band is NaN");
+  if (in->capacity < 0 || !in->pair_offset ||
+      (in->capacity > 0 && (!in->cell || !in->w || !band)))
+    return fail(EMR_E_INVAL, "bad input connections");
+  if (out->capacity < 0 || !out->pair_offset || (n_pairs > 0 && !out->pair_count) ||
+      (out->capacity > 0 && (!out->cell || !out->w)))
+    return fail(EMR_E_INVAL, "bad output connections");
+  emr_status st = check_workspace(out->workspace, out->workspace_bytes,
+                                  (int64_t)align256((size_t)n_pairs * 4));
+  if (st != EMR_OK) return st;
+  const hipStream_t s = (hipStream_t)stream;
+  CallFlags f;
+  if ((st = take_flags(out->workspace, s, &f)) != EMR_OK) return st;
+  emr::BandSelectArgs A{};
+  A.in_offset = in->pair_offset;
+  A.in_cell = in->cell;
+  A.in_w = in->w;
+  A.band = band;
+  A.in_cap = in->capacity;
+  A.theta_band = theta_band;
+  A.totals = (uint32_t*)out->workspace;
+  A.out_offset = out->pair_offset;
+  A.out_cell = out->cell;
+  A.out_w = out->w;
+  A.out_cap = out->capacity;
+  A.n_pairs = (uint32_t)n_pairs;
+  if (n_pairs > 0) HIP_OR_FAIL(emr_launch_band_select(&A, 0, s));
+  if ((st = scan_totals(A.totals, out->pair_count, out->pair_offset, n_pairs, f, s)) != EMR_OK)
+    return st;
+  if (n_pairs > 0) HIP_OR_FAIL(emr_launch_band_select(&A, 1, s));
   f.ok = true;
   return EMR_OK;
 }

@@ -28,7 +28,8 @@ ABI_FUNCTIONS = [
     "emr_profile_read", "emr_stream_chunks", "emr_discover_stream", "emr_pack_population_flat",
     "emr_set_jit", "emr_jit_info", "emr_eval_raw_noalloc", "emr_call_check", "emr_cell_words",
     "emr_hidden_workspace_bytes", "emr_hidden_sources", "emr_express_workspace_bytes",
-    "emr_express", "emr_chain_workspace_bytes", "emr_chain_filter", "emr_record_file_open",
+    "emr_express", "emr_chain_workspace_bytes", "emr_chain_filter", "emr_band_workspace_bytes",
+    "emr_band_values", "emr_band_filter", "emr_record_file_open",
     "emr_record_file_sink", "emr_record_file_close", "emr_build_networks", "emr_networks_info",
     "emr_networks_phase", "emr_activate", "emr_xor_fitness", "emr_free_networks",
     "emr_copy_to_host",
@@ -141,6 +142,9 @@ def lib():
             "emr_express": (I32, [P, P, I32, P, I32, I32, P, I32, F32, P, P]),
             "emr_chain_workspace_bytes": (I32, [I64, I32, P]),
             "emr_chain_filter": (I32, [P, I64, I32, P, P]),
+            "emr_band_workspace_bytes": (I32, [I64, P]),
+            "emr_band_values": (I32, [P, P, I32, P, I32, I32, P, P, P, I64, P]),
+            "emr_band_filter": (I32, [P, P, I64, F32, P, P]),
             "emr_record_file_open": (I32, [C.c_char_p, I64, I32, I64, P, P]),
             "emr_record_file_sink": (I32, [I64, I64, P, P, I64, P]),
             "emr_record_file_close": (I32, [P, P, P]),
@@ -713,6 +717,58 @@ def emr_express(pop: Population, sources, depth: int, rec, type_mask: int = EMR_
                              C.byref(st), _stream_ptr(stream)))
     out["total"], _ = emr_call_check(ws, cap, stream)
     out["n_pairs"] = n_pairs
+    out["capacity"] = cap
+    return out
+
+
+def _conn_struct(conn, workspace=None):
+    ws_ptr, ws_n = (0, 0) if workspace is None else (workspace.data_ptr(), workspace.numel())
+    return emr_connections(conn["cell"].data_ptr(), conn["w"].data_ptr(), conn["capacity"],
+                           conn["pair_count"].data_ptr(), conn["pair_offset"].data_ptr(),
+                           ws_ptr, ws_n)
+
+
+def emr_band_values(pop: Population, sources, depth: int, conn, src_offsets=None, stream=None):
+    """ES-HyperNEAT band values of the connections of a checked emr_express result `conn` (see
+    emr_band_values in include/emr.h), checked; a float32 device tensor aligned with conn's
+    entries."""
+    import torch
+    n_pairs = conn["n_pairs"]
+    wsb = C.c_int64()
+    _check(lib().emr_band_workspace_bytes(n_pairs, C.byref(wsb)))
+    ws = torch.empty(max(wsb.value, 256), dtype=torch.uint8, device="cuda")
+    band = torch.empty(max(conn["capacity"], 1), dtype=torch.float32, device="cuda")
+    offs = _offsets(src_offsets)
+    src = _sources(sources)
+    st = _conn_struct(conn)
+    _check(lib().emr_band_values(pop.handle, src.ctypes.data, len(sources),
+                                 None if offs is None else offs.ctypes.data,
+                                 0 if offs is not None else len(sources), depth, C.byref(st),
+                                 C.c_void_p(band.data_ptr()), C.c_void_p(ws.data_ptr()),
+                                 ws.numel(), _stream_ptr(stream)))
+    emr_call_check(ws, 0, stream)
+    return band
+
+
+def emr_band_filter(conn, band, theta_band: float, capacity=None, stream=None):
+    """The connections of `conn` whose band value exceeds theta_band (see emr_band_filter in
+    include/emr.h), checked; a dict of the emr_express form."""
+    import torch
+    n_pairs = conn["n_pairs"]
+    cap = int(conn["total"]) if capacity is None else int(capacity)
+    wsb = C.c_int64()
+    _check(lib().emr_express_workspace_bytes(n_pairs, C.byref(wsb)))
+    ws = torch.empty(max(wsb.value, 256), dtype=torch.uint8, device="cuda")
+    out = {"cell": torch.empty(max(cap, 1), dtype=torch.int32, device="cuda"),
+           "w": torch.empty(max(cap, 1), dtype=torch.float32, device="cuda"),
+           "pair_count": torch.empty(max(n_pairs, 1), dtype=torch.int64, device="cuda"),
+           "pair_offset": torch.empty(n_pairs + 1, dtype=torch.int64, device="cuda"),
+           "capacity": cap, "n_pairs": n_pairs}
+    st_in = _conn_struct(conn)
+    st_out = _conn_struct(out, ws)
+    _check(lib().emr_band_filter(C.byref(st_in), C.c_void_p(band.data_ptr()), n_pairs,
+                                 C.c_float(theta_band), C.byref(st_out), _stream_ptr(stream)))
+    out["total"], _ = emr_call_check(ws, cap, stream)
     return out
 
 

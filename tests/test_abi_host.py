@@ -118,3 +118,18 @@ def test_network_calls_refuse_null_arguments():
     assert L.emr_copy_to_host(None, None, -1, None) == emr.EMR_E_INVAL
     assert L.emr_copy_to_host(None, None, 0, None) == emr.EMR_OK
     L.emr_free_networks(None)
+
+
+def test_band_calls_refuse_bad_arguments():
+    """Checked on the host before any device work."""
+    L = emr.lib()
+    b = C.c_int64()
+    assert L.emr_band_workspace_bytes(-1, C.byref(b)) == emr.EMR_E_INVAL
+    assert L.emr_band_workspace_bytes(1000, C.byref(b)) == emr.EMR_OK and b.value == 16128
+    subs = W.xor_sources()
+    assert L.emr_band_values(None, subs.ctypes.data, 4, None, 4, 5, None, None, None, 0,
+                             None) == emr.EMR_E_INVAL
+    assert L.emr_band_filter(None, None, 4, C.c_float(0.1), None, None) == emr.EMR_E_INVAL
+    conn = emr.emr_connections(0, 0, 0, 0, 0, 0, 0)
+    assert L.emr_band_filter(C.byref(conn), None, -1, C.c_float(0.1), C.byref(conn),
+                             None) == emr.EMR_E_INVAL

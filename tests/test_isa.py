@@ -17,13 +17,14 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "paper_2608_27612_amd", "csrc", "kernels.hip")
 
 
-@pytest.fixture(scope="module")
-def asm():
+@pytest.fixture(scope="module", params=["kernels.hip", "band.hip"])
+def asm(request):
+    """The kernels that run the interpreter's record step: discovery, and the band values."""
     from paper_2608_27612_amd import build
     with tempfile.TemporaryDirectory() as d:
         out = os.path.join(d, "k.s")
         cmd = [build.HIPCC, "-O3", "-std=c++17", "--cuda-device-only", "-S"] + build.DEVICE_FLAGS \
-            + [SRC, "-o", out]
+            + [os.path.join(os.path.dirname(SRC), request.param), "-o", out]
         subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
         return open(out).read()
 
@@ -94,12 +95,13 @@ def test_m0_only_for_register_indexing(asm):
 
 
 def test_discover_kernels_use_no_scratch(asm):
-    ks = {k: v for k, v in _kernels(asm).items() if "k_discover" in k}
-    assert len(ks) == 2   # one per output mode
+    ks = {k: v for k, v in _kernels(asm).items() if "k_discover" in k or "k_band" in k}
+    assert len(ks) in (1, 2)   # one per output mode, or the band kernel
     for name, body in ks.items():
         assert "scratch_" not in body and "buffer_store" not in body, name
-    sizes = re.findall(r"\.name:\s+(\S*k_discover\S*)\s*\n(?:.*\n)*?\s+\.private_segment_fixed_size:\s+(\d+)",
-                       asm)
+    sizes = re.findall(r"\.name:\s+(\S*k_(?:discover|band)\S*)\s*\n(?:.*\n)*?"
+                       r"\s+\.private_segment_fixed_size:\s+(\d+)", asm)
+    assert sizes
     for name, size in sizes:
         assert int(size) == 0, name
 
@@ -133,7 +135,8 @@ def test_scc_is_not_carried_across_inline_asm(asm):
             assert not _SCC_READERS.match(code), "SCC read after inline asm: " + code.strip()
             if _SCC_WRITERS.match(code) or re.match(r"^\s*s_(branch|endpgm|setpc)", code):
                 break
-    assert blocks >= 18
+    # every record-step walk of the file: 18+ in the discover kernels, 4 in the band kernel
+    assert blocks >= (18 if "k_discover" in asm else 4)
 
 
 def test_record_step_clobbers_scc_and_m0():
