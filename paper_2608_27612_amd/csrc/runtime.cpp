@@ -249,6 +249,8 @@ namespace {
 
 using emr::window_bucket;
 
+void wait_library_calls(int dev);
+
 // The compiled tier of one plan: its groups' programs translated to machine code, written into the
 // code area of a copy of the template code object, loaded as a module on one device.
 struct JitModule {
@@ -264,13 +266,14 @@ struct JitModule {
   JitModule(const JitModule&) = delete;
   JitModule& operator=(const JitModule&) = delete;
   ~JitModule() {
-    // Nothing queued may still run the module's code or read its tables, so the device drains
-    // first (a module goes only when its plan is replaced or its population freed).
+    // Nothing queued may still run the module's code or read its tables, so every call the
+    // library has enqueued on the module's device finishes first (a module goes only when its
+    // plan is replaced or its population freed).
     if (!mod && !d_groups) return;
     int cur = -1;
     (void)hipGetDevice(&cur);
     if (device >= 0 && cur != device) (void)hipSetDevice(device);
-    (void)hipDeviceSynchronize();
+    wait_library_calls(device);
     if (d_groups) (void)hipFree(d_groups);
     if (mod) (void)hipModuleUnload(mod);
     if (device >= 0 && cur >= 0 && cur != device) (void)hipSetDevice(cur);
@@ -557,6 +560,21 @@ emr_status flag_ring(FlagRing** out) {
   g_rings.push_back({dev, R.get()});
   *out = R.release();
   return EMR_OK;
+}
+
+// Waits for every call the library has enqueued on device `dev`: each call's last kernel is
+// followed by its flag slot's event, and a slot is taken again only after its previous call's
+// event has completed, so the slots' latest events cover every call ever enqueued.
+void wait_library_calls(int dev) {
+  std::vector<hipEvent_t> evs;
+  {
+    std::lock_guard<std::mutex> lock(g_ring_mu);
+    for (const auto& e : g_rings)
+      if (e.first == dev)
+        for (int k = 0; k < kFlagSlots; ++k)
+          if (e.second->pending[k]) evs.push_back(e.second->done[k]);
+  }
+  for (hipEvent_t ev : evs) (void)hipEventSynchronize(ev);
 }
 
 // One call's slot: taken before its first kernel, given back after its last (or on failure).
