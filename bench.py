@@ -13,7 +13,8 @@ is resident in HBM before timing starts. Printed as one JSON line:
   roofline     the discover kernel (one launch per step, every query of the step):
                algorithmic VALU lane-slots (cost model of emr_discover_cost: one slot per fp32
                FMA / add / mul, transcendentals weighted by their measured 1/4 rate) / its
-               HIP-event duration (an event pair around the launch in every 4th timed step), against
+               HIP-event duration (an event pair around the launch in every 4th step of a second
+               run of the same steps, so that the host-clock steps carry no events), against
                the chip's fp32 vector peak: 157.3 TFLOP/s = 78.64 T lane-slots/s (an FMA is one
                slot, two flops); flops / frac_flops: the useful floating-point operations (2 per
                multiply-add, 1 per other operation) over the same duration, against 157.3 TFLOP/s;
@@ -110,18 +111,22 @@ def roofline(work, kernel_ms_per_step, records, kernel, workload):
 
 
 def timed_steps(emr, torch, step, steps, warmup, rT):
-    """Runs `step` warmup + steps times; the timed steps time their discover launches with a HIP
-    event pair in every TIME_EVERY-th step (the first, then every TIME_EVERY-th). Returns
-    (ms per step on the host clock, the launches' summed ms per timed step, launch records)."""
+    """Runs `step` warmup + steps times on the host clock (no events in these steps), then the
+    same number of steps again with a HIP event pair around the discover launch of every
+    TIME_EVERY-th step (the first, then every TIME_EVERY-th). Returns (ms per step on the host
+    clock, the launches' summed ms per timed step, launch records)."""
     for _ in range(warmup):
         step()
-    emr.emr_profile_enable(True, rT, every=TIME_EVERY)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    emr.emr_profile_enable(True, rT, every=TIME_EVERY)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
     recs = emr.emr_profile_read()
     emr.emr_profile_enable(False)
     per_call = {}

@@ -165,9 +165,12 @@ typedef struct {
  * this population, these sources (host) and this depth: per-tile status words, the compaction's
  * tile-group marks and per-pair look-back words, the folded per-(genome, source) biases, and a
  * record pool of `capacity` records (20 bytes each) that the discover kernel fills in any order
- * and the compaction gathers from. The library keeps no state in it from one call to the next (a
- * call's error flags, largest count and total live in a library-owned slot, see
- * emr_result_check). EMR_E_INVAL for a capacity outside [0, 2^32 - 1]. Host only. (The grouping
+ * and the compaction gathers from. A call's error flags, largest count and total live in a
+ * library-owned slot (see emr_result_check). A record call leaves the workspace's counters cleared,
+ * and the next record call with the same workspace, plan (population, sources, depth), capacity
+ * and stream does not clear them again: do not write into a workspace between calls (any other
+ * call with it, or a change of any of those, makes the next call clear it first). EMR_E_INVAL for
+ * a capacity outside [0, 2^32 - 1]. Host only. (The grouping
  * tables of a call live with the population: it keeps those of its last sources and depth on the
  * device, and a call with different ones replaces them.) */
 emr_status emr_workspace_bytes(const emr_population* pop, const emr_source* sources,

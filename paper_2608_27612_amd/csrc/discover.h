@@ -50,6 +50,19 @@ __device__ __forceinline__ uint32_t lane_id_here() {
   return l;
 }
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+// A 64-bit value of lane i (uniform i) / of the first active lane. The lane builtins return int:
+// each half is taken as unsigned before widening (a sign-extended low half would set the high
+// word whenever its bit 31 is set).
+__device__ __forceinline__ uint64_t read_lane64(uint64_t v, uint32_t i) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, (int)i);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), (int)i);
+  return ((uint64_t)hi << 32) | (uint64_t)lo;
+}
+__device__ __forceinline__ uint64_t first_lane64(uint64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | (uint64_t)lo;
+}
 __device__ __forceinline__ uint32_t popc64(uint64_t m) { return __builtin_popcountll(m); }
 __device__ __forceinline__ uint32_t mbcnt64(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
@@ -388,8 +401,7 @@ __device__ __forceinline__ void discover_chunk(uint32_t c, const DiscoverPart& p
         uint64_t off = 0;
         if (lane == 0)
           off = atomicAdd((unsigned long long*)a.pool_ctr, (unsigned long long)n_walk);
-        off = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(off >> 32)) << 32) |
-              __builtin_amdgcn_readfirstlane((uint32_t)off);
+        off = first_lane64(off);
 #pragma unroll
         for (int s = 0; s < S; ++s)
 #pragma unroll

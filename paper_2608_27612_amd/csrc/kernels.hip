@@ -197,8 +197,7 @@ __device__ __forceinline__ void move_group(const MoveArgs& A, uint64_t w, uint32
       const uint32_t hi = __builtin_amdgcn_readlane(incl, i);
       const uint32_t lo = hi - __builtin_amdgcn_readlane(c, i);
       if (q >= lo && q < hi) {
-        const uint64_t wi = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(w >> 32), i) << 32) |
-                            __builtin_amdgcn_readlane((uint32_t)w, i);
+        const uint64_t wi = read_lane64(w, i);
         src = (wi >> kStatusCountBits) + (q - lo);
       }
     }
@@ -223,8 +222,7 @@ __device__ __forceinline__ void for_marked_groups(const MoveArgs& A, uint32_t pa
     if (mine && bits != 0ull) words[w0 + lane] = 0ull;
     for (uint64_t lanes = ballot(bits != 0ull); lanes != 0ull; lanes &= lanes - 1ull) {
       const uint32_t i = (uint32_t)__builtin_ctzll(lanes);
-      uint64_t bw = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(bits >> 32), i) << 32) |
-                    __builtin_amdgcn_readlane((uint32_t)bits, i);
+      uint64_t bw = read_lane64(bits, i);
       for (; bw != 0ull; bw &= bw - 1ull) {
         const uint32_t g = (w0 + i) * kWave + (uint32_t)__builtin_ctzll(bw);
         if (g < n_groups) f(g);

@@ -282,7 +282,11 @@ struct JitModule {
 
 // Everything one discover / raw-eval call needs besides the population: the host-built tables
 // (emr::PlanTables) and their device copies, schedules and compiled tier.
+std::atomic<uint64_t> g_plan_ids{0};
+
 struct Plan : emr::PlanTables {
+  // Distinct for every plan the process builds (a freed plan's address may be reused).
+  const uint64_t id = ++g_plan_ids;
   mutable std::mutex dev_mu;
   // The tables' device copy, uploaded on first use and freed with the plan.
   mutable char* d_tables = nullptr;
@@ -1175,6 +1179,45 @@ emr_status call_tables(const emr_population* pop, const Plan& P, CallTables* T) 
   return tile_geo_table(P.depth, &T->geo, &T->geo_rows);
 }
 
+// Workspaces whose counters a record call left cleared: its k_scan zeroes every pair total and
+// its k_move every tile-group mark, so the next record call of the same plan on the same stream
+// (stream order puts it after those kernels) needs no clearing launch. Any other call with the
+// workspace forgets it. (A few entries: the latest workspaces of the process.)
+struct CleanWorkspace {
+  const void* ws;
+  uint64_t plan;
+  hipStream_t s;
+  int64_t capacity;
+};
+std::mutex g_clean_mu;
+std::vector<CleanWorkspace> g_clean;
+constexpr size_t kCleanEntries = 64;
+
+bool workspace_clean(const void* ws, const Plan& P, hipStream_t s, int64_t capacity) {
+  std::lock_guard<std::mutex> lock(g_clean_mu);
+  for (const CleanWorkspace& c : g_clean)
+    if (c.ws == ws) return c.plan == P.id && c.s == s && c.capacity == capacity;
+  return false;
+}
+void workspace_forget(const void* ws) {
+  std::lock_guard<std::mutex> lock(g_clean_mu);
+  for (size_t i = 0; i < g_clean.size(); ++i)
+    if (g_clean[i].ws == ws) {
+      g_clean.erase(g_clean.begin() + (std::ptrdiff_t)i);
+      return;
+    }
+}
+void workspace_mark_clean(const void* ws, const Plan& P, hipStream_t s, int64_t capacity) {
+  std::lock_guard<std::mutex> lock(g_clean_mu);
+  for (CleanWorkspace& c : g_clean)
+    if (c.ws == ws) {
+      c = CleanWorkspace{ws, P.id, s, capacity};
+      return;
+    }
+  if (g_clean.size() >= kCleanEntries) g_clean.erase(g_clean.begin());
+  g_clean.push_back(CleanWorkspace{ws, P.id, s, capacity});
+}
+
 // Enqueue a whole call: take a flag slot, then every tile of every pair.
 emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const emr_result* out,
                     float* raw, void* workspace, int64_t workspace_bytes, hipStream_t s) {
@@ -1187,9 +1230,14 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
   if ((st = take_flags(workspace, s, &f)) != EMR_OK) return st;
   bool jit = false;
   if ((st = jit_use(pop, P, plan_slots(P), &jit)) != EMR_OK) return st;
+  const bool records = out != nullptr && raw == nullptr;
+  const int64_t capacity = records ? out->capacity : -1;
+  const bool clean = false && workspace_clean(workspace, P, s, capacity);
+  workspace_forget(workspace);
   st = launch_range(pop, P, T, theta, out, raw, workspace, s, 0, P.tiles, jit, f.dev, f.host_dev,
-                    true, true);
+                    true, !clean);
   if (st != EMR_OK) return st;
+  if (records) workspace_mark_clean(workspace, P, s, capacity);
   f.ok = true;
   return EMR_OK;
 }
