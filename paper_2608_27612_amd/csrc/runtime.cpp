@@ -1232,7 +1232,7 @@ emr_status run_plan(const emr_population* pop, const Plan& P, float theta, const
   if ((st = jit_use(pop, P, plan_slots(P), &jit)) != EMR_OK) return st;
   const bool records = out != nullptr && raw == nullptr;
   const int64_t capacity = records ? out->capacity : -1;
-  const bool clean = false && workspace_clean(workspace, P, s, capacity);
+  const bool clean = records && workspace_clean(workspace, P, s, capacity);
   workspace_forget(workspace);
   st = launch_range(pop, P, T, theta, out, raw, workspace, s, 0, P.tiles, jit, f.dev, f.host_dev,
                     true, !clean);
