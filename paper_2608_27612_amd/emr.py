@@ -309,6 +309,21 @@ def _sources(sources):
     return arr if len(arr) else _NO_SOURCE
 
 
+_SRC_LAST = [None, None, 0]  # the last sources object passed, its record array and address
+
+
+def _sources_ptr(sources):
+    """(record array, its address) of _sources(sources); a repeated call with the same array
+    object reuses the address (an array's data never moves while the cache holds it)."""
+    if sources is _SRC_LAST[0]:
+        return _SRC_LAST[1], _SRC_LAST[2]
+    arr = _sources(sources)
+    ptr = arr.ctypes.data
+    if isinstance(sources, np.ndarray):
+        _SRC_LAST[0], _SRC_LAST[1], _SRC_LAST[2] = sources, arr, ptr
+    return arr, ptr
+
+
 def _offsets(src_offsets):
     if src_offsets is None:
         return None
@@ -370,10 +385,15 @@ def emr_discover(pop: Population, sources, depth: int, theta: float, res=None, s
     if res is None:
         res = alloc_result(pop, sources, depth, src_offsets, capacity)
     offs = _offsets(src_offsets)
-    out = _result_struct(res)
-    res["_struct"] = out
-    src = _sources(sources)
-    _check(lib().emr_discover(pop.handle, src.ctypes.data, len(sources),
+    out = res.get("_struct")
+    if out is None or out.parent != res["parent"].data_ptr() or \
+            out.workspace != res["workspace"].data_ptr() or out.w4 != res["w4"].data_ptr() or \
+            out.pair_offset != res["pair_offset"].data_ptr() or \
+            out.pair_count != res["pair_count"].data_ptr() or out.capacity != res["capacity"]:
+        out = _result_struct(res)
+        res["_struct"] = out
+    src, src_ptr = _sources_ptr(sources)
+    _check(lib().emr_discover(pop.handle, src_ptr, len(sources),
                               None if offs is None else offs.ctypes.data,
                               0 if offs is not None else len(sources), depth,
                               C.c_float(theta), C.byref(out), _stream_ptr(stream)))
@@ -381,10 +401,18 @@ def emr_discover(pop: Population, sources, depth: int, theta: float, res=None, s
 
 
 def emr_result_check(res, stream=None):
-    """Synchronize and check a discover result; returns (total records, largest pair count)."""
+    """Synchronize and check a discover result; returns (total records, largest pair count).
+    (The check waits for the call through its workspace's flag slot; a stream is passed only when
+    the caller names one.)"""
     out = res.get("_struct") or _result_struct(res)
-    total, mx = C.c_int64(), C.c_int64()
-    _check(lib().emr_result_check(C.byref(out), C.byref(total), C.byref(mx), _stream_ptr(stream)))
+    chk = res.get("_check_args")
+    if chk is None or chk[0] is not out:
+        total, mx = C.c_int64(), C.c_int64()
+        chk = (out, total, mx, C.byref(out), C.byref(total), C.byref(mx))
+        res["_check_args"] = chk
+    _, total, mx, p_out, p_total, p_mx = chk
+    _check(lib().emr_result_check(p_out, p_total, p_mx,
+                                  None if stream is None else _stream_ptr(stream)))
     return total.value, mx.value
 
 
