@@ -3,10 +3,17 @@
 
 One step = one emr_discover call over the whole workload (the sources' bias rows are the plan's,
 every (genome, source, position) is queried, the variance filter is applied and the kept cells are
-compacted per pair) plus emr_result_check (the synchronizing count check). The packed population
-is resident in HBM before timing starts. Printed as one JSON line:
+compacted per pair) plus emr_result_check (the synchronizing count check) of that call. The packed
+population is resident in HBM before timing starts. The timed steps keep two calls in flight: two
+result buffers (each with its workspace) alternate on two streams (default priority), and call i is
+checked after call i + 1 has been enqueued, so the host's check and enqueue, one call's compaction
+and the last workgroups of its discover launch overlap the other call's work instead of leaving the
+GPU idle between calls; every call is still checked. Printed as one JSON line:
 
-  value        CPPN queries per second over the timed steps (host clock, synchronized)
+  value        CPPN queries per second over the timed steps (host clock, synchronized at both
+               ends of the timed region)
+  ms_per_step_sync  the same steps one at a time (each call checked before the next is enqueued):
+               the latency of one synchronous call
   evaluated_queries_per_s  the same for the queries of position-dependent pairs only (a pair
                whose CPPN output does not depend on the position is answered by its per-source
                constant, exactly, without a per-position evaluation)
@@ -123,17 +130,43 @@ def timed_steps(emr, torch, step, steps, warmup, rT):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    recs = event_timed(emr, torch, step, steps, rT)
+    per_call = {}
+    for r in recs:
+        per_call[r["call"]] = per_call.get(r["call"], 0.0) + r["ms"]
+    assert len(per_call) == (steps + TIME_EVERY - 1) // TIME_EVERY
+    return (t1 - t0) * 1e3 / steps, float(np.mean(list(per_call.values()))), recs
+
+
+def event_timed(emr, torch, step, steps, rT):
+    """`steps` steps with a HIP event pair around every TIME_EVERY-th step's discover launch."""
     emr.emr_profile_enable(True, rT, every=TIME_EVERY)
     for _ in range(steps):
         step()
     torch.cuda.synchronize()
     recs = emr.emr_profile_read()
     emr.emr_profile_enable(False)
-    per_call = {}
-    for r in recs:
-        per_call[r["call"]] = per_call.get(r["call"], 0.0) + r["ms"]
-    assert len(per_call) == (steps + TIME_EVERY - 1) // TIME_EVERY
-    return (t1 - t0) * 1e3 / steps, float(np.mean(list(per_call.values()))), recs
+    return recs
+
+
+def pipelined_steps(torch, enqueue, check, steps, warmup):
+    """warmup, then `steps` timed steps two calls deep: enqueue(i) starts call i into buffer
+    i % 2 on stream i % 2, check(i) synchronizes with call i and checks it; call i is checked
+    right after call i + 1 is enqueued (the buffer of call i is enqueued again only after its
+    check). Returns ms per step on the host clock."""
+    def run(n):
+        enqueue(0)
+        for i in range(1, n):
+            enqueue(i)
+            check(i - 1)
+        check(n - 1)
+    if warmup > 0:
+        run(warmup)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(steps)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
 
 
 def measure_call(emr, torch, name, steps, warmup, rT):
@@ -148,13 +181,25 @@ def measure_call(emr, torch, name, steps, warmup, rT):
     def step():
         emr.emr_discover(pop, sources, depth, theta32, res=res)
         emr.emr_result_check(res)
-    ms, kms, recs = timed_steps(emr, torch, step, steps, warmup, rT)
+    ms_sync, kms, recs = timed_steps(emr, torch, step, steps, warmup, rT)
     compiled = {r["compiled"] for r in recs}
     assert len(compiled) == 1, "the timed steps ran both tiers"
     kernel = "emr_discover_jit_records" if compiled == {True} else "k_discover<1>"
     records = int(res["pair_offset"][-1].item())
+    # the pipelined steps: a second result buffer beside the first, one stream each
+    bufs = [res, emr.alloc_result(pop, sources, depth)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    totals = []
+
+    def enqueue(i):
+        emr.emr_discover(pop, sources, depth, theta32, res=bufs[i & 1], stream=streams[i & 1])
+
+    def check(i):
+        totals.append(emr.emr_result_check(bufs[i & 1])[0])
+    ms = pipelined_steps(torch, enqueue, check, steps, warmup)
+    assert set(totals) == {records}, "a pipelined call found a different record count"
     out = {"workload": name, "genomes": len(genomes), "sources": len(sources), "depth": depth,
-           "theta": theta, "steps": steps, "ms_per_step": ms,
+           "theta": theta, "steps": steps, "ms_per_step": ms, "ms_per_step_sync": ms_sync,
            "queries_per_step": int(work["queries"]), "records_per_step": records,
            "queries_per_s": work["queries"] / (ms * 1e-3),
            "evaluated_queries_per_s": work["evaluated"] / (ms * 1e-3),
@@ -426,6 +471,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "ms_per_step_sync": main_line["ms_per_step_sync"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

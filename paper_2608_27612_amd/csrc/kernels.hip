@@ -101,11 +101,19 @@ constexpr int kScanPer = 4;  // consecutive pairs per thread and round
 // from round + kScanPer t (their loads issued together). Writes pair_count, pair_offset
 // (exclusive scan, pair_offset[n_pairs] = the total), clears the totals for the next launch,
 // resets the pool counter, raises the largest count and stores the total in the flags, and, with
-// A.host, hands the flags over.
+// A.host, hands the flags over. No other kernel writes the flag words while this one runs (the
+// call's kernels are ordered on its stream and this is the only writer of the largest count), so
+// thread 0 reads the words it needs together with the first round's totals and writes the final
+// values without reading them again: the kernel waits for memory once before its stores.
 __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs A) {
   __shared__ uint64_t wsum[kScanThreads / kWave];
   __shared__ uint32_t wmax[kScanThreads / kWave];
   const uint32_t t = threadIdx.x, lane = t % kWave, wv = t / kWave;
+  uint32_t f_err = 0, f_max = 0;
+  if (t == 0) {
+    f_err = __hip_atomic_load(A.flags + kFlagErr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    f_max = __hip_atomic_load(A.flags + kFlagMax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   uint64_t carry = 0;
   uint32_t mx = 0;
   for (uint32_t round = 0; round < A.n_pairs; round += kScanThreads * kScanPer) {
@@ -151,19 +159,28 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs A) {
   if (lane == 0) wmax[wv] = mx;
   __syncthreads();
   if (t == 0) {
-    uint32_t m = 0;
+    uint32_t m = f_max;
     for (int k = 0; k < kScanThreads / kWave; ++k) m = max(m, wmax[k]);
     A.pair_offset[A.n_pairs] = (int64_t)carry;
-    if (A.host_counts)
-      A.host_counts[A.n_pairs] =
-          __hip_atomic_load(A.flags + kFlagErr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    raise_max(A.flags + kFlagMax, m);
-    __hip_atomic_store((uint64_t*)(A.flags + kFlagTotal), carry, __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-    // every record of the range is in the pool: a next range reserves from 0
-    __hip_atomic_store((uint64_t*)(A.flags + kFlagPool), 0ull, __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-    if (A.host) hand_over_flags(A.flags, A.host);
+    if (A.host_counts) A.host_counts[A.n_pairs] = f_err;
+    if (A.host) {
+      // the call's last flag writes: its words go to the host and are cleared for the slot's
+      // next call (the pool counter included: every record of the range is in the pool)
+      A.host[kFlagErr] = f_err;
+      A.host[kFlagMax] = m;
+      A.host[kFlagTotal] = (uint32_t)carry;
+      A.host[kFlagTotal + 1] = (uint32_t)(carry >> 32);
+#pragma unroll
+      for (int k = 0; k < kFlagWords; ++k)
+        __hip_atomic_store(A.flags + k, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      __hip_atomic_store(A.flags + kFlagMax, m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store((uint64_t*)(A.flags + kFlagTotal), carry, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      // every record of the range is in the pool: a next range reserves from 0
+      __hip_atomic_store((uint64_t*)(A.flags + kFlagPool), 0ull, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 }
 
@@ -240,36 +257,52 @@ __global__ void __launch_bounds__(kMoveWaves * kWave) k_move(MoveArgs A) {
   const uint32_t lane = lane_id();
   const uint32_t n_waves = gridDim.x * kMoveWaves;
   const uint32_t n_groups = (A.tiles + kWave - 1) / kWave;
-  for (uint32_t pair = __builtin_amdgcn_readfirstlane(blockIdx.x * kMoveWaves + threadIdx.x / kWave);
-       pair < A.n_pairs; pair += n_waves) {
-    if (A.skip && A.skip[pair]) continue;  // no records, no marks
-    const uint32_t count = (uint32_t)min(A.pair_count[pair], (int64_t)0xFFFFFFFFll);
-    const int64_t base = A.pair_offset[pair];
-    const uint64_t* row = A.status + (int64_t)pair * A.tiles;
-    auto load = [&](uint32_t g) -> uint64_t {
-      const uint32_t t = g * kWave + lane;
-      return t < A.tiles ? row[t] : 0ull;
-    };
-    if (n_groups <= kNzMinGroups) {
-      if (count == 0u) continue;
-      const uint64_t w0 = load(0), w1 = n_groups > 1 ? load(1) : 0ull;
+  const uint32_t first = __builtin_amdgcn_readfirstlane(blockIdx.x * kMoveWaves + threadIdx.x / kWave);
+  // A pair's loads are issued together, before any of them is used: its skip mark (read from a
+  // valid stand-in address when the call skips no pair), count and offset, and for a short range
+  // its status words (read even when the pair has no records: they lie inside the status table).
+  auto skipped = [&](uint32_t pair) -> const uint8_t* {
+    return A.skip != nullptr ? A.skip + pair : (const uint8_t*)(A.pair_count + pair);
+  };
+  if (n_groups <= kNzMinGroups) {
+    for (uint32_t pair = first; pair < A.n_pairs; pair += n_waves) {
+      const uint64_t* row = A.status + (int64_t)pair * A.tiles;
+      const uint8_t sv = *skipped(pair);
+      const int64_t count64 = A.pair_count[pair];
+      const int64_t base = A.pair_offset[pair];
+      const uint64_t w0 = lane < A.tiles ? row[lane] : 0ull;
+      const uint64_t w1 = n_groups > 1 && kWave + lane < A.tiles ? row[kWave + lane] : 0ull;
+      const uint32_t count = (uint32_t)min(count64, (int64_t)0xFFFFFFFFll);
+      if ((A.skip != nullptr && sv != 0) || count == 0u) continue;  // no records
       const uint32_t c0 = status_count(w0), c1 = status_count(w1);
       const uint32_t incl0 = wave_incl_scan7(c0), incl1 = wave_incl_scan7(c1);
       move_group(A, w0, c0, incl0, base, 0u, count, lane);
       if (n_groups > 1)
         move_group(A, w1, c1, incl1, base, __builtin_amdgcn_readlane(incl0, kWave - 1), count,
                    lane);
-    } else {
-      uint32_t at = 0;
-      for_marked_groups(A, pair, lane, [&](uint32_t g) {
-        if (count == 0u) return;
-        const uint64_t w = load(g);
-        const uint32_t c = status_count(w);
-        const uint32_t incl = wave_incl_scan7(c);
-        move_group(A, w, c, incl, base, at, count, lane);
-        at += __builtin_amdgcn_readlane(incl, kWave - 1);
-      });
     }
+    return;
+  }
+  for (uint32_t pair = first; pair < A.n_pairs; pair += n_waves) {
+    const uint8_t sv = *skipped(pair);
+    const int64_t count64 = A.pair_count[pair];
+    const int64_t base = A.pair_offset[pair];
+    // (the count and offset are used before the skip test, so that their loads go out with the
+    // mark's instead of after the branch)
+    asm volatile("" ::"v"(count64), "v"(base));
+    if (A.skip != nullptr && sv != 0) continue;  // no records, no marks
+    const uint32_t count = (uint32_t)min(count64, (int64_t)0xFFFFFFFFll);
+    const uint64_t* row = A.status + (int64_t)pair * A.tiles;
+    uint32_t at = 0;
+    for_marked_groups(A, pair, lane, [&](uint32_t g) {
+      if (count == 0u) return;
+      const uint32_t t = g * kWave + lane;
+      const uint64_t w = t < A.tiles ? row[t] : 0ull;
+      const uint32_t c = status_count(w);
+      const uint32_t incl = wave_incl_scan7(c);
+      move_group(A, w, c, incl, base, at, count, lane);
+      at += __builtin_amdgcn_readlane(incl, kWave - 1);
+    });
   }
 }
 

@@ -108,3 +108,38 @@ def test_every_cell_kept_with_a_pool_beyond_2_pow_23(emr):
             np.testing.assert_array_equal(p, np.arange(Q))
             # (equal as floats: a -0.0 node bias may stay -0.0 in one tier and not the other)
             np.testing.assert_array_equal(w.reshape(-1), raw[r, :4 * Q])
+
+
+@pytest.mark.parametrize("depth,n", [(7, 400), (8, 120)])
+def test_two_calls_in_flight_on_two_streams(emr, depth, n):
+    """Two results, each with its workspace and stream, alternate with two calls in flight (call
+    i is checked after call i + 1 is enqueued, as the benchmark's timed steps run): every call's
+    records equal those of a single synchronous call on a fresh workspace, bit for bit, and every
+    call's check reports the same total. The compiled tier runs from the second call on."""
+    import torch
+    genomes = W.population(72, n, 20, 60)
+    sources = W.xor_sources()
+    theta = np.float32(0.03).item()
+    pop = emr.emr_pack_population(genomes)
+    ref = emr.alloc_result(pop, sources, depth)
+    emr.emr_discover(pop, sources, depth, theta, res=ref)
+    total, _ = emr.emr_result_check(ref)
+    want = host(emr, ref)
+    bufs = [emr.alloc_result(pop, sources, depth) for _ in range(2)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    got = []
+
+    def check(i):
+        t, _ = emr.emr_result_check(bufs[i & 1])
+        assert t == total, (i, t, total)
+        got.append(host(emr, bufs[i & 1]))
+
+    n_calls = 9
+    for i in range(n_calls):
+        emr.emr_discover(pop, sources, depth, theta, res=bufs[i & 1], stream=streams[i & 1])
+        if i > 0:
+            check(i - 1)
+    check(n_calls - 1)
+    assert emr.emr_jit_info(pop)["state"] == 1
+    for g in got:
+        same(g, want)
