@@ -539,7 +539,9 @@ emr_status emr_eval_raw_noalloc(const emr_population* pop, const emr_source* sou
 /* Algorithmic VALU work of one emr_discover call under the cost model documented with the
  * benchmark: total lane-operation slots (*slots) and number of queries (*queries). Per query of a
  * (genome, direction) program: one slot per position-dependent edge, the activations' slots
- * (transcendental instructions weighted by transcendental_slots) and 2.5 for the variance; a
+ * (transcendental instructions weighted by transcendental_slots) and 2.5 for the variance, where
+ * a node whose value does not depend on the source counts once for the S sources walked together
+ * (1 / S of it per query: the compiled tier evaluates it once per position); a
  * program whose output does not depend on the position costs 0 (its outputs are per-source
  * constants and their variance is exactly zero). *evaluated: the queries of the pairs whose output
  * depends on the position (the others are answered by their per-source constant); *flops: useful

@@ -45,6 +45,10 @@ constexpr int kFirstAlignedLevel = 4;     // first level whose size is a multipl
 //                                     the dst slot (a in 0..5, EMR_ACT_*);
 //                             7 + a = the node is the output: activation a, value kept
 //                  bit 4      first record of a node: the accumulator starts at bias + ax x + ay y
+//                  bit 5      (first record) the node's value does not depend on the source: no
+//                             path reaches it from the source's coordinates, so its bias rows
+//                             are equal for every source and it takes the same value for every
+//                             source at a position (never set for the output node)
 //                  bits 8..12 dst slot
 //                  bits 16..19 number of edges in this record (0..11)
 //   word 1: float bits of the summed weights of the node's edges from the position's x (first
@@ -62,6 +66,7 @@ constexpr uint32_t kRecTailMask = 15u;
 constexpr uint32_t kRecTailStore = 1u;   // + activation
 constexpr uint32_t kRecTailOutput = 7u;  // + activation
 constexpr uint32_t kRecFirst = 1u << 4;
+constexpr uint32_t kRecShared = 1u << 5;
 constexpr uint32_t kRecDstShift = 8;
 constexpr uint32_t kRecEdgeShift = 16;
 constexpr uint32_t kSlotBits = 5;

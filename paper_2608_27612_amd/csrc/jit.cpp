@@ -8,6 +8,10 @@
 //   - its edges, from record position n - 1 down to 0: acc_m = fma(w, window_m[slot], acc_m);
 //   - its tail: the activation (the packer has scaled its input), stored into the destination
 //     slot of every window, or applied in place for the output node.
+// A node that takes the same value for every source (marked shared by the packer) is evaluated for
+// the first source's instances only, with the operations every source's instances run in the
+// interpreter, and the instances of the other sources read its value from the first source's
+// registers.
 // The slot indices are resolved here, so every vector instruction names fixed registers, and the
 // weights are literal operands: no register indexing, no scalar work per edge, and vector
 // operands only (which lets the hardware issue the instructions at its higher rate). The result
@@ -258,7 +262,16 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
   }
   bool inplace = false;
   uint32_t node_dst = 0;
+  // A node marked shared (kRecShared, with S > 1) takes the same value for every source: it is
+  // evaluated for the first source's P instances only, its inputs being shared values too. A
+  // window slot that holds a shared value has only the first source's registers written; a read
+  // of it by instance s P + j reads instance j's register instead (`shared_slot`, tracked along
+  // the straight-line program: a node's store into a slot decides what the slot holds).
+  bool shared = false;
+  std::vector<uint8_t> shared_slot(W, 0);
+  int MM = M;  // instances the current node evaluates
   auto A = [&](int m) { return inplace ? win(m, node_dst) : acc(m); };  // the node's sum
+  auto rd = [&](int m, uint32_t k) { return win(shared_slot[k] ? m % P : m, k); };
   // A node without x or y terms starts from its bias: folded into its first edge (one v_fmamk
   // per instance, the fma the interpreter's move + v_fmac computes) when that edge is in the
   // node's first record and the bias is in a VGPR (a copy per source, or one for S = 1).
@@ -270,6 +283,8 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
     if (meta & kRecFirst) {
       inplace = in_place[r] != 0;
       node_dst = (meta >> kRecDstShift) & wmask;
+      shared = S > 1 && (meta & kRecShared) != 0;
+      MM = shared ? P : M;
       uint32_t ne0 = (meta >> kRecEdgeShift) & 15u;
       if (ne0 > kRecEdges) ne0 = kRecEdges;
       // The bias rows of the first records of this record's block of kJitRowBlock are loaded
@@ -310,6 +325,20 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
             for (int j = 0; j < P; ++j)
               E.vop2(kOpV2Fmac, "v_fmac_f32_e32", A(j), Emitter::K(R[2]), yr(j));
         }
+      } else if (!has_x && !has_y && shared) {
+        // one bias (a shared node's rows are equal for every source), in the last source's
+        // first accumulator, which no value occupies at a node's start
+        if (wait) E.wait_lgkm0();
+        const int tb = acc((S - 1) * P);
+        if (ne0 > 0) {
+          E.vop1(kOpV1Mov, "v_mov_b32_e32", tb, Emitter::Sg(row(r, 0)), false);
+          fuse = true;
+          bias_base = tb;
+          bias_step = 0;
+        } else {
+          for (int j = 0; j < P; ++j)
+            E.vop1(kOpV1Mov, "v_mov_b32_e32", A(j), Emitter::Sg(row(r, 0)), false);
+        }
       } else if (!has_x && !has_y) {
         if (wait) E.wait_lgkm0();
         if (copies == S) {
@@ -333,7 +362,10 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
         // the partial sums l_j live in the last source's accumulators (free at a node's start)
         // until every source has added its bias to them. With one position term, l_j has two
         // distinct values per tile, computed once each: position j reads l at ls(j) <= j.
+        // (A shared node adds the first source's bias only: the same operations as every
+        // source's in a walk of S sources.)
         const int L = acc((S - 1) * P);
+        const int ns = shared ? 1 : S;
         auto ls = [&](int j) {
           return L + (has_x && has_y ? j : has_x ? (j & ~3) + (j & 1) : (j & ~3) + (j & 2));
         };
@@ -346,10 +378,10 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
             E.vop2(kOpV2Fmac, "v_fmac_f32_e32", L + j, Emitter::K(R[2]), yr(j));
         if (wait) E.wait_lgkm0();
         if (copies == S)  // bias copies in VGPRs: the adds read vector operands only
-          for (int s = 0; s < S; ++s)
+          for (int s = 0; s < ns; ++s)
             E.vop1(kOpV1Mov, "v_mov_b32_e32", T + s, Emitter::Sg(row(r, s)), false);
         // (the last source's sums overwrite l, in decreasing j: l at ls(j) <= j is read first)
-        for (int s = 0; s < S; ++s)
+        for (int s = 0; s < ns; ++s)
           for (int jj = 0; jj < P; ++jj) {
             const int j = s == S - 1 ? P - 1 - jj : jj;
             const Src b = copies == S ? Emitter::V(T + s) : Emitter::Sg(row(r, s));
@@ -365,11 +397,11 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
       const uint32_t slot = (sw >> (kSlotBits * (q % 6))) & wmask;
       const Src w = Emitter::K(R[5 + q]);
       if (fuse) {
-        for (int m = 0; m < M; ++m)
-          E.fmamk(A(m), win(m, slot), R[5 + q], bias_base + (m / P) * bias_step);
+        for (int m = 0; m < MM; ++m)
+          E.fmamk(A(m), rd(m, slot), R[5 + q], bias_base + (m / P) * bias_step);
         fuse = false;
       } else {
-        for (int m = 0; m < M; ++m) E.vop2(kOpV2Fmac, "v_fmac_f32_e32", A(m), w, win(m, slot));
+        for (int m = 0; m < MM; ++m) E.vop2(kOpV2Fmac, "v_fmac_f32_e32", A(m), w, rd(m, slot));
       }
     }
     // tail
@@ -381,7 +413,7 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
     const uint32_t dst = (meta >> kRecDstShift) & wmask;
     auto D = [&](int m) { return store ? win(m, dst) : acc(m); };
     auto each = [&](auto f) {
-      for (int m = 0; m < M; ++m) f(m);
+      for (int m = 0; m < MM; ++m) f(m);
     };
     switch (act) {
       case EMR_ACT_LINEAR:
@@ -417,6 +449,7 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
       default:
         break;  // ids 6..: no activation exists; the interpreter's tail table has none either
     }
+    if (store) shared_slot[dst] = shared ? 1 : 0;
   }
   // the caller reads the accumulators next (two wait states cover a transcendental result)
   E.nop(1);

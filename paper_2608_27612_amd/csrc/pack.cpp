@@ -189,6 +189,21 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       }
     }
     const bool out_varying = varying[out_node] != 0;
+    // Nodes reached from the source's coordinates: (x1, y1) for outgoing queries, (x2, y2)
+    // incoming. Any other node takes the same value for every source at a position.
+    const int sx_role = dir == EMR_DIR_OUT ? EMR_IN_X1 : EMR_IN_X2;
+    const int sy_role = dir == EMR_DIR_OUT ? EMR_IN_Y1 : EMR_IN_Y2;
+    std::vector<char> from_source(n, 0);
+    for (int v : order) {
+      if (!live[v]) continue;
+      const int k = g.kind[v];
+      if (k <= EMR_IN_BIAS) {
+        from_source[v] = (k == sx_role || k == sy_role);
+        continue;
+      }
+      for (int ei : in_edges[v])
+        if (live[edges[ei].src] && from_source[edges[ei].src]) from_source[v] = 1;
+    }
 
     // Register slots for varying computed nodes by liveness: a slot is freed after the last step
     // that reads it, before that step's own result is assigned.
@@ -250,6 +265,7 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
       const int v = vsteps[t];
       first_rec[t] = n_rec;
       float ax = 0.0f, ay = 0.0f;
+      int ax_edges = 0, ay_edges = 0;
       std::vector<std::pair<uint32_t, float>> node_edges;  // (source slot, w) in edge-list order
       for (int ei : in_edges[v]) {
         const Edge& E = edges[ei];
@@ -258,15 +274,18 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
         if (k == vx_role) {
           ax += E.w;  // parallel edges from x add their weights
           inf.fma_xy++;
+          ax_edges++;
         } else if (k == vy_role) {
           ay += E.w;
           inf.fma_xy++;
+          ay_edges++;
         } else {
           node_edges.push_back({(uint32_t)assigned[E.src], E.w});
           inf.fma_node++;
         }
       }
       const bool is_out = out_varying && v == out_node;
+      const bool shared = !is_out && !from_source[v];
       const uint32_t dst = is_out ? 0u : (uint32_t)assigned[v];
       const double c_act = act_input_scale(g.act[v]);
       const size_t ne = node_edges.size();
@@ -277,7 +296,7 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
         const size_t k0 = c * kRecEdges, k1 = std::min(ne, k0 + kRecEdges);
         uint32_t meta = ((uint32_t)(k1 - k0) << kRecEdgeShift) | (dst << kRecDstShift);
         if (c == 0) {
-          meta |= kRecFirst;
+          meta |= kRecFirst | (shared ? kRecShared : 0u);
           blob[r + 1] = fbits(scaled(ax, c_act));
           blob[r + 2] = fbits(scaled(ay, c_act));
         }
@@ -293,6 +312,10 @@ bool pack_genome(const emr_genome& g, std::vector<uint32_t>& blob, ProgDesc desc
         n_rec++;
       }
       inf.act_count[g.act[v]]++;
+      if (shared) {
+        inf.shared_edges += (ax_edges + ay_edges) + (int)ne;
+        inf.shared_act_count[g.act[v]]++;
+      }
     }
     d.n_rec = n_rec;
     inf.n_steps = (int)vsteps.size();

@@ -16,6 +16,9 @@ struct GenomeInfo {
   int fma_xy = 0;        // edges from the position's x / y
   int fma_node = 0;      // edges between varying nodes
   int act_count[6] = {0, 0, 0, 0, 0, 0};  // varying nodes per activation id
+  // The part of the above in nodes whose value does not depend on the source (kRecShared)
+  int shared_edges = 0;  // their edges from x / y and from varying nodes
+  int shared_act_count[6] = {0, 0, 0, 0, 0, 0};
   int window = 0;        // register slots needed
   int n_unodes = 0;      // uniform computed nodes
   int n_rec = 0;         // program records

@@ -34,30 +34,47 @@ bool check_fail(std::string* msg, const char* fmt, ...) {
 
 }  // namespace
 
-double query_base(const GenomeInfo& inf) {
+namespace {
+// Per query of a source, the work of the nodes shared by the S sources of a walk is paid once
+// for all of them: (S - 1) / S of it is left out of each query's count.
+double unshared(int S) { return S > 1 ? 1.0 - 1.0 / S : 0.0; }
+const double kActOther[6] = {0.0, 1.0, 2.0, 1.0, 1.0, 1.0};  // non-transcendental operations
+const double kActTrans[6] = {0.0, 2.0, 2.0, 1.0, 1.0, 0.0};  // transcendental instructions
+}  // namespace
+
+double query_base(const GenomeInfo& inf, int S) {
   if (!inf.out_varying) return 0.0;
-  const double other[6] = {0.0, 1.0, 2.0, 1.0, 1.0, 1.0};
-  double c = inf.fma_xy + inf.fma_node + 2.5;
-  for (int a = 0; a < 6; ++a) c += inf.act_count[a] * other[a];
-  return c;
+  double c = inf.fma_xy + inf.fma_node + 2.5, sh = inf.shared_edges;
+  for (int a = 0; a < 6; ++a) {
+    c += inf.act_count[a] * kActOther[a];
+    sh += inf.shared_act_count[a] * kActOther[a];
+  }
+  return c - unshared(S) * sh;
 }
 
-double query_trans(const GenomeInfo& inf) {
+double query_trans(const GenomeInfo& inf, int S) {
   if (!inf.out_varying) return 0.0;
-  const double trans[6] = {0.0, 2.0, 2.0, 1.0, 1.0, 0.0};
-  double c = 0.0;
-  for (int a = 0; a < 6; ++a) c += inf.act_count[a] * trans[a];
-  return c;
+  double c = 0.0, sh = 0.0;
+  for (int a = 0; a < 6; ++a) {
+    c += inf.act_count[a] * kActTrans[a];
+    sh += inf.shared_act_count[a] * kActTrans[a];
+  }
+  return c - unshared(S) * sh;
 }
 
-double query_slots(const GenomeInfo& inf, double rT) {
-  return query_base(inf) + rT * query_trans(inf);
+double query_slots(const GenomeInfo& inf, double rT, int S) {
+  return query_base(inf, S) + rT * query_trans(inf, S);
 }
 
-double query_flops(const GenomeInfo& inf) {
+double query_flops(const GenomeInfo& inf, int S) {
   if (!inf.out_varying) return 0.0;
-  return 2.0 * (inf.fma_xy + inf.fma_node) + (query_base(inf) - inf.fma_xy - inf.fma_node - 2.5) +
-         query_trans(inf) + 2.5;
+  // a multiply-add per edge counts 2, every other operation 1
+  double c = 2.0 * (inf.fma_xy + inf.fma_node) + 2.5, sh = 2.0 * inf.shared_edges;
+  for (int a = 0; a < 6; ++a) {
+    c += inf.act_count[a] * (kActOther[a] + kActTrans[a]);
+    sh += inf.shared_act_count[a] * (kActOther[a] + kActTrans[a]);
+  }
+  return c - unshared(S) * sh;
 }
 
 int window_bucket(int window) {
@@ -215,12 +232,12 @@ emr_status build_plan_tables(const ProgDesc* desc, const GenomeInfo* info, int32
   // expensive programs come first (the round-robin chunk shares of a first call then end with the
   // cheapest); output order does not depend on this order (each pair has its own totals and
   // offsets).
-  std::vector<double> cost(2 * (size_t)G);
-  for (size_t i = 0; i < cost.size(); ++i) cost[i] = query_slots(info[i], 4.0);
+  // per query of a group's source, its S sources walked together
+  auto cost = [&](const TmpGroup& t) { return query_slots(info[t.desc], 4.0, t.S); };
   std::stable_sort(tmp.begin(), tmp.end(), [&](const TmpGroup& a, const TmpGroup& b) {
     if (a.S != b.S) return a.S < b.S;
     if (a.window != b.window) return a.window < b.window;
-    return cost[a.desc] > cost[b.desc];
+    return cost(a) > cost(b);
   });
   P.groups.reserve(tmp.size());
   uint64_t bias = 0;
@@ -230,7 +247,7 @@ emr_status build_plan_tables(const ProgDesc* desc, const GenomeInfo* info, int32
       P.buckets.push_back({t.S, t.window, (uint32_t)i, 0, 0.0, 0});
     P.buckets.back().count++;
     if (t.g.flags & 1u) P.buckets.back().varying = P.buckets.back().count;
-    P.buckets.back().cost += t.S * cost[t.desc];
+    P.buckets.back().cost += t.S * cost(t);
     t.g.bias_off = (uint32_t)bias;
     P.group_member0.push_back((uint32_t)P.members.size());
     const uint32_t rows = t.g.n_rec + 2;  // output row, one per record at most, prefetch row
@@ -238,7 +255,7 @@ emr_status build_plan_tables(const ProgDesc* desc, const GenomeInfo* info, int32
     bias += 4ull * rows;
     if (bias > 0xFFFFFFFFull) return fail_msg(msg, EMR_E_LIMIT, "bias table too large");
     P.groups.push_back(t.g);
-    P.group_cost.push_back((float)cost[t.desc]);
+    P.group_cost.push_back((float)cost(t));
   }
   // Part order within the launch: the costliest bucket first (its chunks are handed out first).
   std::stable_sort(P.buckets.begin(), P.buckets.end(),
@@ -255,8 +272,8 @@ emr_status build_plan_tables(const ProgDesc* desc, const GenomeInfo* info, int32
       L.cost += b.cost;
       for (uint32_t g = 0; g < b.count; ++g) {
         const GenomeInfo& inf = info[P.members[P.group_member0[b.first + g]].desc];
-        L.slots_base += b.S * query_base(inf);
-        L.slots_trans += b.S * query_trans(inf);
+        L.slots_base += b.S * query_base(inf, b.S);
+        L.slots_trans += b.S * query_trans(inf, b.S);
       }
       L.sources += (double)b.S * b.count;
     }

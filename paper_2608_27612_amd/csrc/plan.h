@@ -17,20 +17,23 @@ namespace emr {
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// Algorithmic VALU slots per query of one (genome, direction) program: one per position-dependent
-// edge, the activation costs (transcendental instructions weighted by rT), and 2.5 for the
-// variance and threshold share of a query.
+// Algorithmic VALU slots per query of one (genome, direction) program evaluated for S sources at
+// once: one per position-dependent edge, the activation costs (transcendental instructions
+// weighted by rT), and 2.5 for the variance and threshold share of a query; the nodes whose value
+// does not depend on the source are evaluated once for the S sources, so each query counts 1 / S
+// of their edges and activations.
 // The cost is base + rT * trans: query_base() is the part without transcendentals, query_trans()
 // their count per query. A program whose output does not depend on the position costs nothing
 // per query: its output is the source's constant (folded once by the bind kernel, like every
 // position-independent node) and the variance of a constant is exactly zero, so the kernels
 // evaluate and test nothing for it.
-double query_base(const GenomeInfo& inf);
-double query_trans(const GenomeInfo& inf);
-double query_slots(const GenomeInfo& inf, double rT);
+double query_base(const GenomeInfo& inf, int S = 1);
+double query_trans(const GenomeInfo& inf, int S = 1);
+double query_slots(const GenomeInfo& inf, double rT, int S = 1);
 // Useful floating-point operations per query: a multiply-add per position-dependent edge counts
-// 2, every other activation operation and each transcendental 1, the variance 2.5.
-double query_flops(const GenomeInfo& inf);
+// 2, every other activation operation and each transcendental 1, the variance 2.5 (shared nodes
+// counted as above).
+double query_flops(const GenomeInfo& inf, int S = 1);
 
 // The register window bucket (4, 8, 16, 32) holding `window` live values, or -1.
 int window_bucket(int window);

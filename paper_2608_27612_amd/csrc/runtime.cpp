@@ -1573,14 +1573,16 @@ emr_status emr_discover_cost(const emr_population* pop, const emr_source* source
   const Plan& P = *plan;
   const double npos = (double)emr::n_positions(depth);
   double total = 0.0, varying = 0.0, fl = 0.0;
-  for (const emr::Member& m : P.members) {
-    const emr::GenomeInfo& inf = pop->info[m.desc];
-    total += query_slots(inf, transcendental_slots) * npos;
-    if (inf.out_varying) {
-      varying += npos;
-      fl += query_flops(inf) * npos;
+  for (const Plan::Bucket& b : P.buckets)
+    for (uint32_t g = b.first; g < b.first + b.count; ++g) {
+      // the group's S sources, walked together (members of one program)
+      const emr::GenomeInfo& inf = pop->info[P.members[P.group_member0[g]].desc];
+      total += b.S * query_slots(inf, transcendental_slots, b.S) * npos;
+      if (inf.out_varying) {
+        varying += b.S * npos;
+        fl += b.S * query_flops(inf, b.S) * npos;
+      }
     }
-  }
   if (slots) *slots = total;
   if (queries) *queries = (double)P.n_pairs * npos;
   if (evaluated) *evaluated = varying;

@@ -241,8 +241,9 @@ def emulate(listing, rows, x, y, M, W, stale_rows=False):
     return V
 
 
-def interpret(blob, desc, dir_, sx, sy, px, py):
-    """Evaluate packed program `desc[dir_]` for source (sx, sy) at positions (px, py) (arrays)."""
+def interpret(blob, desc, dir_, sx, sy, px, py, nodes=None):
+    """Evaluate packed program `desc[dir_]` for source (sx, sy) at positions (px, py) (arrays).
+    With `nodes` (a list), appends (first record, shared mark, value) for every node in order."""
     var_off, n_rec, n_steps, uni_off, flags = (int(v) for v in desc[dir_][:5])
     # uniform program
     U = np.zeros(5 + 300)
@@ -284,12 +285,14 @@ def interpret(blob, desc, dir_, sx, sy, px, py):
         meta = int(w[0])
         tail, first = meta & 15, (meta >> 4) & 1
         dst, ne = (meta >> 8) & 31, (meta >> 16) & 15
-        assert ne <= 11 and (meta >> 20) == 0 and (meta >> 5) & 7 == 0 and (meta >> 13) & 7 == 0
+        assert ne <= 11 and (meta >> 20) == 0 and (meta >> 6) & 3 == 0 and (meta >> 13) & 7 == 0
+        assert first or not (meta >> 5) & 1, "a shared mark outside a node's first record"
         if out is not None:
             raise AssertionError("record after the output node")
         if first:
             assert acc is None, "a node starts before the previous one ended"
             assert fold_rec[step] == r, "the node's bias row is not its first record's"
+            node_first, node_shared = r, (meta >> 5) & 1
             acc = folded[step] + f32(w[1]) * px + f32(w[2]) * py
         else:
             assert acc is not None and w[1] == 0 and w[2] == 0
@@ -307,8 +310,13 @@ def interpret(blob, desc, dir_, sx, sy, px, py):
         if tail <= 6:
             assert dst < window
             vals[dst] = _act_scaled(tail - 1, acc)
+            value = vals[dst]
         else:
+            assert not node_shared, "the output node is marked shared"
             out = _act_scaled(tail - 7, acc)
+            value = out
+        if nodes is not None:
+            nodes.append((node_first, node_shared, np.array(value)))
         acc = None
         step += 1
     assert step == n_steps and out is not None

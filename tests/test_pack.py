@@ -147,3 +147,77 @@ def test_window_limit():
     edges = [(2, 6 + k, 1.0) for k in range(h)] + [(6 + k, 5, 1.0) for k in range(h)]
     st, _, _, _, msg = PI.pack(mk(kinds, [0] * (6 + h), edges))
     assert st == EMR_E_LIMIT, msg
+
+
+def _reached_from(g, roles):
+    """Nodes with an enabled, live path from an input of the given roles (brute force over the
+    edge list, independent of the packer's order)."""
+    kind, src, dst = np.asarray(g["kind"]), np.asarray(g["src"]), np.asarray(g["dst"])
+    en = np.asarray(g["enabled"]).astype(bool)
+    hit = np.isin(kind, roles)
+    for _ in range(len(kind)):
+        nxt = hit.copy()
+        for s, d, e in zip(src, dst, en):
+            if e and hit[s]:
+                nxt[d] = True
+        if (nxt == hit).all():
+            break
+        hit = nxt
+    return hit
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_shared_marks_are_the_nodes_not_reached_from_the_source(seed):
+    """A node's first record carries the shared mark exactly when no path reaches the node from the
+    source's coordinates ((x1, y1) outgoing, (x2, y2) incoming), the output excepted; evaluated for
+    three sources at the same positions, every marked node takes the same value, bit for bit, and
+    the marks cover real work in the workload populations."""
+    px, py = _positions(4)
+    marked = total = 0
+    for g in W.population(200 + seed, 40, 20, 60, biases=True):
+        st, blob, desc, info, msg = PI.pack(g)
+        assert st == 0, msg
+        kind = np.asarray(g["kind"])
+        out = int(np.flatnonzero(kind == 6)[0]) if (kind == 6).any() else None
+        for d, roles in ((0, [0, 1]), (1, [2, 3])):
+            from_src = _reached_from(g, roles)
+            runs = []
+            for sx, sy in ((0.0, -1.0), (0.5, 1.0), (-1.0, -0.25)):
+                nodes = []
+                PI.interpret(blob, desc, d, sx, sy, px, py, nodes=nodes)
+                runs.append(nodes)
+            if not runs[0]:
+                continue
+            # the k-th node of the program is the k-th varying live node in the packer's order:
+            # compare the marks' count with the structural count, and the values across sources
+            shared = [n[1] for n in runs[0]]
+            for k, (r, sh, v) in enumerate(runs[0]):
+                total += 1
+                if sh:
+                    marked += 1
+                    for other in runs[1:]:
+                        np.testing.assert_array_equal(other[k][2], v)
+            # structural count: varying computed nodes, not the output, not reached from the source
+            varying = _reached_from(g, [2, 3] if d == 0 else [0, 1])
+            live = _live(g)
+            want = sum(1 for v in range(len(kind))
+                       if kind[v] > 4 and varying[v] and live[v] and not from_src[v]
+                       and not (v == out))
+            assert sum(shared) == want, (d, shared, want)
+    assert marked > 0.1 * total
+
+
+def _live(g):
+    """Nodes with an enabled path to the output."""
+    kind, src, dst = np.asarray(g["kind"]), np.asarray(g["src"]), np.asarray(g["dst"])
+    en = np.asarray(g["enabled"]).astype(bool)
+    live = kind == 6
+    for _ in range(len(kind)):
+        nxt = live.copy()
+        for s, d, e in zip(src, dst, en):
+            if e and live[d]:
+                nxt[s] = True
+        if (nxt == live).all():
+            break
+        live = nxt
+    return live
