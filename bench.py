@@ -71,9 +71,13 @@ RECORD_BYTES = 20  # a kept cell: parent index (4 bytes) + its four children's o
 METRIC = "CPPN queries/sec incl. variance filter (% VALU peak); ms/gen pop1000 depth7"
 
 
+# The sources that decide what the discover kernel executes: its code, the programs' packing and
+# translation, and the plan and chunk placement.
 KERNEL_SOURCES = ["paper_2608_27612_amd/csrc/kernels.hip", "paper_2608_27612_amd/csrc/discover.h",
                   "paper_2608_27612_amd/csrc/jit.hip", "paper_2608_27612_amd/csrc/jit.cpp",
-                  "paper_2608_27612_amd/csrc/regwin_gen.h", "paper_2608_27612_amd/csrc/emr_internal.h"]
+                  "paper_2608_27612_amd/csrc/regwin_gen.h", "paper_2608_27612_amd/csrc/emr_internal.h",
+                  "paper_2608_27612_amd/csrc/pack.cpp", "paper_2608_27612_amd/csrc/plan.cpp",
+                  "paper_2608_27612_amd/csrc/sched.cpp"]
 
 
 def kernel_source_sha():

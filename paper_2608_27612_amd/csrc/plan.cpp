@@ -190,6 +190,7 @@ emr_status build_plan_tables(const ProgDesc* desc, const GenomeInfo* info, int32
     int S, window;
     uint32_t desc;
     uint32_t src[kMaxGroup];
+    double cost;
   };
   std::vector<TmpGroup> tmp;
   for (int32_t g = 0; g < G; ++g) {
@@ -233,7 +234,8 @@ emr_status build_plan_tables(const ProgDesc* desc, const GenomeInfo* info, int32
   // cheapest); output order does not depend on this order (each pair has its own totals and
   // offsets).
   // per query of a group's source, its S sources walked together
-  auto cost = [&](const TmpGroup& t) { return query_slots(info[t.desc], 4.0, t.S); };
+  for (TmpGroup& t : tmp) t.cost = query_slots(info[t.desc], 4.0, t.S);
+  auto cost = [](const TmpGroup& t) { return t.cost; };
   std::stable_sort(tmp.begin(), tmp.end(), [&](const TmpGroup& a, const TmpGroup& b) {
     if (a.S != b.S) return a.S < b.S;
     if (a.window != b.window) return a.window < b.window;
