@@ -235,6 +235,7 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
   // slot: the same operations in the same order on other registers. Marked at the node's first
   // record.
   std::vector<uint8_t> in_place(n, 0);
+  std::vector<uint8_t> output_node(n, 0);  // at a node's first record: the node is the output
   {
     bool started = false;
     uint32_t first = 0, reads = 0;  // window slots the node's edges read (W <= 32)
@@ -257,6 +258,7 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
       const uint32_t dst = (meta >> kRecDstShift) & wmask;
       if (started && tail == kRecTailStore + EMR_ACT_LINEAR && !((reads >> dst) & 1u))
         in_place[first] = 1;
+      if (started && tail >= kRecTailOutput) output_node[first] = 1;
       started = false;
     }
   }
@@ -283,7 +285,8 @@ bool compile_program(const uint32_t* rec, uint32_t n_rec, bool output_varies, in
     if (meta & kRecFirst) {
       inplace = in_place[r] != 0;
       node_dst = (meta >> kRecDstShift) & wmask;
-      shared = S > 1 && (meta & kRecShared) != 0;
+      // (every source needs its own output: a shared mark on the output node is not followed)
+      shared = S > 1 && (meta & kRecShared) != 0 && !output_node[r];
       MM = shared ? P : M;
       uint32_t ne0 = (meta >> kRecEdgeShift) & 15u;
       if (ne0 > kRecEdges) ne0 = kRecEdges;

@@ -89,6 +89,44 @@ def test_compiled_programs_compute_the_packed_programs():
     assert n > 10
 
 
+def test_shared_nodes_are_evaluated_once_and_a_shared_mark_on_the_output_is_ignored():
+    """With S > 1 a node marked shared is evaluated for the first source's instances only (fewer
+    instructions than the same program with its marks cleared, same values for every source), and
+    a shared mark planted on the output node's first record changes nothing: every source still
+    gets its own output."""
+    rng = np.random.default_rng(12)
+    fewer = planted = 0
+    for gi, blob, desc, d, S, P, Wn in programs(POPS[0] + POPS[1][:2]):
+        if S == 1:
+            continue
+        var_off, n_rec = int(desc[d][0]), int(desc[d][1])
+        metas = [int(blob[var_off + 16 * r]) for r in range(n_rec)]
+        if not any(m & 32 for m in metas):
+            continue
+        srcs = [(float(rng.uniform(-1, 1)), float(rng.uniform(-1, 1))) for _ in range(S)]
+        x, y = PI.positions(rng, P)
+        rows = PI.bias_rows(blob, desc, d, srcs)
+        want = [PI.interpret(blob, desc, d, sx, sy, x, y)[0] for sx, sy in srcs]
+        cleared = blob.copy()
+        for r in range(n_rec):
+            cleared[var_off + 16 * r] &= ~np.uint32(32)
+        w_shared, _ = PI.compile_program(blob, desc[d], S, P, Wn)
+        w_full, _ = PI.compile_program(cleared, desc[d], S, P, Wn)
+        assert len(w_shared) < len(w_full), (gi, d)
+        fewer += 1
+        # plant the mark on the output node's first record (the last node's)
+        out_first = max(r for r in range(n_rec) if metas[r] & 16)
+        bad = blob.copy()
+        bad[var_off + 16 * out_first] |= np.uint32(32)
+        _, listing = PI.compile_program(bad, desc[d], S, P, Wn)
+        V = PI.emulate(listing, rows, x, y, S * P, Wn)
+        for s in range(S):
+            got = np.array([V[4 + s * P + j] for j in range(P)])
+            assert np.allclose(got, want[s], rtol=1e-9, atol=1e-9), (gi, d, s)
+        planted += 1
+    assert fewer > 5 and planted > 5
+
+
 def test_programs_load_only_rows_the_caller_did_not_preload():
     """A program whose nodes all start in records 0 .. 3 uses the preloaded rows and loads
     nothing; a longer one loads every row it uses (so it runs right whatever s[40:55] hold)."""
