@@ -19,9 +19,10 @@ GPU idle between calls; every call is still checked. Printed as one JSON line:
                constant, exactly, without a per-position evaluation)
   roofline     the discover kernel (one launch per step, every query of the step):
                algorithmic VALU lane-slots (cost model of emr_discover_cost: one slot per fp32
-               FMA / add / mul, transcendentals weighted by their measured 1/4 rate) / its
-               HIP-event duration (an event pair around the launch in every 4th step of a second
-               run of the same steps, so that the host-clock steps carry no events), against
+               FMA / add / mul, transcendentals weighted by their documented 1/4 rate, the
+               nodes shared by a walk's sources counted once per walk) / its HIP-event duration
+               (an event pair around the launch in every 4th step of a separate run of the same
+               steps one call at a time, so that the host-clock steps carry no events), against
                the chip's fp32 vector peak: 157.3 TFLOP/s = 78.64 T lane-slots/s (an FMA is one
                slot, two flops); flops / frac_flops: the useful floating-point operations (2 per
                multiply-add, 1 per other operation) over the same duration, against 157.3 TFLOP/s;
@@ -41,7 +42,8 @@ GPU idle between calls; every call is still checked. Printed as one JSON line:
   compiled_tier  the timed steps' compiled programs (the default policy compiles a population's
                programs on its second call, so the warm-up compiles them): count, machine-code
                bytes, host compile and module-load times
-  sub          the other measured workloads, each with the same per-step figures: the population
+  sub          the other measured workloads, each with the same per-step figures (streamed calls
+               run one at a time): the population
                at depth 8, the tabular population (33 sources, depth 6), the single deep CPPN
                streamed at depth 13 (emr_discover_stream, one step = one streamed call), and
                the same CPPN at depth 14 streamed to a record file on disk (one step = open,
