@@ -163,7 +163,7 @@ typedef struct {
 
 /* Device scratch (bytes) needed by an emr_discover call of this capacity (0 for emr_eval_raw) for
  * this population, these sources (host) and this depth: per-tile status words, the compaction's
- * tile-group marks and per-pair look-back words, the folded per-(genome, source) biases, and a
+ * tile-group marks and per-pair record totals, the folded per-(genome, source) biases, and a
  * record pool of `capacity` records (20 bytes each) that the discover kernel fills in any order
  * and the compaction gathers from. A call's error flags, largest count and total live in a
  * library-owned slot (see emr_result_check). A record call leaves the workspace's counters cleared,

@@ -2,9 +2,10 @@
 // the template code object for compiled programs (jit.hip): one lane per parent cell; each lane
 // evaluates the varying CPPN program for S sources of one genome at the cell's four children at
 // once (Section 3.1, the batched query W), reduces the four siblings to their variance in
-// registers, applies var > theta (Section 3.2, Eq. 2), and places the kept cells with a wave
-// ballot at per-tile slots (compacted by k_compact) or through a per-pair decoupled look-back
-// scan, so every pair's records land in ascending parent order with no atomics on the output.
+// registers, applies var > theta (Section 3.2, Eq. 2), and writes the kept cells to a record pool
+// (one reservation per walk that keeps any), leaving each tile's pool offset and count in its
+// status word and each chunk's counts in its pairs' totals; k_scan and k_move then place every
+// pair's records contiguously in ascending parent order.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>

@@ -181,7 +181,7 @@ struct DiscoverScalars {
   float theta16;  // 16 theta
   uint32_t code_bytes;  // compiled tier: size of the code area (0 for the interpreter)
   // Records over more than 2 groups of 64 tiles: bit g % 64 of nz[pair * nz_words + g / 64]
-  // marks a group g of the range that kept a cell (k_compact visits only those).
+  // marks a group g of the range that kept a cell (k_move visits only those).
   uint64_t* nz;
   uint32_t nz_words;
   uint32_t blob_words, n_pairs;
@@ -271,7 +271,7 @@ EMR_HD constexpr int jit_temps(int S, int P, int W) {
 
 // Tiles of one chunk at most (a chunk's record counts are held one per lane, 16 per source).
 constexpr uint32_t kChunkTilesMax = 16;
-// Group marks of the padded placement: a range of more than kNzMinGroups groups of 64 tiles has
+// Group marks of the compaction: a range of more than kNzMinGroups groups of 64 tiles has
 // nz_words(tiles) words of marks per pair, one bit per group.
 constexpr uint32_t kNzMinGroups = 2;
 EMR_HD constexpr uint32_t nz_words(uint32_t tiles) { return ((tiles + 63u) / 64u + 63u) / 64u; }

@@ -1,7 +1,7 @@
 // gfx950 kernels for eager multi-resolution substrate discovery.
 //
 //   k_grid      writes the cell centres of every queried position (Section 3.1, Eq. 1).
-//   k_fill      clears the look-back status words and counters of a workspace.
+//   k_fill      clears the tile-group marks and per-pair totals of a workspace.
 //   k_bind      evaluates the position-independent part of each (genome, source) CPPN once and
 //               folds it into per-step biases (one wave per pair).
 //   k_discover  the hot path: one lane per parent cell; each lane interprets the varying CPPN

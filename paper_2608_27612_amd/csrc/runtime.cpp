@@ -518,7 +518,8 @@ emr_status plan_schedule(const Plan& P, const emr::DiscoverScalars& sc, uint32_t
 // ------------------------------------------------------------------ call flags
 // Each call's kernels raise their error bits (word 0) and largest pair count (word 1) into a slot
 // of a library-owned ring in device memory. A slot is zero when a call takes it; the call's last
-// kernel, k_finalize, writes the words to the slot's pinned host words and clears them again. So
+// kernel (k_scan for a record call, k_finalize otherwise) writes the words to the slot's pinned
+// host words and clears them again. So
 // no copy of the flags goes either way, and the caller's workspace keeps no state from one call
 // to the next.
 constexpr int kFlagSlots = 256;
@@ -1009,11 +1010,12 @@ bool cached_split_parts(const Plan& P, const Plan::Launch& L, bool skip_uniform,
 // records go to `out` pair after pair (pair_offset, pair_count), its capacity also bounding the
 // pool in the workspace; raw outputs go to raw[r * N(D) + p].
 // jit: run the plan's compiled programs (jit_use said so) instead of the interpreter. With
-// `finalize`, k_finalize then hands the call's flags to their pinned words.
+// `finalize`, the range's last kernel (k_scan for records, k_finalize for raw outputs) then hands
+// the call's flags to their pinned words.
 // With `clear` (record mode), the workspace's group marks and per-pair totals are cleared right
 // before the discover launch, once every argument of that launch is ready on the host.
 // flags: the call's device flag words (error bits, largest count); flags_host: their pinned words
-// (device view) for k_finalize.
+// (device view) for that hand-over.
 // may_alloc: the call may allocate on first use: the thread's launch profiling (its events) and
 // the launch's chunk schedule apply (off for the allocation-free call, which runs its chunks
 // round-robin). A compiled-tier launch gets its workgroups' chunk lists once its plan runs again
@@ -1863,8 +1865,8 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
     const uint32_t err = (uint32_t)R.counts_h[b][n_pairs];
     if (err) {
       if (next) *next = c * n_pairs + (c == c0 ? skip : 0);
-      return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x at chunk %lld (1: look-back "
-                  "wait bound, 2: a table entry out of range)", err, (long long)c);
+      return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x at chunk %lld (2: a table entry "
+                  "out of range)", err, (long long)c);
     }
     int64_t n_rec = 0;
     for (int64_t r = 0; r < n_pairs; ++r) n_rec += std::max<int64_t>(R.counts_h[b][r], 0);
@@ -1914,8 +1916,8 @@ emr_status emr_discover_stream(const emr_population* pop, const emr_source* sour
   f.ok = true;
   const uint32_t err = f.host[emr::kFlagErr];
   if (err)
-    return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (1: look-back wait bound, 2: a "
-                "table entry out of range)", err);
+    return fail(EMR_E_DEVICE, "kernel reported error flags 0x%x (2: a table entry out of "
+                "range)", err);
   return EMR_OK;
 }
 

@@ -305,8 +305,9 @@ def test_result_checks_wait_for_their_own_call(emr):
 
 
 def test_many_pairs_csr_offsets(emr):
-    """Per-genome CSR sources with many empty and many busy pairs: the compaction's look-back over
-    pairs gives exact offsets (every pair's records where its offset says) for 6000+ pairs."""
+    """Per-genome CSR sources with many empty and many busy pairs: the compaction's scan over the
+    pairs' totals gives exact offsets (every pair's records where its offset says) for 6000+
+    pairs."""
     rng = np.random.default_rng(71)
     genomes = W.population(71, 300, 12, 40)
     pts, offs = [], [0]
