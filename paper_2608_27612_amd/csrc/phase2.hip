@@ -12,6 +12,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "../../include/emr.h"
 #include "band.h"
 #include "discover.h"
@@ -44,21 +46,67 @@ __device__ __forceinline__ void pair_range(const RecordsIn& R, uint32_t pair, in
 }
 
 // ------------------------------------------------------------------------ hidden nodes
+// The call's records in parallel (a pair's records can number from none to hundreds of
+// thousands, so they are spread by record, not by pair): wave w takes the records
+// [w kMarkSpan, (w + 1) kMarkSpan) and lane l the records w kMarkSpan + l, + 64, ...; a record's
+// pair is the last pair whose offset is at most the record's index (a binary search for the
+// lane's first record, then a gallop forward from the pair before, the indices only growing).
+// A record outside the range of the pair found (offsets out of order) marks nothing.
+constexpr uint32_t kMarkSpan = 16 * kWave;
+
+// The last q in [lo, hi) with off[q] <= r, given off[lo] <= r and (hi = n or off[hi] > r).
+__device__ __forceinline__ uint32_t last_at_most(const int64_t* off, uint32_t lo, uint32_t hi,
+                                                 int64_t r) {
+  while (hi - lo > 1u) {
+    const uint32_t mid = lo + (hi - lo) / 2u;
+    if (off[mid] <= r)
+      lo = mid;
+    else
+      hi = mid;
+  }
+  return lo;
+}
+
 __global__ void __launch_bounds__(256) k_hidden_mark(HiddenArgs A) {
   const uint32_t lane = lane_id();
   const int64_t Q = n_parents(A.rec.depth);
-  FOR_EACH_PAIR_WAVE(pair, A.rec.n_pairs) {
-    const uint32_t info = A.rec.pair_info[2 * pair];
-    const uint32_t g = info >> 1;
-    if ((info & 1u) != 0u || g >= A.n_genomes) continue;  // incoming pairs add no hidden node
-    int64_t lo, hi;
-    pair_range(A.rec, pair, &lo, &hi);
-    uint32_t* bits = A.fresh + (int64_t)g * A.words;
-    for (int64_t i = lo + lane; i < hi; i += kWave) {
-      const uint32_t P = A.rec.parent[i];
+  const uint32_t np = A.rec.n_pairs;
+  if (np == 0u) return;
+  const int64_t* off = A.rec.offset;
+  const int64_t total = min(max(off[np], (int64_t)0), A.rec.cap);  // the call's records held
+  if (off[0] > 0) return;                                           // not a CSR offset table
+  const int64_t n_waves = (int64_t)gridDim.x * (blockDim.x / kWave);
+  for (int64_t base = (int64_t)(blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave) * kMarkSpan;
+       base < total; base += n_waves * kMarkSpan) {
+    uint32_t p = 0u;
+    bool first = true;
+    for (uint32_t j = 0; j < kMarkSpan / kWave; ++j) {
+      const int64_t r = base + (int64_t)j * kWave + lane;
+      if (r >= total) break;
+      if (first) {
+        p = last_at_most(off, 0u, np, r);
+        first = false;
+      } else {
+        // off[p] <= an earlier index < r: widen [p, hi) until off[hi] > r, then search it
+        uint32_t lo = p, step = 1u, hi = p + 1u;
+        while (hi < np && off[hi] <= r) {
+          lo = hi;
+          step = step < (1u << 30) ? 2u * step : step;
+          hi = np - lo > step ? lo + step : np;
+        }
+        p = last_at_most(off, lo, hi, r);
+      }
+      int64_t lo_r, hi_r;
+      pair_range(A.rec, p, &lo_r, &hi_r);
+      if (r < lo_r || r >= hi_r) continue;
+      const uint32_t info = A.rec.pair_info[2 * p];
+      const uint32_t g = info >> 1;
+      if ((info & 1u) != 0u || g >= A.n_genomes) continue;  // incoming pairs add no hidden node
+      const uint32_t P = A.rec.parent[r];
       if ((int64_t)P >= Q) continue;
       // grid positions 4P .. 4P+3; the many pairs of one genome mostly mark cells already marked,
       // so a plain read first keeps them from queueing atomics on the same words
+      uint32_t* bits = A.fresh + (int64_t)g * A.words;
       const uint32_t m = 0xFu << (4u * (P % 8u));
       if ((__hip_atomic_load(bits + P / 8u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & m) != m)
         atomicOr(bits + P / 8u, m);
@@ -301,7 +349,14 @@ static uint32_t wave_blocks(uint32_t n) {  // workgroups of 4 waves, one wave pe
 extern "C" hipError_t emr_launch_hidden(const emr::HiddenArgs* A, int step, hipStream_t s) {
   const uint32_t gb = A->n_genomes == 0 ? 1 : (A->n_genomes > 65535 ? 65535 : A->n_genomes);
   switch (step) {
-    case 0: hipLaunchKernelGGL(emr::k_hidden_mark, dim3(wave_blocks(A->rec.n_pairs)), dim3(256), 0, s, *A); break;
+    case 0: {
+      // waves of kMarkSpan records over the records the buffers can hold (the waves loop when
+      // there are more)
+      const int64_t spans = (A->rec.cap + emr::kMarkSpan - 1) / emr::kMarkSpan;
+      const uint32_t blocks = (uint32_t)std::min<int64_t>(std::max<int64_t>((spans + 3) / 4, 1), 2048);
+      hipLaunchKernelGGL(emr::k_hidden_mark, dim3(blocks), dim3(256), 0, s, *A);
+      break;
+    }
     case 1: hipLaunchKernelGGL(emr::k_hidden_count, dim3(gb), dim3(256), 0, s, *A); break;
     case 2: hipLaunchKernelGGL(emr::k_hidden_emit, dim3(gb), dim3(256), 0, s, *A); break;
     default: return hipErrorInvalidValue;
