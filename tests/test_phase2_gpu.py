@@ -161,3 +161,40 @@ def test_phase2_empty_and_capacity(emr):
     with pytest.raises(emr.EmrError) as e:
         emr.emr_express(pop, sources, 5, res, 15, -1.0, capacity=total)  # 4 per record needed
     assert e.value.status == emr.EMR_E_CAPACITY and str(4 * total) in str(e.value)
+
+
+def test_hidden_sources_of_skewed_records(emr):
+    """Hand-built CSR results whose records are spread as a discovery can spread them at its
+    extremes: long runs of empty pairs, pairs of thousands of records crossing the marking's spans
+    of 1024 records, incoming pairs holding records (which add no node), and, at depth 8, more
+    records than one sweep of the marking kernel's waves covers (8.4M), so its waves loop. Each
+    pair's records are distinct parents in ascending order, as a discovery leaves them. The hidden
+    nodes equal the oracle's set logic applied to the same records."""
+    import torch
+    sources = W.xor_sources()  # 3 outgoing sources and 1 incoming per genome
+    rng = np.random.default_rng(86)
+    for D, G, heavy_share, lo_share in ((7, 24, 0.08, 0.3), (8, 150, 0.7, 0.9)):
+        genomes = W.population(86 + D, G, 12, 40)
+        n_pairs = G * len(sources)
+        _, Q = emr.emr_grid_count(D)
+        pop = emr.emr_pack_population(genomes)
+        counts = np.zeros(n_pairs, np.int64)
+        hot = rng.choice(n_pairs, size=n_pairs // 5, replace=False)
+        counts[hot] = rng.integers(1, 40, size=len(hot))
+        heavy = rng.choice(n_pairs, size=max(2, int(heavy_share * n_pairs)), replace=False)
+        counts[heavy] = rng.integers(int(lo_share * Q), Q + 1, size=len(heavy))
+        counts[n_pairs - 1] = 3  # the last pair (incoming) holds records too
+        offs = np.zeros(n_pairs + 1, np.int64)
+        np.cumsum(counts, out=offs[1:])
+        total = int(offs[-1])
+        assert D == 7 or total > 8 * 1024 * 1024
+        parent = np.concatenate([np.sort(rng.choice(Q, size=int(c), replace=False))
+                                 for c in counts]).astype(np.int64)
+        res = emr.alloc_result(pop, sources, D, capacity=total)
+        res["pair_count"].copy_(torch.from_numpy(counts))
+        res["pair_offset"].copy_(torch.from_numpy(offs))
+        res["parent"][:total].copy_(torch.from_numpy(parent.astype(np.uint32).view(np.int32)))
+        hs = emr.emr_hidden_sources(pop, sources, D, res)
+        want = oracle.hidden_cells({"pair_offset": offs, "parent": parent}, G, sources)
+        check_hidden(emr, hs, want, D)
+        del res, hs
