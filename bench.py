@@ -4,11 +4,12 @@
 One step = one emr_discover call over the whole workload (the sources' bias rows are the plan's,
 every (genome, source, position) is queried, the variance filter is applied and the kept cells are
 compacted per pair) plus emr_result_check (the synchronizing count check) of that call. The packed
-population is resident in HBM before timing starts. The timed steps keep two calls in flight: two
-result buffers (each with its workspace) alternate on two streams (default priority), and call i is
-checked after call i + 1 has been enqueued, so the host's check and enqueue, one call's compaction
-and the last workgroups of its discover launch overlap the other call's work instead of leaving the
-GPU idle between calls; every call is still checked. Printed as one JSON line:
+population is resident in HBM before timing starts. The timed steps keep IN_FLIGHT calls in
+flight: IN_FLIGHT result buffers (each with its workspace) take the calls in turn, each on a stream
+of its own (default priority), and call i is checked after call i + IN_FLIGHT - 1 has been
+enqueued, so the host's check and enqueue, a call's compaction and the last workgroups of its
+discover launch overlap the other calls' work instead of leaving the GPU idle between calls; every
+call is still checked. Printed as one JSON line:
 
   value        CPPN queries per second over the timed steps (host clock, synchronized at both
                ends of the timed region)
@@ -67,6 +68,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 TIME_EVERY = 4  # steps per timed discover launch
+IN_FLIGHT = 4  # calls in flight in the pipelined steps (result buffers, streams)
 VALU_PEAK_SLOTS = 157.3e12 / 2.0  # lane-slots per second (fp32 vector peak, FMA = 2 flops)
 FLOP_PEAK = 157.3e12
 RECORD_BYTES = 20  # a kept cell: parent index (4 bytes) + its four children's outputs (16 bytes)
@@ -155,17 +157,18 @@ def event_timed(emr, torch, step, steps, rT):
     return recs
 
 
-def pipelined_steps(torch, enqueue, check, steps, warmup):
-    """warmup, then `steps` timed steps two calls deep: enqueue(i) starts call i into buffer
-    i % 2 on stream i % 2, check(i) synchronizes with call i and checks it; call i is checked
-    right after call i + 1 is enqueued (the buffer of call i is enqueued again only after its
-    check). Returns ms per step on the host clock."""
+def pipelined_steps(torch, enqueue, check, steps, warmup, depth):
+    """warmup, then `steps` timed steps with depth + 1 calls in flight: enqueue(i) starts call i
+    into buffer i % (depth + 1) on that buffer's stream, check(i) synchronizes with call i and
+    checks it; call i is checked right after call i + depth is enqueued (the buffer of call i is
+    enqueued again only after its check). Returns ms per step on the host clock."""
     def run(n):
-        enqueue(0)
-        for i in range(1, n):
+        for i in range(n):
             enqueue(i)
-            check(i - 1)
-        check(n - 1)
+            if i >= depth:
+                check(i - depth)
+        for i in range(max(0, n - depth), n):
+            check(i)
     if warmup > 0:
         run(warmup)
     torch.cuda.synchronize()
@@ -192,17 +195,18 @@ def measure_call(emr, torch, name, steps, warmup, rT):
     assert len(compiled) == 1, "the timed steps ran both tiers"
     kernel = "emr_discover_jit_records" if compiled == {True} else "k_discover<1>"
     records = int(res["pair_offset"][-1].item())
-    # the pipelined steps: a second result buffer beside the first, one stream each
-    bufs = [res, emr.alloc_result(pop, sources, depth)]
-    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    # the pipelined steps: IN_FLIGHT result buffers (the first one's above), one stream each
+    bufs = [res] + [emr.alloc_result(pop, sources, depth) for _ in range(IN_FLIGHT - 1)]
+    streams = [torch.cuda.Stream() for _ in range(IN_FLIGHT)]
     totals = []
 
     def enqueue(i):
-        emr.emr_discover(pop, sources, depth, theta32, res=bufs[i & 1], stream=streams[i & 1])
+        k = i % IN_FLIGHT
+        emr.emr_discover(pop, sources, depth, theta32, res=bufs[k], stream=streams[k])
 
     def check(i):
-        totals.append(emr.emr_result_check(bufs[i & 1])[0])
-    ms = pipelined_steps(torch, enqueue, check, steps, warmup)
+        totals.append(emr.emr_result_check(bufs[i % IN_FLIGHT])[0])
+    ms = pipelined_steps(torch, enqueue, check, steps, warmup, IN_FLIGHT - 1)
     assert set(totals) == {records}, "a pipelined call found a different record count"
     out = {"workload": name, "genomes": len(genomes), "sources": len(sources), "depth": depth,
            "theta": theta, "steps": steps, "ms_per_step": ms, "ms_per_step_sync": ms_sync,

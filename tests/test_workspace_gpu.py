@@ -110,12 +110,13 @@ def test_every_cell_kept_with_a_pool_beyond_2_pow_23(emr):
             np.testing.assert_array_equal(w.reshape(-1), raw[r, :4 * Q])
 
 
-@pytest.mark.parametrize("depth,n", [(7, 400), (8, 120)])
-def test_two_calls_in_flight_on_two_streams(emr, depth, n):
-    """Two results, each with its workspace and stream, alternate with two calls in flight (call
-    i is checked after call i + 1 is enqueued, as the benchmark's timed steps run): every call's
-    records equal those of a single synchronous call on a fresh workspace, bit for bit, and every
-    call's check reports the same total. The compiled tier runs from the second call on."""
+@pytest.mark.parametrize("depth,n,in_flight", [(7, 400, 2), (7, 400, 4), (8, 120, 4)])
+def test_calls_in_flight_on_their_own_streams(emr, depth, n, in_flight):
+    """Results, each with its workspace and stream, take the calls in turn with `in_flight` calls
+    in flight (call i is checked after call i + in_flight - 1 is enqueued, as the benchmark's timed
+    steps run): every call's records equal those of a single synchronous call on a fresh
+    workspace, bit for bit, and every call's check reports the same total. The compiled tier runs
+    from the second call on."""
     import torch
     genomes = W.population(72, n, 20, 60)
     sources = W.xor_sources()
@@ -125,21 +126,25 @@ def test_two_calls_in_flight_on_two_streams(emr, depth, n):
     emr.emr_discover(pop, sources, depth, theta, res=ref)
     total, _ = emr.emr_result_check(ref)
     want = host(emr, ref)
-    bufs = [emr.alloc_result(pop, sources, depth) for _ in range(2)]
-    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    bufs = [emr.alloc_result(pop, sources, depth) for _ in range(in_flight)]
+    streams = [torch.cuda.Stream() for _ in range(in_flight)]
     got = []
 
     def check(i):
-        t, _ = emr.emr_result_check(bufs[i & 1])
+        t, _ = emr.emr_result_check(bufs[i % in_flight])
         assert t == total, (i, t, total)
-        got.append(host(emr, bufs[i & 1]))
+        got.append(host(emr, bufs[i % in_flight]))
 
-    n_calls = 9
+    n_calls = 3 * in_flight + 1
+    lag = in_flight - 1
     for i in range(n_calls):
-        emr.emr_discover(pop, sources, depth, theta, res=bufs[i & 1], stream=streams[i & 1])
-        if i > 0:
-            check(i - 1)
-    check(n_calls - 1)
+        emr.emr_discover(pop, sources, depth, theta, res=bufs[i % in_flight],
+                         stream=streams[i % in_flight])
+        if i >= lag:
+            check(i - lag)
+    for i in range(n_calls - lag, n_calls):
+        check(i)
+    assert len(got) == n_calls
     assert emr.emr_jit_info(pop)["state"] == 1
     for g in got:
         same(g, want)
