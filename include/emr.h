@@ -184,7 +184,10 @@ emr_status emr_workspace_bytes(const emr_population* pop, const emr_source* sour
  * and keeps P when var > theta (strict; NaN never kept). fp32 throughout.
  * `sources` is host memory (n_sources entries, n_sources = n_shared or src_offsets[n_genomes]).
  * Enqueued on `stream`; the host returns after staging small per-call tables.
- * The workspace must not be shared by calls that overlap in time.
+ * The workspace must not be shared by calls that overlap in time. Calls with distinct workspaces
+ * and outputs are independent (each takes its own flag slot; the population's tables and compiled
+ * code are only read): several may be in flight at once, on one stream or on several, and a
+ * caller can enqueue the next calls before checking the earlier ones with emr_result_check.
  */
 emr_status emr_discover(const emr_population* pop, const emr_source* sources, int32_t n_sources,
                         const int32_t* src_offsets, int32_t n_shared, int32_t depth, float theta,
